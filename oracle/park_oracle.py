@@ -1,0 +1,374 @@
+"""PARK sparse-attention forward -- plain CPU oracle (float64 NumPy).
+
+TEST INFRASTRUCTURE ONLY.  This module is imported by ``tests/``, by
+``__graft_entry__.smoke()`` and by the ``cpu_baseline`` leg of ``bench.py``,
+nothing else.  The HIP library never imports, links or calls it, and it
+imports nothing from the library.  It shares no code with the GPU path except
+that both consume the seeded tensors of ``paper_2609_38978_amd.synth``.
+
+Everything is computed per attention head in float64; bf16/fp32 inputs are
+upcast exactly.  Each function follows one passage of the paper (PARK:
+Accurate Block Retrieval for Sparse Attention in Video Diffusion
+Transformers), cited in its docstring by section, equation or algorithm.
+
+Readings taken where the paper is silent (the same list is kept with the
+design notes of the repository):
+
+* blocks are k-means clusters, ``C = ceil(N / B)`` of them per side;
+* k-means init: ``C`` distinct token indices from a partial Fisher-Yates
+  shuffle driven by SplitMix64, seeded with
+  ``seed XOR (0x9E3779B97F4A7C15 * (2*head + side + 1)) mod 2^64``, where
+  ``side`` is 0 for queries and 1 for keys;
+* k-means runs exactly ``T`` (assign, update) rounds, the labels are those of
+  the T-th assignment; argmin ties go to the lowest cluster id; an empty
+  cluster keeps its previous centroid;
+* the token permutation is the stable argsort of the labels;
+* the stability constant is ``eps = 1e-6`` and ``s_min = 1e-12``;
+* key-block centroids are rounded to float32 before PAMA scores them;
+* empty key blocks get no score (they are left out of the softmax and are
+  never selected); empty query blocks get no mask row;
+* top-p keeps the shortest prefix (descending estimated importance, ties by
+  ascending block id) whose float64 cumulative sum is >= p, all nonempty
+  blocks if rounding never reaches p, and at least one block; top-k keeps
+  ``ceil(rho * N_K - 1e-9)`` blocks clamped to [1, #nonempty];
+* sparse attention renormalises the softmax over the selected keys (the
+  block-sparse flash-attention semantics); with every block kept this is
+  exactly full attention.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+_M64 = (1 << 64) - 1
+_GOLDEN = 0x9E3779B97F4A7C15
+
+
+# --------------------------------------------------------------------------
+# seeded k-means initialisation (the paper only says "initialize from K~")
+# --------------------------------------------------------------------------
+class SplitMix64:
+    """SplitMix64 generator (Steele, Lea & Flood, OOPSLA 2014), as published."""
+
+    def __init__(self, seed: int):
+        self.state = seed & _M64
+
+    def next(self) -> int:
+        self.state = (self.state + _GOLDEN) & _M64
+        z = self.state
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _M64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _M64
+        return z ^ (z >> 31)
+
+
+def init_seed(seed: int, head: int, side: int) -> int:
+    return (seed ^ ((_GOLDEN * (2 * head + side + 1)) & _M64)) & _M64
+
+
+def init_indices(N: int, C: int, seed: int, head: int, side: int) -> np.ndarray:
+    """First C entries of a Fisher-Yates shuffle of range(N) (distinct tokens).
+
+    Step i swaps position i with position ``i + (next() mod (N - i))``.
+    """
+    if not 1 <= C <= N:
+        raise ValueError("need 1 <= C <= N")
+    rng = SplitMix64(init_seed(seed, head, side))
+    a = list(range(N))
+    for i in range(C):
+        j = i + rng.next() % (N - i)
+        a[i], a[j] = a[j], a[i]
+    return np.array(a[:C], dtype=np.int64)
+
+
+# --------------------------------------------------------------------------
+# QRKC: query metric, Cholesky factor, key transform (Sec. 5.2, App. D.2, Alg. 3)
+# --------------------------------------------------------------------------
+def query_metric(Q: np.ndarray, alpha: float = 0.05, eps: float = 1e-6, s_min: float = 1e-12):
+    """Stabilised query second moment and its Cholesky factor (Alg. 3).
+
+    G = Q^T Q / L, symmetrised; s = max(tr(G)/d, s_min);
+    Gbar = (1 - alpha) G + alpha s I + eps s I; Gbar = R R^T with R lower.
+    Raises ``np.linalg.LinAlgError`` when Gbar is not positive definite.
+    """
+    Q = np.asarray(Q, dtype=np.float64)
+    L, d = Q.shape
+    G = (Q.T @ Q) / L
+    G = (G + G.T) / 2.0
+    s = max(np.trace(G) / d, s_min)
+    eye = np.eye(d)
+    Gbar = (1.0 - alpha) * G + alpha * s * eye + eps * s * eye
+    R = np.linalg.cholesky(Gbar)
+    return {"G": G, "s": s, "Gbar": Gbar, "R": R}
+
+
+def transform_keys(K: np.ndarray, R: np.ndarray) -> np.ndarray:
+    """Row form of k~ = R^T k (Eq. (12)): K~ = K R."""
+    return np.asarray(K, dtype=np.float64) @ R
+
+
+# --------------------------------------------------------------------------
+# Euclidean k-means (Sec. 5.2 "standard Euclidean K-means", Alg. 3 loop)
+# --------------------------------------------------------------------------
+def sq_distances(X: np.ndarray, mu: np.ndarray) -> np.ndarray:
+    """Squared Euclidean distances ``[n, C]`` = |x|^2 - 2 x.mu + |mu|^2."""
+    x2 = np.einsum("ij,ij->i", X, X)
+    m2 = np.einsum("ij,ij->i", mu, mu)
+    return x2[:, None] - 2.0 * (X @ mu.T) + m2[None, :]
+
+
+def assign(X: np.ndarray, mu: np.ndarray, chunk: int = 8192) -> np.ndarray:
+    """z_j = argmin_v |x_j - mu_v|^2, ties to the lowest v."""
+    z = np.empty(X.shape[0], dtype=np.int64)
+    for a in range(0, X.shape[0], chunk):
+        z[a:a + chunk] = np.argmin(sq_distances(X[a:a + chunk], mu), axis=1)
+    return z
+
+
+def update(X: np.ndarray, z: np.ndarray, mu: np.ndarray) -> np.ndarray:
+    """mu_v = mean{x_j : z_j = v}; an empty cluster keeps its centroid."""
+    C = mu.shape[0]
+    cnt = np.bincount(z, minlength=C)
+    sums = np.zeros_like(mu)
+    np.add.at(sums, z, X)
+    new = mu.copy()
+    nz = cnt > 0
+    new[nz] = sums[nz] / cnt[nz, None]
+    return new
+
+
+def kmeans(X: np.ndarray, C: int, T: int, init: np.ndarray, labels_hook=None):
+    """T rounds of (assign, update) from centroids X[init].
+
+    Returns the labels of the T-th assignment and the centroids it used.
+    ``labels_hook(t, z, mu)`` may return replacement labels for round t
+    (parity tests use it to follow another implementation's near-tie flips).
+    """
+    X = np.asarray(X, dtype=np.float64)
+    mu = X[np.asarray(init)].copy()
+    z = None
+    for t in range(T):
+        z = assign(X, mu)
+        if labels_hook is not None:
+            z = labels_hook(t, z, mu)
+        if t + 1 < T:
+            mu = update(X, z, mu)
+    return z, mu
+
+
+# --------------------------------------------------------------------------
+# permutation and block layout (Alg. 3 tail; App. E "queries stored contiguously")
+# --------------------------------------------------------------------------
+def stable_argsort(z: np.ndarray, C: int):
+    """pi = stable argsort(z); offsets o[0..C] with o[v+1] - o[v] = n_v."""
+    z = np.asarray(z)
+    perm = np.argsort(z, kind="stable")
+    counts = np.bincount(z, minlength=C)
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    return perm.astype(np.int64), offsets.astype(np.int64)
+
+
+def block_centroids(Kp: np.ndarray, offsets: np.ndarray):
+    """c_v = (1/n_v) sum of the original keys of block v (Eq. (8), Alg. 3).
+
+    Kp are the permuted keys.  The centroids are rounded to float32 (the
+    precision the retrieval kernel scores them in); empty blocks give 0.
+    """
+    Kp = np.asarray(Kp, dtype=np.float64)
+    C = len(offsets) - 1
+    c = np.zeros((C, Kp.shape[1]), dtype=np.float64)
+    n = np.diff(offsets).astype(np.int64)
+    for v in range(C):
+        if n[v] > 0:
+            c[v] = Kp[offsets[v]:offsets[v + 1]].sum(axis=0) / n[v]
+    return c.astype(np.float32), n
+
+
+# --------------------------------------------------------------------------
+# PAMA (Sec. 5.1, Eqs. (8)-(9))
+# --------------------------------------------------------------------------
+def pama_scores(Qp: np.ndarray, c: np.ndarray, n: np.ndarray) -> np.ndarray:
+    """S^_iv = q_i . c_v / sqrt(d) + log n_v; -inf for empty key blocks."""
+    Qp = np.asarray(Qp, dtype=np.float64)
+    d = Qp.shape[1]
+    S = (Qp @ np.asarray(c, dtype=np.float64).T) / math.sqrt(d)
+    with np.errstate(divide="ignore"):
+        logn = np.where(n > 0, np.log(np.maximum(n, 1).astype(np.float64)), -np.inf)
+    return S + logn[None, :]
+
+
+def softmax_rows(S: np.ndarray) -> np.ndarray:
+    m = S.max(axis=1, keepdims=True)
+    E = np.exp(S - m)
+    return E / E.sum(axis=1, keepdims=True)
+
+
+def pama(Qp: np.ndarray, q_offsets: np.ndarray, c: np.ndarray, n: np.ndarray) -> np.ndarray:
+    """W^_uv = (1/n_u) sum_{i in Q_u} softmax_v(S^_i.)_v  (Eq. (9)).
+
+    Rows of empty query blocks are zero.
+    """
+    CQ = len(q_offsets) - 1
+    W = np.zeros((CQ, len(n)), dtype=np.float64)
+    for u in range(CQ):
+        a, b = int(q_offsets[u]), int(q_offsets[u + 1])
+        if b > a:
+            P = softmax_rows(pama_scores(Qp[a:b], c, n))
+            W[u] = P.sum(axis=0) / (b - a)
+    return W
+
+
+# --------------------------------------------------------------------------
+# mask selection (Sec. 3.2 top-p; App. J top-k)
+# --------------------------------------------------------------------------
+def descending_order(w: np.ndarray, valid: np.ndarray) -> np.ndarray:
+    """Valid block ids by decreasing w, ties by increasing id."""
+    ids = np.nonzero(valid)[0]
+    return ids[np.lexsort((ids, -w[ids]))]
+
+
+def topk_count(rho: float, n_blocks: int, n_valid: int) -> int:
+    k = math.ceil(rho * n_blocks - 1e-9)
+    return max(1, min(k, n_valid))
+
+
+def select_row(w: np.ndarray, valid: np.ndarray, mode: str, param: float):
+    """Selected key-block ids of one query block, ascending.
+
+    Also returns the descending order and the cut (number kept) so callers
+    can inspect near-ties.
+    """
+    order = descending_order(w, valid)
+    if len(order) == 0:
+        return np.zeros(0, dtype=np.int64), order, 0
+    if mode == "topk":
+        m = topk_count(param, len(w), len(order))
+    elif mode == "topp":
+        cs = np.cumsum(w[order])
+        hit = np.nonzero(cs >= param)[0]
+        m = int(hit[0]) + 1 if len(hit) else len(order)
+    else:
+        raise ValueError(mode)
+    return np.sort(order[:m]), order, m
+
+
+def select(W: np.ndarray, q_sizes: np.ndarray, k_sizes: np.ndarray, mode: str, param: float):
+    """Block mask as a list of ascending key-block id arrays per query block."""
+    valid = np.asarray(k_sizes) > 0
+    rows = []
+    for u in range(W.shape[0]):
+        if q_sizes[u] == 0:
+            rows.append(np.zeros(0, dtype=np.int64))
+        else:
+            rows.append(select_row(W[u], valid, mode, param)[0])
+    return rows
+
+
+# --------------------------------------------------------------------------
+# attention (Eqs. (1)-(2))
+# --------------------------------------------------------------------------
+def dense_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """O = softmax(Q K^T / sqrt(d)) V (Eq. (1))."""
+    Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
+    A = softmax_rows((Q @ K.T) / math.sqrt(Q.shape[1]))
+    return A @ V
+
+
+def block_sparse_attention(Qp, Kp, Vp, q_offsets, k_offsets, rows, q_perm) -> np.ndarray:
+    """Attention of each query block over the union of its selected key blocks.
+
+    The softmax is renormalised over the kept keys; row i of the permuted
+    queries is written to position q_perm[i] (un-permutation).
+    """
+    Qp, Kp, Vp = (np.asarray(a, dtype=np.float64) for a in (Qp, Kp, Vp))
+    N, d = Qp.shape
+    O = np.zeros((N, Vp.shape[1]), dtype=np.float64)
+    for u, sel in enumerate(rows):
+        a, b = int(q_offsets[u]), int(q_offsets[u + 1])
+        if b == a:
+            continue
+        keys = np.concatenate([np.arange(k_offsets[v], k_offsets[v + 1]) for v in sel])
+        A = softmax_rows((Qp[a:b] @ Kp[keys].T) / math.sqrt(d))
+        O[np.asarray(q_perm[a:b])] = A @ Vp[keys]
+    return O
+
+
+# --------------------------------------------------------------------------
+# whole head (Alg. 3 + Sec. 5.1 + Eq. (2))
+# --------------------------------------------------------------------------
+def cluster_queries(Q, C, T, seed, head):
+    """Euclidean k-means on the queries and their permutation (Sec. 5.2)."""
+    Q = np.asarray(Q, dtype=np.float64)
+    init = init_indices(Q.shape[0], C, seed, head, side=0)
+    z, mu = kmeans(Q, C, T, init)
+    perm, off = stable_argsort(z, C)
+    return {"labels": z, "perm": perm, "offsets": off, "mu": mu, "init": init}
+
+
+def cluster_keys(K, Q, C, T, seed, head, alpha=0.05, eps=1e-6, s_min=1e-12):
+    """QRKC (Alg. 3): k-means on K R, with Gbar = R R^T from the queries."""
+    met = query_metric(Q, alpha, eps, s_min)
+    Kt = transform_keys(K, met["R"])
+    init = init_indices(Kt.shape[0], C, seed, head, side=1)
+    z, mu = kmeans(Kt, C, T, init)
+    perm, off = stable_argsort(z, C)
+    return {"labels": z, "perm": perm, "offsets": off, "mu": mu, "init": init,
+            "Kt": Kt, **met}
+
+
+def park_head(Q, K, V, CQ, CK, T, mode, param, seed=0, head=0, alpha=0.05, eps=1e-6,
+              s_min=1e-12):
+    """PARK forward of one head; returns every intermediate and O."""
+    Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
+    cq = cluster_queries(Q, CQ, T, seed, head)
+    ck = cluster_keys(K, Q, CK, T, seed, head, alpha, eps, s_min)
+    Qp, Kp, Vp = Q[cq["perm"]], K[ck["perm"]], V[ck["perm"]]
+    c, n = block_centroids(Kp, ck["offsets"])
+    W = pama(Qp, cq["offsets"], c, n)
+    rows = select(W, np.diff(cq["offsets"]), n, mode, param)
+    O = block_sparse_attention(Qp, Kp, Vp, cq["offsets"], ck["offsets"], rows, cq["perm"])
+    return {"q": cq, "k": ck, "Qp": Qp, "Kp": Kp, "Vp": Vp, "centroids": c, "sizes": n,
+            "W": W, "rows": rows, "O": O}
+
+
+# --------------------------------------------------------------------------
+# diagnostics of Secs. 3.2 / App. A (used as checks, not on the hot path)
+# --------------------------------------------------------------------------
+def exact_block_importance(Qp, Kp, q_offsets, k_offsets) -> np.ndarray:
+    """W_uv = (1/n_u) sum_{i in Q_u} sum_{j in K_v} A_ij  (Eq. (3))."""
+    A = softmax_rows((np.asarray(Qp, np.float64) @ np.asarray(Kp, np.float64).T)
+                     / math.sqrt(Qp.shape[1]))
+    CQ, CK = len(q_offsets) - 1, len(k_offsets) - 1
+    W = np.zeros((CQ, CK))
+    for u in range(CQ):
+        a, b = q_offsets[u], q_offsets[u + 1]
+        if b == a:
+            continue
+        for v in range(CK):
+            W[u, v] = A[a:b, k_offsets[v]:k_offsets[v + 1]].sum() / (b - a)
+    return W
+
+
+def recall(Qp, Kp, q_offsets, k_offsets, rows) -> float:
+    """Attention recall sum(A * M) / sum(A) of a block mask (Eq. (4))."""
+    A = softmax_rows((np.asarray(Qp, np.float64) @ np.asarray(Kp, np.float64).T)
+                     / math.sqrt(Qp.shape[1]))
+    kept = 0.0
+    for u, sel in enumerate(rows):
+        a, b = q_offsets[u], q_offsets[u + 1]
+        for v in sel:
+            kept += A[a:b, k_offsets[v]:k_offsets[v + 1]].sum()
+    return kept / A.sum()
+
+
+def exact_log_mass(Qp, Kp, k_offsets) -> np.ndarray:
+    """S*_iv = log sum_{j in K_v} exp(q_i . k_j / sqrt(d))  (Eq. (6))."""
+    Z = (np.asarray(Qp, np.float64) @ np.asarray(Kp, np.float64).T) / math.sqrt(Qp.shape[1])
+    CK = len(k_offsets) - 1
+    S = np.full((Z.shape[0], CK), -np.inf)
+    for v in range(CK):
+        a, b = k_offsets[v], k_offsets[v + 1]
+        if b > a:
+            m = Z[:, a:b].max(axis=1)
+            S[:, v] = m + np.log(np.exp(Z[:, a:b] - m[:, None]).sum(axis=1))
+    return S

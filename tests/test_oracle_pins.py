@@ -1,0 +1,451 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than itself: published
+test vectors, closed forms, brute force on tiny inputs, invariants stated in
+the paper, or independent library routines (torch CPU attention, eigh).
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import park_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rng(seed=0):
+    return np.random.default_rng(seed)
+
+
+# ---------------------------------------------------------------- init -----
+def test_splitmix64_published_vectors():
+    with open(os.path.join(GOLDEN, "splitmix64.txt")) as f:
+        rows = [l.split() for l in f if l.strip() and not l.startswith("#")]
+    assert rows
+    for row in rows:
+        seed, expect = int(row[0]), [int(x) for x in row[1:]]
+        g = O.SplitMix64(seed)
+        assert [g.next() for _ in expect] == expect
+
+
+def test_init_indices_distinct_prefix_and_permutation():
+    N = 1000
+    a = O.init_indices(N, 37, seed=5, head=3, side=1)
+    assert len(set(a.tolist())) == 37 and a.min() >= 0 and a.max() < N
+    # Fisher-Yates: a shorter draw is a prefix of a longer one
+    b = O.init_indices(N, 200, seed=5, head=3, side=1)
+    assert np.array_equal(a, b[:37])
+    full = O.init_indices(N, N, seed=5, head=3, side=1)
+    assert sorted(full.tolist()) == list(range(N))
+    # heads and sides draw different streams
+    assert not np.array_equal(a, O.init_indices(N, 37, 5, 3, 0))
+    assert not np.array_equal(a, O.init_indices(N, 37, 5, 4, 1))
+
+
+def test_init_indices_uniform():
+    # each token is picked with probability C/N (chi-square over many seeds)
+    N, C, S = 20, 5, 4000
+    cnt = np.zeros(N)
+    for s in range(S):
+        cnt[O.init_indices(N, C, seed=s, head=0, side=0)] += 1
+    exp = S * C / N
+    chi2 = ((cnt - exp) ** 2 / exp).sum()
+    assert chi2 < 45.0  # 19 dof, p ~ 1e-3
+    # first pick is uniform too
+    first = np.bincount([O.init_indices(N, 1, s, 0, 0)[0] for s in range(S)], minlength=N)
+    chi2 = ((first - S / N) ** 2 / (S / N)).sum()
+    assert chi2 < 45.0
+
+
+# ------------------------------------------------------ query metric ------
+def test_metric_closed_form_diagonal():
+    # rows are scaled basis vectors: G is diagonal with known entries
+    d, L = 4, 8
+    Q = np.zeros((L, d))
+    sig = np.array([1.0, 2.0, 3.0, 4.0])
+    for i in range(L):
+        Q[i, i % d] = sig[i % d]
+    m = O.query_metric(Q, alpha=0.05, eps=1e-6)
+    G = np.diag(sig ** 2 * 2 / L)
+    assert np.allclose(m["G"], G, rtol=0, atol=1e-15)
+    s = np.trace(G) / d
+    assert m["s"] == pytest.approx(s, rel=1e-15)
+    gbar = 0.95 * G + (0.05 + 1e-6) * s * np.eye(d)
+    assert np.allclose(m["Gbar"], gbar, rtol=1e-14, atol=0)
+    assert np.allclose(m["R"], np.sqrt(gbar), rtol=1e-14, atol=0)
+
+
+def test_metric_factor_and_alpha_one():
+    Q = rng(1).standard_normal((300, 16)) * np.linspace(0.1, 3, 16)
+    m = O.query_metric(Q, alpha=0.05, eps=1e-6)
+    R = m["R"]
+    assert np.allclose(R, np.tril(R))
+    assert np.all(np.diag(R) > 0)
+    assert np.abs(R @ R.T - m["Gbar"]).max() <= 1e-12 * np.abs(m["Gbar"]).max()
+    # G is PSD: x^T G x = |Q x|^2 / L
+    x = rng(2).standard_normal(16)
+    assert x @ m["G"] @ x == pytest.approx(np.sum((Q @ x) ** 2) / 300, rel=1e-12)
+    # alpha = 1 gives an isotropic metric
+    m1 = O.query_metric(Q, alpha=1.0, eps=1e-6)
+    assert np.allclose(m1["R"], math.sqrt((1 + 1e-6) * m1["s"]) * np.eye(16), rtol=1e-13, atol=1e-15)
+
+
+def test_metric_scale_floor_and_failure():
+    Z = np.zeros((50, 8))
+    m = O.query_metric(Z)
+    assert m["s"] == 1e-12
+    assert np.allclose(m["Gbar"], (0.05 + 1e-6) * 1e-12 * np.eye(8), rtol=1e-14, atol=0)
+    # rank-deficient queries without shrinkage: Cholesky must fail
+    Q = np.zeros((40, 8))
+    Q[:, :3] = rng(3).standard_normal((40, 3))
+    with pytest.raises(np.linalg.LinAlgError):
+        O.query_metric(Q, alpha=0.0, eps=0.0)
+
+
+def test_transformed_distance_equivalences():
+    # |R^T delta|^2 = delta^T Gbar delta = |Gbar^(1/2) delta|^2; with alpha=eps=0
+    # also = |Q delta|^2 / L (the direct L-dimensional map)
+    L, d = 200, 12
+    Q = rng(4).standard_normal((L, d)) @ rng(5).standard_normal((d, d))
+    K = rng(6).standard_normal((30, d))
+    m = O.query_metric(Q, alpha=0.0, eps=0.0)
+    Kt = O.transform_keys(K, m["R"])
+    w, U = np.linalg.eigh(m["Gbar"])
+    S = U @ np.diag(np.sqrt(np.maximum(w, 0))) @ U.T
+    for j in range(30):
+        for c in range(0, 30, 7):
+            delta = K[j] - K[c]
+            a = np.sum((Kt[j] - Kt[c]) ** 2)
+            b = delta @ m["Gbar"] @ delta
+            e = np.sum((S @ delta) ** 2)
+            f = np.sum((Q @ delta) ** 2) / L
+            assert a == pytest.approx(b, rel=1e-11)
+            assert a == pytest.approx(e, rel=1e-10)
+            assert a == pytest.approx(f, rel=1e-10)
+
+
+# ------------------------------------------------------------ k-means -----
+def brute_assign(X, mu):
+    z = []
+    for x in X:
+        best, bi = None, -1
+        for v, m in enumerate(mu):
+            dist = sum((xa - ma) ** 2 for xa, ma in zip(x, m))
+            if best is None or dist < best:
+                best, bi = dist, v
+        z.append(bi)
+    return np.array(z)
+
+
+def brute_mean(X, z, mu):
+    out = mu.copy()
+    for v in range(len(mu)):
+        rows = [X[j] for j in range(len(X)) if z[j] == v]
+        if rows:
+            out[v] = [sum(r[a] for r in rows) / len(rows) for a in range(X.shape[1])]
+    return out
+
+
+def test_assign_and_update_brute_force():
+    X = rng(7).standard_normal((60, 5))
+    mu = rng(8).standard_normal((7, 5))
+    z = O.assign(X, mu)
+    assert np.array_equal(z, brute_assign(X, mu))
+    new = O.update(X, z, mu)
+    assert np.allclose(new, brute_mean(X, z, mu), rtol=1e-14, atol=1e-15)
+
+
+def test_assign_ties_lowest_id_and_empty_keeps_centroid():
+    X = np.array([[0.0, 0.0], [2.0, 0.0], [10.0, 10.0]])
+    mu = np.array([[1.0, 0.0], [1.0, 0.0], [-50.0, -50.0], [10.0, 10.0]])
+    z = O.assign(X, mu)
+    assert z.tolist() == [0, 0, 3]  # equal distances -> lowest id
+    new = O.update(X, z, mu)
+    assert np.array_equal(new[1], mu[1]) and np.array_equal(new[2], mu[2])
+    assert np.array_equal(new[0], [1.0, 0.0])
+
+
+def test_kmeans_objective_non_increasing():
+    X = rng(9).standard_normal((400, 6)) + np.repeat(rng(10).standard_normal((8, 6)) * 3, 50, 0)
+    init = O.init_indices(400, 10, 0, 0, 0)
+    mu = X[init].copy()
+    prev = np.inf
+    for t in range(8):
+        z = O.assign(X, mu)
+        J = np.sum((X - mu[z]) ** 2)
+        assert J <= prev + 1e-9
+        prev = J
+        mu = O.update(X, z, mu)
+
+
+def test_kmeans_singletons_when_C_equals_N():
+    X = rng(11).standard_normal((40, 4))
+    init = O.init_indices(40, 40, 1, 0, 0)
+    z, _ = O.kmeans(X, 40, 3, init)
+    # every token seeds its own cluster and keeps it
+    assert np.array_equal(init[z], np.arange(40))
+
+
+def test_qrkc_alpha_one_equals_euclidean_kmeans():
+    Q = rng(12).standard_normal((300, 8)) * np.linspace(0.2, 4, 8)
+    K = rng(13).standard_normal((300, 8)) + np.repeat(rng(14).standard_normal((6, 8)) * 2, 50, 0)
+    ck = O.cluster_keys(K, Q, C=12, T=6, seed=3, head=2, alpha=1.0)
+    init = O.init_indices(300, 12, 3, 2, 1)
+    z, _ = O.kmeans(K, 12, 6, init)
+    assert np.array_equal(ck["labels"], z)
+
+
+def test_qrkc_objective_identities():
+    # Jbar = (1-a) J + (a+eps) s J_euc, and the G-form of J equals the
+    # explicit average over queries of squared score errors.
+    L, d = 80, 6
+    Q = rng(15).standard_normal((L, d)) * np.array([0.3, 1, 2, 0.5, 1.5, 3])
+    K = rng(16).standard_normal((L, d))
+    z = rng(17).integers(0, 5, L)
+    c = np.array([K[z == v].mean(0) for v in range(5)])
+    a, eps = 0.05, 1e-6
+    m = O.query_metric(Q, a, eps)
+    delta = K - c[z]
+    J = np.einsum("ja,ab,jb->", delta, m["G"], delta)
+    J_explicit = sum((Q[i] @ delta[j]) ** 2 for i in range(L) for j in range(L)) / L
+    assert J == pytest.approx(J_explicit, rel=1e-11)
+    Jeuc = np.sum(delta ** 2)
+    Kt = O.transform_keys(K, m["R"])
+    ct = np.array([Kt[z == v].mean(0) for v in range(5)])
+    Jbar = np.sum((Kt - ct[z]) ** 2)
+    assert Jbar == pytest.approx((1 - a) * J + (a + eps) * m["s"] * Jeuc, rel=1e-11)
+    # transformed centroids are the transforms of the centroids (linearity)
+    assert np.allclose(ct, c @ m["R"], rtol=1e-12, atol=1e-13)
+
+
+# -------------------------------------------------------- permutation -----
+def test_stable_argsort_properties():
+    z = rng(18).integers(0, 9, 500)
+    z[z == 4] = 5  # force an empty cluster
+    perm, off = O.stable_argsort(z, 9)
+    assert sorted(perm.tolist()) == list(range(500))
+    zs = z[perm]
+    assert np.all(np.diff(zs) >= 0)
+    for v in range(9):
+        seg = perm[off[v]:off[v + 1]]
+        assert np.all(z[seg] == v)
+        assert np.all(np.diff(seg) > 0)  # stable: original order inside a block
+    assert off[4] == off[5] and off[-1] == 500
+
+
+def test_block_centroids_brute_force_and_zero_residual():
+    K = rng(19).standard_normal((100, 8)).astype(np.float32).astype(np.float64)
+    z = rng(20).integers(0, 6, 100)
+    z[z == 2] = 3
+    perm, off = O.stable_argsort(z, 6)
+    c, n = O.block_centroids(K[perm], off)
+    assert c.dtype == np.float32 and n.tolist() == np.bincount(z, minlength=6).tolist()
+    assert np.all(c[2] == 0)
+    for v in range(6):
+        if n[v]:
+            exact = K[z == v].sum(0) / n[v]
+            assert np.array_equal(c[v], exact.astype(np.float32))
+            # residuals about the (unrounded) centroid sum to zero
+            assert np.abs((K[z == v] - exact).sum(0)).max() < 1e-12
+
+
+# --------------------------------------------------------------- PAMA -----
+def test_pama_hand_computed():
+    # two queries, key blocks: block 0 has 1 key at (2,0), block 1 has 3
+    # keys averaging (0,0), block 2 empty.  d = 2.
+    Qp = np.array([[1.0, 0.0], [0.0, 1.0]])
+    c = np.array([[2.0, 0.0], [0.0, 0.0], [9.0, 9.0]], dtype=np.float32)
+    n = np.array([1, 3, 0])
+    S = O.pama_scores(Qp, c, n)
+    r2 = math.sqrt(2.0)
+    assert S[0, 0] == pytest.approx(2 / r2, rel=1e-15)
+    assert S[0, 1] == pytest.approx(math.log(3), rel=1e-15)
+    assert S[1, 0] == pytest.approx(0.0, abs=1e-15)
+    assert np.isneginf(S[:, 2]).all()
+    p00 = math.exp(2 / r2) / (math.exp(2 / r2) + 3)
+    p10 = 1 / (1 + 3)
+    W = O.pama(Qp, np.array([0, 2]), c, n)
+    assert W[0, 0] == pytest.approx((p00 + p10) / 2, rel=1e-14)
+    assert W[0, 1] == pytest.approx(((1 - p00) + (1 - p10)) / 2, rel=1e-14)
+    assert W[0, 2] == 0.0
+
+
+def test_pama_rows_sum_to_one_and_jensen():
+    Qp = rng(21).standard_normal((64, 16))
+    Kp = rng(22).standard_normal((90, 16))
+    koff = np.array([0, 10, 10, 35, 36, 90])
+    c, n = O.block_centroids(Kp, koff)
+    S = O.pama_scores(Qp, c, n)
+    P = O.softmax_rows(S)
+    assert np.allclose(P.sum(1), 1, atol=1e-14)
+    W = O.pama(Qp, np.array([0, 20, 20, 64]), c, n)
+    assert np.allclose(W[[0, 2]].sum(1), 1, atol=1e-14) and np.all(W[1] == 0)
+    # key-centroid estimate is a lower bound of the exact log-mass (Jensen)
+    Kp32 = Kp.copy()
+    # compare with centroids that are exact means (use float64 means here)
+    cexact = np.array([Kp[koff[v]:koff[v + 1]].mean(0) if n[v] else np.zeros(16)
+                       for v in range(5)])
+    Shat = (Qp @ cexact.T) / 4.0 + np.log(np.maximum(n, 1))
+    Sstar = O.exact_log_mass(Qp, Kp32, koff)
+    for v in range(5):
+        if n[v]:
+            assert np.all(Shat[:, v] <= Sstar[:, v] + 1e-12)
+
+
+def test_pama_block_size_one_equals_attention():
+    # singleton key and query blocks: W^ is exactly the dense attention
+    # matrix (log 1 = 0, centroid = key), checked against torch's softmax.
+    N, d = 48, 8
+    Q = rng(23).standard_normal((N, d)).astype(np.float32).astype(np.float64)
+    K = rng(24).standard_normal((N, d)).astype(np.float32).astype(np.float64)
+    qp = rng(25).permutation(N)
+    kp = rng(26).permutation(N)
+    off = np.arange(N + 1)
+    c, n = O.block_centroids(K[kp], off)
+    W = O.pama(Q[qp], off, c, n)
+    A = torch.softmax(torch.from_numpy(Q) @ torch.from_numpy(K).T / math.sqrt(d), dim=1).numpy()
+    assert np.abs(W - A[np.ix_(qp, kp)]).max() < 1e-14
+
+
+def test_pama_identical_keys_equals_exact_importance():
+    # when every key of a block equals its centroid, S^ = S* exactly and
+    # PAMA equals the exact block importance of Eq. (3) (pins log n_v and the
+    # softmax-then-average order).
+    d = 8
+    base = rng(27).standard_normal((5, d)).astype(np.float32).astype(np.float64)
+    sizes = [3, 1, 7, 2, 5]
+    Kp = np.concatenate([np.repeat(base[v:v + 1], s, 0) for v, s in enumerate(sizes)])
+    koff = np.concatenate([[0], np.cumsum(sizes)])
+    Qp = rng(28).standard_normal((30, d)) * 2
+    qoff = np.array([0, 4, 4, 17, 30])
+    c, n = O.block_centroids(Kp, koff)
+    W = O.pama(Qp, qoff, c, n)
+    Wex = O.exact_block_importance(Qp, Kp, qoff, koff)
+    assert np.abs(W - Wex).max() < 1e-13
+
+
+def test_pama_identical_queries_equals_centroid_estimate():
+    d = 6
+    Kp = rng(29).standard_normal((40, d))
+    koff = np.array([0, 5, 19, 40])
+    c, n = O.block_centroids(Kp, koff)
+    q = rng(30).standard_normal(d)
+    Qp = np.repeat(q[None], 9, 0)
+    W = O.pama(Qp, np.array([0, 9]), c, n)
+    S = (c.astype(np.float64) @ q) / math.sqrt(d) + np.log(n)
+    e = np.exp(S - S.max())
+    assert np.allclose(W[0], e / e.sum(), rtol=1e-14, atol=0)
+
+
+# ---------------------------------------------------------- selection -----
+def brute_select(w, valid, mode, param):
+    items = sorted([(-w[v], v) for v in range(len(w)) if valid[v]])
+    if mode == "topk":
+        k = max(1, min(math.ceil(param * len(w) - 1e-9), len(items)))
+        return sorted(v for _, v in items[:k])
+    tot = 0.0
+    out = []
+    for negw, v in items:
+        out.append(v)
+        tot += -negw
+        if tot >= param:
+            break
+    return sorted(out)
+
+
+def test_select_brute_force():
+    r = rng(31)
+    for trial in range(200):
+        C = int(r.integers(1, 40))
+        w = r.random(C) ** 4
+        w[r.random(C) < 0.2] = 0.0
+        if trial % 5 == 0:
+            w = np.round(w * 4) / 4  # many ties
+        valid = r.random(C) < 0.85
+        if not valid.any():
+            valid[0] = True
+        w = np.where(valid, w, 0.0)
+        w = w / w.sum() if w.sum() > 0 else w
+        for mode, param in (("topk", r.random()), ("topp", r.random())):
+            got, _, _ = O.select_row(w, valid, mode, param)
+            assert got.tolist() == brute_select(w, valid, mode, param)
+
+
+def test_select_extremes_and_monotone():
+    r = rng(32)
+    w = r.random(50) ** 3
+    w /= w.sum()
+    valid = np.ones(50, bool)
+    valid[[3, 9]] = False
+    w[[3, 9]] = 0
+    allv = np.nonzero(valid)[0].tolist()
+    assert O.select_row(w, valid, "topk", 1.0)[0].tolist() == allv
+    assert O.select_row(w, valid, "topp", 1.0)[0].tolist() == allv
+    prev = set()
+    for p in np.linspace(0.05, 1.0, 20):
+        cur = set(O.select_row(w, valid, "topp", p)[0].tolist())
+        assert prev <= cur
+        prev = cur
+    prev = set()
+    for rho in np.linspace(0.02, 1.0, 20):
+        cur = set(O.select_row(w, valid, "topk", rho)[0].tolist())
+        assert prev <= cur
+        prev = cur
+    # top-k counts: ceil(rho * N_K)
+    assert len(O.select_row(w, valid, "topk", 0.2)[0]) == 10
+    assert O.topk_count(0.2, 256, 256) == 52 and O.topk_count(0.1, 1861, 1861) == 187
+
+
+# ---------------------------------------------------------- attention -----
+def test_all_blocks_kept_is_dense_attention():
+    N, d = 70, 16
+    r = rng(33)
+    Q, K, V = (r.standard_normal((N, d)) for _ in range(3))
+    qperm, kperm = r.permutation(N), r.permutation(N)
+    qoff = np.array([0, 13, 13, 40, 70])
+    koff = np.array([0, 7, 30, 30, 52, 70])
+    rows = [np.array([0, 1, 3, 4])] * 4  # block 2 is empty, the rest all kept
+    Ob = O.block_sparse_attention(Q[qperm], K[kperm], V[kperm], qoff, koff, rows, qperm)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q)[None], torch.from_numpy(K)[None], torch.from_numpy(V)[None])[0]
+    assert np.abs(Ob - ref.numpy()).max() < 1e-12
+    assert np.abs(O.dense_attention(Q, K, V) - ref.numpy()).max() < 1e-12
+
+
+def test_sparse_attention_ignores_unselected_and_renormalises():
+    N, d = 40, 8
+    r = rng(34)
+    Q, K, V = (r.standard_normal((N, d)) for _ in range(3))
+    qoff = np.array([0, 20, 40])
+    koff = np.array([0, 10, 25, 40])
+    rows = [np.array([1]), np.array([0, 2])]
+    perm = np.arange(N)
+    O1 = O.block_sparse_attention(Q, K, V, qoff, koff, rows, perm)
+    V2 = V.copy()
+    V2[0:10] += 100.0  # block 0 not selected by query block 0
+    O2 = O.block_sparse_attention(Q, K, V2, qoff, koff, rows, perm)
+    assert np.array_equal(O1[:20], O2[:20])
+    # query block 0 attends to keys 10..24 only, softmax renormalised there
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q[:20])[None], torch.from_numpy(K[10:25])[None],
+        torch.from_numpy(V[10:25])[None])[0].numpy()
+    assert np.abs(O1[:20] - ref).max() < 1e-12
+
+
+# --------------------------------------------------------- whole path -----
+def test_tiny_layer_end_to_end_sanity():
+    from paper_2609_38978_amd import synth
+    cfg = synth.CONFIGS["tiny"]
+    q, k, v = synth.make_head(cfg, 0)
+    res = O.park_head(q, k, v, cfg.C, cfg.C, cfg.iters, "topk", cfg.ratio)
+    assert all(len(r) == 16 for r in res["rows"] if len(r))
+    assert res["q"]["offsets"][-1] == cfg.N and res["k"]["offsets"][-1] == cfg.N
+    qoff, koff = res["q"]["offsets"], res["k"]["offsets"]
+    rec = O.recall(res["Qp"], res["Kp"], qoff, koff, res["rows"])
+    assert rec > 0.9  # clustered inputs: 25% of blocks hold most of the mass
+    # the mask keeps most of the exact importance of each query block
+    Wex = O.exact_block_importance(res["Qp"], res["Kp"], qoff, koff)
+    assert np.allclose(Wex[np.diff(qoff) > 0].sum(1), 1, atol=1e-12)
