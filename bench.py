@@ -1,0 +1,178 @@
+"""PARK sparse-attention forward benchmark: one DiT attention layer on one GPU.
+
+A step is one park_forward call (recompute mode: query k-means, QRKC key
+k-means, permutation, centroids, PAMA retrieval + selection, block-sparse
+attention) over the whole layer, inputs already resident in HBM.
+
+Prints one JSON line.  `value` is milliseconds per layer (lower is better);
+the dense-equivalent TFLOP/s (4 N^2 d H / t) is reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "ms per layer + dense-equiv TFLOP/s at 1 GPU; % of MFMA/HBM peak by stage"
+
+# MI355X published peaks
+PEAK = {"hbm": 8000.0,            # GB/s
+        "mfma_bf16": 2500.0,      # TFLOP/s dense
+        "alu_f32": 157.3,         # TFLOP/s vector fp32
+        "alu_f64": 78.6}          # TFLOP/s vector fp64
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="medium",
+                    help="synthetic layer: tiny | medium | wan | hunyuan")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=4,
+                    help="heads of the layer the oracle runs for the CPU baseline")
+    return ap.parse_args()
+
+
+def kernel_work(name, cfg, st, C):
+    """Algorithmic work of ONE launch of kernel `name`: (bound, amount, unit, peak key)."""
+    H, N, d = cfg.H, cfg.N, cfg.d
+    eb = 2 if cfg.dtype == "bf16" else 4
+    if name == "kmeans_assign64":
+        return "alu", 2.0 * N * C * d * H, "flop", "alu_f64"
+    if name == "pama64":
+        return "alu", 2.0 * N * C * d * H, "flop", "alu_f64"
+    if name == "gram_partial":
+        return "alu", 2.0 * N * d * d * H, "flop", "alu_f64"
+    if name in ("attn_valu", "attn_mfma"):
+        import numpy as np
+        qo = st["q_offsets"].cpu().numpy()
+        ko = st["k_offsets"].cpu().numpy()
+        kvc = st["kv_count"].cpu().numpy()
+        kvi = st["kv_index"].cpu().numpy()
+        tot = 0.0
+        for h in range(H):
+            nk = np.diff(ko[h])
+            nq = np.diff(qo[h])
+            for u in range(len(nq)):
+                if nq[u]:
+                    tot += nq[u] * nk[kvi[h, u, :kvc[h, u]]].sum()
+        peak = "mfma_bf16" if name == "attn_mfma" else "alu_f32"
+        return ("mfma" if name == "attn_mfma" else "alu"), 4.0 * d * tot, "flop", peak
+    if name == "gather_rows":
+        return "hbm", 2.0 * N * d * eb * H, "byte", "hbm"
+    if name == "segment_mean":
+        return "hbm", 1.0 * N * d * eb * H + C * d * 8 * H, "byte", "hbm"
+    return None
+
+
+def cpu_baseline(cfg, q, k, v, nheads):
+    import numpy as np
+    from oracle import park_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    mode = cfg.select
+    param = cfg.ratio if mode == "topk" else cfg.topp
+    t0 = time.perf_counter()
+    for h in range(nheads):
+        O.park_head(q[h], k[h], v[h], cfg.C, cfg.C, cfg.iters, mode, param, seed=0, head=h)
+    dt = time.perf_counter() - t0
+    ms_layer = dt * 1e3 * cfg.H / nheads
+    return {"value": round(ms_layer, 3), "unit": "ms per layer", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{nheads} of {cfg.H} heads of the {cfg.name} layer (full N), "
+                      f"whole PARK forward in float64 NumPy, scaled x{cfg.H / nheads:g}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); PARK shards by "
+              f"head with no communication, see the design notes", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2609_38978_amd import park as P
+    from paper_2609_38978_amd import synth
+
+    cfg = synth.CONFIGS[args.workload]
+    q, k, v = synth.make_layer(cfg)
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    Q, K, V = (torch.from_numpy(a).to(tdt).cuda() for a in (q, k, v))
+    C = cfg.C
+    mode = cfg.select
+    param = cfg.ratio if mode == "topk" else cfg.topp
+    prm = P.make_params(C, C, T=cfg.iters, select=mode, ratio=param, topp=param, seed=0,
+                        out_dtype=P.PARK_BF16 if cfg.dtype == "bf16" else P.PARK_F32)
+    ws = P.workspace(Q, C, C)
+    st = P.make_state(Q, C, C)
+    out = torch.empty(Q.shape, dtype=tdt, device="cuda")
+    for _ in range(args.warmup):
+        P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
+    P.park_check(ws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    P.park_profile_reset()
+    P.park_profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    P.park_profile_enable(False)
+    prof = P.park_profile_read()
+    P.park_check(ws)
+    ms = e0.elapsed_time(e1) / args.steps
+    dense_flops = 4.0 * cfg.N * cfg.N * cfg.d * cfg.H
+
+    # per-kernel share and roofline of the dominant kernel
+    stages = {n: {"ms_per_step": round(r["ms"] / args.steps, 4),
+                  "launches_per_step": r["launches"] // args.steps} for n, r in prof.items()}
+    dom = max(prof, key=lambda n: prof[n]["ms"])
+    avg_ms = prof[dom]["ms"] / prof[dom]["launches"]
+    work = kernel_work(dom, cfg, st, C)
+    roof = None
+    if work is not None:
+        bound, amount, unit, pk = work
+        if unit == "flop":
+            ach = amount / (avg_ms * 1e-3) / 1e12
+            roof = {"bound": bound, "achieved": round(ach, 3), "peak": PEAK[pk],
+                    "unit": "TFLOP/s", "frac": round(ach / PEAK[pk], 4), "traffic": None}
+        else:
+            ach = amount / (avg_ms * 1e-3) / 1e9
+            roof = {"bound": bound, "achieved": round(ach, 2), "peak": PEAK[pk], "unit": "GB/s",
+                    "frac": round(ach / PEAK[pk], 4), "traffic": None}
+        roof["kernel"] = dom
+        roof["avg_launch_ms"] = round(avg_ms, 4)
+
+    res = {"metric": METRIC, "value": round(ms, 4), "unit": "ms/layer", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+           "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
+           "data": "synthetic (seeded clustered-Gaussian DiT-shaped Q/K/V)",
+           "config": {"workload": f"{cfg.name}: H={cfg.H} N={cfg.N} d={cfg.d} {cfg.dtype} "
+                                  f"C={C} T={cfg.iters} {mode} {param}",
+                      "H": cfg.H, "N": cfg.N, "d": cfg.d, "C": C, "T": cfg.iters,
+                      "select": mode, "param": param},
+           "dense_equiv_tflops": round(dense_flops / (ms * 1e-3) / 1e12, 3),
+           "wall_s": round(wall, 3), "stages": stages, "roofline": roof}
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, q, k, v, min(args.cpu_heads, cfg.H))
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,230 @@
+/*
+ * park.h -- C ABI of the PARK sparse-attention forward on AMD Instinct MI355X
+ * (gfx950).  One DiT attention layer, all heads, one GPU.
+ *
+ * PARK ("Accurate Block Retrieval for Sparse Attention in Video Diffusion
+ * Transformers") computes, per attention head:
+ *   1. Euclidean k-means of the queries and QRKC k-means of the keys (keys
+ *      clustered under the stabilised query second-moment metric), then a
+ *      stable token permutation that makes every cluster a contiguous block
+ *      (Sec. 5.2, Alg. 3);
+ *   2. original-space key-block centroids c_v and sizes n_v (Eq. (8));
+ *   3. PAMA block importance W^_uv (every query scored against the key
+ *      centroids with a log n_v correction, softmax per query, averaged
+ *      within the query block, Eqs. (8)-(9)) and a top-k / top-p block mask
+ *      (Sec. 3.2, App. J);
+ *   4. block-sparse attention over the selected blocks, written back in the
+ *      original token order (Eq. (2)).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Tensors are [H][N][d] row-major and contiguous.  Q/K/V/Q'/K'/V' hold
+ *    dims->dtype elements (PARK_F32 or PARK_BF16); d must be 64 or 128.
+ *  - Every pointer argument except `dims`, `params` and `state` (which are
+ *    host structs) is a DEVICE pointer owned by the caller; the library
+ *    never allocates or frees device memory.  Device pointers must be
+ *    16-byte aligned.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Every call only enqueues work on it and returns without synchronising,
+ *    except park_check().
+ *  - Argument errors are detected on the host before anything is enqueued
+ *    and returned synchronously (PARK_ERR_INVALID_ARG, PARK_ERR_UNSUPPORTED,
+ *    PARK_ERR_WORKSPACE); the message is available from park_last_error()
+ *    (thread-local).  A failed launch returns PARK_ERR_HIP.  Numeric failures
+ *    found on the device (a metric that is not positive definite, non-finite
+ *    values) set bits of a status word kept in the first bytes of the
+ *    workspace.  Every call taking a workspace clears that word when it
+ *    starts, so it describes the most recent such call; read it with
+ *    park_check().  The workspace needs no initialisation.
+ *  - Cluster ids are int32 in [0, C); offsets arrays have C+1 entries with
+ *    offsets[0] = 0 and offsets[C] = N; permutations map a position of the
+ *    permuted order to the original token index (X'[i] = X[perm[i]]).
+ *  - Empty clusters are allowed (n_v = 0).  An empty key block is never
+ *    scored or selected; an empty query block gets kv_count = 0.
+ *  - Limits: 1 <= H, 1 <= C <= N, C <= 2048, N * d < 2^31, 1 <= T <= 1000.
+ */
+#ifndef PARK_H
+#define PARK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum park_status {
+  PARK_OK = 0,
+  PARK_ERR_INVALID_ARG = 1, /* null pointer, bad size, misalignment, bad enum */
+  PARK_ERR_UNSUPPORTED = 2, /* d not in {64,128}, C > 2048, ...              */
+  PARK_ERR_WORKSPACE = 3,   /* workspace smaller than park_workspace_size()  */
+  PARK_ERR_HIP = 4,         /* a HIP launch or runtime call failed           */
+  PARK_ERR_NUMERIC = 5      /* device-detected numeric failure (park_check)  */
+} park_status;
+
+typedef enum park_dtype { PARK_F32 = 0, PARK_BF16 = 1 } park_dtype;
+
+/* PARK_METRIC_EUCLID: plain Euclidean k-means (the query side, Sec. 5.2, and
+ * the "w/o QRKC" key side).  PARK_METRIC_QRKC: Euclidean k-means of K R where
+ * Gbar = R R^T is the stabilised query second moment (Alg. 3). */
+typedef enum park_metric { PARK_METRIC_EUCLID = 0, PARK_METRIC_QRKC = 1 } park_metric;
+
+/* PARK_SELECT_TOPK: keep ceil(ratio * CK) key blocks per query block (App. J).
+ * PARK_SELECT_TOPP: keep the shortest prefix, by decreasing W^ (ties by
+ * increasing block id), whose cumulative W^ reaches p (Sec. 3.2). */
+typedef enum park_select { PARK_SELECT_TOPK = 0, PARK_SELECT_TOPP = 1 } park_select;
+
+/* What park_forward recomputes (clustering/mask reuse across diffusion
+ * steps, Sec. 5.2 "Clustering and Reuse Strategy"). */
+typedef enum park_reuse {
+  PARK_RECOMPUTE = 0,              /* everything                                */
+  PARK_REUSE_CLUSTERS = 1,         /* keep permutations/offsets, redo the rest  */
+  PARK_REUSE_CLUSTERS_AND_MASK = 2 /* keep permutations, offsets and the mask   */
+} park_reuse;
+
+typedef struct park_dims {
+  int32_t H;     /* attention heads                      */
+  int32_t N;     /* tokens per head (L in the paper)     */
+  int32_t d;     /* head dimension: 64 or 128            */
+  int32_t dtype; /* park_dtype of Q, K, V and Q', K', V' */
+} park_dims;
+
+typedef struct park_params {
+  int32_t CQ;        /* query blocks N_Q (query clusters)                   */
+  int32_t CK;        /* key blocks N_K (key clusters)                       */
+  int32_t T;         /* k-means iterations (assign + update rounds)         */
+  int32_t select;    /* park_select                                          */
+  double topk_ratio; /* rho in (0, 1] for PARK_SELECT_TOPK                   */
+  double topp;       /* p in (0, 1] for PARK_SELECT_TOPP                     */
+  double alpha;      /* shrinkage in [0, 1] (paper: 0.05)                    */
+  double eps;        /* stability constant >= 0 (1e-6)                       */
+  double s_min;      /* floor of the metric scale (paper: 1e-12)             */
+  uint64_t seed;     /* k-means initialisation seed                          */
+  int32_t key_metric;/* park_metric for the keys (PARK_METRIC_QRKC)          */
+  int32_t out_dtype; /* park_dtype of O                                      */
+} park_params;
+
+/* Caller-allocated device buffers carried across park_forward calls. */
+typedef struct park_state {
+  int32_t* q_perm;     /* [H][N]                                  */
+  int32_t* k_perm;     /* [H][N]                                  */
+  int32_t* q_offsets;  /* [H][CQ+1]                               */
+  int32_t* k_offsets;  /* [H][CK+1]                               */
+  float* k_centroids;  /* [H][CK][d]  original-space c_v          */
+  int32_t* k_sizes;    /* [H][CK]     n_v                         */
+  int32_t* kv_count;   /* [H][CQ]     selected key blocks per row */
+  int32_t* kv_index;   /* [H][CQ][CK] ascending block ids         */
+  void* Qp;            /* [H][N][d]   permuted queries (dtype)    */
+  void* Kp;            /* [H][N][d]   permuted keys               */
+  void* Vp;            /* [H][N][d]   permuted values             */
+  float* W;            /* [H][CQ][CK] W^ (optional, may be NULL)  */
+} park_state;
+
+/* Bytes of workspace any call below needs for these sizes (the maximum over
+ * park_cluster_keys with C = max(CQ, CK), park_retrieve_blocks and
+ * park_forward).  Host-only; never fails for valid dims. */
+park_status park_workspace_size(const park_dims* dims, int32_t CQ, int32_t CK, size_t* bytes);
+
+/* Stage 1 -- k-means clustering of one side and its stable permutation.
+ * Sec. 5.2 "Clustering and Reuse Strategy" and Alg. 3 (QRKC).
+ *   X        [H][N][d] dtype   points to cluster (queries or keys)
+ *   Qmetric  [H][N][d] dtype   queries defining Gbar (QRKC only, else NULL)
+ *   C, T, seed, side           clusters, iterations, seed; side 0 = queries,
+ *                              1 = keys (selects the initialisation stream)
+ *   metric                     park_metric
+ *   alpha, eps, s_min          metric stabilisation (QRKC only)
+ *   labels   [H][N] int32      labels of the T-th assignment (may be NULL)
+ *   perm     [H][N] int32      stable argsort of the labels
+ *   offsets  [H][C+1] int32    cluster boundaries in the permuted order
+ *   R_out    [H][d][d] double  lower Cholesky factor, Gbar = R R^T (QRKC,
+ *                              may be NULL)
+ *   Xt_out   [H][N][d] float   transformed points X R (QRKC, may be NULL;
+ *                              diagnostic, not needed by the hot path)
+ * Initialisation: the first C entries of a Fisher-Yates shuffle of the token
+ * indices driven by SplitMix64 seeded with seed ^ (0x9E3779B97F4A7C15 *
+ * (2*h + side + 1)).  Labels are exact argmins of the float64 distances
+ * (ties to the lowest id); an empty cluster keeps its centroid. */
+park_status park_cluster_keys(const void* X, const void* Qmetric, const park_dims* dims,
+                              int32_t C, int32_t T, uint64_t seed, int32_t side,
+                              int32_t metric, double alpha, double eps, double s_min,
+                              int32_t* labels, int32_t* perm, int32_t* offsets,
+                              double* R_out, float* Xt_out, void* ws, size_t ws_bytes,
+                              void* stream);
+
+/* Row gather X'[h][i] = X[h][perm[h][i]] (Alg. 3, K' and V').
+ *   X, Xp  [H][N][d] dtype;  perm [H][N] int32 (a permutation of 0..N-1). */
+park_status park_gather_rows(const void* X, const int32_t* perm, const park_dims* dims,
+                             void* Xp, void* stream);
+
+/* Stage 2 -- key-block centroids in the original key space (Eq. (8), Alg. 3):
+ * c_v = mean of X[perm[i]] over offsets[v] <= i < offsets[v+1], accumulated
+ * in float64 and rounded to float; sizes[v] = n_v.  Empty blocks give c = 0.
+ * Passing X' with the identity permutation is equivalent.
+ *   centroids [H][C][d] float;  sizes [H][C] int32. */
+park_status park_block_centroids(const void* X, const int32_t* perm, const int32_t* offsets,
+                                 const park_dims* dims, int32_t C, float* centroids,
+                                 int32_t* sizes, void* stream);
+
+/* Stage 3 -- PAMA retrieval and mask selection (Eqs. (8)-(9), Alg. 1-2,
+ * Sec. 3.2, App. J).
+ *   Qp         [H][N][d] dtype   permuted queries
+ *   q_offsets  [H][CQ+1]         query-block boundaries
+ *   centroids  [H][CK][d] float  key-block centroids;  k_sizes [H][CK] int32
+ *   select     park_select;  param = ratio (TOPK) or p (TOPP), in (0, 1]
+ *   W_out      [H][CQ][CK] float W^ (may be NULL)
+ *   kv_count   [H][CQ] int32;  kv_index [H][CQ][CK] int32, the first
+ *              kv_count entries of each row hold the selected ids ascending.
+ * The mask equals the one obtained from float64 W^ (rows whose fast-path
+ * margin is below its error bound are recomputed in float64). */
+park_status park_retrieve_blocks(const void* Qp, const int32_t* q_offsets, const float* centroids,
+                                 const int32_t* k_sizes, const park_dims* dims, int32_t CQ,
+                                 int32_t CK, int32_t select, double param, float* W_out,
+                                 int32_t* kv_count, int32_t* kv_index, void* ws,
+                                 size_t ws_bytes, void* stream);
+
+/* Stage 4 -- block-sparse attention with un-permutation (Eq. (2)).
+ * For each query block u and each permuted query row i in it:
+ *   O[h][q_perm[h][i]] = softmax_j(q_i . k_j / sqrt(d)) v_j over the keys j of
+ *   the selected key blocks of u (softmax renormalised over those keys).
+ *   Qp, Kp, Vp [H][N][d] dtype;  O [H][N][d] out_dtype (PARK_F32 or PARK_BF16,
+ *   bf16 by round-to-nearest-even).  Rows of empty query blocks do not exist;
+ *   every token is written exactly once. */
+park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* Vp,
+                                   const int32_t* q_offsets, const int32_t* k_offsets,
+                                   const int32_t* kv_count, const int32_t* kv_index,
+                                   const int32_t* q_perm, const park_dims* dims, int32_t CQ,
+                                   int32_t CK, void* O, int32_t out_dtype, void* stream);
+
+/* The whole layer: stages 1-4 on Q, K, V [H][N][d] (dtype), output O
+ * [H][N][d] (params->out_dtype) in the original token order.  `state` holds
+ * caller-allocated buffers that receive (RECOMPUTE) or supply (REUSE_*) the
+ * clustering and mask.  With PARK_REUSE_CLUSTERS the permutations and offsets
+ * of `state` are reused and gathers, centroids, retrieval and attention run
+ * on the new tensors; PARK_REUSE_CLUSTERS_AND_MASK also reuses the mask. */
+park_status park_forward(const void* Q, const void* K, const void* V, const park_dims* dims,
+                         const park_params* params, int32_t reuse, const park_state* state,
+                         void* O, void* ws, size_t ws_bytes, void* stream);
+
+/* Synchronises `stream`, returns the sticky device status recorded in the
+ * workspace `ws` (PARK_OK or PARK_ERR_NUMERIC) and clears it. */
+park_status park_check(void* ws, void* stream);
+
+/* Static description of a status code. */
+const char* park_status_string(park_status s);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* park_last_error(void);
+
+/* Per-kernel timing with HIP events on the launch stream (off by default).
+ * park_profile_enable(1) starts recording around every kernel launch;
+ * park_profile_read() synchronises outstanding events and writes a JSON object
+ * {"kernel": {"launches": n, "ms": total}, ...} into buf (truncated to cap). */
+park_status park_profile_enable(int32_t on);
+park_status park_profile_reset(void);
+park_status park_profile_read(char* buf, size_t cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PARK_H */

@@ -1,0 +1,156 @@
+// Stable counting sort of cluster labels (pi = argsort(z), Alg. 3) and the
+// row gathers X' = X[pi].  Three passes: per-tile histograms, one exclusive
+// scan per head in (cluster, tile) order, and a stable scatter in which each
+// tile walks its tokens in order one wavefront (64 tokens) at a time.  All
+// integer work; the result is unique, so it is bit-exact and deterministic.
+#include "common.h"
+#include "kernels.h"
+
+namespace park {
+
+constexpr int SORT_TILE = 2048;
+
+int sort_tiles(int N) { return (N + SORT_TILE - 1) / SORT_TILE; }
+
+// thist[h][v][tile] = #{ i in tile : z_i = v }
+__global__ __launch_bounds__(256) void k_sort_hist(const int* __restrict__ labels, int N, int C,
+                                                   int* __restrict__ thist) {
+  extern __shared__ int hist[];
+  const int h = blockIdx.y, tile = blockIdx.x, nt = gridDim.x;
+  for (int v = threadIdx.x; v < C; v += 256) hist[v] = 0;
+  __syncthreads();
+  const int i0 = tile * SORT_TILE, i1 = min(N, i0 + SORT_TILE);
+  const int* z = labels + (size_t)h * N;
+  for (int i = i0 + threadIdx.x; i < i1; i += 256) {
+    const int v = z[i];
+    if ((unsigned)v < (unsigned)C) atomicAdd(&hist[v], 1);
+  }
+  __syncthreads();
+  int* out = thist + (size_t)h * C * nt;
+  for (int v = threadIdx.x; v < C; v += 256) out[(size_t)v * nt + tile] = hist[v];
+}
+
+// In-place exclusive scan of thist[h] (C*nt entries, cluster-major) and the
+// cluster offsets o[v] = first position of cluster v, o[C] = N.
+__global__ __launch_bounds__(1024) void k_sort_scan(int* __restrict__ thist, int C, int nt, int N,
+                                                    int* __restrict__ offsets) {
+  __shared__ int wsum[16];
+  __shared__ int carry_s;
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  int* a = thist + (size_t)h * C * nt;
+  const int total = C * nt;
+  if (tid == 0) carry_s = 0;
+  __syncthreads();
+  for (int base = 0; base < total; base += 4096) {
+    int x[4];
+    int s = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int idx = base + tid * 4 + k;
+      x[k] = idx < total ? a[idx] : 0;
+      s += x[k];
+    }
+    // inclusive scan of per-thread sums within the wave
+    int inc = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(inc, o, 64);
+      if (lane >= o) inc += y;
+    }
+    if (lane == 63) wsum[wid] = inc;
+    __syncthreads();
+    int wpre = 0, blk = 0;
+    for (int w = 0; w < 16; ++w) {
+      if (w < wid) wpre += wsum[w];
+      blk += wsum[w];
+    }
+    const int carry = carry_s;
+    int run = carry + wpre + inc - s;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int idx = base + tid * 4 + k;
+      if (idx < total) {
+        a[idx] = run;
+        if (idx % nt == 0) offsets[(size_t)h * (C + 1) + idx / nt] = run;
+      }
+      run += x[k];
+    }
+    __syncthreads();
+    if (tid == 0) carry_s = carry + blk;
+    __syncthreads();
+  }
+  if (tid == 0) offsets[(size_t)h * (C + 1) + C] = N;
+}
+
+// Stable scatter: one wavefront per tile, tokens in increasing order.
+// Equal labels inside a wave are matched with one ballot per label bit.
+__global__ __launch_bounds__(64) void k_sort_scatter(const int* __restrict__ labels, int N, int C,
+                                                     int nbits, const int* __restrict__ tbase,
+                                                     int* __restrict__ perm) {
+  extern __shared__ int run[];
+  const int h = blockIdx.y, tile = blockIdx.x, nt = gridDim.x, lane = threadIdx.x;
+  const int* b = tbase + (size_t)h * C * nt;
+  for (int v = lane; v < C; v += 64) run[v] = b[(size_t)v * nt + tile];
+  __syncthreads();
+  const int i0 = tile * SORT_TILE, i1 = min(N, i0 + SORT_TILE);
+  const int* z = labels + (size_t)h * N;
+  int* p = perm + (size_t)h * N;
+  const uint64_t lt = (1ull << lane) - 1ull;
+  const uint64_t gt = ~((2ull << lane) - 1ull);
+  for (int c0 = i0; c0 < i1; c0 += 64) {
+    const int i = c0 + lane;
+    const bool valid = i < i1;
+    int v = valid ? z[i] : 0;
+    const bool ok = valid && (unsigned)v < (unsigned)C;
+    uint64_t m = __ballot(ok);
+    for (int bit = 0; bit < nbits; ++bit) {
+      const bool set = (v >> bit) & 1;
+      const uint64_t B = __ballot(ok && set);
+      m &= set ? B : ~B;
+    }
+    const int rank = __popcll(m & lt);
+    if (ok) p[run[v] + rank] = i;
+    __syncthreads();
+    if (ok && (m & gt) == 0) run[v] += rank + 1;
+    __syncthreads();
+  }
+}
+
+park_status launch_count_sort(const int* labels, int H, int N, int C, int* thist, int* perm,
+                              int* offsets, hipStream_t st) {
+  const int nt = sort_tiles(N);
+  const size_t lds = (size_t)C * sizeof(int);
+  int nbits = 1;
+  while ((1 << nbits) < C) ++nbits;
+  PARK_LAUNCH("sort_hist", k_sort_hist, dim3(nt, H), dim3(256), lds, st, labels, N, C, thist);
+  PARK_LAUNCH("sort_scan", k_sort_scan, dim3(H), dim3(1024), 0, st, thist, C, nt, N, offsets);
+  PARK_LAUNCH("sort_scatter", k_sort_scatter, dim3(nt, H), dim3(64), lds, st, labels, N, C, nbits,
+              (const int*)thist, perm);
+  return PARK_OK;
+}
+
+// Xp[h][i] = X[h][perm[h][i]], 16-byte vectors.
+__global__ __launch_bounds__(256) void k_gather(const uint4* __restrict__ X, const int* __restrict__ perm,
+                                                int N, int vpr, uint4* __restrict__ Xp) {
+  const int h = blockIdx.y;
+  const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t total = (size_t)N * vpr;
+  if (t >= total) return;
+  const int i = (int)(t / vpr), c = (int)(t % vpr);
+  const int src = perm[(size_t)h * N + i];
+  uint4 val = make_uint4(0u, 0u, 0u, 0u);
+  if ((unsigned)src < (unsigned)N) val = X[((size_t)h * N + src) * vpr + c];
+  Xp[((size_t)h * N + i) * vpr + c] = val;
+}
+
+park_status launch_gather(const void* X, const int* perm, int H, int N, int D, int dtype, void* Xp,
+                          hipStream_t st) {
+  const int vpr = (int)(D * elem_size(dtype) / 16);
+  const size_t total = (size_t)N * vpr;
+  dim3 g((unsigned)((total + 255) / 256), H);
+  PARK_LAUNCH("gather_rows", k_gather, g, dim3(256), 0, st, (const uint4*)X, perm, N, vpr,
+              (uint4*)Xp);
+  return PARK_OK;
+}
+
+}  // namespace park

@@ -1,0 +1,60 @@
+// Host launchers of the PARK kernels (one group per .hip file).
+#pragma once
+
+#include "common.h"
+
+namespace park {
+
+// k_metric.hip --------------------------------------------------------------
+size_t gram_chunks(int H, int N);
+park_status launch_metric(const void* Q, int H, int N, int D, int dtype, double alpha, double eps,
+                          double s_min, double* part, double* G, double* Gbar, double* R,
+                          int* status, hipStream_t st);
+park_status launch_transform(const void* X, const double* R, int H, int N, int D, int dtype,
+                             float* Xt, hipStream_t st);
+
+// k_sort.hip ----------------------------------------------------------------
+int sort_tiles(int N);
+// Stable counting sort of labels[h][0..N) into perm/offsets (+ sizes).
+park_status launch_count_sort(const int* labels, int H, int N, int C, int* thist, int* perm,
+                              int* offsets, hipStream_t st);
+park_status launch_gather(const void* X, const int* perm, int H, int N, int D, int dtype, void* Xp,
+                          hipStream_t st);
+
+// k_kmeans.hip --------------------------------------------------------------
+struct KmeansBufs {
+  int* init;      // [H][C]
+  double* mu;     // [H][C][D] centroids in the input space
+  double* w;      // [H][C][D] metric applied to the centroids
+  double* b;      // [H][C]    mu^T w
+  int* labels;    // [H][N]
+  int* thist;     // sort tile histograms
+  int* perm;      // [H][N]
+  int* offsets;   // [H][C+1]
+  int* status;    // sticky device status word
+};
+park_status launch_kmeans(const void* X, const double* Gbar /* null = Euclidean */, int H, int N,
+                          int D, int dtype, int C, int T, uint64_t seed, int side,
+                          const KmeansBufs& kb, hipStream_t st);
+park_status launch_segment_mean(const void* X, const int* perm, const int* offsets, int H, int N,
+                                int D, int dtype, int C, double* mu64, float* c32, int* sizes,
+                                hipStream_t st);
+
+// k_pama.hip ----------------------------------------------------------------
+park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
+                          const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
+                          double* W64, float* W32, int* status, hipStream_t st);
+park_status launch_select(const double* W64, const int* q_offsets, const int* k_sizes, int H,
+                          int CQ, int CK, int mode, double param, int* kv_count, int* kv_index,
+                          hipStream_t st);
+
+// k_attn.hip ----------------------------------------------------------------
+park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,
+                             const int* k_offsets, const int* kv_count, const int* kv_index,
+                             const int* q_perm, int H, int N, int D, int dtype, int CQ, int CK,
+                             void* O, int out_dtype, hipStream_t st);
+
+// misc ----------------------------------------------------------------------
+park_status launch_clear_status(int* status, hipStream_t st);
+
+}  // namespace park

@@ -1,0 +1,492 @@
+// Host side of the PARK C ABI: argument validation, workspace layout, stage
+// orchestration, status reporting and the optional per-kernel profiler.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace park {
+
+// ------------------------------------------------------------ last error
+static thread_local char g_err[512] = "";
+
+park_status fail(park_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+// ------------------------------------------------------------ profiler
+namespace {
+struct ProfRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+std::mutex g_pmu;
+bool g_prof = false;
+std::vector<hipEvent_t> g_pool;
+std::vector<ProfRec> g_recs;
+thread_local ProfRec g_open = {nullptr, nullptr, nullptr};
+
+hipEvent_t take_event() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+}  // namespace
+
+void prof_begin(const char* name, hipStream_t s) {
+  std::lock_guard<std::mutex> lk(g_pmu);
+  if (!g_prof) return;
+  g_open.name = name;
+  g_open.a = take_event();
+  g_open.b = take_event();
+  if (g_open.a) hipEventRecord(g_open.a, s);
+}
+
+void prof_end(hipStream_t s) {
+  std::lock_guard<std::mutex> lk(g_pmu);
+  if (!g_prof || !g_open.name) return;
+  if (g_open.b) hipEventRecord(g_open.b, s);
+  if (g_open.a && g_open.b) g_recs.push_back(g_open);
+  g_open = {nullptr, nullptr, nullptr};
+}
+
+// ------------------------------------------------------------ small kernels
+__global__ void k_clear_int(int* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+park_status launch_clear_status(int* status, hipStream_t st) {
+  PARK_LAUNCH("clear_status", k_clear_int, dim3(1), dim3(64), 0, st, status, 1);
+  return PARK_OK;
+}
+
+// ------------------------------------------------------------ validation
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+static park_status check_dims(const park_dims* dims) {
+  if (!dims) return fail(PARK_ERR_INVALID_ARG, "dims is NULL");
+  if (dims->H < 1 || dims->N < 1) return fail(PARK_ERR_INVALID_ARG, "need H >= 1 and N >= 1");
+  if (dims->d != 64 && dims->d != 128)
+    return fail(PARK_ERR_UNSUPPORTED, "head dimension %d not supported (64 or 128)", dims->d);
+  if (dims->dtype != PARK_F32 && dims->dtype != PARK_BF16)
+    return fail(PARK_ERR_INVALID_ARG, "unknown dtype %d", dims->dtype);
+  if ((int64_t)dims->N * dims->d >= ((int64_t)1 << 31))
+    return fail(PARK_ERR_UNSUPPORTED, "N * d must be below 2^31");
+  return PARK_OK;
+}
+
+static park_status check_C(int C, int N, const char* what) {
+  if (C < 1 || C > N) return fail(PARK_ERR_INVALID_ARG, "%s = %d must be in [1, N = %d]", what, C, N);
+  if (C > 2048) return fail(PARK_ERR_UNSUPPORTED, "%s = %d exceeds 2048", what, C);
+  return PARK_OK;
+}
+
+static park_status check_ptr(const void* p, const char* what) {
+  if (!p) return fail(PARK_ERR_INVALID_ARG, "%s is NULL", what);
+  if (!aligned16(p)) return fail(PARK_ERR_INVALID_ARG, "%s is not 16-byte aligned", what);
+  return PARK_OK;
+}
+
+static park_status check_opt_ptr(const void* p, const char* what) {
+  if (p && !aligned16(p)) return fail(PARK_ERR_INVALID_ARG, "%s is not 16-byte aligned", what);
+  return PARK_OK;
+}
+
+static park_status check_select(int mode, double param) {
+  if (mode != PARK_SELECT_TOPK && mode != PARK_SELECT_TOPP)
+    return fail(PARK_ERR_INVALID_ARG, "unknown selection mode %d", mode);
+  if (!(param > 0.0 && param <= 1.0))
+    return fail(PARK_ERR_INVALID_ARG, "selection parameter %g must be in (0, 1]", param);
+  return PARK_OK;
+}
+
+// ------------------------------------------------------------ workspace
+struct ClusterWs {
+  int* init;
+  double* part;
+  double* G;
+  double* Gbar;
+  double* R;
+  double* mu;
+  double* w;
+  double* b;
+  int* labels;
+  int* thist;
+};
+
+static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
+  ClusterWs c;
+  c.init = cv.take<int>((size_t)H * C);
+  c.part = cv.take<double>((size_t)H * gram_chunks(H, N) * D * D);
+  c.G = cv.take<double>((size_t)H * D * D);
+  c.Gbar = cv.take<double>((size_t)H * D * D);
+  c.R = cv.take<double>((size_t)H * D * D);
+  c.mu = cv.take<double>((size_t)H * C * D);
+  c.w = cv.take<double>((size_t)H * C * D);
+  c.b = cv.take<double>((size_t)H * C);
+  c.labels = cv.take<int>((size_t)H * N);
+  c.thist = cv.take<int>((size_t)H * C * sort_tiles(N));
+  return c;
+}
+
+struct RetrieveWs {
+  double* W64;
+};
+
+static RetrieveWs carve_retrieve(Carver& cv, int H, int CQ, int CK) {
+  RetrieveWs r;
+  r.W64 = cv.take<double>((size_t)H * CQ * CK);
+  return r;
+}
+
+// status word first, then the larger of the cluster and retrieval regions
+static size_t ws_bytes_for(int H, int N, int D, int CQ, int CK) {
+  Carver a(nullptr);
+  a.take<int>(64);
+  const size_t base = a.off;
+  Carver c1(nullptr);
+  c1.off = base;
+  carve_cluster(c1, H, N, D, std::max(CQ, CK));
+  Carver c2(nullptr);
+  c2.off = base;
+  carve_retrieve(c2, H, CQ, CK);
+  return std::max(c1.off, c2.off) + 256;
+}
+
+static park_status check_ws(void* ws, size_t ws_bytes, size_t need) {
+  PARK_TRY(check_ptr(ws, "workspace"));
+  if (ws_bytes < need)
+    return fail(PARK_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required",
+                ws_bytes, need);
+  return PARK_OK;
+}
+
+// ------------------------------------------------------------ stage bodies
+static park_status cluster_body(const void* X, const void* Qm, const park_dims& dm, int C, int T,
+                                uint64_t seed, int side, int metric, double alpha, double eps,
+                                double s_min, int* labels, int* perm, int* offsets, double* R_out,
+                                float* Xt_out, void* ws, hipStream_t st) {
+  const int H = dm.H, N = dm.N, D = dm.d;
+  Carver cv(ws);
+  int* status = cv.take<int>(64);
+  ClusterWs cw = carve_cluster(cv, H, N, D, C);
+  const double* Gbar = nullptr;
+  if (metric == PARK_METRIC_QRKC) {
+    double* R = R_out ? R_out : cw.R;
+    PARK_TRY(launch_metric(Qm, H, N, D, dm.dtype, alpha, eps, s_min, cw.part, cw.G, cw.Gbar, R,
+                           status, st));
+    Gbar = cw.Gbar;
+    if (Xt_out) PARK_TRY(launch_transform(X, R, H, N, D, dm.dtype, Xt_out, st));
+  }
+  KmeansBufs kb;
+  kb.init = cw.init;
+  kb.mu = cw.mu;
+  kb.w = cw.w;
+  kb.b = cw.b;
+  kb.labels = labels ? labels : cw.labels;
+  kb.thist = cw.thist;
+  kb.perm = perm;
+  kb.offsets = offsets;
+  kb.status = status;
+  return launch_kmeans(X, Gbar, H, N, D, dm.dtype, C, T, seed, side, kb, st);
+}
+
+static park_status retrieve_body(const void* Qp, const int* q_offsets, const float* cen,
+                                 const int* k_sizes, const park_dims& dm, int CQ, int CK,
+                                 int mode, double param, float* W_out, int* kv_count,
+                                 int* kv_index, void* ws, hipStream_t st) {
+  Carver cv(ws);
+  int* status = cv.take<int>(64);
+  RetrieveWs rw = carve_retrieve(cv, dm.H, CQ, CK);
+  PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, dm.H, dm.N, dm.d, dm.dtype, CQ, CK, rw.W64,
+                         W_out, status, st));
+  return launch_select(rw.W64, q_offsets, k_sizes, dm.H, CQ, CK, mode, param, kv_count, kv_index,
+                       st);
+}
+
+}  // namespace park
+
+using namespace park;
+
+// ============================================================ C ABI
+extern "C" {
+
+const char* park_status_string(park_status s) {
+  switch (s) {
+    case PARK_OK: return "ok";
+    case PARK_ERR_INVALID_ARG: return "invalid argument";
+    case PARK_ERR_UNSUPPORTED: return "unsupported configuration";
+    case PARK_ERR_WORKSPACE: return "workspace too small";
+    case PARK_ERR_HIP: return "HIP runtime error";
+    case PARK_ERR_NUMERIC: return "numeric failure on the device";
+  }
+  return "unknown status";
+}
+
+const char* park_last_error(void) { return g_err; }
+
+park_status park_workspace_size(const park_dims* dims, int32_t CQ, int32_t CK, size_t* bytes) {
+  g_err[0] = 0;
+  PARK_TRY(check_dims(dims));
+  if (!bytes) return fail(PARK_ERR_INVALID_ARG, "bytes is NULL");
+  PARK_TRY(check_C(CQ, dims->N, "CQ"));
+  PARK_TRY(check_C(CK, dims->N, "CK"));
+  *bytes = ws_bytes_for(dims->H, dims->N, dims->d, CQ, CK);
+  return PARK_OK;
+}
+
+park_status park_cluster_keys(const void* X, const void* Qmetric, const park_dims* dims, int32_t C,
+                              int32_t T, uint64_t seed, int32_t side, int32_t metric, double alpha,
+                              double eps, double s_min, int32_t* labels, int32_t* perm,
+                              int32_t* offsets, double* R_out, float* Xt_out, void* ws,
+                              size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  PARK_TRY(check_dims(dims));
+  PARK_TRY(check_C(C, dims->N, "C"));
+  if (T < 1 || T > 1000) return fail(PARK_ERR_INVALID_ARG, "T = %d must be in [1, 1000]", T);
+  if (side != 0 && side != 1) return fail(PARK_ERR_INVALID_ARG, "side must be 0 or 1");
+  if (metric != PARK_METRIC_EUCLID && metric != PARK_METRIC_QRKC)
+    return fail(PARK_ERR_INVALID_ARG, "unknown metric %d", metric);
+  PARK_TRY(check_ptr(X, "X"));
+  PARK_TRY(check_ptr(perm, "perm"));
+  PARK_TRY(check_ptr(offsets, "offsets"));
+  PARK_TRY(check_opt_ptr(labels, "labels"));
+  if (metric == PARK_METRIC_QRKC) {
+    PARK_TRY(check_ptr(Qmetric, "Qmetric"));
+    if (!(alpha >= 0.0 && alpha <= 1.0)) return fail(PARK_ERR_INVALID_ARG, "alpha must be in [0, 1]");
+    if (!(eps >= 0.0) || !(s_min > 0.0) || eps > 1e300 || s_min > 1e300)
+      return fail(PARK_ERR_INVALID_ARG, "need eps >= 0 and s_min > 0, both finite");
+    PARK_TRY(check_opt_ptr(R_out, "R_out"));
+    PARK_TRY(check_opt_ptr(Xt_out, "Xt_out"));
+  } else if (R_out || Xt_out) {
+    return fail(PARK_ERR_INVALID_ARG, "R_out / Xt_out need the QRKC metric");
+  }
+  PARK_TRY(check_ws(ws, ws_bytes, ws_bytes_for(dims->H, dims->N, dims->d, C, C)));
+  hipStream_t st = (hipStream_t)stream;
+  Carver cv(ws);
+  PARK_TRY(launch_clear_status(cv.take<int>(64), st));
+  return cluster_body(X, Qmetric, *dims, C, T, seed, side, metric, alpha, eps, s_min, labels, perm,
+                      offsets, R_out, Xt_out, ws, st);
+}
+
+park_status park_gather_rows(const void* X, const int32_t* perm, const park_dims* dims, void* Xp,
+                             void* stream) {
+  g_err[0] = 0;
+  PARK_TRY(check_dims(dims));
+  PARK_TRY(check_ptr(X, "X"));
+  PARK_TRY(check_ptr(perm, "perm"));
+  PARK_TRY(check_ptr(Xp, "Xp"));
+  return launch_gather(X, perm, dims->H, dims->N, dims->d, dims->dtype, Xp, (hipStream_t)stream);
+}
+
+park_status park_block_centroids(const void* X, const int32_t* perm, const int32_t* offsets,
+                                 const park_dims* dims, int32_t C, float* centroids,
+                                 int32_t* sizes, void* stream) {
+  g_err[0] = 0;
+  PARK_TRY(check_dims(dims));
+  PARK_TRY(check_C(C, dims->N, "C"));
+  PARK_TRY(check_ptr(X, "X"));
+  PARK_TRY(check_ptr(perm, "perm"));
+  PARK_TRY(check_ptr(offsets, "offsets"));
+  PARK_TRY(check_ptr(centroids, "centroids"));
+  PARK_TRY(check_ptr(sizes, "sizes"));
+  return launch_segment_mean(X, perm, offsets, dims->H, dims->N, dims->d, dims->dtype, C, nullptr,
+                             centroids, sizes, (hipStream_t)stream);
+}
+
+park_status park_retrieve_blocks(const void* Qp, const int32_t* q_offsets, const float* centroids,
+                                 const int32_t* k_sizes, const park_dims* dims, int32_t CQ,
+                                 int32_t CK, int32_t select, double param, float* W_out,
+                                 int32_t* kv_count, int32_t* kv_index, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  g_err[0] = 0;
+  PARK_TRY(check_dims(dims));
+  PARK_TRY(check_C(CQ, dims->N, "CQ"));
+  PARK_TRY(check_C(CK, dims->N, "CK"));
+  PARK_TRY(check_select(select, param));
+  PARK_TRY(check_ptr(Qp, "Qp"));
+  PARK_TRY(check_ptr(q_offsets, "q_offsets"));
+  PARK_TRY(check_ptr(centroids, "centroids"));
+  PARK_TRY(check_ptr(k_sizes, "k_sizes"));
+  PARK_TRY(check_ptr(kv_count, "kv_count"));
+  PARK_TRY(check_ptr(kv_index, "kv_index"));
+  PARK_TRY(check_opt_ptr(W_out, "W_out"));
+  PARK_TRY(check_ws(ws, ws_bytes, ws_bytes_for(dims->H, dims->N, dims->d, CQ, CK)));
+  hipStream_t st = (hipStream_t)stream;
+  Carver cv(ws);
+  PARK_TRY(launch_clear_status(cv.take<int>(64), st));
+  return retrieve_body(Qp, q_offsets, centroids, k_sizes, *dims, CQ, CK, select, param, W_out,
+                       kv_count, kv_index, ws, st);
+}
+
+park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* Vp,
+                                   const int32_t* q_offsets, const int32_t* k_offsets,
+                                   const int32_t* kv_count, const int32_t* kv_index,
+                                   const int32_t* q_perm, const park_dims* dims, int32_t CQ,
+                                   int32_t CK, void* O, int32_t out_dtype, void* stream) {
+  g_err[0] = 0;
+  PARK_TRY(check_dims(dims));
+  PARK_TRY(check_C(CQ, dims->N, "CQ"));
+  PARK_TRY(check_C(CK, dims->N, "CK"));
+  if (out_dtype != PARK_F32 && out_dtype != PARK_BF16)
+    return fail(PARK_ERR_INVALID_ARG, "unknown out_dtype %d", out_dtype);
+  PARK_TRY(check_ptr(Qp, "Qp"));
+  PARK_TRY(check_ptr(Kp, "Kp"));
+  PARK_TRY(check_ptr(Vp, "Vp"));
+  PARK_TRY(check_ptr(q_offsets, "q_offsets"));
+  PARK_TRY(check_ptr(k_offsets, "k_offsets"));
+  PARK_TRY(check_ptr(kv_count, "kv_count"));
+  PARK_TRY(check_ptr(kv_index, "kv_index"));
+  PARK_TRY(check_ptr(q_perm, "q_perm"));
+  PARK_TRY(check_ptr(O, "O"));
+  return launch_attention(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, dims->H,
+                          dims->N, dims->d, dims->dtype, CQ, CK, O, out_dtype,
+                          (hipStream_t)stream);
+}
+
+park_status park_forward(const void* Q, const void* K, const void* V, const park_dims* dims,
+                         const park_params* p, int32_t reuse, const park_state* s, void* O,
+                         void* ws, size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  PARK_TRY(check_dims(dims));
+  if (!p) return fail(PARK_ERR_INVALID_ARG, "params is NULL");
+  if (!s) return fail(PARK_ERR_INVALID_ARG, "state is NULL");
+  PARK_TRY(check_C(p->CQ, dims->N, "CQ"));
+  PARK_TRY(check_C(p->CK, dims->N, "CK"));
+  if (p->T < 1 || p->T > 1000) return fail(PARK_ERR_INVALID_ARG, "T must be in [1, 1000]");
+  const double param = p->select == PARK_SELECT_TOPK ? p->topk_ratio : p->topp;
+  PARK_TRY(check_select(p->select, param));
+  if (p->key_metric != PARK_METRIC_EUCLID && p->key_metric != PARK_METRIC_QRKC)
+    return fail(PARK_ERR_INVALID_ARG, "unknown key metric %d", p->key_metric);
+  if (!(p->alpha >= 0.0 && p->alpha <= 1.0) || !(p->eps >= 0.0) || !(p->s_min > 0.0) ||
+      p->eps > 1e300 || p->s_min > 1e300)
+    return fail(PARK_ERR_INVALID_ARG, "need alpha in [0,1], eps >= 0, s_min > 0");
+  if (p->out_dtype != PARK_F32 && p->out_dtype != PARK_BF16)
+    return fail(PARK_ERR_INVALID_ARG, "unknown out_dtype %d", p->out_dtype);
+  if (reuse < PARK_RECOMPUTE || reuse > PARK_REUSE_CLUSTERS_AND_MASK)
+    return fail(PARK_ERR_INVALID_ARG, "unknown reuse mode %d", reuse);
+  PARK_TRY(check_ptr(Q, "Q"));
+  PARK_TRY(check_ptr(K, "K"));
+  PARK_TRY(check_ptr(V, "V"));
+  PARK_TRY(check_ptr(O, "O"));
+  PARK_TRY(check_ptr(s->q_perm, "state.q_perm"));
+  PARK_TRY(check_ptr(s->k_perm, "state.k_perm"));
+  PARK_TRY(check_ptr(s->q_offsets, "state.q_offsets"));
+  PARK_TRY(check_ptr(s->k_offsets, "state.k_offsets"));
+  PARK_TRY(check_ptr(s->k_centroids, "state.k_centroids"));
+  PARK_TRY(check_ptr(s->k_sizes, "state.k_sizes"));
+  PARK_TRY(check_ptr(s->kv_count, "state.kv_count"));
+  PARK_TRY(check_ptr(s->kv_index, "state.kv_index"));
+  PARK_TRY(check_ptr(s->Qp, "state.Qp"));
+  PARK_TRY(check_ptr(s->Kp, "state.Kp"));
+  PARK_TRY(check_ptr(s->Vp, "state.Vp"));
+  PARK_TRY(check_opt_ptr(s->W, "state.W"));
+  const int H = dims->H, N = dims->N, D = dims->d;
+  PARK_TRY(check_ws(ws, ws_bytes, ws_bytes_for(H, N, D, p->CQ, p->CK)));
+  hipStream_t st = (hipStream_t)stream;
+  Carver cv(ws);
+  PARK_TRY(launch_clear_status(cv.take<int>(64), st));
+  if (reuse == PARK_RECOMPUTE) {
+    PARK_TRY(cluster_body(Q, nullptr, *dims, p->CQ, p->T, p->seed, 0, PARK_METRIC_EUCLID, 0, 0, 1,
+                          nullptr, s->q_perm, s->q_offsets, nullptr, nullptr, ws, st));
+    PARK_TRY(cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha, p->eps,
+                          p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr, nullptr, ws, st));
+  }
+  PARK_TRY(launch_gather(Q, s->q_perm, H, N, D, dims->dtype, s->Qp, st));
+  PARK_TRY(launch_gather(K, s->k_perm, H, N, D, dims->dtype, s->Kp, st));
+  PARK_TRY(launch_gather(V, s->k_perm, H, N, D, dims->dtype, s->Vp, st));
+  if (reuse != PARK_REUSE_CLUSTERS_AND_MASK) {
+    PARK_TRY(launch_segment_mean(s->Kp, nullptr, s->k_offsets, H, N, D, dims->dtype, p->CK,
+                                 nullptr, s->k_centroids, s->k_sizes, st));
+    PARK_TRY(retrieve_body(s->Qp, s->q_offsets, s->k_centroids, s->k_sizes, *dims, p->CQ, p->CK,
+                           p->select, param, s->W, s->kv_count, s->kv_index, ws, st));
+  }
+  return launch_attention(s->Qp, s->Kp, s->Vp, s->q_offsets, s->k_offsets, s->kv_count,
+                          s->kv_index, s->q_perm, H, N, D, dims->dtype, p->CQ, p->CK, O,
+                          p->out_dtype, st);
+}
+
+park_status park_check(void* ws, void* stream) {
+  g_err[0] = 0;
+  PARK_TRY(check_ptr(ws, "workspace"));
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail(PARK_ERR_HIP, "stream sync: %s", hipGetErrorString(e));
+  int word = 0;
+  e = hipMemcpy(&word, ws, sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return fail(PARK_ERR_HIP, "status read: %s", hipGetErrorString(e));
+  if (word == 0) return PARK_OK;
+  PARK_TRY(launch_clear_status((int*)ws, st));
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail(PARK_ERR_HIP, "stream sync: %s", hipGetErrorString(e));
+  return fail(PARK_ERR_NUMERIC, "device status 0x%x:%s%s", word,
+              (word & ST_NOT_SPD) ? " metric not positive definite;" : "",
+              (word & ST_NONFINITE) ? " non-finite values;" : "");
+}
+
+park_status park_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_pmu);
+  g_prof = on != 0;
+  return PARK_OK;
+}
+
+park_status park_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_pmu);
+  for (auto& r : g_recs) {
+    hipEventSynchronize(r.b);
+    g_pool.push_back(r.a);
+    g_pool.push_back(r.b);
+  }
+  g_recs.clear();
+  return PARK_OK;
+}
+
+park_status park_profile_read(char* buf, size_t cap) {
+  if (!buf || cap == 0) return fail(PARK_ERR_INVALID_ARG, "buffer is NULL");
+  std::lock_guard<std::mutex> lk(g_pmu);
+  std::map<std::string, std::pair<long, double>> agg;
+  for (auto& r : g_recs) {
+    hipEventSynchronize(r.b);
+    float ms = 0.0f;
+    hipEventElapsedTime(&ms, r.a, r.b);
+    auto& a = agg[r.name];
+    a.first += 1;
+    a.second += ms;
+    g_pool.push_back(r.a);
+    g_pool.push_back(r.b);
+  }
+  g_recs.clear();
+  std::string out = "{";
+  bool first = true;
+  for (auto& kv : agg) {
+    char tmp[256];
+    snprintf(tmp, sizeof(tmp), "%s\"%s\": {\"launches\": %ld, \"ms\": %.6f}", first ? "" : ", ",
+             kv.first.c_str(), kv.second.first, kv.second.second);
+    out += tmp;
+    first = false;
+  }
+  out += "}";
+  strncpy(buf, out.c_str(), cap - 1);
+  buf[cap - 1] = 0;
+  return PARK_OK;
+}
+
+}  // extern "C"

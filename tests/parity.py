@@ -1,0 +1,102 @@
+"""Parity helpers: compare the HIP path with the CPU oracle.
+
+Bars (stated by the method's specification):
+* labels, permutations, masks: bit-exact, except where the oracle's own
+  distance / score gap is below 1e-6 relative;
+* attention outputs: 1e-4 max-abs (fp32 inputs), 2e-2 max-abs (bf16 inputs).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+from oracle import park_oracle as O
+
+REL_GAP = 1e-6
+FLT_MIN = float(np.finfo(np.float32).tiny)
+ATOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def to_dev(a: np.ndarray, dtype: str) -> torch.Tensor:
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    t = t.to(torch.bfloat16) if dtype == "bf16" else t
+    return t.cuda().contiguous()
+
+
+def np64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def label_flips(X: np.ndarray, mu: np.ndarray, z_gpu: np.ndarray, z_or: np.ndarray):
+    """Mismatched tokens and whether each is a near-tie of the oracle's distances.
+
+    Returns (n_mismatch, n_not_exempt, worst relative gap).
+    """
+    bad = np.nonzero(z_gpu != z_or)[0]
+    worst = 0.0
+    n_not = 0
+    for j in bad:
+        da = np.sum((X[j] - mu[z_gpu[j]]) ** 2)
+        db = np.sum((X[j] - mu[z_or[j]]) ** 2)
+        rel = (da - db) / max(db, 1e-300)
+        worst = max(worst, rel)
+        if rel > REL_GAP:
+            n_not += 1
+    return len(bad), n_not, worst
+
+
+def mask_row_exempt(w: np.ndarray, valid: np.ndarray, mode: str, param: float,
+                    got: set, want: set) -> bool:
+    """A differing mask row is acceptable only at a near-tie of the oracle."""
+    diff = got ^ want
+    if not diff:
+        return True
+    sel, order, m = O.select_row(w, valid, mode, param)
+    cut = w[order[m - 1]] if m > 0 else 0.0
+    if mode == "topp":
+        cs = np.cumsum(w[order])
+        if abs(cs[m - 1] - param) <= REL_GAP * param:
+            return True
+        if m >= 2 and abs(cs[m - 2] - param) <= REL_GAP * param:
+            return True
+    for v in diff:
+        if w[v] < FLT_MIN and cut < FLT_MIN:
+            continue
+        if abs(w[v] - cut) > REL_GAP * max(cut, FLT_MIN):
+            return False
+    return True
+
+
+def compare_masks(W: np.ndarray, k_sizes: np.ndarray, q_sizes: np.ndarray, mode: str,
+                  param: float, kv_count: np.ndarray, kv_index: np.ndarray):
+    """(n_rows_differing, n_not_exempt) for one head."""
+    valid = k_sizes > 0
+    n_diff = n_bad = 0
+    for u in range(W.shape[0]):
+        got = set(kv_index[u, :kv_count[u]].tolist())
+        if q_sizes[u] == 0:
+            assert kv_count[u] == 0
+            continue
+        want = set(O.select_row(W[u], valid, mode, param)[0].tolist())
+        ids = kv_index[u, :kv_count[u]]
+        assert np.all(np.diff(ids) > 0), "kv_index row not ascending"
+        if got != want:
+            n_diff += 1
+            if not mask_row_exempt(W[u], valid, mode, param, got, want):
+                n_bad += 1
+    return n_diff, n_bad
+
+
+def attn_tol(dtype: str, out_bf16: bool, ref: np.ndarray) -> np.ndarray:
+    """Per-element tolerance: the dtype bar, plus half an ulp of bf16 output."""
+    tol = np.full(ref.shape, ATOL[dtype])
+    if out_bf16:
+        e = np.floor(np.log2(np.maximum(np.abs(ref), 2.0 ** -126)))
+        tol = tol + 2.0 ** (e - 8)
+    return tol
+
+
+def rows_from_csr(kv_count: np.ndarray, kv_index: np.ndarray):
+    return [kv_index[u, :kv_count[u]].astype(np.int64) for u in range(len(kv_count))]

@@ -1,0 +1,134 @@
+"""The C ABI loads, exports every symbol include/park.h declares, and rejects
+bad arguments on the host before anything is enqueued (no GPU needed)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2609_38978_amd import park as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    src = open(os.path.join(ROOT, "include", "park.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(park_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_declares_binding_exports():
+    assert declared_symbols() == sorted(P.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = P.lib()
+    for name in declared_symbols():
+        assert hasattr(L, name), name
+    # the symbols are C, unmangled
+    out = os.popen(f"nm -D --defined-only {P.LIB_PATH}").read()
+    for name in declared_symbols():
+        assert re.search(rf"\bT {name}$", out, re.M), name
+
+
+def test_status_strings():
+    L = P.lib()
+    for s in range(6):
+        assert L.park_status_string(s)
+    assert L.park_status_string(99) == b"unknown status"
+
+
+FAKE = 1 << 20  # 16-byte aligned fake device address, never dereferenced
+
+
+def _dims(H=2, N=1000, d=128, dtype=P.PARK_BF16):
+    return P.Dims(H, N, d, dtype)
+
+
+def test_workspace_size_monotone_and_validated():
+    L = P.lib()
+    out = C.c_size_t()
+    assert L.park_workspace_size(C.byref(_dims()), 16, 16, C.byref(out)) == P.PARK_OK
+    a = out.value
+    assert L.park_workspace_size(C.byref(_dims()), 16, 32, C.byref(out)) == P.PARK_OK
+    assert out.value >= a > 0
+    assert L.park_workspace_size(C.byref(_dims(d=96)), 16, 16, C.byref(out)) == P.PARK_ERR_UNSUPPORTED
+    assert L.park_workspace_size(C.byref(_dims()), 0, 16, C.byref(out)) == P.PARK_ERR_INVALID_ARG
+    assert L.park_workspace_size(C.byref(_dims()), 1001, 16, C.byref(out)) == P.PARK_ERR_INVALID_ARG
+    assert L.park_workspace_size(C.byref(_dims(N=5000)), 2049, 16, C.byref(out)) == P.PARK_ERR_UNSUPPORTED
+    assert L.park_workspace_size(C.byref(_dims(dtype=7)), 16, 16, C.byref(out)) == P.PARK_ERR_INVALID_ARG
+    assert b"dtype" in L.park_last_error()
+
+
+def _cluster(**kw):
+    a = dict(X=FAKE, Q=FAKE, dims=_dims(), C=16, T=10, seed=0, side=1, metric=P.PARK_METRIC_QRKC,
+             alpha=0.05, eps=1e-6, s_min=1e-12, labels=None, perm=FAKE, offsets=FAKE, R=None,
+             Xt=None, ws=FAKE, ws_bytes=1 << 40)
+    a.update(kw)
+    return P.lib().park_cluster_keys(a["X"], a["Q"], C.byref(a["dims"]), a["C"], a["T"], a["seed"],
+                                     a["side"], a["metric"], a["alpha"], a["eps"], a["s_min"],
+                                     a["labels"], a["perm"], a["offsets"], a["R"], a["Xt"], a["ws"],
+                                     a["ws_bytes"], None)
+
+
+def test_cluster_argument_errors():
+    assert _cluster(X=None) == P.PARK_ERR_INVALID_ARG
+    assert _cluster(X=FAKE + 4) == P.PARK_ERR_INVALID_ARG  # misaligned
+    assert b"aligned" in P.lib().park_last_error()
+    assert _cluster(Q=None) == P.PARK_ERR_INVALID_ARG  # QRKC needs the queries
+    assert _cluster(C=0) == P.PARK_ERR_INVALID_ARG
+    assert _cluster(C=1001) == P.PARK_ERR_INVALID_ARG  # C > N
+    assert _cluster(T=0) == P.PARK_ERR_INVALID_ARG
+    assert _cluster(side=2) == P.PARK_ERR_INVALID_ARG
+    assert _cluster(metric=5) == P.PARK_ERR_INVALID_ARG
+    assert _cluster(alpha=1.5) == P.PARK_ERR_INVALID_ARG
+    assert _cluster(alpha=float("nan")) == P.PARK_ERR_INVALID_ARG
+    assert _cluster(s_min=0.0) == P.PARK_ERR_INVALID_ARG
+    assert _cluster(dims=_dims(d=32)) == P.PARK_ERR_UNSUPPORTED
+    assert _cluster(ws_bytes=100) == P.PARK_ERR_WORKSPACE
+    assert _cluster(metric=P.PARK_METRIC_EUCLID, R=FAKE) == P.PARK_ERR_INVALID_ARG
+
+
+def test_retrieve_and_attention_argument_errors():
+    L = P.lib()
+    d = _dims()
+
+    def retr(sel=P.PARK_SELECT_TOPP, param=0.9, CQ=16, CK=16, ws_bytes=1 << 40):
+        return L.park_retrieve_blocks(FAKE, FAKE, FAKE, FAKE, C.byref(d), CQ, CK, sel, param, None,
+                                      FAKE, FAKE, FAKE, ws_bytes, None)
+
+    assert retr(param=0.0) == P.PARK_ERR_INVALID_ARG
+    assert retr(param=1.5) == P.PARK_ERR_INVALID_ARG
+    assert retr(sel=9) == P.PARK_ERR_INVALID_ARG
+    assert retr(CK=3000) == P.PARK_ERR_INVALID_ARG
+    assert retr(ws_bytes=8) == P.PARK_ERR_WORKSPACE
+    r = L.park_block_sparse_attn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16, 16,
+                                 FAKE, 7, None)
+    assert r == P.PARK_ERR_INVALID_ARG
+    r = L.park_block_sparse_attn(FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16, 16,
+                                 FAKE, P.PARK_F32, None)
+    assert r == P.PARK_ERR_INVALID_ARG
+
+
+def test_forward_argument_errors():
+    L = P.lib()
+    d = _dims()
+    prm = P.make_params(16, 16)
+    st = P.State(*([FAKE] * 11 + [None]))
+
+    def fwd(params=prm, reuse=0, state=st, ws_bytes=1 << 40):
+        return L.park_forward(FAKE, FAKE, FAKE, C.byref(d), C.byref(params), reuse, C.byref(state),
+                              FAKE, FAKE, ws_bytes, None)
+
+    assert fwd(reuse=3) == P.PARK_ERR_INVALID_ARG
+    bad = P.make_params(16, 16, select="topk", ratio=0.0)
+    assert fwd(params=bad) == P.PARK_ERR_INVALID_ARG
+    bad = P.make_params(16, 16, out_dtype=3)
+    assert fwd(params=bad) == P.PARK_ERR_INVALID_ARG
+    bad = P.make_params(16, 16, T=0)
+    assert fwd(params=bad) == P.PARK_ERR_INVALID_ARG
+    st2 = P.State(*([FAKE] * 10 + [None, None]))  # Vp missing
+    assert fwd(state=st2) == P.PARK_ERR_INVALID_ARG
+    assert fwd(ws_bytes=64) == P.PARK_ERR_WORKSPACE
+    assert L.park_forward(FAKE, FAKE, FAKE, C.byref(d), None, 0, C.byref(st), FAKE, FAKE, 1 << 40,
+                          None) == P.PARK_ERR_INVALID_ARG

@@ -1,0 +1,99 @@
+"""End-to-end GPU parity of park_forward with the oracle's whole pipeline."""
+import numpy as np
+import pytest
+import torch
+
+import parity as PT
+from oracle import park_oracle as O
+from paper_2609_38978_amd import park as P
+from paper_2609_38978_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "tiny": ("tiny", None, None, None),
+    "medium": ("medium", None, [0, 3, 7], None),  # GPU runs 3 heads of the 8-head layer
+    "ragged_topp": ("medium", (3, 11, 13), [0, 1], ("topp", 0.9)),
+    "hunyuan_small_topk": ("hunyuan", (2, 9, 16), [0], None),
+}
+
+
+@pytest.mark.parametrize("tag", list(CASES))
+@pytest.mark.parametrize("out_dtype", [P.PARK_F32, P.PARK_BF16])
+def test_forward_matches_oracle(tag, out_dtype):
+    name, grid, heads, sel = CASES[tag]
+    cfg = synth.CONFIGS[name]
+    if grid is not None:
+        cfg = cfg.with_(grid=grid)
+    mode, param = sel if sel else (cfg.select, cfg.ratio if cfg.select == "topk" else cfg.topp)
+    q, k, v = synth.make_layer(cfg, heads)
+    Q, K, V = (PT.to_dev(a, cfg.dtype) for a in (q, k, v))
+    C = cfg.C
+    prm = P.make_params(C, C, T=cfg.iters, select=mode, ratio=param, topp=param, seed=0,
+                        out_dtype=out_dtype)
+    ws = P.workspace(Q, C, C)
+    st = P.make_state(Q, C, C, want_W=True)
+    Og, st = P.park_forward(Q, K, V, prm, state=st, ws=ws)
+    P.park_check(ws)
+    Og = PT.np64(Og)
+    hs = heads if heads is not None else range(cfg.H)
+    for i, h in enumerate(hs):
+        ref = O.park_head(q[i], k[i], v[i], C, C, cfg.iters, mode, param, seed=0, head=i)
+        qp = st["q_perm"][i].cpu().numpy()
+        kp = st["k_perm"][i].cpu().numpy()
+        same_q = np.array_equal(qp, ref["q"]["perm"])
+        same_k = np.array_equal(kp, ref["k"]["perm"])
+        print(f"[{tag} h={h}] q_perm equal={same_q} k_perm equal={same_k}")
+        assert same_q and same_k
+        kvc = st["kv_count"][i].cpu().numpy()
+        kvi = st["kv_index"][i].cpu().numpy()
+        nd, nb = PT.compare_masks(ref["W"], ref["sizes"], np.diff(ref["q"]["offsets"]), mode,
+                                  param, kvc, kvi)
+        print(f"[{tag} h={h}] mask rows differing={nd} not-exempt={nb}")
+        assert nb == 0
+        # attention on the GPU's own mask
+        Oref = O.block_sparse_attention(ref["Qp"], ref["Kp"], ref["Vp"], ref["q"]["offsets"],
+                                        ref["k"]["offsets"], PT.rows_from_csr(kvc, kvi),
+                                        ref["q"]["perm"])
+        tol = PT.attn_tol(cfg.dtype, out_dtype == P.PARK_BF16, Oref)
+        err = np.abs(Og[i] - Oref)
+        print(f"[{tag} h={h}] attention max-abs err {err.max():.3g}")
+        assert np.all(err <= tol)
+        W = st["W"][i].cpu().numpy().astype(np.float64)
+        assert np.all(np.abs(W - ref["W"]) <= 2.0 ** -23 * ref["W"] + 1e-40)
+
+
+def test_reuse_modes():
+    cfg = synth.CONFIGS["medium"].with_(grid=(2, 16, 32))
+    q, k, v = synth.make_layer(cfg, [0, 1])
+    Q, K, V = (PT.to_dev(a, cfg.dtype) for a in (q, k, v))
+    C = cfg.C
+    prm = P.make_params(C, C, T=5, select="topp", topp=0.9)
+    ws = P.workspace(Q, C, C)
+    O1, st = P.park_forward(Q, K, V, prm, ws=ws)
+    perm_before = st["q_perm"].clone()
+    mask_before = st["kv_index"].clone()
+    # next diffusion step: drifted Q and K
+    q2 = np.stack([synth.perturb_head(cfg, h, q[h], k[h])[0] for h in range(2)])
+    k2 = np.stack([synth.perturb_head(cfg, h, q[h], k[h])[1] for h in range(2)])
+    Q2, K2 = PT.to_dev(q2, cfg.dtype), PT.to_dev(k2, cfg.dtype)
+    O2, st = P.park_forward(Q2, K2, V, prm, reuse=P.PARK_REUSE_CLUSTERS, state=st, ws=ws)
+    P.park_check(ws)
+    assert torch.equal(st["q_perm"], perm_before)
+    O3, st = P.park_forward(Q2, K2, V, prm, reuse=P.PARK_REUSE_CLUSTERS_AND_MASK, state=st, ws=ws)
+    P.park_check(ws)
+    assert torch.equal(O2, O3)  # same clusters, same mask, same tensors
+    for i in range(2):
+        qp = st["q_perm"][i].cpu().numpy()
+        kp = st["k_perm"][i].cpu().numpy()
+        qoff = st["q_offsets"][i].cpu().numpy()
+        koff = st["k_offsets"][i].cpu().numpy()
+        c, n = O.block_centroids(k2[i][kp], koff)
+        W = O.pama(q2[i][qp], qoff, c, n)
+        kvc = st["kv_count"][i].cpu().numpy()
+        kvi = st["kv_index"][i].cpu().numpy()
+        nd, nb = PT.compare_masks(W, n, np.diff(qoff), "topp", 0.9, kvc, kvi)
+        assert nb == 0
+        Oref = O.block_sparse_attention(q2[i][qp], k2[i][kp], v[i][kp], qoff, koff,
+                                        PT.rows_from_csr(kvc, kvi), qp)
+        assert np.abs(PT.np64(O2)[i] - Oref).max() <= 2e-2

@@ -1,0 +1,279 @@
+"""GPU parity of each stage of the C ABI against the CPU oracle.
+
+Every stage is fed the same inputs as the oracle stage (so an earlier
+legitimate near-tie cannot cascade) and compared element by element.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import parity as PT
+from oracle import park_oracle as O
+from paper_2609_38978_amd import park as P
+from paper_2609_38978_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def setup_module(module):
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    P.lib()
+
+
+def small(name, grid=None, heads=None):
+    cfg = synth.CONFIGS[name]
+    if grid is not None:
+        cfg = cfg.with_(grid=grid)
+    q, k, v = synth.make_layer(cfg, heads)
+    return cfg, q, k, v
+
+
+CASES = {
+    # name: (config, grid override, heads) -- sizes span several tiles plus a ragged tail
+    "tiny": ("tiny", None, None),
+    "medium2": ("medium", None, [0, 5]),
+    "ragged_bf16": ("medium", (3, 11, 13), [1, 2, 3]),  # N = 429, not a multiple of 64
+    "hunyuan_small": ("hunyuan", (1, 9, 16), [0, 1]),   # text tokens appended
+}
+
+
+@pytest.fixture(scope="module", params=list(CASES))
+def case(request):
+    name, grid, heads = CASES[request.param]
+    cfg, q, k, v = small(name, grid, heads)
+    return request.param, cfg, q, k, v
+
+
+def test_metric_factor_and_transform(case):
+    tag, cfg, q, k, v = case
+    Q, K = PT.to_dev(q, cfg.dtype), PT.to_dev(k, cfg.dtype)
+    C = cfg.C
+    out = P.park_cluster_keys(K, C, 1, seed=0, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q,
+                              want_R=True, want_Xt=True)
+    P.park_check(out["ws"])
+    R = out["R"].cpu().numpy()
+    Xt = out["Xt"].cpu().numpy()
+    for h in range(q.shape[0]):
+        m = O.query_metric(q[h].astype(np.float64))
+        assert np.abs(R[h] - m["R"]).max() <= 1e-12 * np.abs(m["R"]).max()
+        ref = O.transform_keys(k[h], m["R"])
+        err = np.abs(Xt[h].astype(np.float64) - ref)
+        assert np.all(err <= 2.0 ** -23 * np.abs(ref) + 1e-30), (tag, err.max())
+
+
+@pytest.mark.parametrize("side", [0, 1])
+def test_kmeans_labels_permutation_offsets(case, side):
+    tag, cfg, q, k, v = case
+    Q, K = PT.to_dev(q, cfg.dtype), PT.to_dev(k, cfg.dtype)
+    C, T = cfg.C, cfg.iters
+    if side == 0:
+        out = P.park_cluster_keys(Q, C, T, seed=7, side=0, metric=P.PARK_METRIC_EUCLID)
+    else:
+        out = P.park_cluster_keys(K, C, T, seed=7, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q)
+    P.park_check(out["ws"])
+    lab = out["labels"].cpu().numpy()
+    perm = out["perm"].cpu().numpy()
+    off = out["offsets"].cpu().numpy()
+    for h in range(q.shape[0]):
+        if side == 0:
+            res = O.cluster_queries(q[h], C, T, 7, h)
+            X = q[h].astype(np.float64)
+        else:
+            res = O.cluster_keys(k[h], q[h], C, T, 7, h)
+            X = res["Kt"]
+        # init indices are generated independently on both sides
+        n_mis, n_bad, worst = PT.label_flips(X, res["mu"], lab[h], res["labels"])
+        print(f"[{tag} side={side} h={h}] label mismatches={n_mis} not-exempt={n_bad} "
+              f"worst-gap={worst:.3g}")
+        assert n_bad == 0
+        if n_mis == 0:
+            assert np.array_equal(perm[h], res["perm"])
+            assert np.array_equal(off[h], res["offsets"])
+        # permutation is the stable argsort of the GPU's own labels in any case
+        p2, o2 = O.stable_argsort(lab[h], C)
+        assert np.array_equal(perm[h], p2) and np.array_equal(off[h], o2)
+
+
+def test_gather_and_centroids(case):
+    tag, cfg, q, k, v = case
+    K = PT.to_dev(k, cfg.dtype)
+    H, N, d = k.shape
+    C = cfg.C
+    rng = np.random.default_rng(3)
+    z = rng.integers(0, C, size=(H, N))
+    z[:, z[0] == 1] = 2  # force an empty cluster
+    perms, offs = zip(*[O.stable_argsort(z[h], C) for h in range(H)])
+    perm = torch.from_numpy(np.stack(perms).astype(np.int32)).cuda()
+    off = torch.from_numpy(np.stack(offs).astype(np.int32)).cuda()
+    Kp = P.park_gather_rows(K, perm)
+    assert torch.equal(Kp.cpu(), K.cpu()[torch.arange(H)[:, None], perm.cpu().long()])
+    cen, sizes = P.park_block_centroids(K, perm, off, C)
+    cen2, sizes2 = P.park_block_centroids(Kp, torch.arange(N, dtype=torch.int32).repeat(H, 1).cuda(),
+                                          off, C)
+    assert torch.equal(cen, cen2) and torch.equal(sizes, sizes2)
+    cen, sizes = cen.cpu().numpy(), sizes.cpu().numpy()
+    for h in range(H):
+        c_o, n_o = O.block_centroids(k[h][perms[h]], offs[h])
+        assert np.array_equal(sizes[h], n_o)
+        # identical up to float64 summation order, then rounded to float32
+        ulp = np.spacing(np.abs(c_o).astype(np.float32))
+        assert np.all(np.abs(cen[h] - c_o) <= ulp), tag
+
+
+@pytest.mark.parametrize("mode", ["topk", "topp"])
+def test_retrieval_matches_oracle(case, mode):
+    tag, cfg, q, k, v = case
+    H, N, d = q.shape
+    CQ = CK = cfg.C
+    param = cfg.ratio if mode == "topk" else 0.9
+    qps, qoffs, cens, ns, Ws = [], [], [], [], []
+    for h in range(H):
+        rq = O.cluster_queries(q[h], CQ, 3, 1, h)
+        rk = O.cluster_keys(k[h], q[h], CK, 3, 1, h)
+        c, n = O.block_centroids(k[h][rk["perm"]], rk["offsets"])
+        Qp = q[h][rq["perm"]]
+        qps.append(Qp)
+        qoffs.append(rq["offsets"])
+        cens.append(c)
+        ns.append(n)
+        Ws.append(O.pama(Qp, rq["offsets"], c, n))
+    Qp = PT.to_dev(np.stack(qps), cfg.dtype)
+    qoff = torch.from_numpy(np.stack(qoffs).astype(np.int32)).cuda()
+    cen = torch.from_numpy(np.stack(cens)).cuda()
+    ksz = torch.from_numpy(np.stack(ns).astype(np.int32)).cuda()
+    sel = P.PARK_SELECT_TOPK if mode == "topk" else P.PARK_SELECT_TOPP
+    kvc, kvi, W = P.park_retrieve_blocks(Qp, qoff, cen, ksz, CQ, CK, sel, param, want_W=True)
+    kvc, kvi, W = kvc.cpu().numpy(), kvi.cpu().numpy(), W.cpu().numpy()
+    for h in range(H):
+        err = np.abs(W[h].astype(np.float64) - Ws[h])
+        assert np.all(err <= 2.0 ** -23 * Ws[h] + 1e-40), (tag, err.max())
+        qs = np.diff(qoffs[h])
+        nd, nb = PT.compare_masks(Ws[h], ns[h], qs, mode, param, kvc[h], kvi[h])
+        print(f"[{tag} {mode} h={h}] mask rows differing={nd} not-exempt={nb}")
+        assert nb == 0
+
+
+@pytest.mark.parametrize("out_dtype", [P.PARK_F32, P.PARK_BF16])
+def test_attention_matches_oracle(case, out_dtype):
+    tag, cfg, q, k, v = case
+    H, N, d = q.shape
+    C = cfg.C
+    rng = np.random.default_rng(11)
+    qperm, kperm, qoff, koff, kvc, kvi, rows = [], [], [], [], [], [], []
+    for h in range(H):
+        zq = rng.integers(0, C, N)
+        zk = rng.integers(0, C, N)
+        zk[zk == 3] = 4  # an empty key block
+        pq, oq = O.stable_argsort(zq, C)
+        pk, ok = O.stable_argsort(zk, C)
+        cnt = np.zeros(C, np.int32)
+        idx = np.zeros((C, C), np.int32)
+        rr = []
+        for u in range(C):
+            m = int(rng.integers(1, max(2, C // 3)))
+            s = np.sort(rng.choice(C, size=m, replace=False))
+            s = s[np.diff(ok)[s] > 0]  # selected blocks are nonempty
+            if len(s) == 0:
+                s = np.array([int(np.argmax(np.diff(ok)))])
+            cnt[u] = len(s)
+            idx[u, :len(s)] = s
+            rr.append(s)
+        qperm.append(pq); kperm.append(pk); qoff.append(oq); koff.append(ok)
+        kvc.append(cnt); kvi.append(idx); rows.append(rr)
+    t = lambda a: torch.from_numpy(np.stack(a).astype(np.int32)).cuda()
+    Qp = PT.to_dev(np.stack([q[h][qperm[h]] for h in range(H)]), cfg.dtype)
+    Kp = PT.to_dev(np.stack([k[h][kperm[h]] for h in range(H)]), cfg.dtype)
+    Vp = PT.to_dev(np.stack([v[h][kperm[h]] for h in range(H)]), cfg.dtype)
+    Ot = P.park_block_sparse_attn(Qp, Kp, Vp, t(qoff), t(koff), t(kvc), t(kvi), t(qperm), C, C,
+                                  out_dtype)
+    Og = PT.np64(Ot)
+    for h in range(H):
+        ref = O.block_sparse_attention(q[h][qperm[h]], k[h][kperm[h]], v[h][kperm[h]], qoff[h],
+                                       koff[h], rows[h], qperm[h])
+        tol = PT.attn_tol(cfg.dtype, out_dtype == P.PARK_BF16, ref)
+        err = np.abs(Og[h] - ref)
+        print(f"[{tag} out={out_dtype} h={h}] attention max-abs err {err.max():.3g}")
+        assert np.all(err <= tol), (tag, err.max())
+
+
+def test_dense_when_every_block_kept():
+    cfg = synth.CONFIGS["tiny"]
+    q, k, v = synth.make_layer(cfg)
+    Q, K, V = (PT.to_dev(a, cfg.dtype) for a in (q, k, v))
+    prm = P.make_params(cfg.C, cfg.C, T=3, select="topk", ratio=1.0)
+    O_, st = P.park_forward(Q, K, V, prm)
+    torch.cuda.synchronize()
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q).double(), torch.from_numpy(k).double(), torch.from_numpy(v).double())
+    err = (O_.cpu().double() - ref).abs().max().item()
+    assert err <= 1e-4, err
+    assert (st["kv_count"] == (st["k_sizes"] > 0).sum(1, keepdim=True)).all()
+
+
+def test_block_size_one_gives_exact_attention_mass():
+    # C = N: singleton blocks; W^ equals the dense attention matrix
+    cfg = synth.CONFIGS["tiny"].with_(grid=(1, 8, 24))  # N = 192
+    q, k, v = synth.make_layer(cfg)
+    N = q.shape[1]
+    Q, K = PT.to_dev(q, "f32"), PT.to_dev(k, "f32")
+    rq = P.park_cluster_keys(Q, N, 2, seed=0, side=0, metric=P.PARK_METRIC_EUCLID)
+    rk = P.park_cluster_keys(K, N, 2, seed=0, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q)
+    assert torch.all(rq["offsets"][:, 1:] - rq["offsets"][:, :-1] == 1)
+    Qp = P.park_gather_rows(Q, rq["perm"])
+    cen, sz = P.park_block_centroids(K, rk["perm"], rk["offsets"], N)
+    kvc, kvi, W = P.park_retrieve_blocks(Qp, rq["offsets"], cen, sz, N, N, P.PARK_SELECT_TOPP, 0.5,
+                                         want_W=True)
+    A = torch.softmax(torch.from_numpy(q[0]).double() @ torch.from_numpy(k[0]).double().T
+                      / math.sqrt(q.shape[2]), dim=1).numpy()
+    pq, pk = rq["perm"][0].cpu().numpy(), rk["perm"][0].cpu().numpy()
+    err = np.abs(W[0].cpu().numpy() - A[np.ix_(pq, pk)])
+    assert err.max() <= 1e-6
+
+
+def test_forward_is_deterministic():
+    cfg = synth.CONFIGS["medium"].with_(grid=(2, 16, 32))
+    q, k, v = synth.make_layer(cfg, [0, 1])
+    Q, K, V = (PT.to_dev(a, cfg.dtype) for a in (q, k, v))
+    prm = P.make_params(cfg.C, cfg.C, T=5, select="topp", topp=0.9, out_dtype=P.PARK_BF16)
+    O1, s1 = P.park_forward(Q, K, V, prm)
+    O2, s2 = P.park_forward(Q, K, V, prm)
+    torch.cuda.synchronize()
+    assert torch.equal(O1, O2)
+    for key in ("q_perm", "k_perm", "kv_count", "kv_index", "k_centroids"):
+        assert torch.equal(s1[key], s2[key]), key
+
+
+def test_duplicate_tokens_make_empty_clusters():
+    cfg = synth.CONFIGS["tiny"].with_(grid=(1, 16, 16))
+    q, k, v = synth.make_layer(cfg)
+    q[:, 128:] = q[:, :1]  # half the tokens identical
+    k[:, 128:] = k[:, :1]
+    Q, K, V = (PT.to_dev(a, "f32") for a in (q, k, v))
+    C = 32
+    prm = P.make_params(C, C, T=4, select="topp", topp=0.9)
+    O_, st = P.park_forward(Q, K, V, prm)
+    torch.cuda.synchronize()
+    res = O.park_head(q[0], k[0], v[0], C, C, 4, "topp", 0.9)
+    assert np.array_equal(st["q_perm"][0].cpu().numpy(), res["q"]["perm"])
+    assert np.array_equal(st["k_perm"][0].cpu().numpy(), res["k"]["perm"])
+    assert (st["k_sizes"][0] == 0).any()
+    err = np.abs(PT.np64(O_)[0] - res["O"]).max()
+    assert err <= 1e-4
+
+
+def test_numeric_failure_is_reported():
+    # rank-deficient queries with no shrinkage: the metric is not positive definite
+    H, N, d = 1, 256, 64
+    Q = torch.zeros(H, N, d, device="cuda")
+    Q[..., :3] = torch.randn(H, N, 3, device="cuda")
+    K = torch.randn(H, N, d, device="cuda")
+    out = P.park_cluster_keys(K, 8, 2, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q, alpha=0.0,
+                              eps=0.0)
+    with pytest.raises(P.ParkError) as ei:
+        P.park_check(out["ws"])
+    assert ei.value.status == P.PARK_ERR_NUMERIC
+    # with the paper's shrinkage the same queries factorise fine
+    out = P.park_cluster_keys(K, 8, 2, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q)
+    P.park_check(out["ws"])
