@@ -87,11 +87,15 @@ __global__ void k_seed_centroids(const T* __restrict__ X, const int* __restrict_
 
 // w_v = Gbar mu_v (or mu_v), b_v = mu_v . w_v;  16 centroids per workgroup.
 // Gbar is symmetric, so thread (a, group) reads column a of it coalesced and
-// applies each element to 16 / (256 / D) centroids.
+// applies each element to 16 / (256 / D) centroids.  When `w3` is given the
+// fast-path operands are written too: w_v split into three bf16 parts (three
+// planes of H*C*D), b_v in float, and |w_v| rounded up for the error bound.
 template <int D>
 __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
                                               const double* __restrict__ Gbar, int C,
-                                              double* __restrict__ w, double* __restrict__ b) {
+                                              double* __restrict__ w, double* __restrict__ b,
+                                              bf16_t* __restrict__ w3, size_t plane,
+                                              float* __restrict__ b32, float* __restrict__ wn) {
   constexpr int CB = 16, NG = 256 / D, PER = CB / NG;
   __shared__ double ms[CB][D];
   __shared__ double ws[CB][D + 1];
@@ -120,140 +124,391 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
   for (int k = 0; k < PER; ++k) {
     const int r = grp + NG * k;
     ws[r][a] = acc[k];
-    if (v0 + r < C) w[((size_t)h * C + v0 + r) * D + a] = acc[k];
+    if (v0 + r < C) {
+      const size_t o = ((size_t)h * C + v0 + r) * D + a;
+      w[o] = acc[k];
+      if (w3) {
+        // w = w1 + w2 + w3 + r with bf16 parts and |r| <= 2^-24 |w| (1 + 2^-7)
+        const bf16_t p1 = f2bf((float)acc[k]);
+        const double r1 = acc[k] - (double)bf2f(p1);
+        const bf16_t p2 = f2bf((float)r1);
+        const double r2 = r1 - (double)bf2f(p2);
+        w3[o] = p1;
+        w3[o + plane] = p2;
+        w3[o + 2 * plane] = f2bf((float)r2);
+      }
+    }
   }
   __syncthreads();
   if (tid < CB && v0 + tid < C) {
-    double s = 0.0;
-    for (int c = 0; c < D; ++c) s = fma(ms[tid][c], ws[tid][c], s);
+    double s = 0.0, n2 = 0.0;
+    for (int c = 0; c < D; ++c) {
+      s = fma(ms[tid][c], ws[tid][c], s);
+      n2 = fma(ws[tid][c], ws[tid][c], n2);
+    }
     b[(size_t)h * C + v0 + tid] = s;
+    if (b32) {
+      b32[(size_t)h * C + v0 + tid] = (float)s;
+      wn[(size_t)h * C + v0 + tid] = (float)(sqrt(n2) * (1.0 + 1e-6));
+    }
   }
 }
 
-// Exact float64 assignment: labels[j] = argmin_v (b_v - 2 x_j . w_v), ties to
-// the lowest v.  64 tokens x 64 centroids per step, 4x4 per thread.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void k_assign64(const T* __restrict__ X, const double* __restrict__ w,
-                                                  const double* __restrict__ b, int N, int C,
-                                                  int* __restrict__ labels, int* status) {
-  constexpr int TM = 64, TC = 64, DC = 32;
-  __shared__ float xs[TM][D + 1];
-  __shared__ double wsm[TC][DC + 1];
-  __shared__ double bs[TC];
-  __shared__ double rs[16][TM];
-  __shared__ int ri[16][TM];
-  const int h = blockIdx.y, t0 = blockIdx.x * TM, tid = threadIdx.x;
-  const T* Xh = X + (size_t)h * N * D;
-  for (int e = tid; e < TM * D; e += 256) {
-    const int r = e / D, c = e % D;
-    xs[r][c] = (t0 + r < N) ? to_f(Xh[(size_t)(t0 + r) * D + c]) : 0.0f;
-  }
-  const int tg = tid & 15, cg = tid >> 4;
-  double best[4];
-  int bidx[4];
+// Resets the per-head count of tokens left for the float64 assignment.
+__global__ void k_reset_counts(int* __restrict__ nflag, int H) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < H) nflag[i] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// Fast assignment on bf16 MFMA with certification.
+//
+// For a bf16 point x the score s_v = b_v - 2 x.w_v is evaluated with w_v
+// split into three bf16 parts, w = w1 + w2 + w3 + r, |r| <= 2^-24 (1+2^-7)|w|.
+// All products are bf16 x bf16, exact in float.  Each 32-wide k-step of the
+// x.w1 products is summed by one v_mfma_f32_16x16x32_bf16 into a fresh
+// accumulator (<= 32 roundings), the k-step partials are added on the VALU
+// (round-to-nearest), and x.(w2 + w3) runs in a second chain of the same
+// shape whose terms are 2^-8 smaller.  With delta = 2^-23 per MFMA addition
+// (any faithful rounding) the forward error of t^ = x.w is at most
+//   et * sum_a |x_a w_a|,  et = 2^-24 (1.01) + (32 delta + (KS-1) 2^-24) 1.01
+//                            + 2^-8 (64 delta + KS 2^-24) 1.01 + 2^-24 1.01,
+// and with sum_a |x_a w_a| <= |x| |w_v| and the float roundings of b_v and of
+// the score, |s^_v - s_v| <= E_v = 2 et |x| |w_v| + 2^-24 (|b_v| + |s^_v|).
+// A token is certified when, for its fast argmin v1, s^_v - E_v > s^_v1 +
+// E_v1 for every other v: then v1 is the exact argmin.  Otherwise (near-ties,
+// exact ties) it is listed for the float64 assignment.  A 10% margin covers
+// the rounding of |x| and of the bound itself.
+//
+// Workgroup = 256 tokens (4 wavefronts x 4 blocks of 16), centroid tiles of 64
+// staged in LDS.  MFMA orientation: A = 16 centroids x 32 dims, B = 32 dims x
+// 16 tokens, so lane l holds centroids 4(l/16)+r of token l%16.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <int D>
+__global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ X,
+                                                     const bf16_t* __restrict__ w3, size_t plane,
+                                                     const float* __restrict__ b32,
+                                                     const float* __restrict__ wn, int N, int C,
+                                                     int* __restrict__ labels,
+                                                     int* __restrict__ flags,
+                                                     int* __restrict__ nflag) {
+  constexpr int TB = 4, CT = 64, KS = D / 32, WROW = D + 8;
+  constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f;
+  constexpr float ET = U24 * 1.01f + (32.0f * DEL + (KS - 1) * U24) * 1.01f +
+                       0.00390625f * (64.0f * DEL + KS * U24) * 1.01f + U24 * 1.01f;
+  constexpr float MARGIN = 1.1f;
+  __shared__ __attribute__((aligned(16))) bf16_t W1[CT * WROW];
+  __shared__ __attribute__((aligned(16))) bf16_t W2[CT * WROW];
+  __shared__ __attribute__((aligned(16))) bf16_t W3[CT * WROW];
+  __shared__ float bs[CT];
+  __shared__ float ns[CT];
+  const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, g = l >> 4,
+            c16 = l & 15;
+  const int t0 = blockIdx.x * 256 + w * 64;
+  const bf16_t* Xh = X + (size_t)h * N * D;
+  bf16x8_t xf[TB][KS];
+  float xsq[TB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    best[i] = INFINITY;
-    bidx[i] = 0x7fffffff;
-  }
-  const double* wh = w + (size_t)h * C * D;
-  for (int c0 = 0; c0 < C; c0 += TC) {
-    double acc[4][4];
+  for (int tb = 0; tb < TB; ++tb) {
+    xsq[tb] = 0.0f;
+    const int tok = t0 + 16 * tb + c16;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int s = 0; s < KS; ++s) {
+      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+      if (tok < N) raw = *(const uint4*)(Xh + (size_t)tok * D + 32 * s + 8 * g);
+      xf[tb][s] = __builtin_bit_cast(bf16x8_t, raw);
+      const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
-    for (int a0 = 0; a0 < D; a0 += DC) {
-      __syncthreads();
-      for (int e = tid; e < TC * DC; e += 256) {
-        const int r = e / DC, c = e % DC;
-        wsm[r][c] = (c0 + r < C) ? wh[(size_t)(c0 + r) * D + a0 + c] : 0.0;
-      }
-      if (a0 == 0 && tid < TC) bs[tid] = (c0 + tid < C) ? b[(size_t)h * C + c0 + tid] : 0.0;
-      __syncthreads();
-#pragma unroll 4
-      for (int a = 0; a < DC; ++a) {
-        double xv[4], wv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) xv[i] = (double)xs[tg + 16 * i][a0 + a];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) wv[j] = wsm[cg + 16 * j][a];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = fma(xv[i], wv[j], acc[i][j]);
+      for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
+        xsq[tb] = fmaf(lo, lo, fmaf(hi, hi, xsq[tb]));
       }
     }
+  }
+  float kx[TB];  // MARGIN * 2 et |x| (|x| rounded up)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int v = c0 + cg + 16 * j;
-      if (v < C) {
-        const double bv = bs[cg + 16 * j];
+  for (int tb = 0; tb < TB; ++tb) {
+    float xs = xsq[tb] + __shfl_xor(xsq[tb], 16, 64);
+    xs += __shfl_xor(xs, 32, 64);
+    kx[tb] = MARGIN * 2.0f * ET * sqrtf(xs) * 1.0001f;
+  }
+  // per token: best fast score, its index, its upper bound, and the lowest
+  // lower bound among all other centroids
+  float best[TB], ub[TB], lo2[TB];
+  int bidx[TB];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const double s = fma(-2.0, acc[i][j], bv);
-          if (s < best[i] || (s == best[i] && v < bidx[i])) {
-            best[i] = s;
-            bidx[i] = v;
+  for (int tb = 0; tb < TB; ++tb) {
+    best[tb] = INFINITY;
+    ub[tb] = INFINITY;
+    lo2[tb] = INFINITY;
+    bidx[tb] = 0;
+  }
+  const bf16_t* P1 = w3 + (size_t)h * C * D;
+  const bf16_t* P2 = P1 + plane;
+  const bf16_t* P3 = P2 + plane;
+  const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int c0 = 0; c0 < C; c0 += CT) {
+    __syncthreads();
+    for (int e = tid; e < CT * (D / 8); e += 256) {
+      const int r = e / (D / 8), a8 = 8 * (e % (D / 8));
+      uint4 v1 = make_uint4(0u, 0u, 0u, 0u), v2 = v1, v3 = v1;
+      if (c0 + r < C) {
+        const size_t o = (size_t)(c0 + r) * D + a8;
+        v1 = *(const uint4*)(P1 + o);
+        v2 = *(const uint4*)(P2 + o);
+        v3 = *(const uint4*)(P3 + o);
+      }
+      *(uint4*)(W1 + r * WROW + a8) = v1;
+      *(uint4*)(W2 + r * WROW + a8) = v2;
+      *(uint4*)(W3 + r * WROW + a8) = v3;
+    }
+    if (tid < CT) {
+      const bool in = c0 + tid < C;
+      bs[tid] = in ? b32[(size_t)h * C + c0 + tid] : INFINITY;
+      ns[tid] = in ? wn[(size_t)h * C + c0 + tid] : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int cb = 0; cb < CT / 16; ++cb) {
+      f32x4_t shi[TB], srest[TB];
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        shi[tb] = zero;
+        srest[tb] = zero;
+      }
+      const int rowo = (16 * cb + c16) * WROW + 8 * g;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const bf16x8_t a1 = *(const bf16x8_t*)(W1 + rowo + 32 * s);
+        const bf16x8_t a2 = *(const bf16x8_t*)(W2 + rowo + 32 * s);
+        const bf16x8_t a3 = *(const bf16x8_t*)(W3 + rowo + 32 * s);
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          const f32x4_t p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[tb][s], zero, 0, 0, 0);
+          f32x4_t p2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, xf[tb][s], zero, 0, 0, 0);
+          p2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], p2, 0, 0, 0);
+          shi[tb] += p1;
+          srest[tb] += p2;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int vl = 16 * cb + 4 * g + r;
+        const float bv = bs[vl], nv = ns[vl];
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          const float sc = fmaf(-2.0f, shi[tb][r] + srest[tb][r], bv);
+          const float e = fmaf(kx[tb], nv, MARGIN * U24 * (fabsf(bv) + fabsf(sc)));
+          if (sc < best[tb]) {
+            lo2[tb] = fminf(lo2[tb], 2.0f * best[tb] - ub[tb]);  // old best joins the others
+            best[tb] = sc;
+            ub[tb] = sc + e;
+            bidx[tb] = c0 + vl;
+          } else {
+            lo2[tb] = fminf(lo2[tb], sc - e);
           }
         }
       }
     }
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    rs[cg][tg + 16 * i] = best[i];
-    ri[cg][tg + 16 * i] = bidx[i];
-  }
-  __syncthreads();
-  if (tid < TM && t0 + tid < N) {
-    double bb = rs[0][tid];
-    int bi = ri[0][tid];
-    for (int g = 1; g < 16; ++g) {
-      const double s = rs[g][tid];
-      const int v = ri[g][tid];
-      if (s < bb || (s == bb && v < bi)) {
-        bb = s;
-        bi = v;
+  for (int tb = 0; tb < TB; ++tb) {
+    // merge over the four lane groups holding this token
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float ob = __shfl_xor(best[tb], o, 64), ou = __shfl_xor(ub[tb], o, 64);
+      const float ol = __shfl_xor(lo2[tb], o, 64);
+      const int oi = __shfl_xor(bidx[tb], o, 64);
+      if (ob < best[tb] || (ob == best[tb] && oi < bidx[tb])) {
+        lo2[tb] = fminf(fminf(lo2[tb], ol), 2.0f * best[tb] - ub[tb]);
+        best[tb] = ob;
+        ub[tb] = ou;
+        bidx[tb] = oi;
+      } else {
+        lo2[tb] = fminf(fminf(lo2[tb], ol), 2.0f * ob - ou);
       }
     }
-    if (!isfinite(bb) || bi >= C) {
-      raise_status(status, ST_NONFINITE);
-      bi = 0;
+    const int tok = t0 + 16 * tb + c16;
+    if (g == 0 && tok < N) {
+      const bool ok = isfinite(best[tb]) && isfinite(ub[tb]) && (lo2[tb] > ub[tb]);
+      if (ok) {
+        labels[(size_t)h * N + tok] = bidx[tb];
+      } else {
+        const int slot = atomicAdd(nflag + h, 1);
+        flags[(size_t)h * N + slot] = tok;
+      }
     }
-    labels[(size_t)h * N + t0 + tid] = bi;
+  }
+}
+
+// Exact float64 assignment: labels[j] = argmin_v (b_v - 2 x_j . w_v), ties to
+// the lowest v.  TM tokens x 64 centroids per step (centroids staged in LDS
+// in 32-dim slices), 4 tokens x (64 / (256 / (TM / 4))) centroids per
+// thread.  With a token list (list != null) it assigns only the first
+// count[h] listed tokens (the ones the fast path left uncertified);
+// workgroups loop over tiles.
+template <typename T, int D, int TM>
+__global__ __launch_bounds__(256) void k_assign64(const T* __restrict__ X, const double* __restrict__ w,
+                                                  const double* __restrict__ b, int N, int C,
+                                                  const int* __restrict__ list,
+                                                  const int* __restrict__ count,
+                                                  int* __restrict__ labels, int* status) {
+  constexpr int TC = 64, DC = 32;
+  constexpr int TGN = TM / 4;        // token groups (4 tokens each, strided by TGN)
+  constexpr int CGN = 256 / TGN;     // centroid groups
+  constexpr int CPT = TC / CGN;      // centroids per thread and tile (strided by CGN)
+  __shared__ float xs[TM][D + 1];
+  __shared__ double wsm[TC][DC + 1];
+  __shared__ double bs[TC];
+  __shared__ double rs[CGN][TM];
+  __shared__ int ri[CGN][TM];
+  __shared__ int tok_s[TM];
+  const int h = blockIdx.y, tid = threadIdx.x;
+  const int ntok = list ? min(count[h], N) : N;
+  const T* Xh = X + (size_t)h * N * D;
+  const double* wh = w + (size_t)h * C * D;
+  const int tg = tid % TGN, cg = tid / TGN;
+  for (int t0 = blockIdx.x * TM; t0 < ntok; t0 += gridDim.x * TM) {
+    __syncthreads();
+    if (tid < TM) {
+      int tok = -1;
+      if (t0 + tid < ntok) tok = list ? list[(size_t)h * N + t0 + tid] : t0 + tid;
+      tok_s[tid] = ((unsigned)tok < (unsigned)N) ? tok : -1;
+    }
+    __syncthreads();
+    for (int e = tid; e < TM * D; e += 256) {
+      const int r = e / D, c = e % D;
+      const int tok = tok_s[r];
+      xs[r][c] = tok >= 0 ? to_f(Xh[(size_t)tok * D + c]) : 0.0f;
+    }
+    double best[4];
+    int bidx[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      best[i] = INFINITY;
+      bidx[i] = 0x7fffffff;
+    }
+    for (int c0 = 0; c0 < C; c0 += TC) {
+      double acc[4][CPT];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) acc[i][j] = 0.0;
+      for (int a0 = 0; a0 < D; a0 += DC) {
+        __syncthreads();
+        for (int e = tid; e < TC * DC; e += 256) {
+          const int r = e / DC, c = e % DC;
+          wsm[r][c] = (c0 + r < C) ? wh[(size_t)(c0 + r) * D + a0 + c] : 0.0;
+        }
+        if (a0 == 0 && tid < TC) bs[tid] = (c0 + tid < C) ? b[(size_t)h * C + c0 + tid] : 0.0;
+        __syncthreads();
+#pragma unroll 4
+        for (int a = 0; a < DC; ++a) {
+          double xv[4], wv[CPT];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) xv[i] = (double)xs[tg + TGN * i][a0 + a];
+#pragma unroll
+          for (int j = 0; j < CPT; ++j) wv[j] = wsm[cg + CGN * j][a];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < CPT; ++j) acc[i][j] = fma(xv[i], wv[j], acc[i][j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        const int v = c0 + cg + CGN * j;
+        if (v < C) {
+          const double bv = bs[cg + CGN * j];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const double sc = fma(-2.0, acc[i][j], bv);
+            if (sc < best[i] || (sc == best[i] && v < bidx[i])) {
+              best[i] = sc;
+              bidx[i] = v;
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      rs[cg][tg + TGN * i] = best[i];
+      ri[cg][tg + TGN * i] = bidx[i];
+    }
+    __syncthreads();
+    if (tid < TM && tok_s[tid] >= 0) {
+      double bb = rs[0][tid];
+      int bi = ri[0][tid];
+      for (int q = 1; q < CGN; ++q) {
+        const double sc = rs[q][tid];
+        const int v = ri[q][tid];
+        if (sc < bb || (sc == bb && v < bi)) {
+          bb = sc;
+          bi = v;
+        }
+      }
+      if (!isfinite(bb) || bi >= C) {
+        raise_status(status, ST_NONFINITE);
+        bi = 0;
+      }
+      labels[(size_t)h * N + tok_s[tid]] = bi;
+    }
   }
 }
 
 // Segmented mean over permuted rows: block v of head h averages
-// X[perm[i]] (X[i] when perm is null) for offsets[v] <= i < offsets[v+1],
-// summing in float64 in increasing position order.  Empty blocks keep mu64
-// and give c32 = 0.
-template <typename T>
-__global__ void k_segment_mean(const T* __restrict__ X, const int* __restrict__ perm,
-                               const int* __restrict__ offsets, int N, int D, int C,
-                               double* __restrict__ mu64, float* __restrict__ c32,
-                               int* __restrict__ sizes) {
-  const int h = blockIdx.y, v = blockIdx.x, a = threadIdx.x;
+// X[perm[i]] (X[i] when perm is null) for offsets[v] <= i < offsets[v+1] in
+// float64.  256 threads = 16 row lanes x 16 column chunks (D/16 columns
+// each); row lane j sums rows j, j+16, ... and the 16 partial sums are added
+// in lane order, so the result is deterministic.  Empty blocks keep mu64 and
+// give c32 = 0.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_segment_mean(const T* __restrict__ X,
+                                                      const int* __restrict__ perm,
+                                                      const int* __restrict__ offsets, int N,
+                                                      int C, double* __restrict__ mu64,
+                                                      float* __restrict__ c32,
+                                                      int* __restrict__ sizes) {
+  constexpr int RL = 16, CW = D / 16;  // row lanes, columns per thread
+  __shared__ double part[RL][D + 1];
+  const int h = blockIdx.y, v = blockIdx.x, tid = threadIdx.x;
   const int* off = offsets + (size_t)h * (C + 1);
   const int o0 = min(max(off[v], 0), N), o1 = min(max(off[v + 1], o0), N);
   const int n = o1 - o0;
-  if (sizes && a == 0) sizes[(size_t)h * C + v] = n;
-  const size_t dst = ((size_t)h * C + v) * D + a;
+  if (sizes && tid == 0) sizes[(size_t)h * C + v] = n;
+  const size_t dst = ((size_t)h * C + v) * D;
   if (n <= 0) {
-    if (c32) c32[dst] = 0.0f;
+    if (c32)
+      for (int a = tid; a < D; a += 256) c32[dst + a] = 0.0f;
     return;
   }
   const int* p = perm ? perm + (size_t)h * N : nullptr;
   const T* Xh = X + (size_t)h * N * D;
-  double s = 0.0;
-  for (int r = o0; r < o1; ++r) {
+  const int j = tid / 16, c0 = (tid % 16) * CW;
+  double acc[CW];
+#pragma unroll
+  for (int c = 0; c < CW; ++c) acc[c] = 0.0;
+  for (int r = o0 + j; r < o1; r += RL) {
     const int idx = p ? p[r] : r;
-    if ((unsigned)idx < (unsigned)N) s += (double)to_f(Xh[(size_t)idx * D + a]);
+    if ((unsigned)idx < (unsigned)N) {
+      const T* xr = Xh + (size_t)idx * D + c0;
+#pragma unroll
+      for (int c = 0; c < CW; ++c) acc[c] += (double)to_f(xr[c]);
+    }
   }
-  const double m = s / (double)n;
-  if (mu64) mu64[dst] = m;
-  if (c32) c32[dst] = (float)m;
+#pragma unroll
+  for (int c = 0; c < CW; ++c) part[j][c0 + c] = acc[c];
+  __syncthreads();
+  for (int a = tid; a < D; a += 256) {
+    double sum = 0.0;
+    for (int q = 0; q < RL; ++q) sum += part[q][a];
+    const double m = sum / (double)n;
+    if (mu64) mu64[dst + a] = m;
+    if (c32) c32[dst + a] = (float)m;
+  }
 }
 
 // ---------------------------------------------------------------- launchers
@@ -261,12 +516,21 @@ park_status launch_segment_mean(const void* X, const int* perm, const int* offse
                                 int D, int dtype, int C, double* mu64, float* c32, int* sizes,
                                 hipStream_t st) {
   dim3 g(C, H);
-  if (dtype == PARK_BF16)
-    PARK_LAUNCH("segment_mean", k_segment_mean<bf16_t>, g, dim3(D), 0, st, (const bf16_t*)X, perm,
-                offsets, N, D, C, mu64, c32, sizes);
-  else
-    PARK_LAUNCH("segment_mean", k_segment_mean<float>, g, dim3(D), 0, st, (const float*)X, perm,
-                offsets, N, D, C, mu64, c32, sizes);
+  if (D == 128) {
+    if (dtype == PARK_BF16)
+      PARK_LAUNCH("segment_mean", (k_segment_mean<bf16_t, 128>), g, dim3(256), 0, st,
+                  (const bf16_t*)X, perm, offsets, N, C, mu64, c32, sizes);
+    else
+      PARK_LAUNCH("segment_mean", (k_segment_mean<float, 128>), g, dim3(256), 0, st,
+                  (const float*)X, perm, offsets, N, C, mu64, c32, sizes);
+  } else {
+    if (dtype == PARK_BF16)
+      PARK_LAUNCH("segment_mean", (k_segment_mean<bf16_t, 64>), g, dim3(256), 0, st,
+                  (const bf16_t*)X, perm, offsets, N, C, mu64, c32, sizes);
+    else
+      PARK_LAUNCH("segment_mean", (k_segment_mean<float, 64>), g, dim3(256), 0, st,
+                  (const float*)X, perm, offsets, N, C, mu64, c32, sizes);
+  }
   return PARK_OK;
 }
 
@@ -274,18 +538,38 @@ template <typename T, int D>
 static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int C, int T_,
                                uint64_t seed, int side, const KmeansBufs& kb, int* status,
                                hipStream_t st) {
+  constexpr bool fast = sizeof(T) == 2;  // bf16 points: MFMA fast path + float64 refine
+  const size_t plane = (size_t)H * C * D;
   PARK_LAUNCH("kmeans_init", k_init_idx, dim3(H), dim3(1024), 0, st, N, C, seed, side, kb.init);
   PARK_LAUNCH("kmeans_seed", k_seed_centroids<T>, dim3(C, H), dim3(D), 0, st, X,
               (const int*)kb.init, N, D, C, kb.mu);
+  // refine grid: persistent workgroups per head looping over 16-token tiles
+  int rg = (2048 + H - 1) / H;
+  const int max_tiles = (N + 15) / 16;
+  rg = rg < 2 ? 2 : rg;
+  rg = rg > max_tiles ? max_tiles : rg;
   for (int t = 0; t < T_; ++t) {
     PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3((C + 15) / 16, H), dim3(256), 0, st,
-                (const double*)kb.mu, Gbar, C, kb.w, kb.b);
-    PARK_LAUNCH("kmeans_assign64", (k_assign64<T, D>), dim3((N + 63) / 64, H), dim3(256), 0, st, X,
-                (const double*)kb.w, (const double*)kb.b, N, C, kb.labels, status);
+                (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane,
+                fast ? kb.b32 : nullptr, fast ? kb.wn : nullptr);
+    if constexpr (fast) {
+      PARK_LAUNCH("kmeans_reset", k_reset_counts, dim3((H + 63) / 64), dim3(64), 0, st, kb.nflag,
+                  H);
+      PARK_LAUNCH("kmeans_assign_fast", k_assign_fast<D>, dim3((N + 255) / 256, H), dim3(256), 0,
+                  st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane, (const float*)kb.b32,
+                  (const float*)kb.wn, N, C, kb.labels, kb.flags, kb.nflag);
+      PARK_LAUNCH("kmeans_refine64", (k_assign64<T, D, 16>), dim3(rg, H), dim3(256), 0, st, X,
+                  (const double*)kb.w, (const double*)kb.b, N, C, (const int*)kb.flags,
+                  (const int*)kb.nflag, kb.labels, status);
+    } else {
+      PARK_LAUNCH("kmeans_assign64", (k_assign64<T, D, 64>), dim3((N + 63) / 64, H), dim3(256), 0, st,
+                  X, (const double*)kb.w, (const double*)kb.b, N, C, (const int*)nullptr,
+                  (const int*)nullptr, kb.labels, status);
+    }
     if (t + 1 < T_) {
       PARK_TRY(launch_count_sort(kb.labels, H, N, C, kb.thist, kb.perm, kb.offsets, st));
-      PARK_LAUNCH("segment_mean", k_segment_mean<T>, dim3(C, H), dim3(D), 0, st, X,
-                  (const int*)kb.perm, (const int*)kb.offsets, N, D, C, kb.mu, (float*)nullptr,
+      PARK_LAUNCH("segment_mean", (k_segment_mean<T, D>), dim3(C, H), dim3(256), 0, st, X,
+                  (const int*)kb.perm, (const int*)kb.offsets, N, C, kb.mu, (float*)nullptr,
                   (int*)nullptr);
     }
   }

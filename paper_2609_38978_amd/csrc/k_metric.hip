@@ -123,10 +123,11 @@ __global__ __launch_bounds__(256) void k_metric_chol(const double* __restrict__ 
     const double lkk = piv;
     for (int i = k + 1 + tid; i < D; i += 256) A[i * D + k] = A[i * D + k] / lkk;
     __syncthreads();
-    const int m = D - k - 1;
-    for (int e = tid; e < m * m; e += 256) {
-      const int i = k + 1 + e / m, j = k + 1 + e % m;
-      if (j <= i) A[i * D + j] = fma(-A[i * D + k], A[j * D + k], A[i * D + j]);
+    // trailing update of the lower triangle, 16 x 16 thread grid
+    for (int i = k + 1 + (tid >> 4); i < D; i += 16) {
+      const double lik = A[i * D + k];
+      for (int j = k + 1 + (tid & 15); j <= i; j += 16)
+        A[i * D + j] = fma(-lik, A[j * D + k], A[i * D + j]);
     }
     __syncthreads();
   }

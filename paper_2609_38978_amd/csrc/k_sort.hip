@@ -8,18 +8,29 @@
 
 namespace park {
 
-constexpr int SORT_TILE = 2048;
+// Tokens per scatter tile: small enough to give >= ~512 wavefronts over all
+// heads, large enough that the per-head histogram table (C x tiles) stays
+// below 64K entries so the single-workgroup scan stays short.
+int sort_tile(int H, int N, int C) {
+  int t = 256;
+  while ((long)H * ((N + t - 1) / t) > 512 && t < 8192) t *= 2;
+  while ((long)C * ((N + t - 1) / t) > 65536 && t < (1 << 30)) t *= 2;
+  return t;
+}
 
-int sort_tiles(int N) { return (N + SORT_TILE - 1) / SORT_TILE; }
+int sort_tiles(int H, int N, int C) {
+  const int t = sort_tile(H, N, C);
+  return (N + t - 1) / t;
+}
 
 // thist[h][v][tile] = #{ i in tile : z_i = v }
 __global__ __launch_bounds__(256) void k_sort_hist(const int* __restrict__ labels, int N, int C,
-                                                   int* __restrict__ thist) {
+                                                   int tile_sz, int* __restrict__ thist) {
   extern __shared__ int hist[];
   const int h = blockIdx.y, tile = blockIdx.x, nt = gridDim.x;
   for (int v = threadIdx.x; v < C; v += 256) hist[v] = 0;
   __syncthreads();
-  const int i0 = tile * SORT_TILE, i1 = min(N, i0 + SORT_TILE);
+  const int i0 = tile * tile_sz, i1 = min(N, i0 + tile_sz);
   const int* z = labels + (size_t)h * N;
   for (int i = i0 + threadIdx.x; i < i1; i += 256) {
     const int v = z[i];
@@ -85,14 +96,15 @@ __global__ __launch_bounds__(1024) void k_sort_scan(int* __restrict__ thist, int
 // Stable scatter: one wavefront per tile, tokens in increasing order.
 // Equal labels inside a wave are matched with one ballot per label bit.
 __global__ __launch_bounds__(64) void k_sort_scatter(const int* __restrict__ labels, int N, int C,
-                                                     int nbits, const int* __restrict__ tbase,
+                                                     int nbits, int tile_sz,
+                                                     const int* __restrict__ tbase,
                                                      int* __restrict__ perm) {
   extern __shared__ int run[];
   const int h = blockIdx.y, tile = blockIdx.x, nt = gridDim.x, lane = threadIdx.x;
   const int* b = tbase + (size_t)h * C * nt;
   for (int v = lane; v < C; v += 64) run[v] = b[(size_t)v * nt + tile];
   __syncthreads();
-  const int i0 = tile * SORT_TILE, i1 = min(N, i0 + SORT_TILE);
+  const int i0 = tile * tile_sz, i1 = min(N, i0 + tile_sz);
   const int* z = labels + (size_t)h * N;
   int* p = perm + (size_t)h * N;
   const uint64_t lt = (1ull << lane) - 1ull;
@@ -118,14 +130,15 @@ __global__ __launch_bounds__(64) void k_sort_scatter(const int* __restrict__ lab
 
 park_status launch_count_sort(const int* labels, int H, int N, int C, int* thist, int* perm,
                               int* offsets, hipStream_t st) {
-  const int nt = sort_tiles(N);
+  const int tsz = sort_tile(H, N, C);
+  const int nt = (N + tsz - 1) / tsz;
   const size_t lds = (size_t)C * sizeof(int);
   int nbits = 1;
   while ((1 << nbits) < C) ++nbits;
-  PARK_LAUNCH("sort_hist", k_sort_hist, dim3(nt, H), dim3(256), lds, st, labels, N, C, thist);
+  PARK_LAUNCH("sort_hist", k_sort_hist, dim3(nt, H), dim3(256), lds, st, labels, N, C, tsz, thist);
   PARK_LAUNCH("sort_scan", k_sort_scan, dim3(H), dim3(1024), 0, st, thist, C, nt, N, offsets);
   PARK_LAUNCH("sort_scatter", k_sort_scatter, dim3(nt, H), dim3(64), lds, st, labels, N, C, nbits,
-              (const int*)thist, perm);
+              tsz, (const int*)thist, perm);
   return PARK_OK;
 }
 

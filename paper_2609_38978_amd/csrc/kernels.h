@@ -14,7 +14,7 @@ park_status launch_transform(const void* X, const double* R, int H, int N, int D
                              float* Xt, hipStream_t st);
 
 // k_sort.hip ----------------------------------------------------------------
-int sort_tiles(int N);
+int sort_tiles(int H, int N, int C);
 // Stable counting sort of labels[h][0..N) into perm/offsets (+ sizes).
 park_status launch_count_sort(const int* labels, int H, int N, int C, int* thist, int* perm,
                               int* offsets, hipStream_t st);
@@ -32,6 +32,12 @@ struct KmeansBufs {
   int* perm;      // [H][N]
   int* offsets;   // [H][C+1]
   int* status;    // sticky device status word
+  // fast path (bf16 points)
+  bf16_t* w3;     // [3][H][C][D] w as three bf16 parts
+  float* b32;     // [H][C]
+  float* wn;      // [H][C]    |w_v| (rounded up)
+  int* nflag;     // [H]       tokens left for the float64 refine
+  int* flags;     // [H][N]    their indices
 };
 park_status launch_kmeans(const void* X, const double* Gbar /* null = Euclidean */, int H, int N,
                           int D, int dtype, int C, int T, uint64_t seed, int side,

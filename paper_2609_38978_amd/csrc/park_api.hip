@@ -130,6 +130,11 @@ struct ClusterWs {
   double* b;
   int* labels;
   int* thist;
+  bf16_t* w3;
+  float* b32;
+  float* wn;
+  int* nflag;
+  int* flags;
 };
 
 static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
@@ -143,7 +148,12 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   c.w = cv.take<double>((size_t)H * C * D);
   c.b = cv.take<double>((size_t)H * C);
   c.labels = cv.take<int>((size_t)H * N);
-  c.thist = cv.take<int>((size_t)H * C * sort_tiles(N));
+  c.thist = cv.take<int>((size_t)H * C * sort_tiles(H, N, C));
+  c.w3 = cv.take<bf16_t>((size_t)3 * H * C * D);
+  c.b32 = cv.take<float>((size_t)H * C);
+  c.wn = cv.take<float>((size_t)H * C);
+  c.nflag = cv.take<int>((size_t)H);
+  c.flags = cv.take<int>((size_t)H * N);
   return c;
 }
 
@@ -206,6 +216,11 @@ static park_status cluster_body(const void* X, const void* Qm, const park_dims& 
   kb.perm = perm;
   kb.offsets = offsets;
   kb.status = status;
+  kb.w3 = cw.w3;
+  kb.b32 = cw.b32;
+  kb.wn = cw.wn;
+  kb.nflag = cw.nflag;
+  kb.flags = cw.flags;
   return launch_kmeans(X, Gbar, H, N, D, dm.dtype, C, T, seed, side, kb, st);
 }
 
