@@ -87,15 +87,19 @@ __global__ void k_seed_centroids(const T* __restrict__ X, const int* __restrict_
 
 // w_v = Gbar mu_v (or mu_v), b_v = mu_v . w_v;  16 centroids per workgroup.
 // Gbar is symmetric, so thread (a, group) reads column a of it coalesced and
-// applies each element to 16 / (256 / D) centroids.  When `w3` is given the
-// fast-path operands are written too: w_v split into three bf16 parts (three
-// planes of H*C*D), b_v in float, and |w_v| rounded up for the error bound.
+// applies each element to 16 / (256 / D) centroids.  `wT` (optional) receives
+// w transposed, [D][C] per head, for the float64 refinement.  When `w3` is
+// given the fast-path operands are written too: w_v split into three bf16
+// parts (three planes of H*C*D), b_v in float, |w_v| rounded up and the
+// |b_v| term of the error bound (see k_assign_fast).
 template <int D>
 __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
                                               const double* __restrict__ Gbar, int C,
                                               double* __restrict__ w, double* __restrict__ b,
-                                              bf16_t* __restrict__ w3, size_t plane,
-                                              float* __restrict__ b32, float* __restrict__ wn) {
+                                              double* __restrict__ wT, bf16_t* __restrict__ w3,
+                                              size_t plane, float* __restrict__ b32,
+                                              float* __restrict__ wn, float* __restrict__ eb,
+                                              float* __restrict__ bmax, int* __restrict__ nflag) {
   constexpr int CB = 16, NG = 256 / D, PER = CB / NG;
   __shared__ double ms[CB][D];
   __shared__ double ws[CB][D + 1];
@@ -127,6 +131,7 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
     if (v0 + r < C) {
       const size_t o = ((size_t)h * C + v0 + r) * D + a;
       w[o] = acc[k];
+      if (wT) wT[((size_t)h * D + a) * C + v0 + r] = acc[k];
       if (w3) {
         // w = w1 + w2 + w3 + r with bf16 parts and |r| <= 2^-24 |w| (1 + 2^-7)
         const bf16_t p1 = f2bf((float)acc[k]);
@@ -140,6 +145,7 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
     }
   }
   __syncthreads();
+  float fn = 0.0f, fe = 0.0f;
   if (tid < CB && v0 + tid < C) {
     double s = 0.0, n2 = 0.0;
     for (int c = 0; c < D; ++c) {
@@ -148,16 +154,25 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
     }
     b[(size_t)h * C + v0 + tid] = s;
     if (b32) {
+      fn = (float)(sqrt(n2) * (1.0 + 1e-6));
+      fe = (float)(fabs(s) * (2.0 * 1.1 * 5.9604644775390625e-08) * (1.0 + 1e-6));
       b32[(size_t)h * C + v0 + tid] = (float)s;
-      wn[(size_t)h * C + v0 + tid] = (float)(sqrt(n2) * (1.0 + 1e-6));
+      wn[(size_t)h * C + v0 + tid] = fn;
+      eb[(size_t)h * C + v0 + tid] = fe;
     }
   }
-}
-
-// Resets the per-head count of tokens left for the float64 assignment.
-__global__ void k_reset_counts(int* __restrict__ nflag, int H) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < H) nflag[i] = 0;
+  if (b32 && tid < 64) {
+    // this block's maxima of |w_v| and eb_v (reduced by the assignment)
+    for (int o = 8; o > 0; o >>= 1) {
+      fn = fmaxf(fn, __shfl_xor(fn, o, 64));
+      fe = fmaxf(fe, __shfl_xor(fe, o, 64));
+    }
+    if (tid == 0) {
+      bmax[((size_t)h * gridDim.x + blockIdx.x) * 2] = fn;
+      bmax[((size_t)h * gridDim.x + blockIdx.x) * 2 + 1] = fe;
+      if (blockIdx.x == 0) nflag[h] = 0;  // the previous refinement has completed
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -165,24 +180,32 @@ __global__ void k_reset_counts(int* __restrict__ nflag, int H) {
 //
 // For a bf16 point x the score s_v = b_v - 2 x.w_v is evaluated with w_v
 // split into three bf16 parts, w = w1 + w2 + w3 + r, |r| <= 2^-24 (1+2^-7)|w|.
-// All products are bf16 x bf16, exact in float.  Each 32-wide k-step of the
-// x.w1 products is summed by one v_mfma_f32_16x16x32_bf16 into a fresh
-// accumulator (<= 32 roundings), the k-step partials are added on the VALU
-// (round-to-nearest), and x.(w2 + w3) runs in a second chain of the same
-// shape whose terms are 2^-8 smaller.  With delta = 2^-23 per MFMA addition
-// (any faithful rounding) the forward error of t^ = x.w is at most
-//   et * sum_a |x_a w_a|,  et = 2^-24 (1.01) + (32 delta + (KS-1) 2^-24) 1.01
-//                            + 2^-8 (64 delta + KS 2^-24) 1.01 + 2^-24 1.01,
-// and with sum_a |x_a w_a| <= |x| |w_v| and the float roundings of b_v and of
-// the score, |s^_v - s_v| <= E_v = 2 et |x| |w_v| + 2^-24 (|b_v| + |s^_v|).
-// A token is certified when, for its fast argmin v1, s^_v - E_v > s^_v1 +
-// E_v1 for every other v: then v1 is the exact argmin.  Otherwise (near-ties,
-// exact ties) it is listed for the float64 assignment.  A 10% margin covers
-// the rounding of |x| and of the bound itself.
+// All products are bf16 x bf16, exact in float.  x.w1 is accumulated over the
+// D dimensions in one chain of v_mfma_f32_16x16x32_bf16, x.(w2 + w3), whose
+// terms are 2^-8 smaller, in a second chain, and the two are added once.
+// With delta = 2^-23 per addition inside an MFMA (any faithful rounding) and
+// 2^-24 for the VALU roundings, the forward error of t^ = x.w is at most
+//   et sum_a |x_a w_a|,  et = 2^-24 1.01 + (D+1) delta (1 + 2^-7)
+//                            + 2^-8 1.01 (2D+1) delta + 2^-24 1.01,
+// and with sum_a |x_a w_a| <= |x| |w_v|, the float roundings of b_v and of
+// the score, and |s^_v| <= |b_v| + 2.01 |x| |w_v|:
+//   |s^_v - s_v| <= E_v = Kx |w_v| + eb_v,
+//   Kx = 1.1 (2 et + 2.01 2^-24) |x|,  eb_v = 1.1 * 2 * 2^-24 |b_v|
+// (the factor 1.1 covers the rounding of |x| and of the bound itself).  A
+// token is certified when, for its fast argmin v1, s^_v - E_v > s^_v1 + E_v1
+// for every other v: then v1 is the exact argmin.  Otherwise (near-ties,
+// exact ties) it is listed for the float64 refinement.
+//
+// Only scores within E_max = Kx max|w| + max eb of the running best can
+// matter, so the per-score bookkeeping runs only when some lane of the
+// wavefront holds such a score (a wave-uniform branch); a skipped score
+// s^_v > ub + E_max has lower bound s^_v - E_v > ub, above the final best's
+// upper bound.
 //
 // Workgroup = 256 tokens (4 wavefronts x 4 blocks of 16), centroid tiles of 64
-// staged in LDS.  MFMA orientation: A = 16 centroids x 32 dims, B = 32 dims x
-// 16 tokens, so lane l holds centroids 4(l/16)+r of token l%16.
+// staged in LDS with the next tile prefetched into registers.  MFMA
+// orientation: A = 16 centroids x 32 dims, B = 32 dims x 16 tokens, so lane l
+// holds centroids 4(l/16)+r of token l%16.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
@@ -190,20 +213,25 @@ template <int D>
 __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ X,
                                                      const bf16_t* __restrict__ w3, size_t plane,
                                                      const float* __restrict__ b32,
-                                                     const float* __restrict__ wn, int N, int C,
+                                                     const float* __restrict__ wn,
+                                                     const float* __restrict__ eb,
+                                                     const float* __restrict__ bmax, int nbm,
+                                                     int N, int C,
                                                      int* __restrict__ labels,
                                                      int* __restrict__ flags,
                                                      int* __restrict__ nflag) {
-  constexpr int TB = 4, CT = 64, KS = D / 32, WROW = D + 8;
+  constexpr int TB = 4, CT = 64, KS = D / 32, WROW = D + 8, CH = D / 8;
+  constexpr int NL = CT * CH / 256;  // 16-byte chunks of each part per thread and tile
   constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f;
-  constexpr float ET = U24 * 1.01f + (32.0f * DEL + (KS - 1) * U24) * 1.01f +
-                       0.00390625f * (64.0f * DEL + KS * U24) * 1.01f + U24 * 1.01f;
-  constexpr float MARGIN = 1.1f;
+  constexpr float ET = U24 * 1.01f + (D + 1) * DEL * 1.0079f + 0.00390625f * 1.01f * (2 * D + 1) * DEL +
+                       U24 * 1.01f;
+  constexpr float KXC = 1.1f * (2.0f * ET + 2.01f * U24) * 1.0001f;
   __shared__ __attribute__((aligned(16))) bf16_t W1[CT * WROW];
   __shared__ __attribute__((aligned(16))) bf16_t W2[CT * WROW];
   __shared__ __attribute__((aligned(16))) bf16_t W3[CT * WROW];
-  __shared__ float bs[CT];
-  __shared__ float ns[CT];
+  __shared__ __attribute__((aligned(16))) float bs[CT];
+  __shared__ __attribute__((aligned(16))) float ns[CT];
+  __shared__ __attribute__((aligned(16))) float es[CT];
   const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, g = l >> 4,
             c16 = l & 15;
   const int t0 = blockIdx.x * 256 + w * 64;
@@ -227,56 +255,118 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       }
     }
   }
-  float kx[TB];  // MARGIN * 2 et |x| (|x| rounded up)
+  __shared__ float mx_s[2];
+  if (tid < 64) {
+    float a = 0.0f, c = 0.0f;
+    for (int i = tid; i < nbm; i += 64) {
+      a = fmaxf(a, bmax[((size_t)h * nbm + i) * 2]);
+      c = fmaxf(c, bmax[((size_t)h * nbm + i) * 2 + 1]);
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      a = fmaxf(a, __shfl_xor(a, o, 64));
+      c = fmaxf(c, __shfl_xor(c, o, 64));
+    }
+    if (tid == 0) {
+      mx_s[0] = a;
+      mx_s[1] = c;
+    }
+  }
+  __syncthreads();
+  const float nmax = mx_s[0], ebmax = mx_s[1];
+  float kx[TB], emax[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
     float xs = xsq[tb] + __shfl_xor(xsq[tb], 16, 64);
     xs += __shfl_xor(xs, 32, 64);
-    kx[tb] = MARGIN * 2.0f * ET * sqrtf(xs) * 1.0001f;
+    kx[tb] = KXC * sqrtf(xs);
+    emax[tb] = fmaf(kx[tb], nmax, ebmax) * 1.0001f;
   }
-  // per token: best fast score, its index, its upper bound, and the lowest
-  // lower bound among all other centroids
-  float best[TB], ub[TB], lo2[TB];
+  // per token and lane: best fast score, its index, its upper bound, the
+  // lowest lower bound among the lane's other centroids, and the threshold
+  // above which a score cannot matter
+  float best[TB], ub[TB], lo2[TB], thr[TB];
   int bidx[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
     best[tb] = INFINITY;
     ub[tb] = INFINITY;
     lo2[tb] = INFINITY;
+    thr[tb] = INFINITY;
     bidx[tb] = 0;
   }
   const bf16_t* P1 = w3 + (size_t)h * C * D;
   const bf16_t* P2 = P1 + plane;
   const bf16_t* P3 = P2 + plane;
   const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  uint4 r1[NL], r2[NL], r3[NL];
+  float rb = INFINITY, rn = 0.0f, re = 0.0f;
+  // prefetch tile 0
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int e = tid + 256 * i, r = e / CH, ch = e % CH;
+    uint4 v1 = make_uint4(0u, 0u, 0u, 0u), v2 = v1, v3 = v1;
+    if (r < C) {
+      const size_t o = (size_t)r * D + 8 * ch;
+      v1 = *(const uint4*)(P1 + o);
+      v2 = *(const uint4*)(P2 + o);
+      v3 = *(const uint4*)(P3 + o);
+    }
+    r1[i] = v1;
+    r2[i] = v2;
+    r3[i] = v3;
+  }
+  if (tid < CT && tid < C) {
+    rb = b32[(size_t)h * C + tid];
+    rn = wn[(size_t)h * C + tid];
+    re = eb[(size_t)h * C + tid];
+  }
   for (int c0 = 0; c0 < C; c0 += CT) {
     __syncthreads();
-    for (int e = tid; e < CT * (D / 8); e += 256) {
-      const int r = e / (D / 8), a8 = 8 * (e % (D / 8));
-      uint4 v1 = make_uint4(0u, 0u, 0u, 0u), v2 = v1, v3 = v1;
-      if (c0 + r < C) {
-        const size_t o = (size_t)(c0 + r) * D + a8;
-        v1 = *(const uint4*)(P1 + o);
-        v2 = *(const uint4*)(P2 + o);
-        v3 = *(const uint4*)(P3 + o);
-      }
-      *(uint4*)(W1 + r * WROW + a8) = v1;
-      *(uint4*)(W2 + r * WROW + a8) = v2;
-      *(uint4*)(W3 + r * WROW + a8) = v3;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int e = tid + 256 * i, r = e / CH, ch = e % CH;
+      *(uint4*)(W1 + r * WROW + 8 * ch) = r1[i];
+      *(uint4*)(W2 + r * WROW + 8 * ch) = r2[i];
+      *(uint4*)(W3 + r * WROW + 8 * ch) = r3[i];
     }
     if (tid < CT) {
-      const bool in = c0 + tid < C;
-      bs[tid] = in ? b32[(size_t)h * C + c0 + tid] : INFINITY;
-      ns[tid] = in ? wn[(size_t)h * C + c0 + tid] : 0.0f;
+      bs[tid] = rb;
+      ns[tid] = rn;
+      es[tid] = re;
     }
     __syncthreads();
+    const int c1 = c0 + CT;
+    if (c1 < C) {  // prefetch the next tile while this one is scored
+#pragma unroll
+      for (int i = 0; i < NL; ++i) {
+        const int e = tid + 256 * i, r = e / CH, ch = e % CH;
+        uint4 v1 = make_uint4(0u, 0u, 0u, 0u), v2 = v1, v3 = v1;
+        if (c1 + r < C) {
+          const size_t o = (size_t)(c1 + r) * D + 8 * ch;
+          v1 = *(const uint4*)(P1 + o);
+          v2 = *(const uint4*)(P2 + o);
+          v3 = *(const uint4*)(P3 + o);
+        }
+        r1[i] = v1;
+        r2[i] = v2;
+        r3[i] = v3;
+      }
+      rb = INFINITY;
+      rn = 0.0f;
+      re = 0.0f;
+      if (tid < CT && c1 + tid < C) {
+        rb = b32[(size_t)h * C + c1 + tid];
+        rn = wn[(size_t)h * C + c1 + tid];
+        re = eb[(size_t)h * C + c1 + tid];
+      }
+    }
 #pragma unroll
     for (int cb = 0; cb < CT / 16; ++cb) {
-      f32x4_t shi[TB], srest[TB];
+      f32x4_t ahi[TB], arest[TB];
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
-        shi[tb] = zero;
-        srest[tb] = zero;
+        ahi[tb] = zero;
+        arest[tb] = zero;
       }
       const int rowo = (16 * cb + c16) * WROW + 8 * g;
 #pragma unroll
@@ -286,29 +376,43 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
         const bf16x8_t a3 = *(const bf16x8_t*)(W3 + rowo + 32 * s);
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) {
-          const f32x4_t p1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[tb][s], zero, 0, 0, 0);
-          f32x4_t p2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, xf[tb][s], zero, 0, 0, 0);
-          p2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], p2, 0, 0, 0);
-          shi[tb] += p1;
-          srest[tb] += p2;
+          ahi[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[tb][s], ahi[tb], 0, 0, 0);
+          arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, xf[tb][s], arest[tb], 0, 0, 0);
+          arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
         }
       }
+      const float4 b4 = *(const float4*)(bs + 16 * cb + 4 * g);
+      const float bv[4] = {b4.x, b4.y, b4.z, b4.w};
+      float sc[TB][4];
+      bool hit = false;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int vl = 16 * cb + 4 * g + r;
-        const float bv = bs[vl], nv = ns[vl];
+      for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          sc[tb][r] = fmaf(-2.0f, ahi[tb][r] + arest[tb][r], bv[r]);
+          hit |= !(sc[tb][r] > thr[tb]);
+        }
+      if (__any(hit)) {
+        const float4 n4 = *(const float4*)(ns + 16 * cb + 4 * g);
+        const float4 e4 = *(const float4*)(es + 16 * cb + 4 * g);
+        const float nv[4] = {n4.x, n4.y, n4.z, n4.w};
+        const float ev[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) {
-          const float sc = fmaf(-2.0f, shi[tb][r] + srest[tb][r], bv);
-          const float e = fmaf(kx[tb], nv, MARGIN * U24 * (fabsf(bv) + fabsf(sc)));
-          if (sc < best[tb]) {
-            lo2[tb] = fminf(lo2[tb], 2.0f * best[tb] - ub[tb]);  // old best joins the others
-            best[tb] = sc;
-            ub[tb] = sc + e;
-            bidx[tb] = c0 + vl;
-          } else {
-            lo2[tb] = fminf(lo2[tb], sc - e);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float x = sc[tb][r];
+            const float e = fmaf(kx[tb], nv[r], ev[r]);
+            if (x < best[tb]) {
+              lo2[tb] = fminf(lo2[tb], 2.0f * best[tb] - ub[tb]);  // old best joins the others
+              best[tb] = x;
+              ub[tb] = x + e;
+              bidx[tb] = c0 + 16 * cb + 4 * g + r;
+            } else {
+              lo2[tb] = fminf(lo2[tb], x - e);
+            }
           }
+          thr[tb] = ub[tb] + emax[tb];
         }
       }
     }
@@ -339,6 +443,109 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
         const int slot = atomicAdd(nflag + h, 1);
         flags[(size_t)h * N + slot] = tok;
       }
+    }
+  }
+}
+
+// Float64 assignment of the tokens the fast path could not certify: 16 listed
+// tokens per workgroup, the centroids split over the four wavefronts (one
+// centroid per lane, w read transposed so loads are coalesced), the exact
+// minimum (ties to the lowest id) reduced across lanes and wavefronts.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_refine(const T* __restrict__ X,
+                                                const double* __restrict__ wT,
+                                                const double* __restrict__ b, int N, int C,
+                                                const int* __restrict__ flags,
+                                                const int* __restrict__ nflag,
+                                                int* __restrict__ labels, int* status) {
+  constexpr int TT = 16;
+  __shared__ double xs[TT][D];
+  __shared__ double rs[4][TT];
+  __shared__ int ri[4][TT];
+  __shared__ int tok_s[TT];
+  const int h = blockIdx.y, tid = threadIdx.x, wv = tid >> 6, l = tid & 63;
+  const int cnt = min(nflag[h], N);
+  const double* wh = wT + (size_t)h * D * C;
+  const double* bh = b + (size_t)h * C;
+  const int cpw = ((C + 3) / 4 + 63) / 64 * 64;  // centroids per wavefront
+  const int v_begin = wv * cpw, v_end = min(C, v_begin + cpw);
+  for (int t0 = blockIdx.x * TT; t0 < cnt; t0 += gridDim.x * TT) {
+    __syncthreads();
+    if (tid < TT) {
+      const int tok = t0 + tid < cnt ? flags[(size_t)h * N + t0 + tid] : -1;
+      tok_s[tid] = ((unsigned)tok < (unsigned)N) ? tok : -1;
+    }
+    __syncthreads();
+    for (int e = tid; e < TT * D; e += 256) {
+      const int t = e / D, a = e % D;
+      const int tok = tok_s[t];
+      xs[t][a] = tok >= 0 ? (double)to_f(X[((size_t)h * N + tok) * D + a]) : 0.0;
+    }
+    __syncthreads();
+    double best[TT];
+    int bidx[TT];
+#pragma unroll
+    for (int t = 0; t < TT; ++t) {
+      best[t] = INFINITY;
+      bidx[t] = 0x7fffffff;
+    }
+    for (int v0 = v_begin; v0 < v_end; v0 += 64) {
+      const int v = v0 + l;
+      if (v < v_end) {
+        double acc[TT];
+#pragma unroll
+        for (int t = 0; t < TT; ++t) acc[t] = 0.0;
+        for (int a0 = 0; a0 < D; a0 += 16) {
+          double wa[16];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) wa[q] = wh[(size_t)(a0 + q) * C + v];  // 16 loads in flight
+#pragma unroll
+          for (int q = 0; q < 16; ++q)
+#pragma unroll
+            for (int t = 0; t < TT; ++t) acc[t] = fma(xs[t][a0 + q], wa[q], acc[t]);
+        }
+        const double bv = bh[v];
+#pragma unroll
+        for (int t = 0; t < TT; ++t) {
+          const double sc = fma(-2.0, acc[t], bv);
+          if (sc < best[t]) {
+            best[t] = sc;
+            bidx[t] = v;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < TT; ++t) {
+      double bb = best[t];
+      int bi = bidx[t];
+      for (int o = 32; o > 0; o >>= 1) {
+        const double ob = __shfl_xor(bb, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ob < bb || (ob == bb && oi < bi)) {
+          bb = ob;
+          bi = oi;
+        }
+      }
+      if (l == 0) {
+        rs[wv][t] = bb;
+        ri[wv][t] = bi;
+      }
+    }
+    __syncthreads();
+    if (tid < TT && tok_s[tid] >= 0) {
+      double bb = rs[0][tid];
+      int bi = ri[0][tid];
+      for (int q = 1; q < 4; ++q)
+        if (rs[q][tid] < bb || (rs[q][tid] == bb && ri[q][tid] < bi)) {
+          bb = rs[q][tid];
+          bi = ri[q][tid];
+        }
+      if (!isfinite(bb) || bi >= C) {
+        raise_status(status, ST_NONFINITE);
+        bi = 0;
+      }
+      labels[(size_t)h * N + tok_s[tid]] = bi;
     }
   }
 }
@@ -549,17 +756,18 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
   rg = rg < 2 ? 2 : rg;
   rg = rg > max_tiles ? max_tiles : rg;
   for (int t = 0; t < T_; ++t) {
-    PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3((C + 15) / 16, H), dim3(256), 0, st,
-                (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane,
-                fast ? kb.b32 : nullptr, fast ? kb.wn : nullptr);
+    const int nbm = (C + 15) / 16;
+    PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3(nbm, H), dim3(256), 0, st,
+                (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.wT : nullptr,
+                fast ? kb.w3 : nullptr, plane, fast ? kb.b32 : nullptr, fast ? kb.wn : nullptr,
+                fast ? kb.eb : nullptr, kb.hmax, kb.nflag);
     if constexpr (fast) {
-      PARK_LAUNCH("kmeans_reset", k_reset_counts, dim3((H + 63) / 64), dim3(64), 0, st, kb.nflag,
-                  H);
       PARK_LAUNCH("kmeans_assign_fast", k_assign_fast<D>, dim3((N + 255) / 256, H), dim3(256), 0,
                   st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane, (const float*)kb.b32,
-                  (const float*)kb.wn, N, C, kb.labels, kb.flags, kb.nflag);
-      PARK_LAUNCH("kmeans_refine64", (k_assign64<T, D, 16>), dim3(rg, H), dim3(256), 0, st, X,
-                  (const double*)kb.w, (const double*)kb.b, N, C, (const int*)kb.flags,
+                  (const float*)kb.wn, (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C,
+                  kb.labels, kb.flags, kb.nflag);
+      PARK_LAUNCH("kmeans_refine64", (k_refine<T, D>), dim3(rg, H), dim3(256), 0, st, X,
+                  (const double*)kb.wT, (const double*)kb.b, N, C, (const int*)kb.flags,
                   (const int*)kb.nflag, kb.labels, status);
     } else {
       PARK_LAUNCH("kmeans_assign64", (k_assign64<T, D, 64>), dim3((N + 63) / 64, H), dim3(256), 0, st,

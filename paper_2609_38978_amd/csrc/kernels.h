@@ -36,6 +36,9 @@ struct KmeansBufs {
   bf16_t* w3;     // [3][H][C][D] w as three bf16 parts
   float* b32;     // [H][C]
   float* wn;      // [H][C]    |w_v| (rounded up)
+  float* eb;      // [H][C]    |b_v| term of the fast-path error bound
+  float* hmax;    // [H][ceil(C/16)][2] per-block max |w_v|, max eb_v
+  double* wT;     // [H][D][C] w transposed (float64 refinement)
   int* nflag;     // [H]       tokens left for the float64 refine
   int* flags;     // [H][N]    their indices
 };
