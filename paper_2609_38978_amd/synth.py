@@ -91,20 +91,20 @@ CONFIGS["wan_sweep"] = CONFIGS["wan"].with_(name="wan_sweep")
 
 def bf16_round(a: np.ndarray) -> np.ndarray:
     """float32 -> nearest bfloat16 (ties to even), returned as float32."""
-    a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32)
+    import torch
+
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float32).numpy()
 
 
 def _centre_of_tokens(sites: np.ndarray, grid: tuple) -> np.ndarray:
-    tg, hg, wg = grid
-    t = (np.arange(tg) + 0.5) / tg
-    y = (np.arange(hg) + 0.5) / hg
-    x = (np.arange(wg) + 0.5) / wg
-    pos = np.stack(np.meshgrid(t, y, x, indexing="ij"), axis=-1).reshape(-1, 3)
-    d2 = ((pos[:, None, :] - sites[None, :, :]) ** 2).sum(-1)
-    return np.argmin(d2, axis=1)  # first minimum -> lower id on ties
+    """Index of the nearest site for every grid token (raster order, t-major).
+
+    Squared distances are separable over the three grid axes."""
+    axes = [((np.arange(n) + 0.5) / n)[:, None] - sites[None, :, i] for i, n in enumerate(grid)]
+    dt, dy, dx = (a ** 2 for a in axes)
+    d2 = dt[:, None, None, :] + dy[None, :, None, :] + dx[None, None, :, :]
+    return np.argmin(d2.reshape(-1, sites.shape[0]), axis=1)  # ties -> lower id
 
 
 def make_head(cfg: LayerConfig, h: int):
@@ -131,16 +131,20 @@ def make_head(cfg: LayerConfig, h: int):
     return q, k, v
 
 
-def make_layer(cfg: LayerConfig, heads=None):
+def make_layer(cfg: LayerConfig, heads=None, workers: int = 8):
     """Stacked ``[H', N, d]`` float32 Q, K, V for ``heads`` (default: all)."""
-    heads = range(cfg.H) if heads is None else heads
-    qs, ks, vs = [], [], []
-    for h in heads:
-        q, k, v = make_head(cfg, h)
-        qs.append(q)
-        ks.append(k)
-        vs.append(v)
-    return np.stack(qs), np.stack(ks), np.stack(vs)
+    from concurrent.futures import ThreadPoolExecutor
+
+    heads = list(range(cfg.H) if heads is None else heads)
+    out = [np.empty((len(heads), cfg.N, cfg.d), dtype=np.float32) for _ in range(3)]
+
+    def one(i):
+        for dst, src in zip(out, make_head(cfg, heads[i])):
+            dst[i] = src
+
+    with ThreadPoolExecutor(max_workers=max(1, min(workers, len(heads)))) as ex:
+        list(ex.map(one, range(len(heads))))
+    return tuple(out)
 
 
 def perturb_head(cfg: LayerConfig, h: int, q: np.ndarray, k: np.ndarray, sigma: float = 0.05):
