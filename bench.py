@@ -49,6 +49,9 @@ def kernel_work(name, cfg, st, C):
     if name == "kmeans_assign_fast":
         # algorithmic N*C*d multiply-adds; the hi/lo split issues twice that on MFMA
         return "mfma", 2.0 * N * C * d * H, "flop", "mfma_bf16"
+    if name == "pama_fast":
+        # one q.c product per (query, key block); the centroid split issues it 3x on MFMA
+        return "mfma", 2.0 * N * C * d * H, "flop", "mfma_bf16"
     if name == "pama64":
         return "alu", 2.0 * N * C * d * H, "flop", "alu_f64"
     if name == "gram_partial":

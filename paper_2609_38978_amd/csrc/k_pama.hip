@@ -54,16 +54,15 @@ __device__ int block_exclusive_scan_2048(int* a, int n, int* tmp) {
 
 // ---------------------------------------------------------------- PAMA f64
 template <typename T, int D>
-__global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp, const int* __restrict__ q_offsets,
-                                                const float* __restrict__ cen,
-                                                const int* __restrict__ k_sizes, int N, int CQ, int CK,
-                                                double* __restrict__ W64, float* __restrict__ W32,
-                                                int* status) {
+__device__ void pama64_row(const T* __restrict__ Qp, const int* __restrict__ q_offsets,
+                           const float* __restrict__ cen, const int* __restrict__ k_sizes, int h,
+                           int u, int N, int CQ, int CK, double* __restrict__ W64,
+                           float* __restrict__ W32, int* status) {
   constexpr int QT = 4;                 // queries per step
   constexpr int MV = MAXC / 256;        // key blocks per thread
   __shared__ double qs[QT][D];
   __shared__ double red[4][QT];
-  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int* off = q_offsets + (size_t)h * (CQ + 1);
   const int q0 = min(max(off[u], 0), N), q1 = min(max(off[u + 1], q0), N);
   const int nu = q1 - q0;
@@ -96,6 +95,7 @@ __global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp, const 
       for (int k = 0; k < QT; ++k) S[k][m] = 0.0;
       if (on[m]) {
         const float* cv = ch + (size_t)v * D;
+#pragma unroll 8
         for (int a = 0; a < D; ++a) {
           const double c = (double)cv[a];
 #pragma unroll
@@ -160,24 +160,42 @@ __global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp, const 
       if (W32) W32[wrow + v] = (float)wv;
     }
   }
+  __syncthreads();
+}
+
+// float64 PAMA of every query block, or (rows != null) of the listed ones.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp, const int* __restrict__ q_offsets,
+                                                const float* __restrict__ cen,
+                                                const int* __restrict__ k_sizes, int N, int CQ, int CK,
+                                                const int* __restrict__ rows,
+                                                const int* __restrict__ nrows,
+                                                double* __restrict__ W64, float* __restrict__ W32,
+                                                int* status) {
+  const int h = blockIdx.y;
+  const int cnt = rows ? min(nrows[h], CQ) : blockIdx.x + 1;
+  const int step = rows ? gridDim.x : 1;
+  for (int r = blockIdx.x; r < cnt; r += step) {
+    const int u = rows ? rows[(size_t)h * CQ + r] : r;
+    if ((unsigned)u < (unsigned)CQ)
+      pama64_row<T, D>(Qp, q_offsets, cen, k_sizes, h, u, N, CQ, CK, W64, W32, status);
+  }
 }
 
 // ---------------------------------------------------------------- select
 // One workgroup per (query block, head).  Valid key blocks are sorted by
 // (W^ descending, id ascending) with an LDS bitonic sort; the kept prefix is
 // then marked and compacted into ascending ids.
-__global__ __launch_bounds__(256) void k_select64(const double* __restrict__ W64,
-                                                  const int* __restrict__ q_offsets,
-                                                  const int* __restrict__ k_sizes, int CQ, int CK,
-                                                  int P, int mode, double param, int kcount,
-                                                  int* __restrict__ kv_count,
-                                                  int* __restrict__ kv_index) {
+__device__ void select64_row(const double* __restrict__ W64, const int* __restrict__ q_offsets,
+                             const int* __restrict__ k_sizes, int h, int u, int CQ, int CK, int P,
+                             int mode, double param, int kcount, int* __restrict__ kv_count,
+                             int* __restrict__ kv_index) {
   __shared__ double key[MAXC];
   __shared__ int id[MAXC];
   __shared__ int flag[MAXC];
   __shared__ int tmp[4];
   __shared__ int nvalid_s, m_s;
-  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x;
+  const int tid = threadIdx.x;
   const int* off = q_offsets + (size_t)h * (CQ + 1);
   const int nu = off[u + 1] - off[u];
   const size_t row = (size_t)h * CQ + u;
@@ -249,47 +267,507 @@ __global__ __launch_bounds__(256) void k_select64(const double* __restrict__ W64
   for (int e = tid; e < CK; e += 256)
     if (flag[e]) out[id[e]] = e;
   if (tid == 0) kv_count[row] = m;
+  __syncthreads();
+}
+
+// float64 selection of every query block, or (rows != null) of the listed ones.
+__global__ __launch_bounds__(256) void k_select64(const double* __restrict__ W64,
+                                                  const int* __restrict__ q_offsets,
+                                                  const int* __restrict__ k_sizes, int CQ, int CK,
+                                                  int P, int mode, double param, int kcount,
+                                                  const int* __restrict__ rows,
+                                                  const int* __restrict__ nrows,
+                                                  int* __restrict__ kv_count,
+                                                  int* __restrict__ kv_index) {
+  const int h = blockIdx.y;
+  const int cnt = rows ? min(nrows[h], CQ) : blockIdx.x + 1;
+  const int step = rows ? gridDim.x : 1;
+  for (int r = blockIdx.x; r < cnt; r += step) {
+    const int u = rows ? rows[(size_t)h * CQ + r] : r;
+    if ((unsigned)u < (unsigned)CQ)
+      select64_row(W64, q_offsets, k_sizes, h, u, CQ, CK, P, mode, param, kcount, kv_count,
+                   kv_index);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fast PAMA on bf16 MFMA (bf16 queries), with a per-row error bound.
+//
+// Centroids (float) are split into three bf16 parts, c = c1 + c2 + c3 + r with
+// |r| <= 2^-24 |c|.  t = q.c is accumulated as q.c1 (a fresh accumulator per
+// 32-wide k-step, partials added on the VALU) plus q.(c2 + c3) in one chain;
+// with 2^-23 per MFMA addition and 2^-24 per VALU rounding,
+//   |t^ - t| <= et |q| |c|,  et = 2^-24 1.01 + (32 2^-23 + (KS-1) 2^-24) 1.01
+//                                + 2^-8 1.01 (2D) 2^-23 + 2^-24 1.01.
+// The logit S = t/sqrt(d) + log n is formed with one FMA; its error
+//   e_i = isd (et + 1.01 2^-24) |q_i| cmax + 1.01 2^-24 (2 lgmax + 1.01 isd |q_i| cmax)
+// bounds every centroid of query i (cmax = max |c_v|, lgmax = max log n_v).
+// Pass 1 keeps, per lane and query, an online (max, sum of exp2); lanes are
+// merged at the end.  Pass 2 recomputes the logits and accumulates
+// P = exp2((S - m) log2 e) / Z over the queries into per-wavefront LDS
+// columns, which are added in wavefront order (deterministic).
+// Relative error of each W^_uv:
+//   delta_u = max_i (2.02 e_i + dZ_i + 2^-23 (3 + 1.5 argmax_i)) + 17 2^-24
+// where argmax_i = 2 (isd |q_i| cmax + lgmax) log2 e bounds the exp2
+// arguments (an argument x carries a relative exp2 error <= 2^-23 (2 + 1.5|x|))
+// and dZ_i bounds the float normaliser (see the kernel); values below float's
+// normal range carry an extra absolute error, handled by the selection.  Rows whose selection this bound cannot certify are recomputed
+// in float64.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Splits the centroids into three bf16 planes and records log n_v (-inf for
+// empty blocks), |c_v| rounded up, and per-block maxima of |c_v| and |log n_v|.
+template <int D>
+__global__ __launch_bounds__(256) void k_cen_prep(const float* __restrict__ cen,
+                                                  const int* __restrict__ k_sizes, int CK,
+                                                  bf16_t* __restrict__ c3, size_t plane,
+                                                  float* __restrict__ lg, float* __restrict__ cn,
+                                                  float* __restrict__ bmax) {
+  constexpr int CB = 16, TPC = 256 / CB, EPT = D / TPC;
+  __shared__ float part[CB][TPC];
+  const int h = blockIdx.y, v0 = blockIdx.x * CB, tid = threadIdx.x;
+  const int r = tid / TPC, j = tid % TPC, v = v0 + r;
+  float ss = 0.0f;
+  if (v < CK) {
+    const size_t o = ((size_t)h * CK + v) * D + j * EPT;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const float x = cen[o + e];
+      const bf16_t p1 = f2bf(x);
+      const float r1 = x - bf2f(p1);
+      const bf16_t p2 = f2bf(r1);
+      const float r2 = r1 - bf2f(p2);
+      c3[o + e] = p1;
+      c3[o + e + plane] = p2;
+      c3[o + e + 2 * plane] = f2bf(r2);
+      ss = fmaf(x, x, ss);
+    }
+  }
+  part[r][j] = ss;
+  __syncthreads();
+  float fn = 0.0f, fl = 0.0f;
+  if (tid < CB) {
+    const int vv = v0 + tid;
+    if (vv < CK) {
+      float s2 = 0.0f;
+      for (int q = 0; q < TPC; ++q) s2 += part[tid][q];
+      fn = sqrtf(s2) * 1.0001f;
+      const int n = k_sizes[(size_t)h * CK + vv];
+      const float l = n > 0 ? (float)log((double)n) : -INFINITY;
+      cn[(size_t)h * CK + vv] = fn;
+      lg[(size_t)h * CK + vv] = l;
+      fl = n > 0 ? fabsf(l) : 0.0f;
+    }
+  }
+  if (tid < 64) {
+    for (int o = 8; o > 0; o >>= 1) {
+      fn = fmaxf(fn, __shfl_xor(fn, o, 64));
+      fl = fmaxf(fl, __shfl_xor(fl, o, 64));
+    }
+    if (tid == 0) {
+      bmax[((size_t)h * gridDim.x + blockIdx.x) * 2] = fn;
+      bmax[((size_t)h * gridDim.x + blockIdx.x) * 2 + 1] = fl;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void k_pama_fast(const bf16_t* __restrict__ Qp,
+                                                   const int* __restrict__ q_offsets,
+                                                   const bf16_t* __restrict__ c3, size_t plane,
+                                                   const float* __restrict__ lg,
+                                                   const float* __restrict__ bmax, int nbm, int N,
+                                                   int CQ, int CK, float* __restrict__ W32,
+                                                   float* __restrict__ delta) {
+  constexpr int CT = 64, KS = D / 32, CROW = D + 8, CH = D / 8;
+  constexpr int NL = CT * CH / 256;
+  constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f, L2E = 1.4426950408889634f;
+  constexpr float ET = U24 * 1.01f + (32.0f * DEL + (KS - 1) * U24) * 1.01f +
+                       0.00390625f * 1.01f * (2 * D) * DEL + U24 * 1.01f;
+  __shared__ __attribute__((aligned(16))) bf16_t C1[CT * CROW];
+  __shared__ __attribute__((aligned(16))) bf16_t C2[CT * CROW];
+  __shared__ __attribute__((aligned(16))) bf16_t C3[CT * CROW];
+  __shared__ float lgs[CT];
+  __shared__ float wacc[4][MAXC];
+  __shared__ float qn_s[4][16];
+  __shared__ float red[4];
+  __shared__ float mx_s[2];
+  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x, w = tid >> 6, l = tid & 63,
+            g = l >> 4, c16 = l & 15;
+  const int* off = q_offsets + (size_t)h * (CQ + 1);
+  const int q0 = min(max(off[u], 0), N), q1 = min(max(off[u + 1], q0), N);
+  const int nu = q1 - q0;
+  const size_t wrow = ((size_t)h * CQ + u) * CK;
+  if (nu <= 0) {
+    for (int v = tid; v < CK; v += 256) W32[wrow + v] = 0.0f;
+    if (tid == 0) delta[(size_t)h * CQ + u] = 0.0f;
+    return;
+  }
+  if (tid < 64) {
+    float a = 0.0f, c = 0.0f;
+    for (int i = tid; i < nbm; i += 64) {
+      a = fmaxf(a, bmax[((size_t)h * nbm + i) * 2]);
+      c = fmaxf(c, bmax[((size_t)h * nbm + i) * 2 + 1]);
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      a = fmaxf(a, __shfl_xor(a, o, 64));
+      c = fmaxf(c, __shfl_xor(c, o, 64));
+    }
+    if (tid == 0) {
+      mx_s[0] = a;
+      mx_s[1] = c;
+    }
+  }
+  for (int v = tid; v < 4 * MAXC; v += 256) (&wacc[0][0])[v] = 0.0f;
+  __syncthreads();
+  const float cmax = mx_s[0], lgmax = mx_s[1];
+  const float isd = 1.0f / sqrtf((float)D);
+  const bf16_t* P1 = c3 + (size_t)h * CK * D;
+  const bf16_t* P2 = P1 + plane;
+  const bf16_t* P3 = P2 + plane;
+  const float* lgh = lg + (size_t)h * CK;
+  const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  float dmax = 0.0f;  // per-thread max of the row error bound
+
+  for (int r0 = q0; r0 < q1; r0 += 64) {
+    // A operand: this wavefront's 16 queries (query c16, dims 32s + 8g ..)
+    const int qa = r0 + 16 * w + c16;
+    bf16x8_t qf[KS];
+    float qsq = 0.0f;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+      if (qa < q1) raw = *(const uint4*)(Qp + ((size_t)h * N + qa) * D + 32 * s + 8 * g);
+      qf[s] = __builtin_bit_cast(bf16x8_t, raw);
+      const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
+        qsq = fmaf(lo, lo, fmaf(hi, hi, qsq));
+      }
+    }
+    qsq += __shfl_xor(qsq, 16, 64);
+    qsq += __shfl_xor(qsq, 32, 64);
+    if (g == 0) qn_s[w][c16] = sqrtf(qsq) * 1.0001f;
+    // outputs: lane holds queries 4g + r (r = 0..3) of this wavefront
+    bool rv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) rv[r] = r0 + 16 * w + 4 * g + r < q1;
+    float m[4], z[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      m[r] = -INFINITY;
+      z[r] = 0.0f;
+    }
+    for (int pass = 0; pass < 2; ++pass) {
+      float mf[4], iz[4];
+      if (pass == 1) {
+        // merge (max, sum) over the 16 lanes holding the same queries
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float mm = m[r], zz = z[r];
+#pragma unroll
+          for (int o = 1; o < 16; o <<= 1) {
+            const float om = __shfl_xor(mm, o, 64), oz = __shfl_xor(zz, o, 64);
+            const float nm = fmaxf(mm, om);
+            zz = (nm == -INFINITY) ? 0.0f
+                                   : zz * __builtin_amdgcn_exp2f((mm - nm) * L2E) +
+                                         oz * __builtin_amdgcn_exp2f((om - nm) * L2E);
+            mm = nm;
+          }
+          mf[r] = mm;
+          iz[r] = zz > 0.0f ? 1.0f / zz : 0.0f;
+        }
+      }
+      for (int c0 = 0; c0 < CK; c0 += CT) {
+        __syncthreads();
+        for (int e = tid; e < CT * CH; e += 256) {
+          const int rr = e / CH, ch = e % CH;
+          uint4 v1 = make_uint4(0u, 0u, 0u, 0u), v2 = v1, v3 = v1;
+          if (c0 + rr < CK) {
+            const size_t o = (size_t)(c0 + rr) * D + 8 * ch;
+            v1 = *(const uint4*)(P1 + o);
+            v2 = *(const uint4*)(P2 + o);
+            v3 = *(const uint4*)(P3 + o);
+          }
+          *(uint4*)(C1 + rr * CROW + 8 * ch) = v1;
+          *(uint4*)(C2 + rr * CROW + 8 * ch) = v2;
+          *(uint4*)(C3 + rr * CROW + 8 * ch) = v3;
+        }
+        if (tid < CT) lgs[tid] = (c0 + tid < CK) ? lgh[c0 + tid] : -INFINITY;
+        __syncthreads();
+#pragma unroll
+        for (int cb = 0; cb < CT / 16; ++cb) {
+          f32x4_t shi = zero, srest = zero;
+          const int rowo = (16 * cb + c16) * CROW + 8 * g;
+#pragma unroll
+          for (int s = 0; s < KS; ++s) {
+            const bf16x8_t b1 = *(const bf16x8_t*)(C1 + rowo + 32 * s);
+            const bf16x8_t b2 = *(const bf16x8_t*)(C2 + rowo + 32 * s);
+            const bf16x8_t b3 = *(const bf16x8_t*)(C3 + rowo + 32 * s);
+            shi += __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b1, zero, 0, 0, 0);
+            srest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b2, srest, 0, 0, 0);
+            srest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b3, srest, 0, 0, 0);
+          }
+          const float lgv = lgs[16 * cb + c16];  // this lane's centroid
+          if (pass == 0) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float sv = fmaf(shi[r] + srest[r], isd, lgv);
+              if (sv != -INFINITY) {
+                const float nm = fmaxf(m[r], sv);
+                z[r] = z[r] * __builtin_amdgcn_exp2f((m[r] - nm) * L2E) +
+                       __builtin_amdgcn_exp2f((sv - nm) * L2E);
+                m[r] = nm;
+              }
+            }
+          } else {
+            float cs = 0.0f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float sv = fmaf(shi[r] + srest[r], isd, lgv);
+              const float p = (rv[r] && sv != -INFINITY)
+                                  ? __builtin_amdgcn_exp2f((sv - mf[r]) * L2E) * iz[r]
+                                  : 0.0f;
+              cs += p;
+            }
+            cs += __shfl_xor(cs, 16, 64);
+            cs += __shfl_xor(cs, 32, 64);
+            const int v = c0 + 16 * cb + c16;
+            if (g == 0 && v < CK) wacc[w][v] += cs;
+          }
+        }
+      }
+    }
+    // row error bound for this wavefront's queries (lane holds query c16's norm)
+    {
+      const float qn = (16 * w + c16 + r0 < q1) ? qn_s[w][c16] : 0.0f;
+      const float ei = isd * (ET + 1.01f * U24) * qn * cmax +
+                       1.01f * U24 * (2.0f * lgmax + 1.01f * isd * qn * cmax);
+      const float argmax = 2.0f * (isd * qn * cmax + lgmax) * L2E;
+      // normaliser: element exp2 errors weighted by p (sum_j p_j |x_j| <= 2 log2 CK),
+      // the online rescales (their arguments add up to at most argmax), the
+      // lane merges, and the float additions
+      const float dZ = DEL * (10.0f + 3.0f * log2f((float)CK + 1.0f) + 2.0f * (CK / 16 + 1) +
+                              3.0f * argmax) +
+                       2.0f * U24 * (CK / 16 + 24);
+      dmax = fmaxf(dmax, 2.02f * ei + dZ + DEL * (3.0f + 1.5f * argmax));
+    }
+  }
+  __syncthreads();
+  const float inv_n = 1.0f / (float)nu;
+  for (int v = tid; v < CK; v += 256)
+    W32[wrow + v] = (((wacc[0][v] + wacc[1][v]) + wacc[2][v]) + wacc[3][v]) * inv_n;
+  for (int o = 32; o > 0; o >>= 1) dmax = fmaxf(dmax, __shfl_xor(dmax, o, 64));
+  if (l == 0) red[w] = dmax;
+  __syncthreads();
+  if (tid == 0)
+    delta[(size_t)h * CQ + u] =
+        (fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])) + 17.0f * U24) * 1.01f;
+}
+
+// Certified selection on the float W^: sort (W^ descending, id ascending),
+// take the cut, and accept the row only if the cut is robust to the row's
+// relative error delta_u plus an absolute error for values below float's
+// normal range: the last kept block's lower bound must exceed the first
+// dropped block's upper bound and, for top-p, the kept set's bounds must
+// still straddle p.  Accepted rows are written; the others are listed for
+// the float64 path.
+__global__ __launch_bounds__(256) void k_select_fast(const float* __restrict__ W32,
+                                                     const float* __restrict__ delta,
+                                                     const int* __restrict__ q_offsets,
+                                                     const int* __restrict__ k_sizes, int CQ,
+                                                     int CK, int P, int mode, double param,
+                                                     int kcount, int* __restrict__ kv_count,
+                                                     int* __restrict__ kv_index,
+                                                     int* __restrict__ rows,
+                                                     int* __restrict__ nrows) {
+  __shared__ float key[MAXC];
+  __shared__ int id[MAXC];
+  __shared__ int flag[MAXC];
+  __shared__ int tmp[4];
+  __shared__ int nvalid_s, m_s, ok_s;
+  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x;
+  const int* off = q_offsets + (size_t)h * (CQ + 1);
+  const int nu = off[u + 1] - off[u];
+  const size_t row = (size_t)h * CQ + u;
+  if (nu <= 0) {
+    if (tid == 0) kv_count[row] = 0;
+    return;
+  }
+  if (tid == 0) nvalid_s = 0;
+  __syncthreads();
+  int myvalid = 0;
+  for (int e = tid; e < P; e += 256) {
+    const bool ok = e < CK && k_sizes[(size_t)h * CK + e] > 0;
+    key[e] = ok ? W32[row * CK + e] : -1.0f;
+    id[e] = e;
+    if (e < CK) flag[e] = 0;
+    myvalid += ok;
+  }
+  atomicAdd(&nvalid_s, myvalid);
+  __syncthreads();
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int t = tid; t < P / 2; t += 256) {
+        const int i = 2 * t - (t & (j - 1));
+        const int l2 = i + j;
+        const bool up = (i & k) == 0;
+        const float ka = key[i], kb = key[l2];
+        const int ia = id[i], ib = id[l2];
+        const bool a_first = (ka > kb) || (ka == kb && ia < ib);
+        if (a_first != up) {
+          key[i] = kb;
+          key[l2] = ka;
+          id[i] = ib;
+          id[l2] = ia;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const int nvalid = nvalid_s;
+  if (tid == 0) {
+    const double dl = (double)delta[row];
+    const double eps = 4.0 * 1.1754943508222875e-38;  // absolute error near underflow
+    int m;
+    bool ok = true;
+    if (mode == PARK_SELECT_TOPK) {
+      m = kcount < 1 ? 1 : kcount;
+      if (m > nvalid) m = nvalid;
+    } else {
+      double cs = 0.0;
+      m = nvalid;
+      for (int r = 0; r < nvalid; ++r) {
+        cs += (double)key[r];
+        if (cs >= param) {
+          m = r + 1;
+          break;
+        }
+      }
+      // the kept set must reach p and the set without its smallest member not
+      double slo = 0.0, shi = 0.0, minlo = 1e300;
+      for (int r = 0; r < m; ++r) {
+        const double x = (double)key[r];
+        const double lo = x * (1.0 - dl) - eps;
+        slo += lo;
+        shi += x * (1.0 + dl) + eps;
+        minlo = fmin(minlo, lo);
+      }
+      if (m < nvalid) ok = ok && slo >= param * (1.0 + 1e-12);
+      ok = ok && (shi - minlo < param * (1.0 - 1e-12));
+    }
+    if (m < 1 && nvalid > 0) m = 1;
+    if (m < nvalid) {
+      const double a = (double)key[m - 1] * (1.0 - dl) - eps;
+      const double b = (double)key[m] * (1.0 + dl) + eps;
+      ok = ok && (a > b);
+    }
+    m_s = m;
+    ok_s = ok;
+    if (!ok) rows[(size_t)h * CQ + atomicAdd(nrows + h, 1)] = u;
+  }
+  __syncthreads();
+  if (!ok_s) return;
+  const int m = m_s;
+  for (int r = tid; r < m; r += 256) flag[id[r]] = 1;
+  __syncthreads();
+  for (int e = tid; e < CK; e += 256) id[e] = flag[e];
+  __syncthreads();
+  block_exclusive_scan_2048(id, CK, tmp);
+  int* out = kv_index + row * CK;
+  for (int e = tid; e < CK; e += 256)
+    if (flag[e]) out[id[e]] = e;
+  if (tid == 0) kv_count[row] = m;
+}
+
+__global__ void k_zero_counts(int* __restrict__ c, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) c[i] = 0;
 }
 
 // ---------------------------------------------------------------- launchers
-park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
-                          const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
-                          double* W64, float* W32, int* status, hipStream_t st) {
-  dim3 g(CQ, H);
-  if (D == 128) {
-    if (dtype == PARK_BF16)
-      PARK_LAUNCH("pama64", (k_pama64<bf16_t, 128>), g, dim3(256), 0, st, (const bf16_t*)Qp,
-                  q_offsets, cen, k_sizes, N, CQ, CK, W64, W32, status);
-    else
-      PARK_LAUNCH("pama64", (k_pama64<float, 128>), g, dim3(256), 0, st, (const float*)Qp,
-                  q_offsets, cen, k_sizes, N, CQ, CK, W64, W32, status);
-  } else {
-    if (dtype == PARK_BF16)
-      PARK_LAUNCH("pama64", (k_pama64<bf16_t, 64>), g, dim3(256), 0, st, (const bf16_t*)Qp,
-                  q_offsets, cen, k_sizes, N, CQ, CK, W64, W32, status);
-    else
-      PARK_LAUNCH("pama64", (k_pama64<float, 64>), g, dim3(256), 0, st, (const float*)Qp,
-                  q_offsets, cen, k_sizes, N, CQ, CK, W64, W32, status);
+static int topk_count(int CK, double param) {
+  // ceil(rho * N_K) blocks, clamped on the device to [1, #nonempty]
+  const double x = param * (double)CK - 1e-9;
+  int k = (int)x;
+  if ((double)k < x) ++k;
+  return k < 1 ? 1 : k;
+}
+
+static int pow2_at_least(int n) {
+  int P = 2;
+  while (P < n) P <<= 1;
+  return P;
+}
+
+park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* cen,
+                            const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
+                            int mode, double param, const RetrieveBufs& rb, float* W_out,
+                            int* kv_count, int* kv_index, int* status, hipStream_t st) {
+  const int P = pow2_at_least(CK);
+  const int kcount = mode == PARK_SELECT_TOPK ? topk_count(CK, param) : 0;
+  if (dtype != PARK_BF16) {  // float32 queries: float64 PAMA and selection of every row
+    PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, nullptr, nullptr,
+                           rb.W64, W_out, status, st));
+    PARK_LAUNCH("select", k_select64, dim3(CQ, H), dim3(256), 0, st, (const double*)rb.W64,
+                q_offsets, k_sizes, CQ, CK, P, mode, param, kcount, (const int*)nullptr,
+                (const int*)nullptr, kv_count, kv_index);
+    return PARK_OK;
   }
+  const size_t plane = (size_t)H * CK * D;
+  const int nbm = (CK + 15) / 16;
+  float* W32 = W_out ? W_out : rb.W32;
+  if (D == 128) {
+    PARK_LAUNCH("pama_cen_prep", k_cen_prep<128>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
+                rb.c3, plane, rb.lg, rb.cn, rb.bmax);
+    PARK_LAUNCH("pama_fast", k_pama_fast<128>, dim3(CQ, H), dim3(256), 0, st, (const bf16_t*)Qp,
+                q_offsets, (const bf16_t*)rb.c3, plane, (const float*)rb.lg,
+                (const float*)rb.bmax, nbm, N, CQ, CK, W32, rb.delta);
+  } else {
+    PARK_LAUNCH("pama_cen_prep", k_cen_prep<64>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
+                rb.c3, plane, rb.lg, rb.cn, rb.bmax);
+    PARK_LAUNCH("pama_fast", k_pama_fast<64>, dim3(CQ, H), dim3(256), 0, st, (const bf16_t*)Qp,
+                q_offsets, (const bf16_t*)rb.c3, plane, (const float*)rb.lg,
+                (const float*)rb.bmax, nbm, N, CQ, CK, W32, rb.delta);
+  }
+  PARK_LAUNCH("pama_reset", k_zero_counts, dim3((H + 63) / 64), dim3(64), 0, st, rb.nrows, H);
+  PARK_LAUNCH("select_fast", k_select_fast, dim3(CQ, H), dim3(256), 0, st, (const float*)W32,
+              (const float*)rb.delta, q_offsets, k_sizes, CQ, CK, P, mode, param, kcount,
+              kv_count, kv_index, rb.rows, rb.nrows);
+  // rows the float bound could not certify: float64 PAMA and selection
+  int rg = (1024 + H - 1) / H;
+  rg = rg < 1 ? 1 : (rg > CQ ? CQ : rg);
+  PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, rb.rows, rb.nrows,
+                         rb.W64, W32, status, st, rg));
+  PARK_LAUNCH("select_refine", k_select64, dim3(rg, H), dim3(256), 0, st, (const double*)rb.W64,
+              q_offsets, k_sizes, CQ, CK, P, mode, param, kcount, (const int*)rb.rows,
+              (const int*)rb.nrows, kv_count, kv_index);
   return PARK_OK;
 }
 
-park_status launch_select(const double* W64, const int* q_offsets, const int* k_sizes, int H,
-                          int CQ, int CK, int mode, double param, int* kv_count, int* kv_index,
-                          hipStream_t st) {
-  int P = 1;
-  while (P < CK) P <<= 1;
-  if (P < 2) P = 2;
-  int kcount = 0;
-  if (mode == PARK_SELECT_TOPK) {
-    // ceil(rho * N_K) blocks, clamped on the device to [1, #nonempty]
-    double x = param * (double)CK - 1e-9;
-    kcount = (int)x;
-    if ((double)kcount < x) ++kcount;
-    if (kcount < 1) kcount = 1;
+park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
+                          const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
+                          const int* rows, const int* nrows, double* W64, float* W32, int* status,
+                          hipStream_t st, int grid_x) {
+  dim3 g(rows ? grid_x : CQ, H);
+  const char* nm = rows ? "pama_refine64" : "pama64";
+  if (D == 128) {
+    if (dtype == PARK_BF16)
+      PARK_LAUNCH(nm, (k_pama64<bf16_t, 128>), g, dim3(256), 0, st, (const bf16_t*)Qp, q_offsets,
+                  cen, k_sizes, N, CQ, CK, rows, nrows, W64, W32, status);
+    else
+      PARK_LAUNCH(nm, (k_pama64<float, 128>), g, dim3(256), 0, st, (const float*)Qp, q_offsets,
+                  cen, k_sizes, N, CQ, CK, rows, nrows, W64, W32, status);
+  } else {
+    if (dtype == PARK_BF16)
+      PARK_LAUNCH(nm, (k_pama64<bf16_t, 64>), g, dim3(256), 0, st, (const bf16_t*)Qp, q_offsets,
+                  cen, k_sizes, N, CQ, CK, rows, nrows, W64, W32, status);
+    else
+      PARK_LAUNCH(nm, (k_pama64<float, 64>), g, dim3(256), 0, st, (const float*)Qp, q_offsets,
+                  cen, k_sizes, N, CQ, CK, rows, nrows, W64, W32, status);
   }
-  PARK_LAUNCH("select", k_select64, dim3(CQ, H), dim3(256), 0, st, W64, q_offsets, k_sizes, CQ,
-              CK, P, mode, param, kcount, kv_count, kv_index);
   return PARK_OK;
 }
 

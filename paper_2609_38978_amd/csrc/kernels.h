@@ -50,12 +50,25 @@ park_status launch_segment_mean(const void* X, const int* perm, const int* offse
                                 hipStream_t st);
 
 // k_pama.hip ----------------------------------------------------------------
+struct RetrieveBufs {
+  double* W64;    // [H][CQ][CK] float64 W^ (rows recomputed in float64)
+  float* W32;     // [H][CQ][CK] float W^ when the caller gives no W_out
+  float* delta;   // [H][CQ]     relative error bound of each fast row
+  int* rows;      // [H][CQ]     rows left for the float64 path
+  int* nrows;     // [H]
+  bf16_t* c3;     // [3][H][CK][D] centroids as three bf16 parts
+  float* lg;      // [H][CK]     log n_v (-inf for empty blocks)
+  float* cn;      // [H][CK]     |c_v|
+  float* bmax;    // [H][ceil(CK/16)][2] per-block max |c_v|, |log n_v|
+};
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
-                          double* W64, float* W32, int* status, hipStream_t st);
-park_status launch_select(const double* W64, const int* q_offsets, const int* k_sizes, int H,
-                          int CQ, int CK, int mode, double param, int* kv_count, int* kv_index,
-                          hipStream_t st);
+                          const int* rows, const int* nrows, double* W64, float* W32, int* status,
+                          hipStream_t st, int grid_x = 0);
+park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* cen,
+                            const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
+                            int mode, double param, const RetrieveBufs& rb, float* W_out,
+                            int* kv_count, int* kv_index, int* status, hipStream_t st);
 
 // k_attn.hip ----------------------------------------------------------------
 park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,

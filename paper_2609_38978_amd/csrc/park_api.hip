@@ -163,13 +163,17 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   return c;
 }
 
-struct RetrieveWs {
-  double* W64;
-};
-
-static RetrieveWs carve_retrieve(Carver& cv, int H, int CQ, int CK) {
-  RetrieveWs r;
+static RetrieveBufs carve_retrieve(Carver& cv, int H, int D, int CQ, int CK) {
+  RetrieveBufs r;
   r.W64 = cv.take<double>((size_t)H * CQ * CK);
+  r.W32 = cv.take<float>((size_t)H * CQ * CK);
+  r.delta = cv.take<float>((size_t)H * CQ);
+  r.rows = cv.take<int>((size_t)H * CQ);
+  r.nrows = cv.take<int>((size_t)H);
+  r.c3 = cv.take<bf16_t>((size_t)3 * H * CK * D);
+  r.lg = cv.take<float>((size_t)H * CK);
+  r.cn = cv.take<float>((size_t)H * CK);
+  r.bmax = cv.take<float>((size_t)2 * H * ((CK + 15) / 16));
   return r;
 }
 
@@ -183,7 +187,7 @@ static size_t ws_bytes_for(int H, int N, int D, int CQ, int CK) {
   carve_cluster(c1, H, N, D, std::max(CQ, CK));
   Carver c2(nullptr);
   c2.off = base;
-  carve_retrieve(c2, H, CQ, CK);
+  carve_retrieve(c2, H, D, CQ, CK);
   return std::max(c1.off, c2.off) + 256;
 }
 
@@ -239,11 +243,9 @@ static park_status retrieve_body(const void* Qp, const int* q_offsets, const flo
                                  int* kv_index, void* ws, hipStream_t st) {
   Carver cv(ws);
   int* status = cv.take<int>(64);
-  RetrieveWs rw = carve_retrieve(cv, dm.H, CQ, CK);
-  PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, dm.H, dm.N, dm.d, dm.dtype, CQ, CK, rw.W64,
-                         W_out, status, st));
-  return launch_select(rw.W64, q_offsets, k_sizes, dm.H, CQ, CK, mode, param, kv_count, kv_index,
-                       st);
+  RetrieveBufs rb = carve_retrieve(cv, dm.H, dm.d, CQ, CK);
+  return launch_retrieve(Qp, q_offsets, cen, k_sizes, dm.H, dm.N, dm.d, dm.dtype, CQ, CK, mode,
+                         param, rb, W_out, kv_count, kv_index, status, st);
 }
 
 }  // namespace park

@@ -59,8 +59,9 @@ def test_forward_matches_oracle(tag, out_dtype):
         err = np.abs(Og[i] - Oref)
         print(f"[{tag} h={h}] attention max-abs err {err.max():.3g}")
         assert np.all(err <= tol)
-        W = st["W"][i].cpu().numpy().astype(np.float64)
-        assert np.all(np.abs(W - ref["W"]) <= 2.0 ** -23 * ref["W"] + 1e-40)
+        ok, werr = PT.w_error_ok(cfg.dtype, st["W"][i].cpu().numpy(), ref["W"])
+        print(f"[{tag} h={h}] W max-abs err {werr:.3g}")
+        assert ok
 
 
 def test_reuse_modes():
