@@ -37,7 +37,66 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=4,
                     help="heads of the layer the oracle runs for the CPU baseline")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain elementwise copy of MIB MiB (float32 negation, "
+                         "read once, written once) five times: the known-size kernel that "
+                         "scales the FETCH_SIZE / WRITE_SIZE counters to bytes")
     return ap.parse_args()
+
+
+CSRC = os.path.join(ROOT, "paper_2609_38978_amd", "csrc")
+
+
+def kernel_source_digest(stage):
+    """sha256 (16 hex) of the source file that launches `stage`, plus common.h."""
+    import hashlib
+    tag = f'"{stage}"'
+    h = hashlib.sha256()
+    found = False
+    for fn in sorted(os.listdir(CSRC)):
+        if fn.endswith(".hip"):
+            txt = open(os.path.join(CSRC, fn), "rb").read()
+            if tag.encode() in txt:
+                h.update(txt)
+                found = True
+    if not found:
+        return None
+    h.update(open(os.path.join(CSRC, "common.h"), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, stage):
+    """HBM bytes per launch of `stage` from the committed counter summary.
+
+    The summary holds FETCH_SIZE and WRITE_SIZE (KiB per dispatch, averaged
+    over the dispatches of the stage) scaled by what the same counters read for
+    a plain copy of known size.  None when there is no summary for the stage or
+    its source has changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) >= 6 and cells[0] == stage:
+            if cells[2] != kernel_source_digest(stage):
+                return None
+            try:
+                return float(cells[5])
+            except ValueError:
+                return None
+    return None
+
+
+def calibrate_copy(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_kernel": "torch.neg float32", "bytes_read": 4 * n,
+                      "bytes_written": 4 * n, "launches": 5}), flush=True)
 
 
 def kernel_work(name, cfg, st, C):
@@ -105,6 +164,9 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); PARK shards by "
               f"head with no communication, see the design notes", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     import numpy as np
     import torch
 
@@ -162,6 +224,8 @@ def main():
             ach = amount / (avg_ms * 1e-3) / 1e9
             roof = {"bound": bound, "achieved": round(ach, 2), "peak": PEAK[pk], "unit": "GB/s",
                     "frac": round(ach / PEAK[pk], 4), "traffic": None}
+        tb = measured_traffic(cfg.name, dom)
+        roof["traffic"] = None if tb is None else round(tb)
         roof["kernel"] = dom
         roof["avg_launch_ms"] = round(avg_ms, 4)
 
