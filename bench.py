@@ -48,7 +48,7 @@ CSRC = os.path.join(ROOT, "paper_2609_38978_amd", "csrc")
 
 
 def kernel_source_digest(stage):
-    """sha256 (16 hex) of the source file that launches `stage`, plus common.h."""
+    """sha256 (16 hex) of the source file that launches `stage`, common.h and the build flags."""
     import hashlib
     tag = f'"{stage}"'
     h = hashlib.sha256()
@@ -62,6 +62,7 @@ def kernel_source_digest(stage):
     if not found:
         return None
     h.update(open(os.path.join(CSRC, "common.h"), "rb").read())
+    h.update(open(os.path.join(ROOT, "paper_2609_38978_amd", "build.py"), "rb").read())
     return h.hexdigest()[:16]
 
 

@@ -188,12 +188,16 @@ park_status park_retrieve_blocks(const void* Qp, const int32_t* q_offsets, const
  *   the selected key blocks of u (softmax renormalised over those keys).
  *   Qp, Kp, Vp [H][N][d] dtype;  O [H][N][d] out_dtype (PARK_F32 or PARK_BF16,
  *   bf16 by round-to-nearest-even).  Rows of empty query blocks do not exist;
- *   every token is written exactly once. */
+ *   every token is written exactly once.
+ *   ws: device workspace of at least park_workspace_size() bytes for these
+ *   dims, CQ and CK (it holds the per-call work plan); PARK_ERR_WORKSPACE if
+ *   smaller than the attention part of it. */
 park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* Vp,
                                    const int32_t* q_offsets, const int32_t* k_offsets,
                                    const int32_t* kv_count, const int32_t* kv_index,
                                    const int32_t* q_perm, const park_dims* dims, int32_t CQ,
-                                   int32_t CK, void* O, int32_t out_dtype, void* stream);
+                                   int32_t CK, void* O, int32_t out_dtype, void* ws,
+                                   size_t ws_bytes, void* stream);
 
 /* The whole layer: stages 1-4 on Q, K, V [H][N][d] (dtype), output O
  * [H][N][d] (params->out_dtype) in the original token order.  `state` holds

@@ -184,22 +184,36 @@ __global__ __launch_bounds__(256) void k_attn_valu(const T* __restrict__ Qp, con
 }
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA kernel (v_mfma_f32_16x16x32_bf16).  Workgroup = (query block, head),
-// 4 wavefronts of 16 query rows each; 64-key tiles of the key stream are staged
-// in LDS (K row-major, V transposed).  Per tile and wavefront:
+// bf16 MFMA kernel (v_mfma_f32_16x16x32_bf16).
+//
+// Work: each query block is cut into chunks of at most 64 rows (a plan built
+// on the device), one workgroup per chunk, so large blocks spread over many
+// compute units.  The chunks of one head run on one XCD (workgroups are
+// dealt to the 8 XCDs round-robin, so the linear id is remapped): that XCD's
+// L2 then holds the head's keys and values for all its query blocks.
+//
+// Per chunk, 4 wavefronts of 16 query rows walk the key stream (the selected
+// blocks' rows, concatenated) in KT-key tiles.  K and V tiles go straight
+// from HBM into an LDS ring with wave-wide LDS-DMA loads
+// (global_load_lds_dwordx4), row-major with an XOR swizzle of the 16-byte
+// chunks chosen so the reads below are free of bank conflicts; the next
+// tiles are in flight while tile t is computed.  Per tile and wavefront:
 //   S^T = K Q^T  (16 keys x 16 queries per MFMA): lane l holds keys
-//                16b + 4(l/16) + r of query l%16, so the online softmax of a
-//                query reduces over 16 registers and two lane groups only;
+//                16b + 4(l/16) + r of query l%16;
 //   O^T += V^T P^T: the probabilities are reused from registers as the B
 //                operand (k-slot 8g+r <-> key 32c+4g+r, 8g+4+r <-> 32c+16+4g+r)
-//                and V^T supplies the matching keys from LDS.
-// Softmax in base 2: the running maximum is taken on raw scores and each
-// probability costs one FMA and one v_exp_f32; probabilities are rounded to
-// bf16 (RNE) by the packed hardware conversion.
+//                and the A operand (V^T) is read from the row-major V tile
+//                with the LDS transpose read ds_read_b64_tr_b16: within each
+//                16-lane group, lane j receives element j%4 of the 8 bytes
+//                addressed by lanes 4r + j/4, r = 0..3.
+// Softmax in base 2 on raw scores; each probability costs one FMA and one
+// v_exp_f32 and is rounded to bf16 (RNE) by the packed conversion.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 
 template <typename OT>
 __device__ __forceinline__ void store_out4(OT* p, float a, float b, float c, float d);
@@ -214,164 +228,315 @@ __device__ __forceinline__ void store_out4<bf16_t>(bf16_t* p, float a, float b, 
   *(uint2*)p = make_uint2(lo, hi);
 }
 
-// Loads one 64-key tile of K' and V' (rows krow[buf][0..63], -1 = padding)
-// into registers: NKL 16-byte chunks of K and NVL key pairs of V per thread.
-template <int D, int KT, int NKL, int NVL>
-__device__ __forceinline__ void stage_kv(uint4 (&kreg)[NKL], uint4 (&va)[NVL], uint4 (&vb)[NVL],
-                                         const int (&krow)[2][KT], int buf,
-                                         const bf16_t* __restrict__ Kh,
-                                         const bf16_t* __restrict__ Vh, int N, int tid) {
-  constexpr int CH = D / 8;
+// Chunk plan: plan[h][c] = {u, first row, end row, 0} for the c-th chunk (at
+// most 64 rows) of head h, {-1, 0, 0, 0} after the last one.  Chunks past
+// CPH (possible only for non-monotone offsets) are dropped.  One workgroup
+// of 1024 threads per head, CQ <= 2048.
+__global__ __launch_bounds__(1024) void k_attn_plan(const int* __restrict__ q_offsets, int N,
+                                                    int CQ, int CPH, int4* __restrict__ plan) {
+  __shared__ int wsum[16];
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int* qo = q_offsets + (size_t)h * (CQ + 1);
+  int4* ph = plan + (size_t)h * CPH;
+  int a[2], b[2], nc[2];
+  int s = 0;
 #pragma unroll
-  for (int i = 0; i < NKL; ++i) {
-    const int e = tid + 256 * i, key = e / CH, ch = e % CH;
-    const int src = krow[buf][key];
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if ((unsigned)src < (unsigned)N) v = *(const uint4*)(Kh + (size_t)src * D + 8 * ch);
-    kreg[i] = v;
+  for (int k = 0; k < 2; ++k) {
+    const int u = 2 * tid + k;
+    a[k] = b[k] = nc[k] = 0;
+    if (u < CQ) {
+      a[k] = min(max(qo[u], 0), N);
+      b[k] = min(max(qo[u + 1], a[k]), N);
+      nc[k] = (b[k] - a[k] + 63) >> 6;
+    }
+    s += nc[k];
   }
+  int inc = s;
 #pragma unroll
-  for (int i = 0; i < NVL; ++i) {
-    const int e = tid + 256 * i, kp = e % (KT / 2), ch = e / (KT / 2);
-    const int s0 = krow[buf][2 * kp], s1 = krow[buf][2 * kp + 1];
-    uint4 a = make_uint4(0u, 0u, 0u, 0u), b = a;
-    if ((unsigned)s0 < (unsigned)N) a = *(const uint4*)(Vh + (size_t)s0 * D + 8 * ch);
-    if ((unsigned)s1 < (unsigned)N) b = *(const uint4*)(Vh + (size_t)s1 * D + 8 * ch);
-    va[i] = a;
-    vb[i] = b;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
   }
+  if (lane == 63) wsum[wid] = inc;
+  __syncthreads();
+  int pre = 0, total = 0;
+  for (int i = 0; i < 16; ++i) {
+    pre += i < wid ? wsum[i] : 0;
+    total += wsum[i];
+  }
+  int c = pre + inc - s;
+#pragma unroll
+  for (int k = 0; k < 2; ++k)
+    for (int i = 0; i < nc[k]; ++i, ++c)
+      if (c < CPH) ph[c] = make_int4(2 * tid + k, a[k] + 64 * i, min(a[k] + 64 * i + 64, b[k]), 0);
+  for (int cc = total + tid; cc < CPH; cc += 1024) ph[cc] = make_int4(-1, 0, 0, 0);
 }
 
-template <typename OT, int D>
+// Stream table of one query block: ck[j] = {first stream position, first row
+// of Kp} of the j-th selected block (ids outside [0, nblk) are empty),
+// ck[n] = {stream length, -1}.  256 threads, n <= 2048.
+__device__ void stream_table(const int* __restrict__ sel, int n, int nblk,
+                             const int* __restrict__ koff, int2* ck, int* tmp) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  int x[8], st[8];
+  int s = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int i = tid * 8 + k;
+    x[k] = 0;
+    st[k] = -1;
+    if (i < n) {
+      const int v = sel[i];
+      if ((unsigned)v < (unsigned)nblk) {
+        st[k] = koff[v];
+        x[k] = max(0, koff[v + 1] - st[k]);
+      }
+    }
+    s += x[k];
+  }
+  int inc = s;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) tmp[wid] = inc;
+  __syncthreads();
+  int run = inc - s;
+  for (int w = 0; w < wid; ++w) run += tmp[w];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int i = tid * 8 + k;
+    if (i < n) ck[i] = make_int2(run, st[k]);
+    run += x[k];
+    if (i == n - 1) ck[n] = make_int2(run, -1);
+  }
+  if (n == 0 && tid == 0) ck[0] = make_int2(0, -1);
+  __syncthreads();
+}
+
+template <int D, int KT>
+struct AttnTile {
+  static constexpr int CPR = D / 8;          // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;       // rows one wave-wide DMA fills
+  static constexpr int NI = KT / (4 * RPI);  // DMAs per wavefront, tensor and tile
+  static constexpr int ELEMS = KT * D;       // bf16 elements of one K or V tile
+  static_assert(NI >= 1 && NI * 4 * RPI == KT, "tile shape");
+};
+
+// XOR swizzles of the 16-byte chunk index within a row (an involution).
+// K: the 16 rows one S^T MFMA reads land in 16 different bank groups.
+// V: the 8 rows each half-wavefront's transpose read touches do too.
+template <int D>
+__device__ __forceinline__ int swz_k(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+template <int D>
+__device__ __forceinline__ int swz_v(int r) { return D == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); }
+
+// key-tile length and LDS ring depth of the MFMA kernel
+#ifndef PARK_ATTN_KT
+#define PARK_ATTN_KT 32
+#endif
+#ifndef PARK_ATTN_NS
+#define PARK_ATTN_NS 3
+#endif
+
+// One wave-wide LDS DMA: lane l's 16 bytes at g land at LDS byte address
+// lds + 16 l (lds wave-uniform).  Written as inline assembly so that the
+// compiler does not treat the transfer as a pending LDS store: it would
+// otherwise wait for every DMA in flight before each LDS read.  Completion
+// is tracked explicitly with wait_vmcnt() and a barrier.
+__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// waits until at most N vector-memory operations of this wavefront are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <typename OT, int D, int KT, int NS>
 __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t* __restrict__ Qp,
                                                    const bf16_t* __restrict__ Kp,
                                                    const bf16_t* __restrict__ Vp,
-                                                   const int* __restrict__ q_offsets,
                                                    const int* __restrict__ k_offsets,
                                                    const int* __restrict__ kv_count,
                                                    const int* __restrict__ kv_index,
-                                                   const int* __restrict__ q_perm, int N, int CQ,
-                                                   int CK, float scale_log2, OT* __restrict__ O) {
-  constexpr int KT = 64;        // keys per tile
+                                                   const int* __restrict__ q_perm,
+                                                   const int4* __restrict__ plan, int H, int N,
+                                                   int CQ, int CK, int CPH, float scale_log2,
+                                                   OT* __restrict__ O) {
+  using TS = AttnTile<D, KT>;
+  static_assert(KT % 32 == 0 && NS >= 2 && NS <= 4, "tile length / ring depth");
   constexpr int KS = D / 32;    // k-steps of S
   constexpr int DB = D / 16;    // 16-column blocks of O
-  constexpr int KROW = D + 8;   // padded K row (bf16)
-  constexpr int VROW = KT + 4;  // padded V^T row (bf16): 136 B, conflict-free 8-byte reads
-  constexpr int CH = D / 8;     // 16-byte chunks per row
-  constexpr int NKL = KT * CH / 256;        // K chunks loaded per thread
-  constexpr int NVL = (KT / 2) * CH / 256;  // V key-pair chunks loaded per thread
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KROW];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[D * VROW];
-  __shared__ int cum[AT_MAXC + 1];
-  __shared__ int kst[AT_MAXC];
-  __shared__ int krow[2][KT];
+  constexpr int NB = KT / 16;   // 16-key blocks of S per tile
+  constexpr int NCK = KT / 32;  // 32-key steps of O per tile
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  bf16_t* Ks = (bf16_t*)smem;               // [NS][KT][D], swizzled chunks
+  bf16_t* Vs = Ks + NS * TS::ELEMS;         // [NS][KT][D], swizzled chunks
+  int2* ck = (int2*)(Vs + NS * TS::ELEMS);  // [CK + 1]
   __shared__ int tmp[4];
-  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x;
-  const int* qo = q_offsets + (size_t)h * (CQ + 1);
-  const int q0 = min(max(qo[u], 0), N), q1 = min(max(qo[u + 1], q0), N);
-  if (q1 <= q0) return;
+
+  // XCD-aware work item: XCD x (= blockIdx % 8) takes items [x*per, (x+1)*per)
+  const int nitems = H * CPH;
+  const int per = (nitems + 7) >> 3;
+  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (item >= nitems) return;
+  const int4 pc = plan[item];
+  if (pc.x < 0 || pc.x >= CQ) return;
+  const int h = item / CPH, u = pc.x;
+  const int r0 = min(max(pc.y, 0), N), r1 = min(max(pc.z, r0), min(r0 + 64, N));
+  if (r1 <= r0) return;
   const int* koff = k_offsets + (size_t)h * (CK + 1);
   const size_t row = (size_t)h * CQ + u;
   int nsel = kv_count[row];
   nsel = nsel < 0 ? 0 : (nsel > CK ? CK : nsel);
-  const int* sel = kv_index + row * CK;
-  prefix_sizes(sel, nsel, CK, koff, cum, kst, tmp);
-  const int nk = cum[nsel];
+  const int tid = threadIdx.x;
+  stream_table(kv_index + row * CK, nsel, CK, koff, ck, tmp);
+  const int nk = ck[nsel].x;
   const bf16_t* Qh = Qp + (size_t)h * N * D;
   const bf16_t* Kh = Kp + (size_t)h * N * D;
   const bf16_t* Vh = Vp + (size_t)h * N * D;
-  const int w = tid >> 6, l = tid & 63, g = l >> 4, c16 = l & 15;
-  // register staging of one K/V tile (prefetched one tile ahead); the tile's
-  // stream rows come from krow[buf][*], filled by the first 64 threads.
-  uint4 kreg[NKL], va[NVL], vb[NVL];
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l = tid & 63, g = l >> 4, c16 = l & 15;
 
-  for (int r0 = q0; r0 < q1; r0 += 64) {
-    const int qr = r0 + 16 * w + c16;
-    const bool qvalid = qr < q1;
-    const bool wave_on = r0 + 16 * w < q1;
-    bf16x8_t qf[KS];
+  // queries of this wavefront (B operand of S^T)
+  const int qr = r0 + 16 * w + c16;
+  const bool qvalid = qr < r1;
+  const bool wave_on = r0 + 16 * w < r1;
+  bf16x8_t qf[KS];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-      if (qvalid) raw = *(const uint4*)(Qh + (size_t)qr * D + 32 * s + 8 * g);
-      qf[s] = __builtin_bit_cast(bf16x8_t, raw);
-    }
-    float m = -INFINITY, lpart = 0.0f;
-    f32x4_t acc[DB];
+  for (int s = 0; s < KS; ++s) {
+    uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+    if (qvalid) raw = *(const uint4*)(Qh + (size_t)qr * D + 32 * s + 8 * g);
+    qf[s] = __builtin_bit_cast(bf16x8_t, raw);
+  }
+  // make the query loads complete here: otherwise the compiler's wait for
+  // them lands inside the tile loop, where it also drains the DMA ring
 #pragma unroll
-    for (int b = 0; b < DB; ++b) acc[b] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qf[s]));
 
-    if (nk > 0) {
-      if (tid < KT) krow[0][tid] = stream_row(tid, cum, kst, nsel);
-      __syncthreads();
-      stage_kv<D, KT, NKL, NVL>(kreg, va, vb, krow, 0, Kh, Vh, N, tid);
+  // DMA lanes: tile row rr[i], chunk position pch; a cursor into ck per row
+  const int pch = l % TS::CPR;
+  int rr[TS::NI], jj[TS::NI], cj[TS::NI], kj[TS::NI], src[TS::NI];
+  int2 nx[TS::NI];
+#pragma unroll
+  for (int i = 0; i < TS::NI; ++i) {
+    rr[i] = (w * TS::NI + i) * TS::RPI + l / TS::CPR;
+    jj[i] = 0;
+    cj[i] = 0;
+    kj[i] = ck[0].y;
+    nx[i] = ck[nsel > 0 ? 1 : 0];
+    src[i] = 0;
+  }
+  // Kp/Vp row of stream position t*KT + rr[i] (row 0 past the end: in bounds,
+  // its scores are masked)
+  auto advance = [&](int t) {
+#pragma unroll
+    for (int i = 0; i < TS::NI; ++i) {
+      const int pos = t * KT + rr[i];
+      while (pos >= nx[i].x && jj[i] + 1 < nsel) {
+        ++jj[i];
+        cj[i] = nx[i].x;
+        kj[i] = nx[i].y;
+        nx[i] = ck[jj[i] + 1];
+      }
+      const int r = kj[i] + (pos - cj[i]);
+      src[i] = (pos < nk && (unsigned)r < (unsigned)N) ? r : 0;
     }
-    int buf = 0;
-    for (int k0 = 0; k0 < nk; k0 += KT) {
-      __syncthreads();  // previous tile fully consumed
+  };
+  auto issue = [&](int slot) {
+    bf16_t* ks = Ks + slot * TS::ELEMS;
+    bf16_t* vs = Vs + slot * TS::ELEMS;
 #pragma unroll
-      for (int i = 0; i < NKL; ++i) {
-        const int e = tid + 256 * i, key = e / CH, ch = e % CH;
-        *(uint4*)(Ks + key * KROW + 8 * ch) = kreg[i];
+    for (int i = 0; i < TS::NI; ++i) {
+      const bf16_t* gk = Kh + (size_t)src[i] * D + 8 * (pch ^ swz_k<D>(rr[i]));
+      const bf16_t* gv = Vh + (size_t)src[i] * D + 8 * (pch ^ swz_v<D>(rr[i]));
+      const int off = (w * TS::NI + i) * 512;  // 1 KB per wave-wide DMA
+      lds_dma16(gk, lds_addr(ks + off));
+      lds_dma16(gv, lds_addr(vs + off));
+    }
+  };
+
+  float m = -INFINITY, lpart = 0.0f;
+  f32x4_t acc[DB];
+#pragma unroll
+  for (int b = 0; b < DB; ++b) acc[b] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  // per-lane swizzle constants of the reads (independent of the key block)
+  const int swk = swz_k<D>(c16);
+  const int vr = 4 * g + (c16 >> 2);  // V row within a 32-key step (first read)
+  const int swv = swz_v<D>(vr);
+  const int vch = (c16 & 3) >> 1, vhalf = 4 * (c16 & 1);
+
+  // NS-slot ring: tiles t+1 .. t+NS-2 are in flight while tile t is computed;
+  // tile t+NS-1 is issued once every wavefront has finished tile t-1.
+  const int ntiles = (nk + KT - 1) / KT;
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < ntiles) {
+      advance(p);
+      issue(p);
+    }
+  for (int t = 0; t < ntiles; ++t) {
+    const int next = t + NS - 1;
+    if (next < ntiles) advance(next);
+    // own DMAs of tile t done: the younger tiles still in flight may stay so
+    const int younger = min(NS - 2, ntiles - 1 - t);
+    if (NS >= 4 && younger >= 2) wait_vmcnt<2 * 2 * TS::NI>();
+    else if (NS >= 3 && younger >= 1) wait_vmcnt<2 * TS::NI>();
+    else wait_vmcnt<0>();
+    __syncthreads();  // tile t landed everywhere; tile t-1 consumed (its slot is free)
+    if (next < ntiles) issue(next % NS);
+    if (!wave_on) continue;
+    const bf16_t* ks = Ks + (t % NS) * TS::ELEMS;
+    const bf16_t* vs = Vs + (t % NS) * TS::ELEMS;
+    const int k0 = t * KT;
+    f32x4_t st[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      st[b] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      const bf16_t* krow = ks + (16 * b + c16) * D;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const bf16x8_t a = *(const bf16x8_t*)(krow + 8 * ((4 * s + g) ^ swk));
+        st[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[s], st[b], 0, 0, 0);
       }
+    }
+    if (k0 + KT > nk) {  // last tile: mask the keys past the end of the stream
 #pragma unroll
-      for (int i = 0; i < NVL; ++i) {
-        const int e = tid + 256 * i, kp = e % (KT / 2), ch = e / (KT / 2);
-        const uint32_t a0 = va[i].x, a1 = va[i].y, a2 = va[i].z, a3 = va[i].w;
-        const uint32_t b0 = vb[i].x, b1 = vb[i].y, b2 = vb[i].z, b3 = vb[i].w;
-        bf16_t* vt = Vt + (8 * ch) * VROW + 2 * kp;
-        *(uint32_t*)(vt + 0 * VROW) = (a0 & 0xffffu) | (b0 << 16);
-        *(uint32_t*)(vt + 1 * VROW) = (a0 >> 16) | (b0 & 0xffff0000u);
-        *(uint32_t*)(vt + 2 * VROW) = (a1 & 0xffffu) | (b1 << 16);
-        *(uint32_t*)(vt + 3 * VROW) = (a1 >> 16) | (b1 & 0xffff0000u);
-        *(uint32_t*)(vt + 4 * VROW) = (a2 & 0xffffu) | (b2 << 16);
-        *(uint32_t*)(vt + 5 * VROW) = (a2 >> 16) | (b2 & 0xffff0000u);
-        *(uint32_t*)(vt + 6 * VROW) = (a3 & 0xffffu) | (b3 << 16);
-        *(uint32_t*)(vt + 7 * VROW) = (a3 >> 16) | (b3 & 0xffff0000u);
-      }
-      const bool more = k0 + KT < nk;
-      if (more && tid < KT) krow[buf ^ 1][tid] = stream_row(k0 + KT + tid, cum, kst, nsel);
-      __syncthreads();
-      buf ^= 1;
-      if (more) stage_kv<D, KT, NKL, NVL>(kreg, va, vb, krow, buf, Kh, Vh, N, tid);
-      if (!wave_on) continue;
-      f32x4_t st[4];
+      for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        st[b] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int r = 0; r < 4; ++r)
+          if (k0 + 16 * b + 4 * g + r >= nk) st[b][r] = -INFINITY;
+    }
+    float tmax = st[0][0];
 #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          const bf16x8_t a = *(const bf16x8_t*)(Ks + (16 * b + c16) * KROW + 32 * s + 8 * g);
-          st[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[s], st[b], 0, 0, 0);
-        }
-      }
-      // online softmax on raw scores; exp2 argument = (s - m) * scale * log2(e)
-      if (k0 + KT > nk) {  // last tile: mask the keys past the end of the stream
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+      for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, st[b][r]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float mnew = fmaxf(m, tmax);
+    if (__any(mnew != m)) {  // rescale only when some running maximum moved
+      const float alpha = __builtin_amdgcn_exp2f((m - mnew) * scale_log2);
+      lpart *= alpha;
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (k0 + 16 * b + 4 * g + r >= nk) st[b][r] = -INFINITY;
-      }
-      float tmax = st[0][0];
+      for (int b = 0; b < DB; ++b) acc[b] *= alpha;
+    }
+    m = mnew;
+    const float nms = -mnew * scale_log2;
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
+    for (int c = 0; c < NCK; ++c) {
+      bf16x8_t pb;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, st[b][r]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float mnew = fmaxf(m, tmax);
-      if (__any(mnew != m)) {  // rescale only when some running maximum moved
-        const float alpha = __builtin_amdgcn_exp2f((m - mnew) * scale_log2);
-        lpart *= alpha;
-#pragma unroll
-        for (int b = 0; b < DB; ++b) acc[b] *= alpha;
-      }
-      m = mnew;
-      const float nms = -mnew * scale_log2;
-      bf16x8_t pb[2];
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
+      for (int hb = 0; hb < 2; ++hb) {
+        const int b = 2 * c + hb;
         float p[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -380,36 +545,38 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t* __restrict__ Qp
         }
         const bf16x2_t lo = __builtin_convertvector(f32x2_t{p[0], p[1]}, bf16x2_t);
         const bf16x2_t hi = __builtin_convertvector(f32x2_t{p[2], p[3]}, bf16x2_t);
-        pb[b >> 1][(b & 1) * 4 + 0] = lo[0];
-        pb[b >> 1][(b & 1) * 4 + 1] = lo[1];
-        pb[b >> 1][(b & 1) * 4 + 2] = hi[0];
-        pb[b >> 1][(b & 1) * 4 + 3] = hi[1];
+        pb[hb * 4 + 0] = lo[0];
+        pb[hb * 4 + 1] = lo[1];
+        pb[hb * 4 + 2] = hi[0];
+        pb[hb * 4 + 3] = hi[1];
       }
+      const bf16_t* v1 = vs + (32 * c + vr) * D + vhalf;
+      const bf16_t* v2 = v1 + 16 * D;
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int mb = 0; mb < DB; ++mb) {
-          const bf16_t* vrow = Vt + (16 * mb + c16) * VROW + 32 * c + 4 * g;
-          const uint2 lo = *(const uint2*)vrow;
-          const uint2 hi = *(const uint2*)(vrow + 16);
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
-          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[c], acc[mb], 0, 0, 0);
-        }
-    }
-    float lsum = lpart + __shfl_xor(lpart, 16, 64);
-    lsum += __shfl_xor(lsum, 32, 64);
-    if (qvalid) {
-      const int dst = q_perm[(size_t)h * N + qr];
-      if ((unsigned)dst < (unsigned)N) {
-        const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
-        OT* o = O + ((size_t)h * N + dst) * D + 4 * g;
-#pragma unroll
-        for (int mb = 0; mb < DB; ++mb)
-          store_out4<OT>(o + 16 * mb, acc[mb][0] * inv, acc[mb][1] * inv, acc[mb][2] * inv,
-                         acc[mb][3] * inv);
+      for (int mb = 0; mb < DB; ++mb) {
+        const int chk = 8 * ((2 * mb + vch) ^ swv);
+        const i16x4_t t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(v1 + chk));
+        const i16x4_t t2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(v2 + chk));
+        const i16x4_t a0 = t1, a1 = t2;
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, (short __attribute__((ext_vector_type(8)))){a0[0], a0[1], a0[2], a0[3],
+                                                                  a1[0], a1[1], a1[2], a1[3]});
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, acc[mb], 0, 0, 0);
       }
     }
-    __syncthreads();
+  }
+  float lsum = lpart + __shfl_xor(lpart, 16, 64);
+  lsum += __shfl_xor(lsum, 32, 64);
+  if (qvalid) {
+    const int dst = q_perm[(size_t)h * N + qr];
+    if ((unsigned)dst < (unsigned)N) {
+      const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+      OT* o = O + ((size_t)h * N + dst) * D + 4 * g;
+#pragma unroll
+      for (int mb = 0; mb < DB; ++mb)
+        store_out4<OT>(o + 16 * mb, acc[mb][0] * inv, acc[mb][1] * inv, acc[mb][2] * inv,
+                       acc[mb][3] * inv);
+    }
   }
 }
 
@@ -427,31 +594,54 @@ static park_status attn_dispatch_d(const void* Qp, const void* Kp, const void* V
   return PARK_OK;
 }
 
+int attn_chunks_per_head(int N, int CQ) { return CQ + (N + 63) / 64; }
+
+template <typename OT, int D, int KT, int NS>
+static park_status attn_mfma_launch(const void* Qp, const void* Kp, const void* Vp, const int* ko,
+                                    const int* kc, const int* ki, const int* qp,
+                                    const int4* plan, int H, int N, int CQ, int CK, int CPH,
+                                    float sl2, void* O, hipStream_t st) {
+  const size_t lds = (size_t)2 * NS * KT * D * sizeof(bf16_t) + (size_t)(CK + 1) * sizeof(int2);
+  if (hipFuncSetAttribute((const void*)k_attn_mfma<OT, D, KT, NS>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return fail(PARK_ERR_HIP, "attention: cannot reserve %zu bytes of LDS", lds);
+  // 8 * ceil(items / 8) workgroups: every item owns one (see the remap in the kernel)
+  const unsigned nwg = 8u * (((unsigned)H * (unsigned)CPH + 7u) / 8u);
+  PARK_LAUNCH("attn_mfma", (k_attn_mfma<OT, D, KT, NS>), dim3(nwg), dim3(256), lds, st,
+              (const bf16_t*)Qp, (const bf16_t*)Kp, (const bf16_t*)Vp, ko, kc, ki, qp, plan, H, N,
+              CQ, CK, CPH, sl2, (OT*)O);
+  return PARK_OK;
+}
+
 template <typename OT>
 static park_status attn_mfma_d(const void* Qp, const void* Kp, const void* Vp, const int* qo,
                                const int* ko, const int* kc, const int* ki, const int* qp, int H,
-                               int N, int D, int CQ, int CK, void* O, hipStream_t st) {
-  dim3 g(CQ, H);
+                               int N, int D, int CQ, int CK, void* plan, void* O, hipStream_t st) {
+  const int CPH = attn_chunks_per_head(N, CQ);
+  int4* pl = (int4*)plan;
+  PARK_LAUNCH("attn_plan", k_attn_plan, dim3(H), dim3(1024), 0, st, qo, N, CQ, CPH, pl);
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)D));
   if (D == 128)
-    PARK_LAUNCH("attn_mfma", (k_attn_mfma<OT, 128>), g, dim3(256), 0, st, (const bf16_t*)Qp,
-                (const bf16_t*)Kp, (const bf16_t*)Vp, qo, ko, kc, ki, qp, N, CQ, CK, sl2, (OT*)O);
-  else
-    PARK_LAUNCH("attn_mfma", (k_attn_mfma<OT, 64>), g, dim3(256), 0, st, (const bf16_t*)Qp,
-                (const bf16_t*)Kp, (const bf16_t*)Vp, qo, ko, kc, ki, qp, N, CQ, CK, sl2, (OT*)O);
-  return PARK_OK;
+    return attn_mfma_launch<OT, 128, PARK_ATTN_KT, PARK_ATTN_NS>(Qp, Kp, Vp, ko, kc, ki, qp, pl, H,
+                                                               N, CQ, CK, CPH, sl2, O, st);
+  return attn_mfma_launch<OT, 64, PARK_ATTN_KT, PARK_ATTN_NS>(Qp, Kp, Vp, ko, kc, ki, qp, pl, H, N,
+                                                              CQ, CK, CPH, sl2, O, st);
+}
+
+size_t attn_plan_bytes(int H, int N, int CQ) {
+  return (size_t)H * attn_chunks_per_head(N, CQ) * sizeof(int4);
 }
 
 park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,
                              const int* k_offsets, const int* kv_count, const int* kv_index,
                              const int* q_perm, int H, int N, int D, int dtype, int CQ, int CK,
-                             void* O, int out_dtype, hipStream_t st) {
+                             void* O, int out_dtype, void* plan, hipStream_t st) {
   if (dtype == PARK_BF16) {
     if (out_dtype == PARK_BF16)
       return attn_mfma_d<bf16_t>(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, H,
-                                 N, D, CQ, CK, O, st);
+                                 N, D, CQ, CK, plan, O, st);
     return attn_mfma_d<float>(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, H, N,
-                              D, CQ, CK, O, st);
+                              D, CQ, CK, plan, O, st);
   }
   // fp32 inputs: VALU kernel in fp32 (the contraction cannot use bf16 MFMA exactly)
   if (out_dtype == PARK_BF16)

@@ -71,10 +71,12 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
                             int* kv_count, int* kv_index, int* status, hipStream_t st);
 
 // k_attn.hip ----------------------------------------------------------------
+// `plan` is device scratch of attn_plan_bytes(H, N, CQ) bytes (bf16 inputs only)
+size_t attn_plan_bytes(int H, int N, int CQ);
 park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,
                              const int* k_offsets, const int* kv_count, const int* kv_index,
                              const int* q_perm, int H, int N, int D, int dtype, int CQ, int CK,
-                             void* O, int out_dtype, hipStream_t st);
+                             void* O, int out_dtype, void* plan, hipStream_t st);
 
 // misc ----------------------------------------------------------------------
 park_status launch_clear_status(int* status, hipStream_t st);

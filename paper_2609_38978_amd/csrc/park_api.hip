@@ -177,7 +177,21 @@ static RetrieveBufs carve_retrieve(Carver& cv, int H, int D, int CQ, int CK) {
   return r;
 }
 
-// status word first, then the larger of the cluster and retrieval regions
+// attention: the status word, then the chunk plan
+static size_t attn_ws_end(int H, int N, int CQ) {
+  Carver a(nullptr);
+  a.take<int>(64);
+  a.take<int4>(attn_plan_bytes(H, N, CQ) / sizeof(int4));
+  return a.off;
+}
+
+static void* carve_attn_plan(void* ws, int H, int N, int CQ) {
+  Carver cv(ws);
+  cv.take<int>(64);
+  return cv.take<int4>(attn_plan_bytes(H, N, CQ) / sizeof(int4));
+}
+
+// status word first, then the largest of the cluster, retrieval and attention regions
 static size_t ws_bytes_for(int H, int N, int D, int CQ, int CK) {
   Carver a(nullptr);
   a.take<int>(64);
@@ -188,7 +202,7 @@ static size_t ws_bytes_for(int H, int N, int D, int CQ, int CK) {
   Carver c2(nullptr);
   c2.off = base;
   carve_retrieve(c2, H, D, CQ, CK);
-  return std::max(c1.off, c2.off) + 256;
+  return std::max(std::max(c1.off, c2.off), attn_ws_end(H, N, CQ)) + 256;
 }
 
 static park_status check_ws(void* ws, size_t ws_bytes, size_t need) {
@@ -367,7 +381,8 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
                                    const int32_t* q_offsets, const int32_t* k_offsets,
                                    const int32_t* kv_count, const int32_t* kv_index,
                                    const int32_t* q_perm, const park_dims* dims, int32_t CQ,
-                                   int32_t CK, void* O, int32_t out_dtype, void* stream) {
+                                   int32_t CK, void* O, int32_t out_dtype, void* ws,
+                                   size_t ws_bytes, void* stream) {
   g_err[0] = 0;
   PARK_TRY(check_dims(dims));
   PARK_TRY(check_C(CQ, dims->N, "CQ"));
@@ -383,9 +398,13 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
   PARK_TRY(check_ptr(kv_index, "kv_index"));
   PARK_TRY(check_ptr(q_perm, "q_perm"));
   PARK_TRY(check_ptr(O, "O"));
+  PARK_TRY(check_ws(ws, ws_bytes, attn_ws_end(dims->H, dims->N, CQ) + 256));
+  hipStream_t st = (hipStream_t)stream;
+  Carver cv(ws);
+  PARK_TRY(launch_clear_status(cv.take<int>(64), st));
   return launch_attention(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, dims->H,
                           dims->N, dims->d, dims->dtype, CQ, CK, O, out_dtype,
-                          (hipStream_t)stream);
+                          carve_attn_plan(ws, dims->H, dims->N, CQ), st);
 }
 
 park_status park_forward(const void* Q, const void* K, const void* V, const park_dims* dims,
@@ -447,7 +466,7 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
   }
   return launch_attention(s->Qp, s->Kp, s->Vp, s->q_offsets, s->k_offsets, s->kv_count,
                           s->kv_index, s->q_perm, H, N, D, dims->dtype, p->CQ, p->CK, O,
-                          p->out_dtype, st);
+                          p->out_dtype, carve_attn_plan(ws, H, N, p->CQ), st);
 }
 
 park_status park_check(void* ws, void* stream) {

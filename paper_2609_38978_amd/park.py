@@ -75,7 +75,8 @@ def lib():
         "park_gather_rows": [vp, vp, pd, vp, vp],
         "park_block_centroids": [vp, vp, vp, pd, i32, vp, vp, vp],
         "park_retrieve_blocks": [vp, vp, vp, vp, pd, i32, i32, i32, f64, vp, vp, vp, vp, sz, vp],
-        "park_block_sparse_attn": [vp, vp, vp, vp, vp, vp, vp, vp, pd, i32, i32, vp, i32, vp],
+        "park_block_sparse_attn": [vp, vp, vp, vp, vp, vp, vp, vp, pd, i32, i32, vp, i32, vp, sz,
+                                   vp],
         "park_forward": [vp, vp, vp, pd, C.POINTER(Params), i32, C.POINTER(State), vp, vp, sz,
                          vp],
         "park_check": [vp, vp],
@@ -195,14 +196,15 @@ def park_retrieve_blocks(Qp, q_offsets, centroids, k_sizes, CQ: int, CK: int, se
 
 
 def park_block_sparse_attn(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm,
-                           CQ: int, CK: int, out_dtype: int = PARK_F32):
+                           CQ: int, CK: int, out_dtype: int = PARK_F32, ws=None):
     dims = _dims(Qp)
     O = torch.empty(Qp.shape, dtype=torch.float32 if out_dtype == PARK_F32 else torch.bfloat16,
                     **_dev(Qp))
+    ws = workspace(Qp, CQ, CK) if ws is None else ws
     _check(lib().park_block_sparse_attn(_ptr(Qp), _ptr(Kp), _ptr(Vp), _ptr(q_offsets),
                                         _ptr(k_offsets), _ptr(kv_count), _ptr(kv_index),
                                         _ptr(q_perm), C.byref(dims), CQ, CK, _ptr(O), out_dtype,
-                                        _stream()))
+                                        _ptr(ws), ws.numel(), _stream()))
     return O
 
 

@@ -103,11 +103,14 @@ def test_retrieve_and_attention_argument_errors():
     assert retr(CK=3000) == P.PARK_ERR_INVALID_ARG
     assert retr(ws_bytes=8) == P.PARK_ERR_WORKSPACE
     r = L.park_block_sparse_attn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16, 16,
-                                 FAKE, 7, None)
+                                 FAKE, 7, FAKE, 1 << 30, None)
     assert r == P.PARK_ERR_INVALID_ARG
     r = L.park_block_sparse_attn(FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16, 16,
-                                 FAKE, P.PARK_F32, None)
+                                 FAKE, P.PARK_F32, FAKE, 1 << 30, None)
     assert r == P.PARK_ERR_INVALID_ARG
+    r = L.park_block_sparse_attn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16, 16,
+                                 FAKE, P.PARK_F32, FAKE, 8, None)
+    assert r == P.PARK_ERR_WORKSPACE
 
 
 def test_forward_argument_errors():
