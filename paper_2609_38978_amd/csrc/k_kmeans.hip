@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
                                               const double* __restrict__ Gbar, int C,
                                               double* __restrict__ w, double* __restrict__ b,
                                               double* __restrict__ wT, bf16_t* __restrict__ w3,
-                                              size_t plane, float* __restrict__ b32,
+                                              size_t plane, float* __restrict__ b32, int Cpad,
                                               float* __restrict__ wn, float* __restrict__ eb,
                                               float* __restrict__ bmax, int* __restrict__ nflag) {
   constexpr int CB = 16, NG = 256 / D, PER = CB / NG;
@@ -156,11 +156,13 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
     if (b32) {
       fn = (float)(sqrt(n2) * (1.0 + 1e-6));
       fe = (float)(fabs(s) * (2.0 * 1.1 * 5.9604644775390625e-08) * (1.0 + 1e-6));
-      b32[(size_t)h * C + v0 + tid] = (float)s;
+      b32[(size_t)h * Cpad + v0 + tid] = (float)s;
       wn[(size_t)h * C + v0 + tid] = fn;
       eb[(size_t)h * C + v0 + tid] = fe;
     }
   }
+  if (b32 && blockIdx.x == gridDim.x - 1)  // padding scores: never the minimum
+    for (int v = C + tid; v < Cpad; v += 256) b32[(size_t)h * Cpad + v] = INFINITY;
   if (b32 && tid < 64) {
     // this block's maxima of |w_v| and eb_v (reduced by the assignment)
     for (int o = 8; o > 0; o >>= 1) {
@@ -191,28 +193,49 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
 // the score, and |s^_v| <= |b_v| + 2.01 |x| |w_v|:
 //   |s^_v - s_v| <= E_v = Kx |w_v| + eb_v,
 //   Kx = 1.1 (2 et + 2.01 2^-24) |x|,  eb_v = 1.1 * 2 * 2^-24 |b_v|
-// (the factor 1.1 covers the rounding of |x| and of the bound itself).  A
-// token is certified when, for its fast argmin v1, s^_v - E_v > s^_v1 + E_v1
-// for every other v: then v1 is the exact argmin.  Otherwise (near-ties,
-// exact ties) it is listed for the float64 refinement.
+// (the factor 1.1 covers the rounding of |x| and of the bound itself).
 //
-// Only scores within E_max = Kx max|w| + max eb of the running best can
-// matter, so the per-score bookkeeping runs only when some lane of the
-// wavefront holds such a score (a wave-uniform branch); a skipped score
-// s^_v > ub + E_max has lower bound s^_v - E_v > ub, above the final best's
-// upper bound.
+// Certification: with v1 the fast argmin and L the smallest fast score of
+// every other centroid, v1 is the exact argmin when
+//   L - Emax > s^_v1 + E_v1,   Emax = Kx max_v |w_v| + max_v eb_v >= E_v.
+// Otherwise (near-ties, exact ties) the token is listed for the float64
+// refinement.
 //
-// Workgroup = 256 tokens (4 wavefronts x 4 blocks of 16), centroid tiles of 64
-// staged in LDS with the next tile prefetched into registers.  MFMA
-// orientation: A = 16 centroids x 32 dims, B = 32 dims x 16 tokens, so lane l
-// holds centroids 4(l/16)+r of token l%16.
+// Bookkeeping per lane and token (the lane sees a quarter of the centroids):
+// best (score and id) and L.  Each 16-centroid step gives the lane 4 scores;
+// their minimum m either stays above best (the common case: L = min(L, m))
+// or some lane of the wavefront takes the per-score path.  The running best
+// starts at an estimate of the score of the token's previous label (plus a
+// margin) with no id, so after the first iterations almost no score beats
+// it; the estimate never enters L, and a token whose best is still that
+// estimate at the end is listed for refinement.  Correctness does not depend
+// on the estimate, only the number of listed tokens does.
+//
+// Workgroup = 256 tokens (4 wavefronts x 4 blocks of 16).  Centroid tiles of
+// 32 rows of the three parts go from HBM to a two-slot LDS ring by LDS DMA
+// (rows swizzled in 16-byte chunks, see the reads), the next tile in flight
+// while this one is scored.  MFMA orientation: A = 16 centroids x 32 dims,
+// B = 32 dims x 16 tokens, so lane l holds centroids 4(l/16)+r of token l%16.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// One wave-wide LDS DMA (lane l's 16 bytes at g land at LDS byte lds + 16 l),
+// as inline assembly so that the compiler does not drain every DMA in flight
+// before each LDS read; completion is waited for explicitly.
+__device__ __forceinline__ void km_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t km_lds_addr(const void* p) {
+  return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+template <int D>
+__device__ __forceinline__ int km_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
 
 template <int D>
 __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ X,
                                                      const bf16_t* __restrict__ w3, size_t plane,
-                                                     const float* __restrict__ b32,
+                                                     const float* __restrict__ b32, int Cpad,
                                                      const float* __restrict__ wn,
                                                      const float* __restrict__ eb,
                                                      const float* __restrict__ bmax, int nbm,
@@ -220,22 +243,22 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
                                                      int* __restrict__ labels,
                                                      int* __restrict__ flags,
                                                      int* __restrict__ nflag) {
-  constexpr int TB = 4, CT = 64, KS = D / 32, WROW = D + 8, CH = D / 8;
-  constexpr int NL = CT * CH / 256;  // 16-byte chunks of each part per thread and tile
+  constexpr int TB = 4, CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
+  constexpr int NI = 3 * CT / (4 * RPI);  // DMAs per wavefront and tile
+  static_assert(NI * 4 * RPI == 3 * CT, "tile shape");
   constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f;
   constexpr float ET = U24 * 1.01f + (D + 1) * DEL * 1.0079f + 0.00390625f * 1.01f * (2 * D + 1) * DEL +
                        U24 * 1.01f;
   constexpr float KXC = 1.1f * (2.0f * ET + 2.01f * U24) * 1.0001f;
-  __shared__ __attribute__((aligned(16))) bf16_t W1[CT * WROW];
-  __shared__ __attribute__((aligned(16))) bf16_t W2[CT * WROW];
-  __shared__ __attribute__((aligned(16))) bf16_t W3[CT * WROW];
-  __shared__ __attribute__((aligned(16))) float bs[CT];
-  __shared__ __attribute__((aligned(16))) float ns[CT];
-  __shared__ __attribute__((aligned(16))) float es[CT];
-  const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, g = l >> 4,
-            c16 = l & 15;
+  __shared__ __attribute__((aligned(16))) bf16_t Wt[2][3 * CT * D];  // [slot][part][row][D]
+  __shared__ __attribute__((aligned(16))) float Bt[2][CT];
+  __shared__ float mx_s[2];
+  const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int t0 = blockIdx.x * 256 + w * 64;
   const bf16_t* Xh = X + (size_t)h * N * D;
+  const bf16_t* P1 = w3 + (size_t)h * C * D;
+  const float* bh = b32 + (size_t)h * Cpad;
   bf16x8_t xf[TB][KS];
   float xsq[TB];
 #pragma unroll
@@ -255,7 +278,6 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       }
     }
   }
-  __shared__ float mx_s[2];
   if (tid < 64) {
     float a = 0.0f, c = 0.0f;
     for (int i = tid; i < nbm; i += 64) {
@@ -271,109 +293,98 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       mx_s[1] = c;
     }
   }
-  __syncthreads();
-  const float nmax = mx_s[0], ebmax = mx_s[1];
-  float kx[TB], emax[TB];
+  // running best: an estimate of the previous label's score plus a margin
+  float kx[TB], best[TB], L[TB];
+  int bidx[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
     float xs = xsq[tb] + __shfl_xor(xsq[tb], 16, 64);
     xs += __shfl_xor(xs, 32, 64);
     kx[tb] = KXC * sqrtf(xs);
-    emax[tb] = fmaf(kx[tb], nmax, ebmax) * 1.0001f;
+    const int tok = t0 + 16 * tb + c16;
+    int prev = tok < N ? labels[(size_t)h * N + tok] : -1;
+    prev = (unsigned)prev < (unsigned)C ? prev : -1;
+    float dot = 0.0f;
+    if (prev >= 0) {
+      const bf16_t* wp = P1 + (size_t)prev * D + 8 * g;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const uint4 u1 = *(const uint4*)(wp + 32 * s);
+        const uint4 u2 = *(const uint4*)(wp + plane + 32 * s);
+        const uint4 u3 = *(const uint4*)(wp + 2 * plane + 32 * s);
+        const uint4 ux = __builtin_bit_cast(uint4, xf[tb][s]);
+        const uint32_t a1[4] = {u1.x, u1.y, u1.z, u1.w}, a2[4] = {u2.x, u2.y, u2.z, u2.w},
+                       a3[4] = {u3.x, u3.y, u3.z, u3.w}, ax[4] = {ux.x, ux.y, ux.z, ux.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float wl = (__uint_as_float(a1[e] << 16) + __uint_as_float(a2[e] << 16)) +
+                           __uint_as_float(a3[e] << 16);
+          const float wh = (__uint_as_float(a1[e] & 0xffff0000u) +
+                            __uint_as_float(a2[e] & 0xffff0000u)) +
+                           __uint_as_float(a3[e] & 0xffff0000u);
+          dot = fmaf(__uint_as_float(ax[e] << 16), wl, dot);
+          dot = fmaf(__uint_as_float(ax[e] & 0xffff0000u), wh, dot);
+        }
+      }
+    }
+    dot += __shfl_xor(dot, 16, 64);
+    dot += __shfl_xor(dot, 32, 64);
+    best[tb] = INFINITY;
+    if (prev >= 0) {
+      const float e = fmaf(kx[tb], wn[(size_t)h * C + prev], eb[(size_t)h * C + prev]);
+      const float est = fmaf(-2.0f, dot, bh[prev]);
+      best[tb] = est + 2.0f * e + 1e-6f * fabsf(est);
+    }
+    L[tb] = INFINITY;
+    bidx[tb] = -1;
   }
-  // per token and lane: best fast score, its index, its upper bound, the
-  // lowest lower bound among the lane's other centroids, and the threshold
-  // above which a score cannot matter
-  float best[TB], ub[TB], lo2[TB], thr[TB];
-  int bidx[TB];
+  // all global loads done before the tile loop (its waits are explicit)
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
-    best[tb] = INFINITY;
-    ub[tb] = INFINITY;
-    lo2[tb] = INFINITY;
-    thr[tb] = INFINITY;
-    bidx[tb] = 0;
-  }
-  const bf16_t* P1 = w3 + (size_t)h * C * D;
-  const bf16_t* P2 = P1 + plane;
-  const bf16_t* P3 = P2 + plane;
-  const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
-  uint4 r1[NL], r2[NL], r3[NL];
-  float rb = INFINITY, rn = 0.0f, re = 0.0f;
-  // prefetch tile 0
 #pragma unroll
-  for (int i = 0; i < NL; ++i) {
-    const int e = tid + 256 * i, r = e / CH, ch = e % CH;
-    uint4 v1 = make_uint4(0u, 0u, 0u, 0u), v2 = v1, v3 = v1;
-    if (r < C) {
-      const size_t o = (size_t)r * D + 8 * ch;
-      v1 = *(const uint4*)(P1 + o);
-      v2 = *(const uint4*)(P2 + o);
-      v3 = *(const uint4*)(P3 + o);
-    }
-    r1[i] = v1;
-    r2[i] = v2;
-    r3[i] = v3;
+    for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(xf[tb][s]));
+    asm volatile("" ::"v"(best[tb]), "v"(kx[tb]));
   }
-  if (tid < CT && tid < C) {
-    rb = b32[(size_t)h * C + tid];
-    rn = wn[(size_t)h * C + tid];
-    re = eb[(size_t)h * C + tid];
-  }
-  for (int c0 = 0; c0 < C; c0 += CT) {
-    __syncthreads();
+
+  // LDS DMA lanes: row rr[i] of the tile's 3*CT part-rows, chunk pch
+  const int pch = l % CPR;
+  const int ntiles = (C + CT - 1) / CT;
+  auto issue = [&](int tile, int slot) {
+    const int c0 = tile * CT;
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int e = tid + 256 * i, r = e / CH, ch = e % CH;
-      *(uint4*)(W1 + r * WROW + 8 * ch) = r1[i];
-      *(uint4*)(W2 + r * WROW + 8 * ch) = r2[i];
-      *(uint4*)(W3 + r * WROW + 8 * ch) = r3[i];
+    for (int i = 0; i < NI; ++i) {
+      const int row = (w * NI + i) * RPI + l / CPR;
+      const int part = row / CT, r = row % CT;
+      const int v = min(c0 + r, C - 1);
+      const bf16_t* src = P1 + part * plane + (size_t)v * D + 8 * (pch ^ km_swz<D>(r));
+      km_dma16(src, km_lds_addr(&Wt[slot][0] + (w * NI + i) * 512));
     }
-    if (tid < CT) {
-      bs[tid] = rb;
-      ns[tid] = rn;
-      es[tid] = re;
-    }
-    __syncthreads();
-    const int c1 = c0 + CT;
-    if (c1 < C) {  // prefetch the next tile while this one is scored
-#pragma unroll
-      for (int i = 0; i < NL; ++i) {
-        const int e = tid + 256 * i, r = e / CH, ch = e % CH;
-        uint4 v1 = make_uint4(0u, 0u, 0u, 0u), v2 = v1, v3 = v1;
-        if (c1 + r < C) {
-          const size_t o = (size_t)(c1 + r) * D + 8 * ch;
-          v1 = *(const uint4*)(P1 + o);
-          v2 = *(const uint4*)(P2 + o);
-          v3 = *(const uint4*)(P3 + o);
-        }
-        r1[i] = v1;
-        r2[i] = v2;
-        r3[i] = v3;
-      }
-      rb = INFINITY;
-      rn = 0.0f;
-      re = 0.0f;
-      if (tid < CT && c1 + tid < C) {
-        rb = b32[(size_t)h * C + c1 + tid];
-        rn = wn[(size_t)h * C + c1 + tid];
-        re = eb[(size_t)h * C + c1 + tid];
-      }
-    }
+    if (w == 0 && l < CT / 4) km_dma16(bh + c0 + 4 * l, km_lds_addr(&Bt[slot][0]));
+  };
+  if (ntiles > 0) issue(0, 0);
+  const int swk = km_swz<D>(c16);
+  for (int t = 0; t < ntiles; ++t) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // tile t landed; tile t-1 consumed by every wavefront
+    if (t + 1 < ntiles) issue(t + 1, (t + 1) & 1);
+    const bf16_t* W1 = &Wt[t & 1][0];
+    const bf16_t* W2 = W1 + CT * D;
+    const bf16_t* W3 = W2 + CT * D;
 #pragma unroll
     for (int cb = 0; cb < CT / 16; ++cb) {
       f32x4_t ahi[TB], arest[TB];
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
-        ahi[tb] = zero;
-        arest[tb] = zero;
+        ahi[tb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        arest[tb] = ahi[tb];
       }
-      const int rowo = (16 * cb + c16) * WROW + 8 * g;
+      const int rowo = (16 * cb + c16) * D;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        const bf16x8_t a1 = *(const bf16x8_t*)(W1 + rowo + 32 * s);
-        const bf16x8_t a2 = *(const bf16x8_t*)(W2 + rowo + 32 * s);
-        const bf16x8_t a3 = *(const bf16x8_t*)(W3 + rowo + 32 * s);
+        const int co = rowo + 8 * ((4 * s + g) ^ swk);
+        const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
+        const bf16x8_t a2 = *(const bf16x8_t*)(W2 + co);
+        const bf16x8_t a3 = *(const bf16x8_t*)(W3 + co);
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) {
           ahi[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[tb][s], ahi[tb], 0, 0, 0);
@@ -381,62 +392,61 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
           arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
         }
       }
-      const float4 b4 = *(const float4*)(bs + 16 * cb + 4 * g);
+      const float4 b4 = *(const float4*)(&Bt[t & 1][16 * cb + 4 * g]);
       const float bv[4] = {b4.x, b4.y, b4.z, b4.w};
-      float sc[TB][4];
-      bool hit = false;
+      const int vbase = t * CT + 16 * cb + 4 * g;
 #pragma unroll
-      for (int tb = 0; tb < TB; ++tb)
+      for (int tb = 0; tb < TB; ++tb) {
+        float sc[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          sc[tb][r] = fmaf(-2.0f, ahi[tb][r] + arest[tb][r], bv[r]);
-          hit |= !(sc[tb][r] > thr[tb]);
-        }
-      if (__any(hit)) {
-        const float4 n4 = *(const float4*)(ns + 16 * cb + 4 * g);
-        const float4 e4 = *(const float4*)(es + 16 * cb + 4 * g);
-        const float nv[4] = {n4.x, n4.y, n4.z, n4.w};
-        const float ev[4] = {e4.x, e4.y, e4.z, e4.w};
+        for (int r = 0; r < 4; ++r) sc[r] = fmaf(-2.0f, ahi[tb][r] + arest[tb][r], bv[r]);
+        const float m = fminf(fminf(sc[0], sc[1]), fminf(sc[2], sc[3]));
+        const bool c = m < best[tb];
+        if (__any(c)) {
+          if (c) {
 #pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float x = sc[tb][r];
-            const float e = fmaf(kx[tb], nv[r], ev[r]);
-            if (x < best[tb]) {
-              lo2[tb] = fminf(lo2[tb], 2.0f * best[tb] - ub[tb]);  // old best joins the others
-              best[tb] = x;
-              ub[tb] = x + e;
-              bidx[tb] = c0 + 16 * cb + 4 * g + r;
-            } else {
-              lo2[tb] = fminf(lo2[tb], x - e);
+            for (int r = 0; r < 4; ++r) {
+              const bool nb = sc[r] < best[tb];
+              const float out = nb ? (bidx[tb] >= 0 ? best[tb] : INFINITY) : sc[r];
+              L[tb] = fminf(L[tb], out);
+              best[tb] = nb ? sc[r] : best[tb];
+              bidx[tb] = nb ? vbase + r : bidx[tb];
             }
+          } else {
+            L[tb] = fminf(L[tb], m);
           }
-          thr[tb] = ub[tb] + emax[tb];
+        } else {
+          L[tb] = fminf(L[tb], m);
         }
       }
     }
   }
+  const float nmax = mx_s[0], ebmax = mx_s[1];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
-    // merge over the four lane groups holding this token
+    // merge over the four lane groups holding this token (ties: lowest id)
 #pragma unroll
     for (int o = 16; o <= 32; o <<= 1) {
-      const float ob = __shfl_xor(best[tb], o, 64), ou = __shfl_xor(ub[tb], o, 64);
-      const float ol = __shfl_xor(lo2[tb], o, 64);
+      const float ob = __shfl_xor(best[tb], o, 64), oL = __shfl_xor(L[tb], o, 64);
       const int oi = __shfl_xor(bidx[tb], o, 64);
-      if (ob < best[tb] || (ob == best[tb] && oi < bidx[tb])) {
-        lo2[tb] = fminf(fminf(lo2[tb], ol), 2.0f * best[tb] - ub[tb]);
-        best[tb] = ob;
-        ub[tb] = ou;
-        bidx[tb] = oi;
-      } else {
-        lo2[tb] = fminf(fminf(lo2[tb], ol), 2.0f * ob - ou);
-      }
+      const bool mine_valid = bidx[tb] >= 0, other_valid = oi >= 0;
+      const bool take = other_valid && (!mine_valid || ob < best[tb] ||
+                                        (ob == best[tb] && oi < bidx[tb]));
+      const float loser = take ? (mine_valid ? best[tb] : INFINITY)
+                               : (other_valid ? ob : INFINITY);
+      L[tb] = fminf(fminf(L[tb], oL), loser);
+      best[tb] = take ? ob : best[tb];
+      bidx[tb] = take ? oi : bidx[tb];
     }
     const int tok = t0 + 16 * tb + c16;
     if (g == 0 && tok < N) {
-      const bool ok = isfinite(best[tb]) && isfinite(ub[tb]) && (lo2[tb] > ub[tb]);
+      bool ok = false;
+      if (bidx[tb] >= 0 && isfinite(best[tb])) {
+        const int v = bidx[tb];
+        const float e1 = fmaf(kx[tb], wn[(size_t)h * C + v], eb[(size_t)h * C + v]);
+        const float emax = fmaf(kx[tb], nmax, ebmax) * 1.0001f;
+        ok = (L[tb] - emax) > (best[tb] + e1);
+      }
       if (ok) {
         labels[(size_t)h * N + tok] = bidx[tb];
       } else {
@@ -759,12 +769,13 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
     const int nbm = (C + 15) / 16;
     PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3(nbm, H), dim3(256), 0, st,
                 (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.wT : nullptr,
-                fast ? kb.w3 : nullptr, plane, fast ? kb.b32 : nullptr, fast ? kb.wn : nullptr,
+                fast ? kb.w3 : nullptr, plane, fast ? kb.b32 : nullptr, kmeans_cpad(C),
+                fast ? kb.wn : nullptr,
                 fast ? kb.eb : nullptr, kb.hmax, kb.nflag);
     if constexpr (fast) {
       PARK_LAUNCH("kmeans_assign_fast", k_assign_fast<D>, dim3((N + 255) / 256, H), dim3(256), 0,
                   st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane, (const float*)kb.b32,
-                  (const float*)kb.wn, (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C,
+                  kmeans_cpad(C), (const float*)kb.wn, (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C,
                   kb.labels, kb.flags, kb.nflag);
       PARK_LAUNCH("kmeans_refine64", (k_refine<T, D>), dim3(rg, H), dim3(256), 0, st, X,
                   (const double*)kb.wT, (const double*)kb.b, N, C, (const int*)kb.flags,

@@ -22,6 +22,9 @@ park_status launch_gather(const void* X, const int* perm, int H, int N, int D, i
                           hipStream_t st);
 
 // k_kmeans.hip --------------------------------------------------------------
+// centroid count padded to the fast assignment's tile multiple
+inline int kmeans_cpad(int C) { return (C + 63) / 64 * 64; }
+
 struct KmeansBufs {
   int* init;      // [H][C]
   double* mu;     // [H][C][D] centroids in the input space
@@ -34,7 +37,7 @@ struct KmeansBufs {
   int* status;    // sticky device status word
   // fast path (bf16 points)
   bf16_t* w3;     // [3][H][C][D] w as three bf16 parts
-  float* b32;     // [H][C]
+  float* b32;     // [H][kmeans_cpad(C)], padding +inf
   float* wn;      // [H][C]    |w_v| (rounded up)
   float* eb;      // [H][C]    |b_v| term of the fast-path error bound
   float* hmax;    // [H][ceil(C/16)][2] per-block max |w_v|, max eb_v

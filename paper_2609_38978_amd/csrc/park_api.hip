@@ -153,7 +153,7 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   c.labels = cv.take<int>((size_t)H * N);
   c.thist = cv.take<int>((size_t)H * C * sort_tiles(H, N, C));
   c.w3 = cv.take<bf16_t>((size_t)3 * H * C * D);
-  c.b32 = cv.take<float>((size_t)H * C);
+  c.b32 = cv.take<float>((size_t)H * kmeans_cpad(C));
   c.wn = cv.take<float>((size_t)H * C);
   c.eb = cv.take<float>((size_t)H * C);
   c.hmax = cv.take<float>((size_t)2 * H * ((C + 15) / 16));
