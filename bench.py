@@ -35,6 +35,8 @@ def parse():
     ap.add_argument("--workload", default="medium",
                     help="synthetic layer: tiny | medium | wan | hunyuan")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time eager launches only (no HIP graph replay)")
     ap.add_argument("--cpu-heads", type=int, default=4,
                     help="heads of the layer the oracle runs for the CPU baseline")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -190,11 +192,10 @@ def main():
         P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
     P.park_check(ws)
     torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    P.park_profile_reset()
-    P.park_profile_enable(True)
-    torch.cuda.synchronize()
+
+    # (1) eager launches: the measured value
+    stream = torch.cuda.current_stream()
     t0 = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
@@ -202,10 +203,38 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    ms_eager = e0.elapsed_time(e1) / args.steps
+    P.park_check(ws)
+
+    # (2) the same forward captured once in a HIP graph and replayed (reported
+    # beside the eager time); every kernel of the layer runs in every replay
+    ms_graph = None
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
+        graph.replay()
+        torch.cuda.synchronize()
+        gs = torch.cuda.current_stream()
+        e0.record(gs)
+        for _ in range(args.steps):
+            graph.replay()
+        e1.record(gs)
+        torch.cuda.synchronize()
+        ms_graph = e0.elapsed_time(e1) / args.steps
+        P.park_check(ws)
+        del graph
+    ms = ms_eager
+
+    # (3) per-kernel HIP events on the launch stream (a separate eager pass)
+    P.park_profile_reset()
+    P.park_profile_enable(True)
+    for _ in range(args.steps):
+        P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
+    torch.cuda.synchronize()
     P.park_profile_enable(False)
     prof = P.park_profile_read()
     P.park_check(ws)
-    ms = e0.elapsed_time(e1) / args.steps
     dense_flops = 4.0 * cfg.N * cfg.N * cfg.d * cfg.H
 
     # per-kernel share and roofline of the dominant kernel
@@ -239,6 +268,8 @@ def main():
                       "H": cfg.H, "N": cfg.N, "d": cfg.d, "C": C, "T": cfg.iters,
                       "select": mode, "param": param},
            "dense_equiv_tflops": round(dense_flops / (ms * 1e-3) / 1e12, 3),
+           "timing": "eager park_forward calls, events on the launch stream",
+           "graph_ms_per_step": None if ms_graph is None else round(ms_graph, 4),
            "wall_s": round(wall, 3), "stages": stages, "roofline": roof}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, q, k, v, min(args.cpu_heads, cfg.H))

@@ -602,9 +602,12 @@ static park_status attn_mfma_launch(const void* Qp, const void* Kp, const void* 
                                     const int4* plan, int H, int N, int CQ, int CK, int CPH,
                                     float sl2, void* O, hipStream_t st) {
   const size_t lds = (size_t)2 * NS * KT * D * sizeof(bf16_t) + (size_t)(CK + 1) * sizeof(int2);
-  if (hipFuncSetAttribute((const void*)k_attn_mfma<OT, D, KT, NS>,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-    return fail(PARK_ERR_HIP, "attention: cannot reserve %zu bytes of LDS", lds);
+  // reserved once for the largest CK (2048), outside any stream capture that may follow
+  constexpr size_t lds_max = (size_t)2 * NS * KT * D * sizeof(bf16_t) + (size_t)2049 * sizeof(int2);
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)k_attn_mfma<OT, D, KT, NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)lds_max);
+  if (attr != hipSuccess) return fail(PARK_ERR_HIP, "attention: cannot reserve %zu bytes of LDS", lds);
   // 8 * ceil(items / 8) workgroups: every item owns one (see the remap in the kernel)
   const unsigned nwg = 8u * (((unsigned)H * (unsigned)CPH + 7u) / 8u);
   PARK_LAUNCH("attn_mfma", (k_attn_mfma<OT, D, KT, NS>), dim3(nwg), dim3(256), lds, st,

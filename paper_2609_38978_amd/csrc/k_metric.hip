@@ -194,8 +194,10 @@ park_status launch_metric(const void* Q, int H, int N, int D, int dtype, double 
               DD, 1.0 / (double)N, G);
   const size_t lds = (size_t)DD * sizeof(double);
   if (D == 128) {
-    hipFuncSetAttribute((const void*)k_metric_chol<128>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    // set once, outside any stream capture that may follow
+    static const hipError_t attr = hipFuncSetAttribute(
+        (const void*)k_metric_chol<128>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (attr != hipSuccess) return fail(PARK_ERR_HIP, "metric: cannot reserve %zu bytes of LDS", lds);
     PARK_LAUNCH("metric_chol", k_metric_chol<128>, dim3(H), dim3(256), lds, st, G, alpha, eps,
                 s_min, Gbar, R, status);
   } else {
