@@ -37,6 +37,13 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches only (no HIP graph replay)")
+    ap.add_argument("--reuse", default="recompute", choices=["recompute", "clusters", "mask"],
+                    help="recompute everything, or time the next diffusion step (Q, K drifted by "
+                         "N(0, 0.05^2)) reusing the clustering (and the mask)")
+    ap.add_argument("--topp", type=float, default=None, help="override: top-p selection mass")
+    ap.add_argument("--ratio", type=float, default=None, help="override: top-k ratio")
+    ap.add_argument("--block", type=int, default=None, help="override: mean block size B")
+    ap.add_argument("--iters", type=int, default=None, help="override: k-means iterations T")
     ap.add_argument("--cpu-heads", type=int, default=4,
                     help="heads of the layer the oracle runs for the CPU baseline")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -133,10 +140,16 @@ def kernel_work(name, cfg, st, C):
                     tot += nq[u] * nk[kvi[h, u, :kvc[h, u]]].sum()
         peak = "mfma_bf16" if name == "attn_mfma" else "alu_f32"
         return ("mfma" if name == "attn_mfma" else "alu"), 4.0 * d * tot, "flop", peak
-    if name == "gather_rows":
-        return "hbm", 2.0 * N * d * eb * H, "byte", "hbm"
-    if name == "segment_mean":
-        return "hbm", 1.0 * N * d * eb * H + C * d * 8 * H, "byte", "hbm"
+    if name == "gather_rows":  # one of the three gathers: rows read and written, perm read
+        return "hbm", (2.0 * N * d * eb + 4.0 * N) * H, "byte", "hbm"
+    if name == "segment_mean":  # rows read through perm, float64 means written
+        return "hbm", (1.0 * N * d * eb + 4.0 * N + C * d * 8.0) * H, "byte", "hbm"
+    if name == "sort_hist":
+        return "hbm", 4.0 * N * H, "byte", "hbm"
+    if name == "sort_scatter":
+        return "hbm", 8.0 * N * H, "byte", "hbm"
+    if name == "select_fast":  # the float W^ rows and their error bounds
+        return "hbm", 4.0 * C * C * H, "byte", "hbm"
     return None
 
 
@@ -177,19 +190,43 @@ def main():
     from paper_2609_38978_amd import synth
 
     cfg = synth.CONFIGS[args.workload]
+    over = {}
+    if args.topp is not None:
+        over.update(select="topp", topp=args.topp)
+    if args.ratio is not None:
+        over.update(select="topk", ratio=args.ratio)
+    if args.block is not None:
+        over["block"] = args.block
+    if args.iters is not None:
+        over["iters"] = args.iters
+    cfg = cfg.with_(**over)
     q, k, v = synth.make_layer(cfg)
     tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     Q, K, V = (torch.from_numpy(a).to(tdt).cuda() for a in (q, k, v))
     C = cfg.C
     mode = cfg.select
     param = cfg.ratio if mode == "topk" else cfg.topp
+    reuse = {"recompute": P.PARK_RECOMPUTE, "clusters": P.PARK_REUSE_CLUSTERS,
+             "mask": P.PARK_REUSE_CLUSTERS_AND_MASK}[args.reuse]
     prm = P.make_params(C, C, T=cfg.iters, select=mode, ratio=param, topp=param, seed=0,
                         out_dtype=P.PARK_BF16 if cfg.dtype == "bf16" else P.PARK_F32)
     ws = P.workspace(Q, C, C)
     st = P.make_state(Q, C, C)
     out = torch.empty(Q.shape, dtype=tdt, device="cuda")
-    for _ in range(args.warmup):
+    if reuse != P.PARK_RECOMPUTE:
+        # this step's clustering/mask come from the previous step (Q, K); the
+        # timed calls run on the drifted Q2, K2
         P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
+        q2, k2 = synth.perturb_layer(cfg, q, k)
+        Q = torch.from_numpy(q2).to(tdt).cuda()
+        K = torch.from_numpy(k2).to(tdt).cuda()
+        del q2, k2
+
+    def fwd():
+        P.park_forward(Q, K, V, prm, reuse=reuse, state=st, out=out, ws=ws)
+
+    for _ in range(args.warmup):
+        fwd()
     P.park_check(ws)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -199,7 +236,7 @@ def main():
     t0 = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
+        fwd()
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -212,7 +249,7 @@ def main():
     if not args.no_graph:
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
+            fwd()
         graph.replay()
         torch.cuda.synchronize()
         gs = torch.cuda.current_stream()
@@ -230,7 +267,7 @@ def main():
     P.park_profile_reset()
     P.park_profile_enable(True)
     for _ in range(args.steps):
-        P.park_forward(Q, K, V, prm, state=st, out=out, ws=ws)
+        fwd()
     torch.cuda.synchronize()
     P.park_profile_enable(False)
     prof = P.park_profile_read()
@@ -240,6 +277,17 @@ def main():
     # per-kernel share and roofline of the dominant kernel
     stages = {n: {"ms_per_step": round(r["ms"] / args.steps, 4),
                   "launches_per_step": r["launches"] // args.steps} for n, r in prof.items()}
+    stage_roof = {}
+    for n, r in prof.items():
+        wk = kernel_work(n, cfg, st, C)
+        if wk is None or not r["launches"]:
+            continue
+        b_, amt, unit_, pk_ = wk
+        a_ms = r["ms"] / r["launches"]
+        rate = amt / (a_ms * 1e-3) / (1e12 if unit_ == "flop" else 1e9)
+        stage_roof[n] = {"bound": b_, "achieved": round(rate, 3),
+                         "unit": "TFLOP/s" if unit_ == "flop" else "GB/s",
+                         "frac": round(rate / PEAK[pk_], 4)}
     dom = max(prof, key=lambda n: prof[n]["ms"])
     avg_ms = prof[dom]["ms"] / prof[dom]["launches"]
     work = kernel_work(dom, cfg, st, C)
@@ -264,13 +312,15 @@ def main():
            "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
            "data": "synthetic (seeded clustered-Gaussian DiT-shaped Q/K/V)",
            "config": {"workload": f"{cfg.name}: H={cfg.H} N={cfg.N} d={cfg.d} {cfg.dtype} "
-                                  f"C={C} T={cfg.iters} {mode} {param}",
-                      "H": cfg.H, "N": cfg.N, "d": cfg.d, "C": C, "T": cfg.iters,
-                      "select": mode, "param": param},
+                                  f"B={cfg.block} C={C} T={cfg.iters} {mode} {param}"
+                                  + ("" if reuse == P.PARK_RECOMPUTE else f" reuse={args.reuse}"),
+                      "H": cfg.H, "N": cfg.N, "d": cfg.d, "B": cfg.block, "C": C, "T": cfg.iters,
+                      "select": mode, "param": param, "reuse": args.reuse},
            "dense_equiv_tflops": round(dense_flops / (ms * 1e-3) / 1e12, 3),
            "timing": "eager park_forward calls, events on the launch stream",
            "graph_ms_per_step": None if ms_graph is None else round(ms_graph, 4),
-           "wall_s": round(wall, 3), "stages": stages, "roofline": roof}
+           "wall_s": round(wall, 3), "stages": stages, "stage_roofline": stage_roof,
+           "roofline": roof}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, q, k, v, min(args.cpu_heads, cfg.H))
     print(json.dumps(res), flush=True)

@@ -156,3 +156,18 @@ def perturb_head(cfg: LayerConfig, h: int, q: np.ndarray, k: np.ndarray, sigma: 
         q2, k2 = bf16_round(q2), bf16_round(k2)
     return q2.astype(np.float32), k2.astype(np.float32)
 
+
+def perturb_layer(cfg: LayerConfig, q: np.ndarray, k: np.ndarray, heads=None, workers: int = 8):
+    """perturb_head over the stacked ``[H', N, d]`` Q and K (threads over heads)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    heads = list(range(q.shape[0]) if heads is None else heads)
+    q2, k2 = np.empty_like(q), np.empty_like(k)
+
+    def one(i):
+        q2[i], k2[i] = perturb_head(cfg, heads[i], q[i], k[i])
+
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(one, range(len(heads))))
+    return q2, k2
+
