@@ -322,7 +322,8 @@ template <int D>
 __global__ __launch_bounds__(256) void k_cen_prep(const float* __restrict__ cen,
                                                   const int* __restrict__ k_sizes, int CK,
                                                   bf16_t* __restrict__ c3, size_t plane,
-                                                  float* __restrict__ lg, float* __restrict__ cn,
+                                                  float* __restrict__ lg, int CKpad,
+                                                  float* __restrict__ cn,
                                                   float* __restrict__ bmax) {
   constexpr int CB = 16, TPC = 256 / CB, EPT = D / TPC;
   __shared__ float part[CB][TPC];
@@ -356,10 +357,12 @@ __global__ __launch_bounds__(256) void k_cen_prep(const float* __restrict__ cen,
       const int n = k_sizes[(size_t)h * CK + vv];
       const float l = n > 0 ? (float)log((double)n) : -INFINITY;
       cn[(size_t)h * CK + vv] = fn;
-      lg[(size_t)h * CK + vv] = l;
+      lg[(size_t)h * CKpad + vv] = l;
       fl = n > 0 ? fabsf(l) : 0.0f;
     }
   }
+  if (blockIdx.x == gridDim.x - 1)  // padding blocks: never scored
+    for (int vv = CK + tid; vv < CKpad; vv += 256) lg[(size_t)h * CKpad + vv] = -INFINITY;
   if (tid < 64) {
     for (int o = 8; o > 0; o >>= 1) {
       fn = fmaxf(fn, __shfl_xor(fn, o, 64));
@@ -372,29 +375,54 @@ __global__ __launch_bounds__(256) void k_cen_prep(const float* __restrict__ cen,
   }
 }
 
+// One wave-wide LDS DMA (lane l's 16 bytes at g land at LDS byte lds + 16 l),
+// as inline assembly so that the compiler does not drain every DMA in flight
+// before each LDS read; completion is waited for explicitly.
+__device__ __forceinline__ void pm_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t pm_lds_addr(const void* p) {
+  return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+template <int D>
+__device__ __forceinline__ int pm_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+
+// Workgroup = one (query block, head); the block's rows in chunks of 64
+// (4 wavefronts x 16 queries), each chunk streaming the key-block centroids
+// twice (normaliser pass, probability pass).  Centroid tiles of 32 rows of
+// the three parts (and their log n_v) go from HBM to a two-slot LDS ring by
+// LDS DMA, the next tile in flight while this one is scored; rows are
+// swizzled in 16-byte chunks so the B-operand reads are free of bank
+// conflicts.  The (query block, head) items of a head run on one XCD.
+// Online normaliser with one exp2 per logit: for d = S - m (m the running
+// maximum), z += 2^d when d <= 0, else z = z 2^-d + 1 and m = S.
 template <int D>
 __global__ __launch_bounds__(256) void k_pama_fast(const bf16_t* __restrict__ Qp,
                                                    const int* __restrict__ q_offsets,
                                                    const bf16_t* __restrict__ c3, size_t plane,
-                                                   const float* __restrict__ lg,
-                                                   const float* __restrict__ bmax, int nbm, int N,
-                                                   int CQ, int CK, float* __restrict__ W32,
+                                                   const float* __restrict__ lg, int CKpad,
+                                                   const float* __restrict__ bmax, int nbm, int H,
+                                                   int N, int CQ, int CK, float* __restrict__ W32,
                                                    float* __restrict__ delta) {
-  constexpr int CT = 64, KS = D / 32, CROW = D + 8, CH = D / 8;
-  constexpr int NL = CT * CH / 256;
+  constexpr int CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
+  constexpr int NI = 3 * CT / (4 * RPI);  // DMAs per wavefront and tile
+  static_assert(NI * 4 * RPI == 3 * CT, "tile shape");
   constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f, L2E = 1.4426950408889634f;
   constexpr float ET = U24 * 1.01f + (32.0f * DEL + (KS - 1) * U24) * 1.01f +
                        0.00390625f * 1.01f * (2 * D) * DEL + U24 * 1.01f;
-  __shared__ __attribute__((aligned(16))) bf16_t C1[CT * CROW];
-  __shared__ __attribute__((aligned(16))) bf16_t C2[CT * CROW];
-  __shared__ __attribute__((aligned(16))) bf16_t C3[CT * CROW];
-  __shared__ float lgs[CT];
-  __shared__ float wacc[4][MAXC];
+  __shared__ __attribute__((aligned(16))) bf16_t Ct[2][3 * CT * D];  // [slot][part][row][D]
+  __shared__ __attribute__((aligned(16))) float Lt[2][CT];
+  extern __shared__ float wacc[];  // [4][CK]
   __shared__ float qn_s[4][16];
   __shared__ float red[4];
   __shared__ float mx_s[2];
-  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x, w = tid >> 6, l = tid & 63,
-            g = l >> 4, c16 = l & 15;
+  const int nitems = CQ * H, per = (nitems + 7) >> 3;
+  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (item >= nitems) return;
+  const int h = item / CQ, u = item - h * CQ;
+  const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int* off = q_offsets + (size_t)h * (CQ + 1);
   const int q0 = min(max(off[u], 0), N), q1 = min(max(off[u + 1], q0), N);
   const int nu = q1 - q0;
@@ -419,129 +447,135 @@ __global__ __launch_bounds__(256) void k_pama_fast(const bf16_t* __restrict__ Qp
       mx_s[1] = c;
     }
   }
-  for (int v = tid; v < 4 * MAXC; v += 256) (&wacc[0][0])[v] = 0.0f;
-  __syncthreads();
-  const float cmax = mx_s[0], lgmax = mx_s[1];
+  for (int v = tid; v < 4 * CK; v += 256) wacc[v] = 0.0f;
   const float isd = 1.0f / sqrtf((float)D);
   const bf16_t* P1 = c3 + (size_t)h * CK * D;
-  const bf16_t* P2 = P1 + plane;
-  const bf16_t* P3 = P2 + plane;
-  const float* lgh = lg + (size_t)h * CK;
+  const float* lgh = lg + (size_t)h * CKpad;
   const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
   float dmax = 0.0f;  // per-thread max of the row error bound
 
-  for (int r0 = q0; r0 < q1; r0 += 64) {
-    // A operand: this wavefront's 16 queries (query c16, dims 32s + 8g ..)
-    const int qa = r0 + 16 * w + c16;
-    bf16x8_t qf[KS];
-    float qsq = 0.0f;
+  const int pch = l % CPR;
+  const int nt = (CK + CT - 1) / CT;
+  auto issue = [&](int tile, int slot) {
+    const int c0 = tile * CT;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-      if (qa < q1) raw = *(const uint4*)(Qp + ((size_t)h * N + qa) * D + 32 * s + 8 * g);
-      qf[s] = __builtin_bit_cast(bf16x8_t, raw);
-      const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
+    for (int i = 0; i < NI; ++i) {
+      const int row = (w * NI + i) * RPI + l / CPR;
+      const int part = row / CT, r = row % CT;
+      const int v = min(c0 + r, CK - 1);
+      const bf16_t* src = P1 + part * plane + (size_t)v * D + 8 * (pch ^ pm_swz<D>(r));
+      pm_dma16(src, pm_lds_addr(&Ct[slot][0] + (w * NI + i) * 512));
+    }
+    if (w == 0 && l < CT / 4) pm_dma16(lgh + c0 + 4 * l, pm_lds_addr(&Lt[slot][0]));
+  };
+
+  const int nch = (nu + 63) / 64;
+  const int total = nch * 2 * nt;
+  bf16x8_t qf[KS];
+  bool rv[4];
+  float m[4], z[4], mf[4], iz[4];
+  issue(0, 0);
+  const int swc = pm_swz<D>(c16);
+  for (int it = 0; it < total; ++it) {
+    const int tile = it % nt, pass = (it / nt) & 1, r0 = q0 + 64 * (it / (2 * nt));
+    if (tile == 0 && pass == 0) {
+      // A operand: this wavefront's 16 queries of the chunk (query c16, dims 32s + 8g ..)
+      const int qa = r0 + 16 * w + c16;
+      float qsq = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
-        qsq = fmaf(lo, lo, fmaf(hi, hi, qsq));
+      for (int s = 0; s < KS; ++s) {
+        uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+        if (qa < q1) raw = *(const uint4*)(Qp + ((size_t)h * N + qa) * D + 32 * s + 8 * g);
+        qf[s] = __builtin_bit_cast(bf16x8_t, raw);
+        asm volatile("" ::"v"(qf[s]));  // loads complete here, not inside the tile loop
+        const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
+          qsq = fmaf(lo, lo, fmaf(hi, hi, qsq));
+        }
+      }
+      qsq += __shfl_xor(qsq, 16, 64);
+      qsq += __shfl_xor(qsq, 32, 64);
+      if (g == 0) qn_s[w][c16] = sqrtf(qsq) * 1.0001f;
+      // outputs: lane holds queries 4g + r (r = 0..3) of this wavefront
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        rv[r] = r0 + 16 * w + 4 * g + r < q1;
+        m[r] = -INFINITY;
+        z[r] = 0.0f;
       }
     }
-    qsq += __shfl_xor(qsq, 16, 64);
-    qsq += __shfl_xor(qsq, 32, 64);
-    if (g == 0) qn_s[w][c16] = sqrtf(qsq) * 1.0001f;
-    // outputs: lane holds queries 4g + r (r = 0..3) of this wavefront
-    bool rv[4];
+    if (tile == 0 && pass == 1) {
+      // merge (max, sum) over the 16 lanes holding the same queries
 #pragma unroll
-    for (int r = 0; r < 4; ++r) rv[r] = r0 + 16 * w + 4 * g + r < q1;
-    float m[4], z[4];
+      for (int r = 0; r < 4; ++r) {
+        float mm = m[r], zz = z[r];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      m[r] = -INFINITY;
-      z[r] = 0.0f;
+        for (int o = 1; o < 16; o <<= 1) {
+          const float om = __shfl_xor(mm, o, 64), oz = __shfl_xor(zz, o, 64);
+          const float nm = fmaxf(mm, om);
+          zz = (nm == -INFINITY) ? 0.0f
+                                 : zz * __builtin_amdgcn_exp2f((mm - nm) * L2E) +
+                                       oz * __builtin_amdgcn_exp2f((om - nm) * L2E);
+          mm = nm;
+        }
+        mf[r] = mm;
+        iz[r] = zz > 0.0f ? 1.0f / zz : 0.0f;
+      }
     }
-    for (int pass = 0; pass < 2; ++pass) {
-      float mf[4], iz[4];
-      if (pass == 1) {
-        // merge (max, sum) over the 16 lanes holding the same queries
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // tile landed everywhere; previous tile consumed (its slot is free)
+    if (it + 1 < total) issue((it + 1) % nt, (it + 1) & 1);
+    const bf16_t* B1 = &Ct[it & 1][0];
+    const bf16_t* B2 = B1 + CT * D;
+    const bf16_t* B3 = B2 + CT * D;
+    const int c0 = tile * CT;
+#pragma unroll
+    for (int cb = 0; cb < CT / 16; ++cb) {
+      f32x4_t shi = zero, srest = zero;
+      const int rowo = (16 * cb + c16) * D;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const int co = rowo + 8 * ((4 * s + g) ^ swc);
+        const bf16x8_t b1 = *(const bf16x8_t*)(B1 + co);
+        const bf16x8_t b2 = *(const bf16x8_t*)(B2 + co);
+        const bf16x8_t b3 = *(const bf16x8_t*)(B3 + co);
+        shi += __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b1, zero, 0, 0, 0);
+        srest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b2, srest, 0, 0, 0);
+        srest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b3, srest, 0, 0, 0);
+      }
+      const float lgv = Lt[it & 1][16 * cb + c16];  // this lane's centroid
+      if (pass == 0) {
+        if (lgv != -INFINITY) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float sv = fmaf(shi[r] + srest[r], isd, lgv);
+            const float d = sv - m[r];  // +inf while m = -inf
+            const float e = __builtin_amdgcn_exp2f(-fabsf(d) * L2E);
+            z[r] = d <= 0.0f ? z[r] + e : fmaf(z[r], e, 1.0f);
+            m[r] = fmaxf(m[r], sv);
+          }
+        }
+      } else {
+        float cs = 0.0f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          float mm = m[r], zz = z[r];
-#pragma unroll
-          for (int o = 1; o < 16; o <<= 1) {
-            const float om = __shfl_xor(mm, o, 64), oz = __shfl_xor(zz, o, 64);
-            const float nm = fmaxf(mm, om);
-            zz = (nm == -INFINITY) ? 0.0f
-                                   : zz * __builtin_amdgcn_exp2f((mm - nm) * L2E) +
-                                         oz * __builtin_amdgcn_exp2f((om - nm) * L2E);
-            mm = nm;
-          }
-          mf[r] = mm;
-          iz[r] = zz > 0.0f ? 1.0f / zz : 0.0f;
+          const float sv = fmaf(shi[r] + srest[r], isd, lgv);
+          const float p = (rv[r] && sv != -INFINITY)
+                              ? __builtin_amdgcn_exp2f((sv - mf[r]) * L2E) * iz[r]
+                              : 0.0f;
+          cs += p;
         }
-      }
-      for (int c0 = 0; c0 < CK; c0 += CT) {
-        __syncthreads();
-        for (int e = tid; e < CT * CH; e += 256) {
-          const int rr = e / CH, ch = e % CH;
-          uint4 v1 = make_uint4(0u, 0u, 0u, 0u), v2 = v1, v3 = v1;
-          if (c0 + rr < CK) {
-            const size_t o = (size_t)(c0 + rr) * D + 8 * ch;
-            v1 = *(const uint4*)(P1 + o);
-            v2 = *(const uint4*)(P2 + o);
-            v3 = *(const uint4*)(P3 + o);
-          }
-          *(uint4*)(C1 + rr * CROW + 8 * ch) = v1;
-          *(uint4*)(C2 + rr * CROW + 8 * ch) = v2;
-          *(uint4*)(C3 + rr * CROW + 8 * ch) = v3;
-        }
-        if (tid < CT) lgs[tid] = (c0 + tid < CK) ? lgh[c0 + tid] : -INFINITY;
-        __syncthreads();
-#pragma unroll
-        for (int cb = 0; cb < CT / 16; ++cb) {
-          f32x4_t shi = zero, srest = zero;
-          const int rowo = (16 * cb + c16) * CROW + 8 * g;
-#pragma unroll
-          for (int s = 0; s < KS; ++s) {
-            const bf16x8_t b1 = *(const bf16x8_t*)(C1 + rowo + 32 * s);
-            const bf16x8_t b2 = *(const bf16x8_t*)(C2 + rowo + 32 * s);
-            const bf16x8_t b3 = *(const bf16x8_t*)(C3 + rowo + 32 * s);
-            shi += __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b1, zero, 0, 0, 0);
-            srest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b2, srest, 0, 0, 0);
-            srest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b3, srest, 0, 0, 0);
-          }
-          const float lgv = lgs[16 * cb + c16];  // this lane's centroid
-          if (pass == 0) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float sv = fmaf(shi[r] + srest[r], isd, lgv);
-              if (sv != -INFINITY) {
-                const float nm = fmaxf(m[r], sv);
-                z[r] = z[r] * __builtin_amdgcn_exp2f((m[r] - nm) * L2E) +
-                       __builtin_amdgcn_exp2f((sv - nm) * L2E);
-                m[r] = nm;
-              }
-            }
-          } else {
-            float cs = 0.0f;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float sv = fmaf(shi[r] + srest[r], isd, lgv);
-              const float p = (rv[r] && sv != -INFINITY)
-                                  ? __builtin_amdgcn_exp2f((sv - mf[r]) * L2E) * iz[r]
-                                  : 0.0f;
-              cs += p;
-            }
-            cs += __shfl_xor(cs, 16, 64);
-            cs += __shfl_xor(cs, 32, 64);
-            const int v = c0 + 16 * cb + c16;
-            if (g == 0 && v < CK) wacc[w][v] += cs;
-          }
-        }
+        cs += __shfl_xor(cs, 16, 64);
+        cs += __shfl_xor(cs, 32, 64);
+        const int v = c0 + 16 * cb + c16;
+        if (g == 0 && v < CK) wacc[w * CK + v] += cs;
       }
     }
-    // row error bound for this wavefront's queries (lane holds query c16's norm)
-    {
+    if (pass == 1 && tile == nt - 1) {
+      // row error bound for this wavefront's queries (lane holds query c16's norm)
+      const float cmax = mx_s[0], lgmax = mx_s[1];
       const float qn = (16 * w + c16 + r0 < q1) ? qn_s[w][c16] : 0.0f;
       const float ei = isd * (ET + 1.01f * U24) * qn * cmax +
                        1.01f * U24 * (2.0f * lgmax + 1.01f * isd * qn * cmax);
@@ -558,7 +592,7 @@ __global__ __launch_bounds__(256) void k_pama_fast(const bf16_t* __restrict__ Qp
   __syncthreads();
   const float inv_n = 1.0f / (float)nu;
   for (int v = tid; v < CK; v += 256)
-    W32[wrow + v] = (((wacc[0][v] + wacc[1][v]) + wacc[2][v]) + wacc[3][v]) * inv_n;
+    W32[wrow + v] = (((wacc[v] + wacc[CK + v]) + wacc[2 * CK + v]) + wacc[3 * CK + v]) * inv_n;
   for (int o = 32; o > 0; o >>= 1) dmax = fmaxf(dmax, __shfl_xor(dmax, o, 64));
   if (l == 0) red[w] = dmax;
   __syncthreads();
@@ -719,18 +753,30 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   const size_t plane = (size_t)H * CK * D;
   const int nbm = (CK + 15) / 16;
   float* W32 = W_out ? W_out : rb.W32;
+  const int CKpad = pama_ckpad(CK);
+  const unsigned nwg = 8u * (((unsigned)CQ * (unsigned)H + 7u) / 8u);  // XCD remap: every item owns one
+  const size_t lds = (size_t)4 * CK * sizeof(float);
+  // reserved once for the largest CK (2048), outside any stream capture that may follow
+  static const hipError_t attr128 = hipFuncSetAttribute(
+      (const void*)k_pama_fast<128>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)(4 * MAXC * sizeof(float)));
+  static const hipError_t attr64 = hipFuncSetAttribute(
+      (const void*)k_pama_fast<64>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)(4 * MAXC * sizeof(float)));
+  if (attr128 != hipSuccess || attr64 != hipSuccess)
+    return fail(PARK_ERR_HIP, "retrieval: cannot reserve %zu bytes of LDS", lds);
   if (D == 128) {
     PARK_LAUNCH("pama_cen_prep", k_cen_prep<128>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
-                rb.c3, plane, rb.lg, rb.cn, rb.bmax);
-    PARK_LAUNCH("pama_fast", k_pama_fast<128>, dim3(CQ, H), dim3(256), 0, st, (const bf16_t*)Qp,
-                q_offsets, (const bf16_t*)rb.c3, plane, (const float*)rb.lg,
-                (const float*)rb.bmax, nbm, N, CQ, CK, W32, rb.delta);
+                rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
+    PARK_LAUNCH("pama_fast", k_pama_fast<128>, dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
+                q_offsets, (const bf16_t*)rb.c3, plane, (const float*)rb.lg, CKpad,
+                (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
   } else {
     PARK_LAUNCH("pama_cen_prep", k_cen_prep<64>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
-                rb.c3, plane, rb.lg, rb.cn, rb.bmax);
-    PARK_LAUNCH("pama_fast", k_pama_fast<64>, dim3(CQ, H), dim3(256), 0, st, (const bf16_t*)Qp,
-                q_offsets, (const bf16_t*)rb.c3, plane, (const float*)rb.lg,
-                (const float*)rb.bmax, nbm, N, CQ, CK, W32, rb.delta);
+                rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
+    PARK_LAUNCH("pama_fast", k_pama_fast<64>, dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
+                q_offsets, (const bf16_t*)rb.c3, plane, (const float*)rb.lg, CKpad,
+                (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
   }
   PARK_LAUNCH("pama_reset", k_zero_counts, dim3((H + 63) / 64), dim3(64), 0, st, rb.nrows, H);
   PARK_LAUNCH("select_fast", k_select_fast, dim3(CQ, H), dim3(256), 0, st, (const float*)W32,

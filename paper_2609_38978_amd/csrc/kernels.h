@@ -25,6 +25,9 @@ park_status launch_gather(const void* X, const int* perm, int H, int N, int D, i
 // centroid count padded to the fast assignment's tile multiple
 inline int kmeans_cpad(int C) { return (C + 63) / 64 * 64; }
 
+// key-block count padded to the fast retrieval's tile multiple
+inline int pama_ckpad(int CK) { return (CK + 63) / 64 * 64; }
+
 struct KmeansBufs {
   int* init;      // [H][C]
   double* mu;     // [H][C][D] centroids in the input space
@@ -60,7 +63,7 @@ struct RetrieveBufs {
   int* rows;      // [H][CQ]     rows left for the float64 path
   int* nrows;     // [H]
   bf16_t* c3;     // [3][H][CK][D] centroids as three bf16 parts
-  float* lg;      // [H][CK]     log n_v (-inf for empty blocks)
+  float* lg;      // [H][pama_ckpad(CK)] log n_v (-inf for empty and padding blocks)
   float* cn;      // [H][CK]     |c_v|
   float* bmax;    // [H][ceil(CK/16)][2] per-block max |c_v|, |log n_v|
 };

@@ -171,7 +171,7 @@ static RetrieveBufs carve_retrieve(Carver& cv, int H, int D, int CQ, int CK) {
   r.rows = cv.take<int>((size_t)H * CQ);
   r.nrows = cv.take<int>((size_t)H);
   r.c3 = cv.take<bf16_t>((size_t)3 * H * CK * D);
-  r.lg = cv.take<float>((size_t)H * CK);
+  r.lg = cv.take<float>((size_t)H * pama_ckpad(CK));
   r.cn = cv.take<float>((size_t)H * CK);
   r.bmax = cv.take<float>((size_t)2 * H * ((CK + 15) / 16));
   return r;
