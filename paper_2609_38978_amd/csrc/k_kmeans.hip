@@ -96,7 +96,7 @@ template <int D>
 __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
                                               const double* __restrict__ Gbar, int C,
                                               double* __restrict__ w, double* __restrict__ b,
-                                              double* __restrict__ wT, bf16_t* __restrict__ w3,
+                                              bf16_t* __restrict__ w3,
                                               size_t plane, float* __restrict__ b32, int Cpad,
                                               float* __restrict__ wn, float* __restrict__ eb,
                                               float* __restrict__ bmax, int* __restrict__ nflag) {
@@ -131,7 +131,6 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
     if (v0 + r < C) {
       const size_t o = ((size_t)h * C + v0 + r) * D + a;
       w[o] = acc[k];
-      if (wT) wT[((size_t)h * D + a) * C + v0 + r] = acc[k];
       if (w3) {
         // w = w1 + w2 + w3 + r with bf16 parts and |r| <= 2^-24 |w| (1 + 2^-7)
         const bf16_t p1 = f2bf((float)acc[k]);
@@ -157,12 +156,16 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
       fn = (float)(sqrt(n2) * (1.0 + 1e-6));
       fe = (float)(fabs(s) * (2.0 * 1.1 * 5.9604644775390625e-08) * (1.0 + 1e-6));
       b32[(size_t)h * Cpad + v0 + tid] = (float)s;
-      wn[(size_t)h * C + v0 + tid] = fn;
-      eb[(size_t)h * C + v0 + tid] = fe;
+      wn[(size_t)h * Cpad + v0 + tid] = fn;
+      eb[(size_t)h * Cpad + v0 + tid] = fe;
     }
   }
-  if (b32 && blockIdx.x == gridDim.x - 1)  // padding scores: never the minimum
-    for (int v = C + tid; v < Cpad; v += 256) b32[(size_t)h * Cpad + v] = INFINITY;
+  if (b32 && blockIdx.x == gridDim.x - 1)  // padding centroids: score +inf, no error term
+    for (int v = C + tid; v < Cpad; v += 256) {
+      b32[(size_t)h * Cpad + v] = INFINITY;
+      wn[(size_t)h * Cpad + v] = 0.0f;
+      eb[(size_t)h * Cpad + v] = 0.0f;
+    }
   if (b32 && tid < 64) {
     // this block's maxima of |w_v| and eb_v (reduced by the assignment)
     for (int o = 8; o > 0; o >>= 1) {
@@ -242,6 +245,7 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
                                                      int N, int C,
                                                      int* __restrict__ labels,
                                                      int* __restrict__ flags,
+                                                     float* __restrict__ flagu,
                                                      int* __restrict__ nflag) {
   constexpr int TB = 4, CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
   constexpr int NI = 3 * CT / (4 * RPI);  // DMAs per wavefront and tile
@@ -331,7 +335,7 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
     dot += __shfl_xor(dot, 32, 64);
     best[tb] = INFINITY;
     if (prev >= 0) {
-      const float e = fmaf(kx[tb], wn[(size_t)h * C + prev], eb[(size_t)h * C + prev]);
+      const float e = fmaf(kx[tb], wn[(size_t)h * Cpad + prev], eb[(size_t)h * Cpad + prev]);
       const float est = fmaf(-2.0f, dot, bh[prev]);
       best[tb] = est + 2.0f * e + 1e-6f * fabsf(est);
     }
@@ -441,94 +445,294 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
     const int tok = t0 + 16 * tb + c16;
     if (g == 0 && tok < N) {
       bool ok = false;
+      float ub = INFINITY;  // an upper bound of the smallest exact score
       if (bidx[tb] >= 0 && isfinite(best[tb])) {
         const int v = bidx[tb];
-        const float e1 = fmaf(kx[tb], wn[(size_t)h * C + v], eb[(size_t)h * C + v]);
+        const float e1 = fmaf(kx[tb], wn[(size_t)h * Cpad + v], eb[(size_t)h * Cpad + v]);
         const float emax = fmaf(kx[tb], nmax, ebmax) * 1.0001f;
-        ok = (L[tb] - emax) > (best[tb] + e1);
+        ub = best[tb] + e1;
+        ok = (L[tb] - emax) > ub;
       }
       if (ok) {
         labels[(size_t)h * N + tok] = bidx[tb];
       } else {
         const int slot = atomicAdd(nflag + h, 1);
         flags[(size_t)h * N + slot] = tok;
+        flagu[(size_t)h * N + slot] = ub;
       }
     }
   }
 }
 
-// Float64 assignment of the tokens the fast path could not certify: 16 listed
-// tokens per workgroup, the centroids split over the four wavefronts (one
-// centroid per lane, w read transposed so loads are coalesced), the exact
-// minimum (ties to the lowest id) reduced across lanes and wavefronts.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void k_refine(const T* __restrict__ X,
-                                                const double* __restrict__ wT,
-                                                const double* __restrict__ b, int N, int C,
-                                                const int* __restrict__ flags,
-                                                const int* __restrict__ nflag,
-                                                int* __restrict__ labels, int* status) {
-  constexpr int TT = 16;
-  __shared__ double xs[TT][D];
-  __shared__ double rs[4][TT];
-  __shared__ int ri[4][TT];
-  __shared__ int tok_s[TT];
-  const int h = blockIdx.y, tid = threadIdx.x, wv = tid >> 6, l = tid & 63;
+// Float64 assignment of the tokens the fast path could not certify.
+//
+// Every exact score lies in [s^_v - E_v, s^_v + E_v] (same fast scores and
+// bounds as the fast path), so with U the listed upper bound of the smallest
+// exact score, the exact argmin lies in the candidate set
+// {v : s^_v - E_v <= U}.  One sweep over the centroids (MFMA, as in the fast
+// path) collects each token's candidates in LDS; they are then scored in
+// float64 (b_v - 2 x.w_v, partial sums over 8 lanes added in a fixed tree)
+// and the minimum, ties to the lowest id, is the label.
+// Near-ties leave two or three candidates; a token with more than KMAX
+// (exact duplicates, degenerate data) is scored against every centroid.
+// Workgroups take chunks of 256 listed tokens (4 wavefronts x 4 x 16).
+template <int D>
+__global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ X,
+                                                     const bf16_t* __restrict__ w3, size_t plane,
+                                                     const float* __restrict__ b32,
+                                                     const float* __restrict__ wn,
+                                                     const float* __restrict__ eb, int Cpad,
+                                                     const double* __restrict__ w64,
+                                                     const double* __restrict__ b64, int H, int N,
+                                                     int C, int rg,
+                                                     const int* __restrict__ flags,
+                                                     const float* __restrict__ flagu,
+                                                     const int* __restrict__ nflag,
+                                                     int* __restrict__ labels, int* status) {
+  constexpr int TB = 4, CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
+  constexpr int NI = 3 * CT / (4 * RPI);
+  constexpr int KMAX = 4;            // candidates kept per token
+  constexpr int PL = 8, PE = D / PL;  // lanes per scored pair, elements per lane
+  constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f;
+  constexpr float ET = U24 * 1.01f + (D + 1) * DEL * 1.0079f + 0.00390625f * 1.01f * (2 * D + 1) * DEL +
+                       U24 * 1.01f;
+  constexpr float KXC = 1.1f * (2.0f * ET + 2.01f * U24) * 1.0001f;
+  __shared__ __attribute__((aligned(16))) bf16_t Wt[2][3 * CT * D];
+  __shared__ __attribute__((aligned(16))) float Bt[2][CT];
+  __shared__ __attribute__((aligned(16))) float Nt[2][CT];
+  __shared__ __attribute__((aligned(16))) float Et[2][CT];
+  __shared__ int ccount[256];
+  __shared__ int ctok[256];
+  __shared__ int cv[256 * KMAX];    // candidates by token slot
+  __shared__ double cs[256 * KMAX];  // float64 scores of the packed pairs
+  __shared__ int nover;
+  __shared__ int over[256];
+  __shared__ double xrow[D];
+  __shared__ double rbest[4];
+  __shared__ int ridx[4];
+  __shared__ int wsum[4];
+  __shared__ int poff[256];
+  __shared__ int ptl[256 * KMAX];
+  __shared__ int pv[256 * KMAX];
+  __shared__ int npairs;
+  __shared__ double obest[256];
+  __shared__ int oidx[256];
+  // XCD-aware: the workgroups of a head run on one XCD (its L2 holds the head's centroids)
+  const int nitems = H * rg, per = (nitems + 7) >> 3;
+  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (item >= nitems) return;
+  const int h = item / rg, wg = item - h * rg;
+  const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int cnt = min(nflag[h], N);
-  const double* wh = wT + (size_t)h * D * C;
-  const double* bh = b + (size_t)h * C;
-  const int cpw = ((C + 3) / 4 + 63) / 64 * 64;  // centroids per wavefront
-  const int v_begin = wv * cpw, v_end = min(C, v_begin + cpw);
-  for (int t0 = blockIdx.x * TT; t0 < cnt; t0 += gridDim.x * TT) {
-    __syncthreads();
-    if (tid < TT) {
-      const int tok = t0 + tid < cnt ? flags[(size_t)h * N + t0 + tid] : -1;
-      tok_s[tid] = ((unsigned)tok < (unsigned)N) ? tok : -1;
+  const int nchunks = (cnt + 255) / 256;
+  if (wg >= nchunks) return;
+  const bf16_t* Xh = X + (size_t)h * N * D;
+  const bf16_t* P1 = w3 + (size_t)h * C * D;
+  const float* bh = b32 + (size_t)h * Cpad;
+  const float* nh = wn + (size_t)h * Cpad;
+  const float* eh = eb + (size_t)h * Cpad;
+  const double* wh = w64 + (size_t)h * C * D;
+  const double* b64h = b64 + (size_t)h * C;
+  const int pch = l % CPR;
+  const int nt = (C + CT - 1) / CT;
+  auto issue = [&](int tile, int slot) {
+    const int c0 = tile * CT;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int row = (w * NI + i) * RPI + l / CPR;
+      const int part = row / CT, r = row % CT;
+      const int v = min(c0 + r, C - 1);
+      const bf16_t* src = P1 + part * plane + (size_t)v * D + 8 * (pch ^ km_swz<D>(r));
+      km_dma16(src, km_lds_addr(&Wt[slot][0] + (w * NI + i) * 512));
     }
-    __syncthreads();
-    for (int e = tid; e < TT * D; e += 256) {
-      const int t = e / D, a = e % D;
-      const int tok = tok_s[t];
-      xs[t][a] = tok >= 0 ? (double)to_f(X[((size_t)h * N + tok) * D + a]) : 0.0;
+    if (w == 0 && l < CT / 4) {
+      km_dma16(bh + c0 + 4 * l, km_lds_addr(&Bt[slot][0]));
+      km_dma16(nh + c0 + 4 * l, km_lds_addr(&Nt[slot][0]));
+      km_dma16(eh + c0 + 4 * l, km_lds_addr(&Et[slot][0]));
     }
-    __syncthreads();
-    double best[TT];
-    int bidx[TT];
+  };
+  const int swk = km_swz<D>(c16);
+  for (int chunk = wg; chunk < nchunks; chunk += rg) {
+    // this chunk's tokens: wavefront w, block tb, column c16 -> local id 64w + 16tb + c16
+    bf16x8_t xf[TB][KS];
+    float kx[TB], U[TB];
+    int tk[TB];
 #pragma unroll
-    for (int t = 0; t < TT; ++t) {
-      best[t] = INFINITY;
-      bidx[t] = 0x7fffffff;
-    }
-    for (int v0 = v_begin; v0 < v_end; v0 += 64) {
-      const int v = v0 + l;
-      if (v < v_end) {
-        double acc[TT];
+    for (int tb = 0; tb < TB; ++tb) {
+      const int idx = chunk * 256 + 64 * w + 16 * tb + c16;
+      int tok = idx < cnt ? flags[(size_t)h * N + idx] : -1;
+      tok = (unsigned)tok < (unsigned)N ? tok : -1;
+      tk[tb] = tok;
+      U[tb] = tok >= 0 ? flagu[(size_t)h * N + idx] : -INFINITY;
+      if (U[tb] != U[tb]) U[tb] = INFINITY;  // NaN: every centroid is a candidate
+      float xsq = 0.0f;
 #pragma unroll
-        for (int t = 0; t < TT; ++t) acc[t] = 0.0;
-        for (int a0 = 0; a0 < D; a0 += 16) {
-          double wa[16];
+      for (int s = 0; s < KS; ++s) {
+        uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+        if (tok >= 0) raw = *(const uint4*)(Xh + (size_t)tok * D + 32 * s + 8 * g);
+        xf[tb][s] = __builtin_bit_cast(bf16x8_t, raw);
+        asm volatile("" ::"v"(xf[tb][s]));  // loads complete here, not inside the tile loop
+        const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
-          for (int q = 0; q < 16; ++q) wa[q] = wh[(size_t)(a0 + q) * C + v];  // 16 loads in flight
-#pragma unroll
-          for (int q = 0; q < 16; ++q)
-#pragma unroll
-            for (int t = 0; t < TT; ++t) acc[t] = fma(xs[t][a0 + q], wa[q], acc[t]);
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
+          xsq = fmaf(lo, lo, fmaf(hi, hi, xsq));
         }
-        const double bv = bh[v];
+      }
+      xsq += __shfl_xor(xsq, 16, 64);
+      xsq += __shfl_xor(xsq, 32, 64);
+      kx[tb] = KXC * sqrtf(xsq);
+      asm volatile("" ::"v"(U[tb]));
+      if (g == 0) {
+        ccount[64 * w + 16 * tb + c16] = 0;
+        ctok[64 * w + 16 * tb + c16] = tok;
+      }
+    }
+    if (tid == 0) nover = 0;
+    issue(0, 0);
+    for (int t = 0; t < nt; ++t) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();  // tile t landed everywhere; tile t-1 consumed
+      if (t + 1 < nt) issue(t + 1, (t + 1) & 1);
+      const int slot = t & 1;
+      const bf16_t* W1 = &Wt[slot][0];
+      const bf16_t* W2 = W1 + CT * D;
+      const bf16_t* W3 = W2 + CT * D;
 #pragma unroll
-        for (int t = 0; t < TT; ++t) {
-          const double sc = fma(-2.0, acc[t], bv);
-          if (sc < best[t]) {
-            best[t] = sc;
-            bidx[t] = v;
+      for (int cb = 0; cb < CT / 16; ++cb) {
+        f32x4_t ahi[TB], arest[TB];
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          ahi[tb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+          arest[tb] = ahi[tb];
+        }
+        const int rowo = (16 * cb + c16) * D;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const int co = rowo + 8 * ((4 * s + g) ^ swk);
+          const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
+          const bf16x8_t a2 = *(const bf16x8_t*)(W2 + co);
+          const bf16x8_t a3 = *(const bf16x8_t*)(W3 + co);
+#pragma unroll
+          for (int tb = 0; tb < TB; ++tb) {
+            ahi[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[tb][s], ahi[tb], 0, 0, 0);
+            arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, xf[tb][s], arest[tb], 0, 0, 0);
+            arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
+          }
+        }
+        const int cl = 16 * cb + 4 * g;
+        const float4 b4 = *(const float4*)(&Bt[slot][cl]);
+        const float4 n4 = *(const float4*)(&Nt[slot][cl]);
+        const float4 e4 = *(const float4*)(&Et[slot][cl]);
+        const float bv[4] = {b4.x, b4.y, b4.z, b4.w}, nv[4] = {n4.x, n4.y, n4.z, n4.w},
+                    ev[4] = {e4.x, e4.y, e4.z, e4.w};
+        const int vb = t * CT + cl;
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          bool cand[4], anyc = false;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float sc = fmaf(-2.0f, ahi[tb][r] + arest[tb][r], bv[r]);
+            const float er = fmaf(kx[tb], nv[r], ev[r]);
+            cand[r] = vb + r < C && !(sc - er > U[tb]);
+            anyc |= cand[r];
+          }
+          if (__any(anyc)) {
+            const int tl = 64 * w + 16 * tb + c16;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (cand[r]) {
+                const int pos = atomicAdd(&ccount[tl], 1);
+                if (pos < KMAX) cv[tl * KMAX + pos] = vb + r;
+              }
           }
         }
       }
     }
+    __syncthreads();
+    // pack the pairs (token, candidate) of tokens with 1..KMAX candidates;
+    // list the others (more candidates) for the all-centroid pass
+    {
+      const int tl = tid;
+      const int nc = ccount[tl];
+      const bool packed = ctok[tl] >= 0 && nc >= 1 && nc <= KMAX;
+      const int np = packed ? nc : 0;
+      int inc = np;
 #pragma unroll
-    for (int t = 0; t < TT; ++t) {
-      double bb = best[t];
-      int bi = bidx[t];
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(inc, o, 64);
+        if (l >= o) inc += y;
+      }
+      if (l == 63) wsum[w] = inc;
+      if (ctok[tl] >= 0 && !packed) over[atomicAdd(&nover, 1)] = tl;
+      __syncthreads();
+      int pre = 0;
+      for (int q = 0; q < w; ++q) pre += wsum[q];
+      const int start = pre + inc - np;
+      poff[tl] = start;
+      for (int j = 0; j < np; ++j) {
+        ptl[start + j] = tl;
+        pv[start + j] = cv[tl * KMAX + j];
+      }
+      if (tid == 255) npairs = start + np;
+    }
+    __syncthreads();
+    // float64 scores of the packed pairs, PL lanes per pair (PE dimensions each)
+    {
+      const int lp = l / PL, sub = l % PL, np = npairs;
+      for (int base = 0; base < np; base += 64) {
+        double a[2];
+        int pp[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const int p = base + 32 * k + 8 * w + lp;
+          pp[k] = p < np ? p : -1;
+          a[k] = 0.0;
+          if (p < np) {
+            const int tok = ctok[ptl[p]];
+            const bf16_t* xr = Xh + (size_t)tok * D + sub * PE;
+            const double* wr = wh + (size_t)pv[p] * D + sub * PE;
+#pragma unroll
+            for (int e0 = 0; e0 < PE; e0 += 8) {
+              const uint4 xu = *(const uint4*)(xr + e0);
+              const uint32_t q[4] = {xu.x, xu.y, xu.z, xu.w};
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                a[k] = fma((double)__uint_as_float(q[e] << 16), wr[e0 + 2 * e], a[k]);
+                a[k] = fma((double)__uint_as_float(q[e] & 0xffff0000u), wr[e0 + 2 * e + 1], a[k]);
+              }
+            }
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          double t = a[k];
+#pragma unroll
+          for (int o = PL / 2; o > 0; o >>= 1) t += __shfl_xor(t, o, 64);
+          if (sub == 0 && pp[k] >= 0) cs[pp[k]] = fma(-2.0, t, b64h[pv[pp[k]]]);
+        }
+      }
+    }
+    __syncthreads();
+    // tokens with too many candidates: float64 scores of every centroid
+    for (int i = 0; i < nover; ++i) {
+      const int tl = over[i], tok = ctok[tl];
+      for (int a0 = tid; a0 < D; a0 += 256) xrow[a0] = (double)to_f(Xh[(size_t)tok * D + a0]);
+      __syncthreads();
+      double bb = INFINITY;
+      int bi = 0x7fffffff;
+      for (int v = tid; v < C; v += 256) {
+        const double* wr = wh + (size_t)v * D;
+        double acc = 0.0;
+        for (int a0 = 0; a0 < D; ++a0) acc = fma(xrow[a0], wr[a0], acc);
+        const double sc = fma(-2.0, acc, b64h[v]);
+        if (sc < bb) {
+          bb = sc;
+          bi = v;
+        }
+      }
+#pragma unroll
       for (int o = 32; o > 0; o >>= 1) {
         const double ob = __shfl_xor(bb, o, 64);
         const int oi = __shfl_xor(bi, o, 64);
@@ -538,25 +742,51 @@ __global__ __launch_bounds__(256) void k_refine(const T* __restrict__ X,
         }
       }
       if (l == 0) {
-        rs[wv][t] = bb;
-        ri[wv][t] = bi;
+        rbest[w] = bb;
+        ridx[w] = bi;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        for (int q = 1; q < 4; ++q)
+          if (rbest[q] < rbest[0] || (rbest[q] == rbest[0] && ridx[q] < ridx[0])) {
+            rbest[0] = rbest[q];
+            ridx[0] = ridx[q];
+          }
+        obest[tl] = rbest[0];
+        oidx[tl] = ridx[0];
+      }
+      __syncthreads();
+    }
+    // labels: the smallest float64 score, ties to the lowest id
+    {
+      const int tl = tid, tok = ctok[tl], nc = ccount[tl];
+      if (tok >= 0) {
+        double bb;
+        int bi;
+        if (nc >= 1 && nc <= KMAX) {
+          bb = INFINITY;
+          bi = 0x7fffffff;
+          for (int j = 0; j < nc; ++j) {
+            const int p = poff[tl] + j;
+            const double sc = cs[p];
+            const int v = pv[p];
+            if (sc < bb || (sc == bb && v < bi)) {
+              bb = sc;
+              bi = v;
+            }
+          }
+        } else {
+          bb = obest[tl];
+          bi = oidx[tl];
+        }
+        if (!isfinite(bb) || (unsigned)bi >= (unsigned)C) {
+          raise_status(status, ST_NONFINITE);
+          bi = 0;
+        }
+        labels[(size_t)h * N + tok] = bi;
       }
     }
     __syncthreads();
-    if (tid < TT && tok_s[tid] >= 0) {
-      double bb = rs[0][tid];
-      int bi = ri[0][tid];
-      for (int q = 1; q < 4; ++q)
-        if (rs[q][tid] < bb || (rs[q][tid] == bb && ri[q][tid] < bi)) {
-          bb = rs[q][tid];
-          bi = ri[q][tid];
-        }
-      if (!isfinite(bb) || bi >= C) {
-        raise_status(status, ST_NONFINITE);
-        bi = 0;
-      }
-      labels[(size_t)h * N + tok_s[tid]] = bi;
-    }
   }
 }
 
@@ -760,26 +990,27 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
   PARK_LAUNCH("kmeans_init", k_init_idx, dim3(H), dim3(1024), 0, st, N, C, seed, side, kb.init);
   PARK_LAUNCH("kmeans_seed", k_seed_centroids<T>, dim3(C, H), dim3(D), 0, st, X,
               (const int*)kb.init, N, D, C, kb.mu);
-  // refine grid: persistent workgroups per head looping over 16-token tiles
-  int rg = (2048 + H - 1) / H;
-  const int max_tiles = (N + 15) / 16;
+  // refine grid: persistent workgroups per head looping over 256-token chunks
+  int rg = (1024 + H - 1) / H;
+  const int max_tiles = (N + 255) / 256;
   rg = rg < 2 ? 2 : rg;
   rg = rg > max_tiles ? max_tiles : rg;
   for (int t = 0; t < T_; ++t) {
     const int nbm = (C + 15) / 16;
     PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3(nbm, H), dim3(256), 0, st,
-                (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.wT : nullptr,
-                fast ? kb.w3 : nullptr, plane, fast ? kb.b32 : nullptr, kmeans_cpad(C),
+                (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane, fast ? kb.b32 : nullptr, kmeans_cpad(C),
                 fast ? kb.wn : nullptr,
                 fast ? kb.eb : nullptr, kb.hmax, kb.nflag);
     if constexpr (fast) {
       PARK_LAUNCH("kmeans_assign_fast", k_assign_fast<D>, dim3((N + 255) / 256, H), dim3(256), 0,
                   st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane, (const float*)kb.b32,
                   kmeans_cpad(C), (const float*)kb.wn, (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C,
-                  kb.labels, kb.flags, kb.nflag);
-      PARK_LAUNCH("kmeans_refine64", (k_refine<T, D>), dim3(rg, H), dim3(256), 0, st, X,
-                  (const double*)kb.wT, (const double*)kb.b, N, C, (const int*)kb.flags,
-                  (const int*)kb.nflag, kb.labels, status);
+                  kb.labels, kb.flags, kb.flagu, kb.nflag);
+      PARK_LAUNCH("kmeans_refine64", k_refine_cand<D>, dim3(8 * ((rg * H + 7) / 8)),
+                  dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
+                  (const float*)kb.b32, (const float*)kb.wn, (const float*)kb.eb, kmeans_cpad(C),
+                  (const double*)kb.w, (const double*)kb.b, H, N, C, rg, (const int*)kb.flags,
+                  (const float*)kb.flagu, (const int*)kb.nflag, kb.labels, status);
     } else {
       PARK_LAUNCH("kmeans_assign64", (k_assign64<T, D, 64>), dim3((N + 63) / 64, H), dim3(256), 0, st,
                   X, (const double*)kb.w, (const double*)kb.b, N, C, (const int*)nullptr,

@@ -41,12 +41,12 @@ struct KmeansBufs {
   // fast path (bf16 points)
   bf16_t* w3;     // [3][H][C][D] w as three bf16 parts
   float* b32;     // [H][kmeans_cpad(C)], padding +inf
-  float* wn;      // [H][C]    |w_v| (rounded up)
-  float* eb;      // [H][C]    |b_v| term of the fast-path error bound
+  float* wn;      // [H][kmeans_cpad(C)] |w_v| (rounded up), padding 0
+  float* eb;      // [H][kmeans_cpad(C)] |b_v| term of the fast-path bound, padding 0
   float* hmax;    // [H][ceil(C/16)][2] per-block max |w_v|, max eb_v
-  double* wT;     // [H][D][C] w transposed (float64 refinement)
   int* nflag;     // [H]       tokens left for the float64 refine
   int* flags;     // [H][N]    their indices
+  float* flagu;   // [H][N]    and an upper bound of their smallest exact score
 };
 park_status launch_kmeans(const void* X, const double* Gbar /* null = Euclidean */, int H, int N,
                           int D, int dtype, int C, int T, uint64_t seed, int side,

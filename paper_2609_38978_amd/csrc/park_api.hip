@@ -135,9 +135,9 @@ struct ClusterWs {
   float* wn;
   float* eb;
   float* hmax;
-  double* wT;
   int* nflag;
   int* flags;
+  float* flagu;
 };
 
 static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
@@ -154,12 +154,12 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   c.thist = cv.take<int>((size_t)H * C * sort_tiles(H, N, C));
   c.w3 = cv.take<bf16_t>((size_t)3 * H * C * D);
   c.b32 = cv.take<float>((size_t)H * kmeans_cpad(C));
-  c.wn = cv.take<float>((size_t)H * C);
-  c.eb = cv.take<float>((size_t)H * C);
+  c.wn = cv.take<float>((size_t)H * kmeans_cpad(C));
+  c.eb = cv.take<float>((size_t)H * kmeans_cpad(C));
   c.hmax = cv.take<float>((size_t)2 * H * ((C + 15) / 16));
-  c.wT = cv.take<double>((size_t)H * C * D);
   c.nflag = cv.take<int>((size_t)H);
   c.flags = cv.take<int>((size_t)H * N);
+  c.flagu = cv.take<float>((size_t)H * N);
   return c;
 }
 
@@ -245,9 +245,9 @@ static park_status cluster_body(const void* X, const void* Qm, const park_dims& 
   kb.wn = cw.wn;
   kb.eb = cw.eb;
   kb.hmax = cw.hmax;
-  kb.wT = cw.wT;
   kb.nflag = cw.nflag;
   kb.flags = cw.flags;
+  kb.flagu = cw.flagu;
   return launch_kmeans(X, Gbar, H, N, D, dm.dtype, C, T, seed, side, kb, st);
 }
 
