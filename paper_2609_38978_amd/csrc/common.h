@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -54,18 +55,24 @@ struct Carver {
   }
 };
 
-// Per-kernel event profiler (park_profile_*); no-ops unless enabled.
-void prof_begin(const char* name, hipStream_t s);
-void prof_end(hipStream_t s);
+// Per-kernel profiler (park_profile_*).  When enabled, a launch takes two
+// events and is issued with hipExtLaunchKernelGGL, which timestamps the
+// dispatch itself; prof_commit files the pair under the kernel's name.
+bool prof_take(hipEvent_t* a, hipEvent_t* b);
+void prof_commit(const char* name, hipEvent_t a, hipEvent_t b);
 
 // Records the message of a failed call (park_last_error).
 park_status fail(park_status st, const char* fmt, ...);
 
 #define PARK_LAUNCH(name, kernel, grid, block, shmem, stream, ...)                    \
   do {                                                                                \
-    ::park::prof_begin(name, stream);                                                 \
-    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);              \
-    ::park::prof_end(stream);                                                         \
+    hipEvent_t pa_ = nullptr, pb_ = nullptr;                                          \
+    if (::park::prof_take(&pa_, &pb_)) {                                              \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, pa_, pb_, 0, __VA_ARGS__); \
+      ::park::prof_commit(name, pa_, pb_);                                            \
+    } else {                                                                          \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);            \
+    }                                                                                 \
     hipError_t e_ = hipGetLastError();                                                \
     if (e_ != hipSuccess)                                                             \
       return ::park::fail(PARK_ERR_HIP, "%s: %s", name, hipGetErrorString(e_));       \

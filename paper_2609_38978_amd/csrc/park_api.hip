@@ -36,7 +36,6 @@ std::mutex g_pmu;
 bool g_prof = false;
 std::vector<hipEvent_t> g_pool;
 std::vector<ProfRec> g_recs;
-thread_local ProfRec g_open = {nullptr, nullptr, nullptr};
 
 hipEvent_t take_event() {
   if (!g_pool.empty()) {
@@ -50,21 +49,17 @@ hipEvent_t take_event() {
 }
 }  // namespace
 
-void prof_begin(const char* name, hipStream_t s) {
+bool prof_take(hipEvent_t* a, hipEvent_t* b) {
   std::lock_guard<std::mutex> lk(g_pmu);
-  if (!g_prof) return;
-  g_open.name = name;
-  g_open.a = take_event();
-  g_open.b = take_event();
-  if (g_open.a) hipEventRecord(g_open.a, s);
+  if (!g_prof) return false;
+  *a = take_event();
+  *b = take_event();
+  return *a && *b;
 }
 
-void prof_end(hipStream_t s) {
+void prof_commit(const char* name, hipEvent_t a, hipEvent_t b) {
   std::lock_guard<std::mutex> lk(g_pmu);
-  if (!g_prof || !g_open.name) return;
-  if (g_open.b) hipEventRecord(g_open.b, s);
-  if (g_open.a && g_open.b) g_recs.push_back(g_open);
-  g_open = {nullptr, nullptr, nullptr};
+  g_recs.push_back({name, a, b});
 }
 
 // ------------------------------------------------------------ small kernels
