@@ -4,10 +4,9 @@
 //   S^_iv = q_i . c_v / sqrt(d) + log n_v   (n_v = 0: block left out)
 //   P^_iv = softmax_v S^_iv;   W^_uv = (1 / n_u) sum_{i in Q_u} P^_iv
 //
-// k_pama64 evaluates this in float64 with one workgroup per (query block,
-// head): the logit row of every query stays in registers and the column sums
-// in registers of the thread that owns the key block (no HBM round trip, no
-// atomics, fixed summation order).
+// k_pama64 evaluates this in float64 (float64 MFMA) with one workgroup per
+// (query block, head) at a time; the column sums stay in LDS and are added
+// in a fixed order (no HBM round trip, no atomics).
 #include "common.h"
 #include "kernels.h"
 
@@ -53,132 +52,180 @@ __device__ int block_exclusive_scan_2048(int* a, int n, int* tmp) {
 }
 
 // ---------------------------------------------------------------- PAMA f64
+// Float64 PAMA rows on float64 MFMA (v_mfma_f64_16x16x4_f64: A[i][k] and
+// B[k][j] in lane 16k + i / 16k + j, D[g + 4r][c] in lane 16g + c, item r).
+// Workgroup = one (query block, head) at a time; the block's rows in chunks
+// of 64 (4 wavefronts x 16 queries), each chunk streaming the float32
+// centroids twice (normaliser pass, probability pass) through a two-slot LDS
+// ring filled by LDS DMA (rows swizzled in 16-byte chunks so the B-operand
+// reads are free of bank conflicts).  Logits, exponentials and all sums in
+// float64; per-wavefront column sums in LDS, added in wavefront order
+// (deterministic).  With a row list it recomputes only the listed query
+// blocks (the rows the fast path could not certify); the workgroups of a
+// head run on one XCD.
+__device__ __forceinline__ void p64_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t p64_lds_addr(const void* p) {
+  return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
 template <typename T, int D>
-__device__ void pama64_row(const T* __restrict__ Qp, const int* __restrict__ q_offsets,
-                           const float* __restrict__ cen, const int* __restrict__ k_sizes, int h,
-                           int u, int N, int CQ, int CK, double* __restrict__ W64,
-                           float* __restrict__ W32, int* status) {
-  constexpr int QT = 4;                 // queries per step
-  constexpr int MV = MAXC / 256;        // key blocks per thread
-  __shared__ double qs[QT][D];
-  __shared__ double red[4][QT];
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int* off = q_offsets + (size_t)h * (CQ + 1);
-  const int q0 = min(max(off[u], 0), N), q1 = min(max(off[u + 1], q0), N);
-  const int nu = q1 - q0;
-  const size_t wrow = ((size_t)h * CQ + u) * CK;
-  double lg[MV], acc[MV];
-  bool on[MV];
-#pragma unroll
-  for (int m = 0; m < MV; ++m) {
-    const int v = tid + 256 * m;
-    const int n = v < CK ? k_sizes[(size_t)h * CK + v] : 0;
-    on[m] = n > 0;
-    lg[m] = on[m] ? log((double)n) : 0.0;
-    acc[m] = 0.0;
-  }
-  const double sqd = sqrt((double)D);
+__global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp,
+                                                const int* __restrict__ q_offsets,
+                                                const float* __restrict__ cen,
+                                                const int* __restrict__ k_sizes, int H, int N,
+                                                int CQ, int CK, int rg, const int* __restrict__ rows,
+                                                const int* __restrict__ nrows,
+                                                double* __restrict__ W64, float* __restrict__ W32,
+                                                int* status) {
+  constexpr int CT = 32, CPR = D / 4, RPI = 64 / CPR, NI = CT / (4 * RPI), KS = D / 4;
+  static_assert(NI * 4 * RPI == CT, "tile shape");
+  __shared__ __attribute__((aligned(16))) float Ct[2][CT * D];
+  __shared__ double Lt[2][CT];
+  extern __shared__ double wacc64[];  // [4][CK]
+  const int nitems = H * rg, per = (nitems + 7) >> 3;
+  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (item >= nitems) return;
+  const int h = item / rg, wg = item - h * rg;
+  const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int cnt = rows ? min(nrows[h], CQ) : CQ;
   const float* ch = cen + (size_t)h * CK * D;
-  for (int i0 = q0; i0 < q1; i0 += QT) {
-    const int nq = min(QT, q1 - i0);
-    __syncthreads();
-    for (int e = tid; e < QT * D; e += 256) {
-      const int k = e / D, a = e % D;
-      qs[k][a] = k < nq ? (double)to_f(Qp[((size_t)h * N + i0 + k) * D + a]) : 0.0;
+  const int* nh = k_sizes + (size_t)h * CK;
+  const int* off = q_offsets + (size_t)h * (CQ + 1);
+  const T* Qh = Qp + (size_t)h * N * D;
+  const double isd = 1.0 / sqrt((double)D);
+  const int nt = (CK + CT - 1) / CT;
+  const int pch = l % CPR;
+  auto issue = [&](int tile, int slot) {
+    const int c0 = tile * CT;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = (w * NI + i) * RPI + l / CPR;
+      const int v = min(c0 + r, CK - 1);
+      const float* src = ch + (size_t)v * D + 4 * (pch ^ (r & (CPR - 1)));
+      p64_dma16(src, p64_lds_addr(&Ct[slot][0] + (w * NI + i) * 256));
     }
-    __syncthreads();
-    double S[QT][MV];
+    if (tid < CT) {
+      const int v = c0 + tid;
+      const int n = v < CK ? nh[v] : 0;
+      Lt[slot][tid] = n > 0 ? log((double)n) : -INFINITY;
+    }
+  };
+  for (int ri = wg; ri < cnt; ri += rg) {
+    const int u = rows ? rows[(size_t)h * CQ + ri] : ri;
+    if ((unsigned)u >= (unsigned)CQ) continue;  // uniform over the workgroup
+    const int q0 = min(max(off[u], 0), N), q1 = min(max(off[u + 1], q0), N);
+    const int nu = q1 - q0;
+    const size_t wrow = ((size_t)h * CQ + u) * CK;
+    if (nu <= 0) {
+      for (int v = tid; v < CK; v += 256) {
+        if (W64) W64[wrow + v] = 0.0;
+        if (W32) W32[wrow + v] = 0.0f;
+      }
+      continue;
+    }
+    __syncthreads();  // the previous row's column sums have been read
+    for (int v = tid; v < 4 * CK; v += 256) wacc64[v] = 0.0;
+    const int nch = (nu + 63) / 64;
+    const int total = nch * 2 * nt;
+    float qa[KS];  // float holds bf16 and float32 inputs exactly
+    double m[4], z[4], mf[4], iz[4];
+    bool qv[4];
+    issue(0, 0);
+    for (int it = 0; it < total; ++it) {
+      const int tile = it % nt, pass = (it / nt) & 1, r0 = q0 + 64 * (it / (2 * nt));
+      if (tile == 0 && pass == 0) {
+        // A operand: query r0 + 16w + c16, dimensions 4s + g
+        const int qi = r0 + 16 * w + c16;
 #pragma unroll
-    for (int m = 0; m < MV; ++m) {
-      const int v = tid + 256 * m;
+        for (int s = 0; s < KS; ++s)
+          qa[s] = qi < q1 ? to_f(Qh[(size_t)qi * D + 4 * s + g]) : 0.0f;
 #pragma unroll
-      for (int k = 0; k < QT; ++k) S[k][m] = 0.0;
-      if (on[m]) {
-        const float* cv = ch + (size_t)v * D;
-#pragma unroll 8
-        for (int a = 0; a < D; ++a) {
-          const double c = (double)cv[a];
+        for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qa[s]));
 #pragma unroll
-          for (int k = 0; k < QT; ++k) S[k][m] = fma(qs[k][a], c, S[k][m]);
+        for (int r = 0; r < 4; ++r) {
+          qv[r] = r0 + 16 * w + g + 4 * r < q1;  // this lane's output queries g + 4r
+          m[r] = -INFINITY;
+          z[r] = 0.0;
+        }
+      }
+      if (tile == 0 && pass == 1) {
+        // merge (max, sum) over the 16 lanes holding the same queries
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          double mm = m[r], zz = z[r];
+#pragma unroll
+          for (int o = 1; o < 16; o <<= 1) {
+            const double om = __shfl_xor(mm, o, 64), oz = __shfl_xor(zz, o, 64);
+            const double nm = fmax(mm, om);
+            zz = (nm == -INFINITY) ? 0.0 : zz * exp(mm - nm) + oz * exp(om - nm);
+            mm = nm;
+          }
+          mf[r] = mm;
+          iz[r] = zz > 0.0 ? 1.0 / zz : 0.0;
+        }
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();  // tile landed everywhere; previous tile consumed (its slot is free)
+      if (it + 1 < total) issue((it + 1) % nt, (it + 1) & 1);
+      const int slot = it & 1;
+      const float* cs = &Ct[slot][0];
+      const int c0 = tile * CT;
+#pragma unroll
+      for (int cb = 0; cb < CT / 16; ++cb) {
+        const int row = 16 * cb + c16;  // B operand: centroid row, dimension 4s + g
+        const float* crow = cs + row * D + g;
+        const int sw = row & (CPR - 1);
+        float bf[KS];  // all LDS reads first, then the MFMA chains
+#pragma unroll
+        for (int s = 0; s < KS; ++s) bf[s] = crow[4 * (s ^ sw)];
+        f64x4_t acc = {0.0, 0.0, 0.0, 0.0}, acc1 = acc;  // two chains (even / odd k-steps)
+#pragma unroll
+        for (int s = 0; s < KS; s += 2) {
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64((double)qa[s], (double)bf[s], acc, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)qa[s + 1], (double)bf[s + 1], acc1,
+                                                      0, 0, 0);
+        }
+        acc += acc1;
+        const double lg = Lt[slot][row];  // this lane's centroid (column c16)
+        if (pass == 0) {
+          if (lg != -INFINITY) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              // one exp per logit: d = S - m; z += e^d (d <= 0), else z = z e^-d + 1, m = S
+              const double sv = acc[r] * isd + lg;
+              const double d = sv - m[r];
+              const double e = exp(-fabs(d));
+              z[r] = d <= 0.0 ? z[r] + e : fma(z[r], e, 1.0);
+              m[r] = fmax(m[r], sv);
+            }
+          }
+        } else {
+          double cs4 = 0.0;
+          if (lg != -INFINITY) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (qv[r]) cs4 += exp(acc[r] * isd + lg - mf[r]) * iz[r];
+          }
+          cs4 += __shfl_xor(cs4, 16, 64);
+          cs4 += __shfl_xor(cs4, 32, 64);
+          const int v = c0 + row;
+          if (g == 0 && v < CK) wacc64[w * CK + v] += cs4;
         }
       }
     }
-    // logits, row maxima
-    double mx[QT];
-#pragma unroll
-    for (int k = 0; k < QT; ++k) {
-      mx[k] = -INFINITY;
-#pragma unroll
-      for (int m = 0; m < MV; ++m)
-        if (on[m]) {
-          S[k][m] = S[k][m] / sqd + lg[m];
-          mx[k] = fmax(mx[k], S[k][m]);
-        }
-      for (int o = 32; o > 0; o >>= 1) mx[k] = fmax(mx[k], __shfl_xor(mx[k], o, 64));
-    }
-    if (lane == 0)
-#pragma unroll
-      for (int k = 0; k < QT; ++k) red[wid][k] = mx[k];
     __syncthreads();
-#pragma unroll
-    for (int k = 0; k < QT; ++k) mx[k] = fmax(fmax(red[0][k], red[1][k]), fmax(red[2][k], red[3][k]));
-    __syncthreads();
-    // exponentials and row sums
-    double sm[QT];
-#pragma unroll
-    for (int k = 0; k < QT; ++k) {
-      sm[k] = 0.0;
-#pragma unroll
-      for (int m = 0; m < MV; ++m)
-        if (on[m]) {
-          S[k][m] = exp(S[k][m] - mx[k]);
-          sm[k] += S[k][m];
-        }
-      for (int o = 32; o > 0; o >>= 1) sm[k] += __shfl_xor(sm[k], o, 64);
-    }
-    if (lane == 0)
-#pragma unroll
-      for (int k = 0; k < QT; ++k) red[wid][k] = sm[k];
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < QT; ++k) sm[k] = ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
-    // column sums over the queries of the block, in query order
-#pragma unroll
-    for (int k = 0; k < QT; ++k)
-      if (k < nq)
-#pragma unroll
-        for (int m = 0; m < MV; ++m)
-          if (on[m]) acc[m] += S[k][m] / sm[k];
-  }
-#pragma unroll
-  for (int m = 0; m < MV; ++m) {
-    const int v = tid + 256 * m;
-    if (v < CK) {
-      const double wv = nu > 0 ? acc[m] / (double)nu : 0.0;
+    const double inv_n = 1.0 / (double)nu;
+    for (int v = tid; v < CK; v += 256) {
+      const double wv = (((wacc64[v] + wacc64[CK + v]) + wacc64[2 * CK + v]) + wacc64[3 * CK + v]) * inv_n;
       if (!isfinite(wv)) raise_status(status, ST_NONFINITE);
       if (W64) W64[wrow + v] = wv;
       if (W32) W32[wrow + v] = (float)wv;
     }
-  }
-  __syncthreads();
-}
-
-// float64 PAMA of every query block, or (rows != null) of the listed ones.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp, const int* __restrict__ q_offsets,
-                                                const float* __restrict__ cen,
-                                                const int* __restrict__ k_sizes, int N, int CQ, int CK,
-                                                const int* __restrict__ rows,
-                                                const int* __restrict__ nrows,
-                                                double* __restrict__ W64, float* __restrict__ W32,
-                                                int* status) {
-  const int h = blockIdx.y;
-  const int cnt = rows ? min(nrows[h], CQ) : blockIdx.x + 1;
-  const int step = rows ? gridDim.x : 1;
-  for (int r = blockIdx.x; r < cnt; r += step) {
-    const int u = rows ? rows[(size_t)h * CQ + r] : r;
-    if ((unsigned)u < (unsigned)CQ)
-      pama64_row<T, D>(Qp, q_offsets, cen, k_sizes, h, u, N, CQ, CK, W64, W32, status);
   }
 }
 
@@ -797,22 +844,36 @@ park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                           const int* rows, const int* nrows, double* W64, float* W32, int* status,
                           hipStream_t st, int grid_x) {
-  dim3 g(rows ? grid_x : CQ, H);
+  const int rg = rows ? grid_x : CQ;  // workgroups per head
+  const unsigned nwg = 8u * (((unsigned)rg * (unsigned)H + 7u) / 8u);
+  const size_t lds = (size_t)4 * CK * sizeof(double);
   const char* nm = rows ? "pama_refine64" : "pama64";
+  // reserved once for the largest CK (2048), outside any stream capture that may follow
+  static const int lds_max = (int)(4 * MAXC * sizeof(double));
+  static const hipError_t a1 = hipFuncSetAttribute(
+      (const void*)k_pama64<bf16_t, 128>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+  static const hipError_t a2 = hipFuncSetAttribute(
+      (const void*)k_pama64<float, 128>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+  static const hipError_t a3 = hipFuncSetAttribute(
+      (const void*)k_pama64<bf16_t, 64>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+  static const hipError_t a4 = hipFuncSetAttribute(
+      (const void*)k_pama64<float, 64>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+  if (a1 != hipSuccess || a2 != hipSuccess || a3 != hipSuccess || a4 != hipSuccess)
+    return fail(PARK_ERR_HIP, "retrieval: cannot reserve %zu bytes of LDS", lds);
   if (D == 128) {
     if (dtype == PARK_BF16)
-      PARK_LAUNCH(nm, (k_pama64<bf16_t, 128>), g, dim3(256), 0, st, (const bf16_t*)Qp, q_offsets,
-                  cen, k_sizes, N, CQ, CK, rows, nrows, W64, W32, status);
+      PARK_LAUNCH(nm, (k_pama64<bf16_t, 128>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
+                  q_offsets, cen, k_sizes, H, N, CQ, CK, rg, rows, nrows, W64, W32, status);
     else
-      PARK_LAUNCH(nm, (k_pama64<float, 128>), g, dim3(256), 0, st, (const float*)Qp, q_offsets,
-                  cen, k_sizes, N, CQ, CK, rows, nrows, W64, W32, status);
+      PARK_LAUNCH(nm, (k_pama64<float, 128>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
+                  q_offsets, cen, k_sizes, H, N, CQ, CK, rg, rows, nrows, W64, W32, status);
   } else {
     if (dtype == PARK_BF16)
-      PARK_LAUNCH(nm, (k_pama64<bf16_t, 64>), g, dim3(256), 0, st, (const bf16_t*)Qp, q_offsets,
-                  cen, k_sizes, N, CQ, CK, rows, nrows, W64, W32, status);
+      PARK_LAUNCH(nm, (k_pama64<bf16_t, 64>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
+                  q_offsets, cen, k_sizes, H, N, CQ, CK, rg, rows, nrows, W64, W32, status);
     else
-      PARK_LAUNCH(nm, (k_pama64<float, 64>), g, dim3(256), 0, st, (const float*)Qp, q_offsets,
-                  cen, k_sizes, N, CQ, CK, rows, nrows, W64, W32, status);
+      PARK_LAUNCH(nm, (k_pama64<float, 64>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
+                  q_offsets, cen, k_sizes, H, N, CQ, CK, rg, rows, nrows, W64, W32, status);
   }
   return PARK_OK;
 }
