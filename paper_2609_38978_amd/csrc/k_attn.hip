@@ -232,19 +232,74 @@ __device__ __forceinline__ void store_out4<bf16_t>(bf16_t* p, float a, float b, 
 // most 64 rows) of head h, {-1, 0, 0, 0} after the last one.  Chunks past
 // CPH (possible only for non-monotone offsets) are dropped.  One workgroup
 // of 1024 threads per head, CQ <= 2048.
-__global__ __launch_bounds__(1024) void k_attn_plan(const int* __restrict__ q_offsets, int N,
-                                                    int CQ, int CPH, int4* __restrict__ plan) {
+//
+// Query blocks are ordered by a MinHash of their selected key-block sets
+// (min over the selected ids of a fixed integer hash, ties by block id), so
+// blocks that select nearly the same key blocks get neighbouring chunks and
+// run at the same time on the same XCD, where their keys and values are
+// re-read from L2 instead of HBM.
+__device__ __forceinline__ uint32_t attn_hash(uint32_t v) {
+  v ^= v >> 16;
+  v *= 0x7feb352du;
+  v ^= v >> 15;
+  v *= 0x846ca68bu;
+  v ^= v >> 16;
+  return v;
+}
+
+__global__ __launch_bounds__(1024) void k_attn_plan(const int* __restrict__ q_offsets,
+                                                    const int* __restrict__ kv_count,
+                                                    const int* __restrict__ kv_index, int N,
+                                                    int CQ, int CK, int CPH,
+                                                    int4* __restrict__ plan) {
   __shared__ int wsum[16];
+  __shared__ unsigned long long key[2048];
   const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int* qo = q_offsets + (size_t)h * (CQ + 1);
   int4* ph = plan + (size_t)h * CPH;
-  int a[2], b[2], nc[2];
-  int s = 0;
+  // sort keys: (MinHash of the selected set, block id)
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int u = 2 * tid + k;
-    a[k] = b[k] = nc[k] = 0;
+    unsigned long long kk = ~0ull;
     if (u < CQ) {
+      const size_t row = (size_t)h * CQ + u;
+      const int n = min(max(kv_count[row], 0), CK);
+      const int* sel = kv_index + row * CK;
+      uint32_t mh = 0xffffffffu;
+      for (int j = 0; j < n; ++j) mh = min(mh, attn_hash((uint32_t)sel[j]));
+      kk = ((unsigned long long)mh << 32) | (uint32_t)u;
+    }
+    key[u] = kk;
+  }
+  __syncthreads();
+  // bitonic sort of the 2048 keys (padding ~0 sorts last)
+  for (int len = 2; len <= 2048; len <<= 1)
+    for (int j = len >> 1; j > 0; j >>= 1) {
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int i = tid + 1024 * k, ixj = i ^ j;
+        if (ixj > i) {
+          const unsigned long long x = key[i], y = key[ixj];
+          const bool up = (i & len) == 0;
+          if ((x > y) == up) {
+            key[i] = y;
+            key[ixj] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  // chunks of the query blocks in sorted order
+  int a[2], b[2], nc[2], uu[2];
+  int s = 0;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int pos = 2 * tid + k;
+    const int u = pos < CQ ? (int)(uint32_t)key[pos] : -1;
+    uu[k] = u;
+    a[k] = b[k] = nc[k] = 0;
+    if ((unsigned)u < (unsigned)CQ) {
       a[k] = min(max(qo[u], 0), N);
       b[k] = min(max(qo[u + 1], a[k]), N);
       nc[k] = (b[k] - a[k] + 63) >> 6;
@@ -268,7 +323,7 @@ __global__ __launch_bounds__(1024) void k_attn_plan(const int* __restrict__ q_of
 #pragma unroll
   for (int k = 0; k < 2; ++k)
     for (int i = 0; i < nc[k]; ++i, ++c)
-      if (c < CPH) ph[c] = make_int4(2 * tid + k, a[k] + 64 * i, min(a[k] + 64 * i + 64, b[k]), 0);
+      if (c < CPH) ph[c] = make_int4(uu[k], a[k] + 64 * i, min(a[k] + 64 * i + 64, b[k]), 0);
   for (int cc = total + tid; cc < CPH; cc += 1024) ph[cc] = make_int4(-1, 0, 0, 0);
 }
 
@@ -622,7 +677,8 @@ static park_status attn_mfma_d(const void* Qp, const void* Kp, const void* Vp, c
                                int N, int D, int CQ, int CK, void* plan, void* O, hipStream_t st) {
   const int CPH = attn_chunks_per_head(N, CQ);
   int4* pl = (int4*)plan;
-  PARK_LAUNCH("attn_plan", k_attn_plan, dim3(H), dim3(1024), 0, st, qo, N, CQ, CPH, pl);
+  PARK_LAUNCH("attn_plan", k_attn_plan, dim3(H), dim3(1024), 0, st, qo, kc, ki, N, CQ, CK, CPH,
+              pl);
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)D));
   if (D == 128)
     return attn_mfma_launch<OT, 128, PARK_ATTN_KT, PARK_ATTN_NS>(Qp, Kp, Vp, ko, kc, ki, qp, pl, H,
