@@ -184,14 +184,18 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
 // Fast assignment on bf16 MFMA with certification.
 //
 // For a bf16 point x the score s_v = b_v - 2 x.w_v is evaluated with w_v
-// split into three bf16 parts, w = w1 + w2 + w3 + r, |r| <= 2^-24 (1+2^-7)|w|.
-// All products are bf16 x bf16, exact in float.  x.w1 is accumulated over the
-// D dimensions in one chain of v_mfma_f32_16x16x32_bf16, x.(w2 + w3), whose
-// terms are 2^-8 smaller, in a second chain, and the two are added once.
-// With delta = 2^-23 per addition inside an MFMA (any faithful rounding) and
-// 2^-24 for the VALU roundings, the forward error of t^ = x.w is at most
-//   et sum_a |x_a w_a|,  et = 2^-24 1.01 + (D+1) delta (1 + 2^-7)
-//                            + 2^-8 1.01 (2D+1) delta + 2^-24 1.01,
+// split into NP bf16 parts, w = w1 + w2 (+ w3) + r, with |r| <= 2^-16 (1.01)
+// |w| for two parts and 2^-24 (1 + 2^-7)|w| for three.  All products are
+// bf16 x bf16, exact in float.  x.w1 is accumulated over the D dimensions in
+// one chain of v_mfma_f32_16x16x32_bf16, the smaller parts (terms 2^-8
+// smaller) in a second chain, and the two are added once.  With delta =
+// 2^-23 per addition inside an MFMA (any faithful rounding) and 2^-24 for
+// the VALU rounding, the forward error of t^ = x.w is at most
+//   et sum_a |x_a w_a|,  et = er 1.01 + (D+1) delta (1 + 2^-7)
+//                            + 2^-8 1.01 ((NP-1) D + 1) delta + 2^-24 1.01,
+// er the residual bound above.  Two parts take 2/3 of the MFMA work and
+// double the bound; they pay off when the centroid count makes the pass
+// MFMA-bound (C >= 512), three parts otherwise.
 // and with sum_a |x_a w_a| <= |x| |w_v|, the float roundings of b_v and of
 // the score, and |s^_v| <= |b_v| + 2.01 |x| |w_v|:
 //   |s^_v - s_v| <= E_v = Kx |w_v| + eb_v,
@@ -234,8 +238,16 @@ __device__ __forceinline__ uint32_t km_lds_addr(const void* p) {
 }
 template <int D>
 __device__ __forceinline__ int km_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+// waits until at most N vector-memory operations of this wavefront are outstanding
+template <int N>
+__device__ __forceinline__ void km_wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+#ifndef PARK_KM_NS
+#define PARK_KM_NS 3
+#endif
 
-template <int D>
+template <int D, int NP>
 __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ X,
                                                      const bf16_t* __restrict__ w3, size_t plane,
                                                      const float* __restrict__ b32, int Cpad,
@@ -248,14 +260,17 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
                                                      float* __restrict__ flagu,
                                                      int* __restrict__ nflag) {
   constexpr int TB = 4, CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
-  constexpr int NI = 3 * CT / (4 * RPI);  // DMAs per wavefront and tile
-  static_assert(NI * 4 * RPI == 3 * CT, "tile shape");
+  constexpr int NI = NP * CT / (4 * RPI);  // DMAs per wavefront and tile
+  static_assert(NI * 4 * RPI == NP * CT && (NP == 2 || NP == 3), "tile shape");
   constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f;
-  constexpr float ET = U24 * 1.01f + (D + 1) * DEL * 1.0079f + 0.00390625f * 1.01f * (2 * D + 1) * DEL +
-                       U24 * 1.01f;
+  // residual of the split: 2^-16 (two parts) or 2^-24 (three parts), relative
+  constexpr float ER = NP == 2 ? 1.52587891e-05f : U24;
+  constexpr float ET = ER * 1.01f + (D + 1) * DEL * 1.0079f +
+                       0.00390625f * 1.01f * ((NP - 1) * D + 1) * DEL + U24 * 1.01f;
   constexpr float KXC = 1.1f * (2.0f * ET + 2.01f * U24) * 1.0001f;
-  __shared__ __attribute__((aligned(16))) bf16_t Wt[2][3 * CT * D];  // [slot][part][row][D]
-  __shared__ __attribute__((aligned(16))) float Bt[2][CT];
+  constexpr int NS = PARK_KM_NS;  // LDS ring slots: NS - 1 tiles in flight
+  __shared__ __attribute__((aligned(16))) bf16_t Wt[NS][NP * CT * D];  // [slot][part][row][D]
+  __shared__ __attribute__((aligned(16))) float Bt[NS][CT];
   __shared__ float mx_s[2];
   const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -335,9 +350,12 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
     dot += __shfl_xor(dot, 32, 64);
     best[tb] = INFINITY;
     if (prev >= 0) {
-      const float e = fmaf(kx[tb], wn[(size_t)h * Cpad + prev], eb[(size_t)h * Cpad + prev]);
+      // the fast score of prev is within e of its exact score, and the float
+      // estimate (three parts, 32-term lane sums) within 2^-17 |x| |w| of it
+      const float wnp = wn[(size_t)h * Cpad + prev];
+      const float e = fmaf(kx[tb], wnp, eb[(size_t)h * Cpad + prev]);
       const float est = fmaf(-2.0f, dot, bh[prev]);
-      best[tb] = est + 2.0f * e + 1e-6f * fabsf(est);
+      best[tb] = est + 1.05f * e + (7.62939453e-06f / KXC) * kx[tb] * wnp + 1e-7f * fabsf(est);
     }
     L[tb] = INFINITY;
     bidx[tb] = -1;
@@ -365,15 +383,24 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
     }
     if (w == 0 && l < CT / 4) km_dma16(bh + c0 + 4 * l, km_lds_addr(&Bt[slot][0]));
   };
-  if (ntiles > 0) issue(0, 0);
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < ntiles) issue(p, p);
   const int swk = km_swz<D>(c16);
   for (int t = 0; t < ntiles; ++t) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // own DMAs of tile t done (wavefront 0 also fetches the b tile)
+    if (NS > 2 && t + 1 < ntiles) {
+      if (w == 0) km_wait_vmcnt<NI + 1>();
+      else km_wait_vmcnt<NI>();
+    } else {
+      km_wait_vmcnt<0>();
+    }
     __syncthreads();  // tile t landed; tile t-1 consumed by every wavefront
-    if (t + 1 < ntiles) issue(t + 1, (t + 1) & 1);
-    const bf16_t* W1 = &Wt[t & 1][0];
+    if (t + NS - 1 < ntiles) issue(t + NS - 1, (t + NS - 1) % NS);
+    const int slot = t % NS;
+    const bf16_t* W1 = &Wt[slot][0];
     const bf16_t* W2 = W1 + CT * D;
-    const bf16_t* W3 = W2 + CT * D;
+    const bf16_t* W3 = W2 + CT * D;  // third part (NP == 3)
 #pragma unroll
     for (int cb = 0; cb < CT / 16; ++cb) {
       f32x4_t ahi[TB], arest[TB];
@@ -388,15 +415,17 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
         const int co = rowo + 8 * ((4 * s + g) ^ swk);
         const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
         const bf16x8_t a2 = *(const bf16x8_t*)(W2 + co);
-        const bf16x8_t a3 = *(const bf16x8_t*)(W3 + co);
+        bf16x8_t a3;
+        if constexpr (NP == 3) a3 = *(const bf16x8_t*)(W3 + co);
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) {
           ahi[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[tb][s], ahi[tb], 0, 0, 0);
           arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, xf[tb][s], arest[tb], 0, 0, 0);
-          arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
+          if constexpr (NP == 3)
+            arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
         }
       }
-      const float4 b4 = *(const float4*)(&Bt[t & 1][16 * cb + 4 * g]);
+      const float4 b4 = *(const float4*)(&Bt[slot][16 * cb + 4 * g]);
       const float bv[4] = {b4.x, b4.y, b4.z, b4.w};
       const int vbase = t * CT + 16 * cb + 4 * g;
 #pragma unroll
@@ -466,9 +495,11 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
 
 // Float64 assignment of the tokens the fast path could not certify.
 //
-// Every exact score lies in [s^_v - E_v, s^_v + E_v] (same fast scores and
-// bounds as the fast path), so with U the listed upper bound of the smallest
-// exact score, the exact argmin lies in the candidate set
+// Every exact score lies in [s^_v - E_v, s^_v + E_v], here with fast scores on
+// the three-part split (w = w1 + w2 + w3 + r, |r| <= 2^-24 (1+2^-7)|w|, error
+// constant as in the fast path with the two small parts in the second chain),
+// so with U the listed upper bound of the smallest exact score (from the fast
+// path's own scores and bounds), the exact argmin lies in the candidate set
 // {v : s^_v - E_v <= U}.  One sweep over the centroids (MFMA, as in the fast
 // path) collects each token's candidates in LDS; they are then scored in
 // float64 (b_v - 2 x.w_v, partial sums over 8 lanes added in a fixed tree)
@@ -1002,10 +1033,16 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
                 fast ? kb.wn : nullptr,
                 fast ? kb.eb : nullptr, kb.hmax, kb.nflag);
     if constexpr (fast) {
-      PARK_LAUNCH("kmeans_assign_fast", k_assign_fast<D>, dim3((N + 255) / 256, H), dim3(256), 0,
-                  st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane, (const float*)kb.b32,
-                  kmeans_cpad(C), (const float*)kb.wn, (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C,
-                  kb.labels, kb.flags, kb.flagu, kb.nflag);
+      if (C >= 512)
+        PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 2>), dim3((N + 255) / 256, H),
+                    dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
+                    (const float*)kb.b32, kmeans_cpad(C), (const float*)kb.wn, (const float*)kb.eb,
+                    (const float*)kb.hmax, nbm, N, C, kb.labels, kb.flags, kb.flagu, kb.nflag);
+      else
+        PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 3>), dim3((N + 255) / 256, H),
+                    dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
+                    (const float*)kb.b32, kmeans_cpad(C), (const float*)kb.wn, (const float*)kb.eb,
+                    (const float*)kb.hmax, nbm, N, C, kb.labels, kb.flags, kb.flagu, kb.nflag);
       PARK_LAUNCH("kmeans_refine64", k_refine_cand<D>, dim3(8 * ((rg * H + 7) / 8)),
                   dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
                   (const float*)kb.b32, (const float*)kb.wn, (const float*)kb.eb, kmeans_cpad(C),
