@@ -67,75 +67,113 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ 
   G[(size_t)h * DD + e] = s * invN;
 }
 
-// Symmetrise, scale, stabilise and factorise; one workgroup per head, the
-// matrix held in LDS.  Right-looking Cholesky in float64.
+// Symmetrise, scale, stabilise and factorise; one workgroup per head.
+// The 256 threads form a 16 x 16 grid; thread (ti, tj) holds the entries
+// (ti + 16 r, tj + 16 c), r, c < D/16, of the matrix in registers for the
+// whole right-looking Cholesky.  Step k reads column k from a double-buffered
+// LDS vector, applies M[i][j] -= M[i][k] M[j][k] / M[k][k] to the trailing
+// block, and the owners of column k+1 publish it: one barrier per column.
+// Column j keeps its value from step j; L[i][j] = that / sqrt(M[j][j]).
 template <int D>
 __global__ __launch_bounds__(256) void k_metric_chol(const double* __restrict__ G, double alpha,
                                                      double eps, double s_min,
                                                      double* __restrict__ Gbar_out,
                                                      double* __restrict__ R_out, int* status) {
-  extern __shared__ double A[];  // D*D
-  __shared__ double red[256];
-  __shared__ double piv;
+  static_assert(D % 16 == 0 && D <= 128, "16 x 16 thread grid");
+  constexpr int NB = D / 16;
+  __shared__ double col[2][D];
+  __shared__ double pv[D];
+  __shared__ double sc;
   __shared__ int bad;
   const int h = blockIdx.x, tid = threadIdx.x;
+  const int ti = tid >> 4, tj = tid & 15;
   const double* Gh = G + (size_t)h * D * D;
-  for (int e = tid; e < D * D; e += 256) A[e] = Gh[e];
   if (tid == 0) bad = 0;
-  __syncthreads();
+  if (tid < D) pv[tid] = Gh[tid * D + tid];
+  double a[NB][NB];
   // symmetrise: (G + G^T) / 2
-  for (int e = tid; e < D * D; e += 256) {
-    const int i = e / D, j = e % D;
-    if (i < j) {
-      const double v = (A[i * D + j] + A[j * D + i]) / 2.0;
-      A[i * D + j] = v;
-      A[j * D + i] = v;
+#pragma unroll
+  for (int r = 0; r < NB; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c) {
+      const int i = ti + 16 * r, j = tj + 16 * c;
+      a[r][c] = (i == j) ? Gh[i * D + j] : (Gh[i * D + j] + Gh[j * D + i]) / 2.0;
     }
+  __syncthreads();
+  // s = max(tr G / d, s_min), summed in index order
+  if (tid == 0) {
+    double t = 0.0;
+    for (int i = 0; i < D; ++i) t += pv[i];
+    sc = fmax(t / (double)D, s_min);
   }
   __syncthreads();
-  // s = max(tr G / d, s_min)
-  double t = 0.0;
-  if (tid == 0)
-    for (int i = 0; i < D; ++i) t += A[i * D + i];
-  if (tid == 0) red[0] = fmax(t / (double)D, s_min);
-  __syncthreads();
-  const double s = red[0];
+  const double s = sc;
   const double as = alpha * s, es = eps * s;
-  for (int e = tid; e < D * D; e += 256) {
-    const int i = e / D, j = e % D;
-    double v = (1.0 - alpha) * A[e];
-    if (i == j) v = (v + as) + es;
-    if (!isfinite(v)) bad = 1;
-    A[e] = v;
-  }
-  __syncthreads();
   double* Gb = Gbar_out + (size_t)h * D * D;
-  for (int e = tid; e < D * D; e += 256) Gb[e] = A[e];
-  // Cholesky, lower triangle in place
-  for (int k = 0; k < D; ++k) {
-    if (tid == 0) {
-      const double p = A[k * D + k];
-      if (!(p > 0.0) || !isfinite(p)) bad = 1;
-      piv = sqrt(fmax(p, 0.0));
-      A[k * D + k] = piv;
+  bool nf = false;
+#pragma unroll
+  for (int r = 0; r < NB; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c) {
+      const int i = ti + 16 * r, j = tj + 16 * c;
+      double v = (1.0 - alpha) * a[r][c];
+      if (i == j) v = (v + as) + es;
+      nf |= !isfinite(v);
+      a[r][c] = v;
+      Gb[i * D + j] = v;
     }
-    __syncthreads();
-    const double lkk = piv;
-    for (int i = k + 1 + tid; i < D; i += 256) A[i * D + k] = A[i * D + k] / lkk;
-    __syncthreads();
-    // trailing update of the lower triangle, 16 x 16 thread grid
-    for (int i = k + 1 + (tid >> 4); i < D; i += 16) {
-      const double lik = A[i * D + k];
-      for (int j = k + 1 + (tid & 15); j <= i; j += 16)
-        A[i * D + j] = fma(-lik, A[j * D + k], A[i * D + j]);
+  if (nf) bad = 1;
+  if (tj == 0)
+#pragma unroll
+    for (int r = 0; r < NB; ++r) col[0][ti + 16 * r] = a[r][0];
+  __syncthreads();
+#pragma unroll
+  for (int kc = 0; kc < NB; ++kc) {
+#pragma unroll 1
+    for (int kt = 0; kt < 16; ++kt) {
+      const int k = 16 * kc + kt, cur = k & 1;
+      const double p = col[cur][k];
+      if (tid == 0) {
+        if (!(p > 0.0) || !isfinite(p)) bad = 1;
+        pv[k] = sqrt(fmax(p, 0.0));
+      }
+      const double ip = 1.0 / p;
+      double vi[NB], vj[NB];
+#pragma unroll
+      for (int r = kc; r < NB; ++r) {
+        const int i = ti + 16 * r;
+        vi[r] = (i > k) ? col[cur][i] * ip : 0.0;
+      }
+#pragma unroll
+      for (int c = kc; c < NB; ++c) {
+        const int j = tj + 16 * c;
+        vj[c] = (j > k) ? col[cur][j] : 0.0;
+      }
+#pragma unroll
+      for (int r = kc; r < NB; ++r)
+#pragma unroll
+        for (int c = kc; c < NB; ++c) a[r][c] = fma(-vi[r], vj[c], a[r][c]);
+      // publish column k + 1 (rows from its own block on)
+      if (kt < 15) {
+        if (tj == kt + 1)
+#pragma unroll
+          for (int r = kc; r < NB; ++r) col[cur ^ 1][ti + 16 * r] = a[r][kc];
+      } else if (kc + 1 < NB) {
+        if (tj == 0)
+#pragma unroll
+          for (int r = kc + 1; r < NB; ++r) col[cur ^ 1][ti + 16 * r] = a[r][kc + 1];
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
   double* R = R_out + (size_t)h * D * D;
-  for (int e = tid; e < D * D; e += 256) {
-    const int i = e / D, j = e % D;
-    R[e] = (j <= i) ? A[e] : 0.0;
-  }
+#pragma unroll
+  for (int r = 0; r < NB; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c) {
+      const int i = ti + 16 * r, j = tj + 16 * c;
+      R[i * D + j] = (j < i) ? a[r][c] / pv[j] : (j == i ? pv[j] : 0.0);
+    }
   if (tid == 0 && bad) raise_status(status, ST_NOT_SPD);
 }
 
@@ -192,18 +230,12 @@ park_status launch_metric(const void* Q, int H, int N, int D, int dtype, double 
   const int DD = D * D;
   PARK_LAUNCH("gram_reduce", k_gram_reduce, dim3((DD + 255) / 256, H), dim3(256), 0, st, part, nch,
               DD, 1.0 / (double)N, G);
-  const size_t lds = (size_t)DD * sizeof(double);
-  if (D == 128) {
-    // set once, outside any stream capture that may follow
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)k_metric_chol<128>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (attr != hipSuccess) return fail(PARK_ERR_HIP, "metric: cannot reserve %zu bytes of LDS", lds);
-    PARK_LAUNCH("metric_chol", k_metric_chol<128>, dim3(H), dim3(256), lds, st, G, alpha, eps,
+  if (D == 128)
+    PARK_LAUNCH("metric_chol", k_metric_chol<128>, dim3(H), dim3(256), 0, st, G, alpha, eps,
                 s_min, Gbar, R, status);
-  } else {
-    PARK_LAUNCH("metric_chol", k_metric_chol<64>, dim3(H), dim3(256), lds, st, G, alpha, eps,
+  else
+    PARK_LAUNCH("metric_chol", k_metric_chol<64>, dim3(H), dim3(256), 0, st, G, alpha, eps,
                 s_min, Gbar, R, status);
-  }
   return PARK_OK;
 }
 
