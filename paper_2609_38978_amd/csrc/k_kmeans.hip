@@ -209,14 +209,10 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
 // refinement.
 //
 // Bookkeeping per lane and token (the lane sees a quarter of the centroids):
-// best (score and id) and L.  Each 16-centroid step gives the lane 4 scores;
-// their minimum m either stays above best (the common case: L = min(L, m))
-// or some lane of the wavefront takes the per-score path.  The running best
-// starts at an estimate of the score of the token's previous label (plus a
-// margin) with no id, so after the first iterations almost no score beats
-// it; the estimate never enters L, and a token whose best is still that
-// estimate at the end is listed for refinement.  Correctness does not depend
-// on the estimate, only the number of listed tokens does.
+// the two smallest fast scores (best, L) and the id of the smallest, updated
+// without branches from each 16-centroid step's four scores (their minimum,
+// second minimum and first argmin), ties kept at the lower id.  An equal
+// score later in the sweep lands in L, so exact ties are never certified.
 //
 // Workgroup = 256 tokens (4 wavefronts x 4 blocks of 16).  Centroid tiles of
 // 32 rows of the three parts go from HBM to a two-slot LDS ring by LDS DMA
@@ -224,6 +220,7 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
 // while this one is scored.  MFMA orientation: A = 16 centroids x 32 dims,
 // B = 32 dims x 16 tokens, so lane l holds centroids 4(l/16)+r of token l%16.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // One wave-wide LDS DMA (lane l's 16 bytes at g land at LDS byte lds + 16 l),
@@ -292,8 +289,8 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
-        xsq[tb] = fmaf(lo, lo, fmaf(hi, hi, xsq[tb]));
+        const bf16x2_t p2 = __builtin_bit_cast(bf16x2_t, q[e]);
+        xsq[tb] = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, xsq[tb], false);
       }
     }
   }
@@ -312,51 +309,16 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       mx_s[1] = c;
     }
   }
-  // running best: an estimate of the previous label's score plus a margin
   float kx[TB], best[TB], L[TB];
   int bidx[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
     float xs = xsq[tb] + __shfl_xor(xsq[tb], 16, 64);
     xs += __shfl_xor(xs, 32, 64);
-    kx[tb] = KXC * sqrtf(xs);
-    const int tok = t0 + 16 * tb + c16;
-    int prev = tok < N ? labels[(size_t)h * N + tok] : -1;
-    prev = (unsigned)prev < (unsigned)C ? prev : -1;
-    float dot = 0.0f;
-    if (prev >= 0) {
-      const bf16_t* wp = P1 + (size_t)prev * D + 8 * g;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const uint4 u1 = *(const uint4*)(wp + 32 * s);
-        const uint4 u2 = *(const uint4*)(wp + plane + 32 * s);
-        const uint4 u3 = *(const uint4*)(wp + 2 * plane + 32 * s);
-        const uint4 ux = __builtin_bit_cast(uint4, xf[tb][s]);
-        const uint32_t a1[4] = {u1.x, u1.y, u1.z, u1.w}, a2[4] = {u2.x, u2.y, u2.z, u2.w},
-                       a3[4] = {u3.x, u3.y, u3.z, u3.w}, ax[4] = {ux.x, ux.y, ux.z, ux.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float wl = (__uint_as_float(a1[e] << 16) + __uint_as_float(a2[e] << 16)) +
-                           __uint_as_float(a3[e] << 16);
-          const float wh = (__uint_as_float(a1[e] & 0xffff0000u) +
-                            __uint_as_float(a2[e] & 0xffff0000u)) +
-                           __uint_as_float(a3[e] & 0xffff0000u);
-          dot = fmaf(__uint_as_float(ax[e] << 16), wl, dot);
-          dot = fmaf(__uint_as_float(ax[e] & 0xffff0000u), wh, dot);
-        }
-      }
-    }
-    dot += __shfl_xor(dot, 16, 64);
-    dot += __shfl_xor(dot, 32, 64);
+    // |x|^2 below 2^-100 may have lost its square terms to underflow: such a
+    // token gets an infinite bound and is listed for the float64 path
+    kx[tb] = xs >= 7.88860905e-31f ? KXC * sqrtf(xs) : INFINITY;
     best[tb] = INFINITY;
-    if (prev >= 0) {
-      // the fast score of prev is within e of its exact score, and the float
-      // estimate (three parts, 32-term lane sums) within 2^-17 |x| |w| of it
-      const float wnp = wn[(size_t)h * Cpad + prev];
-      const float e = fmaf(kx[tb], wnp, eb[(size_t)h * Cpad + prev]);
-      const float est = fmaf(-2.0f, dot, bh[prev]);
-      best[tb] = est + 1.05f * e + (7.62939453e-06f / KXC) * kx[tb] * wnp + 1e-7f * fabsf(est);
-    }
     L[tb] = INFINITY;
     bidx[tb] = -1;
   }
@@ -365,7 +327,7 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
   for (int tb = 0; tb < TB; ++tb) {
 #pragma unroll
     for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(xf[tb][s]));
-    asm volatile("" ::"v"(best[tb]), "v"(kx[tb]));
+    asm volatile("" ::"v"(kx[tb]));
   }
 
   // LDS DMA lanes: row rr[i] of the tile's 3*CT part-rows, chunk pch
@@ -433,28 +395,24 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
         float sc[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) sc[r] = fmaf(-2.0f, ahi[tb][r] + arest[tb][r], bv[r]);
-        const float m = fminf(fminf(sc[0], sc[1]), fminf(sc[2], sc[3]));
-        const bool c = m < best[tb];
-        if (__any(c)) {
-          if (c) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const bool nb = sc[r] < best[tb];
-              const float out = nb ? (bidx[tb] >= 0 ? best[tb] : INFINITY) : sc[r];
-              L[tb] = fminf(L[tb], out);
-              best[tb] = nb ? sc[r] : best[tb];
-              bidx[tb] = nb ? vbase + r : bidx[tb];
-            }
-          } else {
-            L[tb] = fminf(L[tb], m);
-          }
-        } else {
-          L[tb] = fminf(L[tb], m);
-        }
+        // minimum, second minimum and first argmin of the four
+        const float lo01 = fminf(sc[0], sc[1]), hi01 = fmaxf(sc[0], sc[1]);
+        const float lo23 = fminf(sc[2], sc[3]), hi23 = fmaxf(sc[2], sc[3]);
+        const int i01 = sc[1] < sc[0] ? 1 : 0, i23 = sc[3] < sc[2] ? 3 : 2;
+        const int im = lo23 < lo01 ? i23 : i01;
+        const float m = fminf(lo01, lo23);
+        const float m2 = fminf(fmaxf(lo01, lo23), fminf(hi01, hi23));
+        // two smallest of {best, L, m, m2}
+        const bool nb = m < best[tb];
+        L[tb] = fminf(fminf(L[tb], m2), fmaxf(best[tb], m));
+        best[tb] = fminf(best[tb], m);
+        bidx[tb] = nb ? vbase + im : bidx[tb];
       }
     }
   }
   const float nmax = mx_s[0], ebmax = mx_s[1];
+  bool fl[TB];
+  float ubv[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
     // merge over the four lane groups holding this token (ties: lowest id)
@@ -472,23 +430,42 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       bidx[tb] = take ? oi : bidx[tb];
     }
     const int tok = t0 + 16 * tb + c16;
+    fl[tb] = false;
+    ubv[tb] = INFINITY;  // an upper bound of the smallest exact score
     if (g == 0 && tok < N) {
       bool ok = false;
-      float ub = INFINITY;  // an upper bound of the smallest exact score
       if (bidx[tb] >= 0 && isfinite(best[tb])) {
         const int v = bidx[tb];
         const float e1 = fmaf(kx[tb], wn[(size_t)h * Cpad + v], eb[(size_t)h * Cpad + v]);
         const float emax = fmaf(kx[tb], nmax, ebmax) * 1.0001f;
-        ub = best[tb] + e1;
-        ok = (L[tb] - emax) > ub;
+        ubv[tb] = best[tb] + e1;
+        ok = (L[tb] - emax) > ubv[tb];
       }
-      if (ok) {
-        labels[(size_t)h * N + tok] = bidx[tb];
-      } else {
-        const int slot = atomicAdd(nflag + h, 1);
-        flags[(size_t)h * N + slot] = tok;
-        flagu[(size_t)h * N + slot] = ub;
+      if (ok) labels[(size_t)h * N + tok] = bidx[tb];
+      fl[tb] = !ok;
+    }
+  }
+  // listed tokens: one counter update per wavefront, slots in lane order
+  uint64_t bal[TB];
+  int tot = 0;
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) {
+    bal[tb] = __ballot(fl[tb]);
+    tot += __popcll(bal[tb]);
+  }
+  if (tot > 0) {
+    int base = 0;
+    if (l == 0) base = atomicAdd(nflag + h, tot);
+    base = __shfl(base, 0, 64);
+    const uint64_t below = (1ull << l) - 1ull;
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      if (fl[tb]) {
+        const int slot = base + __popcll(bal[tb] & below);
+        flags[(size_t)h * N + slot] = t0 + 16 * tb + c16;
+        flagu[(size_t)h * N + slot] = ubv[tb];
       }
+      base += __popcll(bal[tb]);
     }
   }
 }
@@ -501,12 +478,14 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
 // so with U the listed upper bound of the smallest exact score (from the fast
 // path's own scores and bounds), the exact argmin lies in the candidate set
 // {v : s^_v - E_v <= U}.  One sweep over the centroids (MFMA, as in the fast
-// path) collects each token's candidates in LDS; they are then scored in
-// float64 (b_v - 2 x.w_v, partial sums over 8 lanes added in a fixed tree)
-// and the minimum, ties to the lowest id, is the label.
-// Near-ties leave two or three candidates; a token with more than KMAX
-// (exact duplicates, degenerate data) is scored against every centroid.
-// Workgroups take chunks of 256 listed tokens (4 wavefronts x 4 x 16).
+// path, centroid tiles through an NS-slot LDS DMA ring) collects each token's
+// candidates in LDS; they are then scored in float64 (b_v - 2 x.w_v, partial
+// sums over PL lanes added in a fixed tree) and the minimum, ties to the
+// lowest id, is the label.  Near-ties leave two or three candidates; a token
+// with more than KMAX (exact duplicates, degenerate data) is scored against
+// every centroid.
+// Workgroups take chunks of 64 listed tokens (16 per wavefront), so that the
+// sweep of one chunk is short and the listed tokens spread over many CUs.
 template <int D>
 __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ X,
                                                      const bf16_t* __restrict__ w3, size_t plane,
@@ -520,34 +499,38 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
                                                      const float* __restrict__ flagu,
                                                      const int* __restrict__ nflag,
                                                      int* __restrict__ labels, int* status) {
-  constexpr int TB = 4, CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
-  constexpr int NI = 3 * CT / (4 * RPI);
-  constexpr int KMAX = 4;            // candidates kept per token
-  constexpr int PL = 8, PE = D / PL;  // lanes per scored pair, elements per lane
+  constexpr int CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
+  constexpr int NI = 3 * CT / (4 * RPI);  // DMAs per wavefront and tile
+  constexpr int NS = PARK_KM_NS;
+  constexpr int TC = 64;                  // listed tokens per chunk
+  constexpr int KMAX = 4;                 // candidates kept per token
+  constexpr int PL = 16, PE = D / PL;     // lanes per scored pair, elements per lane
+  constexpr int KP = 4;                   // pairs per lane group and pass
   constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f;
   constexpr float ET = U24 * 1.01f + (D + 1) * DEL * 1.0079f + 0.00390625f * 1.01f * (2 * D + 1) * DEL +
                        U24 * 1.01f;
   constexpr float KXC = 1.1f * (2.0f * ET + 2.01f * U24) * 1.0001f;
-  __shared__ __attribute__((aligned(16))) bf16_t Wt[2][3 * CT * D];
-  __shared__ __attribute__((aligned(16))) float Bt[2][CT];
-  __shared__ __attribute__((aligned(16))) float Nt[2][CT];
-  __shared__ __attribute__((aligned(16))) float Et[2][CT];
-  __shared__ int ccount[256];
-  __shared__ int ctok[256];
-  __shared__ int cv[256 * KMAX];    // candidates by token slot
-  __shared__ double cs[256 * KMAX];  // float64 scores of the packed pairs
+  __shared__ __attribute__((aligned(16))) bf16_t Wt[NS][3 * CT * D];
+  __shared__ __attribute__((aligned(16))) float Bt[NS][CT];
+  __shared__ __attribute__((aligned(16))) float Nt[NS][CT];
+  __shared__ __attribute__((aligned(16))) float Et[NS][CT];
+  __shared__ int ccount[TC];
+  __shared__ int ctok[TC];
+  __shared__ int cv[TC * KMAX];  // candidates by token slot
+  __shared__ int poff[TC];
+  __shared__ int npairs;
   __shared__ int nover;
-  __shared__ int over[256];
-  __shared__ double xrow[D];
+  __shared__ int over[TC];
   __shared__ double rbest[4];
   __shared__ int ridx[4];
-  __shared__ int wsum[4];
-  __shared__ int poff[256];
-  __shared__ int ptl[256 * KMAX];
-  __shared__ int pv[256 * KMAX];
-  __shared__ int npairs;
-  __shared__ double obest[256];
-  __shared__ int oidx[256];
+  // after the sweep the ring holds the pair lists and float64 scores
+  double* const cs = (double*)&Wt[0][0];  // [TC * KMAX] scores of the packed pairs
+  int* const ptl = (int*)(cs + TC * KMAX);  // [TC * KMAX] token slot of each pair
+  int* const pv = ptl + TC * KMAX;          // [TC * KMAX] centroid of each pair
+  double* const xrow = (double*)(pv + TC * KMAX);  // [D]
+  double* const obest = xrow + D;                  // [TC]
+  int* const oidx = (int*)(obest + TC);            // [TC]
+  static_assert((3 * TC * KMAX + 2 * D + 3 * TC) * 8 <= (int)sizeof(Wt), "aliases fit the ring");
   // XCD-aware: the workgroups of a head run on one XCD (its L2 holds the head's centroids)
   const int nitems = H * rg, per = (nitems + 7) >> 3;
   const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
@@ -556,7 +539,7 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
   const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int cnt = min(nflag[h], N);
-  const int nchunks = (cnt + 255) / 256;
+  const int nchunks = (cnt + TC - 1) / TC;
   if (wg >= nchunks) return;
   const bf16_t* Xh = X + (size_t)h * N * D;
   const bf16_t* P1 = w3 + (size_t)h * C * D;
@@ -584,26 +567,23 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
     }
   };
   const int swk = km_swz<D>(c16);
+  const int tl = 16 * w + c16;  // this lane's token slot in the chunk
   for (int chunk = wg; chunk < nchunks; chunk += rg) {
-    // this chunk's tokens: wavefront w, block tb, column c16 -> local id 64w + 16tb + c16
-    bf16x8_t xf[TB][KS];
-    float kx[TB], U[TB];
-    int tk[TB];
-#pragma unroll
-    for (int tb = 0; tb < TB; ++tb) {
-      const int idx = chunk * 256 + 64 * w + 16 * tb + c16;
+    bf16x8_t xf[KS];
+    float kx, U;
+    {
+      const int idx = chunk * TC + tl;
       int tok = idx < cnt ? flags[(size_t)h * N + idx] : -1;
       tok = (unsigned)tok < (unsigned)N ? tok : -1;
-      tk[tb] = tok;
-      U[tb] = tok >= 0 ? flagu[(size_t)h * N + idx] : -INFINITY;
-      if (U[tb] != U[tb]) U[tb] = INFINITY;  // NaN: every centroid is a candidate
+      U = tok >= 0 ? flagu[(size_t)h * N + idx] : -INFINITY;
+      if (U != U) U = INFINITY;  // NaN: every centroid is a candidate
       float xsq = 0.0f;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         uint4 raw = make_uint4(0u, 0u, 0u, 0u);
         if (tok >= 0) raw = *(const uint4*)(Xh + (size_t)tok * D + 32 * s + 8 * g);
-        xf[tb][s] = __builtin_bit_cast(bf16x8_t, raw);
-        asm volatile("" ::"v"(xf[tb][s]));  // loads complete here, not inside the tile loop
+        xf[s] = __builtin_bit_cast(bf16x8_t, raw);
+        asm volatile("" ::"v"(xf[s]));  // loads complete here, not inside the tile loop
         const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -613,31 +593,34 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
       }
       xsq += __shfl_xor(xsq, 16, 64);
       xsq += __shfl_xor(xsq, 32, 64);
-      kx[tb] = KXC * sqrtf(xsq);
-      asm volatile("" ::"v"(U[tb]));
+      kx = KXC * sqrtf(xsq);
+      asm volatile("" ::"v"(U));
       if (g == 0) {
-        ccount[64 * w + 16 * tb + c16] = 0;
-        ctok[64 * w + 16 * tb + c16] = tok;
+        ccount[tl] = 0;
+        ctok[tl] = tok;
       }
     }
     if (tid == 0) nover = 0;
-    issue(0, 0);
+#pragma unroll
+    for (int p = 0; p < NS - 1; ++p)
+      if (p < nt) issue(p, p);
     for (int t = 0; t < nt; ++t) {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // own DMAs of tile t done (wavefront 0 also fetches the b, |w|, eb tiles)
+      if (NS > 2 && t + 1 < nt) {
+        if (w == 0) km_wait_vmcnt<NI + 3>();
+        else km_wait_vmcnt<NI>();
+      } else {
+        km_wait_vmcnt<0>();
+      }
       __syncthreads();  // tile t landed everywhere; tile t-1 consumed
-      if (t + 1 < nt) issue(t + 1, (t + 1) & 1);
-      const int slot = t & 1;
+      if (t + NS - 1 < nt) issue(t + NS - 1, (t + NS - 1) % NS);
+      const int slot = t % NS;
       const bf16_t* W1 = &Wt[slot][0];
       const bf16_t* W2 = W1 + CT * D;
       const bf16_t* W3 = W2 + CT * D;
 #pragma unroll
       for (int cb = 0; cb < CT / 16; ++cb) {
-        f32x4_t ahi[TB], arest[TB];
-#pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-          ahi[tb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-          arest[tb] = ahi[tb];
-        }
+        f32x4_t ahi = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, arest = ahi;
         const int rowo = (16 * cb + c16) * D;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
@@ -645,12 +628,9 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
           const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
           const bf16x8_t a2 = *(const bf16x8_t*)(W2 + co);
           const bf16x8_t a3 = *(const bf16x8_t*)(W3 + co);
-#pragma unroll
-          for (int tb = 0; tb < TB; ++tb) {
-            ahi[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[tb][s], ahi[tb], 0, 0, 0);
-            arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, xf[tb][s], arest[tb], 0, 0, 0);
-            arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
-          }
+          ahi = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[s], ahi, 0, 0, 0);
+          arest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, xf[s], arest, 0, 0, 0);
+          arest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[s], arest, 0, 0, 0);
         }
         const int cl = 16 * cb + 4 * g;
         const float4 b4 = *(const float4*)(&Bt[slot][cl]);
@@ -659,35 +639,30 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
         const float bv[4] = {b4.x, b4.y, b4.z, b4.w}, nv[4] = {n4.x, n4.y, n4.z, n4.w},
                     ev[4] = {e4.x, e4.y, e4.z, e4.w};
         const int vb = t * CT + cl;
+        bool cand[4], anyc = false;
 #pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-          bool cand[4], anyc = false;
+        for (int r = 0; r < 4; ++r) {
+          const float sc = fmaf(-2.0f, ahi[r] + arest[r], bv[r]);
+          const float er = fmaf(kx, nv[r], ev[r]);
+          cand[r] = vb + r < C && !(sc - er > U);
+          anyc |= cand[r];
+        }
+        if (__any(anyc)) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float sc = fmaf(-2.0f, ahi[tb][r] + arest[tb][r], bv[r]);
-            const float er = fmaf(kx[tb], nv[r], ev[r]);
-            cand[r] = vb + r < C && !(sc - er > U[tb]);
-            anyc |= cand[r];
-          }
-          if (__any(anyc)) {
-            const int tl = 64 * w + 16 * tb + c16;
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (cand[r]) {
-                const int pos = atomicAdd(&ccount[tl], 1);
-                if (pos < KMAX) cv[tl * KMAX + pos] = vb + r;
-              }
-          }
+          for (int r = 0; r < 4; ++r)
+            if (cand[r]) {
+              const int pos = atomicAdd(&ccount[tl], 1);
+              if (pos < KMAX) cv[tl * KMAX + pos] = vb + r;
+            }
         }
       }
     }
     __syncthreads();
     // pack the pairs (token, candidate) of tokens with 1..KMAX candidates;
     // list the others (more candidates) for the all-centroid pass
-    {
-      const int tl = tid;
-      const int nc = ccount[tl];
-      const bool packed = ctok[tl] >= 0 && nc >= 1 && nc <= KMAX;
+    if (w == 0) {
+      const int nc = ccount[l];
+      const bool packed = ctok[l] >= 0 && nc >= 1 && nc <= KMAX;
       const int np = packed ? nc : 0;
       int inc = np;
 #pragma unroll
@@ -695,49 +670,41 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
         const int y = __shfl_up(inc, o, 64);
         if (l >= o) inc += y;
       }
-      if (l == 63) wsum[w] = inc;
-      if (ctok[tl] >= 0 && !packed) over[atomicAdd(&nover, 1)] = tl;
-      __syncthreads();
-      int pre = 0;
-      for (int q = 0; q < w; ++q) pre += wsum[q];
-      const int start = pre + inc - np;
-      poff[tl] = start;
+      const int start = inc - np;
+      poff[l] = start;
       for (int j = 0; j < np; ++j) {
-        ptl[start + j] = tl;
-        pv[start + j] = cv[tl * KMAX + j];
+        ptl[start + j] = l;
+        pv[start + j] = cv[l * KMAX + j];
       }
-      if (tid == 255) npairs = start + np;
+      if (ctok[l] >= 0 && !packed) over[atomicAdd(&nover, 1)] = l;
+      if (l == 63) npairs = inc;
     }
     __syncthreads();
     // float64 scores of the packed pairs, PL lanes per pair (PE dimensions each)
     {
-      const int lp = l / PL, sub = l % PL, np = npairs;
-      for (int base = 0; base < np; base += 64) {
-        double a[2];
-        int pp[2];
+      const int lp = tid / PL, sub = tid % PL, np = npairs;
+      for (int base = 0; base < np; base += KP * (256 / PL)) {
+        double a[KP];
+        int pp[KP];
 #pragma unroll
-        for (int k = 0; k < 2; ++k) {
-          const int p = base + 32 * k + 8 * w + lp;
+        for (int k = 0; k < KP; ++k) {
+          const int p = base + (256 / PL) * k + lp;
           pp[k] = p < np ? p : -1;
           a[k] = 0.0;
           if (p < np) {
             const int tok = ctok[ptl[p]];
-            const bf16_t* xr = Xh + (size_t)tok * D + sub * PE;
+            const uint4 xu = *(const uint4*)(Xh + (size_t)tok * D + sub * PE);
             const double* wr = wh + (size_t)pv[p] * D + sub * PE;
+            const uint32_t q[4] = {xu.x, xu.y, xu.z, xu.w};
 #pragma unroll
-            for (int e0 = 0; e0 < PE; e0 += 8) {
-              const uint4 xu = *(const uint4*)(xr + e0);
-              const uint32_t q[4] = {xu.x, xu.y, xu.z, xu.w};
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                a[k] = fma((double)__uint_as_float(q[e] << 16), wr[e0 + 2 * e], a[k]);
-                a[k] = fma((double)__uint_as_float(q[e] & 0xffff0000u), wr[e0 + 2 * e + 1], a[k]);
-              }
+            for (int e = 0; e < PE / 2; ++e) {
+              a[k] = fma((double)__uint_as_float(q[e] << 16), wr[2 * e], a[k]);
+              a[k] = fma((double)__uint_as_float(q[e] & 0xffff0000u), wr[2 * e + 1], a[k]);
             }
           }
         }
 #pragma unroll
-        for (int k = 0; k < 2; ++k) {
+        for (int k = 0; k < KP; ++k) {
           double t = a[k];
 #pragma unroll
           for (int o = PL / 2; o > 0; o >>= 1) t += __shfl_xor(t, o, 64);
@@ -748,7 +715,7 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
     __syncthreads();
     // tokens with too many candidates: float64 scores of every centroid
     for (int i = 0; i < nover; ++i) {
-      const int tl = over[i], tok = ctok[tl];
+      const int ot = over[i], tok = ctok[ot];
       for (int a0 = tid; a0 < D; a0 += 256) xrow[a0] = (double)to_f(Xh[(size_t)tok * D + a0]);
       __syncthreads();
       double bb = INFINITY;
@@ -783,14 +750,14 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
             rbest[0] = rbest[q];
             ridx[0] = ridx[q];
           }
-        obest[tl] = rbest[0];
-        oidx[tl] = ridx[0];
+        obest[ot] = rbest[0];
+        oidx[ot] = ridx[0];
       }
       __syncthreads();
     }
     // labels: the smallest float64 score, ties to the lowest id
-    {
-      const int tl = tid, tok = ctok[tl], nc = ccount[tl];
+    if (tid < TC) {
+      const int tok = ctok[tid], nc = ccount[tid];
       if (tok >= 0) {
         double bb;
         int bi;
@@ -798,7 +765,7 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
           bb = INFINITY;
           bi = 0x7fffffff;
           for (int j = 0; j < nc; ++j) {
-            const int p = poff[tl] + j;
+            const int p = poff[tid] + j;
             const double sc = cs[p];
             const int v = pv[p];
             if (sc < bb || (sc == bb && v < bi)) {
@@ -807,8 +774,8 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
             }
           }
         } else {
-          bb = obest[tl];
-          bi = oidx[tl];
+          bb = obest[tid];
+          bi = oidx[tid];
         }
         if (!isfinite(bb) || (unsigned)bi >= (unsigned)C) {
           raise_status(status, ST_NONFINITE);
@@ -1021,9 +988,9 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
   PARK_LAUNCH("kmeans_init", k_init_idx, dim3(H), dim3(1024), 0, st, N, C, seed, side, kb.init);
   PARK_LAUNCH("kmeans_seed", k_seed_centroids<T>, dim3(C, H), dim3(D), 0, st, X,
               (const int*)kb.init, N, D, C, kb.mu);
-  // refine grid: persistent workgroups per head looping over 256-token chunks
-  int rg = (1024 + H - 1) / H;
-  const int max_tiles = (N + 255) / 256;
+  // refine grid: persistent workgroups per head looping over 64-token chunks
+  int rg = (2048 + H - 1) / H;
+  const int max_tiles = (N + 63) / 64;
   rg = rg < 2 ? 2 : rg;
   rg = rg > max_tiles ? max_tiles : rg;
   for (int t = 0; t < T_; ++t) {
