@@ -103,6 +103,7 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
   constexpr int CB = 16, NG = 256 / D, PER = CB / NG;
   __shared__ double ms[CB][D];
   __shared__ double ws[CB][D + 1];
+  __shared__ float fnl[CB], fel[CB];
   const int h = blockIdx.y, v0 = blockIdx.x * CB, tid = threadIdx.x;
   for (int e = tid; e < CB * D; e += 256) {
     const int r = e / D, a = e % D;
@@ -144,22 +145,39 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
     }
   }
   __syncthreads();
-  float fn = 0.0f, fe = 0.0f;
-  if (tid < CB && v0 + tid < C) {
+  // b_v and |w_v|^2: 16 lanes per centroid, partial sums added in a fixed tree
+  {
+    constexpr int LPC = 256 / CB;
+    const int r = tid / LPC, sub = tid % LPC;
     double s = 0.0, n2 = 0.0;
-    for (int c = 0; c < D; ++c) {
-      s = fma(ms[tid][c], ws[tid][c], s);
-      n2 = fma(ws[tid][c], ws[tid][c], n2);
+#pragma unroll
+    for (int c = sub; c < D; c += LPC) {
+      s = fma(ms[r][c], ws[r][c], s);
+      n2 = fma(ws[r][c], ws[r][c], n2);
     }
-    b[(size_t)h * C + v0 + tid] = s;
-    if (b32) {
-      fn = (float)(sqrt(n2) * (1.0 + 1e-6));
-      fe = (float)(fabs(s) * (2.0 * 1.1 * 5.9604644775390625e-08) * (1.0 + 1e-6));
-      b32[(size_t)h * Cpad + v0 + tid] = (float)s;
-      wn[(size_t)h * Cpad + v0 + tid] = fn;
-      eb[(size_t)h * Cpad + v0 + tid] = fe;
+#pragma unroll
+    for (int o = LPC / 2; o > 0; o >>= 1) {
+      s += __shfl_xor(s, o, 64);
+      n2 += __shfl_xor(n2, o, 64);
+    }
+    float fnr = 0.0f, fer = 0.0f;
+    if (sub == 0 && v0 + r < C) {
+      b[(size_t)h * C + v0 + r] = s;
+      if (b32) {
+        fnr = (float)(sqrt(n2) * (1.0 + 1e-6));
+        fer = (float)(fabs(s) * (2.0 * 1.1 * 5.9604644775390625e-08) * (1.0 + 1e-6));
+        b32[(size_t)h * Cpad + v0 + r] = (float)s;
+        wn[(size_t)h * Cpad + v0 + r] = fnr;
+        eb[(size_t)h * Cpad + v0 + r] = fer;
+      }
+    }
+    if (sub == 0) {
+      fnl[r] = fnr;
+      fel[r] = fer;
     }
   }
+  __syncthreads();
+  float fn = tid < CB ? fnl[tid] : 0.0f, fe = tid < CB ? fel[tid] : 0.0f;
   if (b32 && blockIdx.x == gridDim.x - 1)  // padding centroids: score +inf, no error term
     for (int v = C + tid; v < Cpad; v += 256) {
       b32[(size_t)h * Cpad + v] = INFINITY;
@@ -936,13 +954,48 @@ __global__ __launch_bounds__(256) void k_segment_mean(const T* __restrict__ X,
   double acc[CW];
 #pragma unroll
   for (int c = 0; c < CW; ++c) acc[c] = 0.0;
-  for (int r = o0 + j; r < o1; r += RL) {
-    const int idx = p ? p[r] : r;
-    if ((unsigned)idx < (unsigned)N) {
-      const T* xr = Xh + (size_t)idx * D + c0;
+  // rows j, j + RL, ... in order; four rows' loads in flight at a time,
+  // each row segment (CW elements) read as 8- or 16-byte vectors
+  constexpr int UR = 4, NW = (int)sizeof(T) * CW / 4;
+  static_assert(NW == 2 || NW % 4 == 0, "row segment of 8 or 16k bytes");
+  for (int r0 = o0 + j; r0 < o1; r0 += UR * RL) {
+    int idx[UR];
 #pragma unroll
-      for (int c = 0; c < CW; ++c) acc[c] += (double)to_f(xr[c]);
+    for (int u = 0; u < UR; ++u) {
+      const int r = r0 + u * RL;
+      idx[u] = r < o1 ? (p ? p[r] : r) : -1;
     }
+    uint32_t xw[UR][NW];
+#pragma unroll
+    for (int u = 0; u < UR; ++u) {
+      const bool ok = (unsigned)idx[u] < (unsigned)N;
+      const T* xr = Xh + (size_t)(ok ? idx[u] : 0) * D + c0;
+      if constexpr (NW == 2) {
+        uint2 q = ok ? *(const uint2*)xr : make_uint2(0u, 0u);
+        xw[u][0] = q.x;
+        xw[u][1] = q.y;
+      } else {
+#pragma unroll
+        for (int k = 0; k < NW / 4; ++k) {
+          const uint4 q = ok ? ((const uint4*)xr)[k] : make_uint4(0u, 0u, 0u, 0u);
+          xw[u][4 * k] = q.x;
+          xw[u][4 * k + 1] = q.y;
+          xw[u][4 * k + 2] = q.z;
+          xw[u][4 * k + 3] = q.w;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UR; ++u)
+#pragma unroll
+      for (int c = 0; c < CW; ++c) {
+        float f;
+        if constexpr (sizeof(T) == 2)
+          f = __uint_as_float((c & 1) ? (xw[u][c >> 1] & 0xffff0000u) : (xw[u][c >> 1] << 16));
+        else
+          f = __uint_as_float(xw[u][c]);
+        acc[c] += (double)f;
+      }
   }
 #pragma unroll
   for (int c = 0; c < CW; ++c) part[j][c0 + c] = acc[c];

@@ -42,55 +42,64 @@ __global__ __launch_bounds__(256) void k_sort_hist(const int* __restrict__ label
 }
 
 // In-place exclusive scan of thist[h] (C*nt entries, cluster-major) and the
-// cluster offsets o[v] = first position of cluster v, o[C] = N.
+// cluster offsets o[v] = first position of cluster v, o[C] = N.  A pass covers
+// SP sub-passes of 4096 entries (4 consecutive per thread, coalesced); all its
+// loads are issued together and the SP block scans share one barrier.
 __global__ __launch_bounds__(1024) void k_sort_scan(int* __restrict__ thist, int C, int nt, int N,
                                                     int* __restrict__ offsets) {
-  __shared__ int wsum[16];
-  __shared__ int carry_s;
+  constexpr int SP = 4;
+  __shared__ int wsum[2][SP][16];
   const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   int* a = thist + (size_t)h * C * nt;
+  int* off = offsets + (size_t)h * (C + 1);
   const int total = C * nt;
-  if (tid == 0) carry_s = 0;
-  __syncthreads();
-  for (int base = 0; base < total; base += 4096) {
-    int x[4];
-    int s = 0;
+  int carry = 0;
+  for (int pass = 0, base = 0; base < total; ++pass, base += SP * 4096) {
+    int x[SP][4], sv[SP], inc[SP];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int idx = base + tid * 4 + k;
-      x[k] = idx < total ? a[idx] : 0;
-      s += x[k];
-    }
-    // inclusive scan of per-thread sums within the wave
-    int inc = s;
+    for (int j = 0; j < SP; ++j)
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(inc, o, 64);
-      if (lane >= o) inc += y;
-    }
-    if (lane == 63) wsum[wid] = inc;
-    __syncthreads();
-    int wpre = 0, blk = 0;
-    for (int w = 0; w < 16; ++w) {
-      if (w < wid) wpre += wsum[w];
-      blk += wsum[w];
-    }
-    const int carry = carry_s;
-    int run = carry + wpre + inc - s;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int idx = base + tid * 4 + k;
-      if (idx < total) {
-        a[idx] = run;
-        if (idx % nt == 0) offsets[(size_t)h * (C + 1) + idx / nt] = run;
+      for (int k = 0; k < 4; ++k) {
+        const int e = base + 4096 * j + 4 * tid + k;
+        x[j][k] = e < total ? a[e] : 0;
       }
-      run += x[k];
+#pragma unroll
+    for (int j = 0; j < SP; ++j) {
+      sv[j] = (x[j][0] + x[j][1]) + (x[j][2] + x[j][3]);
+      inc[j] = sv[j];
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(inc[j], o, 64);
+        if (lane >= o) inc[j] += y;
+      }
+      if (lane == 63) wsum[pass & 1][j][wid] = inc[j];
     }
     __syncthreads();
-    if (tid == 0) carry_s = carry + blk;
-    __syncthreads();
+    int run0 = carry;
+#pragma unroll
+    for (int j = 0; j < SP; ++j) {
+      int wpre = 0, blk = 0;
+#pragma unroll
+      for (int w = 0; w < 16; ++w) {
+        const int ws = wsum[pass & 1][j][w];
+        wpre += w < wid ? ws : 0;
+        blk += ws;
+      }
+      int run = run0 + wpre + inc[j] - sv[j];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = base + 4096 * j + 4 * tid + k;
+        if (e < total) {
+          a[e] = run;
+          if (e % nt == 0) off[e / nt] = run;
+        }
+        run += x[j][k];
+      }
+      run0 += blk;
+    }
+    carry = run0;  // wsum[pass & 1] is rewritten two passes later, after another barrier
   }
-  if (tid == 0) offsets[(size_t)h * (C + 1) + C] = N;
+  if (tid == 0) off[C] = N;
 }
 
 // Stable scatter: one wavefront per tile, tokens in increasing order.
