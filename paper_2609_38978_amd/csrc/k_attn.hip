@@ -257,29 +257,31 @@ __global__ __launch_bounds__(1024) void k_attn_plan(const int* __restrict__ q_of
   const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int* qo = q_offsets + (size_t)h * (CQ + 1);
   int4* ph = plan + (size_t)h * CPH;
-  // sort keys: (MinHash of the selected set, block id)
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int u = 2 * tid + k;
+  // sort keys: (MinHash of the selected set, block id), one wavefront per
+  // block; SZ = the power of two the bitonic sort runs over (padding ~0 last)
+  int SZ = 2;
+  while (SZ < CQ) SZ <<= 1;
+  for (int u = wid; u < SZ; u += 16) {
     unsigned long long kk = ~0ull;
     if (u < CQ) {
       const size_t row = (size_t)h * CQ + u;
       const int n = min(max(kv_count[row], 0), CK);
       const int* sel = kv_index + row * CK;
       uint32_t mh = 0xffffffffu;
-      for (int j = 0; j < n; ++j) mh = min(mh, attn_hash((uint32_t)sel[j]));
+      for (int j = lane; j < n; j += 64) mh = min(mh, attn_hash((uint32_t)sel[j]));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mh = min(mh, (uint32_t)__shfl_xor((int)mh, o, 64));
       kk = ((unsigned long long)mh << 32) | (uint32_t)u;
     }
-    key[u] = kk;
+    if (lane == 0) key[u] = kk;
   }
   __syncthreads();
-  // bitonic sort of the 2048 keys (padding ~0 sorts last)
-  for (int len = 2; len <= 2048; len <<= 1)
+  for (int len = 2; len <= SZ; len <<= 1)
     for (int j = len >> 1; j > 0; j >>= 1) {
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         const int i = tid + 1024 * k, ixj = i ^ j;
-        if (ixj > i) {
+        if (i < SZ && ixj > i) {
           const unsigned long long x = key[i], y = key[ixj];
           const bool up = (i & len) == 0;
           if ((x > y) == up) {

@@ -32,28 +32,51 @@ __global__ __launch_bounds__(1024) void k_init_idx(int N, int C, uint64_t seed, 
   __shared__ int jj[2048];
   __shared__ int root[2048];
   __shared__ int prevt[2048];
+  __shared__ unsigned long long key[2048];
   const int h = blockIdx.x, tid = threadIdx.x;
   const uint64_t sh = seed ^ (0x9E3779B97F4A7C15ull * (uint64_t)(2 * h + side + 1));
-  for (int i = tid; i < C; i += 1024)
-    jj[i] = i + (int)(splitmix64_at(sh, (uint64_t)i) % (uint64_t)(N - i));
+  int SZ = 2;  // power of two the sort below runs over
+  while (SZ < C) SZ <<= 1;
+  for (int i = tid; i < SZ; i += 1024) {
+    if (i < C) {
+      const int j = i + (int)(splitmix64_at(sh, (uint64_t)i) % (uint64_t)(N - i));
+      jj[i] = j;
+      key[i] = ((unsigned long long)j << 11) | (unsigned)i;
+      root[i] = -1;
+    } else {
+      key[i] = ~0ull;
+    }
+  }
   __syncthreads();
-  for (int k = tid; k < C; k += 1024) {
-    int lw = k;  // last m < k with j_m == k (self if none)
-    for (int m = k - 1; m >= 0; --m)
-      if (jj[m] == k) {
-        lw = m;
-        break;
-      }
-    root[k] = lw;
-    int pt = -1;  // last m < k with j_m == j_k
-    const int jk = jj[k];
-    if (jk != k)
-      for (int m = k - 1; m >= 0; --m)
-        if (jj[m] == jk) {
-          pt = m;
-          break;
+  // root[k] = the last step m < k with j_m = k (j_m >= m, so every m with
+  // j_m = k != m qualifies), else k
+  for (int m = tid; m < C; m += 1024) {
+    const int t = jj[m];
+    if (t < C && t != m) atomicMax(&root[t], m);
+  }
+  // prevt[k] = the last step m < k with j_m = j_k: the predecessor of (j_k, k)
+  // in the sorted list of pairs (j, step)
+  for (int len = 2; len <= SZ; len <<= 1)
+    for (int j = len >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < SZ; i += 1024) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const unsigned long long x = key[i], y = key[ixj];
+          const bool up = (i & len) == 0;
+          if ((x > y) == up) {
+            key[i] = y;
+            key[ixj] = x;
+          }
         }
-    prevt[k] = pt;
+      }
+      __syncthreads();
+    }
+  for (int s = tid; s < C; s += 1024) {
+    const unsigned long long x = key[s];
+    const int k = (int)(x & 2047ull);
+    const bool same = s > 0 && (key[s - 1] >> 11) == (x >> 11);
+    prevt[k] = (same && jj[k] != k) ? (int)(key[s - 1] & 2047ull) : -1;
+    if (root[k] < 0) root[k] = k;
   }
   __syncthreads();
   // pointer jumping to the roots: value entering position k at step k
