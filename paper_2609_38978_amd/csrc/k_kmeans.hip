@@ -122,7 +122,7 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
                                               bf16_t* __restrict__ w3,
                                               size_t plane, float* __restrict__ b32, int Cpad,
                                               float* __restrict__ wn, float* __restrict__ eb,
-                                              float* __restrict__ bmax, int* __restrict__ nflag) {
+                                              float* __restrict__ bmax) {
   constexpr int CB = 16, NG = 256 / D, PER = CB / NG;
   __shared__ double ms[CB][D];
   __shared__ double ws[CB][D + 1];
@@ -216,7 +216,6 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
     if (tid == 0) {
       bmax[((size_t)h * gridDim.x + blockIdx.x) * 2] = fn;
       bmax[((size_t)h * gridDim.x + blockIdx.x) * 2 + 1] = fe;
-      if (blockIdx.x == 0) nflag[h] = 0;  // the previous refinement has completed
     }
   }
 }
@@ -310,6 +309,7 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
   __shared__ __attribute__((aligned(16))) bf16_t Wt[NS][NP * CT * D];  // [slot][part][row][D]
   __shared__ __attribute__((aligned(16))) float Bt[NS][CT];
   __shared__ float mx_s[2];
+  __shared__ int wcnt[4];
   const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int t0 = blockIdx.x * 256 + w * 64;
@@ -486,7 +486,8 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       fl[tb] = !ok;
     }
   }
-  // listed tokens: one counter update per wavefront, slots in lane order
+  // listed tokens: this tile's list at flags[h][256 * tile ...] in lane
+  // order, its length in nflag[h][tile]; no atomics
   uint64_t bal[TB];
   int tot = 0;
 #pragma unroll
@@ -494,10 +495,12 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
     bal[tb] = __ballot(fl[tb]);
     tot += __popcll(bal[tb]);
   }
+  if (l == 0) wcnt[w] = tot;
+  __syncthreads();
+  int base = blockIdx.x * 256;
+  for (int q = 0; q < w; ++q) base += wcnt[q];
+  if (tid == 0) nflag[(size_t)h * gridDim.x + blockIdx.x] = wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
   if (tot > 0) {
-    int base = 0;
-    if (l == 0) base = atomicAdd(nflag + h, tot);
-    base = __shfl(base, 0, 64);
     const uint64_t below = (1ull << l) - 1ull;
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
@@ -564,6 +567,8 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
   __shared__ int over[TC];
   __shared__ double rbest[4];
   __shared__ int ridx[4];
+  __shared__ int wsc[4];
+  __shared__ int spos[TC];  // list position of each slot of the chunk (-1: none)
   // after the sweep the ring holds the pair lists and float64 scores
   double* const cs = (double*)&Wt[0][0];  // [TC * KMAX] scores of the packed pairs
   int* const ptl = (int*)(cs + TC * KMAX);  // [TC * KMAX] token slot of each pair
@@ -579,7 +584,16 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
   const int h = item / rg, wg = item - h * rg;
   const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int cnt = min(nflag[h], N);
+  // listed tokens of head h: per 256-token tile lists of the fast pass
+  const int NT = (N + 255) / 256;
+  const int* nf = nflag + (size_t)h * NT;
+  int cnt = 0;
+  for (int t = tid; t < NT; t += 256) cnt += min(max(nf[t], 0), 256);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+  if (l == 0) wsc[w] = cnt;
+  __syncthreads();
+  cnt = wsc[0] + wsc[1] + wsc[2] + wsc[3];
   const int nchunks = (cnt + TC - 1) / TC;
   if (wg >= nchunks) return;
   const bf16_t* Xh = X + (size_t)h * N * D;
@@ -610,13 +624,44 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
   const int swk = km_swz<D>(c16);
   const int tl = 16 * w + c16;  // this lane's token slot in the chunk
   for (int chunk = wg; chunk < nchunks; chunk += rg) {
+    // list positions of this chunk's slots: scan of the tile list lengths
+    __syncthreads();  // wsc and spos of the previous chunk consumed
+    if (tid < TC) spos[tid] = -1;
+    {
+      const int lo = chunk * TC;
+      int carry = 0;
+      for (int p0 = 0; p0 < NT && carry < lo + TC; p0 += 256) {
+        const int t = p0 + tid;
+        const int c = t < NT ? min(max(nf[t], 0), 256) : 0;
+        int inc = c;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(inc, o, 64);
+          if (l >= o) inc += y;
+        }
+        __syncthreads();  // previous piece's wsc read; spos cleared
+        if (l == 63) wsc[w] = inc;
+        __syncthreads();
+        int pre = carry, tot = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          pre += q < w ? wsc[q] : 0;
+          tot += wsc[q];
+        }
+        pre += inc - c;
+        const int a0 = max(pre, lo), a1 = min(pre + c, lo + TC);
+        for (int i = a0; i < a1; ++i) spos[i - lo] = t * 256 + (i - pre);
+        carry += tot;
+      }
+    }
+    __syncthreads();
     bf16x8_t xf[KS];
     float kx, U;
     {
-      const int idx = chunk * TC + tl;
-      int tok = idx < cnt ? flags[(size_t)h * N + idx] : -1;
+      const int sp = spos[tl];
+      int tok = sp >= 0 ? flags[(size_t)h * N + sp] : -1;
       tok = (unsigned)tok < (unsigned)N ? tok : -1;
-      U = tok >= 0 ? flagu[(size_t)h * N + idx] : -INFINITY;
+      U = tok >= 0 ? flagu[(size_t)h * N + sp] : -INFINITY;
       if (U != U) U = INFINITY;  // NaN: every centroid is a candidate
       float xsq = 0.0f;
 #pragma unroll
@@ -1074,7 +1119,7 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
     PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3(nbm, H), dim3(256), 0, st,
                 (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane, fast ? kb.b32 : nullptr, kmeans_cpad(C),
                 fast ? kb.wn : nullptr,
-                fast ? kb.eb : nullptr, kb.hmax, kb.nflag);
+                fast ? kb.eb : nullptr, kb.hmax);
     if constexpr (fast) {
       if (C >= 512)
         PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 2>), dim3((N + 255) / 256, H),

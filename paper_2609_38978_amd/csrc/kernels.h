@@ -44,8 +44,8 @@ struct KmeansBufs {
   float* wn;      // [H][kmeans_cpad(C)] |w_v| (rounded up), padding 0
   float* eb;      // [H][kmeans_cpad(C)] |b_v| term of the fast-path bound, padding 0
   float* hmax;    // [H][ceil(C/16)][2] per-block max |w_v|, max eb_v
-  int* nflag;     // [H]       tokens left for the float64 refine
-  int* flags;     // [H][N]    their indices
+  int* nflag;     // [H][ceil(N/256)] tokens of each 256-token tile left for the float64 refine
+  int* flags;     // [H][N]    their indices, tile t's list at 256 t
   float* flagu;   // [H][N]    and an upper bound of their smallest exact score
 };
 park_status launch_kmeans(const void* X, const double* Gbar /* null = Euclidean */, int H, int N,
