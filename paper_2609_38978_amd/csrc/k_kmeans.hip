@@ -227,7 +227,7 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
 // split into NP bf16 parts, w = w1 + w2 (+ w3) + r, with |r| <= 2^-16 (1.01)
 // |w| for two parts and 2^-24 (1 + 2^-7)|w| for three.  All products are
 // bf16 x bf16, exact in float.  x.w1 is accumulated over the D dimensions in
-// one chain of v_mfma_f32_16x16x32_bf16, the smaller parts (terms 2^-8
+// one chain of v_mfma_f32_32x32x16_bf16, the smaller parts (terms 2^-8
 // smaller) in a second chain, and the two are added once.  With delta =
 // 2^-23 per addition inside an MFMA (any faithful rounding) and 2^-24 for
 // the VALU rounding, the forward error of t^ = x.w is at most
@@ -248,20 +248,22 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
 // Otherwise (near-ties, exact ties) the token is listed for the float64
 // refinement.
 //
-// Bookkeeping per lane and token (the lane sees a quarter of the centroids):
-// the two smallest fast scores (best, L) and the id of the smallest, updated
-// without branches from each 16-centroid step's four scores (their minimum,
-// second minimum and first argmin), ties kept at the lower id.  An equal
-// score later in the sweep lands in L, so exact ties are never certified.
+// Bookkeeping per lane and token (the lane sees half of the centroids): the
+// two smallest fast scores (best <= L) and the id of the smallest, three VALU
+// operations per score: best = min(best, s), L = med3(best, L, s), and the
+// id taken when s < best, so ties keep the lower id and an equal score later
+// in the sweep lands in L (exact ties are never certified).
 //
-// Workgroup = 256 tokens (4 wavefronts x 4 blocks of 16).  Centroid tiles of
-// 32 rows of the three parts go from HBM to a two-slot LDS ring by LDS DMA
-// (rows swizzled in 16-byte chunks, see the reads), the next tile in flight
-// while this one is scored.  MFMA orientation: A = 16 centroids x 32 dims,
-// B = 32 dims x 16 tokens, so lane l holds centroids 4(l/16)+r of token l%16.
+// Workgroup = kmeans_tile tokens (4 wavefronts x TB blocks of 32).  Centroid tiles of
+// 32 rows of the NP parts go from HBM to an NS-slot LDS ring by LDS DMA (rows
+// swizzled in 16-byte chunks, see the reads), later tiles in flight while
+// this one is scored.  MFMA orientation (32x32x16, the shape with twice the
+// throughput of 16x16x32 here): A = 32 centroids x 16 dims, B = 16 dims x 32
+// tokens, so lane l holds centroids 8b + 4(l/32) + r (b, r < 4) of token l%32.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // One wave-wide LDS DMA (lane l's 16 bytes at g land at LDS byte lds + 16 l),
 // as inline assembly so that the compiler does not drain every DMA in flight
@@ -285,7 +287,7 @@ __device__ __forceinline__ void km_wait_vmcnt() {
 #endif
 
 template <int D, int NP>
-__global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ X,
+__global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict__ X,
                                                      const bf16_t* __restrict__ w3, size_t plane,
                                                      const float* __restrict__ b32, int Cpad,
                                                      const float* __restrict__ wn,
@@ -296,9 +298,10 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
                                                      int* __restrict__ flags,
                                                      float* __restrict__ flagu,
                                                      int* __restrict__ nflag) {
-  constexpr int TB = 4, CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
+  constexpr int TB = PARK_KM_TB, CT = 32, KS = D / 16, CPR = D / 8, RPI = 64 / CPR;
   constexpr int NI = NP * CT / (4 * RPI);  // DMAs per wavefront and tile
   static_assert(NI * 4 * RPI == NP * CT && (NP == 2 || NP == 3), "tile shape");
+  static_assert(kmeans_tile == 128 * TB, "tile tokens");
   constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f;
   // residual of the split: 2^-16 (two parts) or 2^-24 (three parts), relative
   constexpr float ER = NP == 2 ? 1.52587891e-05f : U24;
@@ -310,22 +313,42 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
   __shared__ __attribute__((aligned(16))) float Bt[NS][CT];
   __shared__ float mx_s[2];
   __shared__ int wcnt[4];
-  const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
+  const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int t0 = blockIdx.x * 256 + w * 64;
+  const int t0 = blockIdx.x * kmeans_tile + w * 32 * TB;
   const bf16_t* Xh = X + (size_t)h * N * D;
   const bf16_t* P1 = w3 + (size_t)h * C * D;
   const float* bh = b32 + (size_t)h * Cpad;
+  // LDS DMA lanes: row of the tile's NP*CT part-rows, chunk pch
+  const int pch = l % CPR;
+  const int ntiles = (C + CT - 1) / CT;
+  auto issue = [&](int tile, int slot) {
+    const int c0 = tile * CT;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int row = (w * NI + i) * RPI + l / CPR;
+      const int part = row / CT, r = row % CT;
+      const int v = min(c0 + r, C - 1);
+      const bf16_t* src = P1 + part * plane + (size_t)v * D + 8 * (pch ^ km_swz<D>(r));
+      km_dma16(src, km_lds_addr(&Wt[slot][0] + (w * NI + i) * 512));
+    }
+    if (w == 0 && l < CT / 4) km_dma16(bh + c0 + 4 * l, km_lds_addr(&Bt[slot][0]));
+  };
+  // the first tiles travel while the points are loaded
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < ntiles) issue(p, p);
+  // B operand: lane l holds dims 16 s + 8 (l/32) .. + 8 of token t0 + 32 tb + l%32
   bf16x8_t xf[TB][KS];
   float xsq[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
     xsq[tb] = 0.0f;
-    const int tok = t0 + 16 * tb + c16;
+    const int tok = t0 + 32 * tb + c32;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-      if (tok < N) raw = *(const uint4*)(Xh + (size_t)tok * D + 32 * s + 8 * g);
+      if (tok < N) raw = *(const uint4*)(Xh + (size_t)tok * D + 16 * s + 8 * hf);
       xf[tb][s] = __builtin_bit_cast(bf16x8_t, raw);
       const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
@@ -354,8 +377,7 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
   int bidx[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
-    float xs = xsq[tb] + __shfl_xor(xsq[tb], 16, 64);
-    xs += __shfl_xor(xs, 32, 64);
+    const float xs = xsq[tb] + __shfl_xor(xsq[tb], 32, 64);
     // |x|^2 below 2^-100 may have lost its square terms to underflow: such a
     // token gets an infinite bound and is listed for the float64 path
     kx[tb] = xs >= 7.88860905e-31f ? KXC * sqrtf(xs) : INFINITY;
@@ -371,25 +393,8 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
     asm volatile("" ::"v"(kx[tb]));
   }
 
-  // LDS DMA lanes: row rr[i] of the tile's 3*CT part-rows, chunk pch
-  const int pch = l % CPR;
-  const int ntiles = (C + CT - 1) / CT;
-  auto issue = [&](int tile, int slot) {
-    const int c0 = tile * CT;
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int row = (w * NI + i) * RPI + l / CPR;
-      const int part = row / CT, r = row % CT;
-      const int v = min(c0 + r, C - 1);
-      const bf16_t* src = P1 + part * plane + (size_t)v * D + 8 * (pch ^ km_swz<D>(r));
-      km_dma16(src, km_lds_addr(&Wt[slot][0] + (w * NI + i) * 512));
-    }
-    if (w == 0 && l < CT / 4) km_dma16(bh + c0 + 4 * l, km_lds_addr(&Bt[slot][0]));
-  };
-#pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < ntiles) issue(p, p);
-  const int swk = km_swz<D>(c16);
+  const int swk = km_swz<D>(c32);
+  const int rowo = c32 * D;
   for (int t = 0; t < ntiles; ++t) {
     // own DMAs of tile t done (wavefront 0 also fetches the b tile)
     if (NS > 2 && t + 1 < ntiles) {
@@ -404,63 +409,59 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
     const bf16_t* W1 = &Wt[slot][0];
     const bf16_t* W2 = W1 + CT * D;
     const bf16_t* W3 = W2 + CT * D;  // third part (NP == 3)
+    f32x16_t ahi[TB], arest[TB];
 #pragma unroll
-    for (int cb = 0; cb < CT / 16; ++cb) {
-      f32x4_t ahi[TB], arest[TB];
+    for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        ahi[tb][q] = 0.0f;
+        arest[tb][q] = 0.0f;
+      }
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int co = rowo + 8 * ((2 * s + hf) ^ swk);
+      const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
+      const bf16x8_t a2 = *(const bf16x8_t*)(W2 + co);
+      bf16x8_t a3;
+      if constexpr (NP == 3) a3 = *(const bf16x8_t*)(W3 + co);
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
-        ahi[tb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        arest[tb] = ahi[tb];
-      }
-      const int rowo = (16 * cb + c16) * D;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const int co = rowo + 8 * ((4 * s + g) ^ swk);
-        const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
-        const bf16x8_t a2 = *(const bf16x8_t*)(W2 + co);
-        bf16x8_t a3;
-        if constexpr (NP == 3) a3 = *(const bf16x8_t*)(W3 + co);
-#pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-          ahi[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, xf[tb][s], ahi[tb], 0, 0, 0);
-          arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, xf[tb][s], arest[tb], 0, 0, 0);
-          if constexpr (NP == 3)
-            arest[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
-        }
-      }
-      const float4 b4 = *(const float4*)(&Bt[slot][16 * cb + 4 * g]);
-      const float bv[4] = {b4.x, b4.y, b4.z, b4.w};
-      const int vbase = t * CT + 16 * cb + 4 * g;
-#pragma unroll
-      for (int tb = 0; tb < TB; ++tb) {
-        float sc[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sc[r] = fmaf(-2.0f, ahi[tb][r] + arest[tb][r], bv[r]);
-        // minimum, second minimum and first argmin of the four
-        const float lo01 = fminf(sc[0], sc[1]), hi01 = fmaxf(sc[0], sc[1]);
-        const float lo23 = fminf(sc[2], sc[3]), hi23 = fmaxf(sc[2], sc[3]);
-        const int i01 = sc[1] < sc[0] ? 1 : 0, i23 = sc[3] < sc[2] ? 3 : 2;
-        const int im = lo23 < lo01 ? i23 : i01;
-        const float m = fminf(lo01, lo23);
-        const float m2 = fminf(fmaxf(lo01, lo23), fminf(hi01, hi23));
-        // two smallest of {best, L, m, m2}
-        const bool nb = m < best[tb];
-        L[tb] = fminf(fminf(L[tb], m2), fmaxf(best[tb], m));
-        best[tb] = fminf(best[tb], m);
-        bidx[tb] = nb ? vbase + im : bidx[tb];
+        ahi[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xf[tb][s], ahi[tb], 0, 0, 0);
+        arest[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, xf[tb][s], arest[tb], 0, 0, 0);
+        if constexpr (NP == 3)
+          arest[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
       }
     }
+    float bv[16];
+#pragma unroll
+    for (int bq = 0; bq < 4; ++bq) {
+      const float4 b4 = *(const float4*)(&Bt[slot][8 * bq + 4 * hf]);
+      bv[4 * bq] = b4.x;
+      bv[4 * bq + 1] = b4.y;
+      bv[4 * bq + 2] = b4.z;
+      bv[4 * bq + 3] = b4.w;
+    }
+    const int vbase = t * CT + 4 * hf;
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const float sc = fmaf(-2.0f, ahi[tb][q] + arest[tb][q], bv[q]);
+        const bool nb = sc < best[tb];
+        L[tb] = __builtin_amdgcn_fmed3f(best[tb], L[tb], sc);
+        best[tb] = fminf(best[tb], sc);
+        bidx[tb] = nb ? vbase + 8 * (q >> 2) + (q & 3) : bidx[tb];
+      }
   }
   const float nmax = mx_s[0], ebmax = mx_s[1];
   bool fl[TB];
   float ubv[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
-    // merge over the four lane groups holding this token (ties: lowest id)
-#pragma unroll
-    for (int o = 16; o <= 32; o <<= 1) {
-      const float ob = __shfl_xor(best[tb], o, 64), oL = __shfl_xor(L[tb], o, 64);
-      const int oi = __shfl_xor(bidx[tb], o, 64);
+    // merge the two halves holding this token (ties: lowest id)
+    {
+      const float ob = __shfl_xor(best[tb], 32, 64), oL = __shfl_xor(L[tb], 32, 64);
+      const int oi = __shfl_xor(bidx[tb], 32, 64);
       const bool mine_valid = bidx[tb] >= 0, other_valid = oi >= 0;
       const bool take = other_valid && (!mine_valid || ob < best[tb] ||
                                         (ob == best[tb] && oi < bidx[tb]));
@@ -470,10 +471,10 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       best[tb] = take ? ob : best[tb];
       bidx[tb] = take ? oi : bidx[tb];
     }
-    const int tok = t0 + 16 * tb + c16;
+    const int tok = t0 + 32 * tb + c32;
     fl[tb] = false;
     ubv[tb] = INFINITY;  // an upper bound of the smallest exact score
-    if (g == 0 && tok < N) {
+    if (hf == 0 && tok < N) {
       bool ok = false;
       if (bidx[tb] >= 0 && isfinite(best[tb])) {
         const int v = bidx[tb];
@@ -486,7 +487,7 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
       fl[tb] = !ok;
     }
   }
-  // listed tokens: this tile's list at flags[h][256 * tile ...] in lane
+  // listed tokens: this tile's list at flags[h][kmeans_tile * tile ...] in lane
   // order, its length in nflag[h][tile]; no atomics
   uint64_t bal[TB];
   int tot = 0;
@@ -497,7 +498,7 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
   }
   if (l == 0) wcnt[w] = tot;
   __syncthreads();
-  int base = blockIdx.x * 256;
+  int base = blockIdx.x * kmeans_tile;
   for (int q = 0; q < w; ++q) base += wcnt[q];
   if (tid == 0) nflag[(size_t)h * gridDim.x + blockIdx.x] = wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
   if (tot > 0) {
@@ -506,7 +507,7 @@ __global__ __launch_bounds__(256) void k_assign_fast(const bf16_t* __restrict__ 
     for (int tb = 0; tb < TB; ++tb) {
       if (fl[tb]) {
         const int slot = base + __popcll(bal[tb] & below);
-        flags[(size_t)h * N + slot] = t0 + 16 * tb + c16;
+        flags[(size_t)h * N + slot] = t0 + 32 * tb + c32;
         flagu[(size_t)h * N + slot] = ubv[tb];
       }
       base += __popcll(bal[tb]);
@@ -584,11 +585,11 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
   const int h = item / rg, wg = item - h * rg;
   const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // listed tokens of head h: per 256-token tile lists of the fast pass
-  const int NT = (N + 255) / 256;
+  // listed tokens of head h: per-tile lists of the fast pass
+  const int NT = (N + kmeans_tile - 1) / kmeans_tile;
   const int* nf = nflag + (size_t)h * NT;
   int cnt = 0;
-  for (int t = tid; t < NT; t += 256) cnt += min(max(nf[t], 0), 256);
+  for (int t = tid; t < NT; t += 256) cnt += min(max(nf[t], 0), kmeans_tile);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
   if (l == 0) wsc[w] = cnt;
@@ -632,7 +633,7 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
       int carry = 0;
       for (int p0 = 0; p0 < NT && carry < lo + TC; p0 += 256) {
         const int t = p0 + tid;
-        const int c = t < NT ? min(max(nf[t], 0), 256) : 0;
+        const int c = t < NT ? min(max(nf[t], 0), kmeans_tile) : 0;
         int inc = c;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
@@ -650,7 +651,7 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
         }
         pre += inc - c;
         const int a0 = max(pre, lo), a1 = min(pre + c, lo + TC);
-        for (int i = a0; i < a1; ++i) spos[i - lo] = t * 256 + (i - pre);
+        for (int i = a0; i < a1; ++i) spos[i - lo] = t * kmeans_tile + (i - pre);
         carry += tot;
       }
     }
@@ -1122,12 +1123,12 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
                 fast ? kb.eb : nullptr, kb.hmax);
     if constexpr (fast) {
       if (C >= 512)
-        PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 2>), dim3((N + 255) / 256, H),
+        PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 2>), dim3((N + kmeans_tile - 1) / kmeans_tile, H),
                     dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
                     (const float*)kb.b32, kmeans_cpad(C), (const float*)kb.wn, (const float*)kb.eb,
                     (const float*)kb.hmax, nbm, N, C, kb.labels, kb.flags, kb.flagu, kb.nflag);
       else
-        PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 3>), dim3((N + 255) / 256, H),
+        PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 3>), dim3((N + kmeans_tile - 1) / kmeans_tile, H),
                     dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
                     (const float*)kb.b32, kmeans_cpad(C), (const float*)kb.wn, (const float*)kb.eb,
                     (const float*)kb.hmax, nbm, N, C, kb.labels, kb.flags, kb.flagu, kb.nflag);

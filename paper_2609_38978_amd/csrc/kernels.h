@@ -25,6 +25,13 @@ park_status launch_gather(const void* X, const int* perm, int H, int N, int D, i
 // centroid count padded to the fast assignment's tile multiple
 inline int kmeans_cpad(int C) { return (C + 63) / 64 * 64; }
 
+// tokens per fast-assignment workgroup, 128 per block of 32 tokens a
+// wavefront holds; the tokens left for the float64 refine are listed per such tile
+#ifndef PARK_KM_TB
+#define PARK_KM_TB 2
+#endif
+constexpr int kmeans_tile = 128 * PARK_KM_TB;
+
 // key-block count padded to the fast retrieval's tile multiple
 inline int pama_ckpad(int CK) { return (CK + 63) / 64 * 64; }
 
@@ -44,8 +51,8 @@ struct KmeansBufs {
   float* wn;      // [H][kmeans_cpad(C)] |w_v| (rounded up), padding 0
   float* eb;      // [H][kmeans_cpad(C)] |b_v| term of the fast-path bound, padding 0
   float* hmax;    // [H][ceil(C/16)][2] per-block max |w_v|, max eb_v
-  int* nflag;     // [H][ceil(N/256)] tokens of each 256-token tile left for the float64 refine
-  int* flags;     // [H][N]    their indices, tile t's list at 256 t
+  int* nflag;     // [H][ceil(N/kmeans_tile)] tokens of each tile left for the float64 refine
+  int* flags;     // [H][N]    their indices, tile t's list at kmeans_tile * t
   float* flagu;   // [H][N]    and an upper bound of their smallest exact score
 };
 park_status launch_kmeans(const void* X, const double* Gbar /* null = Euclidean */, int H, int N,

@@ -152,7 +152,7 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   c.wn = cv.take<float>((size_t)H * kmeans_cpad(C));
   c.eb = cv.take<float>((size_t)H * kmeans_cpad(C));
   c.hmax = cv.take<float>((size_t)2 * H * ((C + 15) / 16));
-  c.nflag = cv.take<int>((size_t)H * ((N + 255) / 256));
+  c.nflag = cv.take<int>((size_t)H * ((N + kmeans_tile - 1) / kmeans_tile));
   c.flags = cv.take<int>((size_t)H * N);
   c.flagu = cv.take<float>((size_t)H * N);
   return c;
