@@ -362,6 +362,7 @@ __global__ __launch_bounds__(256) void k_select64(const double* __restrict__ W64
 // in float64.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // Splits the centroids into three bf16 planes and records log n_v (-inf for
 // empty blocks), |c_v| rounded up, and per-block maxima of |c_v| and |log n_v|.
@@ -434,51 +435,117 @@ __device__ __forceinline__ uint32_t pm_lds_addr(const void* p) {
 }
 template <int D>
 __device__ __forceinline__ int pm_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+// waits until at most N vector-memory operations of this wavefront are outstanding
+template <int N>
+__device__ __forceinline__ void pm_wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
-// Workgroup = one (query block, head); the block's rows in chunks of 64
-// (4 wavefronts x 16 queries), each chunk streaming the key-block centroids
-// twice (normaliser pass, probability pass).  Centroid tiles of 32 rows of
-// the three parts (and their log n_v) go from HBM to a two-slot LDS ring by
-// LDS DMA, the next tile in flight while this one is scored; rows are
-// swizzled in 16-byte chunks so the B-operand reads are free of bank
-// conflicts.  The (query block, head) items of a head run on one XCD.
-// Online normaliser with one exp2 per logit: for d = S - m (m the running
-// maximum), z += 2^d when d <= 0, else z = z 2^-d + 1 and m = S.
+// Block plan of the fast retrieval: per head, the query blocks sorted by
+// their number of 64-row chunks (descending, ties by id) and dealt in groups
+// of four, one block per wavefront, so the four blocks of a workgroup need
+// about the same number of rounds.  plan[h][g] = four block ids (-1: none).
+// One workgroup of 1024 threads per head, CQ <= 2048.
+__global__ __launch_bounds__(1024) void k_pama_plan(const int* __restrict__ q_offsets, int N, int CQ,
+                                                    int G4, int4* __restrict__ plan) {
+  __shared__ uint32_t key[MAXC];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  const int* off = q_offsets + (size_t)h * (CQ + 1);
+  int SZ = 2;
+  while (SZ < CQ) SZ <<= 1;
+  for (int u = tid; u < SZ; u += 1024) {
+    uint32_t k = 0xffffffffu;
+    if (u < CQ) {
+      const int a = min(max(off[u], 0), N), b = min(max(off[u + 1], a), N);
+      const int nch = min((b - a + 63) >> 6, 65535);
+      k = ((uint32_t)(65535 - nch) << 16) | (uint32_t)u;
+    }
+    key[u] = k;
+  }
+  __syncthreads();
+  for (int len = 2; len <= SZ; len <<= 1)
+    for (int j = len >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < SZ; i += 1024) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const uint32_t x = key[i], y = key[ixj];
+          const bool up = (i & len) == 0;
+          if ((x > y) == up) {
+            key[i] = y;
+            key[ixj] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  for (int g = tid; g < G4; g += 1024) {
+    int u[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int p = 4 * g + k;
+      u[k] = p < CQ ? (int)(key[p] & 0xffffu) : -1;
+    }
+    plan[(size_t)h * G4 + g] = make_int4(u[0], u[1], u[2], u[3]);
+  }
+}
+
+// Fast retrieval.  A workgroup takes four query blocks of one head (one per
+// wavefront, from the plan) and streams the head's key-block centroids
+// through an NS-slot LDS ring (32 rows of the three bf16 parts per tile, LDS
+// DMA, rows swizzled in 16-byte chunks), twice per round of 64-row chunks:
+// pass 1 builds each query's normaliser, pass 2 sums the probabilities over
+// the block's queries.  Every tile serves 256 queries.
+//
+// MFMA 32x32x16 on two 32-query groups per wavefront.  The query fragment
+// (query l%32, dims 16 s + 8 (l/32) ..) and the centroid fragment (centroid
+// l%32, same dims) serve as either operand, so pass 1 computes S^T (lane:
+// one query, centroids 8b + 4(l/32) + r) and pass 2 computes S (lane: one
+// centroid, queries 8b + 4(l/32) + r); each pass then reduces within lanes.
+// Accuracy as in the float error bound below: the c1 part is accumulated in
+// 32-dimension segments (two MFMAs from zero) added in float, the two small
+// parts in one chain over all dimensions.
+//
+// Scores are kept in log2 units, s' = (q.c / sqrt(d) + log n_v) log2 e.
+// Pass 1 keeps per query a reference maximum m and z = sum 2^(s' - m) (one
+// rescale per tile, tile terms added in a tree); pass 2 uses
+// c_q = m + log2 z, so p = 2^(s' - c_q).
 template <int D>
-__global__ __launch_bounds__(256) void k_pama_fast(const bf16_t* __restrict__ Qp,
-                                                   const int* __restrict__ q_offsets,
-                                                   const bf16_t* __restrict__ c3, size_t plane,
-                                                   const float* __restrict__ lg, int CKpad,
-                                                   const float* __restrict__ bmax, int nbm, int H,
-                                                   int N, int CQ, int CK, float* __restrict__ W32,
-                                                   float* __restrict__ delta) {
-  constexpr int CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
+__global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__ Qp,
+                                                      const int* __restrict__ q_offsets,
+                                                      const int4* __restrict__ plan, int G4,
+                                                      const bf16_t* __restrict__ c3, size_t plane,
+                                                      const float* __restrict__ lg, int CKpad,
+                                                      const float* __restrict__ bmax, int nbm, int H,
+                                                      int N, int CQ, int CK, float* __restrict__ W32,
+                                                      float* __restrict__ delta) {
+  constexpr int CT = 32, KS = D / 16, CPR = D / 8, RPI = 64 / CPR;
   constexpr int NI = 3 * CT / (4 * RPI);  // DMAs per wavefront and tile
-  static_assert(NI * 4 * RPI == 3 * CT, "tile shape");
+  static_assert(NI * 4 * RPI == 3 * CT && KS % 2 == 0, "tile shape");
+  constexpr int NS = 3;
   constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f, L2E = 1.4426950408889634f;
-  constexpr float ET = U24 * 1.01f + (32.0f * DEL + (KS - 1) * U24) * 1.01f +
+  constexpr float ET = U24 * 1.01f + (32.0f * DEL + (KS / 2 - 1) * U24) * 1.01f +
                        0.00390625f * 1.01f * (2 * D) * DEL + U24 * 1.01f;
-  __shared__ __attribute__((aligned(16))) bf16_t Ct[2][3 * CT * D];  // [slot][part][row][D]
-  __shared__ __attribute__((aligned(16))) float Lt[2][CT];
-  extern __shared__ float wacc[];  // [4][CK]
-  __shared__ float qn_s[4][16];
-  __shared__ float red[4];
+  __shared__ __attribute__((aligned(16))) bf16_t Ct[NS][3 * CT * D];  // [slot][part][row][D]
+  __shared__ __attribute__((aligned(16))) float Lt[NS][CT];
+  __shared__ __attribute__((aligned(16))) float cbuf[4][64];  // c_q of each wavefront's chunk
+  __shared__ int rnd[4];
   __shared__ float mx_s[2];
-  const int nitems = CQ * H, per = (nitems + 7) >> 3;
+  const int nitems = G4 * H, per = (nitems + 7) >> 3;
   const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
   if (item >= nitems) return;
-  const int h = item / CQ, u = item - h * CQ;
-  const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
+  const int h = item / G4, grp4 = item - h * G4;
+  const int tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int4 pl = plan[(size_t)h * G4 + grp4];
+  const int ub = w == 0 ? pl.x : w == 1 ? pl.y : w == 2 ? pl.z : pl.w;
+  const int u = (unsigned)ub < (unsigned)CQ ? ub : -1;
   const int* off = q_offsets + (size_t)h * (CQ + 1);
-  const int q0 = min(max(off[u], 0), N), q1 = min(max(off[u + 1], q0), N);
+  const int q0 = u >= 0 ? min(max(off[u], 0), N) : 0;
+  const int q1 = u >= 0 ? min(max(off[u + 1], q0), N) : 0;
   const int nu = q1 - q0;
-  const size_t wrow = ((size_t)h * CQ + u) * CK;
-  if (nu <= 0) {
-    for (int v = tid; v < CK; v += 256) W32[wrow + v] = 0.0f;
-    if (tid == 0) delta[(size_t)h * CQ + u] = 0.0f;
-    return;
-  }
+  const int nch = (nu + 63) >> 6;
+  const size_t wrow = ((size_t)h * CQ + (u >= 0 ? u : 0)) * CK;
+  if (l == 0) rnd[w] = nch;
   if (tid < 64) {
     float a = 0.0f, c = 0.0f;
     for (int i = tid; i < nbm; i += 64) {
@@ -494,13 +561,16 @@ __global__ __launch_bounds__(256) void k_pama_fast(const bf16_t* __restrict__ Qp
       mx_s[1] = c;
     }
   }
-  for (int v = tid; v < 4 * CK; v += 256) wacc[v] = 0.0f;
-  const float isd = 1.0f / sqrtf((float)D);
+  __syncthreads();
+  const int nrounds = max(max(rnd[0], rnd[1]), max(rnd[2], rnd[3]));
+  const float cmax = mx_s[0], lgmax = mx_s[1];
+  if (u >= 0 && nu == 0) {  // empty block: zero row, exact
+    for (int v = l; v < CK; v += 64) W32[wrow + v] = 0.0f;
+    if (l == 0) delta[(size_t)h * CQ + u] = 0.0f;
+  }
+  const float isd = 1.0f / sqrtf((float)D), isdL = isd * L2E;
   const bf16_t* P1 = c3 + (size_t)h * CK * D;
   const float* lgh = lg + (size_t)h * CKpad;
-  const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
-  float dmax = 0.0f;  // per-thread max of the row error bound
-
   const int pch = l % CPR;
   const int nt = (CK + CT - 1) / CT;
   auto issue = [&](int tile, int slot) {
@@ -515,26 +585,85 @@ __global__ __launch_bounds__(256) void k_pama_fast(const bf16_t* __restrict__ Qp
     }
     if (w == 0 && l < CT / 4) pm_dma16(lgh + c0 + 4 * l, pm_lds_addr(&Lt[slot][0]));
   };
+  // the centroid fragment of this lane: row c32 of a tile, dims 16 s + 8 hf ..
+  const int crow = c32 * D, cswz = pm_swz<D>(c32);
 
-  const int nch = (nu + 63) / 64;
-  const int total = nch * 2 * nt;
-  bf16x8_t qf[KS];
-  bool rv[4];
-  float m[4], z[4], mf[4], iz[4];
-  issue(0, 0);
-  const int swc = pm_swz<D>(c16);
-  for (int it = 0; it < total; ++it) {
-    const int tile = it % nt, pass = (it / nt) & 1, r0 = q0 + 64 * (it / (2 * nt));
-    if (tile == 0 && pass == 0) {
-      // A operand: this wavefront's 16 queries of the chunk (query c16, dims 32s + 8g ..)
-      const int qa = r0 + 16 * w + c16;
+  float dmax = 0.0f;  // this wavefront's relative error bound
+  const int total = nrounds * 2 * nt;
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < total) issue(p % nt, p);
+  // ring step of tile `it`: own DMAs done, barrier, next tile issued; its slot
+  int it = 0;
+  auto ring_step = [&]() {
+    if (it + 1 < total) {
+      if (w == 0) pm_wait_vmcnt<NI + 1>();
+      else pm_wait_vmcnt<NI>();
+    } else {
+      pm_wait_vmcnt<0>();
+    }
+    __syncthreads();  // tile landed everywhere; the tile before consumed (its slot is free)
+    if (it + NS - 1 < total) issue((it + NS - 1) % nt, (it + NS - 1) % NS);
+    return it % NS;
+  };
+  // products of both query groups with one tile: S^T (pass 1: lane = query,
+  // 16 centroids) or S (pass 2: lane = centroid, 16 queries); c1 part in
+  // 32-dimension segments (two MFMAs from zero) added in float, c2 + c3 in
+  // one chain over all dimensions
+  auto products = [&](const bf16x8_t (*q2)[KS], const bf16_t* B1, bool qa_left, f32x16_t* hi,
+                      f32x16_t* rest) {
+    const bf16_t* B2 = B1 + CT * D;
+    const bf16_t* B3 = B2 + CT * D;
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) rest[g][q] = 0.0f;
+#pragma unroll
+    for (int sp = 0; sp < KS / 2; ++sp) {
+      f32x16_t seg[2];
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) seg[g][q] = 0.0f;
+#pragma unroll
+      for (int s = 2 * sp; s < 2 * sp + 2; ++s) {
+        const int co = crow + 8 * ((2 * s + hf) ^ cswz);
+        const bf16x8_t b1 = *(const bf16x8_t*)(B1 + co);
+        const bf16x8_t b2 = *(const bf16x8_t*)(B2 + co);
+        const bf16x8_t b3 = *(const bf16x8_t*)(B3 + co);
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          if (qa_left) {
+            seg[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q2[g][s], b1, seg[g], 0, 0, 0);
+            rest[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q2[g][s], b2, rest[g], 0, 0, 0);
+            rest[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q2[g][s], b3, rest[g], 0, 0, 0);
+          } else {
+            seg[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, q2[g][s], seg[g], 0, 0, 0);
+            rest[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b2, q2[g][s], rest[g], 0, 0, 0);
+            rest[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b3, q2[g][s], rest[g], 0, 0, 0);
+          }
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < 2; ++g) hi[g] = sp == 0 ? seg[g] : hi[g] + seg[g];
+    }
+  };
+  bf16x8_t qf[2][KS];
+  for (int rr = 0; rr < nrounds; ++rr) {
+    // this round's chunk: queries q0 + 64 rr + 32 g + l%32
+    const bool on = 64 * rr < nu;
+    float m[2], z[2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const int qa = q0 + 64 * rr + 32 * g + c32;
+      const bool qv = on && qa < q1;
       float qsq = 0.0f;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-        if (qa < q1) raw = *(const uint4*)(Qp + ((size_t)h * N + qa) * D + 32 * s + 8 * g);
-        qf[s] = __builtin_bit_cast(bf16x8_t, raw);
-        asm volatile("" ::"v"(qf[s]));  // loads complete here, not inside the tile loop
+        if (qv) raw = *(const uint4*)(Qp + ((size_t)h * N + qa) * D + 16 * s + 8 * hf);
+        qf[g][s] = __builtin_bit_cast(bf16x8_t, raw);
+        asm volatile("" ::"v"(qf[g][s]));  // loads complete here, not inside the ring waits
         const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -542,110 +671,107 @@ __global__ __launch_bounds__(256) void k_pama_fast(const bf16_t* __restrict__ Qp
           qsq = fmaf(lo, lo, fmaf(hi, hi, qsq));
         }
       }
-      qsq += __shfl_xor(qsq, 16, 64);
       qsq += __shfl_xor(qsq, 32, 64);
-      if (g == 0) qn_s[w][c16] = sqrtf(qsq) * 1.0001f;
-      // outputs: lane holds queries 4g + r (r = 0..3) of this wavefront
+      if (qv) {
+        // row error bound of this query (|q| rounded up)
+        const float qn = sqrtf(qsq) * 1.0001f;
+        const float ei = isd * (ET + 1.01f * U24) * qn * cmax +
+                         1.01f * U24 * (3.0f * lgmax + 2.02f * isd * qn * cmax);
+        const float argmax = 2.0f * (isd * qn * cmax + lgmax) * L2E;
+        const float nadd = fmaxf((float)(CK / 16 + 1), (float)(CK / 32 + 5));
+        const float dZ = DEL * (10.0f + 3.0f * log2f((float)CK + 1.0f) + 2.0f * nadd +
+                                3.0f * argmax) +
+                         2.0f * U24 * (nadd + 24.0f);
+        dmax = fmaxf(dmax, 2.02f * ei + dZ +
+                               DEL * (3.0f + 2.5f * argmax + 2.0f * log2f((float)CK + 1.0f)));
+      }
+      m[g] = -INFINITY;
+      z[g] = 0.0f;
+    }
+    // pass 1: lane holds query c32 of each group, centroids c0 + 8b + 4hf + r
+    for (int tile = 0; tile < nt; ++tile, ++it) {
+      const int slot = ring_step();
+      if (!on) continue;
+      f32x16_t hi[2], rest[2];
+      products(qf, &Ct[slot][0], false, hi, rest);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        rv[r] = r0 + 16 * w + 4 * g + r < q1;
-        m[r] = -INFINITY;
-        z[r] = 0.0f;
+      for (int g = 0; g < 2; ++g) {
+        float sv[16];
+#pragma unroll
+        for (int bq = 0; bq < 4; ++bq) {
+          const float4 l4 = *(const float4*)(&Lt[slot][8 * bq + 4 * hf]);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            sv[4 * bq + r] = fmaf(hi[g][4 * bq + r] + rest[g][4 * bq + r], isdL, lv[r] * L2E);
+        }
+        float tmax = fmaxf(sv[0], sv[1]);
+#pragma unroll
+        for (int q = 2; q < 16; ++q) tmax = fmaxf(tmax, sv[q]);
+        const float mn = fmaxf(m[g], tmax);
+        if (mn != -INFINITY) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) sv[q] = __builtin_amdgcn_exp2f(sv[q] - mn);
+#pragma unroll
+          for (int o = 8; o > 0; o >>= 1)
+#pragma unroll
+            for (int q = 0; q < o; ++q) sv[q] += sv[q + o];
+          z[g] = (m[g] == mn ? z[g] : z[g] * __builtin_amdgcn_exp2f(m[g] - mn)) + sv[0];
+          m[g] = mn;
+        }
       }
     }
-    if (tile == 0 && pass == 1) {
-      // merge (max, sum) over the 16 lanes holding the same queries
+    // c_q = m + log2 z per query (halves merged); invalid queries +inf
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float mm = m[r], zz = z[r];
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) {
-          const float om = __shfl_xor(mm, o, 64), oz = __shfl_xor(zz, o, 64);
-          const float nm = fmaxf(mm, om);
-          zz = (nm == -INFINITY) ? 0.0f
-                                 : zz * __builtin_amdgcn_exp2f((mm - nm) * L2E) +
-                                       oz * __builtin_amdgcn_exp2f((om - nm) * L2E);
-          mm = nm;
-        }
-        mf[r] = mm;
-        iz[r] = zz > 0.0f ? 1.0f / zz : 0.0f;
-      }
+    for (int g = 0; g < 2; ++g) {
+      const float om = __shfl_xor(m[g], 32, 64), oz = __shfl_xor(z[g], 32, 64);
+      const float M = fmaxf(m[g], om);
+      float zz = 0.0f;
+      if (M != -INFINITY)
+        zz = z[g] * __builtin_amdgcn_exp2f(m[g] - M) + oz * __builtin_amdgcn_exp2f(om - M);
+      const int qa = q0 + 64 * rr + 32 * g + c32;
+      const float c = (on && qa < q1 && zz > 0.0f) ? M + __builtin_amdgcn_logf(zz) : INFINITY;
+      if (hf == 0) cbuf[w][32 * g + c32] = c;
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();  // tile landed everywhere; previous tile consumed (its slot is free)
-    if (it + 1 < total) issue((it + 1) % nt, (it + 1) & 1);
-    const bf16_t* B1 = &Ct[it & 1][0];
-    const bf16_t* B2 = B1 + CT * D;
-    const bf16_t* B3 = B2 + CT * D;
-    const int c0 = tile * CT;
+    // pass 2: lane holds centroid c0 + c32, queries 8b + 4hf + r of each group
+    for (int tile = 0; tile < nt; ++tile, ++it) {
+      const int slot = ring_step();
+      if (!on) continue;
+      const float lgj = Lt[slot][c32] * L2E;
+      float ws = 0.0f;
+      f32x16_t hi[2], rest[2];
+      products(qf, &Ct[slot][0], true, hi, rest);
 #pragma unroll
-    for (int cb = 0; cb < CT / 16; ++cb) {
-      f32x4_t shi = zero, srest = zero;
-      const int rowo = (16 * cb + c16) * D;
+      for (int g = 0; g < 2; ++g) {
+        float e[16];
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const int co = rowo + 8 * ((4 * s + g) ^ swc);
-        const bf16x8_t b1 = *(const bf16x8_t*)(B1 + co);
-        const bf16x8_t b2 = *(const bf16x8_t*)(B2 + co);
-        const bf16x8_t b3 = *(const bf16x8_t*)(B3 + co);
-        shi += __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b1, zero, 0, 0, 0);
-        srest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b2, srest, 0, 0, 0);
-        srest = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], b3, srest, 0, 0, 0);
-      }
-      const float lgv = Lt[it & 1][16 * cb + c16];  // this lane's centroid
-      if (pass == 0) {
-        if (lgv != -INFINITY) {
+        for (int bq = 0; bq < 4; ++bq) {
+          const float4 c4 = *(const float4*)(&cbuf[w][32 * g + 8 * bq + 4 * hf]);
+          const float cv[4] = {c4.x, c4.y, c4.z, c4.w};
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float sv = fmaf(shi[r] + srest[r], isd, lgv);
-            const float d = sv - m[r];  // +inf while m = -inf
-            const float e = __builtin_amdgcn_exp2f(-fabsf(d) * L2E);
-            z[r] = d <= 0.0f ? z[r] + e : fmaf(z[r], e, 1.0f);
-            m[r] = fmaxf(m[r], sv);
-          }
+          for (int r = 0; r < 4; ++r)
+            e[4 * bq + r] = __builtin_amdgcn_exp2f(
+                fmaf(hi[g][4 * bq + r] + rest[g][4 * bq + r], isdL, lgj) - cv[r]);
         }
-      } else {
-        float cs = 0.0f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float sv = fmaf(shi[r] + srest[r], isd, lgv);
-          const float p = (rv[r] && sv != -INFINITY)
-                              ? __builtin_amdgcn_exp2f((sv - mf[r]) * L2E) * iz[r]
-                              : 0.0f;
-          cs += p;
-        }
-        cs += __shfl_xor(cs, 16, 64);
-        cs += __shfl_xor(cs, 32, 64);
-        const int v = c0 + 16 * cb + c16;
-        if (g == 0 && v < CK) wacc[w * CK + v] += cs;
+        for (int o = 8; o > 0; o >>= 1)
+#pragma unroll
+          for (int q = 0; q < o; ++q) e[q] += e[q + o];
+        ws += e[0];
       }
-    }
-    if (pass == 1 && tile == nt - 1) {
-      // row error bound for this wavefront's queries (lane holds query c16's norm)
-      const float cmax = mx_s[0], lgmax = mx_s[1];
-      const float qn = (16 * w + c16 + r0 < q1) ? qn_s[w][c16] : 0.0f;
-      const float ei = isd * (ET + 1.01f * U24) * qn * cmax +
-                       1.01f * U24 * (2.0f * lgmax + 1.01f * isd * qn * cmax);
-      const float argmax = 2.0f * (isd * qn * cmax + lgmax) * L2E;
-      // normaliser: element exp2 errors weighted by p (sum_j p_j |x_j| <= 2 log2 CK),
-      // the online rescales (their arguments add up to at most argmax), the
-      // lane merges, and the float additions
-      const float dZ = DEL * (10.0f + 3.0f * log2f((float)CK + 1.0f) + 2.0f * (CK / 16 + 1) +
-                              3.0f * argmax) +
-                       2.0f * U24 * (CK / 16 + 24);
-      dmax = fmaxf(dmax, 2.02f * ei + dZ + DEL * (3.0f + 1.5f * argmax));
+      ws += __shfl_xor(ws, 32, 64);
+      const int v = tile * CT + c32;
+      if (hf == 0 && v < CK) {
+        const float add = ws / (float)nu;
+        W32[wrow + v] = rr == 0 ? add : W32[wrow + v] + add;
+      }
     }
   }
-  __syncthreads();
-  const float inv_n = 1.0f / (float)nu;
-  for (int v = tid; v < CK; v += 256)
-    W32[wrow + v] = (((wacc[v] + wacc[CK + v]) + wacc[2 * CK + v]) + wacc[3 * CK + v]) * inv_n;
-  for (int o = 32; o > 0; o >>= 1) dmax = fmaxf(dmax, __shfl_xor(dmax, o, 64));
-  if (l == 0) red[w] = dmax;
-  __syncthreads();
-  if (tid == 0)
-    delta[(size_t)h * CQ + u] =
-        (fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])) + 17.0f * U24) * 1.01f;
+  if (u >= 0 && nu > 0) {
+    for (int o = 32; o > 0; o >>= 1) dmax = fmaxf(dmax, __shfl_xor(dmax, o, 64));
+    if (l == 0)
+      delta[(size_t)h * CQ + u] = (dmax + (17.0f + 2.0f * nch) * U24) * 1.01f;
+  }
 }
 
 // Certified selection on the float W^: sort (W^ descending, id ascending),
@@ -801,29 +927,22 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   const int nbm = (CK + 15) / 16;
   float* W32 = W_out ? W_out : rb.W32;
   const int CKpad = pama_ckpad(CK);
-  const unsigned nwg = 8u * (((unsigned)CQ * (unsigned)H + 7u) / 8u);  // XCD remap: every item owns one
-  const size_t lds = (size_t)4 * CK * sizeof(float);
-  // reserved once for the largest CK (2048), outside any stream capture that may follow
-  static const hipError_t attr128 = hipFuncSetAttribute(
-      (const void*)k_pama_fast<128>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)(4 * MAXC * sizeof(float)));
-  static const hipError_t attr64 = hipFuncSetAttribute(
-      (const void*)k_pama_fast<64>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)(4 * MAXC * sizeof(float)));
-  if (attr128 != hipSuccess || attr64 != hipSuccess)
-    return fail(PARK_ERR_HIP, "retrieval: cannot reserve %zu bytes of LDS", lds);
+  // four query blocks per workgroup (size-sorted plan); XCD remap: every item owns one
+  const int G4 = (CQ + 3) / 4;
+  const unsigned nwg = 8u * (((unsigned)G4 * (unsigned)H + 7u) / 8u);
+  PARK_LAUNCH("pama_plan", k_pama_plan, dim3(H), dim3(1024), 0, st, q_offsets, N, CQ, G4, rb.qplan);
   if (D == 128) {
     PARK_LAUNCH("pama_cen_prep", k_cen_prep<128>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
                 rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
-    PARK_LAUNCH("pama_fast", k_pama_fast<128>, dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
-                q_offsets, (const bf16_t*)rb.c3, plane, (const float*)rb.lg, CKpad,
-                (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
+    PARK_LAUNCH("pama_fast", k_pama_fast<128>, dim3(nwg), dim3(256), 0, st, (const bf16_t*)Qp,
+                q_offsets, (const int4*)rb.qplan, G4, (const bf16_t*)rb.c3, plane,
+                (const float*)rb.lg, CKpad, (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
   } else {
     PARK_LAUNCH("pama_cen_prep", k_cen_prep<64>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
                 rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
-    PARK_LAUNCH("pama_fast", k_pama_fast<64>, dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
-                q_offsets, (const bf16_t*)rb.c3, plane, (const float*)rb.lg, CKpad,
-                (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
+    PARK_LAUNCH("pama_fast", k_pama_fast<64>, dim3(nwg), dim3(256), 0, st, (const bf16_t*)Qp,
+                q_offsets, (const int4*)rb.qplan, G4, (const bf16_t*)rb.c3, plane,
+                (const float*)rb.lg, CKpad, (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
   }
   PARK_LAUNCH("pama_reset", k_zero_counts, dim3((H + 63) / 64), dim3(64), 0, st, rb.nrows, H);
   PARK_LAUNCH("select_fast", k_select_fast, dim3(CQ, H), dim3(256), 0, st, (const float*)W32,

@@ -73,6 +73,7 @@ struct RetrieveBufs {
   float* lg;      // [H][pama_ckpad(CK)] log n_v (-inf for empty and padding blocks)
   float* cn;      // [H][CK]     |c_v|
   float* bmax;    // [H][ceil(CK/16)][2] per-block max |c_v|, |log n_v|
+  int4* qplan;    // [H][ceil(CQ/4)] query blocks of each fast-retrieval workgroup
 };
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,

@@ -169,6 +169,7 @@ static RetrieveBufs carve_retrieve(Carver& cv, int H, int D, int CQ, int CK) {
   r.lg = cv.take<float>((size_t)H * pama_ckpad(CK));
   r.cn = cv.take<float>((size_t)H * CK);
   r.bmax = cv.take<float>((size_t)2 * H * ((CK + 15) / 16));
+  r.qplan = cv.take<int4>((size_t)H * ((CQ + 3) / 4));
   return r;
 }
 
