@@ -188,7 +188,8 @@ park_status park_retrieve_blocks(const void* Qp, const int32_t* q_offsets, const
  *   the selected key blocks of u (softmax renormalised over those keys).
  *   Qp, Kp, Vp [H][N][d] dtype;  O [H][N][d] out_dtype (PARK_F32 or PARK_BF16,
  *   bf16 by round-to-nearest-even).  Rows of empty query blocks do not exist;
- *   every token is written exactly once.
+ *   every token is written exactly once; the rows of a query block with
+ *   kv_count = 0 are written as zeros.
  *   ws: device workspace of at least park_workspace_size() bytes for these
  *   dims, CQ and CK (it holds the per-call work plan); PARK_ERR_WORKSPACE if
  *   smaller than the attention part of it. */

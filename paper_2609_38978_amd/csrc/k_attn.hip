@@ -212,6 +212,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 
@@ -637,6 +638,637 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t* __restrict__ Qp
   }
 }
 
+// ------------------------------------------------------------------------
+// Grouped block-sparse attention.
+//
+// Query blocks that select nearly the same key blocks share one key/value
+// stream: the plan orders the query blocks of a head by two MinHash values of
+// their selected key-block sets and cuts the concatenated rows into groups of
+// at most ATTN_R rows and ATTN_LB query blocks.  A workgroup streams the
+// union of its blocks' selections once (ascending key-block id) and each row
+// keeps only the keys of the key blocks its own query block selected, so the
+// result per row is the same renormalised softmax over its own selection.
+
+#ifndef PARK_ATTN_R
+#define PARK_ATTN_R 128
+#endif
+#ifndef PARK_ATTN_RING
+#define PARK_ATTN_RING 3
+#endif
+constexpr int ATTN_R = PARK_ATTN_R;  // rows per group (32 per wavefront)
+constexpr int ATTN_RING = PARK_ATTN_RING;  // K/V tiles of the LDS ring (all but one in flight)
+constexpr int ATTN_LB = 16;          // query blocks per group (bits of a selection word)
+
+static int attn_windows(int N) { return (N + ATTN_R - 1) / ATTN_R; }
+// groups per head: every window of ATTN_R rows, split further when it holds
+// more than ATTN_LB query blocks (a window boundary cuts at most one block)
+int attn_groups_per_head(int N, int CQ) {
+  const int W = attn_windows(N);
+  return W + (CQ + W + ATTN_LB - 1) / ATTN_LB + 1;
+}
+
+// Group plan of one head (1024 threads, CQ <= 2048):
+//   order[h][i]  query block at sorted position i (-1 past the blocks with rows)
+//   spre[h][i]   rows of the sorted blocks before position i (i <= CQ)
+//   grp[h][g]    {first row, end row, first position, end position}: rows in
+//                the coordinates of the sorted concatenation; {0,0,0,0} when
+//                g is past the last group.
+__global__ __launch_bounds__(1024) void k_attn_gplan(const int* __restrict__ q_offsets,
+                                                     const int* __restrict__ kv_count,
+                                                     const int* __restrict__ kv_index,
+                                                     const int* __restrict__ k_offsets, int N,
+                                                     int CQ, int CK, int GPH,
+                                                     int* __restrict__ order,
+                                                     int* __restrict__ spre,
+                                                     int4* __restrict__ grp) {
+  __shared__ unsigned long long key[2048];
+  __shared__ int pre[2049];
+  __shared__ int tiles[2048];  // key tiles of each query block's own selection (by block id)
+  __shared__ int tpos[2048];   // the same by sorted position
+  __shared__ int wsum[16];
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int* qo = q_offsets + (size_t)h * (CQ + 1);
+  const int* koff = k_offsets + (size_t)h * (CK + 1);
+  int SZ = 2;
+  while (SZ < CQ) SZ <<= 1;
+  // sort keys (first MinHash, top bits of the second, block id); blocks
+  // without rows sort last with the key ~0.  One wavefront per block.
+  for (int u = wid; u < SZ; u += 16) {
+    unsigned long long kk = ~0ull;
+    if (u < CQ) {
+      const int a = min(max(qo[u], 0), N), b = min(max(qo[u + 1], a), N);
+      if (b > a) {
+        const size_t row = (size_t)h * CQ + u;
+        const int n = min(max(kv_count[row], 0), CK);
+        const int* sel = kv_index + row * CK;
+        uint32_t m1 = 0xffffffffu, m2 = 0xffffffffu;
+        int nkey = 0;
+        for (int j = lane; j < n; j += 64) {
+          const uint32_t v = (uint32_t)sel[j];
+          m1 = min(m1, attn_hash(v));
+          m2 = min(m2, attn_hash(v + 7919u));
+          if (v < (uint32_t)CK) nkey += max(0, koff[v + 1] - koff[v]);
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+          m1 = min(m1, (uint32_t)__shfl_xor((int)m1, o, 64));
+          m2 = min(m2, (uint32_t)__shfl_xor((int)m2, o, 64));
+          nkey += __shfl_xor(nkey, o, 64);
+        }
+        if (lane == 0) tiles[u] = (nkey + 31) >> 5;
+        m1 = min(m1, 0xfffffffeu);
+        kk = ((unsigned long long)m1 << 32) | (m2 & 0xfffff800u) | (uint32_t)u;
+      }
+    }
+    if (lane == 0) key[u] = kk;
+  }
+  __syncthreads();
+  for (int len = 2; len <= SZ; len <<= 1)
+    for (int j = len >> 1; j > 0; j >>= 1) {
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int i = tid + 1024 * k, ixj = i ^ j;
+        if (i < SZ && ixj > i) {
+          const unsigned long long x = key[i], y = key[ixj];
+          const bool up = (i & len) == 0;
+          if ((x > y) == up) {
+            key[i] = y;
+            key[ixj] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  // rows of the sorted blocks and their exclusive prefix
+  int x[2], uu[2];
+  int s = 0;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int pos = 2 * tid + k;
+    uu[k] = -1;
+    x[k] = 0;
+    if (pos < CQ && key[pos] != ~0ull) {
+      const int u = (int)(key[pos] & 0x7ffu);
+      const int a = min(max(qo[u], 0), N), b = min(max(qo[u + 1], a), N);
+      uu[k] = u;
+      x[k] = b - a;
+    }
+    s += x[k];
+  }
+  int inc = s;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) wsum[wid] = inc;
+  __syncthreads();
+  int run = inc - s, total = 0;
+  for (int i = 0; i < 16; ++i) {
+    run += i < wid ? wsum[i] : 0;
+    total += wsum[i];
+  }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int pos = 2 * tid + k;
+    if (pos < CQ) {
+      pre[pos] = run;
+      tpos[pos] = uu[k] >= 0 ? tiles[uu[k]] : 0;
+      order[(size_t)h * CQ + pos] = uu[k];
+      spre[(size_t)h * (CQ + 1) + pos] = run;
+    }
+    run += x[k];
+  }
+  if (tid == 0) {
+    pre[CQ] = total;
+    spre[(size_t)h * (CQ + 1) + CQ] = total;
+  }
+  __syncthreads();
+  // windows of ATTN_R rows; a window with more than ATTN_LB blocks is split
+  // into runs of ATTN_LB blocks.  With at most 2048 groups they are ordered
+  // longest first (summed key tiles of their query blocks), so that the
+  // longest ones start first.
+  int4* gh = grp + (size_t)h * GPH;
+  const int W = (total + ATTN_R - 1) / ATTN_R;
+  const bool lpt = GPH <= 2048 && W < (1 << 23);
+  // blocks of window wdw: sorted positions [i0, i1)
+  auto window = [&](int wdw, int& i0, int& i1) {
+    const int ra = wdw * ATTN_R, rb = min(ra + ATTN_R, total);
+    int lo = 0, hi = CQ;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (pre[mid + 1] > ra) hi = mid;
+      else lo = mid + 1;
+    }
+    i0 = lo;
+    hi = CQ;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (pre[mid] >= rb) hi = mid;
+      else lo = mid + 1;
+    }
+    i1 = lo;
+  };
+  auto desc = [&](int wdw, int k, int i0, int i1) {
+    const int ra = wdw * ATTN_R, rb = min(ra + ATTN_R, total);
+    const int ib = i0 + k * ATTN_LB, ie = min(ib + ATTN_LB, i1);
+    return make_int4(max(ra, pre[ib]), min(rb, pre[ie]), ib, ie);
+  };
+  int gbase = 0;
+  for (int w0 = 0; w0 < W; w0 += 1024) {
+    const int wdw = w0 + tid;
+    int i0 = 0, i1 = 0, nsub = 0;
+    if (wdw < W) {
+      window(wdw, i0, i1);
+      nsub = (i1 - i0 + ATTN_LB - 1) / ATTN_LB;
+    }
+    int sinc = nsub;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(sinc, o, 64);
+      if (lane >= o) sinc += y;
+    }
+    __syncthreads();
+    if (lane == 63) wsum[wid] = sinc;
+    __syncthreads();
+    int g = gbase + sinc - nsub, ctot = 0;
+    for (int i = 0; i < 16; ++i) {
+      g += i < wid ? wsum[i] : 0;
+      ctot += wsum[i];
+    }
+    for (int k = 0; k < nsub; ++k, ++g) {
+      if (g >= GPH) continue;
+      const int4 gd = desc(wdw, k, i0, i1);
+      if (lpt) {
+        uint32_t c = 0;
+        for (int i = gd.z; i < gd.w; ++i) c += (uint32_t)tpos[i];
+        key[g] = ((unsigned long long)(0xffffffffu - c) << 32) | ((uint32_t)wdw << 8) | (uint32_t)k;
+      } else {
+        gh[g] = gd;
+      }
+    }
+    gbase += ctot;
+  }
+  if (lpt) {
+    const int G = min(gbase, GPH);
+    int SG = 2;
+    while (SG < G) SG <<= 1;
+    for (int g = G + tid; g < SG; g += 1024) key[g] = ~0ull;
+    __syncthreads();
+    for (int len = 2; len <= SG; len <<= 1)
+      for (int j = len >> 1; j > 0; j >>= 1) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const int i = tid + 1024 * k, ixj = i ^ j;
+          if (i < SG && ixj > i) {
+            const unsigned long long x = key[i], y = key[ixj];
+            const bool up = (i & len) == 0;
+            if ((x > y) == up) {
+              key[i] = y;
+              key[ixj] = x;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    for (int g = tid; g < G; g += 1024) {
+      const uint32_t lo = (uint32_t)key[g];
+      const int wdw = (int)(lo >> 8), k = (int)(lo & 255u);
+      int i0, i1;
+      window(wdw, i0, i1);
+      gh[g] = desc(wdw, k, i0, i1);
+    }
+  }
+  for (int g = gbase + tid; g < GPH; g += 1024) gh[g] = make_int4(0, 0, 0, 0);
+}
+
+// maximum of v over lanes l and l ^ 32 (a cross-half lane swap, no LDS traffic)
+__device__ __forceinline__ float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(v, fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1])));
+}
+
+// makes all K fragments of a tile live at once, so that their LDS reads are
+// issued together instead of one read-wait-MFMA step at a time
+template <int KS>
+__device__ __forceinline__ void frags_ready(const bf16x8_t (&a)[KS]) {
+  if constexpr (KS == 8)
+    asm volatile("" ::"v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]),
+                 "v"(a[7]));
+  else
+    asm volatile("" ::"v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
+}
+
+// waits until this wavefront's DMAs of the oldest tile in flight are done,
+// `younger` (0 .. NS - 2) newer tiles of PER operations each may stay in flight
+template <int PER, int NS>
+__device__ __forceinline__ void wait_oldest(int younger) {
+  static_assert(NS >= 2 && NS <= 8, "ring depth");
+  switch (NS >= 3 ? min(younger, NS - 2) : 0) {
+    case 6: wait_vmcnt<6 * PER>(); break;
+    case 5: wait_vmcnt<5 * PER>(); break;
+    case 4: wait_vmcnt<4 * PER>(); break;
+    case 3: wait_vmcnt<3 * PER>(); break;
+    case 2: wait_vmcnt<2 * PER>(); break;
+    case 1: wait_vmcnt<1 * PER>(); break;
+    default: wait_vmcnt<0>(); break;
+  }
+}
+
+template <int D, int KT, int NW>
+struct GrpTile {
+  static constexpr int CPR = D / 8;           // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;        // rows one wave-wide DMA fills
+  // DMAs per wavefront, tensor and tile, and the wavefronts that issue them
+  static constexpr int NI = KT / (NW * RPI) >= 1 ? KT / (NW * RPI) : 1;
+  static constexpr int DW = KT / (NI * RPI);
+  static constexpr int ELEMS = KT * D;  // bf16 elements of one K or V tile
+  static_assert(DW >= 1 && DW <= NW && NI * DW * RPI == KT, "tile shape");
+};
+
+// V swizzle of the 32x32 transpose reads: the 4 rows x 64 bytes that one
+// half-wavefront reads cover the 64 banks once
+template <int D>
+__device__ __forceinline__ int swz_v32(int r) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); }
+
+template <typename OT, int D, int NW, int NS>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
+    const bf16_t* __restrict__ Qp, const bf16_t* __restrict__ Kp, const bf16_t* __restrict__ Vp,
+    const int* __restrict__ q_offsets, const int* __restrict__ k_offsets,
+    const int* __restrict__ kv_count, const int* __restrict__ kv_index,
+    const int* __restrict__ q_perm, const int* __restrict__ order, const int* __restrict__ spre,
+    const int4* __restrict__ grp, int H, int N, int CQ, int CK, int GPH, float scale_log2,
+    OT* __restrict__ O) {
+  constexpr int KT = 32, NT = 64 * NW;
+  using TS = GrpTile<D, KT, NW>;
+  constexpr int KS = D / 16;  // k-steps of S^T
+  constexpr int DB = D / 32;  // 32-dimension blocks of O^T
+  constexpr int EPT = AT_MAXC / NT;  // key blocks per thread in the union scan
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  bf16_t* Ks = (bf16_t*)smem;                          // [NS][KT][D], swizzled chunks
+  bf16_t* Vs = Ks + NS * TS::ELEMS;                    // [NS][KT][D], swizzled chunks
+  float* bias = (float*)(Vs + NS * TS::ELEMS);         // [NS][ATTN_LB][KT]: 0 or -inf
+  uint32_t* selw = (uint32_t*)(bias + NS * ATTN_LB * KT);  // [CK]
+  int2* ut = (int2*)(selw + ((CK + 3) & ~3));          // [CK + 1]
+  __shared__ int sg_row[ATTN_LB], sg_lr[ATTN_LB + 1], sg_u[ATTN_LB];
+  __shared__ int tmp[2][NW];
+  __shared__ uint32_t tneed[NS][NW];  // query blocks that select a key of the tile, per wavefront
+
+  // XCD-aware work item: XCD x (= blockIdx % 8) takes items [x*per, (x+1)*per)
+  const int nitems = H * GPH;
+  const int per = (nitems + 7) >> 3;
+  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (item >= nitems) return;
+  const int h = item / GPH;
+  const int4 gd = grp[item];
+  const int ib = gd.z, ie = gd.w;
+  if (gd.y <= gd.x || ib < 0 || ie <= ib || ie - ib > ATTN_LB || ie > CQ || gd.y - gd.x > 32 * NW)
+    return;
+  const int nb = ie - ib, tid = threadIdx.x;
+  const int* qo = q_offsets + (size_t)h * (CQ + 1);
+  const int* koff = k_offsets + (size_t)h * (CK + 1);
+  if (tid < nb) {
+    const int i = ib + tid;
+    const int u = min(max(order[(size_t)h * CQ + i], 0), CQ - 1);
+    const int s0 = spre[(size_t)h * (CQ + 1) + i];
+    const int a = max(gd.x, s0);
+    sg_u[tid] = u;
+    sg_row[tid] = min(max(qo[u], 0), N) + (a - s0);
+    sg_lr[tid] = a - gd.x;
+  }
+  if (tid == 0) sg_lr[nb] = gd.y - gd.x;
+  for (int v = tid; v < CK; v += NT) selw[v] = 0u;
+  __syncthreads();
+  // selw[v]: bit b set when query block b of the group selected key block v
+  for (int b = 0; b < nb; ++b) {
+    const size_t row = (size_t)h * CQ + sg_u[b];
+    const int n = min(max(kv_count[row], 0), CK);
+    const int* sel = kv_index + row * CK;
+    for (int j = tid; j < n; j += NT) {
+      const int v = sel[j];
+      if ((unsigned)v < (unsigned)CK) atomicOr(&selw[v], 1u << b);
+    }
+  }
+  __syncthreads();
+  // union table: ut[j] = {first stream position, first row of Kp} of the j-th
+  // selected key block, ut[U] = {stream length, -1}; selw[j] its bits
+  int U, nk;
+  {
+    const int lane = tid & 63, wv = tid >> 6;
+    uint32_t f[EPT];
+    int x[EPT], st[EPT], c = 0, s = 0;
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) {
+      const int v = tid * EPT + k;
+      f[k] = v < CK ? selw[v] : 0u;
+      x[k] = 0;
+      st[k] = -1;
+      if (f[k]) {
+        st[k] = koff[v];
+        x[k] = max(0, koff[v + 1] - st[k]);
+        ++c;
+      }
+      s += x[k];
+    }
+    int ic = c, is = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int yc = __shfl_up(ic, o, 64), ys = __shfl_up(is, o, 64);
+      if (lane >= o) {
+        ic += yc;
+        is += ys;
+      }
+    }
+    if (lane == 63) {
+      tmp[0][wv] = ic;
+      tmp[1][wv] = is;
+    }
+    __syncthreads();  // also: every thread has read its selw entries
+    int jc = ic - c, js = is - s;
+    U = 0;
+    nk = 0;
+    for (int w2 = 0; w2 < NW; ++w2) {
+      jc += w2 < wv ? tmp[0][w2] : 0;
+      js += w2 < wv ? tmp[1][w2] : 0;
+      U += tmp[0][w2];
+      nk += tmp[1][w2];
+    }
+#pragma unroll
+    for (int k = 0; k < EPT; ++k)
+      if (f[k]) {
+        ut[jc] = make_int2(js, st[k]);
+        selw[jc] = f[k];
+        ++jc;
+        js += x[k];
+      }
+    if (tid == 0) ut[U] = make_int2(nk, -1);
+    __syncthreads();
+  }
+  const bf16_t* Qh = Qp + (size_t)h * N * D;
+  const bf16_t* Kh = Kp + (size_t)h * N * D;
+  const bf16_t* Vh = Vp + (size_t)h * N * D;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l = tid & 63, hf = l >> 5, c32 = l & 31;
+
+  // this lane's query row: group row 32 w + c32, query block bq of the group
+  const int gr = 32 * w + c32;
+  const int grows = sg_lr[nb];
+  int bq = 0;
+  while (bq + 1 < nb && sg_lr[bq + 1] <= gr) ++bq;
+  const int qr0 = sg_row[bq] + (gr - sg_lr[bq]);
+  const bool qvalid = gr < grows && (unsigned)qr0 < (unsigned)N;
+  const int qr = qvalid ? qr0 : 0;
+  const bool wave_on = 32 * w < grows;
+  bf16x8_t qf[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+    if (qvalid) raw = *(const uint4*)(Qh + (size_t)qr * D + 16 * s + 8 * hf);
+    qf[s] = __builtin_bit_cast(bf16x8_t, raw);
+  }
+#pragma unroll
+  for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qf[s]));
+
+  // DMA lanes: tile row rr[i], chunk position pch; a cursor into ut per row
+  const int pch = l % TS::CPR;
+  // kb[i]: selection bits (query blocks of the group) of the row's key block
+  // (every lane of a row computes the same cursor)
+  int rr[TS::NI], jj[TS::NI], cj[TS::NI], kj[TS::NI], src[TS::NI];
+  uint32_t sw[TS::NI], kb[TS::NI];
+  int2 nx[TS::NI];
+#pragma unroll
+  for (int i = 0; i < TS::NI; ++i) {
+    rr[i] = (w * TS::NI + i) * TS::RPI + l / TS::CPR;
+    jj[i] = 0;
+    cj[i] = 0;
+    kj[i] = ut[0].y;
+    sw[i] = selw[0];
+    nx[i] = ut[U > 0 ? 1 : 0];
+    src[i] = 0;
+    kb[i] = 0u;
+  }
+  const bool dma_w = w < TS::DW;
+  auto advance = [&](int t) {
+    if (!dma_w) return;
+#pragma unroll
+    for (int i = 0; i < TS::NI; ++i) {
+      const int pos = t * KT + rr[i];
+      while (pos >= nx[i].x && jj[i] + 1 < U) {
+        ++jj[i];
+        cj[i] = nx[i].x;
+        kj[i] = nx[i].y;
+        sw[i] = selw[jj[i]];
+        nx[i] = ut[jj[i] + 1];
+      }
+      const int r = kj[i] + (pos - cj[i]);
+      const bool ok = pos < nk && (unsigned)r < (unsigned)N;
+      src[i] = ok ? r : 0;
+      kb[i] = ok ? sw[i] : 0u;
+    }
+  };
+  auto issue = [&](int slot) {
+    if (!dma_w) return;
+    bf16_t* ks = Ks + slot * TS::ELEMS;
+    bf16_t* vs = Vs + slot * TS::ELEMS;
+#pragma unroll
+    for (int i = 0; i < TS::NI; ++i) {
+      const bf16_t* gk = Kh + (size_t)src[i] * D + 8 * (pch ^ swz_k<D>(rr[i]));
+      const bf16_t* gv = Vh + (size_t)src[i] * D + 8 * (pch ^ swz_v32<D>(rr[i]));
+      const int off = (w * TS::NI + i) * 512;  // 1 KB per wave-wide DMA
+      lds_dma16(gk, lds_addr(ks + off));
+      lds_dma16(gv, lds_addr(vs + off));
+    }
+    // score bias of each (query block, tile row): 0 if the block selected
+    // the row's key block, -inf otherwise (also past the end of the stream)
+    float* bs = bias + slot * ATTN_LB * KT;
+    uint32_t any = 0u;
+#pragma unroll
+    for (int i = 0; i < TS::NI; ++i) {
+      any |= kb[i];
+#pragma unroll
+      for (int b = pch; b < ATTN_LB; b += TS::CPR)
+        bs[b * KT + rr[i]] = ((kb[i] >> b) & 1u) ? 0.0f : -INFINITY;
+    }
+#pragma unroll
+    for (int o = TS::CPR; o < 64; o <<= 1) any |= (uint32_t)__shfl_xor((int)any, o, 64);
+    if (l == 0) tneed[slot][w] = any;
+  };
+
+  // LDS read offsets (bf16 elements, relative to a slot)
+  // K (A operand of S^T): key row c32, chunk 2 s + hf
+  int kofs[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) kofs[s] = c32 * D + 8 * ((2 * s + hf) ^ swz_k<D>(c32));
+  // V^T (A operand of O^T) by transpose reads: in 16-lane group G, lane j
+  // gives row 4 hf + j/4 (+ 16 kappa, + 8 for the second read) and dims
+  // 32 db + 16 (G % 2) + 4 (j % 4); it receives dim 32 db + 16 (G % 2) + j
+  const int G = l >> 4, jg = l & 15;
+  const int vr0 = 4 * hf + (jg >> 2);
+  int vofs[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int col = 32 * db + 16 * (G & 1) + 4 * (jg & 3);
+    vofs[db] = vr0 * D + 8 * ((col >> 3) ^ swz_v32<D>(vr0)) + (col & 7);
+  }
+
+  float m = -INFINITY, lpart = 0.0f;
+  f32x16_t acc[DB];
+#pragma unroll
+  for (int b = 0; b < DB; ++b)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[b][q] = 0.0f;
+  // query blocks of this wavefront's rows, and the bias row of this lane
+  uint32_t wbits = qvalid ? (1u << bq) : 0u;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) wbits |= (uint32_t)__shfl_xor((int)wbits, o, 64);
+  wbits = __builtin_amdgcn_readfirstlane(wbits);
+  const int bofs = (qvalid ? bq : 0) * KT + 4 * hf;
+
+  const int ntiles = (nk + KT - 1) / KT;
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < ntiles) {
+      advance(p);
+      issue(p);
+    }
+  for (int t = 0; t < ntiles; ++t) {
+    const int next = t + NS - 1;
+    if (next < ntiles) advance(next);
+    wait_oldest<2 * TS::NI, NS>(ntiles - 1 - t);
+    __syncthreads();  // tile t landed everywhere; tile t-1 consumed (its slot is free)
+    if (next < ntiles) issue(next % NS);
+    if (!wave_on) continue;
+    // skip the tile when no query block of this wavefront selected any of its keys
+    uint32_t need = 0u;
+#pragma unroll
+    for (int w2 = 0; w2 < TS::DW; ++w2) need |= tneed[t % NS][w2];
+    if (!(__builtin_amdgcn_readfirstlane(need) & wbits)) continue;
+    const int slot = t % NS;
+    const bf16_t* ks = Ks + slot * TS::ELEMS;
+    const bf16_t* vs = Vs + slot * TS::ELEMS;
+    // S^T: 32 keys x 32 queries; lane holds keys 8 b + 4 hf + r of query c32,
+    // starting from the bias of those keys (-inf where the block did not select them)
+    bf16x8_t kf[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) kf[s] = *(const bf16x8_t*)(ks + kofs[s]);
+    f32x16_t st;
+    {
+      const float* br = bias + slot * ATTN_LB * KT + bofs;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const float4 x = *(const float4*)(br + 8 * b);
+        st[4 * b + 0] = x.x;
+        st[4 * b + 1] = x.y;
+        st[4 * b + 2] = x.z;
+        st[4 * b + 3] = x.w;
+      }
+    }
+    frags_ready<KS>(kf);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[s], st, 0, 0, 0);
+    float tmax = fmaxf(st[0], st[1]);
+#pragma unroll
+    for (int q = 2; q < 16; ++q) tmax = fmaxf(tmax, st[q]);
+    tmax = max_xor32(tmax);
+    // the reference maximum moves only when a row maximum exceeds it by more
+    // than 2^8 in probability (softmax is invariant to the shift; p <= 2^8)
+    if (__any((tmax - m) * scale_log2 > 8.0f)) {
+      // rows without a kept key so far keep m = -inf (and alpha = 1)
+      const float mnew = fmaxf(m, tmax);
+      const float alpha = mnew == m ? 1.0f : __builtin_amdgcn_exp2f((m - mnew) * scale_log2);
+      lpart *= alpha;
+#pragma unroll
+      for (int b = 0; b < DB; ++b) acc[b] *= alpha;
+      m = mnew;
+    }
+    const float nms = m == -INFINITY ? 0.0f : -m * scale_log2;
+    float p[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      p[q] = __builtin_amdgcn_exp2f(fmaf(st[q], scale_log2, nms));
+      lpart += p[q];
+    }
+    // O^T += V^T P^T in two 16-key steps; step kp takes scores 8 kp .. 8 kp + 7
+    // (keys 16 kp + 4 hf + r and 16 kp + 8 + 4 hf + r)
+#pragma unroll
+    for (int kp = 0; kp < 2; ++kp) {
+      bf16x8_t pb;
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const bf16x2_t two =
+            __builtin_convertvector(f32x2_t{p[8 * kp + e], p[8 * kp + e + 1]}, bf16x2_t);
+        pb[e] = two[0];
+        pb[e + 1] = two[1];
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const bf16_t* v1 = vs + vofs[db] + 16 * kp * D;
+        const i16x4_t t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)v1);
+        const i16x4_t t2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(v1 + 8 * D));
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, (short __attribute__((ext_vector_type(8)))){t1[0], t1[1], t1[2], t1[3],
+                                                                  t2[0], t2[1], t2[2], t2[3]});
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, acc[db], 0, 0, 0);
+      }
+    }
+  }
+  float lsum = lpart + __shfl_xor(lpart, 32, 64);
+  if (qvalid) {
+    const int dst = q_perm[(size_t)h * N + qr];
+    if ((unsigned)dst < (unsigned)N) {
+      const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+      OT* o = O + ((size_t)h * N + dst) * D + 4 * hf;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int bq4 = 0; bq4 < 4; ++bq4)
+          store_out4<OT>(o + 32 * db + 8 * bq4, acc[db][4 * bq4 + 0] * inv,
+                         acc[db][4 * bq4 + 1] * inv, acc[db][4 * bq4 + 2] * inv,
+                         acc[db][4 * bq4 + 3] * inv);
+    }
+  }
+}
+
 template <typename T, typename OT>
 static park_status attn_dispatch_d(const void* Qp, const void* Kp, const void* Vp, const int* qo,
                                    const int* ko, const int* kc, const int* ki, const int* qp,
@@ -673,24 +1305,74 @@ static park_status attn_mfma_launch(const void* Qp, const void* Kp, const void* 
   return PARK_OK;
 }
 
+#ifndef PARK_ATTN_GROUP
+#define PARK_ATTN_GROUP 1
+#endif
+
+size_t attn_grp_offset(int H, int CQ);
+
+template <typename OT, int D, int NW, int NS>
+static park_status attn_grp_launch(const void* Qp, const void* Kp, const void* Vp, const int* qo,
+                                   const int* ko, const int* kc, const int* ki, const int* qp,
+                                   int H, int N, int CQ, int CK, void* plan, float sl2, void* O,
+                                   hipStream_t st) {
+  const int GPH = attn_groups_per_head(N, CQ);
+  int* order = (int*)plan;
+  int* spre = order + (size_t)H * CQ;
+  int4* grp = (int4*)((char*)plan + attn_grp_offset(H, CQ));
+  PARK_LAUNCH("attn_plan", k_attn_gplan, dim3(H), dim3(1024), 0, st, qo, kc, ki, ko, N, CQ, CK,
+              GPH, order, spre, grp);
+  // K/V ring, score biases, then the union tables (selection words, stream table)
+  constexpr size_t fixed =
+      (size_t)2 * NS * 32 * D * sizeof(bf16_t) + (size_t)NS * ATTN_LB * 32 * 4;
+  const size_t lds = fixed + (size_t)((CK + 3) & ~3) * 4 + (size_t)(CK + 1) * sizeof(int2);
+  // reserved once for the largest CK (2048), outside any stream capture that may follow
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)k_attn_grp<OT, D, NW, NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)(fixed + (size_t)AT_MAXC * 4 + (size_t)(AT_MAXC + 1) * sizeof(int2)));
+  if (attr != hipSuccess)
+    return fail(PARK_ERR_HIP, "attention: cannot reserve %zu bytes of LDS", lds);
+  // 8 * ceil(items / 8) workgroups: every item owns one (see the remap in the kernel)
+  const unsigned nwg = 8u * (((unsigned)H * (unsigned)GPH + 7u) / 8u);
+  PARK_LAUNCH("attn_mfma", (k_attn_grp<OT, D, NW, NS>), dim3(nwg), dim3(64 * NW), lds, st,
+              (const bf16_t*)Qp, (const bf16_t*)Kp, (const bf16_t*)Vp, qo, ko, kc, ki, qp, order,
+              spre, grp, H, N, CQ, CK, GPH, sl2, (OT*)O);
+  return PARK_OK;
+}
+
 template <typename OT>
 static park_status attn_mfma_d(const void* Qp, const void* Kp, const void* Vp, const int* qo,
                                const int* ko, const int* kc, const int* ki, const int* qp, int H,
                                int N, int D, int CQ, int CK, void* plan, void* O, hipStream_t st) {
+  const float sl2 = (float)(1.4426950408889634 / sqrt((double)D));
+#if PARK_ATTN_GROUP
+  if (D == 128)
+    return attn_grp_launch<OT, 128, ATTN_R / 32, ATTN_RING>(Qp, Kp, Vp, qo, ko, kc, ki, qp, H, N,
+                                                             CQ, CK, plan, sl2, O, st);
+  return attn_grp_launch<OT, 64, ATTN_R / 32, ATTN_RING>(Qp, Kp, Vp, qo, ko, kc, ki, qp, H, N, CQ,
+                                                           CK, plan, sl2, O, st);
+#else
   const int CPH = attn_chunks_per_head(N, CQ);
   int4* pl = (int4*)plan;
   PARK_LAUNCH("attn_plan", k_attn_plan, dim3(H), dim3(1024), 0, st, qo, kc, ki, N, CQ, CK, CPH,
               pl);
-  const float sl2 = (float)(1.4426950408889634 / sqrt((double)D));
   if (D == 128)
     return attn_mfma_launch<OT, 128, PARK_ATTN_KT, PARK_ATTN_NS>(Qp, Kp, Vp, ko, kc, ki, qp, pl, H,
                                                                N, CQ, CK, CPH, sl2, O, st);
   return attn_mfma_launch<OT, 64, PARK_ATTN_KT, PARK_ATTN_NS>(Qp, Kp, Vp, ko, kc, ki, qp, pl, H, N,
                                                               CQ, CK, CPH, sl2, O, st);
+#endif
+}
+
+// order [H][CQ], spre [H][CQ + 1], then the groups [H][GPH] at 16-byte alignment
+size_t attn_grp_offset(int H, int CQ) {
+  return (((size_t)H * CQ + (size_t)H * (CQ + 1)) * sizeof(int) + 15) & ~(size_t)15;
 }
 
 size_t attn_plan_bytes(int H, int N, int CQ) {
-  return (size_t)H * attn_chunks_per_head(N, CQ) * sizeof(int4);
+  const size_t grp = attn_grp_offset(H, CQ) + (size_t)H * attn_groups_per_head(N, CQ) * sizeof(int4);
+  const size_t chunks = (size_t)H * attn_chunks_per_head(N, CQ) * sizeof(int4);
+  return grp > chunks ? grp : chunks;
 }
 
 park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,

@@ -22,10 +22,12 @@ def setup_module(module):
     P.lib()
 
 
-def small(name, grid=None, heads=None):
+def small(name, grid=None, heads=None, **kw):
     cfg = synth.CONFIGS[name]
     if grid is not None:
         cfg = cfg.with_(grid=grid)
+    if kw:
+        cfg = cfg.with_(**kw)
     q, k, v = synth.make_layer(cfg, heads)
     return cfg, q, k, v
 
@@ -36,13 +38,14 @@ CASES = {
     "medium2": ("medium", None, [0, 5]),
     "ragged_bf16": ("medium", (3, 11, 13), [1, 2, 3]),  # N = 429, not a multiple of 64
     "hunyuan_small": ("hunyuan", (1, 9, 16), [0, 1]),   # text tokens appended
+    "tiny_bf16_d64": ("tiny", (2, 16, 32), None, {"dtype": "bf16"}),  # bf16 at head_dim 64
 }
 
 
 @pytest.fixture(scope="module", params=list(CASES))
 def case(request):
-    name, grid, heads = CASES[request.param]
-    cfg, q, k, v = small(name, grid, heads)
+    name, grid, heads, *kw = CASES[request.param]
+    cfg, q, k, v = small(name, grid, heads, **(kw[0] if kw else {}))
     return request.param, cfg, q, k, v
 
 
@@ -197,6 +200,61 @@ def test_attention_matches_oracle(case, out_dtype):
         err = np.abs(Og[h] - ref)
         print(f"[{tag} out={out_dtype} h={h}] attention max-abs err {err.max():.3g}")
         assert np.all(err <= tol), (tag, err.max())
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_attention_many_small_query_blocks(d):
+    # query blocks of 0-3 rows (a group of rows then holds more query blocks
+    # than one selection word), a few large ones, and empty selections
+    rng = np.random.default_rng(5)
+    H, N, C = 2, 1500, 700
+    q = rng.standard_normal((H, N, d)).astype(np.float32)
+    k = rng.standard_normal((H, N, d)).astype(np.float32)
+    v = rng.standard_normal((H, N, d)).astype(np.float32)
+    q, k, v = (synth.bf16_round(a) for a in (q, k, v))
+    qperm, kperm, qoff, koff, kvc, kvi, rows = [], [], [], [], [], [], []
+    CK = 48
+    for h in range(H):
+        sizes = rng.choice([0, 1, 2, 3, 150], size=C, p=[0.2, 0.35, 0.25, 0.15, 0.05])
+        sizes[-1] += N - sizes.sum() if sizes.sum() < N else 0
+        while sizes.sum() > N:
+            i = int(np.argmax(sizes)); sizes[i] -= min(sizes[i], sizes.sum() - N)
+        zq = np.repeat(np.arange(C), sizes)
+        zq = zq[rng.permutation(N)]
+        zk = rng.integers(0, CK, N)
+        pq, oq = O.stable_argsort(zq, C)
+        pk, ok = O.stable_argsort(zk, CK)
+        cnt = np.zeros(C, np.int32)
+        idx = np.zeros((C, CK), np.int32)
+        rr = []
+        for u in range(C):
+            m = int(rng.integers(0, 10))  # 0: an empty selection
+            s = np.sort(rng.choice(CK, size=m, replace=False))
+            cnt[u] = len(s)
+            idx[u, :len(s)] = s
+            rr.append(s)
+        qperm.append(pq); kperm.append(pk); qoff.append(oq); koff.append(ok)
+        kvc.append(cnt); kvi.append(idx); rows.append(rr)
+    t = lambda a: torch.from_numpy(np.stack(a).astype(np.int32)).cuda()
+    Qp = PT.to_dev(np.stack([q[h][qperm[h]] for h in range(H)]), "bf16")
+    Kp = PT.to_dev(np.stack([k[h][kperm[h]] for h in range(H)]), "bf16")
+    Vp = PT.to_dev(np.stack([v[h][kperm[h]] for h in range(H)]), "bf16")
+    Ot = P.park_block_sparse_attn(Qp, Kp, Vp, t(qoff), t(koff), t(kvc), t(kvi), t(qperm), C, CK,
+                                  P.PARK_F32)
+    Og = PT.np64(Ot)
+    for h in range(H):
+        # the oracle needs a selection per block: give the empty ones a
+        # placeholder, then expect zero rows for them
+        rr = [s if len(s) else np.array([0]) for s in rows[h]]
+        ref = O.block_sparse_attention(q[h][qperm[h]], k[h][kperm[h]], v[h][kperm[h]], qoff[h],
+                                       koff[h], rr, qperm[h])
+        for u, s in enumerate(rows[h]):
+            if len(s) == 0:
+                ref[qperm[h][qoff[h][u]:qoff[h][u + 1]]] = 0.0
+        tol = PT.attn_tol("bf16", False, ref)
+        err = np.abs(Og[h] - ref)
+        print(f"[small blocks d={d} h={h}] attention max-abs err {err.max():.3g}")
+        assert np.all(err <= tol), err.max()
 
 
 def test_dense_when_every_block_kept():
