@@ -656,7 +656,8 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t* __restrict__ Qp
 #define PARK_ATTN_RING 3
 #endif
 constexpr int ATTN_R = PARK_ATTN_R;  // rows per group (32 per wavefront)
-constexpr int ATTN_RING = PARK_ATTN_RING;  // K/V tiles of the LDS ring (all but one in flight)
+constexpr int ATTN_KSLOTS = PARK_ATTN_RING;  // K tiles in LDS (V: one more)
+constexpr int ATTN_UCAP = 1024;  // key blocks of the union per stream chunk
 constexpr int ATTN_LB = 16;          // query blocks per group (bits of a selection word)
 
 static int attn_windows(int N) { return (N + ATTN_R - 1) / ATTN_R; }
@@ -915,6 +916,9 @@ __device__ __forceinline__ void wait_oldest(int younger) {
   }
 }
 
+// rotation of the rows of block b in a bias tile (a multiple of 4)
+__device__ __forceinline__ int bias_rot(int b) { return 4 * ((b >> 1) & 7); }
+
 template <int D, int KT, int NW>
 struct GrpTile {
   static constexpr int CPR = D / 8;           // 16-byte chunks per row
@@ -931,7 +935,7 @@ struct GrpTile {
 template <int D>
 __device__ __forceinline__ int swz_v32(int r) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); }
 
-template <typename OT, int D, int NW, int NS>
+template <typename OT, int D, int NW>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
     const bf16_t* __restrict__ Qp, const bf16_t* __restrict__ Kp, const bf16_t* __restrict__ Vp,
     const int* __restrict__ q_offsets, const int* __restrict__ k_offsets,
@@ -940,19 +944,21 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
     const int4* __restrict__ grp, int H, int N, int CQ, int CK, int GPH, float scale_log2,
     OT* __restrict__ O) {
   constexpr int KT = 32, NT = 64 * NW;
+  constexpr int NSK = ATTN_KSLOTS, NSV = ATTN_KSLOTS + 1;  // K and V ring slots
   using TS = GrpTile<D, KT, NW>;
-  constexpr int KS = D / 16;  // k-steps of S^T
-  constexpr int DB = D / 32;  // 32-dimension blocks of O^T
+  constexpr int KS = D / 16;         // k-steps of S^T
+  constexpr int DB = D / 32;         // 32-dimension blocks of O^T
   constexpr int EPT = AT_MAXC / NT;  // key blocks per thread in the union scan
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  bf16_t* Ks = (bf16_t*)smem;                          // [NS][KT][D], swizzled chunks
-  bf16_t* Vs = Ks + NS * TS::ELEMS;                    // [NS][KT][D], swizzled chunks
-  float* bias = (float*)(Vs + NS * TS::ELEMS);         // [NS][ATTN_LB][KT]: 0 or -inf
-  uint32_t* selw = (uint32_t*)(bias + NS * ATTN_LB * KT);  // [CK]
-  int2* ut = (int2*)(selw + ((CK + 3) & ~3));          // [CK + 1]
+  bf16_t* Ks = (bf16_t*)smem;                        // [NSK][KT][D], swizzled chunks
+  bf16_t* Vs = Ks + NSK * TS::ELEMS;                 // [NSV][KT][D], swizzled chunks
+  float* bias = (float*)(Vs + NSV * TS::ELEMS);      // [NSK][ATTN_LB][KT]: 0 or -inf
+  uint32_t* flg = (uint32_t*)(bias + NSK * ATTN_LB * KT);  // [AT_MAXC / 2]: 16 bits per key block
+  int2* ut = (int2*)(flg + AT_MAXC / 2);            // [ATTN_UCAP + 1]
+  uint16_t* selw = (uint16_t*)(ut + ATTN_UCAP + 1);  // [ATTN_UCAP]
   __shared__ int sg_row[ATTN_LB], sg_lr[ATTN_LB + 1], sg_u[ATTN_LB];
   __shared__ int tmp[2][NW];
-  __shared__ uint32_t tneed[NS][NW];  // query blocks that select a key of the tile, per wavefront
+  static_assert(ATTN_LB <= 16, "selection words are 16 bits");
 
   // XCD-aware work item: XCD x (= blockIdx % 8) takes items [x*per, (x+1)*per)
   const int nitems = H * GPH;
@@ -977,73 +983,19 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
     sg_lr[tid] = a - gd.x;
   }
   if (tid == 0) sg_lr[nb] = gd.y - gd.x;
-  for (int v = tid; v < CK; v += NT) selw[v] = 0u;
+  for (int v = tid; v < AT_MAXC / 2; v += NT) flg[v] = 0u;
   __syncthreads();
-  // selw[v]: bit b set when query block b of the group selected key block v
+  // bit b of key block v's flag: query block b of the group selected v
   for (int b = 0; b < nb; ++b) {
     const size_t row = (size_t)h * CQ + sg_u[b];
     const int n = min(max(kv_count[row], 0), CK);
     const int* sel = kv_index + row * CK;
     for (int j = tid; j < n; j += NT) {
       const int v = sel[j];
-      if ((unsigned)v < (unsigned)CK) atomicOr(&selw[v], 1u << b);
+      if ((unsigned)v < (unsigned)CK) atomicOr(&flg[v >> 1], (1u << b) << (16 * (v & 1)));
     }
   }
   __syncthreads();
-  // union table: ut[j] = {first stream position, first row of Kp} of the j-th
-  // selected key block, ut[U] = {stream length, -1}; selw[j] its bits
-  int U, nk;
-  {
-    const int lane = tid & 63, wv = tid >> 6;
-    uint32_t f[EPT];
-    int x[EPT], st[EPT], c = 0, s = 0;
-#pragma unroll
-    for (int k = 0; k < EPT; ++k) {
-      const int v = tid * EPT + k;
-      f[k] = v < CK ? selw[v] : 0u;
-      x[k] = 0;
-      st[k] = -1;
-      if (f[k]) {
-        st[k] = koff[v];
-        x[k] = max(0, koff[v + 1] - st[k]);
-        ++c;
-      }
-      s += x[k];
-    }
-    int ic = c, is = s;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int yc = __shfl_up(ic, o, 64), ys = __shfl_up(is, o, 64);
-      if (lane >= o) {
-        ic += yc;
-        is += ys;
-      }
-    }
-    if (lane == 63) {
-      tmp[0][wv] = ic;
-      tmp[1][wv] = is;
-    }
-    __syncthreads();  // also: every thread has read its selw entries
-    int jc = ic - c, js = is - s;
-    U = 0;
-    nk = 0;
-    for (int w2 = 0; w2 < NW; ++w2) {
-      jc += w2 < wv ? tmp[0][w2] : 0;
-      js += w2 < wv ? tmp[1][w2] : 0;
-      U += tmp[0][w2];
-      nk += tmp[1][w2];
-    }
-#pragma unroll
-    for (int k = 0; k < EPT; ++k)
-      if (f[k]) {
-        ut[jc] = make_int2(js, st[k]);
-        selw[jc] = f[k];
-        ++jc;
-        js += x[k];
-      }
-    if (tid == 0) ut[U] = make_int2(nk, -1);
-    __syncthreads();
-  }
   const bf16_t* Qh = Qp + (size_t)h * N * D;
   const bf16_t* Kh = Kp + (size_t)h * N * D;
   const bf16_t* Vh = Vp + (size_t)h * N * D;
@@ -1058,87 +1010,24 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
   const int qr0 = sg_row[bq] + (gr - sg_lr[bq]);
   const bool qvalid = gr < grows && (unsigned)qr0 < (unsigned)N;
   const int qr = qvalid ? qr0 : 0;
-  const bool wave_on = 32 * w < grows;
   bf16x8_t qf[KS];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
+  for (int s2 = 0; s2 < KS; ++s2) {
     uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-    if (qvalid) raw = *(const uint4*)(Qh + (size_t)qr * D + 16 * s + 8 * hf);
-    qf[s] = __builtin_bit_cast(bf16x8_t, raw);
+    if (qvalid) raw = *(const uint4*)(Qh + (size_t)qr * D + 16 * s2 + 8 * hf);
+    qf[s2] = __builtin_bit_cast(bf16x8_t, raw);
   }
 #pragma unroll
-  for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qf[s]));
-
-  // DMA lanes: tile row rr[i], chunk position pch; a cursor into ut per row
-  const int pch = l % TS::CPR;
-  // kb[i]: selection bits (query blocks of the group) of the row's key block
-  // (every lane of a row computes the same cursor)
-  int rr[TS::NI], jj[TS::NI], cj[TS::NI], kj[TS::NI], src[TS::NI];
-  uint32_t sw[TS::NI], kb[TS::NI];
-  int2 nx[TS::NI];
-#pragma unroll
-  for (int i = 0; i < TS::NI; ++i) {
-    rr[i] = (w * TS::NI + i) * TS::RPI + l / TS::CPR;
-    jj[i] = 0;
-    cj[i] = 0;
-    kj[i] = ut[0].y;
-    sw[i] = selw[0];
-    nx[i] = ut[U > 0 ? 1 : 0];
-    src[i] = 0;
-    kb[i] = 0u;
-  }
-  const bool dma_w = w < TS::DW;
-  auto advance = [&](int t) {
-    if (!dma_w) return;
-#pragma unroll
-    for (int i = 0; i < TS::NI; ++i) {
-      const int pos = t * KT + rr[i];
-      while (pos >= nx[i].x && jj[i] + 1 < U) {
-        ++jj[i];
-        cj[i] = nx[i].x;
-        kj[i] = nx[i].y;
-        sw[i] = selw[jj[i]];
-        nx[i] = ut[jj[i] + 1];
-      }
-      const int r = kj[i] + (pos - cj[i]);
-      const bool ok = pos < nk && (unsigned)r < (unsigned)N;
-      src[i] = ok ? r : 0;
-      kb[i] = ok ? sw[i] : 0u;
-    }
-  };
-  auto issue = [&](int slot) {
-    if (!dma_w) return;
-    bf16_t* ks = Ks + slot * TS::ELEMS;
-    bf16_t* vs = Vs + slot * TS::ELEMS;
-#pragma unroll
-    for (int i = 0; i < TS::NI; ++i) {
-      const bf16_t* gk = Kh + (size_t)src[i] * D + 8 * (pch ^ swz_k<D>(rr[i]));
-      const bf16_t* gv = Vh + (size_t)src[i] * D + 8 * (pch ^ swz_v32<D>(rr[i]));
-      const int off = (w * TS::NI + i) * 512;  // 1 KB per wave-wide DMA
-      lds_dma16(gk, lds_addr(ks + off));
-      lds_dma16(gv, lds_addr(vs + off));
-    }
-    // score bias of each (query block, tile row): 0 if the block selected
-    // the row's key block, -inf otherwise (also past the end of the stream)
-    float* bs = bias + slot * ATTN_LB * KT;
-    uint32_t any = 0u;
-#pragma unroll
-    for (int i = 0; i < TS::NI; ++i) {
-      any |= kb[i];
-#pragma unroll
-      for (int b = pch; b < ATTN_LB; b += TS::CPR)
-        bs[b * KT + rr[i]] = ((kb[i] >> b) & 1u) ? 0.0f : -INFINITY;
-    }
-#pragma unroll
-    for (int o = TS::CPR; o < 64; o <<= 1) any |= (uint32_t)__shfl_xor((int)any, o, 64);
-    if (l == 0) tneed[slot][w] = any;
-  };
+  for (int s2 = 0; s2 < KS; ++s2) asm volatile("" ::"v"(qf[s2]));
+  // the bias row of this lane
+  const int bqq = qvalid ? bq : 0;
+  const int brow = bqq * KT, bcol = 4 * hf + bias_rot(bqq);
 
   // LDS read offsets (bf16 elements, relative to a slot)
   // K (A operand of S^T): key row c32, chunk 2 s + hf
   int kofs[KS];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) kofs[s] = c32 * D + 8 * ((2 * s + hf) ^ swz_k<D>(c32));
+  for (int s2 = 0; s2 < KS; ++s2) kofs[s2] = c32 * D + 8 * ((2 * s2 + hf) ^ swz_k<D>(c32));
   // V^T (A operand of O^T) by transpose reads: in 16-lane group G, lane j
   // gives row 4 hf + j/4 (+ 16 kappa, + 8 for the second read) and dims
   // 32 db + 16 (G % 2) + 4 (j % 4); it receives dim 32 db + 16 (G % 2) + j
@@ -1157,100 +1046,244 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
   for (int b = 0; b < DB; ++b)
 #pragma unroll
     for (int q = 0; q < 16; ++q) acc[b][q] = 0.0f;
-  // query blocks of this wavefront's rows, and the bias row of this lane
-  uint32_t wbits = qvalid ? (1u << bq) : 0u;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) wbits |= (uint32_t)__shfl_xor((int)wbits, o, 64);
-  wbits = __builtin_amdgcn_readfirstlane(wbits);
-  const int bofs = (qvalid ? bq : 0) * KT + 4 * hf;
 
-  const int ntiles = (nk + KT - 1) / KT;
+  // DMA lanes: tile row rr[i], chunk position pch; a cursor into ut per row;
+  // kb[i]: selection bits of the row's key block (all lanes of a row agree)
+  const int pch = l % TS::CPR;
+  const bool dma_w = w < TS::DW;
+  int rr[TS::NI];
 #pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < ntiles) {
-      advance(p);
-      issue(p);
-    }
-  for (int t = 0; t < ntiles; ++t) {
-    const int next = t + NS - 1;
-    if (next < ntiles) advance(next);
-    wait_oldest<2 * TS::NI, NS>(ntiles - 1 - t);
-    __syncthreads();  // tile t landed everywhere; tile t-1 consumed (its slot is free)
-    if (next < ntiles) issue(next % NS);
-    if (!wave_on) continue;
-    // skip the tile when no query block of this wavefront selected any of its keys
-    uint32_t need = 0u;
-#pragma unroll
-    for (int w2 = 0; w2 < TS::DW; ++w2) need |= tneed[t % NS][w2];
-    if (!(__builtin_amdgcn_readfirstlane(need) & wbits)) continue;
-    const int slot = t % NS;
-    const bf16_t* ks = Ks + slot * TS::ELEMS;
-    const bf16_t* vs = Vs + slot * TS::ELEMS;
-    // S^T: 32 keys x 32 queries; lane holds keys 8 b + 4 hf + r of query c32,
-    // starting from the bias of those keys (-inf where the block did not select them)
-    bf16x8_t kf[KS];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) kf[s] = *(const bf16x8_t*)(ks + kofs[s]);
-    f32x16_t st;
+  for (int i = 0; i < TS::NI; ++i) rr[i] = (w * TS::NI + i) * TS::RPI + l / TS::CPR;
+
+  // the union (U key blocks) is streamed in chunks of at most ATTN_UCAP key
+  // blocks; the online softmax state carries over from one chunk to the next
+  const int lane = tid & 63, wv = tid >> 6;
+  int U = ATTN_UCAP;
+  for (int ch = 0; ch * ATTN_UCAP < U; ++ch) {
+    // stream table of this chunk: ut[j] = {stream position, first row of Kp}
+    // of its j-th key block, ut[Uc] = {end position, -1}; selw[j] its bits
     {
-      const float* br = bias + slot * ATTN_LB * KT + bofs;
+      uint32_t f[EPT];
+      int x[EPT], kst[EPT], c = 0, s = 0;
+#pragma unroll
+      for (int k = 0; k < EPT; ++k) {
+        const int v = tid * EPT + k;
+        f[k] = v < CK ? (flg[v >> 1] >> (16 * (v & 1))) & 0xffffu : 0u;
+        x[k] = 0;
+        kst[k] = -1;
+        if (f[k]) {
+          kst[k] = koff[v];
+          x[k] = max(0, koff[v + 1] - kst[k]);
+          ++c;
+        }
+        s += x[k];
+      }
+      int ic = c, is = s;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int yc = __shfl_up(ic, o, 64), ys = __shfl_up(is, o, 64);
+        if (lane >= o) {
+          ic += yc;
+          is += ys;
+        }
+      }
+      if (lane == 63) {
+        tmp[0][wv] = ic;
+        tmp[1][wv] = is;
+      }
+      __syncthreads();
+      int jc = ic - c, js = is - s;
+      U = 0;
+      for (int w2 = 0; w2 < NW; ++w2) {
+        jc += w2 < wv ? tmp[0][w2] : 0;
+        js += w2 < wv ? tmp[1][w2] : 0;
+        U += tmp[0][w2];
+      }
+      const int jlo = ch * ATTN_UCAP, jhi = min(jlo + ATTN_UCAP, U);
+#pragma unroll
+      for (int k = 0; k < EPT; ++k)
+        if (f[k]) {
+          if (jc >= jlo && jc < jhi) {
+            ut[jc - jlo] = make_int2(js, kst[k]);
+            selw[jc - jlo] = (uint16_t)f[k];
+            if (jc == jhi - 1) ut[jc - jlo + 1] = make_int2(js + x[k], -1);
+          }
+          ++jc;
+          js += x[k];
+        }
+      __syncthreads();
+    }
+    if (U == 0) break;
+    const int Uc = min(ATTN_UCAP, U - ch * ATTN_UCAP);
+    const int base = ut[0].x, nk = ut[Uc].x - base;
+    int jj[TS::NI], cj[TS::NI], kj[TS::NI], src[TS::NI];
+    uint32_t sw[TS::NI], kb[TS::NI];
+    int2 nx[TS::NI];
+#pragma unroll
+    for (int i = 0; i < TS::NI; ++i) {
+      jj[i] = 0;
+      cj[i] = base;
+      kj[i] = ut[0].y;
+      sw[i] = selw[0];
+      nx[i] = ut[1];
+      src[i] = 0;
+      kb[i] = 0u;
+    }
+    auto advance = [&](int t) {
+      if (!dma_w) return;
+#pragma unroll
+      for (int i = 0; i < TS::NI; ++i) {
+        const int pos = base + t * KT + rr[i];
+        while (pos >= nx[i].x && jj[i] + 1 < Uc) {
+          ++jj[i];
+          cj[i] = nx[i].x;
+          kj[i] = nx[i].y;
+          sw[i] = selw[jj[i]];
+          nx[i] = ut[jj[i] + 1];
+        }
+        const int r = kj[i] + (pos - cj[i]);
+        const bool ok = pos < base + nk && (unsigned)r < (unsigned)N;
+        src[i] = ok ? r : 0;
+        kb[i] = ok ? sw[i] : 0u;
+      }
+    };
+    // tile T: K into slot T % NSK, V into slot T % NSV, with the score bias
+    // of every (query block, tile row)
+    auto issue = [&](int T) {
+      if (!dma_w) return;
+      const int sk = T % NSK, sv = T % NSV;
+      bf16_t* ks = Ks + sk * TS::ELEMS;
+      bf16_t* vs = Vs + sv * TS::ELEMS;
+#pragma unroll
+      for (int i = 0; i < TS::NI; ++i) {
+        const int off = (w * TS::NI + i) * 512;  // 1 KB per wave-wide DMA
+        lds_dma16(Kh + (size_t)src[i] * D + 8 * (pch ^ swz_k<D>(rr[i])), lds_addr(ks + off));
+      }
+#pragma unroll
+      for (int i = 0; i < TS::NI; ++i) {
+        const int off = (w * TS::NI + i) * 512;
+        lds_dma16(Vh + (size_t)src[i] * D + 8 * (pch ^ swz_v32<D>(rr[i])), lds_addr(vs + off));
+      }
+      // row r of block b sits at b * KT + ((r + bias_rot(b)) % KT): groups of
+      // four rows stay contiguous and the 16 blocks of one row land in 16
+      // different banks
+      float* bs = bias + sk * ATTN_LB * KT;
+#pragma unroll
+      for (int i = 0; i < TS::NI; ++i)
+#pragma unroll
+        for (int b = pch; b < ATTN_LB; b += TS::CPR)
+          bs[b * KT + ((rr[i] + bias_rot(b)) & (KT - 1))] = ((kb[i] >> b) & 1u) ? 0.0f : -INFINITY;
+    };
+    // S^T of tile T (32 keys x 32 queries; lane: keys 8 b + 4 hf + r of query
+    // c32), starting from the bias of those keys
+    auto scores = [&](int T, f32x16_t& st) {
+      const int sk = T % NSK;
+      const bf16_t* ks = Ks + sk * TS::ELEMS;
+      bf16x8_t kf[KS];
+#pragma unroll
+      for (int s2 = 0; s2 < KS; ++s2) kf[s2] = *(const bf16x8_t*)(ks + kofs[s2]);
+      const float* br = bias + sk * ATTN_LB * KT + brow;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        const float4 x = *(const float4*)(br + 8 * b);
-        st[4 * b + 0] = x.x;
-        st[4 * b + 1] = x.y;
-        st[4 * b + 2] = x.z;
-        st[4 * b + 3] = x.w;
-      }
-    }
-    frags_ready<KS>(kf);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], qf[s], st, 0, 0, 0);
-    float tmax = fmaxf(st[0], st[1]);
-#pragma unroll
-    for (int q = 2; q < 16; ++q) tmax = fmaxf(tmax, st[q]);
-    tmax = max_xor32(tmax);
-    // the reference maximum moves only when a row maximum exceeds it by more
-    // than 2^8 in probability (softmax is invariant to the shift; p <= 2^8)
-    if (__any((tmax - m) * scale_log2 > 8.0f)) {
-      // rows without a kept key so far keep m = -inf (and alpha = 1)
-      const float mnew = fmaxf(m, tmax);
-      const float alpha = mnew == m ? 1.0f : __builtin_amdgcn_exp2f((m - mnew) * scale_log2);
-      lpart *= alpha;
-#pragma unroll
-      for (int b = 0; b < DB; ++b) acc[b] *= alpha;
-      m = mnew;
-    }
-    const float nms = m == -INFINITY ? 0.0f : -m * scale_log2;
-    float p[16];
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      p[q] = __builtin_amdgcn_exp2f(fmaf(st[q], scale_log2, nms));
-      lpart += p[q];
-    }
-    // O^T += V^T P^T in two 16-key steps; step kp takes scores 8 kp .. 8 kp + 7
-    // (keys 16 kp + 4 hf + r and 16 kp + 8 + 4 hf + r)
-#pragma unroll
-    for (int kp = 0; kp < 2; ++kp) {
-      bf16x8_t pb;
-#pragma unroll
-      for (int e = 0; e < 8; e += 2) {
-        const bf16x2_t two =
-            __builtin_convertvector(f32x2_t{p[8 * kp + e], p[8 * kp + e + 1]}, bf16x2_t);
-        pb[e] = two[0];
-        pb[e + 1] = two[1];
+        const float4 y = *(const float4*)(br + ((bcol + 8 * b) & (KT - 1)));
+        st[4 * b + 0] = y.x;
+        st[4 * b + 1] = y.y;
+        st[4 * b + 2] = y.z;
+        st[4 * b + 3] = y.w;
       }
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const bf16_t* v1 = vs + vofs[db] + 16 * kp * D;
-        const i16x4_t t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)v1);
-        const i16x4_t t2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(v1 + 8 * D));
-        const bf16x8_t a = __builtin_bit_cast(
-            bf16x8_t, (short __attribute__((ext_vector_type(8)))){t1[0], t1[1], t1[2], t1[3],
-                                                                  t2[0], t2[1], t2[2], t2[3]});
-        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, acc[db], 0, 0, 0);
+      for (int s2 = 0; s2 < KS; ++s2)
+        st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s2], qf[s2], st, 0, 0, 0);
+    };
+    const int ntiles = (nk + KT - 1) / KT;
+    // tiles 0 .. NSK - 1 in flight, then S^T of tile 0
+#pragma unroll
+    for (int p = 0; p < NSK; ++p)
+      if (p < ntiles) {
+        advance(p);
+        issue(p);
       }
+    f32x16_t st_next;
+    if (ntiles > 0) {
+      wait_oldest<2 * TS::NI, NSK + 1>(ntiles - 1);
+      __syncthreads();
+      scores(0, st_next);
     }
+    for (int t = 0; t < ntiles; ++t) {
+      // at the top: S^T(t) is in st_next; tiles t+1 .. t+NSK-1 are in flight
+      const f32x16_t st = st_next;
+      const int nxt = t + NSK;
+      if (nxt < ntiles) advance(nxt);
+      // K(t+1) (and with it everything issued before: V(t)) has landed; V(t+1)
+      // and the tiles after t+1 may stay in flight
+      if (t + 2 < ntiles) wait_oldest<TS::NI, 8>(2 * (min(ntiles - 2 - t, NSK - 2)) + 1);
+      else if (t + 1 < ntiles) wait_vmcnt<TS::NI>();
+      else wait_vmcnt<0>();
+      __syncthreads();  // K(t+1), V(t) visible; K(t) and V(t-1) are free
+      if (nxt < ntiles) issue(nxt);
+      // softmax of tile t and O^T += V^T P^T; the scores of tile t+1 are
+      // computed in the same block so that their MFMAs overlap this VALU work
+      // row maximum of tile t and the (lazy) rescale of the running state
+      auto rescale = [&]() {
+        float tmax = fmaxf(st[0], st[1]);
+#pragma unroll
+        for (int q = 2; q < 16; ++q) tmax = fmaxf(tmax, st[q]);
+        tmax = max_xor32(tmax);
+        // the reference maximum moves only when a row maximum exceeds it by
+        // more than 2^8 in probability (softmax is invariant to the shift; p <= 2^8)
+        if (__any((tmax - m) * scale_log2 > 8.0f)) {
+          // rows without a kept key so far keep m = -inf (and alpha = 1)
+          const float mnew = fmaxf(m, tmax);
+          const float alpha = mnew == m ? 1.0f : __builtin_amdgcn_exp2f((m - mnew) * scale_log2);
+          lpart *= alpha;
+#pragma unroll
+          for (int b = 0; b < DB; ++b) acc[b] *= alpha;
+          m = mnew;
+        }
+      };
+      // probabilities of tile t and O^T += V^T P^T in two 16-key steps; step
+      // kp takes scores 8 kp .. 8 kp + 7 (keys 16 kp + 4 hf + r and
+      // 16 kp + 8 + 4 hf + r)
+      auto pv = [&]() {
+        const float nms = m == -INFINITY ? 0.0f : -m * scale_log2;
+        const bf16_t* vs = Vs + (t % NSV) * TS::ELEMS;
+#pragma unroll
+        for (int kp = 0; kp < 2; ++kp) {
+          float p[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            p[e] = __builtin_amdgcn_exp2f(fmaf(st[8 * kp + e], scale_log2, nms));
+            lpart += p[e];
+          }
+          bf16x8_t pb;
+#pragma unroll
+          for (int e = 0; e < 8; e += 2) {
+            const bf16x2_t two = __builtin_convertvector(f32x2_t{p[e], p[e + 1]}, bf16x2_t);
+            pb[e] = two[0];
+            pb[e + 1] = two[1];
+          }
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const bf16_t* v1 = vs + vofs[db] + 16 * kp * D;
+            const i16x4_t t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)v1);
+            const i16x4_t t2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(v1 + 8 * D));
+            const bf16x8_t a = __builtin_bit_cast(
+                bf16x8_t, (short __attribute__((ext_vector_type(8)))){t1[0], t1[1], t1[2], t1[3],
+                                                                      t2[0], t2[1], t2[2], t2[3]});
+            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, acc[db], 0, 0, 0);
+          }
+        }
+      };
+      // every tile is computed by every wavefront (keys that its query blocks
+      // did not select have score -inf, so they add nothing); the scores of
+      // tile t+1 (past the end: a stale slot, never used) are computed in the
+      // same block as the probabilities of tile t so that their MFMAs overlap
+      // that VALU work
+      rescale();
+      scores(t + 1, st_next);
+      pv();
+    }
+    __syncthreads();  // every wavefront is done with this chunk's tables and ring
   }
   float lsum = lpart + __shfl_xor(lpart, 32, 64);
   if (qvalid) {
@@ -1311,7 +1344,7 @@ static park_status attn_mfma_launch(const void* Qp, const void* Kp, const void* 
 
 size_t attn_grp_offset(int H, int CQ);
 
-template <typename OT, int D, int NW, int NS>
+template <typename OT, int D, int NW>
 static park_status attn_grp_launch(const void* Qp, const void* Kp, const void* Vp, const int* qo,
                                    const int* ko, const int* kc, const int* ki, const int* qp,
                                    int H, int N, int CQ, int CK, void* plan, float sl2, void* O,
@@ -1322,19 +1355,17 @@ static park_status attn_grp_launch(const void* Qp, const void* Kp, const void* V
   int4* grp = (int4*)((char*)plan + attn_grp_offset(H, CQ));
   PARK_LAUNCH("attn_plan", k_attn_gplan, dim3(H), dim3(1024), 0, st, qo, kc, ki, ko, N, CQ, CK,
               GPH, order, spre, grp);
-  // K/V ring, score biases, then the union tables (selection words, stream table)
-  constexpr size_t fixed =
-      (size_t)2 * NS * 32 * D * sizeof(bf16_t) + (size_t)NS * ATTN_LB * 32 * 4;
-  const size_t lds = fixed + (size_t)((CK + 3) & ~3) * 4 + (size_t)(CK + 1) * sizeof(int2);
-  // reserved once for the largest CK (2048), outside any stream capture that may follow
+  // K ring, V ring, score biases, key-block flags, stream table, selection words
+  constexpr size_t lds = (size_t)(2 * ATTN_KSLOTS + 1) * 32 * D * sizeof(bf16_t) +
+                         (size_t)ATTN_KSLOTS * ATTN_LB * 32 * 4 + (size_t)AT_MAXC / 2 * 4 +
+                         (size_t)(ATTN_UCAP + 1) * sizeof(int2) + (size_t)ATTN_UCAP * 2;
   static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)k_attn_grp<OT, D, NW, NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)(fixed + (size_t)AT_MAXC * 4 + (size_t)(AT_MAXC + 1) * sizeof(int2)));
+      (const void*)k_attn_grp<OT, D, NW>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess)
     return fail(PARK_ERR_HIP, "attention: cannot reserve %zu bytes of LDS", lds);
   // 8 * ceil(items / 8) workgroups: every item owns one (see the remap in the kernel)
   const unsigned nwg = 8u * (((unsigned)H * (unsigned)GPH + 7u) / 8u);
-  PARK_LAUNCH("attn_mfma", (k_attn_grp<OT, D, NW, NS>), dim3(nwg), dim3(64 * NW), lds, st,
+  PARK_LAUNCH("attn_mfma", (k_attn_grp<OT, D, NW>), dim3(nwg), dim3(64 * NW), lds, st,
               (const bf16_t*)Qp, (const bf16_t*)Kp, (const bf16_t*)Vp, qo, ko, kc, ki, qp, order,
               spre, grp, H, N, CQ, CK, GPH, sl2, (OT*)O);
   return PARK_OK;
@@ -1347,10 +1378,10 @@ static park_status attn_mfma_d(const void* Qp, const void* Kp, const void* Vp, c
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)D));
 #if PARK_ATTN_GROUP
   if (D == 128)
-    return attn_grp_launch<OT, 128, ATTN_R / 32, ATTN_RING>(Qp, Kp, Vp, qo, ko, kc, ki, qp, H, N,
-                                                             CQ, CK, plan, sl2, O, st);
-  return attn_grp_launch<OT, 64, ATTN_R / 32, ATTN_RING>(Qp, Kp, Vp, qo, ko, kc, ki, qp, H, N, CQ,
-                                                           CK, plan, sl2, O, st);
+    return attn_grp_launch<OT, 128, ATTN_R / 32>(Qp, Kp, Vp, qo, ko, kc, ki, qp, H, N, CQ, CK,
+                                                  plan, sl2, O, st);
+  return attn_grp_launch<OT, 64, ATTN_R / 32>(Qp, Kp, Vp, qo, ko, kc, ki, qp, H, N, CQ, CK, plan,
+                                              sl2, O, st);
 #else
   const int CPH = attn_chunks_per_head(N, CQ);
   int4* pl = (int4*)plan;
