@@ -10,49 +10,90 @@
 
 namespace park {
 
-// Partial Gram matrix of one row chunk: part[h][chunk] = sum_r x_r x_r^T.
-// 256 threads on a 16x16 grid; each owns a (D/16)x(D/16) tile of G.
+// Partial Gram matrix of one row chunk, part[h][chunk] = sum_r x_r x_r^T, on
+// fp64 MFMA (products of the bf16 / fp32
+// inputs are exact in fp64, accumulation in fp64).  Lane l takes row
+// r + l/16 of a 4-row step and the E = D/16 consecutive elements
+// E c .. E c + E - 1 (c = l % 16) with one load; value e of the lane is then
+// entry c of the 16-wide column block e, so the block product (a, b) is
+// G[E m + a][E n + b] = sum_r x[r][E m + a] x[r][E n + b] (m, n < 16).  Of
+// the E (E + 1) / 2 blocks with a <= b, wavefront w owns those with index
+// p = w (mod 4); the lower triangle is written by transposition.  Register i
+// of lane l holds output entry (l/16 + 4 i, l % 16).
+typedef double gram_f64x4_t __attribute__((ext_vector_type(4)));
+
 template <typename T, int D>
-__global__ __launch_bounds__(256) void k_gram_partial(const T* __restrict__ X, int N, int rows_per,
-                                                      double* __restrict__ part) {
-  constexpr int TS = D / 16;
-  constexpr int RB = 32;  // rows staged per LDS round
-  __shared__ float xs[RB][D + 4];
+__global__ __launch_bounds__(256) void k_gram_mfma(const T* __restrict__ X, int N, int rows_per,
+                                                   double* __restrict__ part) {
+  constexpr int E = D / 16, NPAIR = E * (E + 1) / 2, PW = (NPAIR + 3) / 4;  // PW: pairs per wavefront
   const int h = blockIdx.y, ch = blockIdx.x, nch = gridDim.x;
   const int r0 = ch * rows_per, r1 = min(N, r0 + rows_per);
-  const int ti = threadIdx.x >> 4, tj = threadIdx.x & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l = threadIdx.x & 63, c = l & 15, rq = l >> 4;
   const T* Xh = X + (size_t)h * N * D;
-  double acc[TS][TS];
+  gram_f64x4_t acc[PW];
 #pragma unroll
-  for (int a = 0; a < TS; ++a)
+  for (int k = 0; k < PW; ++k) acc[k] = gram_f64x4_t{0.0, 0.0, 0.0, 0.0};
+  auto load = [&](int r, double (&x)[E]) {
+    if (r < r1) {
+      if constexpr (sizeof(T) == 2) {
+        const bf16_t* src = (const bf16_t*)Xh + (size_t)r * D + E * c;
+        if constexpr (E == 8) {
+          const uint4 u = *(const uint4*)src;
+          const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-    for (int b = 0; b < TS; ++b) acc[a][b] = 0.0;
-
-  for (int rb = r0; rb < r1; rb += RB) {
-    const int nr = min(RB, r1 - rb);
-    for (int e = threadIdx.x; e < RB * D; e += 256) {
-      const int r = e / D, c = e % D;
-      xs[r][c] = (r < nr) ? to_f(Xh[(size_t)(rb + r) * D + c]) : 0.0f;
+          for (int e = 0; e < 8; ++e)
+            x[e] = (double)__uint_as_float((e & 1) ? (wv[e >> 1] & 0xffff0000u) : (wv[e >> 1] << 16));
+        } else {
+          const uint2 u = *(const uint2*)src;
+          const uint32_t wv[2] = {u.x, u.y};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            x[e] = (double)__uint_as_float((e & 1) ? (wv[e >> 1] & 0xffff0000u) : (wv[e >> 1] << 16));
+        }
+      } else {
+        const float* src = (const float*)Xh + (size_t)r * D + E * c;
+#pragma unroll
+        for (int e = 0; e < E; e += 4) {
+          const float4 f = *(const float4*)(src + e);
+          x[e] = f.x;
+          x[e + 1] = f.y;
+          x[e + 2] = f.z;
+          x[e + 3] = f.w;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < E; ++e) x[e] = 0.0;
     }
-    __syncthreads();
-    for (int r = 0; r < nr; ++r) {
-      double xa[TS], xb[TS];
+  };
+  double x[E], xn[E];
+  load(r0 + rq, x);
+  for (int rb = r0; rb < r1; rb += 4) {
+    load(rb + 4 + rq, xn);  // next step in flight
+    // block pair p = (a, b), a <= b, in row-major order of the upper triangle
 #pragma unroll
-      for (int a = 0; a < TS; ++a) xa[a] = (double)xs[r][ti * TS + a];
+    for (int a = 0, p = 0; a < E; ++a)
 #pragma unroll
-      for (int b = 0; b < TS; ++b) xb[b] = (double)xs[r][tj * TS + b];
+      for (int b = a; b < E; ++b, ++p)
+        if ((p & 3) == w) acc[p >> 2] = __builtin_amdgcn_mfma_f64_16x16x4f64(x[a], x[b], acc[p >> 2], 0, 0, 0);
 #pragma unroll
-      for (int a = 0; a < TS; ++a)
-#pragma unroll
-        for (int b = 0; b < TS; ++b) acc[a][b] = fma(xa[a], xb[b], acc[a][b]);
-    }
-    __syncthreads();
+    for (int e = 0; e < E; ++e) x[e] = xn[e];
   }
   double* out = part + ((size_t)h * nch + ch) * D * D;
 #pragma unroll
-  for (int a = 0; a < TS; ++a)
+  for (int a = 0, p = 0; a < E; ++a)
 #pragma unroll
-    for (int b = 0; b < TS; ++b) out[(ti * TS + a) * D + tj * TS + b] = acc[a][b];
+    for (int b = a; b < E; ++b, ++p) {
+      if ((p & 3) != w) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // lane (c, rq) register i holds entry (rq + 4 i, c) of the 16 x 16 block
+        const int gi = E * (rq + 4 * i) + a, gj = E * c + b;
+        out[(size_t)gi * D + gj] = acc[p >> 2][i];
+        if (a != b) out[(size_t)gj * D + gi] = acc[p >> 2][i];
+      }
+    }
 }
 
 // G[h] = (sum over chunks, in chunk order) / N
@@ -214,17 +255,17 @@ park_status launch_metric(const void* Q, int H, int N, int D, int dtype, double 
   dim3 g1(nch, H);
   if (D == 128) {
     if (dtype == PARK_BF16)
-      PARK_LAUNCH("gram_partial", (k_gram_partial<bf16_t, 128>), g1, dim3(256), 0, st,
+      PARK_LAUNCH("gram_partial", (k_gram_mfma<bf16_t, 128>), g1, dim3(256), 0, st,
                   (const bf16_t*)Q, N, rows_per, part);
     else
-      PARK_LAUNCH("gram_partial", (k_gram_partial<float, 128>), g1, dim3(256), 0, st,
+      PARK_LAUNCH("gram_partial", (k_gram_mfma<float, 128>), g1, dim3(256), 0, st,
                   (const float*)Q, N, rows_per, part);
   } else {
     if (dtype == PARK_BF16)
-      PARK_LAUNCH("gram_partial", (k_gram_partial<bf16_t, 64>), g1, dim3(256), 0, st,
+      PARK_LAUNCH("gram_partial", (k_gram_mfma<bf16_t, 64>), g1, dim3(256), 0, st,
                   (const bf16_t*)Q, N, rows_per, part);
     else
-      PARK_LAUNCH("gram_partial", (k_gram_partial<float, 64>), g1, dim3(256), 0, st,
+      PARK_LAUNCH("gram_partial", (k_gram_mfma<float, 64>), g1, dim3(256), 0, st,
                   (const float*)Q, N, rows_per, part);
   }
   const int DD = D * D;

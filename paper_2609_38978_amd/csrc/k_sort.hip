@@ -8,12 +8,13 @@
 
 namespace park {
 
-// Tokens per scatter tile: small enough to give >= ~512 wavefronts over all
-// heads, large enough that the per-head histogram table (C x tiles) stays
-// below 64K entries so the single-workgroup scan stays short.
+// Tokens per scatter tile: the smallest power of two >= 256 for which the
+// per-head histogram table (C x tiles) stays below 64K entries, so that the
+// single-workgroup scan stays short while the scatter (one wavefront per
+// tile, serial within the tile) gets as many wavefronts as possible.
 int sort_tile(int H, int N, int C) {
+  (void)H;
   int t = 256;
-  while ((long)H * ((N + t - 1) / t) > 512 && t < 8192) t *= 2;
   while ((long)C * ((N + t - 1) / t) > 65536 && t < (1 << 30)) t *= 2;
   return t;
 }
@@ -32,9 +33,17 @@ __global__ __launch_bounds__(256) void k_sort_hist(const int* __restrict__ label
   __syncthreads();
   const int i0 = tile * tile_sz, i1 = min(N, i0 + tile_sz);
   const int* z = labels + (size_t)h * N;
-  for (int i = i0 + threadIdx.x; i < i1; i += 256) {
-    const int v = z[i];
-    if ((unsigned)v < (unsigned)C) atomicAdd(&hist[v], 1);
+  // eight loads in flight per thread
+  for (int c0 = i0; c0 < i1; c0 += 8 * 256) {
+    int v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = c0 + 256 * k + threadIdx.x;
+      v[k] = i < i1 ? z[i] : -1;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if ((unsigned)v[k] < (unsigned)C) atomicAdd(&hist[v[k]], 1);
   }
   __syncthreads();
   int* out = thist + (size_t)h * C * nt;
@@ -118,22 +127,34 @@ __global__ __launch_bounds__(64) void k_sort_scatter(const int* __restrict__ lab
   int* p = perm + (size_t)h * N;
   const uint64_t lt = (1ull << lane) - 1ull;
   const uint64_t gt = ~((2ull << lane) - 1ull);
-  for (int c0 = i0; c0 < i1; c0 += 64) {
-    const int i = c0 + lane;
-    const bool valid = i < i1;
-    int v = valid ? z[i] : 0;
-    const bool ok = valid && (unsigned)v < (unsigned)C;
-    uint64_t m = __ballot(ok);
-    for (int bit = 0; bit < nbits; ++bit) {
-      const bool set = (v >> bit) & 1;
-      const uint64_t B = __ballot(ok && set);
-      m &= set ? B : ~B;
+  // the labels of 16 wavefront steps are loaded together (latency once per
+  // 1024 tokens instead of once per step)
+  constexpr int UN = 16;
+  for (int c00 = i0; c00 < i1; c00 += 64 * UN) {
+    int vv[UN];
+#pragma unroll
+    for (int k = 0; k < UN; ++k) {
+      const int i = c00 + 64 * k + lane;
+      vv[k] = i < i1 ? z[i] : -1;
     }
-    const int rank = __popcll(m & lt);
-    if (ok) p[run[v] + rank] = i;
-    __syncthreads();
-    if (ok && (m & gt) == 0) run[v] += rank + 1;
-    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < UN; ++k) {
+      if (c00 + 64 * k >= i1) break;
+      const int i = c00 + 64 * k + lane;
+      const int v = vv[k];
+      const bool ok = i < i1 && (unsigned)v < (unsigned)C;
+      uint64_t m = __ballot(ok);
+      for (int bit = 0; bit < nbits; ++bit) {
+        const bool set = (v >> bit) & 1;
+        const uint64_t B = __ballot(ok && set);
+        m &= set ? B : ~B;
+      }
+      const int rank = __popcll(m & lt);
+      if (ok) p[run[v] + rank] = i;
+      __syncthreads();
+      if (ok && (m & gt) == 0) run[v] += rank + 1;
+      __syncthreads();
+    }
   }
 }
 
