@@ -1220,7 +1220,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
       else if (t + 1 < ntiles) wait_vmcnt<TS::NI>();
       else wait_vmcnt<0>();
       __syncthreads();  // K(t+1), V(t) visible; K(t) and V(t-1) are free
-      if (nxt < ntiles) issue(nxt);
       // softmax of tile t and O^T += V^T P^T; the scores of tile t+1 are
       // computed in the same block so that their MFMAs overlap this VALU work
       // row maximum of tile t and the (lazy) rescale of the running state
@@ -1282,6 +1281,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
       rescale();
       scores(t + 1, st_next);
       pv();
+      // the DMAs of tile t+NSK go out after this step's compute: a DMA issue
+      // that stalls on a busy memory system then does not hold the MFMAs back
+      if (nxt < ntiles) issue(nxt);
     }
     __syncthreads();  // every wavefront is done with this chunk's tables and ring
   }
