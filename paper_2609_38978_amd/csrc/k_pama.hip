@@ -774,6 +774,294 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
   }
 }
 
+// Top-k on the float W^ of one row by radix selection (no sort): the m-th
+// largest value a (m = kcount clamped to [1, #nonempty]) is found 8 bits at a
+// time (W^ >= 0, so float order is the order of the bit patterns), then the
+// number of values >= a and the largest value below a give the (m+1)-th
+// largest b (= a on a tie).  The row is certified when a (1 - delta) - eps >
+// b (1 + delta) + eps, and then the kept set is exactly {W^ >= a}; otherwise
+// it is listed for the float64 path.  256 threads; `hist` and `aux` need 2048
+// ints, `tmp` 4.
+__device__ void select_topk_radix(const float* __restrict__ w, const int* __restrict__ ksz, int CK,
+                                  int kcount, double dl, int* __restrict__ kv_count,
+                                  int* __restrict__ out, int* __restrict__ rows,
+                                  int* __restrict__ nrows, int u, int* hist, int* aux, int* tmp) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  constexpr int E = MAXC / 256;
+  uint32_t kv[E];
+  int nv = 0;
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int e = tid + 256 * k;
+    const bool ok = e < CK && ksz[e] > 0;
+    // valid keys have bit 31 clear (W^ >= 0); invalid ones are all ones and never match
+    const float x = ok ? w[e] : 0.0f;
+    kv[k] = ok ? (x > 0.0f ? __float_as_uint(x) : 0u) : 0xffffffffu;
+    nv += ok;
+  }
+  // block sum (wave shuffles, then the four wavefront totals)
+  auto block_sum = [&](int x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    __syncthreads();
+    if (lane == 0) tmp[wid] = x;
+    __syncthreads();
+    return tmp[0] + tmp[1] + tmp[2] + tmp[3];
+  };
+  const int nvalid = block_sum(nv);
+  if (nvalid == 0) {
+    if (tid == 0) *kv_count = 0;
+    return;
+  }
+  const int m = min(max(kcount, 1), nvalid);
+  // rank m from the top, 8 bits per pass
+  uint32_t prefix = 0u, pmask = 0u;
+  int r = m;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    hist[tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < E; ++k)
+      if ((kv[k] >> 31) == 0u && (kv[k] & pmask) == prefix) atomicAdd(&hist[(kv[k] >> shift) & 255u], 1);
+    __syncthreads();
+    // counts from the highest digit down: thread t holds digit 255 - t
+    const int c = hist[255 - tid];
+    int inc = c;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(inc, o, 64);
+      if (lane >= o) inc += y;
+    }
+    if (lane == 63) tmp[wid] = inc;
+    __syncthreads();
+    for (int w2 = 0; w2 < wid; ++w2) inc += tmp[w2];
+    if (inc >= r && inc - c < r) {
+      aux[0] = 255 - tid;
+      aux[1] = r - (inc - c);
+    }
+    __syncthreads();
+    prefix |= (uint32_t)aux[0] << shift;
+    pmask |= 255u << shift;
+    r = aux[1];
+    __syncthreads();
+  }
+  const uint32_t a_bits = prefix;
+  int ge = 0;
+  uint32_t lt = 0u;  // the largest value below a (0: none)
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const bool v = (kv[k] >> 31) == 0u;
+    ge += v && kv[k] >= a_bits;
+    if (v && kv[k] < a_bits) lt = max(lt, kv[k]);
+  }
+  const int cnt_ge = block_sum(ge);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) lt = max(lt, (uint32_t)__shfl_xor((int)lt, o, 64));
+  __syncthreads();
+  if (lane == 0) tmp[wid] = (int)lt;
+  __syncthreads();
+  lt = max(max((uint32_t)tmp[0], (uint32_t)tmp[1]), max((uint32_t)tmp[2], (uint32_t)tmp[3]));
+  const double eps = 4.0 * 1.1754943508222875e-38;  // absolute error near underflow
+  bool ok = cnt_ge == m;
+  if (ok && m < nvalid) {
+    const double a = (double)__uint_as_float(a_bits) * (1.0 - dl) - eps;
+    const double b = (double)__uint_as_float(lt) * (1.0 + dl) + eps;
+    ok = a > b;
+  }
+  if (!ok) {
+    if (tid == 0) rows[atomicAdd(nrows, 1)] = u;
+    return;
+  }
+  // kept: W^ >= a; written in ascending id order
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int e = tid + 256 * k;
+    if (e < MAXC) hist[e] = ((kv[k] >> 31) == 0u && kv[k] >= a_bits) ? 1 : 0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < E; ++k) aux[tid + 256 * k] = hist[tid + 256 * k];
+  __syncthreads();
+  block_exclusive_scan_2048(aux, CK, tmp);
+  for (int e = tid; e < CK; e += 256)
+    if (hist[e]) out[aux[e]] = e;
+  if (tid == 0) *kv_count = m;
+}
+
+// Top-p on the float W^ of one row without sorting: the value T of the last
+// kept block (the largest T whose mass {W^ >= T} reaches p) is found 8 bits at
+// a time from per-digit counts and float64 masses.  Those masses are summed
+// with atomics, so T may come out wrong near rounding ties; the certification
+// below uses deterministic sums and only passes for the unique correct set
+// (it reaches p with margin, without its smallest member it does not, and its
+// smallest value is separated from the next one), so an accepted row is right
+// and the others go to the float64 path.  All blocks are kept when the total
+// mass is below p.  256 threads; `hist`, `aux` need 2048 ints, `dh` 256
+// doubles, `tmp` 4 ints, `dtmp` 4 doubles.
+__device__ void select_topp_radix(const float* __restrict__ w, const int* __restrict__ ksz, int CK,
+                                  double p, double dl, int* __restrict__ kv_count,
+                                  int* __restrict__ out, int* __restrict__ rows,
+                                  int* __restrict__ nrows, int u, int* hist, int* aux, double* dh,
+                                  int* tmp, double* dtmp) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  constexpr int E = MAXC / 256;
+  uint32_t kv[E];
+  int nv = 0;
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int e = tid + 256 * k;
+    const bool ok = e < CK && ksz[e] > 0;
+    const float x = ok ? w[e] : 0.0f;
+    kv[k] = ok ? (x > 0.0f ? __float_as_uint(x) : 0u) : 0xffffffffu;
+    nv += ok;
+  }
+  auto valid = [&](int k) { return (kv[k] >> 31) == 0u; };
+  auto isum = [&](int x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    __syncthreads();
+    if (lane == 0) tmp[wid] = x;
+    __syncthreads();
+    return tmp[0] + tmp[1] + tmp[2] + tmp[3];
+  };
+  // deterministic float64 sum: fixed order per thread, shuffles, wavefronts
+  auto dsum = [&](double x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    __syncthreads();
+    if (lane == 0) dtmp[wid] = x;
+    __syncthreads();
+    return (dtmp[0] + dtmp[1]) + (dtmp[2] + dtmp[3]);
+  };
+  auto umax = [&](uint32_t x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x = max(x, (uint32_t)__shfl_xor((int)x, o, 64));
+    __syncthreads();
+    if (lane == 0) tmp[wid] = (int)x;
+    __syncthreads();
+    return max(max((uint32_t)tmp[0], (uint32_t)tmp[1]), max((uint32_t)tmp[2], (uint32_t)tmp[3]));
+  };
+  const int nvalid = isum(nv);
+  if (nvalid == 0) {
+    if (tid == 0) *kv_count = 0;
+    return;
+  }
+  double tl = 0.0;
+#pragma unroll
+  for (int k = 0; k < E; ++k)
+    if (valid(k)) tl += (double)__uint_as_float(kv[k]);
+  const double total = dsum(tl);
+  uint32_t T = 0u;  // bits of the last kept value
+  if (total >= p) {
+    uint32_t prefix = 0u, pmask = 0u;
+    double above = 0.0;  // mass of the values above the current prefix range
+    for (int pass = 0; pass < 4; ++pass) {
+      const int shift = 24 - 8 * pass;
+      hist[tid] = 0;
+      dh[tid] = 0.0;
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < E; ++k)
+        if (valid(k) && (kv[k] & pmask) == prefix) {
+          const int d = (kv[k] >> shift) & 255u;
+          atomicAdd(&hist[d], 1);
+          atomicAdd(&dh[d], (double)__uint_as_float(kv[k]));
+        }
+      __syncthreads();
+      // masses from the highest digit down: thread t holds digit 255 - t
+      const double ms = dh[255 - tid];
+      double inc = ms;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const double y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+      }
+      if (lane == 63) dtmp[wid] = inc;
+      __syncthreads();
+      for (int w2 = 0; w2 < wid; ++w2) inc += dtmp[w2];
+      // the first digit (from the top) at which the mass reaches p; the
+      // lowest digit with values when it is never reached (rounding)
+      const bool cross = above + inc >= p && above + inc - ms < p;
+      const int last = hist[255 - tid] > 0 ? tid : -1;
+      int lastv = last;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) lastv = max(lastv, __shfl_xor(lastv, o, 64));
+      __syncthreads();
+      if (lane == 0) tmp[wid] = lastv;
+      if (tid == 0) aux[0] = -1;
+      __syncthreads();
+      const int lastt = max(max(tmp[0], tmp[1]), max(tmp[2], tmp[3]));
+      if (cross) {
+        aux[0] = 255 - tid;
+        dtmp[0] = above + inc - ms;
+      }
+      __syncthreads();
+      int d = aux[0];
+      double ab = dtmp[0];
+      if (d < 0) {  // not reached inside this range: take its lowest digit
+        d = 255 - lastt;
+        __syncthreads();
+        if (tid == lastt) dtmp[0] = above + inc - ms;
+        __syncthreads();
+        ab = dtmp[0];
+      }
+      above = ab;
+      prefix |= (uint32_t)d << shift;
+      pmask |= 255u << shift;
+      __syncthreads();
+    }
+    T = prefix;
+  } else {
+    // every nonempty block is kept: T = the smallest value
+    uint32_t mn = 0xffffffffu;
+#pragma unroll
+    for (int k = 0; k < E; ++k)
+      if (valid(k)) mn = min(mn, kv[k]);
+    T = ~umax(~mn);
+  }
+  int gt = 0, eq = 0;
+  double ms = 0.0;
+  uint32_t lt = 0u;
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    if (!valid(k)) continue;
+    gt += kv[k] > T;
+    eq += kv[k] == T;
+    if (kv[k] >= T) ms += (double)__uint_as_float(kv[k]);
+    else lt = max(lt, kv[k]);
+  }
+  const int ngt = isum(gt), neq = isum(eq);
+  const double csum = dsum(ms);
+  lt = umax(lt);
+  const int m = ngt + neq;
+  // certification (delta: the row's relative error; eps: absolute error near underflow)
+  const double eps = 4.0 * 1.1754943508222875e-38;
+  const double tv = (double)__uint_as_float(T);
+  const double slo = csum * (1.0 - dl) - m * eps, shi = csum * (1.0 + dl) + m * eps;
+  const double minlo = tv * (1.0 - dl) - eps;
+  bool ok = m >= 1 && shi - minlo < p * (1.0 - 1e-12);
+  if (m < nvalid) {
+    ok = ok && neq == 1 && slo >= p * (1.0 + 1e-12);
+    ok = ok && minlo > (double)__uint_as_float(lt) * (1.0 + dl) + eps;
+  }
+  if (!ok) {
+    if (tid == 0) rows[atomicAdd(nrows, 1)] = u;
+    return;
+  }
+  // kept: W^ >= T; written in ascending id order
+#pragma unroll
+  for (int k = 0; k < E; ++k) hist[tid + 256 * k] = (valid(k) && kv[k] >= T) ? 1 : 0;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < E; ++k) aux[tid + 256 * k] = hist[tid + 256 * k];
+  __syncthreads();
+  block_exclusive_scan_2048(aux, CK, tmp);
+  for (int e = tid; e < CK; e += 256)
+    if (hist[e]) out[aux[e]] = e;
+  if (tid == 0) *kv_count = m;
+}
+
 // Certified selection on the float W^: sort (W^ descending, id ascending),
 // take the cut, and accept the row only if the cut is robust to the row's
 // relative error delta_u plus an absolute error for values below float's
@@ -790,12 +1078,10 @@ __global__ __launch_bounds__(256) void k_select_fast(const float* __restrict__ W
                                                      int* __restrict__ kv_index,
                                                      int* __restrict__ rows,
                                                      int* __restrict__ nrows) {
-  __shared__ float key[MAXC];
-  __shared__ int id[MAXC];
-  __shared__ int flag[MAXC];
+  __shared__ int flag[MAXC], aux[MAXC];
+  __shared__ double dh[256], dtmp[4];
   __shared__ int tmp[4];
-  __shared__ int nvalid_s, m_s, ok_s;
-  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x;
+  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int* off = q_offsets + (size_t)h * (CQ + 1);
   const int nu = off[u + 1] - off[u];
   const size_t row = (size_t)h * CQ + u;
@@ -803,90 +1089,15 @@ __global__ __launch_bounds__(256) void k_select_fast(const float* __restrict__ W
     if (tid == 0) kv_count[row] = 0;
     return;
   }
-  if (tid == 0) nvalid_s = 0;
-  __syncthreads();
-  int myvalid = 0;
-  for (int e = tid; e < P; e += 256) {
-    const bool ok = e < CK && k_sizes[(size_t)h * CK + e] > 0;
-    key[e] = ok ? W32[row * CK + e] : -1.0f;
-    id[e] = e;
-    if (e < CK) flag[e] = 0;
-    myvalid += ok;
+  if (mode == PARK_SELECT_TOPK) {
+    select_topk_radix(W32 + row * CK, k_sizes + (size_t)h * CK, CK, kcount, (double)delta[row],
+                      kv_count + row, kv_index + row * CK, rows + (size_t)h * CQ, nrows + h, u,
+                      flag, aux, tmp);
+    return;
   }
-  atomicAdd(&nvalid_s, myvalid);
-  __syncthreads();
-  for (int k = 2; k <= P; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int t = tid; t < P / 2; t += 256) {
-        const int i = 2 * t - (t & (j - 1));
-        const int l2 = i + j;
-        const bool up = (i & k) == 0;
-        const float ka = key[i], kb = key[l2];
-        const int ia = id[i], ib = id[l2];
-        const bool a_first = (ka > kb) || (ka == kb && ia < ib);
-        if (a_first != up) {
-          key[i] = kb;
-          key[l2] = ka;
-          id[i] = ib;
-          id[l2] = ia;
-        }
-      }
-      __syncthreads();
-    }
-  }
-  const int nvalid = nvalid_s;
-  if (tid == 0) {
-    const double dl = (double)delta[row];
-    const double eps = 4.0 * 1.1754943508222875e-38;  // absolute error near underflow
-    int m;
-    bool ok = true;
-    if (mode == PARK_SELECT_TOPK) {
-      m = kcount < 1 ? 1 : kcount;
-      if (m > nvalid) m = nvalid;
-    } else {
-      double cs = 0.0;
-      m = nvalid;
-      for (int r = 0; r < nvalid; ++r) {
-        cs += (double)key[r];
-        if (cs >= param) {
-          m = r + 1;
-          break;
-        }
-      }
-      // the kept set must reach p and the set without its smallest member not
-      double slo = 0.0, shi = 0.0, minlo = 1e300;
-      for (int r = 0; r < m; ++r) {
-        const double x = (double)key[r];
-        const double lo = x * (1.0 - dl) - eps;
-        slo += lo;
-        shi += x * (1.0 + dl) + eps;
-        minlo = fmin(minlo, lo);
-      }
-      if (m < nvalid) ok = ok && slo >= param * (1.0 + 1e-12);
-      ok = ok && (shi - minlo < param * (1.0 - 1e-12));
-    }
-    if (m < 1 && nvalid > 0) m = 1;
-    if (m < nvalid) {
-      const double a = (double)key[m - 1] * (1.0 - dl) - eps;
-      const double b = (double)key[m] * (1.0 + dl) + eps;
-      ok = ok && (a > b);
-    }
-    m_s = m;
-    ok_s = ok;
-    if (!ok) rows[(size_t)h * CQ + atomicAdd(nrows + h, 1)] = u;
-  }
-  __syncthreads();
-  if (!ok_s) return;
-  const int m = m_s;
-  for (int r = tid; r < m; r += 256) flag[id[r]] = 1;
-  __syncthreads();
-  for (int e = tid; e < CK; e += 256) id[e] = flag[e];
-  __syncthreads();
-  block_exclusive_scan_2048(id, CK, tmp);
-  int* out = kv_index + row * CK;
-  for (int e = tid; e < CK; e += 256)
-    if (flag[e]) out[id[e]] = e;
-  if (tid == 0) kv_count[row] = m;
+  select_topp_radix(W32 + row * CK, k_sizes + (size_t)h * CK, CK, param, (double)delta[row],
+                    kv_count + row, kv_index + row * CK, rows + (size_t)h * CQ, nrows + h, u, flag,
+                    aux, dh, tmp, dtmp);
 }
 
 __global__ void k_zero_counts(int* __restrict__ c, int n) {
