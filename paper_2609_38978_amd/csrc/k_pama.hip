@@ -4,9 +4,10 @@
 //   S^_iv = q_i . c_v / sqrt(d) + log n_v   (n_v = 0: block left out)
 //   P^_iv = softmax_v S^_iv;   W^_uv = (1 / n_u) sum_{i in Q_u} P^_iv
 //
-// k_pama64 evaluates this in float64 (float64 MFMA) with one workgroup per
-// (query block, head) at a time; the column sums stay in LDS and are added
-// in a fixed order (no HBM round trip, no atomics).
+// k_pama64 evaluates this in float64 (float64 MFMA) over items of whole
+// chunks of 64 queries; an item's column sums stay in LDS, and the items of
+// a query block are added up in item order (deterministic, no atomics on
+// values).
 #include "common.h"
 #include "kernels.h"
 
@@ -59,8 +60,8 @@ __device__ int block_exclusive_scan_2048(int* a, int n, int* tmp) {
 // centroids twice (normaliser pass, probability pass) through a two-slot LDS
 // ring filled by LDS DMA (rows swizzled in 16-byte chunks so the B-operand
 // reads are free of bank conflicts).  Logits, exponentials and all sums in
-// float64; per-wavefront column sums in LDS, added in wavefront order
-// (deterministic).  With a row list it recomputes only the listed query
+// float64; a tile's per-wavefront column sums go through LDS and are added to
+// the row's column sums in wavefront order, chunk after chunk (deterministic).  With a row list it recomputes only the listed query
 // blocks (the rows the fast path could not certify); the workgroups of a
 // head run on one XCD.
 __device__ __forceinline__ void p64_dma16(const void* g, uint32_t lds) {
@@ -73,54 +74,72 @@ __device__ __forceinline__ uint32_t p64_lds_addr(const void* p) {
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 template <typename T, int D>
-__global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp,
+__global__ __launch_bounds__(256, 2) void k_pama64(const T* __restrict__ Qp,
                                                 const int* __restrict__ q_offsets,
                                                 const float* __restrict__ cen,
                                                 const int* __restrict__ k_sizes, int H, int N,
-                                                int CQ, int CK, int rg, const int* __restrict__ rows,
-                                                const int* __restrict__ nrows,
+                                                int CQ, int CK, const int4* __restrict__ items,
+                                                int* __restrict__ cnt, double* __restrict__ part,
                                                 double* __restrict__ W64, float* __restrict__ W32,
                                                 int* status) {
   constexpr int CT = 32, CPR = D / 4, RPI = 64 / CPR, NI = CT / (4 * RPI), KS = D / 4;
   static_assert(NI * 4 * RPI == CT, "tile shape");
-  __shared__ __attribute__((aligned(16))) float Ct[2][CT * D];
-  __shared__ double Lt[2][CT];
-  extern __shared__ double wacc64[];  // [4][CK]
-  const int nitems = H * rg, per = (nitems + 7) >> 3;
-  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
-  if (item >= nitems) return;
-  const int h = item / rg, wg = item - h * rg;
+  constexpr int NS = 3;  // centroid ring: one tile in flight while one is used
+  __shared__ __attribute__((aligned(16))) float Ct[NS][CT * D];
+  __shared__ double Lt[NS][CT];
+  __shared__ double stg[2][4][CT];  // per-wavefront column sums of a tile (by step parity)
+  extern __shared__ double wacc64[];  // [CK] column sums of the item, in chunk and wavefront order
+  __shared__ int item_s;
   const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int cnt = rows ? min(nrows[h], CQ) : CQ;
-  const float* ch = cen + (size_t)h * CK * D;
-  const int* nh = k_sizes + (size_t)h * CK;
-  const int* off = q_offsets + (size_t)h * (CQ + 1);
-  const T* Qh = Qp + (size_t)h * N * D;
   const double isd = 1.0 / sqrt((double)D);
   const int nt = (CK + CT - 1) / CT;
   const int pch = l % CPR;
-  auto issue = [&](int tile, int slot) {
-    const int c0 = tile * CT;
+  const int nall = H * CQ, per = (nall + 7) >> 3;
+  for (int k = -1;;) {
+    // next item: from the queue, or (no item list) this workgroup's one row,
+    // rows of a head on one XCD
+    int rid, cb = 0, ce = 1 << 30, slot = -1;
+    if (items) {
+      __syncthreads();  // the previous item is finished with LDS and item_s
+      if (tid == 0) item_s = atomicAdd(&cnt[2], 1);
+      __syncthreads();
+      k = item_s;
+      if (k >= cnt[0]) break;
+      const int4 it = items[k];
+      rid = it.x;
+      cb = it.y;
+      ce = it.z;
+      slot = it.w;
+    } else {
+      if (k >= 0) break;
+      k = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+      if (k >= nall) break;
+      rid = k;
+    }
+    const int h = rid / CQ, u = rid - h * CQ;
+    const float* ch = cen + (size_t)h * CK * D;
+    const int* nh = k_sizes + (size_t)h * CK;
+    const int* off = q_offsets + (size_t)h * (CQ + 1);
+    const T* Qh = Qp + (size_t)h * N * D;
+    auto issue = [&](int tile, int slot) {
+      const int c0 = tile * CT;
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int r = (w * NI + i) * RPI + l / CPR;
-      const int v = min(c0 + r, CK - 1);
-      const float* src = ch + (size_t)v * D + 4 * (pch ^ (r & (CPR - 1)));
-      p64_dma16(src, p64_lds_addr(&Ct[slot][0] + (w * NI + i) * 256));
-    }
-    if (tid < CT) {
-      const int v = c0 + tid;
-      const int n = v < CK ? nh[v] : 0;
-      Lt[slot][tid] = n > 0 ? log((double)n) : -INFINITY;
-    }
-  };
-  for (int ri = wg; ri < cnt; ri += rg) {
-    const int u = rows ? rows[(size_t)h * CQ + ri] : ri;
-    if ((unsigned)u >= (unsigned)CQ) continue;  // uniform over the workgroup
+      for (int i = 0; i < NI; ++i) {
+        const int r = (w * NI + i) * RPI + l / CPR;
+        const int v = min(c0 + r, CK - 1);
+        const float* src = ch + (size_t)v * D + 4 * (pch ^ (r & (CPR - 1)));
+        p64_dma16(src, p64_lds_addr(&Ct[slot][0] + (w * NI + i) * 256));
+      }
+      if (tid < CT) {
+        const int v = c0 + tid;
+        const int n = v < CK ? nh[v] : 0;
+        Lt[slot][tid] = n > 0 ? log((double)n) : -INFINITY;
+      }
+    };
     const int q0 = min(max(off[u], 0), N), q1 = min(max(off[u + 1], q0), N);
     const int nu = q1 - q0;
-    const size_t wrow = ((size_t)h * CQ + u) * CK;
+    const size_t wrow = (size_t)rid * CK;
     if (nu <= 0) {
       for (int v = tid; v < CK; v += 256) {
         if (W64) W64[wrow + v] = 0.0;
@@ -128,16 +147,18 @@ __global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp,
       }
       continue;
     }
-    __syncthreads();  // the previous row's column sums have been read
-    for (int v = tid; v < 4 * CK; v += 256) wacc64[v] = 0.0;
-    const int nch = (nu + 63) / 64;
+    __syncthreads();  // the previous item's column sums have been read
+    for (int v = tid; v < CK; v += 256) wacc64[v] = 0.0;
+    const int nch = min(ce, (nu + 63) / 64) - cb;  // chunks of 64 queries from cb on
     const int total = nch * 2 * nt;
     float qa[KS];  // float holds bf16 and float32 inputs exactly
-    double m[4], z[4], mf[4], iz[4];
+    double m[4], z[4], mf[4];
     bool qv[4];
     issue(0, 0);
+    if (total > 1) issue(1 % nt, 1);
+    int prev_c0 = -1;  // the previous step's tile, when it was a probability-pass tile
     for (int it = 0; it < total; ++it) {
-      const int tile = it % nt, pass = (it / nt) & 1, r0 = q0 + 64 * (it / (2 * nt));
+      const int tile = it % nt, pass = (it / nt) & 1, r0 = q0 + 64 * (cb + it / (2 * nt));
       if (tile == 0 && pass == 0) {
         // A operand: query r0 + 16w + c16, dimensions 4s + g
         const int qi = r0 + 16 * w + c16;
@@ -165,17 +186,24 @@ __global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp,
             zz = (nm == -INFINITY) ? 0.0 : zz * exp(mm - nm) + oz * exp(om - nm);
             mm = nm;
           }
-          mf[r] = mm;
-          iz[r] = zz > 0.0 ? 1.0 / zz : 0.0;
+          // P = exp(S - (m + log z)); rows past the block get exp(-inf) = 0
+          mf[r] = qv[r] && zz > 0.0 ? mm + log(zz) : INFINITY;
         }
       }
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();  // tile landed everywhere; previous tile consumed (its slot is free)
-      if (it + 1 < total) issue((it + 1) % nt, (it + 1) & 1);
-      const int slot = it & 1;
+      // own DMAs of this tile done (the next one may stay in flight)
+      if (it + 1 < total) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI) : "memory");
+      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();  // tile landed everywhere; tile it-1 consumed (its slot is free)
+      if (it + 2 < total) issue((it + 2) % nt, (it + 2) % NS);
+      // the previous probability-pass tile's wavefront sums, in wavefront order
+      if (prev_c0 >= 0 && tid < CT && prev_c0 + tid < CK) {
+        const double (*sg)[CT] = stg[(it - 1) & 1];
+        wacc64[prev_c0 + tid] += ((sg[0][tid] + sg[1][tid]) + sg[2][tid]) + sg[3][tid];
+      }
+      const int slot = it % NS;
       const float* cs = &Ct[slot][0];
       const int c0 = tile * CT;
-#pragma unroll
+#pragma unroll 1
       for (int cb = 0; cb < CT / 16; ++cb) {
         const int row = 16 * cb + c16;  // B operand: centroid row, dimension 4s + g
         const float* crow = cs + row * D + g;
@@ -186,9 +214,11 @@ __global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp,
         f64x4_t acc = {0.0, 0.0, 0.0, 0.0}, acc1 = acc;  // two chains (even / odd k-steps)
 #pragma unroll
         for (int s = 0; s < KS; s += 2) {
-          acc = __builtin_amdgcn_mfma_f64_16x16x4f64((double)qa[s], (double)bf[s], acc, 0, 0, 0);
-          acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)qa[s + 1], (double)bf[s + 1], acc1,
-                                                      0, 0, 0);
+          // widened next to their MFMA (the float64 copies would need twice the registers)
+          float a0 = qa[s], a1 = qa[s + 1];
+          asm volatile("" : "+v"(a0), "+v"(a1));
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a0, (double)bf[s], acc, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a1, (double)bf[s + 1], acc1, 0, 0, 0);
         }
         acc += acc1;
         const double lg = Lt[slot][row];  // this lane's centroid (column c16)
@@ -208,23 +238,195 @@ __global__ __launch_bounds__(256) void k_pama64(const T* __restrict__ Qp,
           double cs4 = 0.0;
           if (lg != -INFINITY) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (qv[r]) cs4 += exp(acc[r] * isd + lg - mf[r]) * iz[r];
+            for (int r = 0; r < 4; ++r) cs4 += exp(fma(acc[r], isd, lg - mf[r]));
           }
           cs4 += __shfl_xor(cs4, 16, 64);
           cs4 += __shfl_xor(cs4, 32, 64);
-          const int v = c0 + row;
-          if (g == 0 && v < CK) wacc64[w * CK + v] += cs4;
+          if (g == 0) stg[it & 1][w][row] = cs4;
         }
       }
+      prev_c0 = pass == 1 ? c0 : -1;
     }
     __syncthreads();
-    const double inv_n = 1.0 / (double)nu;
-    for (int v = tid; v < CK; v += 256) {
-      const double wv = (((wacc64[v] + wacc64[CK + v]) + wacc64[2 * CK + v]) + wacc64[3 * CK + v]) * inv_n;
+    if (prev_c0 >= 0 && tid < CT && prev_c0 + tid < CK) {
+      const double (*sg)[CT] = stg[(total - 1) & 1];
+      wacc64[prev_c0 + tid] += ((sg[0][tid] + sg[1][tid]) + sg[2][tid]) + sg[3][tid];
+    }
+    __syncthreads();
+    if (slot != -1) {  // part of a split row: raw column sums, added up by k_p64_combine
+      double* dst = slot == -2 ? W64 + wrow : part + (size_t)slot * CK;
+      for (int v = tid; v < CK; v += 256) dst[v] = wacc64[v];
+    } else {
+      const double inv_n = 1.0 / (double)nu;
+      for (int v = tid; v < CK; v += 256) {
+        const double wv = wacc64[v] * inv_n;
+        if (!isfinite(wv)) raise_status(status, ST_NONFINITE);
+        if (W64) W64[wrow + v] = wv;
+        if (W32) W32[wrow + v] = (float)wv;
+      }
+    }
+  }
+}
+
+// 1024-thread exclusive scan of one int per thread; `tmp` needs 16 ints.
+__device__ int wg1024_exclusive(int x, int* tmp, int& total) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  int inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) tmp[wid] = inc;
+  __syncthreads();
+  int pre = 0;
+  total = 0;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int t = tmp[v];
+    if (v < wid) pre += t;
+    total += t;
+  }
+  __syncthreads();  // tmp is free for the next scan
+  return pre + inc - x;
+}
+
+// Work list of the float64 pass over the listed rows.  Each row is cut into
+// items of m chunks of 64 queries, m the smallest power of two for which the
+// extra partial-sum rows (one per item after the first of a row) fit in
+// `cap`; a row of one item is finished by its item.  items[k] = {h CQ + u,
+// first chunk, end chunk, slot}: slot -1 finishes the row, -2 leaves the raw
+// column sums in the row's W64 slot, s >= 0 in part[s].  srows[j] = {h CQ +
+// u, first part slot, number of part slots, n_u} for every split row, in row
+// order.  cnt = {items, split rows, queue head, 0}.  One workgroup.
+__global__ __launch_bounds__(1024) void k_p64_plan(const int* __restrict__ q_offsets,
+                                                   const int* __restrict__ rows,
+                                                   const int* __restrict__ nrows, int H, int N,
+                                                   int CQ, int cap, int4* __restrict__ items,
+                                                   int4* __restrict__ srows, int* __restrict__ cnt) {
+  constexpr int NM = 16;    // candidate m = 1, 2, 4, ..., 2^15
+  constexpr int HG = 4096;  // heads per group (the listed rows are walked group by group)
+  __shared__ int tmp[16];
+  __shared__ long long red[16][NM];
+  __shared__ int hp[HG + 1];
+  __shared__ int m_s;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  // hp[k] = listed rows of heads h0 .. h0+k-1; returns the rows of the group
+  auto head_prefix = [&](int h0, int nh) {
+    int base = 0;
+    for (int k0 = 0; k0 < nh; k0 += 1024) {
+      const int k = k0 + tid;
+      const int n = k < nh ? min(max(nrows[h0 + k], 0), CQ) : 0;
+      int t;
+      const int x = wg1024_exclusive(n, tmp, t);
+      if (k < nh) hp[k] = base + x;
+      base += t;
+    }
+    if (tid == 0) hp[nh] = base;
+    __syncthreads();
+    return base;
+  };
+  // listed row j of the group: head h, block u (-1: invalid) and its length
+  auto row_at = [&](int h0, int nh, int j, int& h, int& u) {
+    int lo = 0, hi = nh - 1;  // the last head whose rows start at or before j
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (hp[mid] <= j) lo = mid;
+      else hi = mid - 1;
+    }
+    h = h0 + lo;
+    u = rows[(size_t)h * CQ + (j - hp[lo])];
+    if ((unsigned)u >= (unsigned)CQ) {
+      u = -1;
+      return 0;
+    }
+    const int* off = q_offsets + (size_t)h * (CQ + 1);
+    const int a = min(max(off[u], 0), N), b = min(max(off[u + 1], a), N);
+    return b - a;
+  };
+  long long e[NM];
+#pragma unroll
+  for (int j = 0; j < NM; ++j) e[j] = 0;
+  for (int h0 = 0; h0 < H; h0 += HG) {
+    const int nh = min(HG, H - h0);
+    const int U = head_prefix(h0, nh);
+    for (int j = tid; j < U; j += 1024) {
+      int h, u;
+      const int nch = (row_at(h0, nh, j, h, u) + 63) >> 6;
+#pragma unroll
+      for (int k = 0; k < NM; ++k) e[k] += nch > 0 ? ((nch - 1) >> k) : 0;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NM; ++j) {
+    long long x = e[j];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    if (lane == 0) red[wid][j] = x;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int m = 1 << 30;  // one item per row
+    for (int j = NM - 1; j >= 0; --j) {
+      long long t = 0;
+      for (int v = 0; v < 16; ++v) t += red[v][j];
+      if (t <= (long long)cap) m = 1 << j;
+    }
+    m_s = m;
+  }
+  __syncthreads();
+  const int m = m_s;
+  int ib = 0, sb = 0, rb = 0;  // items, part slots and split rows so far (uniform)
+  for (int h0 = 0; h0 < H; h0 += HG) {
+    const int nh = min(HG, H - h0);
+    const int U = head_prefix(h0, nh);
+    for (int j0 = 0; j0 < U; j0 += 1024) {
+      int h = 0, u = -1, nu = 0;
+      if (j0 + tid < U) nu = row_at(h0, nh, j0 + tid, h, u);
+      const int nch = (nu + 63) >> 6;
+      const int ns = u < 0 ? 0 : (nch > 0 ? (nch - 1) / m + 1 : 1);
+      int t1, t2, t3;
+      const int x1 = wg1024_exclusive(ns, tmp, t1);
+      const int x2 = wg1024_exclusive(ns > 1 ? ns - 1 : 0, tmp, t2);
+      const int x3 = wg1024_exclusive(ns > 1 ? 1 : 0, tmp, t3);
+      const int rid = h * CQ + u;
+      for (int k = 0; k < ns; ++k) {
+        const int sl = ns == 1 ? -1 : (k == 0 ? -2 : sb + x2 + k - 1);
+        items[ib + x1 + k] = make_int4(rid, k * m, k + 1 < ns ? (k + 1) * m : nch, sl);
+      }
+      if (ns > 1) srows[rb + x3] = make_int4(rid, sb + x2, ns - 1, nu);
+      ib += t1;
+      sb += t2;
+      rb += t3;
+    }
+  }
+  if (tid == 0) {
+    cnt[0] = ib;
+    cnt[1] = rb;
+    cnt[2] = 0;
+    cnt[3] = 0;
+  }
+}
+
+// Rows split over several items: W^ = (raw sums in the W64 slot + the part
+// slots, in item order) / n_u.  Grid-stride over the split rows.
+__global__ __launch_bounds__(256) void k_p64_combine(const int4* __restrict__ srows,
+                                                     const int* __restrict__ cnt,
+                                                     const double* __restrict__ part, int CK,
+                                                     double* __restrict__ W64,
+                                                     float* __restrict__ W32, int* status) {
+  const int nr = cnt[1];
+  for (int r = blockIdx.x; r < nr; r += gridDim.x) {
+    const int4 sr = srows[r];
+    const double inv_n = 1.0 / (double)sr.w;
+    double* wr = W64 + (size_t)sr.x * CK;
+    for (int v = threadIdx.x; v < CK; v += 256) {
+      double a = wr[v];
+      for (int j = 0; j < sr.z; ++j) a += part[(size_t)(sr.y + j) * CK + v];
+      const double wv = a * inv_n;
       if (!isfinite(wv)) raise_status(status, ST_NONFINITE);
-      if (W64) W64[wrow + v] = wv;
-      if (W32) W32[wrow + v] = (float)wv;
+      wr[v] = wv;
+      if (W32) W32[(size_t)sr.x * CK + v] = (float)wv;
     }
   }
 }
@@ -1128,7 +1330,7 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   const int kcount = mode == PARK_SELECT_TOPK ? topk_count(CK, param) : 0;
   if (dtype != PARK_BF16) {  // float32 queries: float64 PAMA and selection of every row
     PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, nullptr, nullptr,
-                           rb.W64, W_out, status, st));
+                           nullptr, rb.W64, W_out, status, st));
     PARK_LAUNCH("select", k_select64, dim3(CQ, H), dim3(256), 0, st, (const double*)rb.W64,
                 q_offsets, k_sizes, CQ, CK, P, mode, param, kcount, (const int*)nullptr,
                 (const int*)nullptr, kv_count, kv_index);
@@ -1159,11 +1361,18 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   PARK_LAUNCH("select_fast", k_select_fast, dim3(CQ, H), dim3(256), 0, st, (const float*)W32,
               (const float*)rb.delta, q_offsets, k_sizes, CQ, CK, P, mode, param, kcount,
               kv_count, kv_index, rb.rows, rb.nrows);
-  // rows the float bound could not certify: float64 PAMA and selection
+  // rows the float bound could not certify: float64 PAMA over chunks of 64
+  // queries (work list, queue), split rows added up, then selection
   int rg = (1024 + H - 1) / H;
   rg = rg < 1 ? 1 : (rg > CQ ? CQ : rg);
-  PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, rb.rows, rb.nrows,
-                         rb.W64, W32, status, st, rg));
+  PARK_LAUNCH("pama_plan64", k_p64_plan, dim3(1), dim3(1024), 0, st, q_offsets,
+              (const int*)rb.rows, (const int*)rb.nrows, H, N, CQ, p64_cap(H, CQ), rb.items,
+              rb.srows, rb.pcnt);
+  PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, rb.items, rb.pcnt,
+                         rb.part, rb.W64, W32, status, st));
+  PARK_LAUNCH("pama_combine64", k_p64_combine, dim3(256), dim3(256), 0, st,
+              (const int4*)rb.srows, (const int*)rb.pcnt, (const double*)rb.part, CK, rb.W64, W32,
+              status);
   PARK_LAUNCH("select_refine", k_select64, dim3(rg, H), dim3(256), 0, st, (const double*)rb.W64,
               q_offsets, k_sizes, CQ, CK, P, mode, param, kcount, (const int*)rb.rows,
               (const int*)rb.nrows, kv_count, kv_index);
@@ -1172,14 +1381,15 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
 
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
-                          const int* rows, const int* nrows, double* W64, float* W32, int* status,
-                          hipStream_t st, int grid_x) {
-  const int rg = rows ? grid_x : CQ;  // workgroups per head
-  const unsigned nwg = 8u * (((unsigned)rg * (unsigned)H + 7u) / 8u);
-  const size_t lds = (size_t)4 * CK * sizeof(double);
-  const char* nm = rows ? "pama_refine64" : "pama64";
+                          const int4* items, int* cnt, double* part, double* W64, float* W32,
+                          int* status, hipStream_t st) {
+  // with an item list: a queue drained by two workgroups per CU; without:
+  // one workgroup per row, the rows of a head on one XCD
+  const unsigned nwg = items ? 512u : 8u * (((unsigned)H * (unsigned)CQ + 7u) / 8u);
+  const size_t lds = (size_t)CK * sizeof(double);
+  const char* nm = items ? "pama_refine64" : "pama64";
   // reserved once for the largest CK (2048), outside any stream capture that may follow
-  static const int lds_max = (int)(4 * MAXC * sizeof(double));
+  static const int lds_max = (int)(MAXC * sizeof(double));
   static const hipError_t a1 = hipFuncSetAttribute(
       (const void*)k_pama64<bf16_t, 128>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
   static const hipError_t a2 = hipFuncSetAttribute(
@@ -1193,17 +1403,17 @@ park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen
   if (D == 128) {
     if (dtype == PARK_BF16)
       PARK_LAUNCH(nm, (k_pama64<bf16_t, 128>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
-                  q_offsets, cen, k_sizes, H, N, CQ, CK, rg, rows, nrows, W64, W32, status);
+                  q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
     else
       PARK_LAUNCH(nm, (k_pama64<float, 128>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
-                  q_offsets, cen, k_sizes, H, N, CQ, CK, rg, rows, nrows, W64, W32, status);
+                  q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
   } else {
     if (dtype == PARK_BF16)
       PARK_LAUNCH(nm, (k_pama64<bf16_t, 64>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
-                  q_offsets, cen, k_sizes, H, N, CQ, CK, rg, rows, nrows, W64, W32, status);
+                  q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
     else
       PARK_LAUNCH(nm, (k_pama64<float, 64>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
-                  q_offsets, cen, k_sizes, H, N, CQ, CK, rg, rows, nrows, W64, W32, status);
+                  q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
   }
   return PARK_OK;
 }

@@ -74,11 +74,17 @@ struct RetrieveBufs {
   float* cn;      // [H][CK]     |c_v|
   float* bmax;    // [H][ceil(CK/16)][2] per-block max |c_v|, |log n_v|
   int4* qplan;    // [H][ceil(CQ/4)] query blocks of each fast-retrieval workgroup
+  double* part;   // [p64_cap][CK] raw column sums of the later items of split rows
+  int4* items;    // [H CQ + p64_cap] float64 work list
+  int4* srows;    // [p64_cap] split rows
+  int* pcnt;      // [4] items, split rows, queue head
 };
+// partial-sum rows available to the float64 pass (a quarter of the rows)
+inline int p64_cap(int H, int CQ) { return (H * CQ + 3) / 4; }
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
-                          const int* rows, const int* nrows, double* W64, float* W32, int* status,
-                          hipStream_t st, int grid_x = 0);
+                          const int4* items, int* cnt, double* part, double* W64, float* W32,
+                          int* status, hipStream_t st);
 park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* cen,
                             const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                             int mode, double param, const RetrieveBufs& rb, float* W_out,

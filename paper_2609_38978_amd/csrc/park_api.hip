@@ -170,6 +170,10 @@ static RetrieveBufs carve_retrieve(Carver& cv, int H, int D, int CQ, int CK) {
   r.cn = cv.take<float>((size_t)H * CK);
   r.bmax = cv.take<float>((size_t)2 * H * ((CK + 15) / 16));
   r.qplan = cv.take<int4>((size_t)H * ((CQ + 3) / 4));
+  r.part = cv.take<double>((size_t)p64_cap(H, CQ) * CK);
+  r.items = cv.take<int4>((size_t)H * CQ + p64_cap(H, CQ));
+  r.srows = cv.take<int4>((size_t)p64_cap(H, CQ) + 1);
+  r.pcnt = cv.take<int>(4);
   return r;
 }
 

@@ -368,3 +368,36 @@ def test_retrieval_exact_ties_take_the_float64_path(mode, param):
     kvc, kvi = kvc.cpu().numpy()[0], kvi.cpu().numpy()[0]
     nd, nb = PT.compare_masks(Wo, n, np.diff(rq["offsets"]), mode, param, kvc, kvi)
     assert nb == 0 and nd == 0
+
+
+@pytest.mark.parametrize("sizes", [
+    [700, 60, 240, 1, 299, 600, 50, 50],  # work items of 8 chunks: two rows split in two
+    [150] + [10] * 63,                    # one item per chunk: a row of three items
+    [0, 64, 65, 3000, 128],               # an empty block; 47 chunks cut into items of 16
+], ids=["m8", "m1", "m16"])
+def test_retrieval_float64_work_items(sizes):
+    # every key block has an exact twin and k is odd, so the k-th and (k+1)-th
+    # scores of every row tie: each query block goes through the float64 pass,
+    # whose work items (whole chunks of 64 queries) are summed in item order
+    rng = np.random.default_rng(11)
+    d, CK = 128, 32
+    offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N, CQ = int(offs[-1]), len(sizes)
+    Qp = torch.from_numpy(rng.standard_normal((N, d)).astype(np.float32)).bfloat16().float().numpy()
+    c = (0.3 * rng.standard_normal((CK, d))).astype(np.float32)
+    n = rng.integers(1, 100, CK)
+    c[1::2] = c[0::2]
+    n[1::2] = n[0::2]
+    Wo = O.pama(Qp, offs, c, n)
+    param = 11 / 32  # k = 11
+    kvc, kvi, W = P.park_retrieve_blocks(
+        PT.to_dev(Qp[None], "bf16"), torch.from_numpy(offs[None].astype(np.int32)).cuda(),
+        torch.from_numpy(c[None]).cuda(), torch.from_numpy(n[None].astype(np.int32)).cuda(),
+        CQ, CK, P.PARK_SELECT_TOPK, param, want_W=True)
+    W = W.cpu().numpy()[0]
+    # float64 rows rounded once to float32: within one float32 ulp of the oracle
+    ref = Wo.astype(np.float32)
+    assert np.all(np.abs(W - ref) <= np.spacing(np.abs(ref))), np.abs(W - ref).max()
+    nd, nb = PT.compare_masks(Wo, n, np.diff(offs), "topk", param, kvc.cpu().numpy()[0],
+                              kvi.cpu().numpy()[0])
+    assert nb == 0 and nd == 0
