@@ -226,14 +226,17 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
 // For a bf16 point x the score s_v = b_v - 2 x.w_v is evaluated with w_v
 // split into NP bf16 parts, w = w1 + w2 (+ w3) + r, with |r| <= 2^-16 (1.01)
 // |w| for two parts and 2^-24 (1 + 2^-7)|w| for three.  All products are
-// bf16 x bf16, exact in float.  x.w1 is accumulated over the D dimensions in
-// one chain of v_mfma_f32_32x32x16_bf16, the smaller parts (terms 2^-8
-// smaller) in a second chain, and the two are added once.  With delta =
-// 2^-23 per addition inside an MFMA (any faithful rounding) and 2^-24 for
-// the VALU rounding, the forward error of t^ = x.w is at most
+// bf16 x bf16, exact in float.  With delta = 2^-23 per addition inside an
+// MFMA (any faithful rounding) and 2^-24 for a VALU rounding, the forward
+// error of t^ = x.w is at most
 //   et sum_a |x_a w_a|,  et = er 1.01 + (D+1) delta (1 + 2^-7)
 //                            + 2^-8 1.01 ((NP-1) D + 1) delta + 2^-24 1.01,
-// er the residual bound above.  Two parts take 2/3 of the MFMA work and
+// er the residual bound above.  This covers two orders of evaluation: x.w1
+// and the smaller parts (terms 2^-8 smaller) in two chains of
+// v_mfma_f32_32x32x16_bf16 added once, and (the fast path) the smaller parts'
+// chain continued by the D products of x.w1, whose partial sums are then at
+// most (1 + 2^-8 1.01)(1 + 2^-7) sum_a |x_a w_a|, i.e. D delta (1.012) in
+// place of (D+1) delta (1 + 2^-7) + 2^-24 1.01.  Two parts take 2/3 of the MFMA work and
 // double the bound; they pay off when the centroid count makes the pass
 // MFMA-bound (C >= 512), three parts otherwise.
 // and with sum_a |x_a w_a| <= |x| |w_v|, the float roundings of b_v and of
@@ -374,7 +377,9 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
     }
   }
   float kx[TB], best[TB], L[TB];
-  int bidx[TB];
+  // id of the best centroid minus (first centroid of the current tile + 4 hf),
+  // so that the per-score select takes a constant
+  int brel[TB], bidx[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) {
     const float xs = xsq[tb] + __shfl_xor(xsq[tb], 32, 64);
@@ -383,7 +388,7 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
     kx[tb] = xs >= 7.88860905e-31f ? KXC * sqrtf(xs) : INFINITY;
     best[tb] = INFINITY;
     L[tb] = INFINITY;
-    bidx[tb] = -1;
+    brel[tb] = -(1 << 30);  // no centroid yet
   }
   // all global loads done before the tile loop (its waits are explicit)
 #pragma unroll
@@ -409,28 +414,33 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
     const bf16_t* W1 = &Wt[slot][0];
     const bf16_t* W2 = W1 + CT * D;
     const bf16_t* W3 = W2 + CT * D;  // third part (NP == 3)
-    f32x16_t ahi[TB], arest[TB];
+    // the small parts first, then the leading part on top of them (one
+    // accumulator, no separate addition of the two sums)
+    f32x16_t acc[TB];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        ahi[tb][q] = 0.0f;
-        arest[tb][q] = 0.0f;
-      }
+      for (int q = 0; q < 16; ++q) acc[tb][q] = 0.0f;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int co = rowo + 8 * ((2 * s + hf) ^ swk);
-      const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
       const bf16x8_t a2 = *(const bf16x8_t*)(W2 + co);
       bf16x8_t a3;
       if constexpr (NP == 3) a3 = *(const bf16x8_t*)(W3 + co);
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
-        ahi[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xf[tb][s], ahi[tb], 0, 0, 0);
-        arest[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, xf[tb][s], arest[tb], 0, 0, 0);
+        acc[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, xf[tb][s], acc[tb], 0, 0, 0);
         if constexpr (NP == 3)
-          arest[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, xf[tb][s], arest[tb], 0, 0, 0);
+          acc[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, xf[tb][s], acc[tb], 0, 0, 0);
       }
+    }
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int co = rowo + 8 * ((2 * s + hf) ^ swk);
+      const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb)
+        acc[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xf[tb][s], acc[tb], 0, 0, 0);
     }
     float bv[16];
 #pragma unroll
@@ -441,18 +451,22 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
       bv[4 * bq + 2] = b4.z;
       bv[4 * bq + 3] = b4.w;
     }
-    const int vbase = t * CT + 4 * hf;
 #pragma unroll
-    for (int tb = 0; tb < TB; ++tb)
+    for (int tb = 0; tb < TB; ++tb) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        const float sc = fmaf(-2.0f, ahi[tb][q] + arest[tb][q], bv[q]);
+        const float sc = fmaf(-2.0f, acc[tb][q], bv[q]);
         const bool nb = sc < best[tb];
         L[tb] = __builtin_amdgcn_fmed3f(best[tb], L[tb], sc);
         best[tb] = fminf(best[tb], sc);
-        bidx[tb] = nb ? vbase + 8 * (q >> 2) + (q & 3) : bidx[tb];
+        brel[tb] = nb ? 8 * (q >> 2) + (q & 3) : brel[tb];
       }
+      brel[tb] -= CT;  // relative to the next tile
+    }
   }
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb)
+    bidx[tb] = brel[tb] >= -(1 << 29) ? brel[tb] + ntiles * CT + 4 * hf : -1;
   const float nmax = mx_s[0], ebmax = mx_s[1];
   bool fl[TB];
   float ubv[TB];
