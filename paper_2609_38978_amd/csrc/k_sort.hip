@@ -1,17 +1,19 @@
 // Stable counting sort of cluster labels (pi = argsort(z), Alg. 3) and the
-// row gathers X' = X[pi].  Three passes: per-tile histograms, one exclusive
-// scan per head in (cluster, tile) order, and a stable scatter in which each
-// tile walks its tokens in order one wavefront (64 tokens) at a time.  All
-// integer work; the result is unique, so it is bit-exact and deterministic.
+// row gathers X' = X[pi].  Two passes: per-tile histograms, then a stable
+// scatter in which each tile's workgroup first derives its own bases from the
+// histogram table (cluster totals scanned over clusters, plus the counts of
+// the earlier tiles) and then walks its tokens in order one wavefront (64
+// tokens) at a time.  All integer work; the result is unique, so it is
+// bit-exact and deterministic.
 #include "common.h"
 #include "kernels.h"
 
 namespace park {
 
-// Tokens per scatter tile: the smallest power of two >= 256 for which the
-// per-head histogram table (C x tiles) stays below 64K entries, so that the
-// single-workgroup scan stays short while the scatter (one wavefront per
-// tile, serial within the tile) gets as many wavefronts as possible.
+// Tokens per sort tile: the smallest power of two >= 256 for which the
+// per-head histogram table (C x tiles) stays below 64K entries, so that each
+// scatter workgroup's pass over the table stays short while the scatter gets
+// as many workgroups as possible.
 int sort_tile(int H, int N, int C) {
   (void)H;
   int t = 256;
@@ -24,7 +26,7 @@ int sort_tiles(int H, int N, int C) {
   return (N + t - 1) / t;
 }
 
-// thist[h][v][tile] = #{ i in tile : z_i = v }
+// thist[h][tile][v] = #{ i in tile : z_i = v }
 __global__ __launch_bounds__(256) void k_sort_hist(const int* __restrict__ labels, int N, int C,
                                                    int tile_sz, int* __restrict__ thist) {
   extern __shared__ int hist[];
@@ -46,82 +48,74 @@ __global__ __launch_bounds__(256) void k_sort_hist(const int* __restrict__ label
       if ((unsigned)v[k] < (unsigned)C) atomicAdd(&hist[v[k]], 1);
   }
   __syncthreads();
-  int* out = thist + (size_t)h * C * nt;
-  for (int v = threadIdx.x; v < C; v += 256) out[(size_t)v * nt + tile] = hist[v];
+  int* out = thist + ((size_t)h * nt + tile) * C;
+  for (int v = threadIdx.x; v < C; v += 256) out[v] = hist[v];
 }
 
-// In-place exclusive scan of thist[h] (C*nt entries, cluster-major) and the
-// cluster offsets o[v] = first position of cluster v, o[C] = N.  A pass covers
-// SP sub-passes of 4096 entries (4 consecutive per thread, coalesced); all its
-// loads are issued together and the SP block scans share one barrier.
-__global__ __launch_bounds__(1024) void k_sort_scan(int* __restrict__ thist, int C, int nt, int N,
-                                                    int* __restrict__ offsets) {
-  constexpr int SP = 4;
-  __shared__ int wsum[2][SP][16];
-  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  int* a = thist + (size_t)h * C * nt;
-  int* off = offsets + (size_t)h * (C + 1);
-  const int total = C * nt;
-  int carry = 0;
-  for (int pass = 0, base = 0; base < total; ++pass, base += SP * 4096) {
-    int x[SP][4], sv[SP], inc[SP];
+// Stable scatter.  Bases first: thread v sums cluster v's counts over the
+// tiles before this one and over all tiles (table rows read coalesced, eight
+// in flight), the totals are scanned over clusters, and base_v = start_v +
+// earlier counts; tile 0 also writes the cluster offsets (o[C] = N).  Then
+// wavefront 0 walks the tile's tokens in increasing order; equal labels
+// inside the wavefront are matched with one ballot per label bit.
+__global__ __launch_bounds__(256) void k_sort_scatter(const int* __restrict__ labels, int N, int C,
+                                                      int nbits, int tile_sz,
+                                                      const int* __restrict__ thist,
+                                                      int* __restrict__ perm,
+                                                      int* __restrict__ offsets) {
+  extern __shared__ int run[];  // [C] bases, then [C] totals
+  __shared__ int wsum[4];
+  const int h = blockIdx.y, tile = blockIdx.x, nt = gridDim.x, tid = threadIdx.x;
+  const int lane = tid & 63, wid = tid >> 6;
+  const int* b = thist + (size_t)h * nt * C;
+  int* tot = run + C;
+  for (int v = tid; v < C; v += 256) {
+    int before = 0, all = 0;
+    for (int t0 = 0; t0 < nt; t0 += 8) {
+      int c[8];
 #pragma unroll
-    for (int j = 0; j < SP; ++j)
+      for (int k = 0; k < 8; ++k) c[k] = t0 + k < nt ? b[(size_t)(t0 + k) * C + v] : 0;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int e = base + 4096 * j + 4 * tid + k;
-        x[j][k] = e < total ? a[e] : 0;
+      for (int k = 0; k < 8; ++k) {
+        all += c[k];
+        before += t0 + k < tile ? c[k] : 0;
       }
-#pragma unroll
-    for (int j = 0; j < SP; ++j) {
-      sv[j] = (x[j][0] + x[j][1]) + (x[j][2] + x[j][3]);
-      inc[j] = sv[j];
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(inc[j], o, 64);
-        if (lane >= o) inc[j] += y;
-      }
-      if (lane == 63) wsum[pass & 1][j][wid] = inc[j];
     }
-    __syncthreads();
-    int run0 = carry;
-#pragma unroll
-    for (int j = 0; j < SP; ++j) {
-      int wpre = 0, blk = 0;
-#pragma unroll
-      for (int w = 0; w < 16; ++w) {
-        const int ws = wsum[pass & 1][j][w];
-        wpre += w < wid ? ws : 0;
-        blk += ws;
-      }
-      int run = run0 + wpre + inc[j] - sv[j];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int e = base + 4096 * j + 4 * tid + k;
-        if (e < total) {
-          a[e] = run;
-          if (e % nt == 0) off[e / nt] = run;
-        }
-        run += x[j][k];
-      }
-      run0 += blk;
-    }
-    carry = run0;  // wsum[pass & 1] is rewritten two passes later, after another barrier
+    run[v] = before;
+    tot[v] = all;
   }
-  if (tid == 0) off[C] = N;
-}
-
-// Stable scatter: one wavefront per tile, tokens in increasing order.
-// Equal labels inside a wave are matched with one ballot per label bit.
-__global__ __launch_bounds__(64) void k_sort_scatter(const int* __restrict__ labels, int N, int C,
-                                                     int nbits, int tile_sz,
-                                                     const int* __restrict__ tbase,
-                                                     int* __restrict__ perm) {
-  extern __shared__ int run[];
-  const int h = blockIdx.y, tile = blockIdx.x, nt = gridDim.x, lane = threadIdx.x;
-  const int* b = tbase + (size_t)h * C * nt;
-  for (int v = lane; v < C; v += 64) run[v] = b[(size_t)v * nt + tile];
   __syncthreads();
+  // exclusive scan of tot over the clusters: thread tid owns clusters
+  // [tid * per, (tid + 1) * per)
+  const int per = (C + 255) / 256;
+  int s = 0;
+  for (int k = 0; k < per; ++k) {
+    const int v = tid * per + k;
+    s += v < C ? tot[v] : 0;
+  }
+  int inc = s;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) wsum[wid] = inc;
+  __syncthreads();
+  int pre = inc - s;
+  for (int q = 0; q < wid; ++q) pre += wsum[q];
+  int* off = offsets + (size_t)h * (C + 1);
+  for (int k = 0; k < per; ++k) {
+    const int v = tid * per + k;
+    if (v < C) {
+      const int start = pre;
+      pre += tot[v];
+      run[v] += start;
+      if (tile == 0) off[v] = start;
+    }
+  }
+  if (tile == 0 && tid == 0) off[C] = N;
+  __syncthreads();
+  if (wid != 0) return;
   const int i0 = tile * tile_sz, i1 = min(N, i0 + tile_sz);
   const int* z = labels + (size_t)h * N;
   int* p = perm + (size_t)h * N;
@@ -151,9 +145,11 @@ __global__ __launch_bounds__(64) void k_sort_scatter(const int* __restrict__ lab
       }
       const int rank = __popcll(m & lt);
       if (ok) p[run[v] + rank] = i;
-      __syncthreads();
+      // one wavefront, whose LDS accesses complete in order; the fences keep
+      // the compiler from moving the base reads and updates across each other
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       if (ok && (m & gt) == 0) run[v] += rank + 1;
-      __syncthreads();
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
   }
 }
@@ -162,13 +158,12 @@ park_status launch_count_sort(const int* labels, int H, int N, int C, int* thist
                               int* offsets, hipStream_t st) {
   const int tsz = sort_tile(H, N, C);
   const int nt = (N + tsz - 1) / tsz;
-  const size_t lds = (size_t)C * sizeof(int);
   int nbits = 1;
   while ((1 << nbits) < C) ++nbits;
-  PARK_LAUNCH("sort_hist", k_sort_hist, dim3(nt, H), dim3(256), lds, st, labels, N, C, tsz, thist);
-  PARK_LAUNCH("sort_scan", k_sort_scan, dim3(H), dim3(1024), 0, st, thist, C, nt, N, offsets);
-  PARK_LAUNCH("sort_scatter", k_sort_scatter, dim3(nt, H), dim3(64), lds, st, labels, N, C, nbits,
-              tsz, (const int*)thist, perm);
+  PARK_LAUNCH("sort_hist", k_sort_hist, dim3(nt, H), dim3(256), (size_t)C * sizeof(int), st, labels,
+              N, C, tsz, thist);
+  PARK_LAUNCH("sort_scatter", k_sort_scatter, dim3(nt, H), dim3(256), (size_t)2 * C * sizeof(int),
+              st, labels, N, C, nbits, tsz, (const int*)thist, perm, offsets);
   return PARK_OK;
 }
 
