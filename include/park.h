@@ -205,7 +205,13 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
  * caller-allocated buffers that receive (RECOMPUTE) or supply (REUSE_*) the
  * clustering and mask.  With PARK_REUSE_CLUSTERS the permutations and offsets
  * of `state` are reused and gathers, centroids, retrieval and attention run
- * on the new tensors; PARK_REUSE_CLUSTERS_AND_MASK also reuses the mask. */
+ * on the new tensors; PARK_REUSE_CLUSTERS_AND_MASK also reuses the mask.
+ * With RECOMPUTE the query side's clustering runs on a side stream of the
+ * device (created by the library, default priority) that forks from `stream`
+ * and joins back into it, beside the key side's on `stream`: work queued on
+ * `stream` before and after the call stays ordered with the whole layer, and
+ * a capture of `stream` records the fork and the join.  Calls on one device
+ * share that side stream. */
 park_status park_forward(const void* Q, const void* K, const void* V, const park_dims* dims,
                          const park_params* params, int32_t reuse, const park_state* state,
                          void* O, void* ws, size_t ws_bytes, void* stream);

@@ -198,7 +198,8 @@ static size_t ws_bytes_for(int H, int N, int D, int CQ, int CK) {
   const size_t base = a.off;
   Carver c1(nullptr);
   c1.off = base;
-  carve_cluster(c1, H, N, D, std::max(CQ, CK));
+  carve_cluster(c1, H, N, D, CQ);  // query side
+  carve_cluster(c1, H, N, D, CK);  // key side (the two sides can run at the same time)
   Carver c2(nullptr);
   c2.off = base;
   carve_retrieve(c2, H, D, CQ, CK);
@@ -213,15 +214,68 @@ static park_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   return PARK_OK;
 }
 
+// ------------------------------------------------------------ side stream
+// The query side's clustering runs on a second stream of the device, beside
+// the key side's (metric and k-means) on the caller's stream: the two share
+// nothing but the status word, which kernels only OR into.  The stream
+// (default priority) and its fork/join events are created on the first call
+// that is not being captured; until then the sides run one after the other.
+// Recording an event and making the other stream wait on it happen under one
+// lock, so concurrent calls on one device cannot swap each other's events.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+static std::mutex g_side_mu;
+static SideStream g_side[64];
+
+static SideStream* side_stream(hipStream_t st) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lk(g_side_mu);
+  SideStream& a = g_side[dev];
+  if (!a.s) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
+      return nullptr;
+    hipStream_t s2 = nullptr;
+    hipEvent_t e1 = nullptr, e2 = nullptr;
+    if (hipStreamCreateWithFlags(&s2, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e1, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&e2, hipEventDisableTiming) != hipSuccess) {
+      if (e1) hipEventDestroy(e1);
+      hipStreamDestroy(s2);
+      return nullptr;
+    }
+    a.s = s2;
+    a.fork = e1;
+    a.join = e2;
+  }
+  return &a;
+}
+
+// `to` waits for the work `from` holds so far
+static park_status stream_after(SideStream* a, hipEvent_t ev, hipStream_t from, hipStream_t to) {
+  std::lock_guard<std::mutex> lk(g_side_mu);
+  hipError_t e = hipEventRecord(ev, from);
+  if (e == hipSuccess) e = hipStreamWaitEvent(to, ev, 0);
+  if (e != hipSuccess) return fail(PARK_ERR_HIP, "side stream: %s", hipGetErrorString(e));
+  (void)a;
+  return PARK_OK;
+}
+
 // ------------------------------------------------------------ stage bodies
+// `region` (optional) is the cluster workspace to use; by default the first
+// region after the status word.
 static park_status cluster_body(const void* X, const void* Qm, const park_dims& dm, int C, int T,
                                 uint64_t seed, int side, int metric, double alpha, double eps,
                                 double s_min, int* labels, int* perm, int* offsets, double* R_out,
-                                float* Xt_out, void* ws, hipStream_t st) {
+                                float* Xt_out, void* ws, hipStream_t st,
+                                const ClusterWs* region = nullptr) {
   const int H = dm.H, N = dm.N, D = dm.d;
   Carver cv(ws);
   int* status = cv.take<int>(64);
-  ClusterWs cw = carve_cluster(cv, H, N, D, C);
+  ClusterWs cw = region ? *region : carve_cluster(cv, H, N, D, C);
   const double* Gbar = nullptr;
   if (metric == PARK_METRIC_QRKC) {
     double* R = R_out ? R_out : cw.R;
@@ -450,10 +504,27 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
   Carver cv(ws);
   PARK_TRY(launch_clear_status(cv.take<int>(64), st));
   if (reuse == PARK_RECOMPUTE) {
-    PARK_TRY(cluster_body(Q, nullptr, *dims, p->CQ, p->T, p->seed, 0, PARK_METRIC_EUCLID, 0, 0, 1,
-                          nullptr, s->q_perm, s->q_offsets, nullptr, nullptr, ws, st));
-    PARK_TRY(cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha, p->eps,
-                          p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr, nullptr, ws, st));
+    // query side on the side stream, key side here, joined before the gathers
+    Carver rc(ws);
+    rc.take<int>(64);
+    const ClusterWs cq = carve_cluster(rc, H, N, D, p->CQ);
+    const ClusterWs ck = carve_cluster(rc, H, N, D, p->CK);
+    SideStream* side = side_stream(st);
+    hipStream_t sq = st;
+    if (side) {
+      PARK_TRY(stream_after(side, side->fork, st, side->s));
+      sq = side->s;
+    }
+    const park_status rq = cluster_body(Q, nullptr, *dims, p->CQ, p->T, p->seed, 0,
+                                        PARK_METRIC_EUCLID, 0, 0, 1, nullptr, s->q_perm,
+                                        s->q_offsets, nullptr, nullptr, ws, sq, &cq);
+    const park_status rk = rq != PARK_OK ? rq
+                                         : cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1,
+                                                        p->key_metric, p->alpha, p->eps, p->s_min,
+                                                        nullptr, s->k_perm, s->k_offsets, nullptr,
+                                                        nullptr, ws, st, &ck);
+    if (side) PARK_TRY(stream_after(side, side->join, sq, st));  // joined also after an error
+    PARK_TRY(rk);
   }
   PARK_TRY(launch_gather(Q, s->q_perm, H, N, D, dims->dtype, s->Qp, st));
   PARK_TRY(launch_gather(K, s->k_perm, H, N, D, dims->dtype, s->Kp, st));
