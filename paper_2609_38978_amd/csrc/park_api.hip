@@ -266,24 +266,28 @@ static park_status stream_after(SideStream* a, hipEvent_t ev, hipStream_t from, 
 
 // ------------------------------------------------------------ stage bodies
 // `region` (optional) is the cluster workspace to use; by default the first
-// region after the status word.
+// region after the status word.  `parts`: 1 the metric (and transform), 2 the
+// k-means (a metric already in the region), 3 both.
 static park_status cluster_body(const void* X, const void* Qm, const park_dims& dm, int C, int T,
                                 uint64_t seed, int side, int metric, double alpha, double eps,
                                 double s_min, int* labels, int* perm, int* offsets, double* R_out,
                                 float* Xt_out, void* ws, hipStream_t st,
-                                const ClusterWs* region = nullptr) {
+                                const ClusterWs* region = nullptr, int parts = 3) {
   const int H = dm.H, N = dm.N, D = dm.d;
   Carver cv(ws);
   int* status = cv.take<int>(64);
   ClusterWs cw = region ? *region : carve_cluster(cv, H, N, D, C);
   const double* Gbar = nullptr;
   if (metric == PARK_METRIC_QRKC) {
-    double* R = R_out ? R_out : cw.R;
-    PARK_TRY(launch_metric(Qm, H, N, D, dm.dtype, alpha, eps, s_min, cw.part, cw.G, cw.Gbar, R,
-                           status, st));
+    if (parts & 1) {
+      double* R = R_out ? R_out : cw.R;
+      PARK_TRY(launch_metric(Qm, H, N, D, dm.dtype, alpha, eps, s_min, cw.part, cw.G, cw.Gbar, R,
+                             status, st));
+      if (Xt_out) PARK_TRY(launch_transform(X, R, H, N, D, dm.dtype, Xt_out, st));
+    }
     Gbar = cw.Gbar;
-    if (Xt_out) PARK_TRY(launch_transform(X, R, H, N, D, dm.dtype, Xt_out, st));
   }
+  if (!(parts & 2)) return PARK_OK;
   KmeansBufs kb;
   kb.init = cw.init;
   kb.mu = cw.mu;
@@ -509,22 +513,26 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
     rc.take<int>(64);
     const ClusterWs cq = carve_cluster(rc, H, N, D, p->CQ);
     const ClusterWs ck = carve_cluster(rc, H, N, D, p->CK);
+    // queued in this order so that both streams get work early: the key
+    // side's metric, the whole query side, the key side's k-means
     SideStream* side = side_stream(st);
     hipStream_t sq = st;
     if (side) {
       PARK_TRY(stream_after(side, side->fork, st, side->s));
       sq = side->s;
     }
-    const park_status rq = cluster_body(Q, nullptr, *dims, p->CQ, p->T, p->seed, 0,
-                                        PARK_METRIC_EUCLID, 0, 0, 1, nullptr, s->q_perm,
-                                        s->q_offsets, nullptr, nullptr, ws, sq, &cq);
-    const park_status rk = rq != PARK_OK ? rq
-                                         : cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1,
-                                                        p->key_metric, p->alpha, p->eps, p->s_min,
-                                                        nullptr, s->k_perm, s->k_offsets, nullptr,
-                                                        nullptr, ws, st, &ck);
+    park_status r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha,
+                                 p->eps, p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr,
+                                 nullptr, ws, st, &ck, 1);
+    if (r == PARK_OK)
+      r = cluster_body(Q, nullptr, *dims, p->CQ, p->T, p->seed, 0, PARK_METRIC_EUCLID, 0, 0, 1,
+                       nullptr, s->q_perm, s->q_offsets, nullptr, nullptr, ws, sq, &cq);
+    if (r == PARK_OK)
+      r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha, p->eps,
+                       p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr, nullptr, ws, st, &ck,
+                       2);
     if (side) PARK_TRY(stream_after(side, side->join, sq, st));  // joined also after an error
-    PARK_TRY(rk);
+    PARK_TRY(r);
   }
   PARK_TRY(launch_gather(Q, s->q_perm, H, N, D, dims->dtype, s->Qp, st));
   PARK_TRY(launch_gather(K, s->k_perm, H, N, D, dims->dtype, s->Kp, st));
