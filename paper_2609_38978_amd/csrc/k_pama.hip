@@ -643,60 +643,91 @@ __device__ __forceinline__ void pm_wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// Block plan of the fast retrieval: per head, the query blocks sorted by
-// their number of 64-row chunks (descending, ties by id) and dealt in groups
-// of four, one block per wavefront, so the four blocks of a workgroup need
-// about the same number of rounds.  plan[h][g] = four block ids (-1: none).
-// One workgroup of 1024 threads per head, CQ <= 2048.
-__global__ __launch_bounds__(1024) void k_pama_plan(const int* __restrict__ q_offsets, int N, int CQ,
-                                                    int G4, int4* __restrict__ plan) {
-  __shared__ uint32_t key[MAXC];
-  const int h = blockIdx.x, tid = threadIdx.x;
+// Work list of the fast retrieval: per head, every query block in rounds of
+// 64 queries, one round per wavefront and four per workgroup, in block order.
+// items[h][k] = {block u, round r, part slot (-1 for round 0), rounds of u};
+// round 0 writes the block's row of W^, later rounds a row of `part`
+// (slot = pstart[u] + r - 1), added up in round order by k_pama_combine.
+// nitem[h] = number of items, pstart[h][u] = rows of `part` taken by the
+// blocks before u (every round after a block's first takes one).  The
+// per-row error bounds are cleared for the workgroups' atomic maxima.  One
+// workgroup of 1024 threads per head, CQ <= 2048.
+__global__ __launch_bounds__(1024) void k_pama_plan(const int* __restrict__ q_offsets, int N,
+                                                    int CQ, int icap, int4* __restrict__ items,
+                                                    int* __restrict__ nitem,
+                                                    int* __restrict__ pstart,
+                                                    float* __restrict__ delta) {
+  __shared__ int st[MAXC + 1];
+  __shared__ int ps[MAXC + 1];
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int* off = q_offsets + (size_t)h * (CQ + 1);
-  int SZ = 2;
-  while (SZ < CQ) SZ <<= 1;
-  for (int u = tid; u < SZ; u += 1024) {
-    uint32_t k = 0xffffffffu;
+  // two blocks per thread: rounds, then a workgroup scan
+  int c[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int u = 2 * tid + k;
+    c[k] = 0;
     if (u < CQ) {
       const int a = min(max(off[u], 0), N), b = min(max(off[u + 1], a), N);
-      const int nch = min((b - a + 63) >> 6, 65535);
-      k = ((uint32_t)(65535 - nch) << 16) | (uint32_t)u;
+      c[k] = (b - a + 63) >> 6;
+      delta[(size_t)h * CQ + u] = 0.0f;
     }
-    key[u] = k;
+  }
+  // exclusive scans of the rounds (items) and of the rounds after the first
+  // (part rows), packed in one 64-bit word (32 bits each)
+  const int e0 = c[0] > 1 ? c[0] - 1 : 0, e1 = c[1] > 1 ? c[1] - 1 : 0;
+  const long long sum = (long long)(c[0] + c[1]) | ((long long)(e0 + e1) << 32);
+  long long inc = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const long long y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  __shared__ long long tmp64[16];
+  if (lane == 63) tmp64[wid] = inc;
+  __syncthreads();
+  long long pre = inc - sum, tot = 0;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    pre += q < wid ? tmp64[q] : 0;
+    tot += tmp64[q];
+  }
+  const int pi = (int)(pre & 0xffffffffll), pp = (int)(pre >> 32);
+  if (2 * tid < CQ) {
+    st[2 * tid] = pi;
+    ps[2 * tid] = pp;
+  }
+  if (2 * tid + 1 < CQ) {
+    st[2 * tid + 1] = pi + c[0];
+    ps[2 * tid + 1] = pp + e0;
+  }
+  if (tid == 0) {
+    st[CQ] = (int)(tot & 0xffffffffll);
+    ps[CQ] = (int)(tot >> 32);
   }
   __syncthreads();
-  for (int len = 2; len <= SZ; len <<= 1)
-    for (int j = len >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < SZ; i += 1024) {
-        const int ixj = i ^ j;
-        if (ixj > i) {
-          const uint32_t x = key[i], y = key[ixj];
-          const bool up = (i & len) == 0;
-          if ((x > y) == up) {
-            key[i] = y;
-            key[ixj] = x;
-          }
-        }
-      }
-      __syncthreads();
+  const int tot_items = st[CQ];
+  for (int u = tid; u <= CQ; u += 1024) pstart[(size_t)h * (CQ + 1) + u] = ps[u];
+  if (tid == 0) nitem[h] = min(tot_items, icap);
+  const int T = min(tot_items, icap);
+  for (int k = tid; k < T; k += 1024) {
+    int lo = 0, hi = CQ - 1;  // the last block whose items start at or before k
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (st[mid] <= k) lo = mid;
+      else hi = mid - 1;
     }
-  for (int g = tid; g < G4; g += 1024) {
-    int u[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int p = 4 * g + k;
-      u[k] = p < CQ ? (int)(key[p] & 0xffffu) : -1;
-    }
-    plan[(size_t)h * G4 + g] = make_int4(u[0], u[1], u[2], u[3]);
+    const int r = k - st[lo], nr = st[lo + 1] - st[lo];
+    items[(size_t)h * icap + k] = make_int4(lo, r, r == 0 ? -1 : ps[lo] + r - 1, nr);
   }
 }
 
-// Fast retrieval.  A workgroup takes four query blocks of one head (one per
-// wavefront, from the plan) and streams the head's key-block centroids
-// through an NS-slot LDS ring (32 rows of the three bf16 parts per tile, LDS
-// DMA, rows swizzled in 16-byte chunks), twice per round of 64-row chunks:
-// pass 1 builds each query's normaliser, pass 2 sums the probabilities over
-// the block's queries.  Every tile serves 256 queries.
+// Fast retrieval.  A workgroup takes four items of one head (one round of 64
+// queries of a query block per wavefront, from the plan) and streams the
+// head's key-block centroids through an NS-slot LDS ring (32 rows of the
+// three bf16 parts per tile, LDS DMA, rows swizzled in 16-byte chunks),
+// twice: pass 1 builds each query's normaliser, pass 2 sums the
+// probabilities over the round's queries.  Every tile serves 256 queries.
 //
 // MFMA 32x32x16 on two 32-query groups per wavefront.  The query fragment
 // (query l%32, dims 16 s + 8 (l/32) ..) and the centroid fragment (centroid
@@ -714,7 +745,9 @@ __global__ __launch_bounds__(1024) void k_pama_plan(const int* __restrict__ q_of
 template <int D>
 __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__ Qp,
                                                       const int* __restrict__ q_offsets,
-                                                      const int4* __restrict__ plan, int G4,
+                                                      const int4* __restrict__ items,
+                                                      const int* __restrict__ nitem, int icap,
+                                                      float* __restrict__ part, int pcap,
                                                       const bf16_t* __restrict__ c3, size_t plane,
                                                       const float* __restrict__ lg, int CKpad,
                                                       const float* __restrict__ bmax, int nbm, int H,
@@ -730,24 +763,26 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
   __shared__ __attribute__((aligned(16))) bf16_t Ct[NS][3 * CT * D];  // [slot][part][row][D]
   __shared__ __attribute__((aligned(16))) float Lt[NS][CT];
   __shared__ __attribute__((aligned(16))) float cbuf[4][64];  // c_q of each wavefront's chunk
-  __shared__ int rnd[4];
   __shared__ float mx_s[2];
-  const int nitems = G4 * H, per = (nitems + 7) >> 3;
-  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
-  if (item >= nitems) return;
-  const int h = item / G4, grp4 = item - h * G4;
+  // workgroups of a head on one XCD (its L2 holds the head's centroids)
+  const int G = (icap + 3) / 4, nwgs = G * H, per = (nwgs + 7) >> 3;
+  const int wgi = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (wgi >= nwgs) return;
+  const int h = wgi / G, grp4 = wgi - h * G;
+  const int T = min(nitem[h], icap);
+  if (4 * grp4 >= T) return;
   const int tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int4 pl = plan[(size_t)h * G4 + grp4];
-  const int ub = w == 0 ? pl.x : w == 1 ? pl.y : w == 2 ? pl.z : pl.w;
-  const int u = (unsigned)ub < (unsigned)CQ ? ub : -1;
+  const int k = 4 * grp4 + w;
+  const int4 itm = k < T ? items[(size_t)h * icap + k] : make_int4(-1, 0, -1, 0);
+  const int u = (unsigned)itm.x < (unsigned)CQ ? itm.x : -1;
+  const int rb = itm.y, pslot = itm.z;
   const int* off = q_offsets + (size_t)h * (CQ + 1);
   const int q0 = u >= 0 ? min(max(off[u], 0), N) : 0;
   const int q1 = u >= 0 ? min(max(off[u + 1], q0), N) : 0;
   const int nu = q1 - q0;
-  const int nch = (nu + 63) >> 6;
   const size_t wrow = ((size_t)h * CQ + (u >= 0 ? u : 0)) * CK;
-  if (l == 0) rnd[w] = nch;
+  float* prow = (pslot >= 0 && pslot < pcap) ? part + ((size_t)h * pcap + pslot) * CK : nullptr;
   if (tid < 64) {
     float a = 0.0f, c = 0.0f;
     for (int i = tid; i < nbm; i += 64) {
@@ -764,12 +799,7 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
     }
   }
   __syncthreads();
-  const int nrounds = max(max(rnd[0], rnd[1]), max(rnd[2], rnd[3]));
   const float cmax = mx_s[0], lgmax = mx_s[1];
-  if (u >= 0 && nu == 0) {  // empty block: zero row, exact
-    for (int v = l; v < CK; v += 64) W32[wrow + v] = 0.0f;
-    if (l == 0) delta[(size_t)h * CQ + u] = 0.0f;
-  }
   const float isd = 1.0f / sqrtf((float)D), isdL = isd * L2E;
   const bf16_t* P1 = c3 + (size_t)h * CK * D;
   const float* lgh = lg + (size_t)h * CKpad;
@@ -791,7 +821,7 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
   const int crow = c32 * D, cswz = pm_swz<D>(c32);
 
   float dmax = 0.0f;  // this wavefront's relative error bound
-  const int total = nrounds * 2 * nt;
+  const int total = 2 * nt;
 #pragma unroll
   for (int p = 0; p < NS - 1; ++p)
     if (p < total) issue(p % nt, p);
@@ -851,9 +881,10 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
     }
   };
   bf16x8_t qf[2][KS];
-  for (int rr = 0; rr < nrounds; ++rr) {
-    // this round's chunk: queries q0 + 64 rr + 32 g + l%32
-    const bool on = 64 * rr < nu;
+  {
+    // this wavefront's round: queries q0 + 64 rb + 32 g + l%32
+    const int rr = rb;
+    const bool on = u >= 0 && 64 * rr < nu;
     float m[2], z[2];
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
@@ -965,14 +996,52 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
       const int v = tile * CT + c32;
       if (hf == 0 && v < CK) {
         const float add = ws / (float)nu;
-        W32[wrow + v] = rr == 0 ? add : W32[wrow + v] + add;
+        if (rr == 0) W32[wrow + v] = add;
+        else if (prow) prow[v] = add;
       }
     }
   }
   if (u >= 0 && nu > 0) {
+    // the row's bound: the largest over its rounds (non-negative floats
+    // order as their bit patterns), finished by k_pama_combine
     for (int o = 32; o > 0; o >>= 1) dmax = fmaxf(dmax, __shfl_xor(dmax, o, 64));
-    if (l == 0)
-      delta[(size_t)h * CQ + u] = (dmax + (17.0f + 2.0f * nch) * U24) * 1.01f;
+    if (l == 0) atomicMax((int*)&delta[(size_t)h * CQ + u], __float_as_int(dmax));
+  }
+}
+
+// Rows of the fast retrieval: W^ = round 0 + round 1 + ... in round order
+// (the additions a single pass over the rounds would make), empty blocks a
+// zero row; the bound becomes delta_u = (max over rounds + (17 + 2 rounds)
+// 2^-24) 1.01.  Grid-stride over the rows of all heads.
+__global__ __launch_bounds__(256) void k_pama_combine(const int* __restrict__ q_offsets,
+                                                      const int* __restrict__ pstart, int H,
+                                                      int N, int CQ, int CK,
+                                                      const float* __restrict__ part, int pcap,
+                                                      float* __restrict__ W32,
+                                                      float* __restrict__ delta) {
+  constexpr float U24 = 5.9604645e-08f;
+  for (int row = blockIdx.x; row < H * CQ; row += gridDim.x) {
+    const int h = row / CQ, u = row - h * CQ;
+    const int* off = q_offsets + (size_t)h * (CQ + 1);
+    const int a = min(max(off[u], 0), N), b = min(max(off[u + 1], a), N);
+    const int nch = (b - a + 63) >> 6;
+    float* wr = W32 + (size_t)row * CK;
+    if (nch == 0) {
+      for (int v = threadIdx.x; v < CK; v += 256) wr[v] = 0.0f;
+      if (threadIdx.x == 0) delta[row] = 0.0f;
+      continue;
+    }
+    if (threadIdx.x == 0) delta[row] = (delta[row] + (17.0f + 2.0f * nch) * U24) * 1.01f;
+    if (nch == 1) continue;
+    const int s0 = pstart[(size_t)h * (CQ + 1) + u];  // part row of round 1
+    for (int v = threadIdx.x; v < CK; v += 256) {
+      float acc = wr[v];
+      for (int r = 1; r < nch; ++r) {
+        const int sl = s0 + r - 1;
+        if (sl < pcap) acc = acc + part[((size_t)h * pcap + sl) * CK + v];
+      }
+      wr[v] = acc;
+    }
   }
 }
 
@@ -1340,23 +1409,29 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   const int nbm = (CK + 15) / 16;
   float* W32 = W_out ? W_out : rb.W32;
   const int CKpad = pama_ckpad(CK);
-  // four query blocks per workgroup (size-sorted plan); XCD remap: every item owns one
-  const int G4 = (CQ + 3) / 4;
-  const unsigned nwg = 8u * (((unsigned)G4 * (unsigned)H + 7u) / 8u);
-  PARK_LAUNCH("pama_plan", k_pama_plan, dim3(H), dim3(1024), 0, st, q_offsets, N, CQ, G4, rb.qplan);
+  // rounds of 64 queries, four per workgroup (work list per head)
+  const int icap = pama_icap(N, CQ), pcap = pama_pcap(N);
+  const unsigned nwg = 8u * ((((unsigned)icap + 3u) / 4u * (unsigned)H + 7u) / 8u);
+  float* part = (float*)rb.W64;  // free until the float64 rows are computed
+  PARK_LAUNCH("pama_plan", k_pama_plan, dim3(H), dim3(1024), 0, st, q_offsets, N, CQ, icap,
+              rb.qitems, rb.nitem, rb.qstart, rb.delta);
   if (D == 128) {
     PARK_LAUNCH("pama_cen_prep", k_cen_prep<128>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
                 rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
     PARK_LAUNCH("pama_fast", k_pama_fast<128>, dim3(nwg), dim3(256), 0, st, (const bf16_t*)Qp,
-                q_offsets, (const int4*)rb.qplan, G4, (const bf16_t*)rb.c3, plane,
+                q_offsets, (const int4*)rb.qitems, (const int*)rb.nitem, icap, part, pcap,
+                (const bf16_t*)rb.c3, plane,
                 (const float*)rb.lg, CKpad, (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
   } else {
     PARK_LAUNCH("pama_cen_prep", k_cen_prep<64>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
                 rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
     PARK_LAUNCH("pama_fast", k_pama_fast<64>, dim3(nwg), dim3(256), 0, st, (const bf16_t*)Qp,
-                q_offsets, (const int4*)rb.qplan, G4, (const bf16_t*)rb.c3, plane,
+                q_offsets, (const int4*)rb.qitems, (const int*)rb.nitem, icap, part, pcap,
+                (const bf16_t*)rb.c3, plane,
                 (const float*)rb.lg, CKpad, (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
   }
+  PARK_LAUNCH("pama_combine", k_pama_combine, dim3(1024), dim3(256), 0, st, q_offsets,
+              (const int*)rb.qstart, H, N, CQ, CK, (const float*)part, pcap, W32, rb.delta);
   PARK_LAUNCH("pama_reset", k_zero_counts, dim3((H + 63) / 64), dim3(64), 0, st, rb.nrows, H);
   PARK_LAUNCH("select_fast", k_select_fast, dim3(CQ, H), dim3(256), 0, st, (const float*)W32,
               (const float*)rb.delta, q_offsets, k_sizes, CQ, CK, P, mode, param, kcount,

@@ -158,9 +158,10 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   return c;
 }
 
-static RetrieveBufs carve_retrieve(Carver& cv, int H, int D, int CQ, int CK) {
+static RetrieveBufs carve_retrieve(Carver& cv, int H, int N, int D, int CQ, int CK) {
   RetrieveBufs r;
-  r.W64 = cv.take<double>((size_t)H * CQ * CK);
+  // float64 rows; before them, the fast pass's round partial sums (float)
+  r.W64 = cv.take<double>(std::max((size_t)H * CQ * CK, ((size_t)H * pama_pcap(N) * CK + 1) / 2));
   r.W32 = cv.take<float>((size_t)H * CQ * CK);
   r.delta = cv.take<float>((size_t)H * CQ);
   r.rows = cv.take<int>((size_t)H * CQ);
@@ -169,7 +170,9 @@ static RetrieveBufs carve_retrieve(Carver& cv, int H, int D, int CQ, int CK) {
   r.lg = cv.take<float>((size_t)H * pama_ckpad(CK));
   r.cn = cv.take<float>((size_t)H * CK);
   r.bmax = cv.take<float>((size_t)2 * H * ((CK + 15) / 16));
-  r.qplan = cv.take<int4>((size_t)H * ((CQ + 3) / 4));
+  r.qitems = cv.take<int4>((size_t)H * pama_icap(N, CQ));
+  r.nitem = cv.take<int>((size_t)H);
+  r.qstart = cv.take<int>((size_t)H * (CQ + 1));
   r.part = cv.take<double>((size_t)p64_cap(H, CQ) * CK);
   r.items = cv.take<int4>((size_t)H * CQ + p64_cap(H, CQ));
   r.srows = cv.take<int4>((size_t)p64_cap(H, CQ) + 1);
@@ -202,7 +205,7 @@ static size_t ws_bytes_for(int H, int N, int D, int CQ, int CK) {
   carve_cluster(c1, H, N, D, CK);  // key side (the two sides can run at the same time)
   Carver c2(nullptr);
   c2.off = base;
-  carve_retrieve(c2, H, D, CQ, CK);
+  carve_retrieve(c2, H, N, D, CQ, CK);
   return std::max(std::max(c1.off, c2.off), attn_ws_end(H, N, CQ)) + 256;
 }
 
@@ -315,7 +318,7 @@ static park_status retrieve_body(const void* Qp, const int* q_offsets, const flo
                                  int* kv_index, void* ws, hipStream_t st) {
   Carver cv(ws);
   int* status = cv.take<int>(64);
-  RetrieveBufs rb = carve_retrieve(cv, dm.H, dm.d, CQ, CK);
+  RetrieveBufs rb = carve_retrieve(cv, dm.H, dm.N, dm.d, CQ, CK);
   return launch_retrieve(Qp, q_offsets, cen, k_sizes, dm.H, dm.N, dm.d, dm.dtype, CQ, CK, mode,
                          param, rb, W_out, kv_count, kv_index, status, st);
 }
