@@ -108,40 +108,22 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ 
   G[(size_t)h * DD + e] = s * invN;
 }
 
-// Symmetrise, scale, stabilise and factorise; one workgroup per head.
-// The 256 threads form a 16 x 16 grid; thread (ti, tj) holds the entries
-// (ti + 16 r, tj + 16 c), r, c < D/16, of the matrix in registers for the
-// whole right-looking Cholesky.  Step k reads column k from a double-buffered
-// LDS vector, applies M[i][j] -= M[i][k] M[j][k] / M[k][k] to the trailing
-// block, and the owners of column k+1 publish it: one barrier per column.
-// Column j keeps its value from step j; L[i][j] = that / sqrt(M[j][j]).
+// Symmetrise, scale and stabilise (Eq. (11)):
+//   Gbar = (1 - alpha) (G + G^T) / 2 + (alpha s + eps s) I,
+//   s = max(tr G / d, s_min) (trace summed in index order);
+// one workgroup per head.  A non-finite entry raises ST_NOT_SPD.
 template <int D>
-__global__ __launch_bounds__(256) void k_metric_chol(const double* __restrict__ G, double alpha,
+__global__ __launch_bounds__(256) void k_metric_gbar(const double* __restrict__ G, double alpha,
                                                      double eps, double s_min,
-                                                     double* __restrict__ Gbar_out,
-                                                     double* __restrict__ R_out, int* status) {
-  static_assert(D % 16 == 0 && D <= 128, "16 x 16 thread grid");
-  constexpr int NB = D / 16;
-  __shared__ double col[2][D];
+                                                     double* __restrict__ Gbar_out, int* status) {
   __shared__ double pv[D];
   __shared__ double sc;
   __shared__ int bad;
   const int h = blockIdx.x, tid = threadIdx.x;
-  const int ti = tid >> 4, tj = tid & 15;
   const double* Gh = G + (size_t)h * D * D;
   if (tid == 0) bad = 0;
   if (tid < D) pv[tid] = Gh[tid * D + tid];
-  double a[NB][NB];
-  // symmetrise: (G + G^T) / 2
-#pragma unroll
-  for (int r = 0; r < NB; ++r)
-#pragma unroll
-    for (int c = 0; c < NB; ++c) {
-      const int i = ti + 16 * r, j = tj + 16 * c;
-      a[r][c] = (i == j) ? Gh[i * D + j] : (Gh[i * D + j] + Gh[j * D + i]) / 2.0;
-    }
   __syncthreads();
-  // s = max(tr G / d, s_min), summed in index order
   if (tid == 0) {
     double t = 0.0;
     for (int i = 0; i < D; ++i) t += pv[i];
@@ -152,18 +134,44 @@ __global__ __launch_bounds__(256) void k_metric_chol(const double* __restrict__ 
   const double as = alpha * s, es = eps * s;
   double* Gb = Gbar_out + (size_t)h * D * D;
   bool nf = false;
+  for (int e = tid; e < D * D; e += 256) {
+    const int i = e / D, j = e - i * D;
+    double v = (i == j) ? Gh[i * D + j] : (Gh[i * D + j] + Gh[j * D + i]) / 2.0;
+    v = (1.0 - alpha) * v;
+    if (i == j) v = (v + as) + es;
+    nf |= !isfinite(v);
+    Gb[e] = v;
+  }
+  if (nf) bad = 1;
+  __syncthreads();
+  if (tid == 0 && bad) raise_status(status, ST_NOT_SPD);
+}
+
+// Cholesky factor of Gbar = L L^T (R = L; x~ = R^T x); one workgroup per
+// head.  The 256 threads form a 16 x 16 grid; thread (ti, tj) holds the
+// entries (ti + 16 r, tj + 16 c), r, c < D/16, of the matrix in registers for
+// the whole right-looking Cholesky.  Step k reads column k from a
+// double-buffered LDS vector, applies M[i][j] -= M[i][k] M[j][k] / M[k][k] to
+// the trailing block, and the owners of column k+1 publish it: one barrier
+// per column.  Column j keeps its value from step j; L[i][j] = that /
+// sqrt(M[j][j]).  A pivot that is not positive raises ST_NOT_SPD.
+template <int D>
+__global__ __launch_bounds__(256) void k_metric_chol(const double* __restrict__ Gbar,
+                                                     double* __restrict__ R_out, int* status) {
+  static_assert(D % 16 == 0 && D <= 128, "16 x 16 thread grid");
+  constexpr int NB = D / 16;
+  __shared__ double col[2][D];
+  __shared__ double pv[D];
+  __shared__ int bad;
+  const int h = blockIdx.x, tid = threadIdx.x;
+  const int ti = tid >> 4, tj = tid & 15;
+  const double* Gb = Gbar + (size_t)h * D * D;
+  if (tid == 0) bad = 0;
+  double a[NB][NB];
 #pragma unroll
   for (int r = 0; r < NB; ++r)
 #pragma unroll
-    for (int c = 0; c < NB; ++c) {
-      const int i = ti + 16 * r, j = tj + 16 * c;
-      double v = (1.0 - alpha) * a[r][c];
-      if (i == j) v = (v + as) + es;
-      nf |= !isfinite(v);
-      a[r][c] = v;
-      Gb[i * D + j] = v;
-    }
-  if (nf) bad = 1;
+    for (int c = 0; c < NB; ++c) a[r][c] = Gb[(ti + 16 * r) * D + tj + 16 * c];
   if (tj == 0)
 #pragma unroll
     for (int r = 0; r < NB; ++r) col[0][ti + 16 * r] = a[r][0];
@@ -248,8 +256,8 @@ size_t gram_chunks(int H, int N) {
 }
 
 park_status launch_metric(const void* Q, int H, int N, int D, int dtype, double alpha, double eps,
-                          double s_min, double* part, double* G, double* Gbar, double* R,
-                          int* status, hipStream_t st) {
+                          double s_min, double* part, double* G, double* Gbar, int* status,
+                          hipStream_t st) {
   const int nch = (int)gram_chunks(H, N);
   const int rows_per = (N + nch - 1) / nch;
   dim3 g1(nch, H);
@@ -272,11 +280,20 @@ park_status launch_metric(const void* Q, int H, int N, int D, int dtype, double 
   PARK_LAUNCH("gram_reduce", k_gram_reduce, dim3((DD + 255) / 256, H), dim3(256), 0, st, part, nch,
               DD, 1.0 / (double)N, G);
   if (D == 128)
-    PARK_LAUNCH("metric_chol", k_metric_chol<128>, dim3(H), dim3(256), 0, st, G, alpha, eps,
-                s_min, Gbar, R, status);
+    PARK_LAUNCH("metric_gbar", k_metric_gbar<128>, dim3(H), dim3(256), 0, st, G, alpha, eps,
+                s_min, Gbar, status);
   else
-    PARK_LAUNCH("metric_chol", k_metric_chol<64>, dim3(H), dim3(256), 0, st, G, alpha, eps,
-                s_min, Gbar, R, status);
+    PARK_LAUNCH("metric_gbar", k_metric_gbar<64>, dim3(H), dim3(256), 0, st, G, alpha, eps,
+                s_min, Gbar, status);
+  return PARK_OK;
+}
+
+park_status launch_metric_factor(const double* Gbar, int H, int D, double* R, int* status,
+                                 hipStream_t st) {
+  if (D == 128)
+    PARK_LAUNCH("metric_chol", k_metric_chol<128>, dim3(H), dim3(256), 0, st, Gbar, R, status);
+  else
+    PARK_LAUNCH("metric_chol", k_metric_chol<64>, dim3(H), dim3(256), 0, st, Gbar, R, status);
   return PARK_OK;
 }
 

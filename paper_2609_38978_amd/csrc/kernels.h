@@ -7,9 +7,13 @@ namespace park {
 
 // k_metric.hip --------------------------------------------------------------
 size_t gram_chunks(int H, int N);
+// G = Q^T Q / N and Gbar (Eq. (11)); then, separately, the Cholesky factor R of
+// Gbar (the k-means only needs Gbar)
 park_status launch_metric(const void* Q, int H, int N, int D, int dtype, double alpha, double eps,
-                          double s_min, double* part, double* G, double* Gbar, double* R,
-                          int* status, hipStream_t st);
+                          double s_min, double* part, double* G, double* Gbar, int* status,
+                          hipStream_t st);
+park_status launch_metric_factor(const double* Gbar, int H, int D, double* R, int* status,
+                                 hipStream_t st);
 park_status launch_transform(const void* X, const double* R, int H, int N, int D, int dtype,
                              float* Xt, hipStream_t st);
 

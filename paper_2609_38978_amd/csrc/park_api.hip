@@ -218,16 +218,18 @@ static park_status check_ws(void* ws, size_t ws_bytes, size_t need) {
 }
 
 // ------------------------------------------------------------ side stream
-// The query side's clustering runs on a second stream of the device, beside
-// the key side's (metric and k-means) on the caller's stream: the two share
-// nothing but the status word, which kernels only OR into.  The stream
+// The query side's clustering and the Cholesky factor of the key side's
+// metric run on a second stream of the device, beside the key side's Gbar
+// and k-means on the caller's stream: they share nothing but the status word,
+// which kernels only OR into, and Gbar, which all of them only read.  The stream
 // (default priority) and its fork/join events are created on the first call
 // that is not being captured; until then the sides run one after the other.
-// Recording an event and making the other stream wait on it happen under one
-// lock, so concurrent calls on one device cannot swap each other's events.
+// A call holds the device's lock while it queues its work, so concurrent calls
+// on one device cannot swap each other's events.
 struct SideStream {
   hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr, gbar = nullptr;
+  std::mutex mu;  // held while a call queues its work (the events are shared)
 };
 static std::mutex g_side_mu;
 static SideStream g_side[64];
@@ -242,50 +244,53 @@ static SideStream* side_stream(hipStream_t st) {
     if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
       return nullptr;
     hipStream_t s2 = nullptr;
-    hipEvent_t e1 = nullptr, e2 = nullptr;
+    hipEvent_t e[3] = {nullptr, nullptr, nullptr};
     if (hipStreamCreateWithFlags(&s2, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    if (hipEventCreateWithFlags(&e1, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&e2, hipEventDisableTiming) != hipSuccess) {
-      if (e1) hipEventDestroy(e1);
-      hipStreamDestroy(s2);
-      return nullptr;
-    }
+    for (int i = 0; i < 3; ++i)
+      if (hipEventCreateWithFlags(&e[i], hipEventDisableTiming) != hipSuccess) {
+        for (int j = 0; j < i; ++j) hipEventDestroy(e[j]);
+        hipStreamDestroy(s2);
+        return nullptr;
+      }
     a.s = s2;
-    a.fork = e1;
-    a.join = e2;
+    a.fork = e[0];
+    a.join = e[1];
+    a.gbar = e[2];
   }
   return &a;
 }
 
-// `to` waits for the work `from` holds so far
-static park_status stream_after(SideStream* a, hipEvent_t ev, hipStream_t from, hipStream_t to) {
-  std::lock_guard<std::mutex> lk(g_side_mu);
-  hipError_t e = hipEventRecord(ev, from);
-  if (e == hipSuccess) e = hipStreamWaitEvent(to, ev, 0);
-  if (e != hipSuccess) return fail(PARK_ERR_HIP, "side stream: %s", hipGetErrorString(e));
-  (void)a;
-  return PARK_OK;
+static park_status ev_record(hipEvent_t ev, hipStream_t s) {
+  const hipError_t e = hipEventRecord(ev, s);
+  return e == hipSuccess ? PARK_OK : fail(PARK_ERR_HIP, "event record: %s", hipGetErrorString(e));
+}
+static park_status ev_wait(hipStream_t s, hipEvent_t ev) {
+  const hipError_t e = hipStreamWaitEvent(s, ev, 0);
+  return e == hipSuccess ? PARK_OK : fail(PARK_ERR_HIP, "stream wait: %s", hipGetErrorString(e));
 }
 
 // ------------------------------------------------------------ stage bodies
 // `region` (optional) is the cluster workspace to use; by default the first
-// region after the status word.  `parts`: 1 the metric (and transform), 2 the
-// k-means (a metric already in the region), 3 both.
+// region after the status word.  `parts`: bit 1 the metric Gbar, bit 4 its
+// Cholesky factor R (and the transform), bit 2 the k-means (with the Gbar
+// already in the region); 7 all, in that order.
 static park_status cluster_body(const void* X, const void* Qm, const park_dims& dm, int C, int T,
                                 uint64_t seed, int side, int metric, double alpha, double eps,
                                 double s_min, int* labels, int* perm, int* offsets, double* R_out,
                                 float* Xt_out, void* ws, hipStream_t st,
-                                const ClusterWs* region = nullptr, int parts = 3) {
+                                const ClusterWs* region = nullptr, int parts = 7) {
   const int H = dm.H, N = dm.N, D = dm.d;
   Carver cv(ws);
   int* status = cv.take<int>(64);
   ClusterWs cw = region ? *region : carve_cluster(cv, H, N, D, C);
   const double* Gbar = nullptr;
   if (metric == PARK_METRIC_QRKC) {
-    if (parts & 1) {
-      double* R = R_out ? R_out : cw.R;
-      PARK_TRY(launch_metric(Qm, H, N, D, dm.dtype, alpha, eps, s_min, cw.part, cw.G, cw.Gbar, R,
+    if (parts & 1)
+      PARK_TRY(launch_metric(Qm, H, N, D, dm.dtype, alpha, eps, s_min, cw.part, cw.G, cw.Gbar,
                              status, st));
+    if (parts & 4) {
+      double* R = R_out ? R_out : cw.R;
+      PARK_TRY(launch_metric_factor(cw.Gbar, H, D, R, status, st));
       if (Xt_out) PARK_TRY(launch_transform(X, R, H, N, D, dm.dtype, Xt_out, st));
     }
     Gbar = cw.Gbar;
@@ -517,24 +522,36 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
     const ClusterWs cq = carve_cluster(rc, H, N, D, p->CQ);
     const ClusterWs ck = carve_cluster(rc, H, N, D, p->CK);
     // queued in this order so that both streams get work early: the key
-    // side's metric, the whole query side, the key side's k-means
+    // side's metric Gbar, the whole query side and then the factor of Gbar
+    // (side stream), the key side's k-means (which needs only Gbar)
     SideStream* side = side_stream(st);
-    hipStream_t sq = st;
+    hipStream_t sq = side ? side->s : st;
+    std::unique_lock<std::mutex> lk;
     if (side) {
-      PARK_TRY(stream_after(side, side->fork, st, side->s));
-      sq = side->s;
+      lk = std::unique_lock<std::mutex>(side->mu);
+      PARK_TRY(ev_record(side->fork, st));
+      PARK_TRY(ev_wait(sq, side->fork));
     }
     park_status r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha,
                                  p->eps, p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr,
                                  nullptr, ws, st, &ck, 1);
+    if (side) PARK_TRY(ev_record(side->gbar, st));
     if (r == PARK_OK)
       r = cluster_body(Q, nullptr, *dims, p->CQ, p->T, p->seed, 0, PARK_METRIC_EUCLID, 0, 0, 1,
                        nullptr, s->q_perm, s->q_offsets, nullptr, nullptr, ws, sq, &cq);
+    if (side) PARK_TRY(ev_wait(sq, side->gbar));
+    if (r == PARK_OK)
+      r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha, p->eps,
+                       p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr, nullptr, ws, sq, &ck,
+                       4);
     if (r == PARK_OK)
       r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha, p->eps,
                        p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr, nullptr, ws, st, &ck,
                        2);
-    if (side) PARK_TRY(stream_after(side, side->join, sq, st));  // joined also after an error
+    if (side) {  // joined also after an error
+      PARK_TRY(ev_record(side->join, sq));
+      PARK_TRY(ev_wait(st, side->join));
+    }
     PARK_TRY(r);
   }
   PARK_TRY(launch_gather(Q, s->q_perm, H, N, D, dims->dtype, s->Qp, st));
