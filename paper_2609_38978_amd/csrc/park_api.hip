@@ -1,6 +1,7 @@
 // Host side of the PARK C ABI: argument validation, workspace layout, stage
 // orchestration, status reporting and the optional per-kernel profiler.
 #include <stdarg.h>
+#include <stdlib.h>
 #include <stdio.h>
 #include <string.h>
 
@@ -235,6 +236,13 @@ static std::mutex g_side_mu;
 static SideStream g_side[64];
 
 static SideStream* side_stream(hipStream_t st) {
+  // PARK_SIDE_STREAM=0 keeps everything on the caller's stream (kernel
+  // durations then carry no overlap with the other side's kernels)
+  static const bool off = [] {
+    const char* e = getenv("PARK_SIDE_STREAM");
+    return e && e[0] == '0';
+  }();
+  if (off) return nullptr;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
   std::lock_guard<std::mutex> lk(g_side_mu);
