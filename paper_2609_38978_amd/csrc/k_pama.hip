@@ -73,8 +73,11 @@ __device__ __forceinline__ uint32_t p64_lds_addr(const void* p) {
 }
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
-template <typename T, int D>
-__global__ __launch_bounds__(256, 2) void k_pama64(const T* __restrict__ Qp,
+// W2: two wavefronts per SIMD (centroid blocks of a tile one after the other,
+// registers within 256); otherwise one wavefront per SIMD with the two blocks
+// of a tile unrolled together (shorter steps, for small item counts).
+template <typename T, int D, bool W2>
+__global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict__ Qp,
                                                 const int* __restrict__ q_offsets,
                                                 const float* __restrict__ cen,
                                                 const int* __restrict__ k_sizes, int H, int N,
@@ -203,7 +206,8 @@ __global__ __launch_bounds__(256, 2) void k_pama64(const T* __restrict__ Qp,
       const int slot = it % NS;
       const float* cs = &Ct[slot][0];
       const int c0 = tile * CT;
-#pragma unroll 1
+      constexpr int UNR = W2 ? 1 : CT / 16;
+#pragma unroll UNR
       for (int cb = 0; cb < CT / 16; ++cb) {
         const int row = 16 * cb + c16;  // B operand: centroid row, dimension 4s + g
         const float* crow = cs + row * D + g;
@@ -1454,43 +1458,50 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   return PARK_OK;
 }
 
+template <int D, bool W2>
+static park_status pama64_launch(const char* nm, unsigned nwg, size_t lds, const void* Qp,
+                                 int dtype, const int* q_offsets, const float* cen,
+                                 const int* k_sizes, int H, int N, int CQ, int CK,
+                                 const int4* items, int* cnt, double* part, double* W64,
+                                 float* W32, int* status, hipStream_t st) {
+  // reserved once for the largest CK (2048), outside any stream capture that may follow
+  static const int lds_max = (int)(MAXC * sizeof(double));
+  static const hipError_t a1 = hipFuncSetAttribute(
+      (const void*)k_pama64<bf16_t, D, W2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+  static const hipError_t a2 = hipFuncSetAttribute(
+      (const void*)k_pama64<float, D, W2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+  if (a1 != hipSuccess || a2 != hipSuccess)
+    return fail(PARK_ERR_HIP, "retrieval: cannot reserve %zu bytes of LDS", lds);
+  if (dtype == PARK_BF16)
+    PARK_LAUNCH(nm, (k_pama64<bf16_t, D, W2>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
+                q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
+  else
+    PARK_LAUNCH(nm, (k_pama64<float, D, W2>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
+                q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
+  return PARK_OK;
+}
+
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                           const int4* items, int* cnt, double* part, double* W64, float* W32,
                           int* status, hipStream_t st) {
-  // with an item list: a queue drained by two workgroups per CU; without:
-  // one workgroup per row, the rows of a head on one XCD
+  // with an item list: a queue drained by a fixed grid; without: one
+  // workgroup per row, the rows of a head on one XCD
   const unsigned nwg = items ? 512u : 8u * (((unsigned)H * (unsigned)CQ + 7u) / 8u);
   const size_t lds = (size_t)CK * sizeof(double);
   const char* nm = items ? "pama_refine64" : "pama64";
-  // reserved once for the largest CK (2048), outside any stream capture that may follow
-  static const int lds_max = (int)(MAXC * sizeof(double));
-  static const hipError_t a1 = hipFuncSetAttribute(
-      (const void*)k_pama64<bf16_t, 128>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-  static const hipError_t a2 = hipFuncSetAttribute(
-      (const void*)k_pama64<float, 128>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-  static const hipError_t a3 = hipFuncSetAttribute(
-      (const void*)k_pama64<bf16_t, 64>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-  static const hipError_t a4 = hipFuncSetAttribute(
-      (const void*)k_pama64<float, 64>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-  if (a1 != hipSuccess || a2 != hipSuccess || a3 != hipSuccess || a4 != hipSuccess)
-    return fail(PARK_ERR_HIP, "retrieval: cannot reserve %zu bytes of LDS", lds);
-  if (D == 128) {
-    if (dtype == PARK_BF16)
-      PARK_LAUNCH(nm, (k_pama64<bf16_t, 128>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
-                  q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
-    else
-      PARK_LAUNCH(nm, (k_pama64<float, 128>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
-                  q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
-  } else {
-    if (dtype == PARK_BF16)
-      PARK_LAUNCH(nm, (k_pama64<bf16_t, 64>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
-                  q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
-    else
-      PARK_LAUNCH(nm, (k_pama64<float, 64>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
-                  q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
-  }
-  return PARK_OK;
+  // small layers have few items: the shorter steps of one wavefront per SIMD
+  // win; large ones fill the chip, and two wavefronts per SIMD hide latency
+  const bool w2 = (long)H * CQ >= 8192;
+  if (D == 128)
+    return w2 ? pama64_launch<128, true>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N,
+                                         CQ, CK, items, cnt, part, W64, W32, status, st)
+              : pama64_launch<128, false>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N,
+                                          CQ, CK, items, cnt, part, W64, W32, status, st);
+  return w2 ? pama64_launch<64, true>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N, CQ,
+                                      CK, items, cnt, part, W64, W32, status, st)
+            : pama64_launch<64, false>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N, CQ,
+                                       CK, items, cnt, part, W64, W32, status, st);
 }
 
 }  // namespace park
