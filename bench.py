@@ -44,6 +44,13 @@ def parse():
     ap.add_argument("--ratio", type=float, default=None, help="override: top-k ratio")
     ap.add_argument("--block", type=int, default=None, help="override: mean block size B")
     ap.add_argument("--iters", type=int, default=None, help="override: k-means iterations T")
+    ap.add_argument("--estimator", default="pama", choices=["pama", "qcentroid"],
+                    help="block-importance estimate: PAMA, or the query-centroid estimate "
+                         "(the 'w/o PAMA' ablation)")
+    ap.add_argument("--blocks", default="cluster", choices=["cluster", "fixed"],
+                    help="blocks = k-means clusters, or fixed chunks of the cluster order")
+    ap.add_argument("--key-metric", default="qrkc", choices=["qrkc", "euclid"],
+                    help="key clustering: QRKC, or Euclidean k-means (the 'w/o QRKC' ablation)")
     ap.add_argument("--cpu-heads", type=int, default=4,
                     help="heads of the layer the oracle runs for the CPU baseline")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -153,7 +160,7 @@ def kernel_work(name, cfg, st, C):
     return None
 
 
-def cpu_baseline(cfg, q, k, v, nheads):
+def cpu_baseline(cfg, q, k, v, nheads, variant):
     import numpy as np
     from oracle import park_oracle as O
     try:
@@ -165,7 +172,8 @@ def cpu_baseline(cfg, q, k, v, nheads):
     param = cfg.ratio if mode == "topk" else cfg.topp
     t0 = time.perf_counter()
     for h in range(nheads):
-        O.park_head(q[h], k[h], v[h], cfg.C, cfg.C, cfg.iters, mode, param, seed=0, head=h)
+        O.park_head(q[h], k[h], v[h], cfg.C, cfg.C, cfg.iters, mode, param, seed=0, head=h,
+                    **variant)
     dt = time.perf_counter() - t0
     ms_layer = dt * 1e3 * cfg.H / nheads
     return {"value": round(ms_layer, 3), "unit": "ms per layer", "cores": int(threads),
@@ -208,8 +216,15 @@ def main():
     param = cfg.ratio if mode == "topk" else cfg.topp
     reuse = {"recompute": P.PARK_RECOMPUTE, "clusters": P.PARK_REUSE_CLUSTERS,
              "mask": P.PARK_REUSE_CLUSTERS_AND_MASK}[args.reuse]
+    variant = {"estimator": args.estimator, "blocks": args.blocks, "key_metric": args.key_metric}
     prm = P.make_params(C, C, T=cfg.iters, select=mode, ratio=param, topp=param, seed=0,
-                        out_dtype=P.PARK_BF16 if cfg.dtype == "bf16" else P.PARK_F32)
+                        out_dtype=P.PARK_BF16 if cfg.dtype == "bf16" else P.PARK_F32,
+                        estimator={"pama": P.PARK_EST_PAMA,
+                                   "qcentroid": P.PARK_EST_QCENTROID}[args.estimator],
+                        block_mode={"cluster": P.PARK_BLOCKS_CLUSTER,
+                                    "fixed": P.PARK_BLOCKS_FIXED}[args.blocks],
+                        key_metric={"qrkc": P.PARK_METRIC_QRKC,
+                                    "euclid": P.PARK_METRIC_EUCLID}[args.key_metric])
     ws = P.workspace(Q, C, C)
     st = P.make_state(Q, C, C)
     out = torch.empty(Q.shape, dtype=tdt, device="cuda")
@@ -313,16 +328,18 @@ def main():
            "data": "synthetic (seeded clustered-Gaussian DiT-shaped Q/K/V)",
            "config": {"workload": f"{cfg.name}: H={cfg.H} N={cfg.N} d={cfg.d} {cfg.dtype} "
                                   f"B={cfg.block} C={C} T={cfg.iters} {mode} {param}"
-                                  + ("" if reuse == P.PARK_RECOMPUTE else f" reuse={args.reuse}"),
+                                  + ("" if reuse == P.PARK_RECOMPUTE else f" reuse={args.reuse}")
+                                  + "".join(f" {k}={v}" for k, v in variant.items()
+                                            if v not in ("pama", "cluster", "qrkc")),
                       "H": cfg.H, "N": cfg.N, "d": cfg.d, "B": cfg.block, "C": C, "T": cfg.iters,
-                      "select": mode, "param": param, "reuse": args.reuse},
+                      "select": mode, "param": param, "reuse": args.reuse, **variant},
            "dense_equiv_tflops": round(dense_flops / (ms * 1e-3) / 1e12, 3),
            "timing": "eager park_forward calls, events on the launch stream",
            "graph_ms_per_step": None if ms_graph is None else round(ms_graph, 4),
            "wall_s": round(wall, 3), "stages": stages, "stage_roofline": stage_roof,
            "roofline": roof}
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, q, k, v, min(args.cpu_heads, cfg.H))
+        res["cpu_baseline"] = cpu_baseline(cfg, q, k, v, min(args.cpu_heads, cfg.H), variant)
     print(json.dumps(res), flush=True)
 
 

@@ -82,6 +82,22 @@ typedef enum park_reuse {
   PARK_REUSE_CLUSTERS_AND_MASK = 2 /* keep permutations, offsets and the mask   */
 } park_reuse;
 
+/* How park_forward estimates block importance (Sec. 5.1 and the ablation of
+ * Sec. 6).  PARK_EST_PAMA: per-query softmax over the key-block scores, then
+ * the mean over the query block (Eqs. (8)-(9)).  PARK_EST_QCENTROID: the
+ * query-centroid estimate of Sec. 4.1, softmax_v(qbar_u . c_v / sqrt(d) +
+ * log n_v) with qbar_u the mean of the block's queries rounded to float (the
+ * "w/o PAMA" variant); its rows are computed in float64. */
+typedef enum park_estimator { PARK_EST_PAMA = 0, PARK_EST_QCENTROID = 1 } park_estimator;
+
+/* What a block is.  PARK_BLOCKS_CLUSTER: block v is k-means cluster v (Alg. 3:
+ * K_v = {j : z_j = v}, variable sizes).  PARK_BLOCKS_FIXED: the tokens are
+ * still ordered by cluster (stable argsort of the labels), but block v is the
+ * fixed chunk [v b, min((v+1) b, N)) of that order with b = ceil(N / C), so
+ * every block has b tokens except a shorter last one (and empty trailing
+ * blocks when C b - N >= b). */
+typedef enum park_block_mode { PARK_BLOCKS_CLUSTER = 0, PARK_BLOCKS_FIXED = 1 } park_block_mode;
+
 typedef struct park_dims {
   int32_t H;     /* attention heads                      */
   int32_t N;     /* tokens per head (L in the paper)     */
@@ -102,6 +118,8 @@ typedef struct park_params {
   uint64_t seed;     /* k-means initialisation seed                          */
   int32_t key_metric;/* park_metric for the keys (PARK_METRIC_QRKC)          */
   int32_t out_dtype; /* park_dtype of O                                      */
+  int32_t estimator; /* park_estimator (PARK_EST_PAMA)                        */
+  int32_t block_mode;/* park_block_mode (PARK_BLOCKS_CLUSTER)                 */
 } park_params;
 
 /* Caller-allocated device buffers carried across park_forward calls. */

@@ -168,6 +168,18 @@ def stable_argsort(z: np.ndarray, C: int):
     return perm.astype(np.int64), offsets.astype(np.int64)
 
 
+def fixed_tile_offsets(N: int, C: int) -> np.ndarray:
+    """Blocks as fixed chunks of the cluster-sorted order: o_v = min(v b, N).
+
+    The literal reading of a block size with a padded last block: b =
+    ceil(N / C) tokens per block, a shorter last block, and empty trailing
+    blocks when C b - N >= b.  The tokens keep the order of the stable
+    argsort of the cluster labels (Alg. 3).
+    """
+    b = -(-N // C)
+    return np.minimum(np.arange(C + 1, dtype=np.int64) * b, N)
+
+
 def block_centroids(Kp: np.ndarray, offsets: np.ndarray):
     """c_v = (1/n_v) sum of the original keys of block v (Eq. (8), Alg. 3).
 
@@ -215,6 +227,28 @@ def pama(Qp: np.ndarray, q_offsets: np.ndarray, c: np.ndarray, n: np.ndarray) ->
         if b > a:
             P = softmax_rows(pama_scores(Qp[a:b], c, n))
             W[u] = P.sum(axis=0) / (b - a)
+    return W
+
+
+def query_centroid_estimate(Qp: np.ndarray, q_offsets: np.ndarray, c: np.ndarray,
+                            n: np.ndarray) -> np.ndarray:
+    """W^centroid_uv = phi_v(qbar_u), the query-centroid estimate (Sec. 4.1).
+
+    The queries of block u are replaced by their mean before the softmax:
+    phi_v(q) is the weight a single query q gives key block v under the
+    PAMA score of Eq. (8), so the row is softmax_v(qbar_u . c_v / sqrt(d) +
+    log n_v).  This is the "w/o PAMA" variant of the ablation (Sec. 6).
+    qbar_u is rounded to float32, like the key-block centroids.  Rows of
+    empty query blocks are zero.
+    """
+    Qp = np.asarray(Qp, dtype=np.float64)
+    CQ = len(q_offsets) - 1
+    W = np.zeros((CQ, len(n)), dtype=np.float64)
+    for u in range(CQ):
+        a, b = int(q_offsets[u]), int(q_offsets[u + 1])
+        if b > a:
+            qbar = (Qp[a:b].sum(axis=0) / (b - a)).astype(np.float32)
+            W[u] = softmax_rows(pama_scores(qbar[None, :], c, n))[0]
     return W
 
 
@@ -317,14 +351,36 @@ def cluster_keys(K, Q, C, T, seed, head, alpha=0.05, eps=1e-6, s_min=1e-12):
 
 
 def park_head(Q, K, V, CQ, CK, T, mode, param, seed=0, head=0, alpha=0.05, eps=1e-6,
-              s_min=1e-12):
-    """PARK forward of one head; returns every intermediate and O."""
+              s_min=1e-12, estimator="pama", blocks="cluster", key_metric="qrkc"):
+    """PARK forward of one head; returns every intermediate and O.
+
+    estimator: "pama" (Eqs. (8)-(9)) or "qcentroid" (the query-centroid
+    estimate, the "w/o PAMA" ablation).  blocks: "cluster" (block v is
+    cluster v) or "fixed" (fixed chunks of the cluster-sorted order).
+    key_metric: "qrkc" (Alg. 3) or "euclid" (the "w/o QRKC" ablation).
+    """
     Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
     cq = cluster_queries(Q, CQ, T, seed, head)
-    ck = cluster_keys(K, Q, CK, T, seed, head, alpha, eps, s_min)
+    if key_metric == "qrkc":
+        ck = cluster_keys(K, Q, CK, T, seed, head, alpha, eps, s_min)
+    else:
+        init = init_indices(K.shape[0], CK, seed, head, side=1)
+        z, mu = kmeans(K, CK, T, init)
+        perm, off = stable_argsort(z, CK)
+        ck = {"labels": z, "perm": perm, "offsets": off, "mu": mu, "init": init}
+    if blocks == "fixed":
+        cq = {**cq, "offsets": fixed_tile_offsets(Q.shape[0], CQ)}
+        ck = {**ck, "offsets": fixed_tile_offsets(K.shape[0], CK)}
+    elif blocks != "cluster":
+        raise ValueError(blocks)
     Qp, Kp, Vp = Q[cq["perm"]], K[ck["perm"]], V[ck["perm"]]
     c, n = block_centroids(Kp, ck["offsets"])
-    W = pama(Qp, cq["offsets"], c, n)
+    if estimator == "pama":
+        W = pama(Qp, cq["offsets"], c, n)
+    elif estimator == "qcentroid":
+        W = query_centroid_estimate(Qp, cq["offsets"], c, n)
+    else:
+        raise ValueError(estimator)
     rows = select(W, np.diff(cq["offsets"]), n, mode, param)
     O = block_sparse_attention(Qp, Kp, Vp, cq["offsets"], ck["offsets"], rows, cq["perm"])
     return {"q": cq, "k": ck, "Qp": Qp, "Kp": Kp, "Vp": Vp, "centroids": c, "sizes": n,

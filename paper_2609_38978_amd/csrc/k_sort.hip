@@ -191,4 +191,57 @@ park_status launch_gather(const void* X, const int* perm, int H, int N, int D, i
   return PARK_OK;
 }
 
+// Fixed-tile blocks of the cluster-ordered tokens: offsets[h][v] =
+// min(v b, N) for v = 0..C, b = ceil(N / C).
+__global__ __launch_bounds__(256) void k_fixed_offsets(int N, int C, int b,
+                                                       int* __restrict__ offsets) {
+  const int h = blockIdx.y;
+  const int v = blockIdx.x * 256 + threadIdx.x;
+  if (v > C) return;
+  const long o = (long)v * b;
+  offsets[(size_t)h * (C + 1) + v] = o < (long)N ? (int)o : N;
+}
+
+park_status launch_fixed_offsets(int H, int N, int C, int* offsets, hipStream_t st) {
+  const int b = (N + C - 1) / C;
+  PARK_LAUNCH("fixed_offsets", k_fixed_offsets, dim3((C + 1 + 255) / 256, H), dim3(256), 0, st,
+              N, C, b, offsets);
+  return PARK_OK;
+}
+
+// Rows of the nonempty blocks packed in block order: row u of x (sizes[u] >
+// 0) moves to row r_u = #{w < u : sizes[w] > 0} of out, and the unit
+// offsets uoff[h][u] = r_u (uoff[h][C] = the count) give each nonempty block
+// exactly that one row.  One workgroup per (block, head).
+__global__ __launch_bounds__(256) void k_compact_rows(const float* __restrict__ x,
+                                                      const int* __restrict__ sizes, int C, int D,
+                                                      float* __restrict__ out,
+                                                      int* __restrict__ uoff) {
+  __shared__ int red[4];
+  const int h = blockIdx.y, u = blockIdx.x, tid = threadIdx.x;
+  const int* sz = sizes + (size_t)h * C;
+  int cnt = 0;
+  for (int w = tid; w < u; w += 256) cnt += sz[w] > 0 ? 1 : 0;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+  if ((tid & 63) == 0) red[tid >> 6] = cnt;
+  __syncthreads();
+  const int r = red[0] + red[1] + red[2] + red[3];
+  const bool keep = sz[u] > 0;
+  if (tid == 0) {
+    uoff[(size_t)h * (C + 1) + u] = r;
+    if (u == C - 1) uoff[(size_t)h * (C + 1) + C] = r + (keep ? 1 : 0);
+  }
+  if (keep)
+    for (int a = tid; a < D; a += 256)
+      out[((size_t)h * C + r) * D + a] = x[((size_t)h * C + u) * D + a];
+}
+
+park_status launch_compact_rows(const float* x, const int* sizes, int H, int C, int D, float* out,
+                                int* uoff, hipStream_t st) {
+  PARK_LAUNCH("compact_rows", k_compact_rows, dim3(C, H), dim3(256), 0, st, x, sizes, C, D, out,
+              uoff);
+  return PARK_OK;
+}
+
 }  // namespace park

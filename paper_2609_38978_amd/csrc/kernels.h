@@ -24,6 +24,12 @@ park_status launch_count_sort(const int* labels, int H, int N, int C, int* thist
                               int* offsets, hipStream_t st);
 park_status launch_gather(const void* X, const int* perm, int H, int N, int D, int dtype, void* Xp,
                           hipStream_t st);
+// fixed-tile block boundaries min(v ceil(N/C), N), v = 0..C, for every head
+park_status launch_fixed_offsets(int H, int N, int C, int* offsets, hipStream_t st);
+// rows of the nonempty blocks (sizes > 0) of x [H][C][D] packed into out
+// [H][C][D] in block order, with offsets [H][C+1] giving each such block its row
+park_status launch_compact_rows(const float* x, const int* sizes, int H, int C, int D, float* out,
+                                int* uoff, hipStream_t st);
 
 // k_kmeans.hip --------------------------------------------------------------
 // centroid count padded to the fast assignment's tile multiple

@@ -195,6 +195,24 @@ static void* carve_attn_plan(void* ws, int H, int N, int CQ) {
   return cv.take<int4>(attn_plan_bytes(H, N, CQ) / sizeof(int4));
 }
 
+// query-centroid estimator: the block means of the queries, packed, and the
+// offsets giving each nonempty query block its one row
+struct QcenBufs {
+  float* qbar;   // [H][CQ][D]
+  float* qrows;  // [H][CQ][D]
+  int* qsizes;   // [H][CQ]
+  int* uoff;     // [H][CQ+1]
+};
+
+static QcenBufs carve_qcen(Carver& cv, int H, int D, int CQ) {
+  QcenBufs q;
+  q.qbar = cv.take<float>((size_t)H * CQ * D);
+  q.qrows = cv.take<float>((size_t)H * CQ * D);
+  q.qsizes = cv.take<int>((size_t)H * CQ);
+  q.uoff = cv.take<int>((size_t)H * (CQ + 1));
+  return q;
+}
+
 // status word first, then the largest of the cluster, retrieval and attention regions
 static size_t ws_bytes_for(int H, int N, int D, int CQ, int CK) {
   Carver a(nullptr);
@@ -207,7 +225,11 @@ static size_t ws_bytes_for(int H, int N, int D, int CQ, int CK) {
   Carver c2(nullptr);
   c2.off = base;
   carve_retrieve(c2, H, N, D, CQ, CK);
-  return std::max(std::max(c1.off, c2.off), attn_ws_end(H, N, CQ)) + 256;
+  Carver c3(nullptr);  // query-centroid estimator: CQ float rows per head
+  c3.off = base;
+  carve_qcen(c3, H, D, CQ);
+  carve_retrieve(c3, H, CQ, D, CQ, CK);
+  return std::max(std::max(std::max(c1.off, c2.off), c3.off), attn_ws_end(H, N, CQ)) + 256;
 }
 
 static park_status check_ws(void* ws, size_t ws_bytes, size_t need) {
@@ -500,6 +522,10 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
     return fail(PARK_ERR_INVALID_ARG, "need alpha in [0,1], eps >= 0, s_min > 0");
   if (p->out_dtype != PARK_F32 && p->out_dtype != PARK_BF16)
     return fail(PARK_ERR_INVALID_ARG, "unknown out_dtype %d", p->out_dtype);
+  if (p->estimator != PARK_EST_PAMA && p->estimator != PARK_EST_QCENTROID)
+    return fail(PARK_ERR_INVALID_ARG, "unknown estimator %d", p->estimator);
+  if (p->block_mode != PARK_BLOCKS_CLUSTER && p->block_mode != PARK_BLOCKS_FIXED)
+    return fail(PARK_ERR_INVALID_ARG, "unknown block mode %d", p->block_mode);
   if (reuse < PARK_RECOMPUTE || reuse > PARK_REUSE_CLUSTERS_AND_MASK)
     return fail(PARK_ERR_INVALID_ARG, "unknown reuse mode %d", reuse);
   PARK_TRY(check_ptr(Q, "Q"));
@@ -561,6 +587,10 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
       PARK_TRY(ev_wait(st, side->join));
     }
     PARK_TRY(r);
+    if (p->block_mode == PARK_BLOCKS_FIXED) {  // same order, fixed chunks of it
+      PARK_TRY(launch_fixed_offsets(H, N, p->CQ, s->q_offsets, st));
+      PARK_TRY(launch_fixed_offsets(H, N, p->CK, s->k_offsets, st));
+    }
   }
   PARK_TRY(launch_gather(Q, s->q_perm, H, N, D, dims->dtype, s->Qp, st));
   PARK_TRY(launch_gather(K, s->k_perm, H, N, D, dims->dtype, s->Kp, st));
@@ -568,8 +598,23 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
   if (reuse != PARK_REUSE_CLUSTERS_AND_MASK) {
     PARK_TRY(launch_segment_mean(s->Kp, nullptr, s->k_offsets, H, N, D, dims->dtype, p->CK,
                                  nullptr, s->k_centroids, s->k_sizes, st));
-    PARK_TRY(retrieve_body(s->Qp, s->q_offsets, s->k_centroids, s->k_sizes, *dims, p->CQ, p->CK,
-                           p->select, param, s->W, s->kv_count, s->kv_index, ws, st));
+    if (p->estimator == PARK_EST_PAMA) {
+      PARK_TRY(retrieve_body(s->Qp, s->q_offsets, s->k_centroids, s->k_sizes, *dims, p->CQ,
+                             p->CK, p->select, param, s->W, s->kv_count, s->kv_index, ws, st));
+    } else {
+      // query-centroid estimate: one float row (the block mean) per nonempty
+      // query block, scored and selected by the float64 retrieval path
+      Carver qc(ws);
+      int* status = qc.take<int>(64);
+      const QcenBufs qb = carve_qcen(qc, H, D, p->CQ);
+      const RetrieveBufs rb = carve_retrieve(qc, H, p->CQ, D, p->CQ, p->CK);
+      PARK_TRY(launch_segment_mean(s->Qp, nullptr, s->q_offsets, H, N, D, dims->dtype, p->CQ,
+                                   nullptr, qb.qbar, qb.qsizes, st));
+      PARK_TRY(launch_compact_rows(qb.qbar, qb.qsizes, H, p->CQ, D, qb.qrows, qb.uoff, st));
+      PARK_TRY(launch_retrieve(qb.qrows, qb.uoff, s->k_centroids, s->k_sizes, H, p->CQ, D,
+                               PARK_F32, p->CQ, p->CK, p->select, param, rb, s->W, s->kv_count,
+                               s->kv_index, status, st));
+    }
   }
   return launch_attention(s->Qp, s->Kp, s->Vp, s->q_offsets, s->k_offsets, s->kv_count,
                           s->kv_index, s->q_perm, H, N, D, dims->dtype, p->CQ, p->CK, O,

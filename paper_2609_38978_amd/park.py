@@ -20,6 +20,8 @@ PARK_F32, PARK_BF16 = 0, 1
 PARK_METRIC_EUCLID, PARK_METRIC_QRKC = 0, 1
 PARK_SELECT_TOPK, PARK_SELECT_TOPP = 0, 1
 PARK_RECOMPUTE, PARK_REUSE_CLUSTERS, PARK_REUSE_CLUSTERS_AND_MASK = 0, 1, 2
+PARK_EST_PAMA, PARK_EST_QCENTROID = 0, 1
+PARK_BLOCKS_CLUSTER, PARK_BLOCKS_FIXED = 0, 1
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpark.so")
 
@@ -46,7 +48,8 @@ class Params(C.Structure):
     _fields_ = [("CQ", C.c_int32), ("CK", C.c_int32), ("T", C.c_int32), ("select", C.c_int32),
                 ("topk_ratio", C.c_double), ("topp", C.c_double), ("alpha", C.c_double),
                 ("eps", C.c_double), ("s_min", C.c_double), ("seed", C.c_uint64),
-                ("key_metric", C.c_int32), ("out_dtype", C.c_int32)]
+                ("key_metric", C.c_int32), ("out_dtype", C.c_int32),
+                ("estimator", C.c_int32), ("block_mode", C.c_int32)]
 
 
 class State(C.Structure):
@@ -209,9 +212,11 @@ def park_block_sparse_attn(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index,
 
 
 def make_params(CQ, CK, T=10, select="topk", ratio=0.25, topp=0.9, alpha=0.05, eps=1e-6,
-                s_min=1e-12, seed=0, key_metric=PARK_METRIC_QRKC, out_dtype=PARK_F32) -> Params:
+                s_min=1e-12, seed=0, key_metric=PARK_METRIC_QRKC, out_dtype=PARK_F32,
+                estimator=PARK_EST_PAMA, block_mode=PARK_BLOCKS_CLUSTER) -> Params:
     sel = PARK_SELECT_TOPK if select in ("topk", PARK_SELECT_TOPK) else PARK_SELECT_TOPP
-    return Params(CQ, CK, T, sel, ratio, topp, alpha, eps, s_min, seed, key_metric, out_dtype)
+    return Params(CQ, CK, T, sel, ratio, topp, alpha, eps, s_min, seed, key_metric, out_dtype,
+                  estimator, block_mode)
 
 
 def make_state(Q, CQ: int, CK: int, want_W: bool = False) -> dict:

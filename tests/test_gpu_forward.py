@@ -98,3 +98,65 @@ def test_reuse_modes():
         Oref = O.block_sparse_attention(q2[i][qp], k2[i][kp], v[i][kp], qoff, koff,
                                         PT.rows_from_csr(kvc, kvi), qp)
         assert np.abs(PT.np64(O2)[i] - Oref).max() <= 2e-2
+
+
+# Ablation variants and the fixed-tile block mode through park_forward:
+# (config, grid override, heads, selection, estimator, block mode, key metric)
+VARIANTS = {
+    "qcentroid_tiny": ("tiny", None, None, None, "qcentroid", "cluster", "qrkc"),
+    "qcentroid_medium_topp": ("medium", (2, 16, 32), [0, 5], ("topp", 0.9), "qcentroid",
+                              "cluster", "qrkc"),
+    "fixed_tiny": ("tiny", None, None, None, "pama", "fixed", "qrkc"),
+    "fixed_ragged_topp": ("medium", (3, 11, 13), [0, 1], ("topp", 0.9), "pama", "fixed", "qrkc"),
+    "fixed_qcentroid_hunyuan": ("hunyuan", (2, 9, 16), [0], None, "qcentroid", "fixed", "qrkc"),
+    "euclid_keys_medium": ("medium", (2, 16, 32), [1, 2], None, "pama", "cluster", "euclid"),
+}
+
+
+@pytest.mark.parametrize("tag", list(VARIANTS))
+def test_forward_variants_match_oracle(tag):
+    name, grid, heads, sel, est, blocks, metric = VARIANTS[tag]
+    cfg = synth.CONFIGS[name]
+    if grid is not None:
+        cfg = cfg.with_(grid=grid)
+    mode, param = sel if sel else (cfg.select, cfg.ratio if cfg.select == "topk" else cfg.topp)
+    q, k, v = synth.make_layer(cfg, heads)
+    Q, K, V = (PT.to_dev(a, cfg.dtype) for a in (q, k, v))
+    C = cfg.C
+    prm = P.make_params(C, C, T=cfg.iters, select=mode, ratio=param, topp=param, seed=0,
+                        out_dtype=P.PARK_F32,
+                        estimator={"pama": P.PARK_EST_PAMA, "qcentroid": P.PARK_EST_QCENTROID}[est],
+                        block_mode={"cluster": P.PARK_BLOCKS_CLUSTER,
+                                    "fixed": P.PARK_BLOCKS_FIXED}[blocks],
+                        key_metric={"qrkc": P.PARK_METRIC_QRKC,
+                                    "euclid": P.PARK_METRIC_EUCLID}[metric])
+    ws = P.workspace(Q, C, C)
+    st = P.make_state(Q, C, C, want_W=True)
+    Og, st = P.park_forward(Q, K, V, prm, state=st, ws=ws)
+    P.park_check(ws)
+    Og = PT.np64(Og)
+    hs = heads if heads is not None else range(cfg.H)
+    for i, h in enumerate(hs):
+        print(f"[{tag} h={h}] N={cfg.N} C={C} {mode} {param}", flush=True)
+        ref = O.park_head(q[i], k[i], v[i], C, C, cfg.iters, mode, param, seed=0, head=i,
+                          estimator=est, blocks=blocks, key_metric=metric)
+        assert np.array_equal(st["q_perm"][i].cpu().numpy(), ref["q"]["perm"])
+        assert np.array_equal(st["k_perm"][i].cpu().numpy(), ref["k"]["perm"])
+        assert np.array_equal(st["q_offsets"][i].cpu().numpy(), ref["q"]["offsets"])
+        assert np.array_equal(st["k_offsets"][i].cpu().numpy(), ref["k"]["offsets"])
+        assert np.array_equal(st["k_sizes"][i].cpu().numpy(), ref["sizes"])
+        kvc = st["kv_count"][i].cpu().numpy()
+        kvi = st["kv_index"][i].cpu().numpy()
+        nd, nb = PT.compare_masks(ref["W"], ref["sizes"], np.diff(ref["q"]["offsets"]), mode,
+                                  param, kvc, kvi)
+        print(f"[{tag} h={h}] mask rows differing={nd} not-exempt={nb}")
+        assert nb == 0
+        Oref = O.block_sparse_attention(ref["Qp"], ref["Kp"], ref["Vp"], ref["q"]["offsets"],
+                                        ref["k"]["offsets"], PT.rows_from_csr(kvc, kvi),
+                                        ref["q"]["perm"])
+        err = np.abs(Og[i] - Oref)
+        print(f"[{tag} h={h}] attention max-abs err {err.max():.3g}")
+        assert np.all(err <= PT.attn_tol(cfg.dtype, False, Oref))
+        ok, werr = PT.w_error_ok(cfg.dtype, st["W"][i].cpu().numpy(), ref["W"])
+        print(f"[{tag} h={h}] W max-abs err {werr:.3g}")
+        assert ok

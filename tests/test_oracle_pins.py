@@ -449,3 +449,94 @@ def test_tiny_layer_end_to_end_sanity():
     # the mask keeps most of the exact importance of each query block
     Wex = O.exact_block_importance(res["Qp"], res["Kp"], qoff, koff)
     assert np.allclose(Wex[np.diff(qoff) > 0].sum(1), 1, atol=1e-12)
+
+
+# ------------------------------------------- query-centroid estimate -----
+def test_query_centroid_estimate_equals_pama_for_constant_blocks():
+    # Sec. 4.1: the query-centroid gap is driven by the within-block query
+    # covariance; with identical queries in every block it vanishes, and the
+    # estimate is PAMA itself.  Rows sum to one; empty query blocks are zero.
+    d = 8
+    Kp = rng(60).standard_normal((50, d))
+    koff = np.array([0, 9, 9, 31, 50])
+    c, n = O.block_centroids(Kp, koff)
+    base = rng(61).standard_normal((3, d)).astype(np.float32).astype(np.float64)
+    sizes = [4, 0, 7, 2]
+    Qp = np.concatenate([np.repeat(base[min(u, 2):min(u, 2) + 1], s, 0)
+                         for u, s in enumerate(sizes)])
+    qoff = np.concatenate([[0], np.cumsum(sizes)])
+    Wc = O.query_centroid_estimate(Qp, qoff, c, n)
+    Wp = O.pama(Qp, qoff, c, n)
+    assert np.abs(Wc - Wp).max() < 1e-15
+    assert np.all(Wc[1] == 0)
+    nz = np.array(sizes) > 0
+    assert np.abs(Wc[nz].sum(axis=1) - 1).max() < 1e-14
+    assert np.all(Wc[:, 1] == 0)  # the empty key block gets no weight
+
+
+def test_query_centroid_estimate_gap_is_second_order():
+    # Sec. 4.1 / App. C: W - W^centroid = 1/2 <H_phi(qbar), Sigma_Q> + higher
+    # order, so for the block {qbar + e delta, qbar - e delta} the gap shrinks
+    # by ~4 when e halves (a first-order mistake, e.g. scoring one query
+    # instead of the mean, would shrink it by ~2).
+    d = 8
+    Kp = rng(62).standard_normal((40, d)) * 2
+    koff = np.array([0, 10, 25, 40])
+    c, n = O.block_centroids(Kp, koff)
+    qbar = rng(63).standard_normal(d).astype(np.float32).astype(np.float64)
+    delta = rng(64).standard_normal(d)
+    gaps = []
+    for e in (2.0 ** -6, 2.0 ** -7):
+        Qp = np.stack([qbar + e * delta, qbar - e * delta])
+        Qp = Qp.astype(np.float32).astype(np.float64)
+        off = np.array([0, 2])
+        Wp = O.pama(Qp, off, c, n)
+        Wc = O.query_centroid_estimate(Qp, off, c, n)
+        gaps.append(np.abs(Wp - Wc).max())
+    assert 3.5 < gaps[0] / gaps[1] < 4.5
+
+
+def test_query_centroid_estimate_single_tokens_is_attention():
+    # singleton query and key blocks: qbar = q, c = k, log 1 = 0, so the
+    # estimate is the dense attention matrix (torch softmax).
+    N, d = 40, 8
+    Q = rng(65).standard_normal((N, d)).astype(np.float32).astype(np.float64)
+    K = rng(66).standard_normal((N, d)).astype(np.float32).astype(np.float64)
+    qp, kp = rng(67).permutation(N), rng(68).permutation(N)
+    off = np.arange(N + 1)
+    c, n = O.block_centroids(K[kp], off)
+    W = O.query_centroid_estimate(Q[qp], off, c, n)
+    A = torch.softmax(torch.from_numpy(Q) @ torch.from_numpy(K).T / math.sqrt(d), dim=1).numpy()
+    assert np.abs(W - A[np.ix_(qp, kp)]).max() < 1e-14
+
+
+# -------------------------------------------------- fixed-tile blocks -----
+@pytest.mark.parametrize("N,C", [(4096, 64), (75600, 1182), (100, 30), (129, 2), (7, 7)])
+def test_fixed_tile_offsets_partition(N, C):
+    # blocks of b = ceil(N / C) consecutive tokens, a shorter last block, and
+    # empty blocks only at the end; together a partition of range(N)
+    off = O.fixed_tile_offsets(N, C)
+    b = -(-N // C)
+    sz = np.diff(off)
+    assert len(off) == C + 1 and off[0] == 0 and off[-1] == N
+    assert np.all(sz >= 0) and np.all(sz <= b)
+    full = np.nonzero(sz)[0]
+    assert np.all(sz[full[:-1]] == b) and np.all(sz[full[-1] + 1:] == 0)
+    assert len(full) == -(-N // b)
+
+
+def test_fixed_tiles_end_to_end_pins():
+    # fixed tiles with every key block kept: dense attention (torch SDPA);
+    # with one token per block (C = N): W^ is the exact attention mass.
+    N, d = 96, 8
+    r = rng(69)
+    Q, K, V = (r.standard_normal((N, d)) for _ in range(3))
+    out = O.park_head(Q, K, V, 12, 12, 3, "topk", 1.0, blocks="fixed")
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q)[None], torch.from_numpy(K)[None], torch.from_numpy(V)[None])[0]
+    assert np.abs(out["O"] - ref.numpy()).max() < 1e-12
+    assert np.array_equal(out["q"]["offsets"], np.arange(13) * 8)
+    Qs, Ks = (x.astype(np.float32).astype(np.float64) for x in (Q[:24], K[:24]))
+    one = O.park_head(Qs, Ks, V[:24], 24, 24, 2, "topk", 0.5, blocks="fixed")
+    A = torch.softmax(torch.from_numpy(Qs) @ torch.from_numpy(Ks).T / math.sqrt(d), 1).numpy()
+    assert np.abs(one["W"] - A[np.ix_(one["q"]["perm"], one["k"]["perm"])]).max() < 1e-13
