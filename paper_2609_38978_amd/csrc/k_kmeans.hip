@@ -116,19 +116,22 @@ __global__ void k_seed_centroids(const T* __restrict__ X, const int* __restrict_
 // parts (three planes of H*C*D), b_v in float, |w_v| rounded up and the
 // |b_v| term of the error bound (see k_assign_fast).
 template <int D>
-__global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
+__global__ __launch_bounds__(1024) void k_prep(const double* __restrict__ mu,
                                               const double* __restrict__ Gbar, int C,
                                               double* __restrict__ w, double* __restrict__ b,
                                               bf16_t* __restrict__ w3,
                                               size_t plane, float* __restrict__ b32, int Cpad,
                                               float* __restrict__ wn, float* __restrict__ eb,
                                               float* __restrict__ bmax) {
-  constexpr int CB = 16, NG = 256 / D, PER = CB / NG;
+  // 1024 threads: D lanes per centroid group, 16 / (1024 / D) centroids per
+  // thread, so each thread's float64 chain over the D columns stays short
+  constexpr int NT = 1024, CB = 16, NG = NT / D, PER = CB / NG;
+  static_assert(PER >= 1 && CB % NG == 0, "centroid groups");
   __shared__ double ms[CB][D];
   __shared__ double ws[CB][D + 1];
   __shared__ float fnl[CB], fel[CB];
   const int h = blockIdx.y, v0 = blockIdx.x * CB, tid = threadIdx.x;
-  for (int e = tid; e < CB * D; e += 256) {
+  for (int e = tid; e < CB * D; e += NT) {
     const int r = e / D, a = e % D;
     ms[r][a] = (v0 + r < C) ? mu[((size_t)h * C + v0 + r) * D + a] : 0.0;
   }
@@ -168,8 +171,9 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
     }
   }
   __syncthreads();
-  // b_v and |w_v|^2: 16 lanes per centroid, partial sums added in a fixed tree
-  {
+  // b_v and |w_v|^2: 16 lanes per centroid (the first four wavefronts),
+  // partial sums added in a fixed tree
+  if (tid < 256) {
     constexpr int LPC = 256 / CB;
     const int r = tid / LPC, sub = tid % LPC;
     double s = 0.0, n2 = 0.0;
@@ -202,7 +206,7 @@ __global__ __launch_bounds__(256) void k_prep(const double* __restrict__ mu,
   __syncthreads();
   float fn = tid < CB ? fnl[tid] : 0.0f, fe = tid < CB ? fel[tid] : 0.0f;
   if (b32 && blockIdx.x == gridDim.x - 1)  // padding centroids: score +inf, no error term
-    for (int v = C + tid; v < Cpad; v += 256) {
+    for (int v = C + tid; v < Cpad; v += NT) {
       b32[(size_t)h * Cpad + v] = INFINITY;
       wn[(size_t)h * Cpad + v] = 0.0f;
       eb[(size_t)h * Cpad + v] = 0.0f;
@@ -1131,7 +1135,7 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
   rg = rg > max_tiles ? max_tiles : rg;
   for (int t = 0; t < T_; ++t) {
     const int nbm = (C + 15) / 16;
-    PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3(nbm, H), dim3(256), 0, st,
+    PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3(nbm, H), dim3(1024), 0, st,
                 (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane, fast ? kb.b32 : nullptr, kmeans_cpad(C),
                 fast ? kb.wn : nullptr,
                 fast ? kb.eb : nullptr, kb.hmax);
