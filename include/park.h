@@ -158,6 +158,12 @@ park_status park_workspace_size(const park_dims* dims, int32_t CQ, int32_t CK, s
  *                              may be NULL)
  *   Xt_out   [H][N][d] float   transformed points X R (QRKC, may be NULL;
  *                              diagnostic, not needed by the hot path)
+ * Metric (App. D): the k-means needs only Gbar -- its quadratic form
+ * (k - mu)^T Gbar (k - mu) is the squared distance of both the Cholesky and
+ * the symmetric-square-root realisation -- so any positive semidefinite Gbar
+ * works, including a rank-deficient one (alpha = eps = 0 with rank-deficient
+ * queries).  The Cholesky factor is taken only when R_out or Xt_out is given;
+ * then a Gbar that is not positive definite is PARK_ERR_NUMERIC (park_check).
  * Initialisation: the first C entries of a Fisher-Yates shuffle of the token
  * indices driven by SplitMix64 seeded with seed ^ (0x9E3779B97F4A7C15 *
  * (2*h + side + 1)).  Labels are exact argmins of the float64 distances

@@ -102,6 +102,27 @@ def query_metric(Q: np.ndarray, alpha: float = 0.05, eps: float = 1e-6, s_min: f
     return {"G": G, "s": s, "Gbar": Gbar, "R": R}
 
 
+def query_metric_sqrt(Q: np.ndarray, alpha: float = 0.05, eps: float = 1e-6,
+                      s_min: float = 1e-12):
+    """The same Gbar with its symmetric square root (App. D).
+
+    Gbar = U Lambda U^T (eigh), Gbar^(1/2) = U Lambda^(1/2) U^T; eigenvalues
+    that rounding leaves below zero are taken as zero.  Unlike the Cholesky
+    factor it exists for a rank-deficient Gbar.  k~ = Gbar^(1/2) k, and since
+    the root is symmetric the row form is K~ = K Gbar^(1/2).
+    """
+    Q = np.asarray(Q, dtype=np.float64)
+    L, d = Q.shape
+    G = (Q.T @ Q) / L
+    G = (G + G.T) / 2.0
+    s = max(np.trace(G) / d, s_min)
+    eye = np.eye(d)
+    Gbar = (1.0 - alpha) * G + alpha * s * eye + eps * s * eye
+    lam, U = np.linalg.eigh(Gbar)
+    S = (U * np.sqrt(np.maximum(lam, 0.0))) @ U.T
+    return {"G": G, "s": s, "Gbar": Gbar, "R": S}
+
+
 def transform_keys(K: np.ndarray, R: np.ndarray) -> np.ndarray:
     """Row form of k~ = R^T k (Eq. (12)): K~ = K R."""
     return np.asarray(K, dtype=np.float64) @ R
@@ -339,9 +360,14 @@ def cluster_queries(Q, C, T, seed, head):
     return {"labels": z, "perm": perm, "offsets": off, "mu": mu, "init": init}
 
 
-def cluster_keys(K, Q, C, T, seed, head, alpha=0.05, eps=1e-6, s_min=1e-12):
-    """QRKC (Alg. 3): k-means on K R, with Gbar = R R^T from the queries."""
-    met = query_metric(Q, alpha, eps, s_min)
+def cluster_keys(K, Q, C, T, seed, head, alpha=0.05, eps=1e-6, s_min=1e-12,
+                 realisation="cholesky"):
+    """QRKC (Alg. 3): k-means on K R, with Gbar = R R^T from the queries.
+
+    realisation "sqrt" uses the symmetric square root instead of the
+    Cholesky factor (App. D): the same distances, and defined for a
+    rank-deficient Gbar."""
+    met = (query_metric if realisation == "cholesky" else query_metric_sqrt)(Q, alpha, eps, s_min)
     Kt = transform_keys(K, met["R"])
     init = init_indices(Kt.shape[0], C, seed, head, side=1)
     z, mu = kmeans(Kt, C, T, init)

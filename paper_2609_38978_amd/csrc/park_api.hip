@@ -251,7 +251,7 @@ static park_status check_ws(void* ws, size_t ws_bytes, size_t need) {
 // on one device cannot swap each other's events.
 struct SideStream {
   hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr, gbar = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   std::mutex mu;  // held while a call queues its work (the events are shared)
 };
 static std::mutex g_side_mu;
@@ -274,9 +274,9 @@ static SideStream* side_stream(hipStream_t st) {
     if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
       return nullptr;
     hipStream_t s2 = nullptr;
-    hipEvent_t e[3] = {nullptr, nullptr, nullptr};
+    hipEvent_t e[2] = {nullptr, nullptr};
     if (hipStreamCreateWithFlags(&s2, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    for (int i = 0; i < 3; ++i)
+    for (int i = 0; i < 2; ++i)
       if (hipEventCreateWithFlags(&e[i], hipEventDisableTiming) != hipSuccess) {
         for (int j = 0; j < i; ++j) hipEventDestroy(e[j]);
         hipStreamDestroy(s2);
@@ -285,7 +285,6 @@ static SideStream* side_stream(hipStream_t st) {
     a.s = s2;
     a.fork = e[0];
     a.join = e[1];
-    a.gbar = e[2];
   }
   return &a;
 }
@@ -419,8 +418,11 @@ park_status park_cluster_keys(const void* X, const void* Qmetric, const park_dim
   hipStream_t st = (hipStream_t)stream;
   Carver cv(ws);
   PARK_TRY(launch_clear_status(cv.take<int>(64), st));
+  // the k-means needs only Gbar (any positive semidefinite one: its quadratic
+  // form is the symmetric-square-root realisation); the Cholesky factor is
+  // taken, and must exist, only when R or X R is asked for
   return cluster_body(X, Qmetric, *dims, C, T, seed, side, metric, alpha, eps, s_min, labels, perm,
-                      offsets, R_out, Xt_out, ws, st);
+                      offsets, R_out, Xt_out, ws, st, nullptr, (R_out || Xt_out) ? 7 : 3);
 }
 
 park_status park_gather_rows(const void* X, const int32_t* perm, const park_dims* dims, void* Xp,
@@ -556,8 +558,10 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
     const ClusterWs cq = carve_cluster(rc, H, N, D, p->CQ);
     const ClusterWs ck = carve_cluster(rc, H, N, D, p->CK);
     // queued in this order so that both streams get work early: the key
-    // side's metric Gbar, the whole query side and then the factor of Gbar
-    // (side stream), the key side's k-means (which needs only Gbar)
+    // side's metric Gbar, the whole query side (side stream), the key side's
+    // k-means.  The k-means needs only Gbar, whose quadratic form is the
+    // symmetric-square-root realisation of the metric, so no factor is taken
+    // and a rank-deficient (positive semidefinite) Gbar is fine
     SideStream* side = side_stream(st);
     hipStream_t sq = side ? side->s : st;
     std::unique_lock<std::mutex> lk;
@@ -569,15 +573,9 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
     park_status r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha,
                                  p->eps, p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr,
                                  nullptr, ws, st, &ck, 1);
-    if (side) PARK_TRY(ev_record(side->gbar, st));
     if (r == PARK_OK)
       r = cluster_body(Q, nullptr, *dims, p->CQ, p->T, p->seed, 0, PARK_METRIC_EUCLID, 0, 0, 1,
                        nullptr, s->q_perm, s->q_offsets, nullptr, nullptr, ws, sq, &cq);
-    if (side) PARK_TRY(ev_wait(sq, side->gbar));
-    if (r == PARK_OK)
-      r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha, p->eps,
-                       p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr, nullptr, ws, sq, &ck,
-                       4);
     if (r == PARK_OK)
       r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha, p->eps,
                        p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr, nullptr, ws, st, &ck,

@@ -335,8 +335,9 @@ def test_numeric_failure_is_reported():
     Q = torch.zeros(H, N, d, device="cuda")
     Q[..., :3] = torch.randn(H, N, 3, device="cuda")
     K = torch.randn(H, N, d, device="cuda")
+    # (only the Cholesky factor needs positive definiteness: ask for it)
     out = P.park_cluster_keys(K, 8, 2, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q, alpha=0.0,
-                              eps=0.0)
+                              eps=0.0, want_R=True)
     with pytest.raises(P.ParkError) as ei:
         P.park_check(out["ws"])
     assert ei.value.status == P.PARK_ERR_NUMERIC
@@ -401,3 +402,37 @@ def test_retrieval_float64_work_items(sizes):
     nd, nb = PT.compare_masks(Wo, n, np.diff(offs), "topk", param, kvc.cpu().numpy()[0],
                               kvi.cpu().numpy()[0])
     assert nb == 0 and nd == 0
+
+
+@pytest.mark.parametrize("dtype,N,d,C", [("fp32", 256, 64, 8), ("bf16", 2048, 128, 32)])
+def test_rank_deficient_metric_clusters_like_the_square_root(dtype, N, d, C):
+    # App. D: the symmetric square root realises the metric when Gbar is
+    # rank deficient; the k-means (which uses Gbar's quadratic form) runs and
+    # matches the oracle's square-root path label for label (up to exempt
+    # near-ties).  Queries span three feature directions, no shrinkage.
+    r = np.random.default_rng(11)
+    q = np.zeros((1, N, d), dtype=np.float32)
+    q[0, :, :3] = r.standard_normal((N, 3))
+    k = (r.standard_normal((1, N, d)) * 2).astype(np.float32)
+    Q, K = PT.to_dev(q, dtype), PT.to_dev(k, dtype)
+    qh = PT.np64(Q)[0]
+    kh = PT.np64(K)[0]
+    T = 4
+    print(f"[rank-deficient {dtype} N={N} d={d} C={C}]", flush=True)
+    out = P.park_cluster_keys(K, C, T, seed=5, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q,
+                              alpha=0.0, eps=0.0)
+    P.park_check(out["ws"])
+    lab = out["labels"][0].cpu().numpy()
+    res = O.cluster_keys(kh, qh, C, T, 5, 0, alpha=0.0, eps=0.0, realisation="sqrt")
+    n_mis, n_bad, worst = PT.label_flips(res["Kt"], res["mu"], lab, res["labels"])
+    print(f"label mismatches={n_mis} not-exempt={n_bad} worst-gap={worst:.3g}")
+    assert n_bad == 0
+    p2, o2 = O.stable_argsort(lab, C)
+    assert np.array_equal(out["perm"][0].cpu().numpy(), p2)
+    assert np.array_equal(out["offsets"][0].cpu().numpy(), o2)
+    # and the whole layer runs on the same metric
+    prm = P.make_params(C, C, T=T, select="topk", ratio=0.25, alpha=0.0, eps=0.0, seed=5)
+    ws = P.workspace(Q, C, C)
+    Og, st = P.park_forward(Q, K, K, prm, ws=ws)
+    P.park_check(ws)
+    assert np.array_equal(st["k_perm"][0].cpu().numpy(), out["perm"][0].cpu().numpy())

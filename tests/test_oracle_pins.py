@@ -540,3 +540,44 @@ def test_fixed_tiles_end_to_end_pins():
     one = O.park_head(Qs, Ks, V[:24], 24, 24, 2, "topk", 0.5, blocks="fixed")
     A = torch.softmax(torch.from_numpy(Qs) @ torch.from_numpy(Ks).T / math.sqrt(d), 1).numpy()
     assert np.abs(one["W"] - A[np.ix_(one["q"]["perm"], one["k"]["perm"])]).max() < 1e-13
+
+
+# -------------------------------------- symmetric-square-root metric -----
+def test_sqrt_realisation_same_distances_and_rank_deficient():
+    # App. D: |Gbar^(1/2) delta|^2 = delta^T Gbar delta = |R^T delta|^2, and
+    # the square root exists where Cholesky does not (rank-deficient Gbar).
+    r = rng(70)
+    Q = r.standard_normal((300, 12)) @ np.diag(np.linspace(0.2, 3.0, 12))
+    ch, sq = O.query_metric(Q), O.query_metric_sqrt(Q)
+    S = sq["R"]
+    assert np.array_equal(ch["Gbar"], sq["Gbar"])
+    assert np.abs(S - S.T).max() == 0 or np.abs(S - S.T).max() < 1e-14
+    assert np.abs(S @ S - sq["Gbar"]).max() < 1e-12 * np.abs(sq["Gbar"]).max()
+    delta = r.standard_normal((20, 12))
+    qf = np.einsum("nd,de,ne->n", delta, sq["Gbar"], delta)
+    assert np.allclose((delta @ S) ** 2 @ np.ones(12), qf, rtol=1e-12)
+    assert np.allclose(((delta @ ch["R"]) ** 2).sum(1), qf, rtol=1e-12)
+    # three informative feature directions, no shrinkage: rank 3
+    Qd = np.zeros((200, 10))
+    Qd[:, :3] = r.standard_normal((200, 3))
+    with pytest.raises(np.linalg.LinAlgError):
+        O.query_metric(Qd, alpha=0.0, eps=0.0)
+    m = O.query_metric_sqrt(Qd, alpha=0.0, eps=0.0)
+    assert np.linalg.matrix_rank(m["R"], tol=1e-10) == 3
+    assert np.abs(m["R"] @ m["R"] - m["Gbar"]).max() < 1e-12
+    d2 = r.standard_normal((15, 10))
+    assert np.allclose(((d2 @ m["R"]) ** 2).sum(1),
+                       np.einsum("nd,de,ne->n", d2, m["Gbar"], d2), rtol=1e-10, atol=1e-13)
+
+
+def test_sqrt_and_cholesky_cluster_alike():
+    # the two realisations give the same QRKC objective (App. D), hence the
+    # same k-means labels on well-separated data
+    r = rng(71)
+    cen = r.standard_normal((6, 8)) * 6
+    K = np.repeat(cen, 20, 0) + r.standard_normal((120, 8)) * 0.3
+    Q = r.standard_normal((120, 8))
+    a = O.cluster_keys(K, Q, 6, 5, 3, 0)
+    b = O.cluster_keys(K, Q, 6, 5, 3, 0, realisation="sqrt")
+    assert np.array_equal(a["labels"], b["labels"])
+    assert np.array_equal(a["perm"], b["perm"])
