@@ -240,6 +240,22 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
                          const park_params* params, int32_t reuse, const park_state* state,
                          void* O, void* ws, size_t ws_bytes, void* stream);
 
+/* Recomputation schedule across denoising steps (Sec. 5.2 "Clustering and
+ * Reuse Strategy"; App. "Clustering and Sparse-Mask Reuse"): the clustering
+ * and the mask are computed at the steps of the set `steps` and reused at the
+ * steps in between.  Host-only, touches no device.
+ *   step       denoising step index >= 0
+ *   steps      [n_steps] strictly increasing step indices >= 0 (host memory)
+ *   reuse_out  receives PARK_RECOMPUTE when step is in `steps`,
+ *              PARK_REUSE_CLUSTERS_AND_MASK after the first of them, and
+ *              PARK_STEP_DENSE before it (no clustering or mask exists yet:
+ *              the caller runs dense attention, the warm-up of the schedule).
+ * PARK_ERR_INVALID_ARG for a null pointer, n_steps < 1, a negative step or a
+ * schedule that is not strictly increasing. */
+#define PARK_STEP_DENSE (-1)
+park_status park_schedule_step(int32_t step, const int32_t* steps, int32_t n_steps,
+                               int32_t* reuse_out);
+
 /* Synchronises `stream`, returns the sticky device status recorded in the
  * workspace `ws` (PARK_OK or PARK_ERR_NUMERIC) and clears it. */
 park_status park_check(void* ws, void* stream);

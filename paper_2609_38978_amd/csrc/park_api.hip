@@ -619,6 +619,27 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
                           p->out_dtype, carve_attn_plan(ws, H, N, p->CQ), st);
 }
 
+park_status park_schedule_step(int32_t step, const int32_t* steps, int32_t n_steps,
+                               int32_t* reuse_out) {
+  g_err[0] = 0;
+  if (!steps || !reuse_out) return fail(PARK_ERR_INVALID_ARG, "steps / reuse_out is NULL");
+  if (n_steps < 1) return fail(PARK_ERR_INVALID_ARG, "the schedule needs at least one step");
+  if (step < 0) return fail(PARK_ERR_INVALID_ARG, "step %d is negative", step);
+  for (int i = 0; i < n_steps; ++i) {
+    if (steps[i] < 0) return fail(PARK_ERR_INVALID_ARG, "schedule entry %d is negative", i);
+    if (i > 0 && steps[i] <= steps[i - 1])
+      return fail(PARK_ERR_INVALID_ARG, "schedule is not strictly increasing at entry %d", i);
+  }
+  int32_t mode = PARK_STEP_DENSE;
+  if (step >= steps[0]) {
+    mode = PARK_REUSE_CLUSTERS_AND_MASK;
+    for (int i = 0; i < n_steps; ++i)
+      if (steps[i] == step) mode = PARK_RECOMPUTE;
+  }
+  *reuse_out = mode;
+  return PARK_OK;
+}
+
 park_status park_check(void* ws, void* stream) {
   g_err[0] = 0;
   PARK_TRY(check_ptr(ws, "workspace"));

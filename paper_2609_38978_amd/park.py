@@ -30,7 +30,7 @@ EXPORTS = (
     "park_workspace_size", "park_cluster_keys", "park_gather_rows", "park_block_centroids",
     "park_retrieve_blocks", "park_block_sparse_attn", "park_forward", "park_check",
     "park_status_string", "park_last_error", "park_profile_enable", "park_profile_reset",
-    "park_profile_read",
+    "park_profile_read", "park_schedule_step",
 )
 
 
@@ -83,6 +83,7 @@ def lib():
         "park_forward": [vp, vp, vp, pd, C.POINTER(Params), i32, C.POINTER(State), vp, vp, sz,
                          vp],
         "park_check": [vp, vp],
+        "park_schedule_step": [i32, C.POINTER(C.c_int32), i32, C.POINTER(C.c_int32)],
         "park_status_string": [i32],
         "park_last_error": [],
         "park_profile_enable": [i32],
@@ -250,6 +251,18 @@ def park_forward(Q, K, V, params: Params, reuse: int = PARK_RECOMPUTE, state: di
     _check(lib().park_forward(_ptr(Q), _ptr(K), _ptr(V), C.byref(dims), C.byref(params), reuse,
                               C.byref(s), _ptr(out), _ptr(ws), ws.numel(), _stream()))
     return out, state
+
+
+PARK_STEP_DENSE = -1
+
+
+def park_schedule_step(step: int, steps) -> int:
+    """Mode of denoising step `step` under the recomputation set `steps`:
+    PARK_RECOMPUTE, PARK_REUSE_CLUSTERS_AND_MASK or PARK_STEP_DENSE."""
+    arr = (C.c_int32 * len(steps))(*steps)
+    out = C.c_int32(0)
+    _check(lib().park_schedule_step(int(step), arr, len(steps), C.byref(out)))
+    return out.value
 
 
 def park_check(ws):

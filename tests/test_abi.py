@@ -135,3 +135,19 @@ def test_forward_argument_errors():
     assert fwd(ws_bytes=64) == P.PARK_ERR_WORKSPACE
     assert L.park_forward(FAKE, FAKE, FAKE, C.byref(d), None, 0, C.byref(st), FAKE, FAKE, 1 << 40,
                           None) == P.PARK_ERR_INVALID_ARG
+
+
+def test_schedule_step_host_logic():
+    # clustering and mask computed at the steps of the set, reused between
+    # them, dense attention before the first (no GPU involved)
+    sched = [10, 20, 30]
+    modes = [P.park_schedule_step(t, sched) for t in range(50)]
+    assert all(m == P.PARK_STEP_DENSE for m in modes[:10])
+    for t in range(10, 50):
+        want = P.PARK_RECOMPUTE if t in sched else P.PARK_REUSE_CLUSTERS_AND_MASK
+        assert modes[t] == want, t
+    assert P.park_schedule_step(0, [0]) == P.PARK_RECOMPUTE
+    for bad_step, bad_sched in ((-1, [3]), (4, [3, 3]), (4, [5, 2]), (4, [-1, 2]), (1, [])):
+        with pytest.raises(P.ParkError) as ei:
+            P.park_schedule_step(bad_step, bad_sched)
+        assert ei.value.status == P.PARK_ERR_INVALID_ARG

@@ -160,3 +160,45 @@ def test_forward_variants_match_oracle(tag):
         ok, werr = PT.w_error_ok(cfg.dtype, st["W"][i].cpu().numpy(), ref["W"])
         print(f"[{tag} h={h}] W max-abs err {werr:.3g}")
         assert ok
+
+
+def test_schedule_drives_recompute_and_reuse():
+    # a short denoising run with recomputation set {1, 3}: the mode of each
+    # step comes from park_schedule_step; reused steps keep the clustering and
+    # mask of the last recompute and match the oracle's attention on them
+    cfg = synth.CONFIGS["medium"].with_(grid=(2, 16, 32))
+    q, k, v = synth.make_layer(cfg, [0, 1])
+    C = cfg.C
+    prm = P.make_params(C, C, T=4, select="topp", topp=0.9)
+    Q0, V = PT.to_dev(q, cfg.dtype), PT.to_dev(v, cfg.dtype)
+    ws = P.workspace(Q0, C, C)
+    st = P.make_state(Q0, C, C)
+    sched = [1, 3]
+    qs, ks = q, k
+    last = None
+    for step in range(5):
+        mode = P.park_schedule_step(step, sched)
+        print(f"[schedule] step {step} mode {mode}", flush=True)
+        if step > 0:  # the next denoising step's drifted queries and keys
+            qs = np.stack([synth.perturb_head(cfg, h, qs[h], ks[h])[0] for h in range(2)])
+            ks = np.stack([synth.perturb_head(cfg, h, q[h], ks[h])[1] for h in range(2)])
+        if mode == P.PARK_STEP_DENSE:
+            assert step == 0
+            continue
+        Q, K = PT.to_dev(qs, cfg.dtype), PT.to_dev(ks, cfg.dtype)
+        Og, st = P.park_forward(Q, K, V, prm, reuse=mode, state=st, ws=ws)
+        P.park_check(ws)
+        if mode == P.PARK_RECOMPUTE:
+            last = (st["q_perm"].clone(), st["kv_index"].clone())
+            continue
+        assert mode == P.PARK_REUSE_CLUSTERS_AND_MASK and step in (2, 4)
+        assert torch.equal(st["q_perm"], last[0]) and torch.equal(st["kv_index"], last[1])
+        for i in range(2):
+            qp = st["q_perm"][i].cpu().numpy()
+            kp = st["k_perm"][i].cpu().numpy()
+            Oref = O.block_sparse_attention(
+                PT.np64(Q)[i][qp], PT.np64(K)[i][kp], v[i][kp], st["q_offsets"][i].cpu().numpy(),
+                st["k_offsets"][i].cpu().numpy(),
+                PT.rows_from_csr(st["kv_count"][i].cpu().numpy(), st["kv_index"][i].cpu().numpy()),
+                qp)
+            assert np.abs(PT.np64(Og)[i] - Oref).max() <= 2e-2
