@@ -115,17 +115,18 @@ __global__ void k_seed_centroids(const T* __restrict__ X, const int* __restrict_
 // given the fast-path operands are written too: w_v split into three bf16
 // parts (three planes of H*C*D), b_v in float, |w_v| rounded up and the
 // |b_v| term of the error bound (see k_assign_fast).
-template <int D>
-__global__ __launch_bounds__(1024) void k_prep(const double* __restrict__ mu,
+template <int D, int NT>
+__global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
                                               const double* __restrict__ Gbar, int C,
                                               double* __restrict__ w, double* __restrict__ b,
                                               bf16_t* __restrict__ w3,
                                               size_t plane, float* __restrict__ b32, int Cpad,
                                               float* __restrict__ wn, float* __restrict__ eb,
                                               float* __restrict__ bmax) {
-  // 1024 threads: D lanes per centroid group, 16 / (1024 / D) centroids per
-  // thread, so each thread's float64 chain over the D columns stays short
-  constexpr int NT = 1024, CB = 16, NG = NT / D, PER = CB / NG;
+  // NT threads: D lanes per centroid group, 16 / (NT / D) centroids per
+  // thread.  1024 threads shorten each thread's float64 chain over the D
+  // columns (small grids); 256 read the metric rows fewer times (large grids)
+  constexpr int CB = 16, NG = NT / D, PER = CB / NG;
   static_assert(PER >= 1 && CB % NG == 0, "centroid groups");
   __shared__ double ms[CB][D];
   __shared__ double ws[CB][D + 1];
@@ -1135,10 +1136,16 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
   rg = rg > max_tiles ? max_tiles : rg;
   for (int t = 0; t < T_; ++t) {
     const int nbm = (C + 15) / 16;
-    PARK_LAUNCH("kmeans_prep", k_prep<D>, dim3(nbm, H), dim3(1024), 0, st,
-                (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane, fast ? kb.b32 : nullptr, kmeans_cpad(C),
-                fast ? kb.wn : nullptr,
-                fast ? kb.eb : nullptr, kb.hmax);
+    if ((long)nbm * H < 512)
+      PARK_LAUNCH("kmeans_prep", (k_prep<D, 1024>), dim3(nbm, H), dim3(1024), 0, st,
+                  (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane,
+                  fast ? kb.b32 : nullptr, kmeans_cpad(C), fast ? kb.wn : nullptr,
+                  fast ? kb.eb : nullptr, kb.hmax);
+    else
+      PARK_LAUNCH("kmeans_prep", (k_prep<D, 256>), dim3(nbm, H), dim3(256), 0, st,
+                  (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane,
+                  fast ? kb.b32 : nullptr, kmeans_cpad(C), fast ? kb.wn : nullptr,
+                  fast ? kb.eb : nullptr, kb.hmax);
     if constexpr (fast) {
       if (C >= 512)
         PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 2>), dim3((N + kmeans_tile - 1) / kmeans_tile, H),
