@@ -32,8 +32,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="medium",
-                    help="synthetic layer: tiny | medium | wan | hunyuan")
+    ap.add_argument("--workload", default="hunyuan",
+                    help="synthetic layer: tiny | medium | wan | hunyuan (default: the "
+                         "HunyuanVideo-shaped layer, the largest single-GPU configuration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches only (no HIP graph replay)")
@@ -51,8 +52,9 @@ def parse():
                     help="blocks = k-means clusters, or fixed chunks of the cluster order")
     ap.add_argument("--key-metric", default="qrkc", choices=["qrkc", "euclid"],
                     help="key clustering: QRKC, or Euclidean k-means (the 'w/o QRKC' ablation)")
-    ap.add_argument("--cpu-heads", type=int, default=4,
-                    help="heads of the layer the oracle runs for the CPU baseline")
+    ap.add_argument("--cpu-heads", type=int, default=None,
+                    help="heads of the layer the oracle runs for the CPU baseline (default: 4 "
+                         "below 50k tokens per head, else 1: about 10-30 s of host work)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB (float32 negation, "
                          "read once, written once) five times: the known-size kernel that "
@@ -160,14 +162,32 @@ def kernel_work(name, cfg, st, C):
     return None
 
 
-def cpu_baseline(cfg, q, k, v, nheads, variant):
-    import numpy as np
-    from oracle import park_oracle as O
+def host_info():
+    """CPU model, logical CPUs, CPUs this process may run on, BLAS threads."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = None
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        threads = os.cpu_count()
+        blas = None
+    return {"cpu_model": model, "os_cpu_count": os.cpu_count(), "affinity": affinity,
+            "blas_threads": blas}
+
+
+def cpu_baseline(cfg, q, k, v, nheads, variant):
+    from oracle import park_oracle as O
+    info = host_info()
     mode = cfg.select
     param = cfg.ratio if mode == "topk" else cfg.topp
     t0 = time.perf_counter()
@@ -176,10 +196,12 @@ def cpu_baseline(cfg, q, k, v, nheads, variant):
                     **variant)
     dt = time.perf_counter() - t0
     ms_layer = dt * 1e3 * cfg.H / nheads
-    return {"value": round(ms_layer, 3), "unit": "ms per layer", "cores": int(threads),
+    cores = info["blas_threads"] or info["affinity"] or os.cpu_count()
+    return {"value": round(ms_layer, 3), "unit": "ms per layer", "cores": int(cores),
             "kind": "oracle",
             "sample": f"{nheads} of {cfg.H} heads of the {cfg.name} layer (full N), "
-                      f"whole PARK forward in float64 NumPy, scaled x{cfg.H / nheads:g}"}
+                      f"whole PARK forward in float64 NumPy ({dt:.1f} s), scaled x{cfg.H / nheads:g}",
+            **info}
 
 
 def main():
@@ -339,7 +361,8 @@ def main():
            "wall_s": round(wall, 3), "stages": stages, "stage_roofline": stage_roof,
            "roofline": roof}
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, q, k, v, min(args.cpu_heads, cfg.H), variant)
+        nh = args.cpu_heads if args.cpu_heads is not None else (4 if cfg.N < 50000 else 1)
+        res["cpu_baseline"] = cpu_baseline(cfg, q, k, v, min(nh, cfg.H), variant)
     print(json.dumps(res), flush=True)
 
 

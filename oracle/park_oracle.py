@@ -454,3 +454,154 @@ def exact_log_mass(Qp, Kp, k_offsets) -> np.ndarray:
             m = Z[:, a:b].max(axis=1)
             S[:, v] = m + np.log(np.exp(Z[:, a:b] - m[:, None]).sum(axis=1))
     return S
+
+
+# --------------------------------------------------------------------------
+# mismatch diagnostics (App. A "Direct Evaluation of Retrieval Mismatches",
+# App. B "Key-Space and QK-Score Approximation Errors"); reported on
+# synthetic layers, never on the hot path
+# --------------------------------------------------------------------------
+def block_means(Kp, offsets) -> np.ndarray:
+    """Float64 mean of the keys of every block (0 for an empty block)."""
+    Kp = np.asarray(Kp, dtype=np.float64)
+    C = len(offsets) - 1
+    c = np.zeros((C, Kp.shape[1]))
+    for v in range(C):
+        a, b = int(offsets[v]), int(offsets[v + 1])
+        if b > a:
+            c[v] = Kp[a:b].sum(axis=0) / (b - a)
+    return c
+
+
+def tv_error(W_hat, W, q_sizes) -> float:
+    """Attention-weight TV error of one head (App. A, M1).
+
+    E_TV = sum_u (n_u / L) * (1/2) sum_v |W^_uv - W_uv|: the total-variation
+    distance between the estimated and the exact block-weight distribution of
+    each query block, weighted by the block's share of the L queries.
+    """
+    W_hat = np.asarray(W_hat, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    n = np.asarray(q_sizes, dtype=np.float64)
+    L = n.sum()
+    per_block = 0.5 * np.abs(W_hat - W).sum(axis=1)
+    return float((n / L * per_block).sum())
+
+
+def centred_log_mass_rmse(S_star, S_hat) -> float:
+    """Mean centred log-mass RMSE of one head (App. A, M2).
+
+    Delta_iv = S*_iv - S^_iv on the nonempty key blocks (the columns where
+    S* is finite); delta_iv = Delta_iv minus its mean over those blocks (a
+    per-query offset does not change a softmax); E_LM = (1/L) sum_i
+    sqrt(mean_v delta_iv^2).
+    """
+    S_star = np.asarray(S_star, dtype=np.float64)
+    S_hat = np.asarray(S_hat, dtype=np.float64)
+    valid = np.isfinite(S_star[0])
+    Delta = S_star[:, valid] - S_hat[:, valid]
+    delta = Delta - Delta.mean(axis=1, keepdims=True)
+    return float(np.sqrt((delta ** 2).mean(axis=1)).mean())
+
+
+def log_mass_estimate(Qp, c, n) -> np.ndarray:
+    """S^_iv = q_i . c_v / sqrt(d) + log n_v with float64 centroids c (Eq. (8));
+    -inf for an empty block."""
+    Qp = np.asarray(Qp, dtype=np.float64)
+    S = (Qp @ np.asarray(c, dtype=np.float64).T) / math.sqrt(Qp.shape[1])
+    n = np.asarray(n)
+    with np.errstate(divide="ignore"):
+        logn = np.where(n > 0, np.log(np.maximum(n, 1).astype(np.float64)), -np.inf)
+    return S + logn[None, :]
+
+
+def key_space_errors(K, Q, labels, c):
+    """Raw-key MSE and QK-score squared error of a key clustering (App. B).
+
+    D_key = (1/L_K) sum_j |k_j - c_v(j)|^2 (not divided by d);
+    D_QK = (1/(L_Q L_K)) sum_i sum_j [q_i . (k_j - c_v(j)) / sqrt(d)]^2.
+    ``c`` are the clusters' centroids in the original key space.  Returns
+    (D_key, D_QK); the double sum is taken over query chunks.
+    """
+    K = np.asarray(K, dtype=np.float64)
+    Q = np.asarray(Q, dtype=np.float64)
+    R = K - np.asarray(c, dtype=np.float64)[np.asarray(labels)]
+    Lk, d = K.shape
+    Lq = Q.shape[0]
+    d_key = float((R ** 2).sum() / Lk)
+    tot = 0.0
+    for a in range(0, Lq, 512):
+        E = (Q[a:a + 512] @ R.T) / math.sqrt(d)
+        tot += float((E ** 2).sum())
+    return d_key, tot / (Lq * Lk)
+
+
+def query_centroid_full_keys(Qp, q_offsets, Kp, k_offsets) -> np.ndarray:
+    """W^_uv = phi_v(qbar_u) with every original key (App. A, the query-centroid
+    error with full keys): the block's mean query attends over all keys and
+    the weights of each key block are summed.  Rows of empty query blocks are
+    zero."""
+    Qp = np.asarray(Qp, dtype=np.float64)
+    Kp = np.asarray(Kp, dtype=np.float64)
+    CQ, CK = len(q_offsets) - 1, len(k_offsets) - 1
+    W = np.zeros((CQ, CK))
+    for u in range(CQ):
+        a, b = int(q_offsets[u]), int(q_offsets[u + 1])
+        if b == a:
+            continue
+        qbar = Qp[a:b].sum(axis=0) / (b - a)
+        p = softmax_rows((qbar[None, :] @ Kp.T) / math.sqrt(Qp.shape[1]))[0]
+        for v in range(CK):
+            W[u, v] = p[int(k_offsets[v]):int(k_offsets[v + 1])].sum()
+    return W
+
+
+def mismatch_report(Q, K, CQ, CK, T, seed=0, head=0, alpha=0.05, eps=1e-6, s_min=1e-12):
+    """The App. A / App. B diagnostics of one head on given Q, K.
+
+    M1: Euclidean query and key partitions; TV of PAMA (per-query), of the
+    query-centroid estimate, and of the query centroid with full keys, each
+    against the exact block importance (Eq. (3)).  M2: all original queries;
+    centred log-mass RMSE under the Euclidean and the QRKC key partition,
+    each against the exact log-mass of its own partition (Eq. (6)).  App. B:
+    D_key and D_QK of both key partitions.  Everything in float64.
+    """
+    Q = np.asarray(Q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    N = Q.shape[0]
+    cq = cluster_queries(Q, CQ, T, seed, head)
+    ke = kmeans(K, CK, T, init_indices(N, CK, seed, head, side=1))[0]
+    kq = cluster_keys(K, Q, CK, T, seed, head, alpha, eps, s_min)["labels"]
+    out = {}
+    # M1 on the Euclidean partitions
+    Qp = Q[cq["perm"]]
+    perm_e, off_e = stable_argsort(ke, CK)
+    Kp = K[perm_e]
+    c = block_means(Kp, off_e)
+    n = np.diff(off_e)
+    W_exact = exact_block_importance(Qp, Kp, cq["offsets"], off_e)
+    qs = np.diff(cq["offsets"])
+    S_hat = log_mass_estimate(Qp, c, n)
+    W_per = np.zeros_like(W_exact)
+    W_cen = np.zeros_like(W_exact)
+    for u in range(CQ):
+        a, b = int(cq["offsets"][u]), int(cq["offsets"][u + 1])
+        if b > a:
+            W_per[u] = softmax_rows(S_hat[a:b]).sum(axis=0) / (b - a)
+            qbar = Qp[a:b].sum(axis=0) / (b - a)
+            W_cen[u] = softmax_rows(log_mass_estimate(qbar[None, :], c, n))[0]
+    W_full = query_centroid_full_keys(Qp, cq["offsets"], Kp, off_e)
+    out["tv_per_query"] = tv_error(W_per, W_exact, qs)
+    out["tv_query_centroid"] = tv_error(W_cen, W_exact, qs)
+    out["tv_query_centroid_full_keys"] = tv_error(W_full, W_exact, qs)
+    # M2 and App. B for both key partitions
+    for name, z in (("euclid", ke), ("qrkc", kq)):
+        perm, off = stable_argsort(z, CK)
+        Kp = K[perm]
+        c = block_means(Kp, off)
+        out[f"log_mass_rmse_{name}"] = centred_log_mass_rmse(
+            exact_log_mass(Q, Kp, off), log_mass_estimate(Q, c, np.diff(off)))
+        d_key, d_qk = key_space_errors(K, Q, z, c)
+        out[f"d_key_{name}"] = d_key
+        out[f"d_qk_{name}"] = d_qk
+    return out

@@ -20,8 +20,9 @@ Recipe (per configuration and head ``h``):
   video tokens; their Q, K and V are N(0,1) (drawn last, Q then K then V).
 * bf16 configurations are rounded to bfloat16 with round-to-nearest-even;
   the arrays returned here are float32 holding bf16-representable values.
-* Re-use probe: the second call of the sweep perturbs Q and K by
-  N(0, 0.05^2) drawn from ``SeedSequence([0, h, 1])``.
+* Re-use probe: step s >= 1 of a denoising run perturbs the previous
+  step's Q and K by N(0, 0.05^2) drawn from ``SeedSequence([0, h, s])``
+  (the second call of the sweep is step 1).
 
 The paper measures on activations of Wan2.1-14B and HunyuanVideo generating
 720p video from VBench prompts; those models and prompts are not available,
@@ -147,9 +148,11 @@ def make_layer(cfg: LayerConfig, heads=None, workers: int = 8):
     return tuple(out)
 
 
-def perturb_head(cfg: LayerConfig, h: int, q: np.ndarray, k: np.ndarray, sigma: float = 0.05):
-    """Re-use probe: Q and K of the next diffusion step, drifted by N(0, sigma^2)."""
-    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([cfg.seed, h, 1])))
+def perturb_head(cfg: LayerConfig, h: int, q: np.ndarray, k: np.ndarray, sigma: float = 0.05,
+                 step: int = 1):
+    """Re-use probe: Q and K of diffusion step ``step`` (>= 1), the previous
+    step's drifted by N(0, sigma^2) from ``SeedSequence([seed, h, step])``."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([cfg.seed, h, step])))
     q2 = q + np.float32(sigma) * rng.standard_normal(q.shape, dtype=np.float32)
     k2 = k + np.float32(sigma) * rng.standard_normal(k.shape, dtype=np.float32)
     if cfg.dtype == "bf16":

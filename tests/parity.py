@@ -49,19 +49,34 @@ def label_flips(X: np.ndarray, mu: np.ndarray, z_gpu: np.ndarray, z_or: np.ndarr
 
 def mask_row_exempt(w: np.ndarray, valid: np.ndarray, mode: str, param: float,
                     got: set, want: set) -> bool:
-    """A differing mask row is acceptable only at a near-tie of the oracle."""
-    diff = got ^ want
-    if not diff:
+    """A differing mask row is acceptable only at a near-tie of the oracle.
+
+    Top-p: when the oracle's cumulative mass at the cut lies within 1e-6 p
+    of p, the next block (order[m]) may be added; when the mass one block
+    earlier does, the last kept block (order[m-1]) may be dropped -- only that
+    block.  Beyond that, a near-tie in value can only swap blocks: the two
+    rows must keep as many blocks, and every block in which they differ must
+    have an oracle weight within 1e-6 (relative) of the cut weight (or both
+    below FLT_MIN).
+    """
+    if got == want:
         return True
     sel, order, m = O.select_row(w, valid, mode, param)
     cut = w[order[m - 1]] if m > 0 else 0.0
-    if mode == "topp":
+    got, want = set(got), set(want)
+    if mode == "topp" and m > 0:
         cs = np.cumsum(w[order])
-        if abs(cs[m - 1] - param) <= REL_GAP * param:
-            return True
+        if abs(cs[m - 1] - param) <= REL_GAP * param and m < len(order):
+            extra = int(order[m])
+            if extra in got and extra not in want:
+                got.discard(extra)
         if m >= 2 and abs(cs[m - 2] - param) <= REL_GAP * param:
-            return True
-    for v in diff:
+            last = int(order[m - 1])
+            if last in want and last not in got:
+                want.discard(last)
+    if len(got) != len(want):
+        return False
+    for v in got ^ want:
         if w[v] < FLT_MIN and cut < FLT_MIN:
             continue
         if abs(w[v] - cut) > REL_GAP * max(cut, FLT_MIN):

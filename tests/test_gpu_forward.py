@@ -179,9 +179,10 @@ def test_schedule_drives_recompute_and_reuse():
     for step in range(5):
         mode = P.park_schedule_step(step, sched)
         print(f"[schedule] step {step} mode {mode}", flush=True)
-        if step > 0:  # the next denoising step's drifted queries and keys
-            qs = np.stack([synth.perturb_head(cfg, h, qs[h], ks[h])[0] for h in range(2)])
-            ks = np.stack([synth.perturb_head(cfg, h, q[h], ks[h])[1] for h in range(2)])
+        if step > 0:  # the next denoising step's drifted queries and keys (fresh drift per step)
+            pq = [synth.perturb_head(cfg, h, qs[h], ks[h], step=step) for h in range(2)]
+            qs = np.stack([a for a, _ in pq])
+            ks = np.stack([b for _, b in pq])
         if mode == P.PARK_STEP_DENSE:
             assert step == 0
             continue

@@ -581,3 +581,207 @@ def test_sqrt_and_cholesky_cluster_alike():
     b = O.cluster_keys(K, Q, 6, 5, 3, 0, realisation="sqrt")
     assert np.array_equal(a["labels"], b["labels"])
     assert np.array_equal(a["perm"], b["perm"])
+
+
+# ------------------------------------- recall and exact log-mass pins -----
+def _brute_attention(Q, K):
+    """Row softmax of Q K^T / sqrt(d) by explicit loops over math.exp."""
+    n, d = Q.shape
+    A = np.zeros((n, K.shape[0]))
+    for i in range(n):
+        s = [sum(Q[i, t] * K[j, t] for t in range(d)) / math.sqrt(d) for j in range(K.shape[0])]
+        m = max(s)
+        e = [math.exp(x - m) for x in s]
+        z = sum(e)
+        A[i] = [x / z for x in e]
+    return A
+
+
+def test_recall_all_blocks_kept_is_one():
+    Qp = rng(70).standard_normal((30, 8))
+    Kp = rng(71).standard_normal((40, 8))
+    qoff = np.array([0, 7, 7, 30])
+    koff = np.array([0, 5, 5, 22, 40])
+    every = [np.array([0, 1, 2, 3]), np.array([], dtype=np.int64), np.array([0, 1, 2, 3])]
+    assert O.recall(Qp, Kp, qoff, koff, every) == pytest.approx(1.0, abs=1e-14)
+    assert O.recall(Qp, Kp, qoff, koff, [np.array([], dtype=np.int64)] * 3) == 0.0
+
+
+def test_recall_hand_sized_brute_force():
+    # Eq. (4): the attention mass inside the mask over the total (= number of
+    # queries, since each row of A sums to one), on a case where the two query
+    # blocks keep different, asymmetric key blocks: swapping the roles of u
+    # and v, or summing the wrong block's columns, changes the value
+    Q = np.array([[1.0, 0.0], [0.8, 0.3], [0.0, 1.0], [-0.5, 0.9], [0.2, -0.7]])
+    K = np.array([[2.0, 0.0], [0.0, 1.5], [-1.0, 1.0], [0.5, 0.5]])
+    qoff = np.array([0, 2, 5])
+    koff = np.array([0, 1, 3, 4])
+    rows = [np.array([0]), np.array([1, 2])]
+    A = _brute_attention(Q, K)
+    want = (A[0:2, 0:1].sum() + A[2:5, 1:3].sum() + A[2:5, 3:4].sum()) / 5.0
+    assert O.recall(Q, K, qoff, koff, rows) == pytest.approx(want, rel=1e-13)
+    swapped = (A[0:2, 1:4].sum() + A[2:5, 0:1].sum()) / 5.0
+    assert abs(want - swapped) > 0.05
+
+
+def test_recall_block_size_one_is_kept_attention_mass():
+    # singleton blocks: recall is the sum of the kept entries of A over N
+    Q = rng(72).standard_normal((6, 3))
+    K = rng(73).standard_normal((6, 3))
+    off = np.arange(7)
+    rows = [np.array([0, 2]), np.array([5]), np.array([1, 3, 4]), np.array([0]),
+            np.array([2, 3]), np.array([])]
+    A = _brute_attention(Q, K)
+    want = sum(A[i, j] for i, r in enumerate(rows) for j in r) / 6.0
+    assert O.recall(Q, K, off, off, [np.asarray(r, dtype=np.int64) for r in rows]) == \
+        pytest.approx(want, rel=1e-13)
+
+
+def test_exact_log_mass_closed_forms():
+    d = 4
+    Q = rng(74).standard_normal((9, d))
+    # a singleton block: S* is the raw scaled score
+    K1 = rng(75).standard_normal((3, d))
+    S = O.exact_log_mass(Q, K1, np.array([0, 1, 2, 3]))
+    assert np.allclose(S, Q @ K1.T / math.sqrt(d), rtol=0, atol=1e-14)
+    # n identical keys: S* = score + log n
+    k = rng(76).standard_normal(d)
+    Kid = np.tile(k, (5, 1))
+    S = O.exact_log_mass(Q, Kid, np.array([0, 5]))
+    assert np.allclose(S[:, 0], Q @ k / math.sqrt(d) + math.log(5), rtol=0, atol=1e-13)
+    # two keys c +- eps e: S* - S^ = log cosh(eps q.e / sqrt(d)) (the key-side
+    # error of Sec. 4.2 in closed form), S^ = q.c / sqrt(d) + log 2
+    c, e, eps = rng(77).standard_normal(d), rng(78).standard_normal(d), 0.7
+    K2 = np.stack([c + eps * e, c - eps * e])
+    S = O.exact_log_mass(Q, K2, np.array([0, 2]))[:, 0]
+    Shat = Q @ c / math.sqrt(d) + math.log(2)
+    b = eps * (Q @ e) / math.sqrt(d)
+    assert np.allclose(S - Shat, np.log(np.cosh(b)), rtol=0, atol=1e-13)
+    # empty block
+    S = O.exact_log_mass(Q, K2, np.array([0, 0, 2]))
+    assert np.isneginf(S[:, 0]).all()
+
+
+# ------------------------------------------- mismatch diagnostics pins -----
+def test_tv_error_hand_example():
+    # block 0 (3 queries): rows [1,0,0] vs [0,1,0] -> TV 1; block 1 (1 query):
+    # [0.5,0.5,0] vs [0.5,0.25,0.25] -> TV 0.25; empty block 2 has no weight
+    Wh = np.array([[1.0, 0.0, 0.0], [0.5, 0.5, 0.0], [0.0, 0.0, 0.0]])
+    W = np.array([[0.0, 1.0, 0.0], [0.5, 0.25, 0.25], [0.3, 0.3, 0.4]])
+    assert O.tv_error(Wh, W, np.array([3, 1, 0])) == pytest.approx(3 / 4 * 1 + 1 / 4 * 0.25)
+    assert O.tv_error(W, W, np.array([3, 1, 0])) == 0.0
+    # symmetric, in [0, 1] for distributions
+    assert O.tv_error(W, Wh, np.array([3, 1, 0])) == O.tv_error(Wh, W, np.array([3, 1, 0]))
+
+
+def test_tv_zero_when_pama_is_exact():
+    # identical keys in every key block make PAMA the exact block importance
+    # (Eq. (3)), so its TV error vanishes; the query-centroid estimate does not
+    d = 6
+    Q = rng(80).standard_normal((24, d))
+    base = rng(81).standard_normal((4, d))
+    Kp = np.repeat(base, [3, 5, 1, 7], axis=0)
+    koff = np.array([0, 3, 8, 9, 16])
+    qoff = np.array([0, 10, 24])
+    c = O.block_means(Kp, koff)
+    n = np.diff(koff)
+    W = O.exact_block_importance(Q, Kp, qoff, koff)
+    S = O.log_mass_estimate(Q, c, n)
+    Wp = np.stack([O.softmax_rows(S[a:b]).mean(0) for a, b in ((0, 10), (10, 24))])
+    assert O.tv_error(Wp, W, np.diff(qoff)) < 1e-14
+    Wc = O.query_centroid_full_keys(Q, qoff, Kp, koff)
+    assert O.tv_error(Wc, W, np.diff(qoff)) > 1e-3
+
+
+def test_query_centroid_full_keys_brute_force():
+    Q = rng(82).standard_normal((7, 3))
+    K = rng(83).standard_normal((9, 3))
+    qoff = np.array([0, 4, 4, 7])
+    koff = np.array([0, 2, 6, 9])
+    W = O.query_centroid_full_keys(Q, qoff, K, koff)
+    for u, (a, b) in enumerate(((0, 4), (4, 4), (4, 7))):
+        if b == a:
+            assert np.all(W[u] == 0)
+            continue
+        A = _brute_attention(Q[a:b].mean(0, keepdims=True), K)[0]
+        assert np.allclose(W[u], [A[0:2].sum(), A[2:6].sum(), A[6:9].sum()], atol=1e-14)
+    # with one query per block it is the exact block importance
+    off = np.arange(8)
+    assert np.allclose(O.query_centroid_full_keys(Q, off, K, koff),
+                       O.exact_block_importance(Q, K, off, koff), atol=1e-14)
+
+
+def test_centred_log_mass_rmse_closed_forms():
+    # hand example: one query with Delta = [3, 1] (mean 2, delta = [1, -1]) and
+    # one with Delta = [0, 4] (delta = [-2, 2]): E_LM = (1 + 2) / 2
+    Sstar = np.array([[3.0, 1.0, -np.inf], [0.0, 4.0, -np.inf]])
+    Shat = np.zeros((2, 3))
+    Shat[:, 2] = -np.inf
+    assert O.centred_log_mass_rmse(Sstar, Shat) == pytest.approx(1.5)
+    # a per-query offset does not count
+    assert O.centred_log_mass_rmse(Sstar, Shat + np.array([[7.0], [-2.0]])) == pytest.approx(1.5)
+    # two-key blocks c_v +- eps e_v: Delta = log cosh(eps q.e_v / sqrt(d)) exactly
+    d = 4
+    Q = rng(84).standard_normal((5, d))
+    cs = rng(85).standard_normal((3, d))
+    es = rng(86).standard_normal((3, d))
+    Kp = np.concatenate([np.stack([cs[v] + 0.5 * es[v], cs[v] - 0.5 * es[v]]) for v in range(3)])
+    off = np.array([0, 2, 4, 6])
+    Sstar = O.exact_log_mass(Q, Kp, off)
+    Shat = O.log_mass_estimate(Q, O.block_means(Kp, off), np.diff(off))
+    Dl = np.log(np.cosh(0.5 * (Q @ es.T) / math.sqrt(d)))
+    want = np.sqrt(((Dl - Dl.mean(1, keepdims=True)) ** 2).mean(1)).mean()
+    assert O.centred_log_mass_rmse(Sstar, Shat) == pytest.approx(want, rel=1e-12)
+    # singleton blocks: the estimate is exact
+    Sstar = O.exact_log_mass(Q, Kp, np.arange(7))
+    Shat = O.log_mass_estimate(Q, Kp, np.ones(6, dtype=int))
+    assert O.centred_log_mass_rmse(Sstar, Shat) < 1e-14
+
+
+def test_key_space_errors_brute_force_and_objective():
+    d = 3
+    Q = rng(87).standard_normal((6, d))
+    K = rng(88).standard_normal((8, d))
+    z = np.array([0, 1, 0, 2, 1, 1, 0, 2])
+    c = np.stack([K[z == v].mean(0) for v in range(3)])
+    dk, dq = O.key_space_errors(K, Q, z, c)
+    bk = sum(sum((K[j, t] - c[z[j], t]) ** 2 for t in range(d)) for j in range(8)) / 8
+    bq = sum(sum(Q[i, t] * (K[j, t] - c[z[j], t]) for t in range(d)) ** 2 / d
+             for i in range(6) for j in range(8)) / 48
+    assert dk == pytest.approx(bk, rel=1e-13) and dq == pytest.approx(bq, rel=1e-13)
+    # D_QK is the QRKC objective of Eq. (10) (metric G_Q = Q^T Q / L_Q,
+    # no stabilisation) divided by L_K d
+    G = Q.T @ Q / 6
+    J = sum((K[j] - c[z[j]]) @ G @ (K[j] - c[z[j]]) for j in range(8))
+    assert dq == pytest.approx(J / (8 * d), rel=1e-13)
+    # singletons: no error; one cluster: D_key is the total variance
+    assert O.key_space_errors(K, Q, np.arange(8), K) == (0.0, 0.0)
+    dk1, _ = O.key_space_errors(K, Q, np.zeros(8, dtype=int), K.mean(0, keepdims=True))
+    assert dk1 == pytest.approx(((K - K.mean(0)) ** 2).sum() / 8, rel=1e-13)
+
+
+def test_mismatch_directions():
+    # The paper's directional claims (App. A, App. B) where they must hold.
+    # (1) Clustered layer from the seeded generator: per-query PAMA has a far
+    # lower TV error than the query-centroid estimate (M1).
+    from paper_2609_38978_amd import synth
+    cfg = synth.CONFIGS["tiny"].with_(grid=(2, 16, 32))
+    q, k, _ = synth.make_head(cfg, 0)
+    rep = O.mismatch_report(q, k, cfg.C, cfg.C, 6)
+    print("generator", rep)
+    assert rep["tv_per_query"] < 0.5 * rep["tv_query_centroid"]
+    # (2) Queries spread along two directions only, keys in blobs: QRKC
+    # clusters keys by QK-score error, so it lowers D_QK and the centred
+    # log-mass error and raises the raw-key MSE relative to Euclidean k-means
+    # (M2, App. B).  With isotropic queries the two metrics nearly coincide.
+    r = rng(90)
+    d, N = 16, 768
+    basis = np.linalg.qr(r.standard_normal((d, 2)))[0]
+    Q = 3.0 * r.standard_normal((N, 2)) @ basis.T + 0.05 * r.standard_normal((N, d))
+    cent = 2.0 * r.standard_normal((24, d))
+    K = cent[r.integers(0, 24, N)] + 0.5 * r.standard_normal((N, d))
+    rep = O.mismatch_report(Q, K, 12, 24, 8)
+    print("anisotropic queries", rep)
+    assert rep["d_qk_qrkc"] < 0.5 * rep["d_qk_euclid"]
+    assert rep["d_key_qrkc"] > rep["d_key_euclid"]
+    assert rep["log_mass_rmse_qrkc"] < 0.5 * rep["log_mass_rmse_euclid"]
