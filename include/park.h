@@ -138,6 +138,15 @@ typedef struct park_state {
   float* W;            /* [H][CQ][CK] W^ (optional, may be NULL)  */
 } park_state;
 
+/* Byte sizes of the caller-allocated park_state buffers for these dims and
+ * block counts, in the order the members are declared (q_perm, k_perm,
+ * q_offsets, k_offsets, k_centroids, k_sizes, kv_count, kv_index, Qp, Kp,
+ * Vp, W): bytes[i] for member i, PARK_STATE_NBUF entries.  Host-only.
+ * PARK_ERR_INVALID_ARG if bytes is NULL or n < PARK_STATE_NBUF. */
+#define PARK_STATE_NBUF 12
+park_status park_state_sizes(const park_dims* dims, int32_t CQ, int32_t CK, size_t* bytes,
+                             int32_t n);
+
 /* Bytes of workspace any call below needs for these sizes (the maximum over
  * park_cluster_keys with C = max(CQ, CK), park_retrieve_blocks and
  * park_forward).  Host-only; never fails for valid dims. */
@@ -214,6 +223,11 @@ park_status park_retrieve_blocks(const void* Qp, const int32_t* q_offsets, const
  *   bf16 by round-to-nearest-even).  Rows of empty query blocks do not exist;
  *   every token is written exactly once; the rows of a query block with
  *   kv_count = 0 are written as zeros.
+ *   lse [H][N] float (may be NULL): the natural-log normaliser of each row,
+ *   log sum_j exp(q_i . k_j / sqrt(d)) over the same keys, in the original
+ *   token order like O (lse[h][q_perm[h][i]]); -inf for a row whose query
+ *   block selected no key.  It is what merges this output with attention
+ *   over other keys (the log-sum-exp of the two normalisers).
  *   ws: device workspace of at least park_workspace_size() bytes for these
  *   dims, CQ and CK (it holds the per-call work plan); PARK_ERR_WORKSPACE if
  *   smaller than the attention part of it. */
@@ -221,7 +235,7 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
                                    const int32_t* q_offsets, const int32_t* k_offsets,
                                    const int32_t* kv_count, const int32_t* kv_index,
                                    const int32_t* q_perm, const park_dims* dims, int32_t CQ,
-                                   int32_t CK, void* O, int32_t out_dtype, void* ws,
+                                   int32_t CK, void* O, int32_t out_dtype, float* lse, void* ws,
                                    size_t ws_bytes, void* stream);
 
 /* The whole layer: stages 1-4 on Q, K, V [H][N][d] (dtype), output O
@@ -255,6 +269,21 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
 #define PARK_STEP_DENSE (-1)
 park_status park_schedule_step(int32_t step, const int32_t* steps, int32_t n_steps,
                                int32_t* reuse_out);
+
+/* Hardware probes (used by tests of the error models behind the certified
+ * fast paths of park_cluster_keys and park_retrieve_blocks; not part of the
+ * forward).  Device pointers, asynchronous on `stream`.
+ *   park_probe_exp2: y[i] = 2^x[i] by the v_exp_f32 instruction the retrieval
+ *     and attention kernels use;  x, y [n] float, n >= 0.
+ *   park_probe_mfma_bf16: for each of nprob problems, C = C0 + A B as a chain
+ *     of K/16 v_mfma_f32_32x32x16_bf16 in increasing k (the score chains of
+ *     the k-means and PAMA kernels);  A [nprob][32][K] and Bt [nprob][32][K]
+ *     bf16 (Bt holds the columns of B), C0, C [nprob][32][32] float;  K a
+ *     positive multiple of 16, at most 4096.
+ * PARK_ERR_INVALID_ARG for a null or misaligned pointer or a bad size. */
+park_status park_probe_exp2(const float* x, float* y, int64_t n, void* stream);
+park_status park_probe_mfma_bf16(const uint16_t* A, const uint16_t* Bt, const float* C0, float* C,
+                                 int32_t nprob, int32_t K, void* stream);
 
 /* Synchronises `stream`, returns the sticky device status recorded in the
  * workspace `ws` (PARK_OK or PARK_ERR_NUMERIC) and clears it. */

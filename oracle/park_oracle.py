@@ -348,6 +348,29 @@ def block_sparse_attention(Qp, Kp, Vp, q_offsets, k_offsets, rows, q_perm) -> np
     return O
 
 
+def block_sparse_lse(Qp, Kp, q_offsets, k_offsets, rows, q_perm) -> np.ndarray:
+    """Natural-log normaliser of each row of the block-sparse attention.
+
+    lse_i = log sum_j exp(q_i . k_j / sqrt(d)) over the keys of the selected
+    key blocks of i's query block (the denominator of Eq. (2) renormalised over
+    the kept keys), stored at position q_perm[i]; -inf when nothing is kept.
+    """
+    Qp, Kp = (np.asarray(a, dtype=np.float64) for a in (Qp, Kp))
+    N, d = Qp.shape
+    out = np.full(N, -np.inf)
+    for u, sel in enumerate(rows):
+        a, b = int(q_offsets[u]), int(q_offsets[u + 1])
+        if b == a or len(sel) == 0:
+            continue
+        keys = np.concatenate([np.arange(k_offsets[v], k_offsets[v + 1]) for v in sel])
+        if len(keys) == 0:
+            continue
+        Z = (Qp[a:b] @ Kp[keys].T) / math.sqrt(d)
+        m = Z.max(axis=1)
+        out[np.asarray(q_perm[a:b])] = m + np.log(np.exp(Z - m[:, None]).sum(axis=1))
+    return out
+
+
 # --------------------------------------------------------------------------
 # whole head (Alg. 3 + Sec. 5.1 + Eq. (2))
 # --------------------------------------------------------------------------

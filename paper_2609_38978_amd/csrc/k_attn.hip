@@ -87,7 +87,8 @@ __global__ __launch_bounds__(256) void k_attn_valu(const T* __restrict__ Qp, con
                                                    const int* __restrict__ kv_count,
                                                    const int* __restrict__ kv_index,
                                                    const int* __restrict__ q_perm, int N, int CQ,
-                                                   int CK, OT* __restrict__ O) {
+                                                   int CK, OT* __restrict__ O,
+                                                   float* __restrict__ lse) {
   constexpr int RT = 32, KT = 32, TPR = 8, CPT = D / TPR, KPT = KT / TPR;
   __shared__ float qs[RT][D + 1];
   __shared__ float ks[KT][D + 1];
@@ -178,36 +179,15 @@ __global__ __launch_bounds__(256) void k_attn_valu(const T* __restrict__ Qp, con
         OT* o = O + ((size_t)h * N + dst) * D + sub * CPT;
 #pragma unroll
         for (int c = 0; c < CPT; ++c) store_out<OT>(o + c, acc[c] * inv);
+        // natural-log normaliser of the row: mrow is the largest scaled score
+        if (lse && sub == 0) lse[(size_t)h * N + dst] = lrow > 0.0f ? mrow + logf(lrow) : -INFINITY;
       }
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA kernel (v_mfma_f32_16x16x32_bf16).
-//
-// Work: each query block is cut into chunks of at most 64 rows (a plan built
-// on the device), one workgroup per chunk, so large blocks spread over many
-// compute units.  The chunks of one head run on one XCD (workgroups are
-// dealt to the 8 XCDs round-robin, so the linear id is remapped): that XCD's
-// L2 then holds the head's keys and values for all its query blocks.
-//
-// Per chunk, 4 wavefronts of 16 query rows walk the key stream (the selected
-// blocks' rows, concatenated) in KT-key tiles.  K and V tiles go straight
-// from HBM into an LDS ring with wave-wide LDS-DMA loads
-// (global_load_lds_dwordx4), row-major with an XOR swizzle of the 16-byte
-// chunks chosen so the reads below are free of bank conflicts; the next
-// tiles are in flight while tile t is computed.  Per tile and wavefront:
-//   S^T = K Q^T  (16 keys x 16 queries per MFMA): lane l holds keys
-//                16b + 4(l/16) + r of query l%16;
-//   O^T += V^T P^T: the probabilities are reused from registers as the B
-//                operand (k-slot 8g+r <-> key 32c+4g+r, 8g+4+r <-> 32c+16+4g+r)
-//                and the A operand (V^T) is read from the row-major V tile
-//                with the LDS transpose read ds_read_b64_tr_b16: within each
-//                16-lane group, lane j receives element j%4 of the 8 bytes
-//                addressed by lanes 4r + j/4, r = 0..3.
-// Softmax in base 2 on raw scores; each probability costs one FMA and one
-// v_exp_f32 and is rounded to bf16 (RNE) by the packed conversion.
+// bf16 MFMA path: operand and accumulator vector types, output stores.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -229,16 +209,9 @@ __device__ __forceinline__ void store_out4<bf16_t>(bf16_t* p, float a, float b, 
   *(uint2*)p = make_uint2(lo, hi);
 }
 
-// Chunk plan: plan[h][c] = {u, first row, end row, 0} for the c-th chunk (at
-// most 64 rows) of head h, {-1, 0, 0, 0} after the last one.  Chunks past
-// CPH (possible only for non-monotone offsets) are dropped.  One workgroup
-// of 1024 threads per head, CQ <= 2048.
-//
-// Query blocks are ordered by a MinHash of their selected key-block sets
-// (min over the selected ids of a fixed integer hash, ties by block id), so
-// blocks that select nearly the same key blocks get neighbouring chunks and
-// run at the same time on the same XCD, where their keys and values are
-// re-read from L2 instead of HBM.
+// MinHash of a selected key-block set: min over the selected ids of a fixed
+// integer hash (an avalanche mixer), used to order query blocks so that blocks
+// selecting nearly the same key blocks are neighbours.
 __device__ __forceinline__ uint32_t attn_hash(uint32_t v) {
   v ^= v >> 16;
   v *= 0x7feb352du;
@@ -248,155 +221,10 @@ __device__ __forceinline__ uint32_t attn_hash(uint32_t v) {
   return v;
 }
 
-__global__ __launch_bounds__(1024) void k_attn_plan(const int* __restrict__ q_offsets,
-                                                    const int* __restrict__ kv_count,
-                                                    const int* __restrict__ kv_index, int N,
-                                                    int CQ, int CK, int CPH,
-                                                    int4* __restrict__ plan) {
-  __shared__ int wsum[16];
-  __shared__ unsigned long long key[2048];
-  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int* qo = q_offsets + (size_t)h * (CQ + 1);
-  int4* ph = plan + (size_t)h * CPH;
-  // sort keys: (MinHash of the selected set, block id), one wavefront per
-  // block; SZ = the power of two the bitonic sort runs over (padding ~0 last)
-  int SZ = 2;
-  while (SZ < CQ) SZ <<= 1;
-  for (int u = wid; u < SZ; u += 16) {
-    unsigned long long kk = ~0ull;
-    if (u < CQ) {
-      const size_t row = (size_t)h * CQ + u;
-      const int n = min(max(kv_count[row], 0), CK);
-      const int* sel = kv_index + row * CK;
-      uint32_t mh = 0xffffffffu;
-      for (int j = lane; j < n; j += 64) mh = min(mh, attn_hash((uint32_t)sel[j]));
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) mh = min(mh, (uint32_t)__shfl_xor((int)mh, o, 64));
-      kk = ((unsigned long long)mh << 32) | (uint32_t)u;
-    }
-    if (lane == 0) key[u] = kk;
-  }
-  __syncthreads();
-  for (int len = 2; len <= SZ; len <<= 1)
-    for (int j = len >> 1; j > 0; j >>= 1) {
-#pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        const int i = tid + 1024 * k, ixj = i ^ j;
-        if (i < SZ && ixj > i) {
-          const unsigned long long x = key[i], y = key[ixj];
-          const bool up = (i & len) == 0;
-          if ((x > y) == up) {
-            key[i] = y;
-            key[ixj] = x;
-          }
-        }
-      }
-      __syncthreads();
-    }
-  // chunks of the query blocks in sorted order
-  int a[2], b[2], nc[2], uu[2];
-  int s = 0;
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int pos = 2 * tid + k;
-    const int u = pos < CQ ? (int)(uint32_t)key[pos] : -1;
-    uu[k] = u;
-    a[k] = b[k] = nc[k] = 0;
-    if ((unsigned)u < (unsigned)CQ) {
-      a[k] = min(max(qo[u], 0), N);
-      b[k] = min(max(qo[u + 1], a[k]), N);
-      nc[k] = (b[k] - a[k] + 63) >> 6;
-    }
-    s += nc[k];
-  }
-  int inc = s;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += y;
-  }
-  if (lane == 63) wsum[wid] = inc;
-  __syncthreads();
-  int pre = 0, total = 0;
-  for (int i = 0; i < 16; ++i) {
-    pre += i < wid ? wsum[i] : 0;
-    total += wsum[i];
-  }
-  int c = pre + inc - s;
-#pragma unroll
-  for (int k = 0; k < 2; ++k)
-    for (int i = 0; i < nc[k]; ++i, ++c)
-      if (c < CPH) ph[c] = make_int4(uu[k], a[k] + 64 * i, min(a[k] + 64 * i + 64, b[k]), 0);
-  for (int cc = total + tid; cc < CPH; cc += 1024) ph[cc] = make_int4(-1, 0, 0, 0);
-}
-
-// Stream table of one query block: ck[j] = {first stream position, first row
-// of Kp} of the j-th selected block (ids outside [0, nblk) are empty),
-// ck[n] = {stream length, -1}.  256 threads, n <= 2048.
-__device__ void stream_table(const int* __restrict__ sel, int n, int nblk,
-                             const int* __restrict__ koff, int2* ck, int* tmp) {
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  int x[8], st[8];
-  int s = 0;
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int i = tid * 8 + k;
-    x[k] = 0;
-    st[k] = -1;
-    if (i < n) {
-      const int v = sel[i];
-      if ((unsigned)v < (unsigned)nblk) {
-        st[k] = koff[v];
-        x[k] = max(0, koff[v + 1] - st[k]);
-      }
-    }
-    s += x[k];
-  }
-  int inc = s;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += y;
-  }
-  if (lane == 63) tmp[wid] = inc;
-  __syncthreads();
-  int run = inc - s;
-  for (int w = 0; w < wid; ++w) run += tmp[w];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int i = tid * 8 + k;
-    if (i < n) ck[i] = make_int2(run, st[k]);
-    run += x[k];
-    if (i == n - 1) ck[n] = make_int2(run, -1);
-  }
-  if (n == 0 && tid == 0) ck[0] = make_int2(0, -1);
-  __syncthreads();
-}
-
-template <int D, int KT>
-struct AttnTile {
-  static constexpr int CPR = D / 8;          // 16-byte chunks per row
-  static constexpr int RPI = 64 / CPR;       // rows one wave-wide DMA fills
-  static constexpr int NI = KT / (4 * RPI);  // DMAs per wavefront, tensor and tile
-  static constexpr int ELEMS = KT * D;       // bf16 elements of one K or V tile
-  static_assert(NI >= 1 && NI * 4 * RPI == KT, "tile shape");
-};
-
-// XOR swizzles of the 16-byte chunk index within a row (an involution).
-// K: the 16 rows one S^T MFMA reads land in 16 different bank groups.
-// V: the 8 rows each half-wavefront's transpose read touches do too.
+// XOR swizzle of the 16-byte chunk index within a K row (an involution): the
+// 16 rows one S^T MFMA reads land in 16 different bank groups.
 template <int D>
 __device__ __forceinline__ int swz_k(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
-template <int D>
-__device__ __forceinline__ int swz_v(int r) { return D == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); }
-
-// key-tile length and LDS ring depth of the MFMA kernel
-#ifndef PARK_ATTN_KT
-#define PARK_ATTN_KT 32
-#endif
-#ifndef PARK_ATTN_NS
-#define PARK_ATTN_NS 3
-#endif
 
 // One wave-wide LDS DMA: lane l's 16 bytes at g land at LDS byte address
 // lds + 16 l (lds wave-uniform).  Written as inline assembly so that the
@@ -416,226 +244,6 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-template <typename OT, int D, int KT, int NS>
-__global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t* __restrict__ Qp,
-                                                   const bf16_t* __restrict__ Kp,
-                                                   const bf16_t* __restrict__ Vp,
-                                                   const int* __restrict__ k_offsets,
-                                                   const int* __restrict__ kv_count,
-                                                   const int* __restrict__ kv_index,
-                                                   const int* __restrict__ q_perm,
-                                                   const int4* __restrict__ plan, int H, int N,
-                                                   int CQ, int CK, int CPH, float scale_log2,
-                                                   OT* __restrict__ O) {
-  using TS = AttnTile<D, KT>;
-  static_assert(KT % 32 == 0 && NS >= 2 && NS <= 4, "tile length / ring depth");
-  constexpr int KS = D / 32;    // k-steps of S
-  constexpr int DB = D / 16;    // 16-column blocks of O
-  constexpr int NB = KT / 16;   // 16-key blocks of S per tile
-  constexpr int NCK = KT / 32;  // 32-key steps of O per tile
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  bf16_t* Ks = (bf16_t*)smem;               // [NS][KT][D], swizzled chunks
-  bf16_t* Vs = Ks + NS * TS::ELEMS;         // [NS][KT][D], swizzled chunks
-  int2* ck = (int2*)(Vs + NS * TS::ELEMS);  // [CK + 1]
-  __shared__ int tmp[4];
-
-  // XCD-aware work item: XCD x (= blockIdx % 8) takes items [x*per, (x+1)*per)
-  const int nitems = H * CPH;
-  const int per = (nitems + 7) >> 3;
-  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
-  if (item >= nitems) return;
-  const int4 pc = plan[item];
-  if (pc.x < 0 || pc.x >= CQ) return;
-  const int h = item / CPH, u = pc.x;
-  const int r0 = min(max(pc.y, 0), N), r1 = min(max(pc.z, r0), min(r0 + 64, N));
-  if (r1 <= r0) return;
-  const int* koff = k_offsets + (size_t)h * (CK + 1);
-  const size_t row = (size_t)h * CQ + u;
-  int nsel = kv_count[row];
-  nsel = nsel < 0 ? 0 : (nsel > CK ? CK : nsel);
-  const int tid = threadIdx.x;
-  stream_table(kv_index + row * CK, nsel, CK, koff, ck, tmp);
-  const int nk = ck[nsel].x;
-  const bf16_t* Qh = Qp + (size_t)h * N * D;
-  const bf16_t* Kh = Kp + (size_t)h * N * D;
-  const bf16_t* Vh = Vp + (size_t)h * N * D;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int l = tid & 63, g = l >> 4, c16 = l & 15;
-
-  // queries of this wavefront (B operand of S^T)
-  const int qr = r0 + 16 * w + c16;
-  const bool qvalid = qr < r1;
-  const bool wave_on = r0 + 16 * w < r1;
-  bf16x8_t qf[KS];
-#pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-    if (qvalid) raw = *(const uint4*)(Qh + (size_t)qr * D + 32 * s + 8 * g);
-    qf[s] = __builtin_bit_cast(bf16x8_t, raw);
-  }
-  // make the query loads complete here: otherwise the compiler's wait for
-  // them lands inside the tile loop, where it also drains the DMA ring
-#pragma unroll
-  for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qf[s]));
-
-  // DMA lanes: tile row rr[i], chunk position pch; a cursor into ck per row
-  const int pch = l % TS::CPR;
-  int rr[TS::NI], jj[TS::NI], cj[TS::NI], kj[TS::NI], src[TS::NI];
-  int2 nx[TS::NI];
-#pragma unroll
-  for (int i = 0; i < TS::NI; ++i) {
-    rr[i] = (w * TS::NI + i) * TS::RPI + l / TS::CPR;
-    jj[i] = 0;
-    cj[i] = 0;
-    kj[i] = ck[0].y;
-    nx[i] = ck[nsel > 0 ? 1 : 0];
-    src[i] = 0;
-  }
-  // Kp/Vp row of stream position t*KT + rr[i] (row 0 past the end: in bounds,
-  // its scores are masked)
-  auto advance = [&](int t) {
-#pragma unroll
-    for (int i = 0; i < TS::NI; ++i) {
-      const int pos = t * KT + rr[i];
-      while (pos >= nx[i].x && jj[i] + 1 < nsel) {
-        ++jj[i];
-        cj[i] = nx[i].x;
-        kj[i] = nx[i].y;
-        nx[i] = ck[jj[i] + 1];
-      }
-      const int r = kj[i] + (pos - cj[i]);
-      src[i] = (pos < nk && (unsigned)r < (unsigned)N) ? r : 0;
-    }
-  };
-  auto issue = [&](int slot) {
-    bf16_t* ks = Ks + slot * TS::ELEMS;
-    bf16_t* vs = Vs + slot * TS::ELEMS;
-#pragma unroll
-    for (int i = 0; i < TS::NI; ++i) {
-      const bf16_t* gk = Kh + (size_t)src[i] * D + 8 * (pch ^ swz_k<D>(rr[i]));
-      const bf16_t* gv = Vh + (size_t)src[i] * D + 8 * (pch ^ swz_v<D>(rr[i]));
-      const int off = (w * TS::NI + i) * 512;  // 1 KB per wave-wide DMA
-      lds_dma16(gk, lds_addr(ks + off));
-      lds_dma16(gv, lds_addr(vs + off));
-    }
-  };
-
-  float m = -INFINITY, lpart = 0.0f;
-  f32x4_t acc[DB];
-#pragma unroll
-  for (int b = 0; b < DB; ++b) acc[b] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-  // per-lane swizzle constants of the reads (independent of the key block)
-  const int swk = swz_k<D>(c16);
-  const int vr = 4 * g + (c16 >> 2);  // V row within a 32-key step (first read)
-  const int swv = swz_v<D>(vr);
-  const int vch = (c16 & 3) >> 1, vhalf = 4 * (c16 & 1);
-
-  // NS-slot ring: tiles t+1 .. t+NS-2 are in flight while tile t is computed;
-  // tile t+NS-1 is issued once every wavefront has finished tile t-1.
-  const int ntiles = (nk + KT - 1) / KT;
-#pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < ntiles) {
-      advance(p);
-      issue(p);
-    }
-  for (int t = 0; t < ntiles; ++t) {
-    const int next = t + NS - 1;
-    if (next < ntiles) advance(next);
-    // own DMAs of tile t done: the younger tiles still in flight may stay so
-    const int younger = min(NS - 2, ntiles - 1 - t);
-    if (NS >= 4 && younger >= 2) wait_vmcnt<2 * 2 * TS::NI>();
-    else if (NS >= 3 && younger >= 1) wait_vmcnt<2 * TS::NI>();
-    else wait_vmcnt<0>();
-    __syncthreads();  // tile t landed everywhere; tile t-1 consumed (its slot is free)
-    if (next < ntiles) issue(next % NS);
-    if (!wave_on) continue;
-    const bf16_t* ks = Ks + (t % NS) * TS::ELEMS;
-    const bf16_t* vs = Vs + (t % NS) * TS::ELEMS;
-    const int k0 = t * KT;
-    f32x4_t st[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      st[b] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-      const bf16_t* krow = ks + (16 * b + c16) * D;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const bf16x8_t a = *(const bf16x8_t*)(krow + 8 * ((4 * s + g) ^ swk));
-        st[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[s], st[b], 0, 0, 0);
-      }
-    }
-    if (k0 + KT > nk) {  // last tile: mask the keys past the end of the stream
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (k0 + 16 * b + 4 * g + r >= nk) st[b][r] = -INFINITY;
-    }
-    float tmax = st[0][0];
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, st[b][r]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(m, tmax);
-    if (__any(mnew != m)) {  // rescale only when some running maximum moved
-      const float alpha = __builtin_amdgcn_exp2f((m - mnew) * scale_log2);
-      lpart *= alpha;
-#pragma unroll
-      for (int b = 0; b < DB; ++b) acc[b] *= alpha;
-    }
-    m = mnew;
-    const float nms = -mnew * scale_log2;
-#pragma unroll
-    for (int c = 0; c < NCK; ++c) {
-      bf16x8_t pb;
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        const int b = 2 * c + hb;
-        float p[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          p[r] = __builtin_amdgcn_exp2f(fmaf(st[b][r], scale_log2, nms));
-          lpart += p[r];
-        }
-        const bf16x2_t lo = __builtin_convertvector(f32x2_t{p[0], p[1]}, bf16x2_t);
-        const bf16x2_t hi = __builtin_convertvector(f32x2_t{p[2], p[3]}, bf16x2_t);
-        pb[hb * 4 + 0] = lo[0];
-        pb[hb * 4 + 1] = lo[1];
-        pb[hb * 4 + 2] = hi[0];
-        pb[hb * 4 + 3] = hi[1];
-      }
-      const bf16_t* v1 = vs + (32 * c + vr) * D + vhalf;
-      const bf16_t* v2 = v1 + 16 * D;
-#pragma unroll
-      for (int mb = 0; mb < DB; ++mb) {
-        const int chk = 8 * ((2 * mb + vch) ^ swv);
-        const i16x4_t t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(v1 + chk));
-        const i16x4_t t2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(v2 + chk));
-        const i16x4_t a0 = t1, a1 = t2;
-        const bf16x8_t a = __builtin_bit_cast(
-            bf16x8_t, (short __attribute__((ext_vector_type(8)))){a0[0], a0[1], a0[2], a0[3],
-                                                                  a1[0], a1[1], a1[2], a1[3]});
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, acc[mb], 0, 0, 0);
-      }
-    }
-  }
-  float lsum = lpart + __shfl_xor(lpart, 16, 64);
-  lsum += __shfl_xor(lsum, 32, 64);
-  if (qvalid) {
-    const int dst = q_perm[(size_t)h * N + qr];
-    if ((unsigned)dst < (unsigned)N) {
-      const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
-      OT* o = O + ((size_t)h * N + dst) * D + 4 * g;
-#pragma unroll
-      for (int mb = 0; mb < DB; ++mb)
-        store_out4<OT>(o + 16 * mb, acc[mb][0] * inv, acc[mb][1] * inv, acc[mb][2] * inv,
-                       acc[mb][3] * inv);
-    }
-  }
 }
 
 // ------------------------------------------------------------------------
@@ -942,7 +550,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
     const int* __restrict__ kv_count, const int* __restrict__ kv_index,
     const int* __restrict__ q_perm, const int* __restrict__ order, const int* __restrict__ spre,
     const int4* __restrict__ grp, int H, int N, int CQ, int CK, int GPH, float scale_log2,
-    OT* __restrict__ O) {
+    OT* __restrict__ O, float* __restrict__ lse) {
   constexpr int KT = 32, NT = 64 * NW;
   constexpr int NSK = ATTN_KSLOTS, NSV = ATTN_KSLOTS + 1;  // K and V ring slots
   using TS = GrpTile<D, KT, NW>;
@@ -1292,6 +900,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
     const int dst = q_perm[(size_t)h * N + qr];
     if ((unsigned)dst < (unsigned)N) {
       const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+      // natural-log normaliser: the probabilities are exp2((s - m) scale_log2)
+      // of raw scores s, so sum_j exp(s_j / sqrt(d)) = exp(m / sqrt(d)) lsum
+      if (lse && hf == 0)
+        lse[(size_t)h * N + dst] =
+            lsum > 0.0f ? m * (scale_log2 * 0.69314718055994531f) + logf(lsum) : -INFINITY;
       OT* o = O + ((size_t)h * N + dst) * D + 4 * hf;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
@@ -1307,42 +920,17 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
 template <typename T, typename OT>
 static park_status attn_dispatch_d(const void* Qp, const void* Kp, const void* Vp, const int* qo,
                                    const int* ko, const int* kc, const int* ki, const int* qp,
-                                   int H, int N, int D, int CQ, int CK, void* O, hipStream_t st) {
+                                   int H, int N, int D, int CQ, int CK, void* O, float* lse,
+                                   hipStream_t st) {
   dim3 g(CQ, H);
   if (D == 128)
     PARK_LAUNCH("attn_valu", (k_attn_valu<T, OT, 128>), g, dim3(256), 0, st, (const T*)Qp,
-                (const T*)Kp, (const T*)Vp, qo, ko, kc, ki, qp, N, CQ, CK, (OT*)O);
+                (const T*)Kp, (const T*)Vp, qo, ko, kc, ki, qp, N, CQ, CK, (OT*)O, lse);
   else
     PARK_LAUNCH("attn_valu", (k_attn_valu<T, OT, 64>), g, dim3(256), 0, st, (const T*)Qp,
-                (const T*)Kp, (const T*)Vp, qo, ko, kc, ki, qp, N, CQ, CK, (OT*)O);
+                (const T*)Kp, (const T*)Vp, qo, ko, kc, ki, qp, N, CQ, CK, (OT*)O, lse);
   return PARK_OK;
 }
-
-int attn_chunks_per_head(int N, int CQ) { return CQ + (N + 63) / 64; }
-
-template <typename OT, int D, int KT, int NS>
-static park_status attn_mfma_launch(const void* Qp, const void* Kp, const void* Vp, const int* ko,
-                                    const int* kc, const int* ki, const int* qp,
-                                    const int4* plan, int H, int N, int CQ, int CK, int CPH,
-                                    float sl2, void* O, hipStream_t st) {
-  const size_t lds = (size_t)2 * NS * KT * D * sizeof(bf16_t) + (size_t)(CK + 1) * sizeof(int2);
-  // reserved once for the largest CK (2048), outside any stream capture that may follow
-  constexpr size_t lds_max = (size_t)2 * NS * KT * D * sizeof(bf16_t) + (size_t)2049 * sizeof(int2);
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)k_attn_mfma<OT, D, KT, NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)lds_max);
-  if (attr != hipSuccess) return fail(PARK_ERR_HIP, "attention: cannot reserve %zu bytes of LDS", lds);
-  // 8 * ceil(items / 8) workgroups: every item owns one (see the remap in the kernel)
-  const unsigned nwg = 8u * (((unsigned)H * (unsigned)CPH + 7u) / 8u);
-  PARK_LAUNCH("attn_mfma", (k_attn_mfma<OT, D, KT, NS>), dim3(nwg), dim3(256), lds, st,
-              (const bf16_t*)Qp, (const bf16_t*)Kp, (const bf16_t*)Vp, ko, kc, ki, qp, plan, H, N,
-              CQ, CK, CPH, sl2, (OT*)O);
-  return PARK_OK;
-}
-
-#ifndef PARK_ATTN_GROUP
-#define PARK_ATTN_GROUP 1
-#endif
 
 size_t attn_grp_offset(int H, int CQ);
 
@@ -1350,7 +938,7 @@ template <typename OT, int D, int NW>
 static park_status attn_grp_launch(const void* Qp, const void* Kp, const void* Vp, const int* qo,
                                    const int* ko, const int* kc, const int* ki, const int* qp,
                                    int H, int N, int CQ, int CK, void* plan, float sl2, void* O,
-                                   hipStream_t st) {
+                                   float* lse, hipStream_t st) {
   const int GPH = attn_groups_per_head(N, CQ);
   int* order = (int*)plan;
   int* spre = order + (size_t)H * CQ;
@@ -1369,32 +957,21 @@ static park_status attn_grp_launch(const void* Qp, const void* Kp, const void* V
   const unsigned nwg = 8u * (((unsigned)H * (unsigned)GPH + 7u) / 8u);
   PARK_LAUNCH("attn_mfma", (k_attn_grp<OT, D, NW>), dim3(nwg), dim3(64 * NW), lds, st,
               (const bf16_t*)Qp, (const bf16_t*)Kp, (const bf16_t*)Vp, qo, ko, kc, ki, qp, order,
-              spre, grp, H, N, CQ, CK, GPH, sl2, (OT*)O);
+              spre, grp, H, N, CQ, CK, GPH, sl2, (OT*)O, lse);
   return PARK_OK;
 }
 
 template <typename OT>
 static park_status attn_mfma_d(const void* Qp, const void* Kp, const void* Vp, const int* qo,
                                const int* ko, const int* kc, const int* ki, const int* qp, int H,
-                               int N, int D, int CQ, int CK, void* plan, void* O, hipStream_t st) {
+                               int N, int D, int CQ, int CK, void* plan, void* O, float* lse,
+                               hipStream_t st) {
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)D));
-#if PARK_ATTN_GROUP
   if (D == 128)
     return attn_grp_launch<OT, 128, ATTN_R / 32>(Qp, Kp, Vp, qo, ko, kc, ki, qp, H, N, CQ, CK,
-                                                  plan, sl2, O, st);
+                                                  plan, sl2, O, lse, st);
   return attn_grp_launch<OT, 64, ATTN_R / 32>(Qp, Kp, Vp, qo, ko, kc, ki, qp, H, N, CQ, CK, plan,
-                                              sl2, O, st);
-#else
-  const int CPH = attn_chunks_per_head(N, CQ);
-  int4* pl = (int4*)plan;
-  PARK_LAUNCH("attn_plan", k_attn_plan, dim3(H), dim3(1024), 0, st, qo, kc, ki, N, CQ, CK, CPH,
-              pl);
-  if (D == 128)
-    return attn_mfma_launch<OT, 128, PARK_ATTN_KT, PARK_ATTN_NS>(Qp, Kp, Vp, ko, kc, ki, qp, pl, H,
-                                                               N, CQ, CK, CPH, sl2, O, st);
-  return attn_mfma_launch<OT, 64, PARK_ATTN_KT, PARK_ATTN_NS>(Qp, Kp, Vp, ko, kc, ki, qp, pl, H, N,
-                                                              CQ, CK, CPH, sl2, O, st);
-#endif
+                                              sl2, O, lse, st);
 }
 
 // order [H][CQ], spre [H][CQ + 1], then the groups [H][GPH] at 16-byte alignment
@@ -1403,28 +980,27 @@ size_t attn_grp_offset(int H, int CQ) {
 }
 
 size_t attn_plan_bytes(int H, int N, int CQ) {
-  const size_t grp = attn_grp_offset(H, CQ) + (size_t)H * attn_groups_per_head(N, CQ) * sizeof(int4);
-  const size_t chunks = (size_t)H * attn_chunks_per_head(N, CQ) * sizeof(int4);
-  return grp > chunks ? grp : chunks;
+  return attn_grp_offset(H, CQ) + (size_t)H * attn_groups_per_head(N, CQ) * sizeof(int4);
 }
 
 park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,
                              const int* k_offsets, const int* kv_count, const int* kv_index,
                              const int* q_perm, int H, int N, int D, int dtype, int CQ, int CK,
-                             void* O, int out_dtype, void* plan, hipStream_t st) {
+                             void* O, int out_dtype, float* lse, void* plan,
+                             hipStream_t st) {
   if (dtype == PARK_BF16) {
     if (out_dtype == PARK_BF16)
       return attn_mfma_d<bf16_t>(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, H,
-                                 N, D, CQ, CK, plan, O, st);
+                                 N, D, CQ, CK, plan, O, lse, st);
     return attn_mfma_d<float>(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, H, N,
-                              D, CQ, CK, plan, O, st);
+                              D, CQ, CK, plan, O, lse, st);
   }
   // fp32 inputs: VALU kernel in fp32 (the contraction cannot use bf16 MFMA exactly)
   if (out_dtype == PARK_BF16)
     return attn_dispatch_d<float, bf16_t>(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index,
-                                          q_perm, H, N, D, CQ, CK, O, st);
+                                          q_perm, H, N, D, CQ, CK, O, lse, st);
   return attn_dispatch_d<float, float>(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index,
-                                       q_perm, H, N, D, CQ, CK, O, st);
+                                       q_perm, H, N, D, CQ, CK, O, lse, st);
 }
 
 }  // namespace park

@@ -111,7 +111,8 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ 
 // Symmetrise, scale and stabilise (Eq. (11)):
 //   Gbar = (1 - alpha) (G + G^T) / 2 + (alpha s + eps s) I,
 //   s = max(tr G / d, s_min) (trace summed in index order);
-// one workgroup per head.  A non-finite entry raises ST_NOT_SPD.
+// one workgroup per head.  A non-finite entry (non-finite queries) raises
+// ST_NONFINITE.
 template <int D>
 __global__ __launch_bounds__(256) void k_metric_gbar(const double* __restrict__ G, double alpha,
                                                      double eps, double s_min,
@@ -144,7 +145,7 @@ __global__ __launch_bounds__(256) void k_metric_gbar(const double* __restrict__ 
   }
   if (nf) bad = 1;
   __syncthreads();
-  if (tid == 0 && bad) raise_status(status, ST_NOT_SPD);
+  if (tid == 0 && bad) raise_status(status, ST_NONFINITE);
 }
 
 // Cholesky factor of Gbar = L L^T (R = L; x~ = R^T x); one workgroup per

@@ -461,7 +461,11 @@ __device__ void select64_row(const double* __restrict__ W64, const int* __restri
   int myvalid = 0;
   for (int e = tid; e < P; e += 256) {
     const bool ok = e < CK && k_sizes[(size_t)h * CK + e] > 0;
-    key[e] = ok ? W64[row * CK + e] : -1.0;
+    // a NaN weight (non-finite input, already reported) ranks as 0, as in the
+    // fast selection, so the order stays total and the kept prefix only holds
+    // valid ids
+    const double wv = ok ? W64[row * CK + e] : -1.0;
+    key[e] = ok ? (wv == wv ? wv : 0.0) : -1.0;
     id[e] = e;
     if (e < CK) flag[e] = 0;
     myvalid += ok;

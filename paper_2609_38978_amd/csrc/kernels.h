@@ -113,7 +113,12 @@ size_t attn_plan_bytes(int H, int N, int CQ);
 park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,
                              const int* k_offsets, const int* kv_count, const int* kv_index,
                              const int* q_perm, int H, int N, int D, int dtype, int CQ, int CK,
-                             void* O, int out_dtype, void* plan, hipStream_t st);
+                             void* O, int out_dtype, float* lse, void* plan, hipStream_t st);
+
+// k_probe.hip ---------------------------------------------------------------
+park_status launch_probe_exp2(const float* x, float* y, long n, hipStream_t st);
+park_status launch_probe_mfma(const bf16_t* A, const bf16_t* Bt, const float* C0, float* C,
+                              int nprob, int K, hipStream_t st);
 
 // misc ----------------------------------------------------------------------
 park_status launch_clear_status(int* status, hipStream_t st);

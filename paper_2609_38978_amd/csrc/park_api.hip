@@ -388,6 +388,25 @@ park_status park_workspace_size(const park_dims* dims, int32_t CQ, int32_t CK, s
   return PARK_OK;
 }
 
+park_status park_state_sizes(const park_dims* dims, int32_t CQ, int32_t CK, size_t* bytes,
+                             int32_t n) {
+  g_err[0] = 0;
+  PARK_TRY(check_dims(dims));
+  if (!bytes) return fail(PARK_ERR_INVALID_ARG, "bytes is NULL");
+  if (n < PARK_STATE_NBUF)
+    return fail(PARK_ERR_INVALID_ARG, "bytes has %d entries, %d needed", n, PARK_STATE_NBUF);
+  PARK_TRY(check_C(CQ, dims->N, "CQ"));
+  PARK_TRY(check_C(CK, dims->N, "CK"));
+  const size_t H = dims->H, N = dims->N, D = dims->d;
+  const size_t el = dims->dtype == PARK_BF16 ? 2 : 4;
+  const size_t b[PARK_STATE_NBUF] = {
+      H * N * 4,            H * N * 4,            H * (CQ + 1) * 4,    H * (CK + 1) * 4,
+      H * CK * D * 4,       H * CK * 4,           H * CQ * 4,          H * CQ * CK * 4,
+      H * N * D * el,       H * N * D * el,       H * N * D * el,      H * CQ * CK * 4};
+  for (int i = 0; i < PARK_STATE_NBUF; ++i) bytes[i] = b[i];
+  return PARK_OK;
+}
+
 park_status park_cluster_keys(const void* X, const void* Qmetric, const park_dims* dims, int32_t C,
                               int32_t T, uint64_t seed, int32_t side, int32_t metric, double alpha,
                               double eps, double s_min, int32_t* labels, int32_t* perm,
@@ -479,7 +498,7 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
                                    const int32_t* q_offsets, const int32_t* k_offsets,
                                    const int32_t* kv_count, const int32_t* kv_index,
                                    const int32_t* q_perm, const park_dims* dims, int32_t CQ,
-                                   int32_t CK, void* O, int32_t out_dtype, void* ws,
+                                   int32_t CK, void* O, int32_t out_dtype, float* lse, void* ws,
                                    size_t ws_bytes, void* stream) {
   g_err[0] = 0;
   PARK_TRY(check_dims(dims));
@@ -496,12 +515,13 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
   PARK_TRY(check_ptr(kv_index, "kv_index"));
   PARK_TRY(check_ptr(q_perm, "q_perm"));
   PARK_TRY(check_ptr(O, "O"));
+  PARK_TRY(check_opt_ptr(lse, "lse"));
   PARK_TRY(check_ws(ws, ws_bytes, attn_ws_end(dims->H, dims->N, CQ) + 256));
   hipStream_t st = (hipStream_t)stream;
   Carver cv(ws);
   PARK_TRY(launch_clear_status(cv.take<int>(64), st));
   return launch_attention(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, dims->H,
-                          dims->N, dims->d, dims->dtype, CQ, CK, O, out_dtype,
+                          dims->N, dims->d, dims->dtype, CQ, CK, O, out_dtype, lse,
                           carve_attn_plan(ws, dims->H, dims->N, CQ), st);
 }
 
@@ -616,7 +636,7 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
   }
   return launch_attention(s->Qp, s->Kp, s->Vp, s->q_offsets, s->k_offsets, s->kv_count,
                           s->kv_index, s->q_perm, H, N, D, dims->dtype, p->CQ, p->CK, O,
-                          p->out_dtype, carve_attn_plan(ws, H, N, p->CQ), st);
+                          p->out_dtype, nullptr, carve_attn_plan(ws, H, N, p->CQ), st);
 }
 
 park_status park_schedule_step(int32_t step, const int32_t* steps, int32_t n_steps,
@@ -638,6 +658,31 @@ park_status park_schedule_step(int32_t step, const int32_t* steps, int32_t n_ste
   }
   *reuse_out = mode;
   return PARK_OK;
+}
+
+park_status park_probe_exp2(const float* x, float* y, int64_t n, void* stream) {
+  g_err[0] = 0;
+  if (n < 0 || n > ((int64_t)1 << 40)) return fail(PARK_ERR_INVALID_ARG, "n = %lld", (long long)n);
+  if (n > 0) {
+    PARK_TRY(check_ptr(x, "x"));
+    PARK_TRY(check_ptr(y, "y"));
+  }
+  return launch_probe_exp2(x, y, (long)n, (hipStream_t)stream);
+}
+
+park_status park_probe_mfma_bf16(const uint16_t* A, const uint16_t* Bt, const float* C0, float* C,
+                                 int32_t nprob, int32_t K, void* stream) {
+  g_err[0] = 0;
+  if (nprob < 0) return fail(PARK_ERR_INVALID_ARG, "nprob = %d", nprob);
+  if (K < 16 || K > 4096 || K % 16)
+    return fail(PARK_ERR_INVALID_ARG, "K = %d must be a multiple of 16 in [16, 4096]", K);
+  if (nprob > 0) {
+    PARK_TRY(check_ptr(A, "A"));
+    PARK_TRY(check_ptr(Bt, "Bt"));
+    PARK_TRY(check_ptr(C0, "C0"));
+    PARK_TRY(check_ptr(C, "C"));
+  }
+  return launch_probe_mfma(A, Bt, C0, C, nprob, K, (hipStream_t)stream);
 }
 
 park_status park_check(void* ws, void* stream) {

@@ -30,7 +30,8 @@ EXPORTS = (
     "park_workspace_size", "park_cluster_keys", "park_gather_rows", "park_block_centroids",
     "park_retrieve_blocks", "park_block_sparse_attn", "park_forward", "park_check",
     "park_status_string", "park_last_error", "park_profile_enable", "park_profile_reset",
-    "park_profile_read", "park_schedule_step",
+    "park_profile_read", "park_schedule_step", "park_state_sizes", "park_probe_exp2",
+    "park_probe_mfma_bf16",
 )
 
 
@@ -78,11 +79,14 @@ def lib():
         "park_gather_rows": [vp, vp, pd, vp, vp],
         "park_block_centroids": [vp, vp, vp, pd, i32, vp, vp, vp],
         "park_retrieve_blocks": [vp, vp, vp, vp, pd, i32, i32, i32, f64, vp, vp, vp, vp, sz, vp],
-        "park_block_sparse_attn": [vp, vp, vp, vp, vp, vp, vp, vp, pd, i32, i32, vp, i32, vp, sz,
-                                   vp],
+        "park_block_sparse_attn": [vp, vp, vp, vp, vp, vp, vp, vp, pd, i32, i32, vp, i32, vp, vp,
+                                   sz, vp],
+        "park_state_sizes": [pd, i32, i32, C.POINTER(C.c_size_t), i32],
         "park_forward": [vp, vp, vp, pd, C.POINTER(Params), i32, C.POINTER(State), vp, vp, sz,
                          vp],
         "park_check": [vp, vp],
+        "park_probe_exp2": [vp, vp, C.c_int64, vp],
+        "park_probe_mfma_bf16": [vp, vp, vp, vp, i32, i32, vp],
         "park_schedule_step": [i32, C.POINTER(C.c_int32), i32, C.POINTER(C.c_int32)],
         "park_status_string": [i32],
         "park_last_error": [],
@@ -200,16 +204,32 @@ def park_retrieve_blocks(Qp, q_offsets, centroids, k_sizes, CQ: int, CK: int, se
 
 
 def park_block_sparse_attn(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm,
-                           CQ: int, CK: int, out_dtype: int = PARK_F32, ws=None):
+                           CQ: int, CK: int, out_dtype: int = PARK_F32, ws=None,
+                           want_lse: bool = False):
+    """Returns O, or (O, lse [H, N] float32) when want_lse."""
     dims = _dims(Qp)
     O = torch.empty(Qp.shape, dtype=torch.float32 if out_dtype == PARK_F32 else torch.bfloat16,
                     **_dev(Qp))
+    lse = torch.empty(Qp.shape[:2], dtype=torch.float32, **_dev(Qp)) if want_lse else None
     ws = workspace(Qp, CQ, CK) if ws is None else ws
     _check(lib().park_block_sparse_attn(_ptr(Qp), _ptr(Kp), _ptr(Vp), _ptr(q_offsets),
                                         _ptr(k_offsets), _ptr(kv_count), _ptr(kv_index),
                                         _ptr(q_perm), C.byref(dims), CQ, CK, _ptr(O), out_dtype,
-                                        _ptr(ws), ws.numel(), _stream()))
-    return O
+                                        _ptr(lse), _ptr(ws), ws.numel(), _stream()))
+    return (O, lse) if want_lse else O
+
+
+STATE_FIELDS = ("q_perm", "k_perm", "q_offsets", "k_offsets", "k_centroids", "k_sizes",
+                "kv_count", "kv_index", "Qp", "Kp", "Vp", "W")
+
+
+def park_state_sizes(H: int, N: int, d: int, dtype: int, CQ: int, CK: int) -> dict:
+    """Bytes of each park_state buffer, keyed by member name."""
+    n = len(STATE_FIELDS)
+    out = (C.c_size_t * n)()
+    dims = Dims(H, N, d, dtype)
+    _check(lib().park_state_sizes(C.byref(dims), CQ, CK, out, n))
+    return dict(zip(STATE_FIELDS, out))
 
 
 def make_params(CQ, CK, T=10, select="topk", ratio=0.25, topp=0.9, alpha=0.05, eps=1e-6,
@@ -263,6 +283,23 @@ def park_schedule_step(step: int, steps) -> int:
     out = C.c_int32(0)
     _check(lib().park_schedule_step(int(step), arr, len(steps), C.byref(out)))
     return out.value
+
+
+def park_probe_exp2(x):
+    """2^x by the device's v_exp_f32 (x: float32 CUDA tensor)."""
+    x = x.contiguous()
+    y = torch.empty_like(x)
+    _check(lib().park_probe_exp2(_ptr(x), _ptr(y), x.numel(), _stream()))
+    return y
+
+
+def park_probe_mfma_bf16(A, Bt, C0):
+    """C0 + A Bt^T by a chain of 32x32x16 bf16 MFMAs (A, Bt: [P, 32, K] bf16, C0: [P, 32, 32])."""
+    A, Bt, C0 = A.contiguous(), Bt.contiguous(), C0.contiguous()
+    out = torch.empty_like(C0)
+    _check(lib().park_probe_mfma_bf16(_ptr(A), _ptr(Bt), _ptr(C0), _ptr(out), A.shape[0],
+                                      A.shape[2], _stream()))
+    return out
 
 
 def park_check(ws):

@@ -113,6 +113,44 @@ def attn_tol(dtype: str, out_bf16: bool, ref: np.ndarray) -> np.ndarray:
     return tol
 
 
+def lse_tol(Qp: np.ndarray, Kp: np.ndarray, q_offsets, k_offsets, rows, q_perm,
+            lse_ref: np.ndarray) -> np.ndarray:
+    """Per-row bound on the error of a float32 log-normaliser (in token order).
+
+    A score q.k / sqrt(d) accumulated in float32 over d products (exact for
+    bf16 operands, one rounding for float32 ones) errs by at most
+    (d + 1) 2^-23 sum_t |q_t k_t| / sqrt(d); a log-sum-exp moves by at most
+    the largest score error.  The float32 sum of the probabilities (each from
+    one exp, relative error <= 2^-22) adds about (n_keys / 4 + 16) 2^-23
+    relative, and the final scale, log and add 2^-22 (|lse| + 1).
+    """
+    Qp, Kp = np.abs(np.asarray(Qp, np.float64)), np.abs(np.asarray(Kp, np.float64))
+    N, d = Qp.shape
+    tol = np.zeros(N)
+    for u, sel in enumerate(rows):
+        a, b = int(q_offsets[u]), int(q_offsets[u + 1])
+        if b == a or len(sel) == 0:
+            continue
+        keys = np.concatenate([np.arange(k_offsets[v], k_offsets[v + 1]) for v in sel])
+        if len(keys) == 0:
+            continue
+        smax = (Qp[a:b] @ Kp[keys].T).max(axis=1) / math.sqrt(d)
+        t = (d + 1) * 2.0 ** -23 * smax + (len(keys) / 4 + 16) * 2.0 ** -23
+        tol[np.asarray(q_perm[a:b])] = t
+    return tol + 2.0 ** -22 * (np.where(np.isfinite(lse_ref), np.abs(lse_ref), 0.0) + 1.0)
+
+
+def lse_ok(got: np.ndarray, ref: np.ndarray, tol: np.ndarray) -> tuple[bool, float]:
+    """-inf exactly where the reference is -inf, else within tol; (ok, worst err / tol)."""
+    inf_r, inf_g = np.isneginf(ref), np.isneginf(got)
+    if not np.array_equal(inf_r, inf_g) or not np.all(np.isfinite(got[~inf_g])):
+        return False, float("inf")
+    if inf_r.all():
+        return True, 0.0
+    ratio = np.abs(got[~inf_r] - ref[~inf_r]) / tol[~inf_r]
+    return bool(ratio.max() <= 1.0), float(ratio.max())
+
+
 def w_error_ok(dtype: str, W: np.ndarray, ref: np.ndarray) -> tuple[bool, float]:
     """Block-score matrix W^ against the oracle's float64 value.
 

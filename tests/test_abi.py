@@ -102,15 +102,35 @@ def test_retrieve_and_attention_argument_errors():
     assert retr(sel=9) == P.PARK_ERR_INVALID_ARG
     assert retr(CK=3000) == P.PARK_ERR_INVALID_ARG
     assert retr(ws_bytes=8) == P.PARK_ERR_WORKSPACE
-    r = L.park_block_sparse_attn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16, 16,
-                                 FAKE, 7, FAKE, 1 << 30, None)
-    assert r == P.PARK_ERR_INVALID_ARG
-    r = L.park_block_sparse_attn(FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16, 16,
-                                 FAKE, P.PARK_F32, FAKE, 1 << 30, None)
-    assert r == P.PARK_ERR_INVALID_ARG
-    r = L.park_block_sparse_attn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16, 16,
-                                 FAKE, P.PARK_F32, FAKE, 8, None)
-    assert r == P.PARK_ERR_WORKSPACE
+    def attn(V=FAKE, out_dtype=P.PARK_F32, lse=None, ws_bytes=1 << 30):
+        return L.park_block_sparse_attn(FAKE, FAKE, V, FAKE, FAKE, FAKE, FAKE, FAKE, C.byref(d), 16,
+                                        16, FAKE, out_dtype, lse, FAKE, ws_bytes, None)
+
+    assert attn(out_dtype=7) == P.PARK_ERR_INVALID_ARG
+    assert attn(V=None) == P.PARK_ERR_INVALID_ARG
+    assert attn(lse=FAKE + 4) == P.PARK_ERR_INVALID_ARG  # lse misaligned
+    assert b"lse" in L.park_last_error()
+    assert attn(ws_bytes=8) == P.PARK_ERR_WORKSPACE
+
+
+def test_state_sizes():
+    # one entry per park_state member, matching the buffers the binding allocates
+    L = P.lib()
+    H, N, d, CQ, CK = 3, 1000, 128, 16, 24
+    n = len(P.STATE_FIELDS)
+    out = (C.c_size_t * n)()
+    assert L.park_state_sizes(C.byref(_dims(H, N, d, P.PARK_BF16)), CQ, CK, out, n) == P.PARK_OK
+    want = {"q_perm": H * N * 4, "k_perm": H * N * 4, "q_offsets": H * (CQ + 1) * 4,
+            "k_offsets": H * (CK + 1) * 4, "k_centroids": H * CK * d * 4, "k_sizes": H * CK * 4,
+            "kv_count": H * CQ * 4, "kv_index": H * CQ * CK * 4, "Qp": H * N * d * 2,
+            "Kp": H * N * d * 2, "Vp": H * N * d * 2, "W": H * CQ * CK * 4}
+    assert dict(zip(P.STATE_FIELDS, out)) == want
+    assert [f for f, _ in P.State._fields_] == list(P.STATE_FIELDS)
+    assert L.park_state_sizes(C.byref(_dims(H, N, 64, P.PARK_F32)), CQ, CK, out, n) == P.PARK_OK
+    assert out[8] == H * N * 64 * 4
+    assert L.park_state_sizes(C.byref(_dims()), 16, 16, out, n - 1) == P.PARK_ERR_INVALID_ARG
+    assert L.park_state_sizes(C.byref(_dims()), 16, 16, None, n) == P.PARK_ERR_INVALID_ARG
+    assert L.park_state_sizes(C.byref(_dims()), 0, 16, out, n) == P.PARK_ERR_INVALID_ARG
 
 
 def test_forward_argument_errors():
@@ -151,3 +171,14 @@ def test_schedule_step_host_logic():
         with pytest.raises(P.ParkError) as ei:
             P.park_schedule_step(bad_step, bad_sched)
         assert ei.value.status == P.PARK_ERR_INVALID_ARG
+
+
+def test_probe_argument_errors():
+    L = P.lib()
+    assert L.park_probe_exp2(FAKE, FAKE, -1, None) == P.PARK_ERR_INVALID_ARG
+    assert L.park_probe_exp2(None, FAKE, 5, None) == P.PARK_ERR_INVALID_ARG
+    assert L.park_probe_exp2(None, None, 0, None) == P.PARK_OK  # nothing to do
+    for K in (0, 8, 24, 4112):
+        assert L.park_probe_mfma_bf16(FAKE, FAKE, FAKE, FAKE, 1, K, None) == P.PARK_ERR_INVALID_ARG
+    assert L.park_probe_mfma_bf16(FAKE, FAKE, FAKE + 8, FAKE, 1, 32, None) == P.PARK_ERR_INVALID_ARG
+    assert L.park_probe_mfma_bf16(FAKE, FAKE, FAKE, FAKE, -1, 32, None) == P.PARK_ERR_INVALID_ARG

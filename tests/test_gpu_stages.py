@@ -190,16 +190,22 @@ def test_attention_matches_oracle(case, out_dtype):
     Qp = PT.to_dev(np.stack([q[h][qperm[h]] for h in range(H)]), cfg.dtype)
     Kp = PT.to_dev(np.stack([k[h][kperm[h]] for h in range(H)]), cfg.dtype)
     Vp = PT.to_dev(np.stack([v[h][kperm[h]] for h in range(H)]), cfg.dtype)
-    Ot = P.park_block_sparse_attn(Qp, Kp, Vp, t(qoff), t(koff), t(kvc), t(kvi), t(qperm), C, C,
-                                  out_dtype)
+    Ot, Lt = P.park_block_sparse_attn(Qp, Kp, Vp, t(qoff), t(koff), t(kvc), t(kvi), t(qperm), C,
+                                      C, out_dtype, want_lse=True)
     Og = PT.np64(Ot)
+    Lg = Lt.double().cpu().numpy()
     for h in range(H):
-        ref = O.block_sparse_attention(q[h][qperm[h]], k[h][kperm[h]], v[h][kperm[h]], qoff[h],
-                                       koff[h], rows[h], qperm[h])
+        args = (q[h][qperm[h]], k[h][kperm[h]])
+        ref = O.block_sparse_attention(*args, v[h][kperm[h]], qoff[h], koff[h], rows[h], qperm[h])
         tol = PT.attn_tol(cfg.dtype, out_dtype == P.PARK_BF16, ref)
         err = np.abs(Og[h] - ref)
         print(f"[{tag} out={out_dtype} h={h}] attention max-abs err {err.max():.3g}")
         assert np.all(err <= tol), (tag, err.max())
+        lref = O.block_sparse_lse(*args, qoff[h], koff[h], rows[h], qperm[h])
+        ok, worst = PT.lse_ok(Lg[h], lref, PT.lse_tol(*args, qoff[h], koff[h], rows[h], qperm[h],
+                                                      lref))
+        print(f"[{tag} out={out_dtype} h={h}] lse worst err / bound {worst:.3g}")
+        assert ok, (tag, worst)
 
 
 @pytest.mark.parametrize("d", [64, 128])
@@ -239,9 +245,10 @@ def test_attention_many_small_query_blocks(d):
     Qp = PT.to_dev(np.stack([q[h][qperm[h]] for h in range(H)]), "bf16")
     Kp = PT.to_dev(np.stack([k[h][kperm[h]] for h in range(H)]), "bf16")
     Vp = PT.to_dev(np.stack([v[h][kperm[h]] for h in range(H)]), "bf16")
-    Ot = P.park_block_sparse_attn(Qp, Kp, Vp, t(qoff), t(koff), t(kvc), t(kvi), t(qperm), C, CK,
-                                  P.PARK_F32)
+    Ot, Lt = P.park_block_sparse_attn(Qp, Kp, Vp, t(qoff), t(koff), t(kvc), t(kvi), t(qperm), C,
+                                      CK, P.PARK_F32, want_lse=True)
     Og = PT.np64(Ot)
+    Lg = Lt.double().cpu().numpy()
     for h in range(H):
         # the oracle needs a selection per block: give the empty ones a
         # placeholder, then expect zero rows for them
@@ -255,6 +262,13 @@ def test_attention_many_small_query_blocks(d):
         err = np.abs(Og[h] - ref)
         print(f"[small blocks d={d} h={h}] attention max-abs err {err.max():.3g}")
         assert np.all(err <= tol), err.max()
+        # empty selections have lse = -inf
+        args = (q[h][qperm[h]], k[h][kperm[h]])
+        lref = O.block_sparse_lse(*args, qoff[h], koff[h], rows[h], qperm[h])
+        ok, worst = PT.lse_ok(Lg[h], lref, PT.lse_tol(*args, qoff[h], koff[h], rows[h], qperm[h],
+                                                      lref))
+        print(f"[small blocks d={d} h={h}] lse worst err / bound {worst:.3g}")
+        assert ok, worst
 
 
 def test_dense_when_every_block_kept():

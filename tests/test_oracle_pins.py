@@ -785,3 +785,29 @@ def test_mismatch_directions():
     assert rep["d_qk_qrkc"] < 0.5 * rep["d_qk_euclid"]
     assert rep["d_key_qrkc"] > rep["d_key_euclid"]
     assert rep["log_mass_rmse_qrkc"] < 0.5 * rep["log_mass_rmse_euclid"]
+
+
+def test_block_sparse_lse_pins():
+    from scipy.special import logsumexp
+    d = 8
+    Q = rng(95).standard_normal((30, d))
+    K = rng(96).standard_normal((25, d))
+    qoff = np.array([0, 12, 12, 30])
+    koff = np.array([0, 4, 4, 13, 25])
+    perm = rng(97).permutation(30)
+    # every block kept: the dense row log-sum-exp (scipy), un-permuted
+    every = [np.array([0, 1, 2, 3])] * 3
+    lse = O.block_sparse_lse(Q, K, qoff, koff, every, perm)
+    want = np.empty(30)
+    want[perm] = logsumexp(Q @ K.T / math.sqrt(d), axis=1)
+    assert np.allclose(lse, want, rtol=0, atol=1e-13)
+    # a selection: the log-sum-exp over the kept blocks of their exact
+    # log-masses S*_iv (Eq. (6)); nothing kept gives -inf
+    rows = [np.array([0, 3]), np.array([], dtype=np.int64), np.array([1, 2])]
+    lse = O.block_sparse_lse(Q, K, qoff, koff, rows, perm)
+    S = O.exact_log_mass(Q, K, koff)
+    assert np.allclose(lse[perm[:12]], logsumexp(S[:12][:, [0, 3]], axis=1), atol=1e-13)
+    assert np.allclose(lse[perm[12:]], logsumexp(S[12:][:, [2]], axis=1), atol=1e-13)
+    rows[0] = np.array([1])  # an empty key block only: nothing kept
+    lse = O.block_sparse_lse(Q, K, qoff, koff, rows, perm)
+    assert np.isneginf(lse[perm[:12]]).all()
