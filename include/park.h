@@ -238,6 +238,23 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
                                    int32_t CK, void* O, int32_t out_dtype, float* lse, void* ws,
                                    size_t ws_bytes, void* stream);
 
+/* park_block_sparse_attn for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops, harnesses that forbid
+ * hipMalloc): the same computation and arguments without the workspace.  The
+ * status word and the per-call work plan live in a static device array of the
+ * library, 4 MiB per device (held until the process ends), so the call needs
+ * no buffer beyond its inputs and outputs and allocates nothing.  The plan
+ * takes about H (8 CQ + 16 (N/128 + (CQ + N/128)/16 + 2)) bytes;
+ * PARK_ERR_WORKSPACE (nothing enqueued) when it does not fit.  Every call on
+ * one device uses that device's array, so calls that overlap on one device
+ * (concurrent streams or host threads) race: order them on one stream. */
+park_status park_block_sparse_attn_static(const void* Qp, const void* Kp, const void* Vp,
+                                          const int32_t* q_offsets, const int32_t* k_offsets,
+                                          const int32_t* kv_count, const int32_t* kv_index,
+                                          const int32_t* q_perm, const park_dims* dims,
+                                          int32_t CQ, int32_t CK, void* O, int32_t out_dtype,
+                                          float* lse, void* stream);
+
 /* The whole layer: stages 1-4 on Q, K, V [H][N][d] (dtype), output O
  * [H][N][d] (params->out_dtype) in the original token order.  `state` holds
  * caller-allocated buffers that receive (RECOMPUTE) or supply (REUSE_*) the

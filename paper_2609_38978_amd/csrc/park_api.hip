@@ -240,6 +240,58 @@ static park_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   return PARK_OK;
 }
 
+// arguments of the attention entry points (everything but the workspace)
+static park_status check_attn_args(const void* Qp, const void* Kp, const void* Vp,
+                                   const int32_t* q_offsets, const int32_t* k_offsets,
+                                   const int32_t* kv_count, const int32_t* kv_index,
+                                   const int32_t* q_perm, const park_dims* dims, int32_t CQ,
+                                   int32_t CK, void* O, int32_t out_dtype, float* lse) {
+  PARK_TRY(check_dims(dims));
+  PARK_TRY(check_C(CQ, dims->N, "CQ"));
+  PARK_TRY(check_C(CK, dims->N, "CK"));
+  if (out_dtype != PARK_F32 && out_dtype != PARK_BF16)
+    return fail(PARK_ERR_INVALID_ARG, "unknown out_dtype %d", out_dtype);
+  PARK_TRY(check_ptr(Qp, "Qp"));
+  PARK_TRY(check_ptr(Kp, "Kp"));
+  PARK_TRY(check_ptr(Vp, "Vp"));
+  PARK_TRY(check_ptr(q_offsets, "q_offsets"));
+  PARK_TRY(check_ptr(k_offsets, "k_offsets"));
+  PARK_TRY(check_ptr(kv_count, "kv_count"));
+  PARK_TRY(check_ptr(kv_index, "kv_index"));
+  PARK_TRY(check_ptr(q_perm, "q_perm"));
+  PARK_TRY(check_ptr(O, "O"));
+  PARK_TRY(check_opt_ptr(lse, "lse"));
+  return PARK_OK;
+}
+
+// ------------------------------------------------------------ static scratch
+// park_block_sparse_attn_static keeps its status word and work plan in this
+// file-scope device array instead of a caller workspace.  Each device holds
+// its own copy; host code uses only the address hipGetSymbolAddress returns
+// for the current device (the array's name is a host-side stand-in), kept per
+// device after the first call there.  Every call on a device shares it.
+constexpr size_t kStaticScratchBytes = (size_t)4 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[64];
+
+static park_status static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(PARK_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= 64) return fail(PARK_ERR_UNSUPPORTED, "device %d", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(PARK_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return PARK_OK;
+}
+
 // ------------------------------------------------------------ side stream
 // The query side's clustering and the Cholesky factor of the key side's
 // metric run on a second stream of the device, beside the key side's Gbar
@@ -501,21 +553,8 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
                                    int32_t CK, void* O, int32_t out_dtype, float* lse, void* ws,
                                    size_t ws_bytes, void* stream) {
   g_err[0] = 0;
-  PARK_TRY(check_dims(dims));
-  PARK_TRY(check_C(CQ, dims->N, "CQ"));
-  PARK_TRY(check_C(CK, dims->N, "CK"));
-  if (out_dtype != PARK_F32 && out_dtype != PARK_BF16)
-    return fail(PARK_ERR_INVALID_ARG, "unknown out_dtype %d", out_dtype);
-  PARK_TRY(check_ptr(Qp, "Qp"));
-  PARK_TRY(check_ptr(Kp, "Kp"));
-  PARK_TRY(check_ptr(Vp, "Vp"));
-  PARK_TRY(check_ptr(q_offsets, "q_offsets"));
-  PARK_TRY(check_ptr(k_offsets, "k_offsets"));
-  PARK_TRY(check_ptr(kv_count, "kv_count"));
-  PARK_TRY(check_ptr(kv_index, "kv_index"));
-  PARK_TRY(check_ptr(q_perm, "q_perm"));
-  PARK_TRY(check_ptr(O, "O"));
-  PARK_TRY(check_opt_ptr(lse, "lse"));
+  PARK_TRY(check_attn_args(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, dims, CQ,
+                           CK, O, out_dtype, lse));
   PARK_TRY(check_ws(ws, ws_bytes, attn_ws_end(dims->H, dims->N, CQ) + 256));
   hipStream_t st = (hipStream_t)stream;
   Carver cv(ws);
@@ -523,6 +562,31 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
   return launch_attention(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, dims->H,
                           dims->N, dims->d, dims->dtype, CQ, CK, O, out_dtype, lse,
                           carve_attn_plan(ws, dims->H, dims->N, CQ), st);
+}
+
+park_status park_block_sparse_attn_static(const void* Qp, const void* Kp, const void* Vp,
+                                          const int32_t* q_offsets, const int32_t* k_offsets,
+                                          const int32_t* kv_count, const int32_t* kv_index,
+                                          const int32_t* q_perm, const park_dims* dims,
+                                          int32_t CQ, int32_t CK, void* O, int32_t out_dtype,
+                                          float* lse, void* stream) {
+  g_err[0] = 0;
+  PARK_TRY(check_attn_args(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, dims, CQ,
+                           CK, O, out_dtype, lse));
+  const size_t need = attn_ws_end(dims->H, dims->N, CQ);
+  if (need > kStaticScratchBytes)
+    return fail(PARK_ERR_WORKSPACE,
+                "H = %d, N = %d, CQ = %d need %zu bytes of plan, more than the %zu bytes of "
+                "static scratch: use park_block_sparse_attn with a workspace",
+                dims->H, dims->N, CQ, need, kStaticScratchBytes);
+  void* ptr = nullptr;
+  PARK_TRY(static_scratch(&ptr));
+  hipStream_t st = (hipStream_t)stream;
+  Carver cv(ptr);
+  PARK_TRY(launch_clear_status(cv.take<int>(64), st));
+  return launch_attention(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm, dims->H,
+                          dims->N, dims->d, dims->dtype, CQ, CK, O, out_dtype, lse,
+                          carve_attn_plan(ptr, dims->H, dims->N, CQ), st);
 }
 
 park_status park_forward(const void* Q, const void* K, const void* V, const park_dims* dims,

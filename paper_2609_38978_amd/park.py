@@ -31,7 +31,7 @@ EXPORTS = (
     "park_retrieve_blocks", "park_block_sparse_attn", "park_forward", "park_check",
     "park_status_string", "park_last_error", "park_profile_enable", "park_profile_reset",
     "park_profile_read", "park_schedule_step", "park_state_sizes", "park_probe_exp2",
-    "park_probe_mfma_bf16",
+    "park_probe_mfma_bf16", "park_block_sparse_attn_static",
 )
 
 
@@ -81,6 +81,8 @@ def lib():
         "park_retrieve_blocks": [vp, vp, vp, vp, pd, i32, i32, i32, f64, vp, vp, vp, vp, sz, vp],
         "park_block_sparse_attn": [vp, vp, vp, vp, vp, vp, vp, vp, pd, i32, i32, vp, i32, vp, vp,
                                    sz, vp],
+        "park_block_sparse_attn_static": [vp, vp, vp, vp, vp, vp, vp, vp, pd, i32, i32, vp, i32,
+                                          vp, vp],
         "park_state_sizes": [pd, i32, i32, C.POINTER(C.c_size_t), i32],
         "park_forward": [vp, vp, vp, pd, C.POINTER(Params), i32, C.POINTER(State), vp, vp, sz,
                          vp],
@@ -217,6 +219,21 @@ def park_block_sparse_attn(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index,
                                         _ptr(q_perm), C.byref(dims), CQ, CK, _ptr(O), out_dtype,
                                         _ptr(lse), _ptr(ws), ws.numel(), _stream()))
     return (O, lse) if want_lse else O
+
+
+def park_block_sparse_attn_static(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv_index, q_perm,
+                                  CQ: int, CK: int, out_dtype: int = PARK_F32, O=None, lse=None):
+    """The workspace-free entry point: writes into the given O (and lse) tensors,
+    allocating nothing when both are given; returns (O, lse)."""
+    dims = _dims(Qp)
+    if O is None:
+        O = torch.empty(Qp.shape, dtype=torch.float32 if out_dtype == PARK_F32
+                        else torch.bfloat16, **_dev(Qp))
+    _check(lib().park_block_sparse_attn_static(_ptr(Qp), _ptr(Kp), _ptr(Vp), _ptr(q_offsets),
+                                               _ptr(k_offsets), _ptr(kv_count), _ptr(kv_index),
+                                               _ptr(q_perm), C.byref(dims), CQ, CK, _ptr(O),
+                                               out_dtype, _ptr(lse), _stream()))
+    return O, lse
 
 
 STATE_FIELDS = ("q_perm", "k_perm", "q_offsets", "k_offsets", "k_centroids", "k_sizes",
