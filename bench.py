@@ -127,6 +127,15 @@ def kernel_work(name, cfg, st, C):
     if name == "kmeans_assign_fast":
         # algorithmic N*C*d multiply-adds; the hi/lo split issues twice that on MFMA
         return "mfma", 2.0 * N * C * d * H, "flop", "mfma_bf16"
+    if name == "kmeans_assign_cand":
+        # the filtered rounds score each token against its tile's candidate
+        # union only (a few percent of the centroids): the gathered token rows
+        # are the dominant traffic
+        return "hbm", (1.0 * N * d * eb + 8.0 * N) * H, "byte", "hbm"
+    if name == "kfilter_radius":  # token rows through perm, their norm bounds
+        return "hbm", (1.0 * N * d * eb + 12.0 * N + C * d * 8.0) * H, "byte", "hbm"
+    if name == "kfilter_cand":  # mu . w_v for every centroid pair, three split products
+        return "mfma", 3.0 * 2.0 * C * C * d * H, "flop", "mfma_bf16"
     if name == "pama_fast":
         # one q.c product per (query, key block); the centroid split issues it 3x on MFMA
         return "mfma", 2.0 * N * C * d * H, "flop", "mfma_bf16"
@@ -160,6 +169,60 @@ def kernel_work(name, cfg, st, C):
     if name == "select_fast":  # the float W^ rows and their error bounds
         return "hbm", 4.0 * C * C * H, "byte", "hbm"
     return None
+
+
+def attention_flops(ws, st, cfg, ms_attn):
+    """Useful and issued MFMA flops of the block-sparse attention launch.
+
+    useful = 4 d sum_u n_u sum_{v in sel(u)} n_v (each query row against the
+    keys of its own block's selection).  The grouped kernel streams, per group
+    of at most 128 rows (four wavefronts of 32), the union of its query
+    blocks' selections in 32-key tiles (in chunks of at most 1024 key blocks)
+    and every wavefront computes every tile, so issued = 4 d 128 32 x (tiles
+    summed over groups).  The groups are read from the work plan the launch
+    left in the workspace: after the 256-byte status region, order [H][CQ],
+    row prefix [H][CQ+1] (int32), then the groups int4 [H][GPH] at 16-byte
+    alignment, GPH = W + ceil((CQ + W) / 16) + 1, W = ceil(N / 128)."""
+    import numpy as np
+    H, N, d = cfg.H, cfg.N, cfg.d
+    CQ = st["q_offsets"].shape[1] - 1
+    qo = st["q_offsets"].cpu().numpy()
+    ko = st["k_offsets"].cpu().numpy()
+    kvc = st["kv_count"].cpu().numpy()
+    kvi = st["kv_index"].cpu().numpy()
+    W = -(-N // 128)
+    GPH = W + -(-(CQ + W) // 16) + 1
+    goff = ((H * CQ + H * (CQ + 1)) * 4 + 15) & ~15
+    raw = ws[256:256 + goff + H * GPH * 16].cpu().numpy()
+    order = raw[:H * CQ * 4].view(np.int32).reshape(H, CQ)
+    grp = raw[goff:goff + H * GPH * 16].view(np.int32).reshape(H, GPH, 4)
+    useful = 0.0
+    tiles = 0
+    for h in range(H):
+        nk = np.diff(ko[h]).astype(np.int64)
+        nq = np.diff(qo[h]).astype(np.int64)
+        for u in range(CQ):
+            if nq[u]:
+                useful += float(nq[u] * nk[kvi[h, u, :kvc[h, u]]].sum())
+        for g in range(GPH):
+            r0, r1, i0, i1 = grp[h, g]
+            if r1 <= r0 or i1 <= i0:
+                continue
+            blocks = order[h, i0:i1]
+            blocks = blocks[(blocks >= 0) & (blocks < CQ)]
+            sel = [kvi[h, u, :kvc[h, u]] for u in blocks]
+            union = np.unique(np.concatenate(sel)) if sel else np.zeros(0, np.int64)
+            union = union[(union >= 0) & (union < len(nk))]
+            for c0 in range(0, len(union), 1024):
+                tiles += int(-(-int(nk[union[c0:c0 + 1024]].sum()) // 32))
+    useful *= 4.0 * d
+    issued = 4.0 * d * 128 * 32 * tiles
+    t = ms_attn * 1e-3
+    return {"useful_tflop": round(useful / 1e12, 3), "issued_tflop": round(issued / 1e12, 3),
+            "issued_over_useful": round(issued / max(useful, 1.0), 3),
+            "useful_tflops": round(useful / t / 1e12, 2), "issued_tflops": round(issued / t / 1e12, 2),
+            "useful_frac": round(useful / t / 1e12 / PEAK["mfma_bf16"], 4),
+            "issued_frac": round(issued / t / 1e12 / PEAK["mfma_bf16"], 4)}
 
 
 def host_info():
@@ -360,6 +423,9 @@ def main():
            "graph_ms_per_step": None if ms_graph is None else round(ms_graph, 4),
            "wall_s": round(wall, 3), "stages": stages, "stage_roofline": stage_roof,
            "roofline": roof}
+    if "attn_mfma" in prof and prof["attn_mfma"]["launches"]:
+        res["attention_flops"] = attention_flops(ws, st, cfg, prof["attn_mfma"]["ms"] /
+                                                 prof["attn_mfma"]["launches"])
     if not args.no_cpu_baseline:
         nh = args.cpu_heads if args.cpu_heads is not None else (4 if cfg.N < 50000 else 1)
         res["cpu_baseline"] = cpu_baseline(cfg, q, k, v, min(nh, cfg.H), variant)

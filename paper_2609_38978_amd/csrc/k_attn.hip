@@ -263,6 +263,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 #ifndef PARK_ATTN_RING
 #define PARK_ATTN_RING 3
 #endif
+#ifndef PARK_ATTN_HEADMAJOR
+#define PARK_ATTN_HEADMAJOR 1
+#endif
 constexpr int ATTN_R = PARK_ATTN_R;  // rows per group (32 per wavefront)
 constexpr int ATTN_KSLOTS = PARK_ATTN_RING;  // K tiles in LDS (V: one more)
 constexpr int ATTN_UCAP = 1024;  // key blocks of the union per stream chunk
@@ -568,10 +571,17 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
   __shared__ int tmp[2][NW];
   static_assert(ATTN_LB <= 16, "selection words are 16 bits");
 
-  // XCD-aware work item: XCD x (= blockIdx % 8) takes items [x*per, (x+1)*per)
   const int nitems = H * GPH;
+#if PARK_ATTN_HEADMAJOR
+  // head-major over the whole chip: consecutive workgroups (dealt to the 8
+  // XCDs in turn) take the groups of one head, so only a head or two are in
+  // flight at a time and their keys and values stay in the Infinity Cache
+  const int item = (int)blockIdx.x;
+#else
+  // XCD-aware work item: XCD x (= blockIdx % 8) takes items [x*per, (x+1)*per)
   const int per = (nitems + 7) >> 3;
   const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+#endif
   if (item >= nitems) return;
   const int h = item / GPH;
   const int4 gd = grp[item];

@@ -8,6 +8,8 @@
 // since argmin_v |x~ - mu~_v|^2 = argmin_v (b_v - 2 x . w_v).  The Euclidean
 // side uses w_v = mu_v.  Centroids are means of the input-space points, the
 // image under R^T of the transformed-space means (linearity).
+#include <stdlib.h>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -122,7 +124,8 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
                                               bf16_t* __restrict__ w3,
                                               size_t plane, float* __restrict__ b32, int Cpad,
                                               float* __restrict__ wn, float* __restrict__ eb,
-                                              float* __restrict__ bmax) {
+                                              float* __restrict__ bmax, bf16_t* __restrict__ m2,
+                                              float* __restrict__ mn) {
   // NT threads: D lanes per centroid group, 16 / (NT / D) centroids per
   // thread.  1024 threads shorten each thread's float64 chain over the D
   // columns (small grids); 256 read the metric rows fewer times (large grids)
@@ -169,6 +172,12 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
         w3[o + plane] = p2;
         w3[o + 2 * plane] = f2bf((float)r2);
       }
+      if (m2) {  // the centroid itself in two bf16 parts (candidate filter)
+        const double mv = ms[r][a];
+        const bf16_t q1 = f2bf((float)mv);
+        m2[o] = q1;
+        m2[o + plane] = f2bf((float)(mv - (double)bf2f(q1)));
+      }
     }
   }
   __syncthreads();
@@ -177,17 +186,20 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
   if (tid < 256) {
     constexpr int LPC = 256 / CB;
     const int r = tid / LPC, sub = tid % LPC;
-    double s = 0.0, n2 = 0.0;
+    double s = 0.0, n2 = 0.0, m2s = 0.0;
 #pragma unroll
     for (int c = sub; c < D; c += LPC) {
       s = fma(ms[r][c], ws[r][c], s);
       n2 = fma(ws[r][c], ws[r][c], n2);
+      m2s = fma(ms[r][c], ms[r][c], m2s);
     }
 #pragma unroll
     for (int o = LPC / 2; o > 0; o >>= 1) {
       s += __shfl_xor(s, o, 64);
       n2 += __shfl_xor(n2, o, 64);
+      m2s += __shfl_xor(m2s, o, 64);
     }
+    if (mn && sub == 0 && v0 + r < C) mn[(size_t)h * C + v0 + r] = (float)(sqrt(m2s) * (1.0 + 1e-6));
     float fnr = 0.0f, fer = 0.0f;
     if (sub == 0 && v0 + r < C) {
       b[(size_t)h * C + v0 + r] = s;
@@ -1120,6 +1132,13 @@ park_status launch_segment_mean(const void* X, const int* perm, const int* offse
   return PARK_OK;
 }
 
+// PARK_KMEANS_FILTER=0 runs every assignment round dense (the same labels;
+// for timing the filter against the dense sweep)
+static bool kmeans_filter_enabled() {
+  const char* e = getenv("PARK_KMEANS_FILTER");
+  return !(e && e[0] == '0');
+}
+
 template <typename T, int D>
 static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int C, int T_,
                                uint64_t seed, int side, const KmeansBufs& kb, int* status,
@@ -1134,20 +1153,30 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
   const int max_tiles = (N + 63) / 64;
   rg = rg < 2 ? 2 : rg;
   rg = rg > max_tiles ? max_tiles : rg;
+  // the exact candidate filter for the rounds after the first (bf16 points),
+  // where the dense sweep is MFMA-bound (C >= 512); below that the dense
+  // round is a few tens of microseconds and the filter's passes cost more
+  const bool filt = fast && kb.kf != nullptr && C >= 512 && kmeans_filter_enabled();
+  if constexpr (fast)
+    if (filt) PARK_TRY(launch_kfilter_setup((const bf16_t*)X, Gbar, H, N, D, *kb.kf, st));
+  bf16_t* m2 = filt ? kb.kf->m2 : nullptr;
+  float* mn = filt ? kb.kf->mn : nullptr;
   for (int t = 0; t < T_; ++t) {
     const int nbm = (C + 15) / 16;
     if ((long)nbm * H < 512)
       PARK_LAUNCH("kmeans_prep", (k_prep<D, 1024>), dim3(nbm, H), dim3(1024), 0, st,
                   (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane,
                   fast ? kb.b32 : nullptr, kmeans_cpad(C), fast ? kb.wn : nullptr,
-                  fast ? kb.eb : nullptr, kb.hmax);
+                  fast ? kb.eb : nullptr, kb.hmax, m2, mn);
     else
       PARK_LAUNCH("kmeans_prep", (k_prep<D, 256>), dim3(nbm, H), dim3(256), 0, st,
                   (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane,
                   fast ? kb.b32 : nullptr, kmeans_cpad(C), fast ? kb.wn : nullptr,
-                  fast ? kb.eb : nullptr, kb.hmax);
+                  fast ? kb.eb : nullptr, kb.hmax, m2, mn);
     if constexpr (fast) {
-      if (C >= 512)
+      if (filt && t > 0)
+        PARK_TRY(launch_kfilter_round((const bf16_t*)X, H, N, D, C, kb, *kb.kf, st));
+      else if (C >= 512)
         PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 2>), dim3((N + kmeans_tile - 1) / kmeans_tile, H),
                     dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
                     (const float*)kb.b32, kmeans_cpad(C), (const float*)kb.wn, (const float*)kb.eb,

@@ -45,6 +45,17 @@ constexpr int kmeans_tile = 128 * PARK_KM_TB;
 // key-block count padded to the fast retrieval's tile multiple
 inline int pama_ckpad(int CK) { return (CK + 63) / 64 * 64; }
 
+// exact candidate filter of the k-means rounds after the first (k_kfilter.hip)
+struct KfilterBufs {
+  bf16_t* g2;       // [2][H][D][D] Gbar in two bf16 parts (QRKC side)
+  double* gmax;     // [H] largest absolute row sum of Gbar
+  double* xn;       // [H][N] upper bound of x^T Gbar x (|x|^2 on the Euclidean side)
+  double* r2;       // [H][C] squared cluster radius bound, -1 for an empty cluster
+  uint32_t* cand;   // [H][C][64] candidate-set bit rows
+  bf16_t* m2;       // [2][H][C][D] centroids in two bf16 parts
+  float* mn;        // [H][C] |mu_v| rounded up
+};
+
 struct KmeansBufs {
   int* init;      // [H][C]
   double* mu;     // [H][C][D] centroids in the input space
@@ -64,6 +75,7 @@ struct KmeansBufs {
   int* nflag;     // [H][ceil(N/kmeans_tile)] tokens of each tile left for the float64 refine
   int* flags;     // [H][N]    their indices, tile t's list at kmeans_tile * t
   float* flagu;   // [H][N]    and an upper bound of their smallest exact score
+  const KfilterBufs* kf = nullptr;  // candidate filter (bf16 points; null: every round dense)
 };
 park_status launch_kmeans(const void* X, const double* Gbar /* null = Euclidean */, int H, int N,
                           int D, int dtype, int C, int T, uint64_t seed, int side,
@@ -114,6 +126,15 @@ park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, con
                              const int* k_offsets, const int* kv_count, const int* kv_index,
                              const int* q_perm, int H, int N, int D, int dtype, int CQ, int CK,
                              void* O, int out_dtype, float* lse, void* plan, hipStream_t st);
+
+// k_kfilter.hip -------------------------------------------------------------
+// once per k-means call: Gbar's parts (QRKC) and the token norms
+park_status launch_kfilter_setup(const bf16_t* X, const double* Gbar, int H, int N, int D,
+                                 const KfilterBufs& kf, hipStream_t st);
+// one round t >= 1: radii, candidate sets, filtered assignment (listing the
+// uncertified tokens for k_refine_cand as the dense assignment does)
+park_status launch_kfilter_round(const bf16_t* X, int H, int N, int D, int C,
+                                 const KmeansBufs& kb, const KfilterBufs& kf, hipStream_t st);
 
 // k_probe.hip ---------------------------------------------------------------
 park_status launch_probe_exp2(const float* x, float* y, long n, hipStream_t st);

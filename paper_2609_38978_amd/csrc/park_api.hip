@@ -134,6 +134,7 @@ struct ClusterWs {
   int* nflag;
   int* flags;
   float* flagu;
+  KfilterBufs kf;
 };
 
 static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
@@ -156,6 +157,13 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   c.nflag = cv.take<int>((size_t)H * ((N + kmeans_tile - 1) / kmeans_tile));
   c.flags = cv.take<int>((size_t)H * N);
   c.flagu = cv.take<float>((size_t)H * N);
+  c.kf.g2 = cv.take<bf16_t>((size_t)2 * H * D * D);
+  c.kf.gmax = cv.take<double>((size_t)H);
+  c.kf.xn = cv.take<double>((size_t)H * N);
+  c.kf.r2 = cv.take<double>((size_t)H * C);
+  c.kf.cand = cv.take<uint32_t>((size_t)H * C * 64);
+  c.kf.m2 = cv.take<bf16_t>((size_t)2 * H * C * D);
+  c.kf.mn = cv.take<float>((size_t)H * C);
   return c;
 }
 
@@ -395,6 +403,7 @@ static park_status cluster_body(const void* X, const void* Qm, const park_dims& 
   kb.nflag = cw.nflag;
   kb.flags = cw.flags;
   kb.flagu = cw.flagu;
+  kb.kf = &cw.kf;
   return launch_kmeans(X, Gbar, H, N, D, dm.dtype, C, T, seed, side, kb, st);
 }
 
