@@ -450,3 +450,50 @@ def test_rank_deficient_metric_clusters_like_the_square_root(dtype, N, d, C):
     Og, st = P.park_forward(Q, K, K, prm, ws=ws)
     P.park_check(ws)
     assert np.array_equal(st["k_perm"][0].cpu().numpy(), out["perm"][0].cpu().numpy())
+
+
+# The exact candidate filter of the k-means rounds after the first runs where
+# C >= 512; small layers with many clusters exercise it (and clusters with a
+# single or no token, and centroids pulled far apart by the 2N(0,1) centres).
+@pytest.mark.parametrize("name,grid,C,side", [("medium", (2, 32, 64), 600, 0),
+                                              ("medium", (2, 32, 64), 600, 1),
+                                              ("hunyuan", (2, 16, 32), 700, 1),
+                                              ("medium", (1, 32, 32), 1024, 1)])
+def test_kmeans_candidate_filter_matches_oracle_and_dense(name, grid, C, side):
+    import os
+    cfg = synth.CONFIGS[name].with_(grid=grid)
+    q, k, _ = synth.make_layer(cfg, [0, 1])
+    Q, K = PT.to_dev(q, cfg.dtype), PT.to_dev(k, cfg.dtype)
+    T = 6
+    print(f"[filter {name} N={cfg.N} C={C} side={side}]", flush=True)
+
+    def run():
+        if side == 0:
+            o = P.park_cluster_keys(Q, C, T, seed=3, side=0, metric=P.PARK_METRIC_EUCLID)
+        else:
+            o = P.park_cluster_keys(K, C, T, seed=3, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q)
+        P.park_check(o["ws"])
+        return o["labels"].cpu().numpy(), o["perm"].cpu().numpy(), o["offsets"].cpu().numpy()
+
+    lab, perm, off = run()
+    os.environ["PARK_KMEANS_FILTER"] = "0"
+    try:
+        lab_d, perm_d, off_d = run()
+    finally:
+        del os.environ["PARK_KMEANS_FILTER"]
+    # the filter changes which centroids are scored, never the labels
+    assert np.array_equal(lab, lab_d) and np.array_equal(perm, perm_d)
+    assert np.array_equal(off, off_d)
+    for h in range(2):
+        if side == 0:
+            res = O.cluster_queries(q[h], C, T, 3, h)
+            X = q[h].astype(np.float64)
+        else:
+            res = O.cluster_keys(k[h], q[h], C, T, 3, h)
+            X = res["Kt"]
+        n_mis, n_bad, worst = PT.label_flips(X, res["mu"], lab[h], res["labels"])
+        print(f"[filter h={h}] label mismatches={n_mis} not-exempt={n_bad} worst-gap={worst:.3g}; "
+              f"empty clusters={int((np.diff(off[h]) == 0).sum())}", flush=True)
+        assert n_bad == 0
+        p2, o2 = O.stable_argsort(lab[h], C)
+        assert np.array_equal(perm[h], p2) and np.array_equal(off[h], o2)
