@@ -308,9 +308,18 @@ __global__ __launch_bounds__(256) void k_cand(const bf16_t* __restrict__ m2, siz
   const double man = (double)mn[(size_t)h * C + ar];
   const double ana = man * (double)wn[(size_t)h * Cpad + ar];
   uint32_t* crow = cand + ((size_t)h * C + ar) * 64;
-  __shared__ double vb_s[4][32], vw_s[4][32], vm_s[4][32];
+  // b_v, |w_v| and |mu_v| |w_v| of this workgroup's 16 centroid tiles, read once
+  __shared__ double vb_s[512], vw_s[512], vm_s[512];
   const int nvt = (C + 31) / 32;
   const int vt_end = min(nvt, (int)(blockIdx.z + 1) * 16);
+  for (int e = tid; e < 512; e += 256) {
+    const int vr = min((int)blockIdx.z * 512 + e, C - 1);
+    const double wv = (double)wn[(size_t)h * Cpad + vr];
+    vb_s[e] = b[(size_t)h * C + vr];
+    vw_s[e] = wv;
+    vm_s[e] = (double)mn[(size_t)h * C + vr] * wv;
+  }
+  __syncthreads();
   // operands of the next centroid tile are loaded while this one is scored
   kf_bf16x8_t w1n[KS], w2n[KS];
   auto load_w = [&](int vt, kf_bf16x8_t* f1, kf_bf16x8_t* f2) {
@@ -326,7 +335,6 @@ __global__ __launch_bounds__(256) void k_cand(const bf16_t* __restrict__ m2, siz
   if (vt < vt_end) load_w(vt, w1n, w2n);
   for (; vt < vt_end; vt += 4) {
     const int v0 = vt * 32;
-    const int vr = min(v0 + c32, C - 1);
     kf_bf16x8_t w1f[KS], w2f[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
@@ -334,12 +342,7 @@ __global__ __launch_bounds__(256) void k_cand(const bf16_t* __restrict__ m2, siz
       w2f[s] = w2n[s];
     }
     if (vt + 4 < vt_end) load_w(vt + 4, w1n, w2n);
-    if (hf == 0) {  // b_v, |w_v| and |mu_v| |w_v| of this tile, read once
-      const double wv = (double)wn[(size_t)h * Cpad + vr];
-      vb_s[w][c32] = b[(size_t)h * C + vr];
-      vw_s[w][c32] = wv;
-      vm_s[w][c32] = (double)mn[(size_t)h * C + vr] * wv;
-    }
+
     kf_f32x16_t acc;
 #pragma unroll
     for (int q = 0; q < 16; ++q) acc[q] = 0.0f;
@@ -355,12 +358,13 @@ __global__ __launch_bounds__(256) void k_cand(const bf16_t* __restrict__ m2, siz
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const int vi = 8 * (q >> 2) + 4 * hf + (q & 3), v = v0 + vi;
+      const int li = v0 - (int)blockIdx.z * 512 + vi;
       if (v < C && ra >= 0.0) {
-        const double bv = vb_s[w][vi];
-        const double wnv = vw_s[w][vi];
+        const double bv = vb_s[li];
+        const double wnv = vw_s[li];
         const double t = (double)acc[q];
         const double lo = ba + bv - 2.0 * t - 2.0 * EC * man * wnv -
-                          1e-12 * (fabs(ba) + fabs(bv) + ana + vm_s[w][vi]);
+                          1e-12 * (fabs(ba) + fabs(bv) + ana + vm_s[li]);
         const bool keep = v == a || !(lo > 4.0 * ra * (1.0 + 1e-9) + 1e-9 * (fabs(ba) + fabs(bv)));
         bits |= keep ? (1u << (8 * (q >> 2) + 4 * hf + (q & 3))) : 0u;
       }
@@ -381,8 +385,12 @@ __global__ __launch_bounds__(256) void k_cand(const bf16_t* __restrict__ m2, siz
 // exact argmin over all centroids; the certification uses the maxima of the
 // error terms over all centroids.  Uncertified tokens are listed for the
 // float64 refinement as before.
+// workgroups per CU of the two-part filtered assignment (its LDS allows 3)
+#ifndef PARK_KM_CAND_OCC
+#define PARK_KM_CAND_OCC 3
+#endif
 template <int D, int NP>
-__global__ __launch_bounds__(256, 2) void k_assign_cand(
+__global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_cand(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ w3, size_t plane,
     const float* __restrict__ b32, int Cpad, const float* __restrict__ wn,
     const float* __restrict__ eb, const float* __restrict__ bmax, int nbm, int N, int C,
