@@ -98,6 +98,13 @@ typedef enum park_estimator { PARK_EST_PAMA = 0, PARK_EST_QCENTROID = 1 } park_e
  * blocks when C b - N >= b). */
 typedef enum park_block_mode { PARK_BLOCKS_CLUSTER = 0, PARK_BLOCKS_FIXED = 1 } park_block_mode;
 
+/* How park_forward's recomputation initialises the two k-means.
+ * PARK_INIT_SEEDED: from C distinct tokens drawn by the seeded shuffle (as
+ * park_cluster_keys).  PARK_INIT_WARM: from the centroids in state.q_mu and
+ * state.k_mu, the means of the final clusters of the previous recompute
+ * (clusters change little between diffusion steps, Sec. 5.2). */
+typedef enum park_init { PARK_INIT_SEEDED = 0, PARK_INIT_WARM = 1 } park_init;
+
 typedef struct park_dims {
   int32_t H;     /* attention heads                      */
   int32_t N;     /* tokens per head (L in the paper)     */
@@ -120,6 +127,7 @@ typedef struct park_params {
   int32_t out_dtype; /* park_dtype of O                                      */
   int32_t estimator; /* park_estimator (PARK_EST_PAMA)                        */
   int32_t block_mode;/* park_block_mode (PARK_BLOCKS_CLUSTER)                 */
+  int32_t init;      /* park_init of a recomputation (PARK_INIT_SEEDED)      */
 } park_params;
 
 /* Caller-allocated device buffers carried across park_forward calls. */
@@ -136,14 +144,18 @@ typedef struct park_state {
   void* Kp;            /* [H][N][d]   permuted keys               */
   void* Vp;            /* [H][N][d]   permuted values             */
   float* W;            /* [H][CQ][CK] W^ (optional, may be NULL)  */
+  double* q_mu;        /* [H][CQ][d]  query centroids (may be NULL): written with the means
+                          of the final query clusters by every recomputation, read as the
+                          starting centroids by PARK_INIT_WARM                            */
+  double* k_mu;        /* [H][CK][d]  key centroids in the original key space, likewise */
 } park_state;
 
 /* Byte sizes of the caller-allocated park_state buffers for these dims and
  * block counts, in the order the members are declared (q_perm, k_perm,
  * q_offsets, k_offsets, k_centroids, k_sizes, kv_count, kv_index, Qp, Kp,
- * Vp, W): bytes[i] for member i, PARK_STATE_NBUF entries.  Host-only.
- * PARK_ERR_INVALID_ARG if bytes is NULL or n < PARK_STATE_NBUF. */
-#define PARK_STATE_NBUF 12
+ * Vp, W, q_mu, k_mu): bytes[i] for member i, PARK_STATE_NBUF entries.
+ * Host-only.  PARK_ERR_INVALID_ARG if bytes is NULL or n < PARK_STATE_NBUF. */
+#define PARK_STATE_NBUF 14
 park_status park_state_sizes(const park_dims* dims, int32_t CQ, int32_t CK, size_t* bytes,
                              int32_t n);
 
@@ -261,6 +273,10 @@ park_status park_block_sparse_attn_static(const void* Qp, const void* Kp, const 
  * clustering and mask.  With PARK_REUSE_CLUSTERS the permutations and offsets
  * of `state` are reused and gathers, centroids, retrieval and attention run
  * on the new tensors; PARK_REUSE_CLUSTERS_AND_MASK also reuses the mask.
+ * A recomputation with params->init = PARK_INIT_WARM starts both k-means
+ * from state.q_mu / state.k_mu (then required, PARK_ERR_INVALID_ARG
+ * otherwise); any recomputation given those buffers leaves the means of its
+ * final clusters there.
  * With RECOMPUTE the query side's clustering runs on a side stream of the
  * device (created by the library, default priority) that forks from `stream`
  * and joins back into it, beside the key side's on `stream`: work queued on

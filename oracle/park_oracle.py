@@ -158,15 +158,16 @@ def update(X: np.ndarray, z: np.ndarray, mu: np.ndarray) -> np.ndarray:
     return new
 
 
-def kmeans(X: np.ndarray, C: int, T: int, init: np.ndarray, labels_hook=None):
-    """T rounds of (assign, update) from centroids X[init].
+def kmeans(X: np.ndarray, C: int, T: int, init: np.ndarray, labels_hook=None, mu0=None):
+    """T rounds of (assign, update) from centroids X[init], or from the given
+    centroids ``mu0`` (a warm start, e.g. the previous recomputation's means).
 
     Returns the labels of the T-th assignment and the centroids it used.
     ``labels_hook(t, z, mu)`` may return replacement labels for round t
     (parity tests use it to follow another implementation's near-tie flips).
     """
     X = np.asarray(X, dtype=np.float64)
-    mu = X[np.asarray(init)].copy()
+    mu = (X[np.asarray(init)] if mu0 is None else np.asarray(mu0, dtype=np.float64)).copy()
     z = None
     for t in range(T):
         z = assign(X, mu)
@@ -175,6 +176,14 @@ def kmeans(X: np.ndarray, C: int, T: int, init: np.ndarray, labels_hook=None):
         if t + 1 < T:
             mu = update(X, z, mu)
     return z, mu
+
+
+def final_means(X, z, mu_last):
+    """Means of the final clusters, an empty cluster keeping mu_last (its
+    centroid in the last assignment): the starting centroids a warm-started
+    recomputation takes from the previous one (clusters change little between
+    adjacent diffusion steps, Sec. 5.2)."""
+    return update(np.asarray(X, dtype=np.float64), np.asarray(z), np.asarray(mu_last, np.float64))
 
 
 # --------------------------------------------------------------------------
@@ -374,26 +383,28 @@ def block_sparse_lse(Qp, Kp, q_offsets, k_offsets, rows, q_perm) -> np.ndarray:
 # --------------------------------------------------------------------------
 # whole head (Alg. 3 + Sec. 5.1 + Eq. (2))
 # --------------------------------------------------------------------------
-def cluster_queries(Q, C, T, seed, head):
-    """Euclidean k-means on the queries and their permutation (Sec. 5.2)."""
+def cluster_queries(Q, C, T, seed, head, mu0=None):
+    """Euclidean k-means on the queries and their permutation (Sec. 5.2);
+    ``mu0`` replaces the seeded init by given starting centroids."""
     Q = np.asarray(Q, dtype=np.float64)
     init = init_indices(Q.shape[0], C, seed, head, side=0)
-    z, mu = kmeans(Q, C, T, init)
+    z, mu = kmeans(Q, C, T, init, mu0=mu0)
     perm, off = stable_argsort(z, C)
     return {"labels": z, "perm": perm, "offsets": off, "mu": mu, "init": init}
 
 
 def cluster_keys(K, Q, C, T, seed, head, alpha=0.05, eps=1e-6, s_min=1e-12,
-                 realisation="cholesky"):
+                 realisation="cholesky", mu0=None):
     """QRKC (Alg. 3): k-means on K R, with Gbar = R R^T from the queries.
 
     realisation "sqrt" uses the symmetric square root instead of the
     Cholesky factor (App. D): the same distances, and defined for a
-    rank-deficient Gbar."""
+    rank-deficient Gbar.  ``mu0`` (original key space) replaces the seeded
+    init: the transformed starting centroids are mu0 R."""
     met = (query_metric if realisation == "cholesky" else query_metric_sqrt)(Q, alpha, eps, s_min)
     Kt = transform_keys(K, met["R"])
     init = init_indices(Kt.shape[0], C, seed, head, side=1)
-    z, mu = kmeans(Kt, C, T, init)
+    z, mu = kmeans(Kt, C, T, init, mu0=None if mu0 is None else transform_keys(mu0, met["R"]))
     perm, off = stable_argsort(z, C)
     return {"labels": z, "perm": perm, "offsets": off, "mu": mu, "init": init,
             "Kt": Kt, **met}

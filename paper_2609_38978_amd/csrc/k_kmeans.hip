@@ -102,6 +102,13 @@ __global__ __launch_bounds__(1024) void k_init_idx(int N, int C, uint64_t seed, 
   }
 }
 
+// plain float64 copy (warm-start centroids in, final means out)
+__global__ __launch_bounds__(256) void k_copy64(const double* __restrict__ src,
+                                                double* __restrict__ dst, long n) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+
 template <typename T>
 __global__ void k_seed_centroids(const T* __restrict__ X, const int* __restrict__ init, int N, int D,
                                  int C, double* __restrict__ mu) {
@@ -1145,9 +1152,15 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
                                hipStream_t st) {
   constexpr bool fast = sizeof(T) == 2;  // bf16 points: MFMA fast path + float64 refine
   const size_t plane = (size_t)H * C * D;
-  PARK_LAUNCH("kmeans_init", k_init_idx, dim3(H), dim3(1024), 0, st, N, C, seed, side, kb.init);
-  PARK_LAUNCH("kmeans_seed", k_seed_centroids<T>, dim3(C, H), dim3(D), 0, st, X,
-              (const int*)kb.init, N, D, C, kb.mu);
+  const long ncen = (long)H * C * D;
+  if (kb.mu_init) {  // warm start: the caller's centroids (the previous recompute's means)
+    PARK_LAUNCH("kmeans_warm", k_copy64, dim3((unsigned)((ncen + 255) / 256)), dim3(256), 0, st,
+                kb.mu_init, kb.mu, ncen);
+  } else {
+    PARK_LAUNCH("kmeans_init", k_init_idx, dim3(H), dim3(1024), 0, st, N, C, seed, side, kb.init);
+    PARK_LAUNCH("kmeans_seed", k_seed_centroids<T>, dim3(C, H), dim3(D), 0, st, X,
+                (const int*)kb.init, N, D, C, kb.mu);
+  }
   // refine grid: persistent workgroups per head looping over 64-token chunks
   int rg = (2048 + H - 1) / H;
   const int max_tiles = (N + 63) / 64;
@@ -1203,7 +1216,17 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
                   (int*)nullptr);
     }
   }
-  return launch_count_sort(kb.labels, H, N, C, kb.thist, kb.perm, kb.offsets, st);
+  PARK_TRY(launch_count_sort(kb.labels, H, N, C, kb.thist, kb.perm, kb.offsets, st));
+  if (kb.mu_out) {
+    // the means of the final clusters (an empty cluster keeps the centroid
+    // of the last assignment): the next recompute's warm start
+    PARK_LAUNCH("kmeans_warm", k_copy64, dim3((unsigned)((ncen + 255) / 256)), dim3(256), 0, st,
+                (const double*)kb.mu, kb.mu_out, ncen);
+    PARK_LAUNCH("segment_mean", (k_segment_mean<T, D>), dim3(C, H), dim3(256), 0, st, X,
+                (const int*)kb.perm, (const int*)kb.offsets, N, C, kb.mu_out, (float*)nullptr,
+                (int*)nullptr);
+  }
+  return PARK_OK;
 }
 
 park_status launch_kmeans(const void* X, const double* Gbar, int H, int N, int D, int dtype, int C,

@@ -76,6 +76,8 @@ struct KmeansBufs {
   int* flags;     // [H][N]    their indices, tile t's list at kmeans_tile * t
   float* flagu;   // [H][N]    and an upper bound of their smallest exact score
   const KfilterBufs* kf = nullptr;  // candidate filter (bf16 points; null: every round dense)
+  const double* mu_init = nullptr;  // [H][C][D] starting centroids (null: seeded init)
+  double* mu_out = nullptr;         // [H][C][D] receives the means of the final clusters
 };
 park_status launch_kmeans(const void* X, const double* Gbar /* null = Euclidean */, int H, int N,
                           int D, int dtype, int C, int T, uint64_t seed, int side,

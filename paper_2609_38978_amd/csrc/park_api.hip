@@ -367,7 +367,8 @@ static park_status cluster_body(const void* X, const void* Qm, const park_dims& 
                                 uint64_t seed, int side, int metric, double alpha, double eps,
                                 double s_min, int* labels, int* perm, int* offsets, double* R_out,
                                 float* Xt_out, void* ws, hipStream_t st,
-                                const ClusterWs* region = nullptr, int parts = 7) {
+                                const ClusterWs* region = nullptr, int parts = 7,
+                                const double* mu_init = nullptr, double* mu_out = nullptr) {
   const int H = dm.H, N = dm.N, D = dm.d;
   Carver cv(ws);
   int* status = cv.take<int>(64);
@@ -404,6 +405,8 @@ static park_status cluster_body(const void* X, const void* Qm, const park_dims& 
   kb.flags = cw.flags;
   kb.flagu = cw.flagu;
   kb.kf = &cw.kf;
+  kb.mu_init = mu_init;
+  kb.mu_out = mu_out;
   return launch_kmeans(X, Gbar, H, N, D, dm.dtype, C, T, seed, side, kb, st);
 }
 
@@ -463,7 +466,8 @@ park_status park_state_sizes(const park_dims* dims, int32_t CQ, int32_t CK, size
   const size_t b[PARK_STATE_NBUF] = {
       H * N * 4,            H * N * 4,            H * (CQ + 1) * 4,    H * (CK + 1) * 4,
       H * CK * D * 4,       H * CK * 4,           H * CQ * 4,          H * CQ * CK * 4,
-      H * N * D * el,       H * N * D * el,       H * N * D * el,      H * CQ * CK * 4};
+      H * N * D * el,       H * N * D * el,       H * N * D * el,      H * CQ * CK * 4,
+      H * CQ * D * 8,       H * CK * D * 8};
   for (int i = 0; i < PARK_STATE_NBUF; ++i) bytes[i] = b[i];
   return PARK_OK;
 }
@@ -621,6 +625,10 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
     return fail(PARK_ERR_INVALID_ARG, "unknown estimator %d", p->estimator);
   if (p->block_mode != PARK_BLOCKS_CLUSTER && p->block_mode != PARK_BLOCKS_FIXED)
     return fail(PARK_ERR_INVALID_ARG, "unknown block mode %d", p->block_mode);
+  if (p->init != PARK_INIT_SEEDED && p->init != PARK_INIT_WARM)
+    return fail(PARK_ERR_INVALID_ARG, "unknown init %d", p->init);
+  if (p->init == PARK_INIT_WARM && reuse == PARK_RECOMPUTE && (!s->q_mu || !s->k_mu))
+    return fail(PARK_ERR_INVALID_ARG, "PARK_INIT_WARM needs state.q_mu and state.k_mu");
   if (reuse < PARK_RECOMPUTE || reuse > PARK_REUSE_CLUSTERS_AND_MASK)
     return fail(PARK_ERR_INVALID_ARG, "unknown reuse mode %d", reuse);
   PARK_TRY(check_ptr(Q, "Q"));
@@ -639,6 +647,8 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
   PARK_TRY(check_ptr(s->Kp, "state.Kp"));
   PARK_TRY(check_ptr(s->Vp, "state.Vp"));
   PARK_TRY(check_opt_ptr(s->W, "state.W"));
+  PARK_TRY(check_opt_ptr(s->q_mu, "state.q_mu"));
+  PARK_TRY(check_opt_ptr(s->k_mu, "state.k_mu"));
   const int H = dims->H, N = dims->N, D = dims->d;
   PARK_TRY(check_ws(ws, ws_bytes, ws_bytes_for(H, N, D, p->CQ, p->CK)));
   hipStream_t st = (hipStream_t)stream;
@@ -663,16 +673,20 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
       PARK_TRY(ev_record(side->fork, st));
       PARK_TRY(ev_wait(sq, side->fork));
     }
+    // warm start: both sides from the previous recompute's means; either way
+    // the final means are left in state.q_mu / k_mu when they are given
+    const bool warm = p->init == PARK_INIT_WARM;
     park_status r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha,
                                  p->eps, p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr,
                                  nullptr, ws, st, &ck, 1);
     if (r == PARK_OK)
       r = cluster_body(Q, nullptr, *dims, p->CQ, p->T, p->seed, 0, PARK_METRIC_EUCLID, 0, 0, 1,
-                       nullptr, s->q_perm, s->q_offsets, nullptr, nullptr, ws, sq, &cq);
+                       nullptr, s->q_perm, s->q_offsets, nullptr, nullptr, ws, sq, &cq, 7,
+                       warm ? s->q_mu : nullptr, s->q_mu);
     if (r == PARK_OK)
       r = cluster_body(K, Q, *dims, p->CK, p->T, p->seed, 1, p->key_metric, p->alpha, p->eps,
                        p->s_min, nullptr, s->k_perm, s->k_offsets, nullptr, nullptr, ws, st, &ck,
-                       2);
+                       2, warm ? s->k_mu : nullptr, s->k_mu);
     if (side) {  // joined also after an error
       PARK_TRY(ev_record(side->join, sq));
       PARK_TRY(ev_wait(st, side->join));

@@ -22,6 +22,7 @@ PARK_SELECT_TOPK, PARK_SELECT_TOPP = 0, 1
 PARK_RECOMPUTE, PARK_REUSE_CLUSTERS, PARK_REUSE_CLUSTERS_AND_MASK = 0, 1, 2
 PARK_EST_PAMA, PARK_EST_QCENTROID = 0, 1
 PARK_BLOCKS_CLUSTER, PARK_BLOCKS_FIXED = 0, 1
+PARK_INIT_SEEDED, PARK_INIT_WARM = 0, 1
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpark.so")
 
@@ -50,13 +51,13 @@ class Params(C.Structure):
                 ("topk_ratio", C.c_double), ("topp", C.c_double), ("alpha", C.c_double),
                 ("eps", C.c_double), ("s_min", C.c_double), ("seed", C.c_uint64),
                 ("key_metric", C.c_int32), ("out_dtype", C.c_int32),
-                ("estimator", C.c_int32), ("block_mode", C.c_int32)]
+                ("estimator", C.c_int32), ("block_mode", C.c_int32), ("init", C.c_int32)]
 
 
 class State(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("q_perm", "k_perm", "q_offsets", "k_offsets",
                                           "k_centroids", "k_sizes", "kv_count", "kv_index",
-                                          "Qp", "Kp", "Vp", "W")]
+                                          "Qp", "Kp", "Vp", "W", "q_mu", "k_mu")]
 
 
 _lib = None
@@ -237,7 +238,7 @@ def park_block_sparse_attn_static(Qp, Kp, Vp, q_offsets, k_offsets, kv_count, kv
 
 
 STATE_FIELDS = ("q_perm", "k_perm", "q_offsets", "k_offsets", "k_centroids", "k_sizes",
-                "kv_count", "kv_index", "Qp", "Kp", "Vp", "W")
+                "kv_count", "kv_index", "Qp", "Kp", "Vp", "W", "q_mu", "k_mu")
 
 
 def park_state_sizes(H: int, N: int, d: int, dtype: int, CQ: int, CK: int) -> dict:
@@ -251,14 +252,17 @@ def park_state_sizes(H: int, N: int, d: int, dtype: int, CQ: int, CK: int) -> di
 
 def make_params(CQ, CK, T=10, select="topk", ratio=0.25, topp=0.9, alpha=0.05, eps=1e-6,
                 s_min=1e-12, seed=0, key_metric=PARK_METRIC_QRKC, out_dtype=PARK_F32,
-                estimator=PARK_EST_PAMA, block_mode=PARK_BLOCKS_CLUSTER) -> Params:
+                estimator=PARK_EST_PAMA, block_mode=PARK_BLOCKS_CLUSTER,
+                init=PARK_INIT_SEEDED) -> Params:
     sel = PARK_SELECT_TOPK if select in ("topk", PARK_SELECT_TOPK) else PARK_SELECT_TOPP
     return Params(CQ, CK, T, sel, ratio, topp, alpha, eps, s_min, seed, key_metric, out_dtype,
-                  estimator, block_mode)
+                  estimator, block_mode, init)
 
 
-def make_state(Q, CQ: int, CK: int, want_W: bool = False) -> dict:
-    """Caller-owned device buffers for park_forward (a dict of tensors)."""
+def make_state(Q, CQ: int, CK: int, want_W: bool = False, want_mu: bool = False) -> dict:
+    """Caller-owned device buffers for park_forward (a dict of tensors); want_mu
+    adds the float64 centroids a warm-started recomputation reads and every
+    recomputation writes."""
     H, N, d = Q.shape
     i32 = dict(dtype=torch.int32, **_dev(Q))
     st = {"q_perm": torch.empty(H, N, **i32), "k_perm": torch.empty(H, N, **i32),
@@ -267,12 +271,14 @@ def make_state(Q, CQ: int, CK: int, want_W: bool = False) -> dict:
           "k_sizes": torch.empty(H, CK, **i32), "kv_count": torch.empty(H, CQ, **i32),
           "kv_index": torch.empty(H, CQ, CK, **i32), "Qp": torch.empty_like(Q),
           "Kp": torch.empty_like(Q), "Vp": torch.empty_like(Q),
-          "W": torch.empty(H, CQ, CK, dtype=torch.float32, **_dev(Q)) if want_W else None}
+          "W": torch.empty(H, CQ, CK, dtype=torch.float32, **_dev(Q)) if want_W else None,
+          "q_mu": torch.empty(H, CQ, d, dtype=torch.float64, **_dev(Q)) if want_mu else None,
+          "k_mu": torch.empty(H, CK, d, dtype=torch.float64, **_dev(Q)) if want_mu else None}
     return st
 
 
 def _state_struct(st: dict) -> State:
-    return State(*[(None if st[n] is None else st[n].data_ptr()) for n, _ in State._fields_])
+    return State(*[(None if st.get(n) is None else st[n].data_ptr()) for n, _ in State._fields_])
 
 
 def park_forward(Q, K, V, params: Params, reuse: int = PARK_RECOMPUTE, state: dict | None = None,

@@ -123,7 +123,8 @@ def test_state_sizes():
     want = {"q_perm": H * N * 4, "k_perm": H * N * 4, "q_offsets": H * (CQ + 1) * 4,
             "k_offsets": H * (CK + 1) * 4, "k_centroids": H * CK * d * 4, "k_sizes": H * CK * 4,
             "kv_count": H * CQ * 4, "kv_index": H * CQ * CK * 4, "Qp": H * N * d * 2,
-            "Kp": H * N * d * 2, "Vp": H * N * d * 2, "W": H * CQ * CK * 4}
+            "Kp": H * N * d * 2, "Vp": H * N * d * 2, "W": H * CQ * CK * 4,
+            "q_mu": H * CQ * d * 8, "k_mu": H * CK * d * 8}
     assert dict(zip(P.STATE_FIELDS, out)) == want
     assert [f for f, _ in P.State._fields_] == list(P.STATE_FIELDS)
     assert L.park_state_sizes(C.byref(_dims(H, N, 64, P.PARK_F32)), CQ, CK, out, n) == P.PARK_OK
@@ -155,6 +156,13 @@ def test_forward_argument_errors():
     assert fwd(ws_bytes=64) == P.PARK_ERR_WORKSPACE
     assert L.park_forward(FAKE, FAKE, FAKE, C.byref(d), None, 0, C.byref(st), FAKE, FAKE, 1 << 40,
                           None) == P.PARK_ERR_INVALID_ARG
+    # a warm-started recomputation needs the centroid buffers of the state
+    warm = P.make_params(16, 16, init=P.PARK_INIT_WARM)
+    assert fwd(params=warm) == P.PARK_ERR_INVALID_ARG
+    assert b"q_mu" in L.park_last_error()
+    assert fwd(params=P.make_params(16, 16, init=5)) == P.PARK_ERR_INVALID_ARG
+    st3 = P.State(*([FAKE] * 11 + [None, FAKE + 8, FAKE]))  # q_mu misaligned
+    assert fwd(state=st3) == P.PARK_ERR_INVALID_ARG
 
 
 def test_schedule_step_host_logic():

@@ -203,3 +203,58 @@ def test_schedule_drives_recompute_and_reuse():
                 PT.rows_from_csr(st["kv_count"][i].cpu().numpy(), st["kv_index"][i].cpu().numpy()),
                 qp)
             assert np.abs(PT.np64(Og)[i] - Oref).max() <= 2e-2
+
+
+@pytest.mark.parametrize("name,grid,block", [("medium", (2, 16, 32), 64), ("medium", (2, 32, 64), 8)])
+def test_warm_start_matches_oracle(name, grid, block):
+    # a recomputation leaves the means of its final clusters in the state; the
+    # next one (drifted Q, K) starts both k-means from them.  Block 8 puts the
+    # layer above 512 clusters, where the rounds after the first are filtered.
+    cfg = synth.CONFIGS[name].with_(grid=grid, block=block)
+    q, k, v = synth.make_layer(cfg, [0, 1])
+    C, T = cfg.C, 4
+    print(f"[warm start N={cfg.N} C={C}]", flush=True)
+    Q, K, V = (PT.to_dev(a, cfg.dtype) for a in (q, k, v))
+    prm = P.make_params(C, C, T=T, select="topp", topp=0.9)
+    ws = P.workspace(Q, C, C)
+    st = P.make_state(Q, C, C, want_mu=True)
+    _, st = P.park_forward(Q, K, V, prm, state=st, ws=ws)
+    P.park_check(ws)
+    qmu, kmu = st["q_mu"].cpu().numpy(), st["k_mu"].cpu().numpy()
+    for i in range(2):  # stored means: the means of the final clusters
+        for X, side in ((q[i], "q"), (k[i], "k")):
+            perm = st[f"{side}_perm"][i].cpu().numpy()
+            off = st[f"{side}_offsets"][i].cpu().numpy()
+            mu = (qmu if side == "q" else kmu)[i]
+            for u in range(C):
+                if off[u + 1] > off[u]:
+                    want = X[perm[off[u]:off[u + 1]]].astype(np.float64).mean(0)
+                    assert np.allclose(mu[u], want, rtol=1e-12, atol=1e-12), (side, u)
+    # next step, warm-started from those means
+    pq = [synth.perturb_head(cfg, h, q[h], k[h], step=1) for h in range(2)]
+    q2, k2 = np.stack([a for a, _ in pq]), np.stack([b for _, b in pq])
+    Q2, K2 = PT.to_dev(q2, cfg.dtype), PT.to_dev(k2, cfg.dtype)
+    warm = P.make_params(C, C, T=T, select="topp", topp=0.9, init=P.PARK_INIT_WARM)
+    Og, st = P.park_forward(Q2, K2, V, warm, state=st, ws=ws)
+    P.park_check(ws)
+    for i in range(2):
+        rq = O.cluster_queries(q2[i], C, T, 0, i, mu0=qmu[i])
+        rk = O.cluster_keys(k2[i], q2[i], C, T, 0, i, mu0=kmu[i])
+        for side, r, X in (("q", rq, q2[i].astype(np.float64)), ("k", rk, rk["Kt"])):
+            perm = st[f"{side}_perm"][i].cpu().numpy()
+            off = st[f"{side}_offsets"][i].cpu().numpy()
+            z = np.empty(cfg.N, np.int64)
+            for u in range(C):
+                z[perm[off[u]:off[u + 1]]] = u
+            nm, nb, worst = PT.label_flips(X, r["mu"], z, r["labels"])
+            print(f"[warm start h={i} {side}] label mismatches={nm} not-exempt={nb}", flush=True)
+            assert nb == 0
+            p2, o2 = O.stable_argsort(z, C)
+            assert np.array_equal(p2, perm) and np.array_equal(o2, off)
+        kvc = st["kv_count"][i].cpu().numpy()
+        kvi = st["kv_index"][i].cpu().numpy()
+        qp, kp = st["q_perm"][i].cpu().numpy(), st["k_perm"][i].cpu().numpy()
+        qoff, koff = st["q_offsets"][i].cpu().numpy(), st["k_offsets"][i].cpu().numpy()
+        Oref = O.block_sparse_attention(q2[i][qp], k2[i][kp], v[i][kp], qoff, koff,
+                                        PT.rows_from_csr(kvc, kvi), qp)
+        assert np.abs(PT.np64(Og)[i] - Oref).max() <= 2e-2

@@ -811,3 +811,33 @@ def test_block_sparse_lse_pins():
     rows[0] = np.array([1])  # an empty key block only: nothing kept
     lse = O.block_sparse_lse(Q, K, qoff, koff, rows, perm)
     assert np.isneginf(lse[perm[:12]]).all()
+
+
+# ------------------------------------------------------------ warm start -----
+def test_warm_start_pins():
+    X = rng(100).standard_normal((300, 5))
+    init = O.init_indices(300, 12, seed=4, head=0, side=0)
+    # starting from the seeded centroids is the seeded run
+    z1, mu1 = O.kmeans(X, 12, 6, init)
+    z2, mu2 = O.kmeans(X, 12, 6, init, mu0=X[init])
+    assert np.array_equal(z1, z2) and np.array_equal(mu1, mu2)
+    # final means: brute force, empty clusters keep their centroid
+    z = z1.copy()
+    z[z == 3] = 4
+    m = O.final_means(X, z, mu1)
+    for v in range(12):
+        want = X[z == v].mean(0) if np.any(z == v) else mu1[v]
+        assert np.allclose(m[v], want, rtol=0, atol=1e-14)
+    # a warm start at a fixed point of Lloyd's iteration stays there
+    zc, muc = O.kmeans(X, 12, 60, init)
+    fixed = O.final_means(X, zc, muc)
+    z3, mu3 = O.kmeans(X, 12, 3, init, mu0=fixed)
+    assert np.array_equal(z3, zc) and np.allclose(mu3, fixed, atol=1e-14)
+    # keys: a warm start in the original key space is transformed by R
+    Q = rng(101).standard_normal((300, 5))
+    K = rng(102).standard_normal((300, 5))
+    r = O.cluster_keys(K, Q, 12, 4, 0, 0)
+    mu_in = O.final_means(K, r["labels"], r["mu"] @ np.linalg.inv(r["R"]))
+    r2 = O.cluster_keys(K, Q, 12, 2, 0, 0, mu0=mu_in)
+    zt = O.assign(r["Kt"], mu_in @ r["R"])
+    assert np.array_equal(r2["labels"], O.assign(r["Kt"], O.update(r["Kt"], zt, mu_in @ r["R"])))
