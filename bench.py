@@ -52,6 +52,8 @@ def parse():
                     help="blocks = k-means clusters, or fixed chunks of the cluster order")
     ap.add_argument("--key-metric", default="qrkc", choices=["qrkc", "euclid"],
                     help="key clustering: QRKC, or Euclidean k-means (the 'w/o QRKC' ablation)")
+    ap.add_argument("--alpha", type=float, default=0.05,
+                    help="shrinkage of the key metric toward the isotropic one (App. D)")
     ap.add_argument("--cpu-heads", type=int, default=None,
                     help="heads of the layer the oracle runs for the CPU baseline (default: 4 "
                          "below 50k tokens per head, else 1: about 10-30 s of host work)")
@@ -301,8 +303,10 @@ def main():
     param = cfg.ratio if mode == "topk" else cfg.topp
     reuse = {"recompute": P.PARK_RECOMPUTE, "clusters": P.PARK_REUSE_CLUSTERS,
              "mask": P.PARK_REUSE_CLUSTERS_AND_MASK}[args.reuse]
-    variant = {"estimator": args.estimator, "blocks": args.blocks, "key_metric": args.key_metric}
+    variant = {"estimator": args.estimator, "blocks": args.blocks, "key_metric": args.key_metric,
+               "alpha": args.alpha}
     prm = P.make_params(C, C, T=cfg.iters, select=mode, ratio=param, topp=param, seed=0,
+                        alpha=args.alpha,
                         out_dtype=P.PARK_BF16 if cfg.dtype == "bf16" else P.PARK_F32,
                         estimator={"pama": P.PARK_EST_PAMA,
                                    "qcentroid": P.PARK_EST_QCENTROID}[args.estimator],
@@ -415,7 +419,7 @@ def main():
                                   f"B={cfg.block} C={C} T={cfg.iters} {mode} {param}"
                                   + ("" if reuse == P.PARK_RECOMPUTE else f" reuse={args.reuse}")
                                   + "".join(f" {k}={v}" for k, v in variant.items()
-                                            if v not in ("pama", "cluster", "qrkc")),
+                                            if v not in ("pama", "cluster", "qrkc", 0.05)),
                       "H": cfg.H, "N": cfg.N, "d": cfg.d, "B": cfg.block, "C": C, "T": cfg.iters,
                       "select": mode, "param": param, "reuse": args.reuse, **variant},
            "dense_equiv_tflops": round(dense_flops / (ms * 1e-3) / 1e12, 3),

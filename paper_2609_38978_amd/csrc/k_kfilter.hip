@@ -23,6 +23,8 @@
 //   k_cand         the bit matrix of S_a on bf16 MFMA over split operands
 //   k_assign_cand  the certified bf16-MFMA assignment of each tile of sorted
 //                  tokens against the union of its clusters' candidate sets
+//   k_refine_union float64 labels of the tokens it cannot certify, against
+//                  the same union
 #include "common.h"
 #include "kernels.h"
 
@@ -44,6 +46,19 @@ __device__ __forceinline__ int kf_swz(int r) { return D == 128 ? (r & 15) : ((r 
 template <int N>
 __device__ __forceinline__ void kf_wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// OR of the candidate rows of clusters alo..ahi into uw[64] (LDS, cleared
+// before): word-parallel, each of the 256 threads ORs one word of every
+// fourth row in registers (independent loads), then one LDS atomic.  Rows
+// of empty clusters are all zero.
+__device__ __forceinline__ void kf_union_rows(const uint32_t* __restrict__ ch, int alo, int ahi,
+                                              int nwd, uint32_t* uw, int tid) {
+  const int word = tid & 63, ph = tid >> 6;
+  uint32_t x = 0u;
+  if (word < nwd)
+    for (int a = alo + ph; a <= ahi; a += 4) x |= ch[(size_t)a * 64 + word];
+  if (x) atomicOr(&uw[word], x);
 }
 
 // ------------------------------------------------------------ Gbar split
@@ -85,96 +100,113 @@ __global__ __launch_bounds__(256) void k_gsplit(const double* __restrict__ Gbar,
 // products) and the split residual, |y^_b - y_b| <= et sum_a |Gbar_ba x_a|,
 // et = 2^-16 1.01 + (2D + 1) 2^-23 1.0079 + 2^-24, and |x|^T |Gbar| |x| <=
 // gmax |x|^2, so xn = x . y^ + 1.01 et gmax |x|^2 is an upper bound.
-// Workgroup: 4 wavefronts x 128 tokens; Gbar's parts are read through L1/L2.
+// QRKC: a few workgroups per head, each keeping Gbar's two parts in LDS
+// (16-byte chunks of a row XOR-swizzled by the row, so the 16 rows of a
+// quarter-wavefront's operand read fall in distinct banks) and looping over
+// chunks of 512 tokens (4 wavefronts x 4 blocks of 32).
+template <int D>
+__global__ __launch_bounds__(256) void k_xnorm_euclid(const bf16_t* __restrict__ X, int N,
+                                                      double* __restrict__ xn) {
+  // |x|^2 in float64 (the squares of bf16 values are exact): 16 lanes per
+  // token, four tokens per step
+  constexpr int PE = D / 16;
+  const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  const int g = l >> 4, sub = l & 15;
+  for (int k = 0; k < 32; ++k) {
+    const int t = blockIdx.x * 512 + w * 128 + 4 * k + g;
+    const bool ok = t < N;
+    const bf16_t* r = X + ((size_t)h * N + (ok ? t : 0)) * D + PE * sub;
+    uint32_t q[PE / 2];
+    if constexpr (PE == 8) {
+      const uint4 raw = ok ? *(const uint4*)r : make_uint4(0u, 0u, 0u, 0u);
+      q[0] = raw.x; q[1] = raw.y; q[2] = raw.z; q[3] = raw.w;
+    } else {
+      const uint2 raw = ok ? *(const uint2*)r : make_uint2(0u, 0u);
+      q[0] = raw.x; q[1] = raw.y;
+    }
+    double s2 = 0.0;
+#pragma unroll
+    for (int e = 0; e < PE / 2; ++e) {
+      const double x0 = (double)__uint_as_float(q[e] << 16);
+      const double x1 = (double)__uint_as_float(q[e] & 0xffff0000u);
+      s2 = fma(x0, x0, fma(x1, x1, s2));
+    }
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) s2 += __shfl_xor(s2, o, 64);
+    if (sub == 0 && ok) xn[(size_t)h * N + t] = s2 * (1.0 + 1e-13);
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void k_xnorm(const bf16_t* __restrict__ X,
                                                const bf16_t* __restrict__ g2, size_t plane,
                                                const double* __restrict__ gmax, int N,
                                                double* __restrict__ xn) {
-  constexpr int KS = D / 16;
+  constexpr int KS = D / 16, CPR = D / 8;
   const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
   const int w = tid >> 6;
-  if (!g2) {
-    // |x|^2 in float64 (the squares of bf16 values are exact): 16 lanes per
-    // token, four tokens per step, 512 tokens per workgroup
-    constexpr int PE = D / 16;
-    const int g = l >> 4, sub = l & 15;
-    for (int k = 0; k < 32; ++k) {
-      const int t = blockIdx.x * 512 + w * 128 + 4 * k + g;
-      const bool ok = t < N;
-      const bf16_t* r = X + ((size_t)h * N + (ok ? t : 0)) * D + PE * sub;
-      uint32_t q[PE / 2];
-      if constexpr (PE == 8) {
-        const uint4 raw = ok ? *(const uint4*)r : make_uint4(0u, 0u, 0u, 0u);
-        q[0] = raw.x; q[1] = raw.y; q[2] = raw.z; q[3] = raw.w;
-      } else {
-        const uint2 raw = ok ? *(const uint2*)r : make_uint2(0u, 0u);
-        q[0] = raw.x; q[1] = raw.y;
-      }
-      double s2 = 0.0;
-#pragma unroll
-      for (int e = 0; e < PE / 2; ++e) {
-        const double x0 = (double)__uint_as_float(q[e] << 16);
-        const double x1 = (double)__uint_as_float(q[e] & 0xffff0000u);
-        s2 = fma(x0, x0, fma(x1, x1, s2));
-      }
-#pragma unroll
-      for (int o = 8; o > 0; o >>= 1) s2 += __shfl_xor(s2, o, 64);
-      if (sub == 0 && ok) xn[(size_t)h * N + t] = s2 * (1.0 + 1e-13);
+  const int nchunk = (N + 511) / 512;
+  __shared__ __attribute__((aligned(16))) bf16_t Gs[2 * D * D];
+  {
+    const bf16_t* G1 = g2 + (size_t)h * D * D;
+    for (int e = tid; e < 2 * D * CPR; e += 256) {
+      const int part = e / (D * CPR), rem = e % (D * CPR), row = rem / CPR, c = rem % CPR;
+      const uint4 v = *(const uint4*)(G1 + part * plane + (size_t)row * D + 8 * c);
+      *(uint4*)(Gs + part * D * D + row * D + 8 * (c ^ kf_swz<D>(row))) = v;
     }
-    return;
   }
-  // four blocks of 32 tokens per wavefront share every Gbar fragment
-  const bf16_t* G1 = g2 + (size_t)h * D * D;
-  const bf16_t* G2 = G1 + plane;
+  __syncthreads();
+  const bf16_t* L1 = Gs;
+  const bf16_t* L2 = Gs + D * D;
   constexpr double ET = 1.52587890625e-05 * 1.01 + (2 * D + 1) * 1.1920928955078125e-07 * 1.0079 +
                         5.9604644775390625e-08;
   const double gm = gmax[h];
-  for (int tb = 0; tb < 4; ++tb) {
-    const int t = blockIdx.x * 512 + w * 128 + 32 * tb + c32;
-    const bool ok = t < N;
-    const bf16_t* r = X + ((size_t)h * N + (ok ? t : 0)) * D;
-    kf_bf16x8_t xf[KS];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-      if (ok) raw = *(const uint4*)(r + 16 * s + 8 * hf);
-      xf[s] = __builtin_bit_cast(kf_bf16x8_t, raw);
-    }
-    double acc64 = 0.0, xx = 0.0;
-#pragma unroll
-    for (int rt = 0; rt < D / 32; ++rt) {
-      kf_f32x16_t y;
-#pragma unroll
-      for (int q = 0; q < 16; ++q) y[q] = 0.0f;
-      const size_t ro = (size_t)(32 * rt + c32) * D + 8 * hf;
+  for (int ck = blockIdx.x; ck < nchunk; ck += gridDim.x)
+    for (int tb = 0; tb < 4; ++tb) {
+      const int t = ck * 512 + w * 128 + 32 * tb + c32;
+      const bool ok = t < N;
+      const bf16_t* r = X + ((size_t)h * N + (ok ? t : 0)) * D;
+      kf_bf16x8_t xf[KS];
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        const kf_bf16x8_t a2 = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(G2 + ro + 16 * s));
-        y = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, xf[s], y, 0, 0, 0);
+        uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+        if (ok) raw = *(const uint4*)(r + 16 * s + 8 * hf);
+        xf[s] = __builtin_bit_cast(kf_bf16x8_t, raw);
       }
+      double acc64 = 0.0, xx = 0.0;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const kf_bf16x8_t a1 = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(G1 + ro + 16 * s));
-        y = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xf[s], y, 0, 0, 0);
-      }
-      // lane holds y at rows 32 rt + 8 b + 4 hf + r of token c32
+      for (int rt = 0; rt < D / 32; ++rt) {
+        kf_f32x16_t y;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const uint2 raw = ok ? *(const uint2*)(r + 32 * rt + 8 * b + 4 * hf) : make_uint2(0u, 0u);
-        const float xv[4] = {__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xffff0000u),
-                             __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xffff0000u)};
+        for (int q = 0; q < 16; ++q) y[q] = 0.0f;
+        const int row = 32 * rt + c32, ro = row * D, sw = kf_swz<D>(row);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc64 = fma((double)xv[q], (double)y[4 * b + q], acc64);
-          xx = fma((double)xv[q], (double)xv[q], xx);
+        for (int s = 0; s < KS; ++s) {
+          const kf_bf16x8_t a2 = *(const kf_bf16x8_t*)(L2 + ro + 8 * ((2 * s + hf) ^ sw));
+          y = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, xf[s], y, 0, 0, 0);
+        }
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const kf_bf16x8_t a1 = *(const kf_bf16x8_t*)(L1 + ro + 8 * ((2 * s + hf) ^ sw));
+          y = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xf[s], y, 0, 0, 0);
+        }
+        // lane holds y at rows 32 rt + 8 b + 4 hf + r of token c32
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const uint2 raw = ok ? *(const uint2*)(r + 32 * rt + 8 * b + 4 * hf) : make_uint2(0u, 0u);
+          const float xv[4] = {__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xffff0000u),
+                               __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xffff0000u)};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            acc64 = fma((double)xv[q], (double)y[4 * b + q], acc64);
+            xx = fma((double)xv[q], (double)xv[q], xx);
+          }
         }
       }
+      acc64 += __shfl_xor(acc64, 32, 64);
+      xx += __shfl_xor(xx, 32, 64);
+      if (hf == 0 && ok) xn[(size_t)h * N + t] = acc64 + 1.01 * ET * gm * xx;
     }
-    acc64 += __shfl_xor(acc64, 32, 64);
-    xx += __shfl_xor(xx, 32, 64);
-    if (hf == 0 && ok) xn[(size_t)h * N + t] = acc64 + 1.01 * ET * gm * xx;
-  }
 }
 
 // ------------------------------------------------------------ cluster radii
@@ -274,103 +306,126 @@ __global__ __launch_bounds__(256) void k_radius(const bf16_t* __restrict__ X,
 // and of the sum below 1e-12 of the magnitudes involved,
 //   D(mu_a, mu_v)^2 >= lo = b_a + b_v - 2 t^ - 2 ec |mu_a| |w_v|
 //                           - 1e-12 (|b_a| + |b_v| + |mu_a| |w_a| + |mu_v| |w_v|).
-// v is dropped when lo > 4 r2[a] (1 + 1e-9) + 1e-9 (|b_a| + |b_v|): then its
-// exact score exceeds mu_a's by far more than the float64 scores can err, so
-// the float64 argmin never needs it either.  v = a is always kept; rows of
-// empty clusters (r2 < 0) are left unwritten (no token reads them).
-// Workgroup: one 32-cluster tile a0 (B operand: mu parts) and a group of 16
-// centroid tiles v0 (A operand: w parts), four per wavefront, the next
-// tile's operands loaded while one is scored.
+// v is dropped from S_a when lo > 4 r2[a] (1 + 1e-9) + 1e-9 (|b_a| + |b_v|):
+// then its exact score exceeds mu_a's by far more than the float64 scores
+// can err, so the float64 argmin never needs it either.  v = a is always
+// kept; rows of empty clusters (r2 < 0) are all zero.  The distance is
+// symmetric (t^ bounds mu_v . w_a = mu_a . w_v as well), so each pair of
+// tiles is computed once: the pair (A, V) with V >= A writes word V of the
+// rows of A (test with r2[a]) and, for V > A, word A of the rows of V (test
+// with r2[v], bits gathered across lanes by ballots).  Every word of every
+// row has exactly one writer.
+// Workgroup: one 32-cluster tile A (the B operand: mu parts, in LDS for the
+// four wavefronts) and a group of 16 centroid tiles (the A operand: w parts,
+// four per wavefront).
 template <int D>
-__global__ __launch_bounds__(256) void k_cand(const bf16_t* __restrict__ m2, size_t mplane,
-                                              const bf16_t* __restrict__ w3, size_t wplane,
-                                              const float* __restrict__ mn,
-                                              const float* __restrict__ wn, int Cpad,
-                                              const double* __restrict__ b,
-                                              const double* __restrict__ r2, int C,
-                                              uint32_t* __restrict__ cand) {
-  constexpr int KS = D / 16;
+__global__ __launch_bounds__(256, 2) void k_cand(const bf16_t* __restrict__ m2, size_t mplane,
+                                                 const bf16_t* __restrict__ w3, size_t wplane,
+                                                 const float* __restrict__ mn,
+                                                 const float* __restrict__ wn, int Cpad,
+                                                 const double* __restrict__ b,
+                                                 const double* __restrict__ r2, int C,
+                                                 uint32_t* __restrict__ cand) {
+  constexpr int KS = D / 16, CPR = D / 8;
   constexpr double EC = 3.2 * 1.52587890625e-05 + (3 * D + 1) * 1.1920928955078125e-07 * 1.02;
   const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
   const int w = tid >> 6;
-  const int a0 = blockIdx.x * 32, a = a0 + c32;
+  const int at = blockIdx.x, a0 = at * 32, a = a0 + c32;
+  const int nvt = (C + 31) / 32;
+  const int vt_beg = max(at, (int)blockIdx.z * 16), vt_end = min(nvt, (int)(blockIdx.z + 1) * 16);
+  if (vt_beg >= vt_end) return;  // the transposed writes of other tile pairs cover these
   const bool aval = a < C;
   const int ar = aval ? a : C - 1;
-  kf_bf16x8_t m1f[KS], m2f[KS];
-  const bf16_t* M1 = m2 + ((size_t)h * C + ar) * D + 8 * hf;
-#pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    m1f[s] = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(M1 + 16 * s));
-    m2f[s] = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(M1 + mplane + 16 * s));
+  // the tile's centroids in two bf16 parts, 16-byte chunks swizzled by the row
+  __shared__ __attribute__((aligned(16))) bf16_t Ms[2 * 32 * D];
+  for (int e = tid; e < 2 * 32 * CPR; e += 256) {
+    const int part = e / (32 * CPR), rem = e % (32 * CPR), row = rem / CPR, c = rem % CPR;
+    const int rr = min(a0 + row, C - 1);
+    const uint4 v = *(const uint4*)(m2 + part * mplane + ((size_t)h * C + rr) * D + 8 * c);
+    *(uint4*)(Ms + part * 32 * D + row * D + 8 * (c ^ kf_swz<D>(row))) = v;
   }
   const double ra = aval ? r2[(size_t)h * C + a] : -1.0;
   const double ba = b[(size_t)h * C + ar];
   const double man = (double)mn[(size_t)h * C + ar];
   const double ana = man * (double)wn[(size_t)h * Cpad + ar];
   uint32_t* crow = cand + ((size_t)h * C + ar) * 64;
-  // b_v, |w_v| and |mu_v| |w_v| of this workgroup's 16 centroid tiles, read once
-  __shared__ double vb_s[512], vw_s[512], vm_s[512];
-  const int nvt = (C + 31) / 32;
-  const int vt_end = min(nvt, (int)(blockIdx.z + 1) * 16);
+  // b_v, |w_v|, |mu_v| |w_v| and r2[v] of this workgroup's 16 centroid tiles
+  __shared__ double vb_s[512], vw_s[512], vm_s[512], vr_s[512];
   for (int e = tid; e < 512; e += 256) {
-    const int vr = min((int)blockIdx.z * 512 + e, C - 1);
+    const int v = (int)blockIdx.z * 512 + e, vr = min(v, C - 1);
     const double wv = (double)wn[(size_t)h * Cpad + vr];
     vb_s[e] = b[(size_t)h * C + vr];
     vw_s[e] = wv;
     vm_s[e] = (double)mn[(size_t)h * C + vr] * wv;
+    vr_s[e] = v < C ? r2[(size_t)h * C + v] : -1.0;
   }
   __syncthreads();
-  // operands of the next centroid tile are loaded while this one is scored
-  kf_bf16x8_t w1n[KS], w2n[KS];
-  auto load_w = [&](int vt, kf_bf16x8_t* f1, kf_bf16x8_t* f2) {
-    const int vr = min(vt * 32 + c32, C - 1);
-    const bf16_t* W1 = w3 + ((size_t)h * C + vr) * D + 8 * hf;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      f1[s] = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(W1 + 16 * s));
-      f2[s] = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(W1 + wplane + 16 * s));
-    }
-  };
-  int vt = blockIdx.z * 16 + w;
-  if (vt < vt_end) load_w(vt, w1n, w2n);
-  for (; vt < vt_end; vt += 4) {
+  const int rowo = c32 * D, swk = kf_swz<D>(c32);
+  const bf16_t* M1 = Ms;
+  const bf16_t* M2 = Ms + 32 * D;
+  for (int vt = vt_beg + w; vt < vt_end; vt += 4) {
     const int v0 = vt * 32;
     kf_bf16x8_t w1f[KS], w2f[KS];
+    {
+      const int vr = min(v0 + c32, C - 1);
+      const bf16_t* W1 = w3 + ((size_t)h * C + vr) * D + 8 * hf;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      w1f[s] = w1n[s];
-      w2f[s] = w2n[s];
+      for (int s2 = 0; s2 < KS; ++s2) {
+        w1f[s2] = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(W1 + 16 * s2));
+        w2f[s2] = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(W1 + wplane + 16 * s2));
+      }
     }
-    if (vt + 4 < vt_end) load_w(vt + 4, w1n, w2n);
 
     kf_f32x16_t acc;
 #pragma unroll
     for (int q = 0; q < 16; ++q) acc[q] = 0.0f;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w2f[s], m1f[s], acc, 0, 0, 0);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1f[s], m2f[s], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1f[s], m1f[s], acc, 0, 0, 0);
+    for (int s2 = 0; s2 < KS; ++s2) {
+      const kf_bf16x8_t m1 = *(const kf_bf16x8_t*)(M1 + rowo + 8 * ((2 * s2 + hf) ^ swk));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w2f[s2], m1, acc, 0, 0, 0);
     }
-    // lane: pairs (a, v0 + 8 bq + 4 hf + r)
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2) {
+      const int co = rowo + 8 * ((2 * s2 + hf) ^ swk);
+      const kf_bf16x8_t m1 = *(const kf_bf16x8_t*)(M1 + co);
+      const kf_bf16x8_t mm2 = *(const kf_bf16x8_t*)(M2 + co);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1f[s2], mm2, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1f[s2], m1, acc, 0, 0, 0);
+    }
+    // lane: pairs (a, v0 + 8 bq + 4 hf + r) for q = 4 bq + r
     uint32_t bits = 0u;
+    uint32_t tw[16];  // transposed: bit (a, v) of row v, by q
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const int vi = 8 * (q >> 2) + 4 * hf + (q & 3), v = v0 + vi;
       const int li = v0 - (int)blockIdx.z * 512 + vi;
-      if (v < C && ra >= 0.0) {
-        const double bv = vb_s[li];
-        const double wnv = vw_s[li];
-        const double t = (double)acc[q];
-        const double lo = ba + bv - 2.0 * t - 2.0 * EC * man * wnv -
-                          1e-12 * (fabs(ba) + fabs(bv) + ana + vm_s[li]);
-        const bool keep = v == a || !(lo > 4.0 * ra * (1.0 + 1e-9) + 1e-9 * (fabs(ba) + fabs(bv)));
-        bits |= keep ? (1u << (8 * (q >> 2) + 4 * hf + (q & 3))) : 0u;
-      }
+      const double bv = vb_s[li];
+      const double t = (double)acc[q];
+      const double lo = ba + bv - 2.0 * t - 2.0 * EC * man * vw_s[li] -
+                        1e-12 * (fabs(ba) + fabs(bv) + ana + vm_s[li]);
+      const double gap = 1e-9 * (fabs(ba) + fabs(bv));
+      const bool inr = v < C && aval;
+      const bool keep = inr && ra >= 0.0 && (v == a || !(lo > 4.0 * ra * (1.0 + 1e-9) + gap));
+      const double rv = vr_s[li];
+      const bool keept = inr && rv >= 0.0 && !(lo > 4.0 * rv * (1.0 + 1e-9) + gap);
+      bits |= keep ? (1u << vi) : 0u;
+      const unsigned long long bal = __ballot(keept);
+      tw[q] = (uint32_t)(hf == 0 ? bal : (bal >> 32));
     }
     bits |= (uint32_t)__shfl_xor((int)bits, 32, 64);
-    if (hf == 0 && aval && ra >= 0.0) crow[vt] = bits;
+    if (hf == 0 && aval) crow[vt] = bits;
+    if (vt > at) {
+      // word `at` of the rows v of this tile: lane (hf, r, bq) with c32 =
+      // 8 bq + r (r < 4) writes row v0 + 8 bq + 4 hf + r
+      const int r = c32 & 7, bq = c32 >> 3;
+      if (r < 4) {
+        const int vi = 8 * bq + 4 * hf + r;
+        uint32_t word = 0u;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) word = (q == 4 * bq + r) ? tw[q] : word;
+        if (v0 + vi < C) cand[((size_t)h * C + v0 + vi) * 64 + at] = word;
+      }
+    }
   }
 }
 
@@ -385,9 +440,14 @@ __global__ __launch_bounds__(256) void k_cand(const bf16_t* __restrict__ m2, siz
 // exact argmin over all centroids; the certification uses the maxima of the
 // error terms over all centroids.  Uncertified tokens are listed for the
 // float64 refinement as before.
-// workgroups per CU of the two-part filtered assignment (its LDS allows 3)
+// workgroups per CU of the two-part filtered assignment (its LDS allows 3;
+// 3 caps it at 168 registers, which spills, and measured no faster than 2)
+// bf16 parts of w in the filtered assignment at C >= 512 (3 below)
+#ifndef PARK_KM_CAND_NP
+#define PARK_KM_CAND_NP 2
+#endif
 #ifndef PARK_KM_CAND_OCC
-#define PARK_KM_CAND_OCC 3
+#define PARK_KM_CAND_OCC 2
 #endif
 template <int D, int NP>
 __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_cand(
@@ -395,8 +455,9 @@ __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_
     const float* __restrict__ b32, int Cpad, const float* __restrict__ wn,
     const float* __restrict__ eb, const float* __restrict__ bmax, int nbm, int N, int C,
     const int* __restrict__ perm, const uint32_t* __restrict__ cand,
-    const double* __restrict__ r2, int* __restrict__ labels, int* __restrict__ flags,
-    float* __restrict__ flagu, int* __restrict__ nflag) {
+    int* __restrict__ labels, int* __restrict__ flags,
+    float* __restrict__ flagu, int* __restrict__ nflag, const double* __restrict__ xn,
+    unsigned long long* __restrict__ dmax) {
   constexpr int TB = PARK_KM_TB, CT = 32, KS = D / 16, CPR = D / 8, RPI = 64 / CPR;
   constexpr int NI = NP * CT / (4 * RPI);
   static_assert(NI * 4 * RPI == NP * CT && (NP == 2 || NP == 3), "tile shape");
@@ -415,6 +476,7 @@ __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_
   __shared__ int seg[2];
   __shared__ float mx_s[2];
   __shared__ int wcnt[4];
+  __shared__ unsigned long long dm_s[64];  // radius bounds of clusters alo .. alo + 63
   const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int p0 = blockIdx.x * kmeans_tile;
@@ -428,19 +490,14 @@ __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_
     seg[0] = (unsigned)ta < (unsigned)N ? zh[ta] : 0;
     seg[1] = (unsigned)tb < (unsigned)N ? zh[tb] : C - 1;
   }
-  if (tid < 64) uw[tid] = 0u;
+  if (tid < 64) {
+    uw[tid] = 0u;
+    dm_s[tid] = 0ull;
+  }
   __syncthreads();
   const int alo = min(max(seg[0], 0), C - 1), ahi = min(max(seg[1], alo), C - 1);
-  const uint32_t* ch = cand + (size_t)h * C * 64;
-  const double* rh = r2 + (size_t)h * C;
   const int nwd = (C + 31) / 32;
-  for (int e = tid; e < (ahi - alo + 1) * nwd; e += 256) {
-    const int a = alo + e / nwd, word = e % nwd;
-    if (rh[a] >= 0.0) {
-      const uint32_t x = ch[(size_t)a * 64 + word];
-      if (x) atomicOr(&uw[word], x);
-    }
-  }
+  kf_union_rows(cand + (size_t)h * C * 64, alo, ahi, nwd, uw, tid);
   __syncthreads();
   if (tid < 64) {
     const uint32_t x = tid * 32 < C ? uw[tid] : 0u;
@@ -626,14 +683,24 @@ __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_
     ubv[tb] = INFINITY;
     if (hf == 0 && tok >= 0) {
       bool ok = false;
+      float e1 = 0.0f;
       if (bidx[tb] >= 0 && isfinite(best[tb])) {
         const int v = bidx[tb];
-        const float e1 = fmaf(kx[tb], wn[(size_t)h * Cpad + v], eb[(size_t)h * Cpad + v]);
+        e1 = fmaf(kx[tb], wn[(size_t)h * Cpad + v], eb[(size_t)h * Cpad + v]);
         const float emax = fmaf(kx[tb], nmax, ebmax) * 1.0001f;
         ubv[tb] = best[tb] + e1;
         ok = (L[tb] - emax) > ubv[tb];
       }
-      if (ok) labels[(size_t)h * N + tok] = bidx[tb];
+      if (ok) {
+        const int v = bidx[tb];
+        labels[(size_t)h * N + tok] = v;
+        // D(x, mu_v)^2 <= x^T Gbar x + (the exact score's upper bound); the
+        // 1e-6 e1 term covers the float64 score against the exact one
+        const double d2 = fmax(xn[(size_t)h * N + tok] + (double)ubv[tb] + 1e-6 * (double)e1, 0.0);
+        const unsigned long long bits = (unsigned long long)__double_as_longlong(d2);
+        if ((unsigned)(v - alo) < 64u) atomicMax(&dm_s[v - alo], bits);
+        else atomicMax(&dmax[(size_t)h * C + v], bits);
+      }
       fl[tb] = !ok;
     }
   }
@@ -646,6 +713,8 @@ __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_
   }
   if (l == 0) wcnt[w] = tot;
   __syncthreads();
+  if (tid < 64 && alo + tid < C && dm_s[tid] != 0ull)
+    atomicMax(&dmax[(size_t)h * C + alo + tid], dm_s[tid]);
   int base = blockIdx.x * kmeans_tile;
   for (int q = 0; q < w; ++q) base += wcnt[q];
   if (tid == 0) nflag[(size_t)h * gridDim.x + blockIdx.x] = wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
@@ -663,6 +732,342 @@ __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_
   }
 }
 
+// ------------------------------------------------------------ refine on the union
+// Exact float64 labels of the tokens k_assign_cand could not certify.  A
+// listed token keeps its previous label a (the assignment wrote only the
+// certified ones), and S_a holds all its minimisers (top of this file), so
+// the union of the listed tokens' sets holds every listed token's exact
+// argmin.  As in the all-centroid refine (k_refine_cand), every exact score
+// lies in [s^_v - E_v, s^_v + E_v] with s^_v on the three-part split of w
+// (same error constant), so with U the listed upper bound of a token's
+// smallest exact score its argmin lies in {v : s^_v - E_v <= U}; those
+// candidates (near-ties leave two or three) are scored in float64 in the
+// all-centroid refine's order (16 lanes per pair, D/16 consecutive
+// dimensions each, a butterfly over the 16), and the smallest score, ties to
+// the lowest id, is the label.  A token with more than KMAX candidates is
+// scored against every union row in the same way.
+// One wavefront per tile of sorted tokens (a head's tiles on one XCD), no
+// LDS ring: each lane reads its union row's three bf16 parts of w directly
+// (the A operand of a 32x32x16 MFMA, 32 union rows per step) against 32
+// listed tokens (the B operand).  A tile whose union exceeds kUnionMaxRows or
+// whose work (token chunks x row steps) exceeds kUnionRefineMax keeps its
+// list for the all-centroid refine, which runs next; a tile handled here
+// clears its list length.
+constexpr int kUnionMaxRows = 512;
+constexpr int kUnionRefineMax = 16;
+
+template <int D>
+__global__ __launch_bounds__(64) void k_refine_union(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ w3, size_t plane,
+    const float* __restrict__ b32, const float* __restrict__ wn, const float* __restrict__ eb,
+    int Cpad, const double* __restrict__ w64, const double* __restrict__ b64,
+    const uint32_t* __restrict__ cand, int H, int N, int C, int NT, const int* __restrict__ flags,
+    const float* __restrict__ flagu, int* __restrict__ nflag, int* __restrict__ labels,
+    int* __restrict__ status, const double* __restrict__ xn,
+    unsigned long long* __restrict__ dmax) {
+  constexpr int KS = D / 16;  // k-steps of a 32x32x16 chain
+  constexpr int TC = 32;      // listed tokens per chunk
+  constexpr int KMAX = 4;     // candidates kept per token
+  constexpr int PL = 16, PE = D / PL, KP = 4;
+  constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f;
+  constexpr float ET = U24 * 1.01f + (D + 1) * DEL * 1.0079f +
+                       0.00390625f * 1.01f * (2 * D + 1) * DEL + U24 * 1.01f;
+  constexpr float KXC = 1.1f * (2.0f * ET + 2.01f * U24) * 1.0001f;
+  static_assert(PE == 4 || PE == 8, "lane slice");
+  __shared__ uint16_t ul[kUnionMaxRows];
+  __shared__ float ubs[kUnionMaxRows], uns[kUnionMaxRows], ues[kUnionMaxRows];
+  __shared__ int dl[kmeans_tile];
+  __shared__ int ccount[TC], cpos[TC * KMAX], ptk[TC * KMAX], ppos[TC * KMAX];
+  __shared__ double cs[TC * KMAX];
+  __shared__ int ctok[TC], over[TC], pst[TC];
+  __shared__ float cx2[TC];
+  __shared__ double obest[TC];
+  __shared__ int oidx[TC];
+  const int l = threadIdx.x, hf = l >> 5, c32 = l & 31;
+  const int nitems = H * NT, per = (nitems + 7) >> 3;
+  const int item = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (item >= nitems) return;
+  const int h = item / NT, t = item - h * NT;
+  const int p0 = t * kmeans_tile, pend = min(N, p0 + kmeans_tile);
+  const int n = min(max(nflag[(size_t)h * NT + t], 0), pend - p0);
+  if (n <= 0) return;
+  const int* fh = flags + (size_t)h * N + p0;
+  const float* fu = flagu + (size_t)h * N + p0;
+  int* zh = labels + (size_t)h * N;
+  // distinct previous labels of the listed tokens (non-decreasing along the
+  // list, which follows the sorted order; a repeat only costs a second OR)
+  int nd = 0, last = -1;
+  for (int i0 = 0; i0 < n; i0 += 64) {
+    const int i = i0 + l;
+    int a = -1;
+    if (i < n) {
+      const int tk = fh[i];
+      if ((unsigned)tk < (unsigned)N) {
+        const int z = zh[tk];
+        a = (unsigned)z < (unsigned)C ? z : -1;
+      }
+    }
+    int prev = __shfl_up(a, 1, 64);
+    if (l == 0) prev = last;
+    const bool st = a >= 0 && a != prev;
+    const unsigned long long bal = __ballot(st);
+    if (st) dl[nd + __popcll(bal & ((1ull << l) - 1ull))] = a;
+    nd += __popcll(bal);
+    last = __shfl(a, 63, 64);
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // dl complete for every lane
+  // union of their candidate sets: lane = word of the bit rows
+  const int nwd = (C + 31) / 32;
+  uint32_t bits = 0u;
+  if (l < nwd)
+    for (int k = 0; k < nd; ++k) bits |= cand[((size_t)h * C + dl[k]) * 64 + l];
+  int inc = __popc(bits);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (l >= o) inc += y;
+  }
+  const int U = __shfl(inc, 63, 64);
+  const int nrt = (U + 31) / 32;
+  if (U > kUnionMaxRows || ((n + TC - 1) / TC) * nrt > kUnionRefineMax)
+    return;  // left to the all-centroid refine
+  {
+    int pos = inc - __popc(bits);
+    while (bits) {
+      const int bit = __ffs(bits) - 1;
+      ul[pos++] = (uint16_t)(l * 32 + bit);
+      bits &= bits - 1u;
+    }
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // ul complete
+  for (int j = l; j < U; j += 64) {
+    const int v = ul[j];
+    ubs[j] = b32[(size_t)h * Cpad + v];
+    uns[j] = wn[(size_t)h * Cpad + v];
+    ues[j] = eb[(size_t)h * Cpad + v];
+  }
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+  const bf16_t* Xh = X + (size_t)h * N * D;
+  const bf16_t* Wh = w3 + (size_t)h * C * D;
+  const double* wh = w64 + (size_t)h * C * D;
+  const double* bh = b64 + (size_t)h * C;
+  const int g = l >> 4, sub = l & 15;
+  for (int i0 = 0; i0 < n; i0 += TC) {
+    // token c32 of the chunk: the B operand (dims 16 s + 8 hf) and its bound
+    const int i = i0 + c32;
+    int tok = i < n ? fh[i] : -1;
+    tok = (unsigned)tok < (unsigned)N ? tok : -1;
+    float Ub = tok >= 0 ? fu[i] : -INFINITY;
+    if (Ub != Ub) Ub = INFINITY;  // NaN: every row is a candidate
+    kf_bf16x8_t xf[KS];
+    float xsq = 0.0f;
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2) {
+      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+      if (tok >= 0) raw = *(const uint4*)(Xh + (size_t)tok * D + 16 * s2 + 8 * hf);
+      xf[s2] = __builtin_bit_cast(kf_bf16x8_t, raw);
+      const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
+        xsq = fmaf(lo, lo, fmaf(hi, hi, xsq));
+      }
+    }
+    xsq += __shfl_xor(xsq, 32, 64);
+    const float kx = KXC * sqrtf(xsq);
+    if (hf == 0) {
+      ccount[c32] = 0;
+      ctok[c32] = tok;
+      cx2[c32] = xsq;
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    // candidates: union rows 32 rt + 8 bq + 4 hf + r of token c32 (q = 4 bq + r)
+    for (int rt = 0; rt < nrt; ++rt) {
+      const int v = ul[min(32 * rt + c32, U - 1)];
+      const bf16_t* A1 = Wh + (size_t)v * D + 8 * hf;
+      kf_f32x16_t ahi, arest;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        ahi[q] = 0.0f;
+        arest[q] = 0.0f;
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < KS; ++s2) {
+        const kf_bf16x8_t a1 = __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(A1 + 16 * s2));
+        const kf_bf16x8_t a2 =
+            __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(A1 + plane + 16 * s2));
+        const kf_bf16x8_t a3 =
+            __builtin_bit_cast(kf_bf16x8_t, *(const uint4*)(A1 + 2 * plane + 16 * s2));
+        ahi = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xf[s2], ahi, 0, 0, 0);
+        arest = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, xf[s2], arest, 0, 0, 0);
+        arest = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, xf[s2], arest, 0, 0, 0);
+      }
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int pos = 32 * rt + 8 * (q >> 2) + 4 * hf + (q & 3);
+        if (pos < U && tok >= 0) {
+          const float sc = fmaf(-2.0f, ahi[q] + arest[q], ubs[pos]);
+          const float er = fmaf(kx, uns[pos], ues[pos]);
+          if (!(sc - er > Ub)) {
+            const int k = atomicAdd(&ccount[c32], 1);
+            if (k < KMAX) cpos[c32 * KMAX + k] = pos;
+          }
+        }
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    // pairs of the tokens with 1 .. KMAX candidates; the others over the union
+    int np = 0, nover = 0;
+    {
+      const int nc = l < TC ? ccount[l] : 0;
+      const bool tv = l < TC && ctok[l] >= 0;
+      const bool packed = tv && nc >= 1 && nc <= KMAX;
+      const int mine = packed ? nc : 0;
+      int pinc = mine;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(pinc, o, 64);
+        if (l >= o) pinc += y;
+      }
+      for (int j = 0; j < mine; ++j) {
+        ptk[pinc - mine + j] = l;
+        ppos[pinc - mine + j] = cpos[l * KMAX + j];
+      }
+      if (l < TC) pst[l] = pinc - mine;
+      np = __shfl(pinc, 63, 64);
+      const bool ov = tv && !packed;
+      const unsigned long long bo = __ballot(ov);
+      if (ov) over[__popcll(bo & ((1ull << l) - 1ull))] = l;
+      nover = __popcll(bo);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    // float64 scores of the pairs, 16 lanes each, KP pairs per group and pass
+    for (int base = 0; base < np; base += 4 * KP) {
+      double a[KP];
+      int pp[KP];
+#pragma unroll
+      for (int k = 0; k < KP; ++k) {
+        const int p = base + 4 * k + g;
+        pp[k] = p < np ? p : -1;
+        a[k] = 0.0;
+        if (p < np) {
+          const int tk = ctok[ptk[p]];
+          const int v = ul[ppos[p]];
+          uint32_t q[PE / 2];
+          if constexpr (PE == 8) {
+            const uint4 xu = *(const uint4*)(Xh + (size_t)tk * D + sub * PE);
+            q[0] = xu.x;
+            q[1] = xu.y;
+            q[2] = xu.z;
+            q[3] = xu.w;
+          } else {
+            const uint2 xu = *(const uint2*)(Xh + (size_t)tk * D + sub * PE);
+            q[0] = xu.x;
+            q[1] = xu.y;
+          }
+          const double* wr = wh + (size_t)v * D + sub * PE;
+#pragma unroll
+          for (int e = 0; e < PE / 2; ++e) {
+            a[k] = fma((double)__uint_as_float(q[e] << 16), wr[2 * e], a[k]);
+            a[k] = fma((double)__uint_as_float(q[e] & 0xffff0000u), wr[2 * e + 1], a[k]);
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < KP; ++k) {
+        double tt = a[k];
+#pragma unroll
+        for (int o = PL / 2; o > 0; o >>= 1) tt += __shfl_xor(tt, o, 64);
+        if (sub == 0 && pp[k] >= 0) cs[pp[k]] = fma(-2.0, tt, bh[ul[ppos[pp[k]]]]);
+      }
+    }
+    // tokens with too many candidates: every union row, 16 lanes per row
+    for (int k = 0; k < nover; ++k) {
+      const int ot = over[k], tk = ctok[ot];
+      uint32_t q[PE / 2];
+      if constexpr (PE == 8) {
+        const uint4 xu = *(const uint4*)(Xh + (size_t)tk * D + sub * PE);
+        q[0] = xu.x;
+        q[1] = xu.y;
+        q[2] = xu.z;
+        q[3] = xu.w;
+      } else {
+        const uint2 xu = *(const uint2*)(Xh + (size_t)tk * D + sub * PE);
+        q[0] = xu.x;
+        q[1] = xu.y;
+      }
+      double bb = INFINITY;
+      int bi = 0x7fffffff;
+      for (int j0 = g; j0 - g < U; j0 += 4) {
+        const int j = min(j0, U - 1);
+        const int v = ul[j];
+        const double* wr = wh + (size_t)v * D + sub * PE;
+        double acc = 0.0;
+#pragma unroll
+        for (int e = 0; e < PE / 2; ++e) {
+          acc = fma((double)__uint_as_float(q[e] << 16), wr[2 * e], acc);
+          acc = fma((double)__uint_as_float(q[e] & 0xffff0000u), wr[2 * e + 1], acc);
+        }
+#pragma unroll
+        for (int o = PL / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+        const double sc = fma(-2.0, acc, bh[v]);
+        if (j0 < U && (sc < bb || (sc == bb && v < bi))) {
+          bb = sc;
+          bi = v;
+        }
+      }
+#pragma unroll
+      for (int o = 16; o < 64; o <<= 1) {
+        const double ob = __shfl_xor(bb, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ob < bb || (ob == bb && oi < bi)) {
+          bb = ob;
+          bi = oi;
+        }
+      }
+      if (l == 0) {
+        obest[ot] = bb;
+        oidx[ot] = bi;
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    // labels: the smallest float64 score, ties to the lowest id
+    if (l < TC && ctok[l] >= 0) {
+      const int tk = ctok[l], nc = ccount[l];
+      double bb = INFINITY;
+      int bi = 0x7fffffff;
+      if (nc >= 1 && nc <= KMAX) {
+        for (int j = 0; j < nc; ++j) {
+          const double sc = cs[pst[l] + j];
+          const int v = ul[cpos[l * KMAX + j]];
+          if (sc < bb || (sc == bb && v < bi)) {
+            bb = sc;
+            bi = v;
+          }
+        }
+      } else {
+        bb = obest[l];
+        bi = oidx[l];
+      }
+      if (!isfinite(bb) || (unsigned)bi >= (unsigned)C) {
+        raise_status(status, ST_NONFINITE);
+        bi = 0;
+      } else {
+        // radius bound of the next round: x^T Gbar x + the float64 score,
+        // with a margin far above its rounding error
+        const double d2 = fmax(xn[(size_t)h * N + tk] + bb +
+                                   1e-12 * (fabs(bh[bi]) + 2.0 * sqrt((double)cx2[l]) *
+                                                               (double)wn[(size_t)h * Cpad + bi]),
+                               0.0);
+        atomicMax(&dmax[(size_t)h * C + bi], (unsigned long long)__double_as_longlong(d2));
+      }
+      zh[tk] = bi;
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // LDS lists consumed before the next chunk
+  }
+  if (l == 0) nflag[(size_t)h * NT + t] = 0;
+}
+
 // ---------------------------------------------------------------- launchers
 park_status launch_kfilter_setup(const bf16_t* X, const double* Gbar, int H, int N, int D,
                                  const KfilterBufs& kf, hipStream_t st) {
@@ -675,62 +1080,88 @@ park_status launch_kfilter_setup(const bf16_t* X, const double* Gbar, int H, int
       PARK_LAUNCH("kfilter_gsplit", k_gsplit<64>, dim3(H), dim3(256), 0, st, Gbar, kf.g2, gplane,
                   kf.gmax);
   }
-  const dim3 g((N + 511) / 512, H);
+  // QRKC: 16 workgroups per head, each with Gbar in LDS for all its chunks
+  const int nchunk = (N + 511) / 512;
+  const dim3 g(Gbar ? (nchunk < 16 ? nchunk : 16) : nchunk, H);
   const bf16_t* g2 = Gbar ? kf.g2 : nullptr;
-  if (D == 128)
+  if (!Gbar) {
+    if (D == 128)
+      PARK_LAUNCH("kfilter_xnorm", k_xnorm_euclid<128>, g, dim3(256), 0, st, X, N, kf.xn);
+    else
+      PARK_LAUNCH("kfilter_xnorm", k_xnorm_euclid<64>, g, dim3(256), 0, st, X, N, kf.xn);
+  } else if (D == 128) {
     PARK_LAUNCH("kfilter_xnorm", k_xnorm<128>, g, dim3(256), 0, st, X, g2, gplane,
                 (const double*)kf.gmax, N, kf.xn);
-  else
+  } else {
     PARK_LAUNCH("kfilter_xnorm", k_xnorm<64>, g, dim3(256), 0, st, X, g2, gplane,
                 (const double*)kf.gmax, N, kf.xn);
+  }
   return PARK_OK;
 }
 
 park_status launch_kfilter_round(const bf16_t* X, int H, int N, int D, int C,
-                                 const KmeansBufs& kb, const KfilterBufs& kf, hipStream_t st) {
+                                 const KmeansBufs& kb, const KfilterBufs& kf, bool measure_radius,
+                                 hipStream_t st) {
   const int Cpad = kmeans_cpad(C);
   const size_t plane = (size_t)H * C * D;
   const int nbm = (C + 15) / 16;
   const dim3 gr((C + 3) / 4, H), gc((C + 31) / 32, H, ((C + 31) / 32 + 15) / 16),
       ga((N + kmeans_tile - 1) / kmeans_tile, H);
+  // refine on the union: one wavefront per tile, a head's tiles on one XCD
+  const int NT = (N + kmeans_tile - 1) / kmeans_tile;
+  const dim3 gu(8 * ((H * NT + 7) / 8));
   if (D == 128) {
-    PARK_LAUNCH("kfilter_radius", k_radius<128>, gr, dim3(256), 0, st, X, (const int*)kb.perm,
-                (const int*)kb.offsets, (const double*)kf.xn, (const double*)kb.w,
-                (const double*)kb.b, N, C, kf.r2);
+    if (measure_radius)
+      PARK_LAUNCH("kfilter_radius", k_radius<128>, gr, dim3(256), 0, st, X, (const int*)kb.perm,
+                  (const int*)kb.offsets, (const double*)kf.xn, (const double*)kb.w,
+                  (const double*)kb.b, N, C, kf.r2);
     PARK_LAUNCH("kfilter_cand", k_cand<128>, gc, dim3(256), 0, st, (const bf16_t*)kf.m2, plane,
                 (const bf16_t*)kb.w3, plane, (const float*)kf.mn, (const float*)kb.wn, Cpad,
                 (const double*)kb.b, (const double*)kf.r2, C, kf.cand);
-    if (C >= 512)
+    if (C >= 512 && PARK_KM_CAND_NP == 2)
       PARK_LAUNCH("kmeans_assign_cand", (k_assign_cand<128, 2>), ga, dim3(256), 0, st, X,
                   (const bf16_t*)kb.w3, plane, (const float*)kb.b32, Cpad, (const float*)kb.wn,
                   (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C, (const int*)kb.perm,
-                  (const uint32_t*)kf.cand, (const double*)kf.r2, kb.labels, kb.flags, kb.flagu,
-                  kb.nflag);
+                  (const uint32_t*)kf.cand, kb.labels, kb.flags, kb.flagu,
+                  kb.nflag, (const double*)kf.xn, kf.dmax);
     else
       PARK_LAUNCH("kmeans_assign_cand", (k_assign_cand<128, 3>), ga, dim3(256), 0, st, X,
                   (const bf16_t*)kb.w3, plane, (const float*)kb.b32, Cpad, (const float*)kb.wn,
                   (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C, (const int*)kb.perm,
-                  (const uint32_t*)kf.cand, (const double*)kf.r2, kb.labels, kb.flags, kb.flagu,
-                  kb.nflag);
+                  (const uint32_t*)kf.cand, kb.labels, kb.flags, kb.flagu,
+                  kb.nflag, (const double*)kf.xn, kf.dmax);
+    PARK_LAUNCH("kmeans_refine_union", k_refine_union<128>, gu, dim3(64), 0, st, X,
+                (const bf16_t*)kb.w3, plane, (const float*)kb.b32, (const float*)kb.wn,
+                (const float*)kb.eb, Cpad, (const double*)kb.w, (const double*)kb.b,
+                (const uint32_t*)kf.cand, H, N, C, NT, (const int*)kb.flags,
+                (const float*)kb.flagu, kb.nflag, kb.labels, kb.status, (const double*)kf.xn,
+                kf.dmax);
   } else {
-    PARK_LAUNCH("kfilter_radius", k_radius<64>, gr, dim3(256), 0, st, X, (const int*)kb.perm,
-                (const int*)kb.offsets, (const double*)kf.xn, (const double*)kb.w,
-                (const double*)kb.b, N, C, kf.r2);
+    if (measure_radius)
+      PARK_LAUNCH("kfilter_radius", k_radius<64>, gr, dim3(256), 0, st, X, (const int*)kb.perm,
+                  (const int*)kb.offsets, (const double*)kf.xn, (const double*)kb.w,
+                  (const double*)kb.b, N, C, kf.r2);
     PARK_LAUNCH("kfilter_cand", k_cand<64>, gc, dim3(256), 0, st, (const bf16_t*)kf.m2, plane,
                 (const bf16_t*)kb.w3, plane, (const float*)kf.mn, (const float*)kb.wn, Cpad,
                 (const double*)kb.b, (const double*)kf.r2, C, kf.cand);
-    if (C >= 512)
+    if (C >= 512 && PARK_KM_CAND_NP == 2)
       PARK_LAUNCH("kmeans_assign_cand", (k_assign_cand<64, 2>), ga, dim3(256), 0, st, X,
                   (const bf16_t*)kb.w3, plane, (const float*)kb.b32, Cpad, (const float*)kb.wn,
                   (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C, (const int*)kb.perm,
-                  (const uint32_t*)kf.cand, (const double*)kf.r2, kb.labels, kb.flags, kb.flagu,
-                  kb.nflag);
+                  (const uint32_t*)kf.cand, kb.labels, kb.flags, kb.flagu,
+                  kb.nflag, (const double*)kf.xn, kf.dmax);
     else
       PARK_LAUNCH("kmeans_assign_cand", (k_assign_cand<64, 3>), ga, dim3(256), 0, st, X,
                   (const bf16_t*)kb.w3, plane, (const float*)kb.b32, Cpad, (const float*)kb.wn,
                   (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C, (const int*)kb.perm,
-                  (const uint32_t*)kf.cand, (const double*)kf.r2, kb.labels, kb.flags, kb.flagu,
-                  kb.nflag);
+                  (const uint32_t*)kf.cand, kb.labels, kb.flags, kb.flagu,
+                  kb.nflag, (const double*)kf.xn, kf.dmax);
+    PARK_LAUNCH("kmeans_refine_union", k_refine_union<64>, gu, dim3(64), 0, st, X,
+                (const bf16_t*)kb.w3, plane, (const float*)kb.b32, (const float*)kb.wn,
+                (const float*)kb.eb, Cpad, (const double*)kb.w, (const double*)kb.b,
+                (const uint32_t*)kf.cand, H, N, C, NT, (const int*)kb.flags,
+                (const float*)kb.flagu, kb.nflag, kb.labels, kb.status, (const double*)kf.xn,
+                kf.dmax);
   }
   return PARK_OK;
 }

@@ -119,11 +119,21 @@ __global__ void k_seed_centroids(const T* __restrict__ X, const int* __restrict_
 
 // w_v = Gbar mu_v (or mu_v), b_v = mu_v . w_v;  16 centroids per workgroup.
 // Gbar is symmetric, so thread (a, group) reads column a of it coalesced and
-// applies each element to 16 / (256 / D) centroids.  `wT` (optional) receives
-// w transposed, [D][C] per head, for the float64 refinement.  When `w3` is
-// given the fast-path operands are written too: w_v split into three bf16
-// parts (three planes of H*C*D), b_v in float, |w_v| rounded up and the
-// |b_v| term of the error bound (see k_assign_fast).
+// applies each element to 16 / (256 / D) centroids.  When `w3` is given the
+// fast-path operands are written too: w_v split into three bf16 parts (three
+// planes of H*C*D), b_v in float, |w_v| rounded up and the |b_v| term of the
+// error bound (see k_assign_fast); `m2`/`mn` give the candidate filter the
+// centroids in two bf16 parts and |mu_v|.
+//
+// Cluster radii for the candidate filter (rmode 2): the previous assignment
+// left in dmax[a] an upper bound of max D(x, mu_a^old)^2 over the tokens it
+// labelled a, and by the triangle inequality every such token has
+// D(x, mu_a) <= sqrt(dmax[a]) + D(mu_a^old, mu_a).  The move is
+// D(mu_old, mu)^2 = b - 2 mu . w_old + b_old (w_old, b_old: this buffer's
+// values before the update), rounded up by a margin of 1e-9 of the
+// magnitudes involved; r2[a] = (sqrt(dmax) + move)^2, rounded up, or -1 for
+// a cluster the sort left empty.  rmode >= 1 then clears dmax for the
+// coming assignment.
 template <int D, int NT>
 __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
                                               const double* __restrict__ Gbar, int C,
@@ -132,7 +142,10 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
                                               size_t plane, float* __restrict__ b32, int Cpad,
                                               float* __restrict__ wn, float* __restrict__ eb,
                                               float* __restrict__ bmax, bf16_t* __restrict__ m2,
-                                              float* __restrict__ mn) {
+                                              float* __restrict__ mn,
+                                              const int* __restrict__ offsets,
+                                              double* __restrict__ r2,
+                                              unsigned long long* __restrict__ dmax, int rmode) {
   // NT threads: D lanes per centroid group, 16 / (NT / D) centroids per
   // thread.  1024 threads shorten each thread's float64 chain over the D
   // columns (small grids); 256 read the metric rows fewer times (large grids)
@@ -168,7 +181,7 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
     ws[r][a] = acc[k];
     if (v0 + r < C) {
       const size_t o = ((size_t)h * C + v0 + r) * D + a;
-      w[o] = acc[k];
+      // (w itself is written at the end: the radius bound reads the old w)
       if (w3) {
         // w = w1 + w2 + w3 + r with bf16 parts and |r| <= 2^-24 |w| (1 + 2^-7)
         const bf16_t p1 = f2bf((float)acc[k]);
@@ -193,18 +206,46 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
   if (tid < 256) {
     constexpr int LPC = 256 / CB;
     const int r = tid / LPC, sub = tid % LPC;
-    double s = 0.0, n2 = 0.0, m2s = 0.0;
+    double s = 0.0, n2 = 0.0, m2s = 0.0, dso = 0.0, dsa = 0.0;
+    const double* wold = w + ((size_t)h * C + min(v0 + r, C - 1)) * D;
 #pragma unroll
     for (int c = sub; c < D; c += LPC) {
       s = fma(ms[r][c], ws[r][c], s);
       n2 = fma(ws[r][c], ws[r][c], n2);
       m2s = fma(ms[r][c], ms[r][c], m2s);
+      if (rmode == 2) {
+        const double wo = wold[c];
+        dso = fma(ms[r][c], wo, dso);
+        dsa += fabs(ms[r][c] * wo);
+      }
     }
 #pragma unroll
     for (int o = LPC / 2; o > 0; o >>= 1) {
       s += __shfl_xor(s, o, 64);
       n2 += __shfl_xor(n2, o, 64);
       m2s += __shfl_xor(m2s, o, 64);
+      if (rmode == 2) {
+        dso += __shfl_xor(dso, o, 64);
+        dsa += __shfl_xor(dsa, o, 64);
+      }
+    }
+    if (rmode >= 1 && sub == 0 && v0 + r < C) {
+      const size_t cidx = (size_t)h * C + v0 + r;
+      if (rmode == 2) {
+        const int* off = offsets + (size_t)h * (C + 1);
+        const int n = off[v0 + r + 1] - off[v0 + r];
+        double rr = -1.0;
+        if (n > 0) {
+          const double bo = b[cidx];  // b before the update (this thread writes it below)
+          const double mv2 = s - 2.0 * dso + bo + 1e-9 * (fabs(s) + fabs(bo) + 2.0 * dsa);
+          const double mv = sqrt(fmax(mv2, 0.0)) * (1.0 + 1e-12);
+          const double dm = fmax(__longlong_as_double((long long)dmax[cidx]), 0.0);
+          const double R = sqrt(dm) * (1.0 + 1e-12) + mv;
+          rr = R * R * (1.0 + 1e-12);
+        }
+        r2[cidx] = rr;
+      }
+      dmax[cidx] = 0ull;
     }
     if (mn && sub == 0 && v0 + r < C) mn[(size_t)h * C + v0 + r] = (float)(sqrt(m2s) * (1.0 + 1e-6));
     float fnr = 0.0f, fer = 0.0f;
@@ -224,6 +265,11 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
     }
   }
   __syncthreads();
+  // w itself (the reduction above has read the old values)
+  for (int e = tid; e < CB * D; e += NT) {
+    const int r = e / D, a = e % D;
+    if (v0 + r < C) w[((size_t)h * C + v0 + r) * D + a] = ws[r][a];
+  }
   float fn = tid < CB ? fnl[tid] : 0.0f, fe = tid < CB ? fel[tid] : 0.0f;
   if (b32 && blockIdx.x == gridDim.x - 1)  // padding centroids: score +inf, no error term
     for (int v = C + tid; v < Cpad; v += NT) {
@@ -581,7 +627,9 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
                                                      const int* __restrict__ flags,
                                                      const float* __restrict__ flagu,
                                                      const int* __restrict__ nflag,
-                                                     int* __restrict__ labels, int* status) {
+                                                     int* __restrict__ labels, int* status,
+                                                     const double* __restrict__ xn,
+                                                     unsigned long long* __restrict__ dmax) {
   constexpr int CT = 32, KS = D / 32, CPR = D / 8, RPI = 64 / CPR;
   constexpr int NI = 3 * CT / (4 * RPI);  // DMAs per wavefront and tile
   constexpr int NS = PARK_KM_NS;
@@ -608,6 +656,7 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
   __shared__ int ridx[4];
   __shared__ int wsc[4];
   __shared__ int spos[TC];  // list position of each slot of the chunk (-1: none)
+  __shared__ float cx2[TC];  // |x|^2 of each slot's token
   // after the sweep the ring holds the pair lists and float64 scores
   double* const cs = (double*)&Wt[0][0];  // [TC * KMAX] scores of the packed pairs
   int* const ptl = (int*)(cs + TC * KMAX);  // [TC * KMAX] token slot of each pair
@@ -723,6 +772,7 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
       if (g == 0) {
         ccount[tl] = 0;
         ctok[tl] = tok;
+        cx2[tl] = xsq;
       }
     }
     if (tid == 0) nover = 0;
@@ -818,9 +868,19 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
           a[k] = 0.0;
           if (p < np) {
             const int tok = ctok[ptl[p]];
-            const uint4 xu = *(const uint4*)(Xh + (size_t)tok * D + sub * PE);
+            uint32_t q[PE / 2];  // this lane's PE dimensions, two bf16 per word
+            if constexpr (PE == 8) {
+              const uint4 xu = *(const uint4*)(Xh + (size_t)tok * D + sub * PE);
+              q[0] = xu.x;
+              q[1] = xu.y;
+              q[2] = xu.z;
+              q[3] = xu.w;
+            } else {
+              const uint2 xu = *(const uint2*)(Xh + (size_t)tok * D + sub * PE);
+              q[0] = xu.x;
+              q[1] = xu.y;
+            }
             const double* wr = wh + (size_t)pv[p] * D + sub * PE;
-            const uint32_t q[4] = {xu.x, xu.y, xu.z, xu.w};
 #pragma unroll
             for (int e = 0; e < PE / 2; ++e) {
               a[k] = fma((double)__uint_as_float(q[e] << 16), wr[2 * e], a[k]);
@@ -905,6 +965,13 @@ __global__ __launch_bounds__(256) void k_refine_cand(const bf16_t* __restrict__ 
         if (!isfinite(bb) || (unsigned)bi >= (unsigned)C) {
           raise_status(status, ST_NONFINITE);
           bi = 0;
+        } else if (dmax) {
+          // radius bound of the next filtered round (see k_prep)
+          const double d2 = fmax(xn[(size_t)h * N + tok] + bb +
+                                     1e-12 * (fabs(b64h[bi]) +
+                                              2.0 * sqrt((double)cx2[tid]) * (double)nh[bi]),
+                                 0.0);
+          atomicMax(&dmax[(size_t)h * C + bi], (unsigned long long)__double_as_longlong(d2));
         }
         labels[(size_t)h * N + tok] = bi;
       }
@@ -1146,6 +1213,13 @@ static bool kmeans_filter_enabled() {
   return !(e && e[0] == '0');
 }
 
+// PARK_KFILTER_EXACT_RADIUS=1 measures every round's radii with k_radius
+// instead of bounding them from the previous assignment (the same labels)
+static bool kfilter_exact_radius() {
+  const char* e = getenv("PARK_KFILTER_EXACT_RADIUS");
+  return e && e[0] == '1';
+}
+
 template <typename T, int D>
 static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int C, int T_,
                                uint64_t seed, int side, const KmeansBufs& kb, int* status,
@@ -1170,25 +1244,33 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
   // where the dense sweep is MFMA-bound (C >= 512); below that the dense
   // round is a few tens of microseconds and the filter's passes cost more
   const bool filt = fast && kb.kf != nullptr && C >= 512 && kmeans_filter_enabled();
+  const bool exact_radius = kfilter_exact_radius();
   if constexpr (fast)
     if (filt) PARK_TRY(launch_kfilter_setup((const bf16_t*)X, Gbar, H, N, D, *kb.kf, st));
   bf16_t* m2 = filt ? kb.kf->m2 : nullptr;
   float* mn = filt ? kb.kf->mn : nullptr;
   for (int t = 0; t < T_; ++t) {
     const int nbm = (C + 15) / 16;
+    // radii: round 1 measures them (k_radius); later rounds bound them from
+    // the previous assignment's distances and the centroids' moves
+    const int rmode = !filt || t == 0 ? 0 : (t == 1 || exact_radius ? 1 : 2);
+    double* r2 = filt ? kb.kf->r2 : nullptr;
+    unsigned long long* dmax = filt ? kb.kf->dmax : nullptr;
     if ((long)nbm * H < 512)
       PARK_LAUNCH("kmeans_prep", (k_prep<D, 1024>), dim3(nbm, H), dim3(1024), 0, st,
                   (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane,
                   fast ? kb.b32 : nullptr, kmeans_cpad(C), fast ? kb.wn : nullptr,
-                  fast ? kb.eb : nullptr, kb.hmax, m2, mn);
+                  fast ? kb.eb : nullptr, kb.hmax, m2, mn, (const int*)kb.offsets, r2, dmax,
+                  rmode);
     else
       PARK_LAUNCH("kmeans_prep", (k_prep<D, 256>), dim3(nbm, H), dim3(256), 0, st,
                   (const double*)kb.mu, Gbar, C, kb.w, kb.b, fast ? kb.w3 : nullptr, plane,
                   fast ? kb.b32 : nullptr, kmeans_cpad(C), fast ? kb.wn : nullptr,
-                  fast ? kb.eb : nullptr, kb.hmax, m2, mn);
+                  fast ? kb.eb : nullptr, kb.hmax, m2, mn, (const int*)kb.offsets, r2, dmax,
+                  rmode);
     if constexpr (fast) {
       if (filt && t > 0)
-        PARK_TRY(launch_kfilter_round((const bf16_t*)X, H, N, D, C, kb, *kb.kf, st));
+        PARK_TRY(launch_kfilter_round((const bf16_t*)X, H, N, D, C, kb, *kb.kf, rmode == 1, st));
       else if (C >= 512)
         PARK_LAUNCH("kmeans_assign_fast", (k_assign_fast<D, 2>), dim3((N + kmeans_tile - 1) / kmeans_tile, H),
                     dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
@@ -1203,7 +1285,9 @@ static park_status kmeans_impl(const T* X, const double* Gbar, int H, int N, int
                   dim3(256), 0, st, (const bf16_t*)X, (const bf16_t*)kb.w3, plane,
                   (const float*)kb.b32, (const float*)kb.wn, (const float*)kb.eb, kmeans_cpad(C),
                   (const double*)kb.w, (const double*)kb.b, H, N, C, rg, (const int*)kb.flags,
-                  (const float*)kb.flagu, (const int*)kb.nflag, kb.labels, status);
+                  (const float*)kb.flagu, (const int*)kb.nflag, kb.labels, status,
+                  filt && t > 0 ? (const double*)kb.kf->xn : nullptr,
+                  filt && t > 0 ? kb.kf->dmax : nullptr);
     } else {
       PARK_LAUNCH("kmeans_assign64", (k_assign64<T, D, 64>), dim3((N + 63) / 64, H), dim3(256), 0, st,
                   X, (const double*)kb.w, (const double*)kb.b, N, C, (const int*)nullptr,

@@ -54,6 +54,10 @@ struct KfilterBufs {
   uint32_t* cand;   // [H][C][64] candidate-set bit rows
   bf16_t* m2;       // [2][H][C][D] centroids in two bf16 parts
   float* mn;        // [H][C] |mu_v| rounded up
+  // [H][C] bit patterns of non-negative doubles: per cluster, the largest
+  // upper bound of D(x, mu_a)^2 over the tokens an assignment gave label a
+  // (the radius of the next round, before the centroid's move)
+  unsigned long long* dmax;
 };
 
 struct KmeansBufs {
@@ -135,8 +139,11 @@ park_status launch_kfilter_setup(const bf16_t* X, const double* Gbar, int H, int
                                  const KfilterBufs& kf, hipStream_t st);
 // one round t >= 1: radii, candidate sets, filtered assignment (listing the
 // uncertified tokens for k_refine_cand as the dense assignment does)
+// measure_radius: r2 from k_radius (otherwise k_prep has bounded it from the
+// previous assignment's distances)
 park_status launch_kfilter_round(const bf16_t* X, int H, int N, int D, int C,
-                                 const KmeansBufs& kb, const KfilterBufs& kf, hipStream_t st);
+                                 const KmeansBufs& kb, const KfilterBufs& kf, bool measure_radius,
+                                 hipStream_t st);
 
 // k_probe.hip ---------------------------------------------------------------
 park_status launch_probe_exp2(const float* x, float* y, long n, hipStream_t st);

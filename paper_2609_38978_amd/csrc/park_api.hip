@@ -164,6 +164,7 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   c.kf.cand = cv.take<uint32_t>((size_t)H * C * 64);
   c.kf.m2 = cv.take<bf16_t>((size_t)2 * H * C * D);
   c.kf.mn = cv.take<float>((size_t)H * C);
+  c.kf.dmax = cv.take<unsigned long long>((size_t)H * C);
   return c;
 }
 
@@ -301,10 +302,9 @@ static park_status static_scratch(void** out) {
 }
 
 // ------------------------------------------------------------ side stream
-// The query side's clustering and the Cholesky factor of the key side's
-// metric run on a second stream of the device, beside the key side's Gbar
-// and k-means on the caller's stream: they share nothing but the status word,
-// which kernels only OR into, and Gbar, which all of them only read.  The stream
+// The query side's clustering runs on a second stream of the device, beside
+// the key side's metric Gbar and k-means on the caller's stream: the two
+// share nothing but the status word, which kernels only OR into.  The stream
 // (default priority) and its fork/join events are created on the first call
 // that is not being captured; until then the sides run one after the other.
 // A call holds the device's lock while it queues its work, so concurrent calls

@@ -452,6 +452,42 @@ def test_rank_deficient_metric_clusters_like_the_square_root(dtype, N, d, C):
     assert np.array_equal(st["k_perm"][0].cpu().numpy(), out["perm"][0].cpu().numpy())
 
 
+# App. D: the shrinkage alpha moves the key metric from the query-response
+# metric (alpha = 0) to the isotropic one (alpha = 1).  Queries spread along
+# two directions make the partitions differ along the sweep; C = 640 runs the
+# candidate filter.  At alpha = 1 the partition is the Euclidean one.
+@pytest.mark.parametrize("alpha,C", [(0.0, 64), (0.05, 64), (0.25, 64), (0.5, 64), (1.0, 64),
+                                     (0.25, 640)])
+def test_alpha_sweep_key_clustering_matches_oracle(alpha, C):
+    r = np.random.default_rng(21)
+    H, N, d, T = 2, 4096, 128, 5
+    basis = np.linalg.qr(r.standard_normal((d, 2)))[0]
+    q = 3.0 * r.standard_normal((H, N, 2)) @ basis.T + 0.05 * r.standard_normal((H, N, d))
+    cent = 2.0 * r.standard_normal((48, d))
+    k = cent[r.integers(0, 48, (H, N))] + 0.5 * r.standard_normal((H, N, d))
+    Q, K = PT.to_dev(q.astype(np.float32), "bf16"), PT.to_dev(k.astype(np.float32), "bf16")
+    qh, kh = PT.np64(Q), PT.np64(K)
+    print(f"[alpha sweep alpha={alpha} N={N} C={C}]", flush=True)
+    out = P.park_cluster_keys(K, C, T, seed=3, side=1, metric=P.PARK_METRIC_QRKC, Qmetric=Q,
+                              alpha=alpha)
+    P.park_check(out["ws"])
+    for h in range(H):
+        res = O.cluster_keys(kh[h], qh[h], C, T, 3, h, alpha=alpha)
+        lab = out["labels"][h].cpu().numpy()
+        n_mis, n_bad, worst = PT.label_flips(res["Kt"], res["mu"], lab, res["labels"])
+        print(f"  head {h}: label mismatches={n_mis} not-exempt={n_bad} worst-gap={worst:.3g}")
+        assert n_bad == 0
+        p2, o2 = O.stable_argsort(lab, C)
+        assert np.array_equal(out["perm"][h].cpu().numpy(), p2)
+        assert np.array_equal(out["offsets"][h].cpu().numpy(), o2)
+        if alpha == 1.0:
+            # the Euclidean k-means of the raw keys from the same init
+            ze, me = O.kmeans(kh[h], C, T, O.init_indices(N, C, 3, h, side=1))
+            n_mis, n_bad, _ = PT.label_flips(kh[h], me, lab, ze)
+            print(f"  head {h}: against Euclidean k-means mismatches={n_mis} not-exempt={n_bad}")
+            assert n_bad == 0
+
+
 # The exact candidate filter of the k-means rounds after the first runs where
 # C >= 512; small layers with many clusters exercise it (and clusters with a
 # single or no token, and centroids pulled far apart by the 2N(0,1) centres).
@@ -481,9 +517,16 @@ def test_kmeans_candidate_filter_matches_oracle_and_dense(name, grid, C, side):
         lab_d, perm_d, off_d = run()
     finally:
         del os.environ["PARK_KMEANS_FILTER"]
-    # the filter changes which centroids are scored, never the labels
-    assert np.array_equal(lab, lab_d) and np.array_equal(perm, perm_d)
-    assert np.array_equal(off, off_d)
+    # radii measured every round instead of bounded from the previous round
+    os.environ["PARK_KFILTER_EXACT_RADIUS"] = "1"
+    try:
+        lab_r, perm_r, off_r = run()
+    finally:
+        del os.environ["PARK_KFILTER_EXACT_RADIUS"]
+    # the filter and its radii change which centroids are scored, never the labels
+    for lb, pb, ob in ((lab_d, perm_d, off_d), (lab_r, perm_r, off_r)):
+        assert np.array_equal(lab, lb) and np.array_equal(perm, pb)
+        assert np.array_equal(off, ob)
     for h in range(2):
         if side == 0:
             res = O.cluster_queries(q[h], C, T, 3, h)

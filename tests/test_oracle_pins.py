@@ -787,6 +787,37 @@ def test_mismatch_directions():
     assert rep["log_mass_rmse_qrkc"] < 0.5 * rep["log_mass_rmse_euclid"]
 
 
+def test_alpha_sweep_of_the_key_metric():
+    # App. D: alpha moves the key metric from the query-response metric
+    # (alpha -> 0) to the isotropic one (alpha = 1).  At alpha = 1 the key
+    # partition is Euclidean k-means' (a scaled metric, the same init), so
+    # every diagnostic equals the Euclidean one; at the paper's alpha the
+    # partition follows the queries' directions (lower D_QK and log-mass
+    # error, higher raw-key MSE than alpha = 1).  Same anisotropic layer as
+    # the directional test above.
+    r = rng(90)
+    d, N = 16, 768
+    basis = np.linalg.qr(r.standard_normal((d, 2)))[0]
+    Q = 3.0 * r.standard_normal((N, 2)) @ basis.T + 0.05 * r.standard_normal((N, d))
+    cent = 2.0 * r.standard_normal((24, d))
+    K = cent[r.integers(0, 24, N)] + 0.5 * r.standard_normal((N, d))
+    rows = {}
+    for alpha in (0.0, 0.05, 0.25, 0.5, 1.0):
+        rep = O.mismatch_report(Q, K, 12, 24, 8, alpha=alpha)
+        rows[alpha] = rep
+        print(f"alpha={alpha:<5} D_QK={rep['d_qk_qrkc']:.4g} D_key={rep['d_key_qrkc']:.4g} "
+              f"log-mass RMSE={rep['log_mass_rmse_qrkc']:.4g}  (Euclidean: "
+              f"{rep['d_qk_euclid']:.4g}, {rep['d_key_euclid']:.4g}, "
+              f"{rep['log_mass_rmse_euclid']:.4g})")
+    one = rows[1.0]
+    for key in ("d_qk", "d_key", "log_mass_rmse"):
+        assert one[f"{key}_qrkc"] == pytest.approx(one[f"{key}_euclid"], rel=1e-12)
+    small = rows[0.05]
+    assert small["d_qk_qrkc"] < 0.5 * one["d_qk_qrkc"]
+    assert small["d_key_qrkc"] > one["d_key_qrkc"]
+    assert small["log_mass_rmse_qrkc"] < 0.5 * one["log_mass_rmse_qrkc"]
+
+
 def test_block_sparse_lse_pins():
     from scipy.special import logsumexp
     d = 8
