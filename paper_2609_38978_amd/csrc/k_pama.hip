@@ -84,7 +84,8 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
                                                 int CQ, int CK, const int4* __restrict__ items,
                                                 int* __restrict__ cnt, double* __restrict__ part,
                                                 double* __restrict__ W64, float* __restrict__ W32,
-                                                int* status) {
+                                                const int* __restrict__ bandc,
+                                                const int* __restrict__ kv_index, int* status) {
   constexpr int CT = 32, CPR = D / 4, RPI = 64 / CPR, NI = CT / (4 * RPI), KS = D / 4;
   static_assert(NI * 4 * RPI == CT, "tile shape");
   constexpr int NS = 3;  // centroid ring: one tile in flight while one is used
@@ -125,18 +126,32 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
     const int* nh = k_sizes + (size_t)h * CK;
     const int* off = q_offsets + (size_t)h * (CQ + 1);
     const T* Qh = Qp + (size_t)h * N * D;
-    auto issue = [&](int tile, int slot) {
-      const int c0 = tile * CT;
+    // band rows: the probability pass covers only the listed (ambiguous)
+    // blocks, which sit at the end of the row of kv_index; the normaliser
+    // pass always covers every block
+    const int nb = bandc ? min(bandc[rid], CK) : -1;
+    const int* blist = nb >= 0 ? kv_index + (size_t)rid * CK + (CK - nb) : nullptr;
+    const int nt2 = nb >= 0 ? (nb + CT - 1) / CT : nt;
+    const int Lc = nt + nt2;  // steps per chunk of 64 queries
+    // column of tile row r in a pass (-1: none)
+    auto column = [&](int pass, int tile, int r) {
+      const int ix = tile * CT + r;
+      if (pass == 1 && nb >= 0) return ix < nb ? min(max(blist[ix], 0), CK - 1) : -1;
+      return ix < CK ? ix : -1;
+    };
+    auto issue = [&](int step, int slot) {
+      const int j = step % Lc, pass = j >= nt ? 1 : 0, tile = pass ? j - nt : j;
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int r = (w * NI + i) * RPI + l / CPR;
-        const int v = min(c0 + r, CK - 1);
+        const int c = column(pass, tile, r);
+        const int v = c >= 0 ? c : CK - 1;
         const float* src = ch + (size_t)v * D + 4 * (pch ^ (r & (CPR - 1)));
         p64_dma16(src, p64_lds_addr(&Ct[slot][0] + (w * NI + i) * 256));
       }
       if (tid < CT) {
-        const int v = c0 + tid;
-        const int n = v < CK ? nh[v] : 0;
+        const int v = column(pass, tile, tid);
+        const int n = v >= 0 ? nh[v] : 0;
         Lt[slot][tid] = n > 0 ? log((double)n) : -INFINITY;
       }
     };
@@ -153,15 +168,16 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
     __syncthreads();  // the previous item's column sums have been read
     for (int v = tid; v < CK; v += 256) wacc64[v] = 0.0;
     const int nch = min(ce, (nu + 63) / 64) - cb;  // chunks of 64 queries from cb on
-    const int total = nch * 2 * nt;
+    const int total = nch * Lc;
     float qa[KS];  // float holds bf16 and float32 inputs exactly
     double m[4], z[4], mf[4];
     bool qv[4];
     issue(0, 0);
-    if (total > 1) issue(1 % nt, 1);
-    int prev_c0 = -1;  // the previous step's tile, when it was a probability-pass tile
+    if (total > 1) issue(1, 1);
+    int prev_t = -1;  // the previous step's tile, when it was a probability-pass tile
     for (int it = 0; it < total; ++it) {
-      const int tile = it % nt, pass = (it / nt) & 1, r0 = q0 + 64 * (cb + it / (2 * nt));
+      const int j = it % Lc, pass = j >= nt ? 1 : 0, tile = pass ? j - nt : j;
+      const int r0 = q0 + 64 * (cb + it / Lc);
       if (tile == 0 && pass == 0) {
         // A operand: query r0 + 16w + c16, dimensions 4s + g
         const int qi = r0 + 16 * w + c16;
@@ -197,15 +213,15 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
       if (it + 1 < total) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI) : "memory");
       else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();  // tile landed everywhere; tile it-1 consumed (its slot is free)
-      if (it + 2 < total) issue((it + 2) % nt, (it + 2) % NS);
+      if (it + 2 < total) issue(it + 2, (it + 2) % NS);
       // the previous probability-pass tile's wavefront sums, in wavefront order
-      if (prev_c0 >= 0 && tid < CT && prev_c0 + tid < CK) {
+      if (prev_t >= 0 && tid < CT) {
+        const int col = column(1, prev_t, tid);
         const double (*sg)[CT] = stg[(it - 1) & 1];
-        wacc64[prev_c0 + tid] += ((sg[0][tid] + sg[1][tid]) + sg[2][tid]) + sg[3][tid];
+        if (col >= 0) wacc64[col] += ((sg[0][tid] + sg[1][tid]) + sg[2][tid]) + sg[3][tid];
       }
       const int slot = it % NS;
       const float* cs = &Ct[slot][0];
-      const int c0 = tile * CT;
       constexpr int UNR = W2 ? 1 : CT / 16;
 #pragma unroll UNR
       for (int cb = 0; cb < CT / 16; ++cb) {
@@ -249,12 +265,13 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
           if (g == 0) stg[it & 1][w][row] = cs4;
         }
       }
-      prev_c0 = pass == 1 ? c0 : -1;
+      prev_t = pass == 1 ? tile : -1;
     }
     __syncthreads();
-    if (prev_c0 >= 0 && tid < CT && prev_c0 + tid < CK) {
+    if (prev_t >= 0 && tid < CT) {
+      const int col = column(1, prev_t, tid);
       const double (*sg)[CT] = stg[(total - 1) & 1];
-      wacc64[prev_c0 + tid] += ((sg[0][tid] + sg[1][tid]) + sg[2][tid]) + sg[3][tid];
+      if (col >= 0) wacc64[col] += ((sg[0][tid] + sg[1][tid]) + sg[2][tid]) + sg[3][tid];
     }
     __syncthreads();
     if (slot != -1) {  // part of a split row: raw column sums, added up by k_p64_combine
@@ -535,15 +552,82 @@ __global__ __launch_bounds__(256) void k_select64(const double* __restrict__ W64
                                                   const int* __restrict__ rows,
                                                   const int* __restrict__ nrows,
                                                   int* __restrict__ kv_count,
-                                                  int* __restrict__ kv_index) {
+                                                  int* __restrict__ kv_index,
+                                                  const int* __restrict__ bandc) {
   const int h = blockIdx.y;
   const int cnt = rows ? min(nrows[h], CQ) : blockIdx.x + 1;
   const int step = rows ? gridDim.x : 1;
   for (int r = blockIdx.x; r < cnt; r += step) {
     const int u = rows ? rows[(size_t)h * CQ + r] : r;
-    if ((unsigned)u < (unsigned)CQ)
-      select64_row(W64, q_offsets, k_sizes, h, u, CQ, CK, P, mode, param, kcount, kv_count,
-                   kv_index);
+    if ((unsigned)u >= (unsigned)CQ) continue;
+    if (bandc && bandc[(size_t)h * CQ + u] >= 0) continue;  // k_select_band's row
+    select64_row(W64, q_offsets, k_sizes, h, u, CQ, CK, P, mode, param, kcount, kv_count,
+                 kv_index);
+  }
+}
+
+// Top-k rows settled by their band (see select_topk_radix): the certain
+// blocks (the row's first kv_count[row] entries) plus the top m - kv_count
+// band blocks (the row's last bandc[row] entries) by float64 W^ (descending,
+// ties to the lowest id), written in ascending id order.  The band is small:
+// ranks by pairwise comparison.
+__global__ __launch_bounds__(256) void k_select_band(const double* __restrict__ W64,
+                                                     const int* __restrict__ k_sizes, int CQ,
+                                                     int CK, int kcount,
+                                                     const int* __restrict__ rows,
+                                                     const int* __restrict__ nrows,
+                                                     const int* __restrict__ bandc,
+                                                     int* __restrict__ kv_count,
+                                                     int* __restrict__ kv_index) {
+  __shared__ int flag[MAXC];
+  __shared__ int bid[MAXC];
+  __shared__ double bval[MAXC];
+  __shared__ int tmp[4];
+  const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int cnt = min(nrows[h], CQ);
+  for (int r = blockIdx.x; r < cnt; r += gridDim.x) {
+    const int u = rows[(size_t)h * CQ + r];
+    if ((unsigned)u >= (unsigned)CQ) continue;
+    const size_t row = (size_t)h * CQ + u;
+    const int nb = min(bandc[row], CK);
+    if (nb < 0) continue;
+    const int nin = min(max(kv_count[row], 0), CK - nb);
+    int* out = kv_index + row * CK;
+    int nv = 0;
+    for (int e = tid; e < CK; e += 256) {
+      nv += k_sizes[(size_t)h * CK + e] > 0;
+      flag[e] = 0;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) nv += __shfl_xor(nv, o, 64);
+    __syncthreads();  // flag cleared; tmp free
+    if (lane == 0) tmp[wid] = nv;
+    for (int i = tid; i < nb; i += 256) {
+      const int v = min(max(out[CK - nb + i], 0), CK - 1);
+      const double x = W64[row * CK + v];
+      bid[i] = v;
+      bval[i] = x == x ? x : 0.0;  // a NaN weight (already reported) ranks as 0
+    }
+    for (int i = tid; i < nin; i += 256) flag[min(max(out[i], 0), CK - 1)] = 1;
+    __syncthreads();
+    const int nvalid = tmp[0] + tmp[1] + tmp[2] + tmp[3];
+    const int m = min(max(kcount, 1), nvalid);
+    const int need = m - nin;
+    for (int i = tid; i < nb; i += 256) {
+      const double x = bval[i];
+      const int v = bid[i];
+      int rank = 0;
+      for (int j = 0; j < nb; ++j) rank += (bval[j] > x) || (bval[j] == x && bid[j] < v);
+      if (rank < need) flag[v] = 1;
+    }
+    __syncthreads();
+    for (int e = tid; e < CK; e += 256) bid[e] = flag[e];
+    __syncthreads();
+    block_exclusive_scan_2048(bid, CK, tmp);
+    for (int e = tid; e < CK; e += 256)
+      if (flag[e]) out[bid[e]] = e;
+    if (tid == 0) kv_count[row] = m;
+    __syncthreads();
   }
 }
 
@@ -1064,7 +1148,8 @@ __global__ __launch_bounds__(256) void k_pama_combine(const int* __restrict__ q_
 __device__ void select_topk_radix(const float* __restrict__ w, const int* __restrict__ ksz, int CK,
                                   int kcount, double dl, int* __restrict__ kv_count,
                                   int* __restrict__ out, int* __restrict__ rows,
-                                  int* __restrict__ nrows, int u, int* hist, int* aux, int* tmp) {
+                                  int* __restrict__ nrows, int u, int* hist, int* aux, int* tmp,
+                                  int* __restrict__ bandc) {
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   constexpr int E = MAXC / 256;
   uint32_t kv[E];
@@ -1148,8 +1233,54 @@ __device__ void select_topk_radix(const float* __restrict__ w, const int* __rest
     const double b = (double)__uint_as_float(lt) * (1.0 + dl) + eps;
     ok = a > b;
   }
+  if (!ok && bandc) {
+    // the blocks the bound places for certain: in the exact top m when their
+    // lower bound exceeds the upper bound of the (m+1)-th largest W^ (every
+    // block from position m + 1 on is then below them), out of it when their
+    // upper bound is below the lower bound of the m-th (m blocks are above
+    // them); the others (the band) are settled by their float64 weights.
+    // Certain blocks go to the row's start, the band to its end (ascending).
+    const double wm = (double)__uint_as_float(a_bits);
+    const double wm1 = cnt_ge > m ? wm : (double)__uint_as_float(lt);
+    const double tin = wm1 * (1.0 + dl) + eps, tout = wm * (1.0 - dl) - eps;
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      const int e = tid + 256 * k;
+      const bool v = (kv[k] >> 31) == 0u;
+      const double x = (double)__uint_as_float(kv[k]);
+      const bool sin = v && x * (1.0 - dl) - eps > tin;
+      const bool sout = v && x * (1.0 + dl) + eps < tout;
+      if (e < MAXC) {
+        hist[e] = sin ? 1 : 0;
+        aux[e] = (v && !sin && !sout) ? 1 : 0;
+      }
+    }
+    __syncthreads();
+    const int nin = block_exclusive_scan_2048(hist, CK, tmp);
+    const int nb = block_exclusive_scan_2048(aux, CK, tmp);
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      const int e = tid + 256 * k;
+      if (e < CK && (kv[k] >> 31) == 0u) {
+        const double x = (double)__uint_as_float(kv[k]);
+        const bool sin = x * (1.0 - dl) - eps > tin;
+        const bool sout = x * (1.0 + dl) + eps < tout;
+        if (sin) out[hist[e]] = e;
+        else if (!sout) out[CK - nb + aux[e]] = e;
+      }
+    }
+    if (tid == 0) {
+      *kv_count = nin;
+      *bandc = nb;
+      rows[atomicAdd(nrows, 1)] = u;
+    }
+    return;
+  }
   if (!ok) {
-    if (tid == 0) rows[atomicAdd(nrows, 1)] = u;
+    if (tid == 0) {
+      if (bandc) *bandc = -1;
+      rows[atomicAdd(nrows, 1)] = u;
+    }
     return;
   }
   // kept: W^ >= a; written in ascending id order
@@ -1356,7 +1487,8 @@ __global__ __launch_bounds__(256) void k_select_fast(const float* __restrict__ W
                                                      int kcount, int* __restrict__ kv_count,
                                                      int* __restrict__ kv_index,
                                                      int* __restrict__ rows,
-                                                     int* __restrict__ nrows) {
+                                                     int* __restrict__ nrows,
+                                                     int* __restrict__ bandc) {
   __shared__ int flag[MAXC], aux[MAXC];
   __shared__ double dh[256], dtmp[4];
   __shared__ int tmp[4];
@@ -1371,9 +1503,10 @@ __global__ __launch_bounds__(256) void k_select_fast(const float* __restrict__ W
   if (mode == PARK_SELECT_TOPK) {
     select_topk_radix(W32 + row * CK, k_sizes + (size_t)h * CK, CK, kcount, (double)delta[row],
                       kv_count + row, kv_index + row * CK, rows + (size_t)h * CQ, nrows + h, u,
-                      flag, aux, tmp);
+                      flag, aux, tmp, bandc ? bandc + row : nullptr);
     return;
   }
+  if (bandc && tid == 0) bandc[row] = -1;  // a top-p row left to float64 is recomputed whole
   select_topp_radix(W32 + row * CK, k_sizes + (size_t)h * CK, CK, param, (double)delta[row],
                     kv_count + row, kv_index + row * CK, rows + (size_t)h * CQ, nrows + h, u, flag,
                     aux, dh, tmp, dtmp);
@@ -1407,10 +1540,10 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   const int kcount = mode == PARK_SELECT_TOPK ? topk_count(CK, param) : 0;
   if (dtype != PARK_BF16) {  // float32 queries: float64 PAMA and selection of every row
     PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, nullptr, nullptr,
-                           nullptr, rb.W64, W_out, status, st));
+                           nullptr, rb.W64, W_out, nullptr, nullptr, status, st));
     PARK_LAUNCH("select", k_select64, dim3(CQ, H), dim3(256), 0, st, (const double*)rb.W64,
                 q_offsets, k_sizes, CQ, CK, P, mode, param, kcount, (const int*)nullptr,
-                (const int*)nullptr, kv_count, kv_index);
+                (const int*)nullptr, kv_count, kv_index, (const int*)nullptr);
     return PARK_OK;
   }
   const size_t plane = (size_t)H * CK * D;
@@ -1441,9 +1574,14 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   PARK_LAUNCH("pama_combine", k_pama_combine, dim3(1024), dim3(256), 0, st, q_offsets,
               (const int*)rb.qstart, H, N, CQ, CK, (const float*)part, pcap, W32, rb.delta);
   PARK_LAUNCH("pama_reset", k_zero_counts, dim3((H + 63) / 64), dim3(64), 0, st, rb.nrows, H);
+  // top-k rows the bound cannot settle are settled by their band of
+  // ambiguous blocks (float64 weights of those blocks only); not when the
+  // caller asked for W^ (its float64 rows are then written whole)
+  int* bandc = (mode == PARK_SELECT_TOPK && !W_out) ? rb.bandc : nullptr;
+  float* W32r = bandc ? nullptr : W32;
   PARK_LAUNCH("select_fast", k_select_fast, dim3(CQ, H), dim3(256), 0, st, (const float*)W32,
               (const float*)rb.delta, q_offsets, k_sizes, CQ, CK, P, mode, param, kcount,
-              kv_count, kv_index, rb.rows, rb.nrows);
+              kv_count, kv_index, rb.rows, rb.nrows, bandc);
   // rows the float bound could not certify: float64 PAMA over chunks of 64
   // queries (work list, queue), split rows added up, then selection
   int rg = (1024 + H - 1) / H;
@@ -1452,13 +1590,17 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
               (const int*)rb.rows, (const int*)rb.nrows, H, N, CQ, p64_cap(H, CQ), rb.items,
               rb.srows, rb.pcnt);
   PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, rb.items, rb.pcnt,
-                         rb.part, rb.W64, W32, status, st));
+                         rb.part, rb.W64, W32r, bandc, kv_index, status, st));
   PARK_LAUNCH("pama_combine64", k_p64_combine, dim3(256), dim3(256), 0, st,
-              (const int4*)rb.srows, (const int*)rb.pcnt, (const double*)rb.part, CK, rb.W64, W32,
+              (const int4*)rb.srows, (const int*)rb.pcnt, (const double*)rb.part, CK, rb.W64, W32r,
               status);
   PARK_LAUNCH("select_refine", k_select64, dim3(rg, H), dim3(256), 0, st, (const double*)rb.W64,
               q_offsets, k_sizes, CQ, CK, P, mode, param, kcount, (const int*)rb.rows,
-              (const int*)rb.nrows, kv_count, kv_index);
+              (const int*)rb.nrows, kv_count, kv_index, (const int*)bandc);
+  if (bandc)
+    PARK_LAUNCH("select_band", k_select_band, dim3(rg, H), dim3(256), 0, st,
+                (const double*)rb.W64, k_sizes, CQ, CK, kcount, (const int*)rb.rows,
+                (const int*)rb.nrows, (const int*)bandc, kv_count, kv_index);
   return PARK_OK;
 }
 
@@ -1467,7 +1609,8 @@ static park_status pama64_launch(const char* nm, unsigned nwg, size_t lds, const
                                  int dtype, const int* q_offsets, const float* cen,
                                  const int* k_sizes, int H, int N, int CQ, int CK,
                                  const int4* items, int* cnt, double* part, double* W64,
-                                 float* W32, int* status, hipStream_t st) {
+                                 float* W32, const int* bandc, const int* kv_index, int* status,
+                                 hipStream_t st) {
   // reserved once for the largest CK (2048), outside any stream capture that may follow
   static const int lds_max = (int)(MAXC * sizeof(double));
   static const hipError_t a1 = hipFuncSetAttribute(
@@ -1478,17 +1621,19 @@ static park_status pama64_launch(const char* nm, unsigned nwg, size_t lds, const
     return fail(PARK_ERR_HIP, "retrieval: cannot reserve %zu bytes of LDS", lds);
   if (dtype == PARK_BF16)
     PARK_LAUNCH(nm, (k_pama64<bf16_t, D, W2>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
-                q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
+                q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, bandc, kv_index,
+                status);
   else
     PARK_LAUNCH(nm, (k_pama64<float, D, W2>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
-                q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, status);
+                q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, bandc, kv_index,
+                status);
   return PARK_OK;
 }
 
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                           const int4* items, int* cnt, double* part, double* W64, float* W32,
-                          int* status, hipStream_t st) {
+                          const int* bandc, const int* kv_index, int* status, hipStream_t st) {
   // with an item list: a queue drained by a fixed grid; without: one
   // workgroup per row, the rows of a head on one XCD
   const unsigned nwg = items ? 512u : 8u * (((unsigned)H * (unsigned)CQ + 7u) / 8u);
@@ -1499,13 +1644,13 @@ park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen
   const bool w2 = (long)H * CQ >= 8192;
   if (D == 128)
     return w2 ? pama64_launch<128, true>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N,
-                                         CQ, CK, items, cnt, part, W64, W32, status, st)
+                                         CQ, CK, items, cnt, part, W64, W32, bandc, kv_index, status, st)
               : pama64_launch<128, false>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N,
-                                          CQ, CK, items, cnt, part, W64, W32, status, st);
+                                          CQ, CK, items, cnt, part, W64, W32, bandc, kv_index, status, st);
   return w2 ? pama64_launch<64, true>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N, CQ,
-                                      CK, items, cnt, part, W64, W32, status, st)
+                                      CK, items, cnt, part, W64, W32, bandc, kv_index, status, st)
             : pama64_launch<64, false>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N, CQ,
-                                       CK, items, cnt, part, W64, W32, status, st);
+                                       CK, items, cnt, part, W64, W32, bandc, kv_index, status, st);
 }
 
 }  // namespace park

@@ -108,6 +108,11 @@ struct RetrieveBufs {
   int4* items;    // [H CQ + p64_cap] float64 work list
   int4* srows;    // [p64_cap] split rows
   int* pcnt;      // [4] items, split rows, queue head
+  // [H][CQ] top-k rows the float bound could not settle: the number of
+  // ambiguous blocks ("band") whose float64 weights decide the cut, -1 for a
+  // row recomputed whole; the certain blocks and the band are listed in the
+  // row of kv_index until the float64 selection writes it
+  int* bandc;
 };
 // fast retrieval: items (rounds of 64 queries) per head, and rows of round
 // partial sums per head (every round after a block's first), kept in the
@@ -119,7 +124,7 @@ inline int p64_cap(int H, int CQ) { return (H * CQ + 3) / 4; }
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                           const int4* items, int* cnt, double* part, double* W64, float* W32,
-                          int* status, hipStream_t st);
+                          const int* bandc, const int* kv_index, int* status, hipStream_t st);
 park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* cen,
                             const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                             int mode, double param, const RetrieveBufs& rb, float* W_out,

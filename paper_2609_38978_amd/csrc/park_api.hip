@@ -187,6 +187,7 @@ static RetrieveBufs carve_retrieve(Carver& cv, int H, int N, int D, int CQ, int 
   r.items = cv.take<int4>((size_t)H * CQ + p64_cap(H, CQ));
   r.srows = cv.take<int4>((size_t)p64_cap(H, CQ) + 1);
   r.pcnt = cv.take<int>(4);
+  r.bandc = cv.take<int>((size_t)H * CQ);
   return r;
 }
 

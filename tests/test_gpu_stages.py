@@ -149,14 +149,22 @@ def test_retrieval_matches_oracle(case, mode):
     sel = P.PARK_SELECT_TOPK if mode == "topk" else P.PARK_SELECT_TOPP
     kvc, kvi, W = P.park_retrieve_blocks(Qp, qoff, cen, ksz, CQ, CK, sel, param, want_W=True)
     kvc, kvi, W = kvc.cpu().numpy(), kvi.cpu().numpy(), W.cpu().numpy()
+    # without W^ the top-k rows the bound cannot settle take the band path
+    kvc2, kvi2, _ = P.park_retrieve_blocks(Qp, qoff, cen, ksz, CQ, CK, sel, param)
+    kvc2, kvi2 = kvc2.cpu().numpy(), kvi2.cpu().numpy()
     for h in range(H):
         ok, werr = PT.w_error_ok(cfg.dtype, W[h], Ws[h])
         print(f"[{tag} {mode} h={h}] W max-abs err {werr:.3g}")
         assert ok, (tag, werr)
         qs = np.diff(qoffs[h])
-        nd, nb = PT.compare_masks(Ws[h], ns[h], qs, mode, param, kvc[h], kvi[h])
-        print(f"[{tag} {mode} h={h}] mask rows differing={nd} not-exempt={nb}")
-        assert nb == 0
+        for kc, ki in ((kvc[h], kvi[h]), (kvc2[h], kvi2[h])):
+            nd, nb = PT.compare_masks(Ws[h], ns[h], qs, mode, param, kc, ki)
+            print(f"[{tag} {mode} h={h}] mask rows differing={nd} not-exempt={nb}")
+            assert nb == 0
+        # both paths give the same masks
+        assert np.array_equal(kvc[h], kvc2[h])
+        for u in range(CQ):
+            assert np.array_equal(kvi[h][u, :kvc[h][u]], kvi2[h][u, :kvc2[h][u]]), (h, u)
 
 
 @pytest.mark.parametrize("out_dtype", [P.PARK_F32, P.PARK_BF16])
@@ -376,13 +384,17 @@ def test_retrieval_exact_ties_take_the_float64_path(mode, param):
     Qp = q[0][rq["perm"]]
     Wo = O.pama(Qp, rq["offsets"], c, n)
     sel = P.PARK_SELECT_TOPK if mode == "topk" else P.PARK_SELECT_TOPP
-    kvc, kvi, W = P.park_retrieve_blocks(
-        PT.to_dev(Qp[None], "bf16"), torch.from_numpy(rq["offsets"][None].astype(np.int32)).cuda(),
-        torch.from_numpy(c[None]).cuda(), torch.from_numpy(n[None].astype(np.int32)).cuda(),
-        CQ, CK, sel, param, want_W=True)
-    kvc, kvi = kvc.cpu().numpy()[0], kvi.cpu().numpy()[0]
-    nd, nb = PT.compare_masks(Wo, n, np.diff(rq["offsets"]), mode, param, kvc, kvi)
-    assert nb == 0 and nd == 0
+    args = (PT.to_dev(Qp[None], "bf16"),
+            torch.from_numpy(rq["offsets"][None].astype(np.int32)).cuda(),
+            torch.from_numpy(c[None]).cuda(), torch.from_numpy(n[None].astype(np.int32)).cuda(),
+            CQ, CK, sel, param)
+    # with W^ asked for (float64 rows whole) and without (top-k: only the
+    # band of ambiguous blocks in float64)
+    for want_W in (True, False):
+        kvc, kvi, W = P.park_retrieve_blocks(*args, want_W=want_W)
+        kvc, kvi = kvc.cpu().numpy()[0], kvi.cpu().numpy()[0]
+        nd, nb = PT.compare_masks(Wo, n, np.diff(rq["offsets"]), mode, param, kvc, kvi)
+        assert nb == 0 and nd == 0, want_W
 
 
 @pytest.mark.parametrize("sizes", [
