@@ -279,6 +279,91 @@ int attn_groups_per_head(int N, int CQ) {
   return W + (CQ + W + ATTN_LB - 1) / ATTN_LB + 1;
 }
 
+// Selection families.  fam[h][u] = the smallest query block v (u itself
+// included) whose selected key-block set overlaps u's with Jaccard index above
+// 1/2 (3 |S_u & S_v| > |S_u| + |S_v|).  Blocks whose selections are nearly the
+// same (on video latents: query clusters of the same content) then share one
+// value, and sorting by fam[fam[u]] makes the blocks of a family neighbours in
+// the group plan.
+//
+// k_attn_selbits: the selection of every (head, query block) as a 64-word bit
+// row (CK <= 2048), one wavefront per row, and fam = u.
+__global__ __launch_bounds__(256) void k_attn_selbits(const int* __restrict__ kv_count,
+                                                      const int* __restrict__ kv_index, int H,
+                                                      int CQ, int CK, uint32_t* __restrict__ bits,
+                                                      int* __restrict__ fam) {
+  __shared__ uint32_t rowb[4][64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const size_t row = (size_t)blockIdx.x * 4 + wid;
+  const bool valid = row < (size_t)H * CQ;
+  rowb[wid][lane] = 0u;
+  __syncthreads();
+  if (valid) {
+    const int n = min(max(kv_count[row], 0), CK);
+    const int* sel = kv_index + row * CK;
+    for (int j = lane; j < n; j += 64) {
+      const int v = sel[j];
+      if ((unsigned)v < (unsigned)CK) atomicOr(&rowb[wid][v >> 5], 1u << (v & 31));
+    }
+  }
+  __syncthreads();
+  if (valid) {
+    bits[row * 64 + lane] = rowb[wid][lane];
+    if (lane == 0) fam[row] = (int)(row % (size_t)CQ);
+  }
+}
+
+// k_attn_family: workgroup = a pair of 64-block tiles (tu, tv <= tu) of a
+// head; thread (r, kk) holds row u = 64 tu + r in registers and compares it
+// with rows v = 64 tv + kk + 4 j < u (LDS); the smallest qualifying v goes to
+// fam[u] by atomicMin (order-independent).
+__global__ __launch_bounds__(256) void k_attn_family(const int* __restrict__ kv_count,
+                                                     const uint32_t* __restrict__ bits, int CQ,
+                                                     int CK, int* __restrict__ fam) {
+  __shared__ uint4 vb[64][17];  // 64 bit rows of the v tile (+1 chunk: conflict-free)
+  __shared__ int vcnt[64];
+  const int h = blockIdx.y, p = (int)blockIdx.x, tid = threadIdx.x;
+  int tu = (int)((sqrtf(8.0f * (float)p + 1.0f) - 1.0f) * 0.5f);
+  while ((tu + 1) * (tu + 2) / 2 <= p) ++tu;
+  while (tu * (tu + 1) / 2 > p) --tu;
+  const int tv = p - tu * (tu + 1) / 2;
+  const int W4 = ((CK + 31) / 32 + 3) / 4;  // 16-byte chunks holding the selection bits
+  const uint4* bh = (const uint4*)(bits + (size_t)h * CQ * 64);
+  for (int e = tid; e < 64 * 16; e += 256) {
+    const int k = e >> 4, c = e & 15, v = tv * 64 + k;
+    vb[k][c] = v < CQ ? bh[(size_t)v * 16 + c] : make_uint4(0u, 0u, 0u, 0u);
+  }
+  if (tid < 64) {
+    const int v = tv * 64 + tid;
+    vcnt[tid] = v < CQ ? min(max(kv_count[(size_t)h * CQ + v], 0), CK) : 0;
+  }
+  const int r = tid & 63, kk = tid >> 6, u = tu * 64 + r;
+  uint4 ur[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) ur[c] = u < CQ ? bh[(size_t)u * 16 + c] : make_uint4(0u, 0u, 0u, 0u);
+  const int cu = u < CQ ? min(max(kv_count[(size_t)h * CQ + u], 0), CK) : 0;
+  __syncthreads();
+  if (u >= CQ || cu == 0) return;  // no barrier follows
+  int cand = 0x7fffffff;
+  for (int j = 0; j < 16; ++j) {
+    const int k = kk + 4 * j, v = tv * 64 + k;
+    if (v >= u) break;
+    int inter = 0;
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+      if (c < W4) {
+        const uint4 y = vb[k][c];
+        inter += __popc(ur[c].x & y.x) + __popc(ur[c].y & y.y) + __popc(ur[c].z & y.z) +
+                 __popc(ur[c].w & y.w);
+      }
+    if (3 * inter > cu + vcnt[k]) {
+      cand = v;
+      break;
+    }
+  }
+  if (cand != 0x7fffffff) atomicMin(&fam[(size_t)h * CQ + u], cand);
+}
+
 // Group plan of one head (1024 threads, CQ <= 2048):
 //   order[h][i]  query block at sorted position i (-1 past the blocks with rows)
 //   spre[h][i]   rows of the sorted blocks before position i (i <= CQ)
@@ -288,7 +373,8 @@ int attn_groups_per_head(int N, int CQ) {
 __global__ __launch_bounds__(1024) void k_attn_gplan(const int* __restrict__ q_offsets,
                                                      const int* __restrict__ kv_count,
                                                      const int* __restrict__ kv_index,
-                                                     const int* __restrict__ k_offsets, int N,
+                                                     const int* __restrict__ k_offsets,
+                                                     const int* __restrict__ fam, int N,
                                                      int CQ, int CK, int GPH,
                                                      int* __restrict__ order,
                                                      int* __restrict__ spre,
@@ -303,8 +389,9 @@ __global__ __launch_bounds__(1024) void k_attn_gplan(const int* __restrict__ q_o
   const int* koff = k_offsets + (size_t)h * (CK + 1);
   int SZ = 2;
   while (SZ < CQ) SZ <<= 1;
-  // sort keys (first MinHash, top bits of the second, block id); blocks
-  // without rows sort last with the key ~0.  One wavefront per block.
+  // sort keys (selection family, top bits of the first MinHash, top bits of
+  // the second, block id); blocks without rows sort last with the key ~0.
+  // One wavefront per block.
   for (int u = wid; u < SZ; u += 16) {
     unsigned long long kk = ~0ull;
     if (u < CQ) {
@@ -328,8 +415,13 @@ __global__ __launch_bounds__(1024) void k_attn_gplan(const int* __restrict__ q_o
           nkey += __shfl_xor(nkey, o, 64);
         }
         if (lane == 0) tiles[u] = (nkey + 31) >> 5;
-        m1 = min(m1, 0xfffffffeu);
-        kk = ((unsigned long long)m1 << 32) | (m2 & 0xfffff800u) | (uint32_t)u;
+        // family label: the partner of u's smallest partner (one pointer jump)
+        const int* fh = fam + (size_t)h * CQ;
+        int f = fh[u];
+        f = (unsigned)f < (unsigned)CQ ? fh[f] : u;
+        f = (unsigned)f < (unsigned)CQ ? f : u;
+        kk = ((unsigned long long)f << 52) | ((unsigned long long)(m1 >> 12) << 32) |
+             (m2 & 0xfffff800u) | (uint32_t)u;
       }
     }
     if (lane == 0) key[u] = kk;
@@ -943,6 +1035,8 @@ static park_status attn_dispatch_d(const void* Qp, const void* Kp, const void* V
 }
 
 size_t attn_grp_offset(int H, int CQ);
+// the families [H][CQ], padded to 16 bytes (the bit rows follow)
+static size_t attn_fam_bytes(int H, int CQ) { return ((size_t)H * CQ * sizeof(int) + 15) & ~(size_t)15; }
 
 template <typename OT, int D, int NW>
 static park_status attn_grp_launch(const void* Qp, const void* Kp, const void* Vp, const int* qo,
@@ -953,8 +1047,15 @@ static park_status attn_grp_launch(const void* Qp, const void* Kp, const void* V
   int* order = (int*)plan;
   int* spre = order + (size_t)H * CQ;
   int4* grp = (int4*)((char*)plan + attn_grp_offset(H, CQ));
-  PARK_LAUNCH("attn_plan", k_attn_gplan, dim3(H), dim3(1024), 0, st, qo, kc, ki, ko, N, CQ, CK,
-              GPH, order, spre, grp);
+  int* fam = (int*)(grp + (size_t)H * GPH);
+  uint32_t* bits = (uint32_t*)((char*)fam + attn_fam_bytes(H, CQ));
+  const unsigned nrow = (unsigned)H * (unsigned)CQ, ntile = (unsigned)(CQ + 63) / 64;
+  PARK_LAUNCH("attn_selbits", k_attn_selbits, dim3((nrow + 3) / 4), dim3(256), 0, st, kc, ki, H,
+              CQ, CK, bits, fam);
+  PARK_LAUNCH("attn_family", k_attn_family, dim3(ntile * (ntile + 1) / 2, H), dim3(256), 0, st,
+              kc, bits, CQ, CK, fam);
+  PARK_LAUNCH("attn_plan", k_attn_gplan, dim3(H), dim3(1024), 0, st, qo, kc, ki, ko, fam, N, CQ,
+              CK, GPH, order, spre, grp);
   // K ring, V ring, score biases, key-block flags, stream table, selection words
   constexpr size_t lds = (size_t)(2 * ATTN_KSLOTS + 1) * 32 * D * sizeof(bf16_t) +
                          (size_t)ATTN_KSLOTS * ATTN_LB * 32 * 4 + (size_t)AT_MAXC / 2 * 4 +
@@ -984,13 +1085,16 @@ static park_status attn_mfma_d(const void* Qp, const void* Kp, const void* Vp, c
                                               sl2, O, lse, st);
 }
 
-// order [H][CQ], spre [H][CQ + 1], then the groups [H][GPH] at 16-byte alignment
+// order [H][CQ], spre [H][CQ + 1], then the groups [H][GPH] at 16-byte
+// alignment, the selection families [H][CQ] (padded to 16 bytes) and the
+// selection bit rows [H][CQ][64]
 size_t attn_grp_offset(int H, int CQ) {
   return (((size_t)H * CQ + (size_t)H * (CQ + 1)) * sizeof(int) + 15) & ~(size_t)15;
 }
 
 size_t attn_plan_bytes(int H, int N, int CQ) {
-  return attn_grp_offset(H, CQ) + (size_t)H * attn_groups_per_head(N, CQ) * sizeof(int4);
+  return attn_grp_offset(H, CQ) + (size_t)H * attn_groups_per_head(N, CQ) * sizeof(int4) +
+         attn_fam_bytes(H, CQ) + (size_t)H * CQ * 64 * sizeof(uint32_t);
 }
 
 park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,

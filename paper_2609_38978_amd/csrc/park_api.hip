@@ -280,7 +280,7 @@ static park_status check_attn_args(const void* Qp, const void* Kp, const void* V
 // its own copy; host code uses only the address hipGetSymbolAddress returns
 // for the current device (the array's name is a host-side stand-in), kept per
 // device after the first call there.  Every call on a device shares it.
-constexpr size_t kStaticScratchBytes = (size_t)4 << 20;
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
 static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 static std::mutex g_scratch_mu;
 static void* g_scratch_ptr[64];

@@ -279,6 +279,76 @@ def test_attention_many_small_query_blocks(d):
         assert ok, worst
 
 
+def test_attention_plan_selection_families():
+    # query blocks drawn from a few families of nearly equal selections: the
+    # plan's family of block u is the smallest v <= u with Jaccard(S_u, S_v)
+    # > 1/2, the blocks of one family are neighbours in the plan's order, and
+    # the output still matches the oracle
+    rng = np.random.default_rng(11)
+    H, N, d, CQ, CK = 2, 3000, 128, 90, 120
+    q, k, v = (synth.bf16_round(rng.standard_normal((H, N, d)).astype(np.float32))
+               for _ in range(3))
+    qperm, kperm, qoff, koff, kvc, kvi, rows, fams = [], [], [], [], [], [], [], []
+    for h in range(H):
+        zq = rng.integers(0, CQ, N)
+        zk = rng.integers(0, CK, N)
+        pq, oq = O.stable_argsort(zq, CQ)
+        pk, ok = O.stable_argsort(zk, CK)
+        base = [rng.choice(CK, size=30, replace=False) for _ in range(6)]
+        cnt = np.zeros(CQ, np.int32)
+        idx = np.zeros((CQ, CK), np.int32)
+        rr, sets = [], []
+        for u in range(CQ):
+            s = set(base[int(rng.integers(0, 6))].tolist())
+            drop = rng.choice(sorted(s), size=int(rng.integers(0, 12)), replace=False)
+            s -= set(drop.tolist())
+            s |= set(rng.choice(CK, size=int(rng.integers(0, 12)), replace=False).tolist())
+            s = np.array(sorted(s))
+            cnt[u] = len(s)
+            idx[u, :len(s)] = s
+            rr.append(s)
+            sets.append(set(s.tolist()))
+        fam = np.arange(CQ)
+        for u in range(CQ):
+            for w in range(u):
+                inter = len(sets[u] & sets[w])
+                if 3 * inter > len(sets[u]) + len(sets[w]):
+                    fam[u] = w
+                    break
+        qperm.append(pq); kperm.append(pk); qoff.append(oq); koff.append(ok)
+        kvc.append(cnt); kvi.append(idx); rows.append(rr); fams.append(fam)
+    t = lambda a: torch.from_numpy(np.stack(a).astype(np.int32)).cuda()
+    Qp = PT.to_dev(np.stack([q[h][qperm[h]] for h in range(H)]), "bf16")
+    Kp = PT.to_dev(np.stack([k[h][kperm[h]] for h in range(H)]), "bf16")
+    Vp = PT.to_dev(np.stack([v[h][kperm[h]] for h in range(H)]), "bf16")
+    ws = P.workspace(Qp, CQ, CK)
+    Ot = P.park_block_sparse_attn(Qp, Kp, Vp, t(qoff), t(koff), t(kvc), t(kvi), t(qperm), CQ, CK,
+                                  P.PARK_F32, ws=ws)
+    torch.cuda.synchronize()
+    # plan layout after the 256-byte status region: order [H][CQ], row
+    # prefix [H][CQ+1], groups int4 [H][GPH] (16-byte aligned), families [H][CQ]
+    W = -(-N // 128)
+    GPH = W + -(-(CQ + W) // 16) + 1
+    goff = ((H * CQ + H * (CQ + 1)) * 4 + 15) & ~15
+    raw = ws.cpu().numpy()[256:].view(np.uint8)
+    order = raw[:H * CQ * 4].view(np.int32).reshape(H, CQ)
+    fam_dev = raw[goff + H * GPH * 16:goff + H * GPH * 16 + H * CQ * 4].view(np.int32).reshape(H, CQ)
+    Og = PT.np64(Ot)
+    for h in range(H):
+        assert np.array_equal(fam_dev[h], fams[h])
+        lab = fams[h][fams[h]]
+        seq = lab[order[h][order[h] >= 0]]
+        # each label occupies one contiguous run of the order
+        runs = [int(x) for i, x in enumerate(seq) if i == 0 or seq[i - 1] != x]
+        assert len(runs) == len(set(runs)), runs
+        ref = O.block_sparse_attention(q[h][qperm[h]], k[h][kperm[h]], v[h][kperm[h]], qoff[h],
+                                       koff[h], rows[h], qperm[h])
+        err = np.abs(Og[h] - ref)
+        print(f"[families h={h}] {len(set(lab.tolist()))} families, attention max-abs err "
+              f"{err.max():.3g}")
+        assert np.all(err <= PT.attn_tol("bf16", False, ref)), err.max()
+
+
 def test_dense_when_every_block_kept():
     cfg = synth.CONFIGS["tiny"]
     q, k, v = synth.make_layer(cfg)
