@@ -735,13 +735,14 @@ __device__ __forceinline__ void pm_wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// Work list of the fast retrieval: per head, every query block in rounds of
-// 64 queries, one round per wavefront and four per workgroup, in block order.
-// items[h][k] = {block u, round r, part slot (-1 for round 0), rounds of u};
-// round 0 writes the block's row of W^, later rounds a row of `part`
-// (slot = pstart[u] + r - 1), added up in round order by k_pama_combine.
+// Work list of the fast retrieval: per head, every query block in chunks of
+// 32 queries, in block order; a wavefront takes two consecutive chunks (they
+// may belong to different blocks) and a workgroup eight.
+// items[h][k] = {block u, chunk r, part slot (-1 for chunk 0), chunks of u};
+// chunk 0 writes the block's row of W^, later chunks a row of `part`
+// (slot = pstart[u] + r - 1), added up in chunk order by k_pama_combine.
 // nitem[h] = number of items, pstart[h][u] = rows of `part` taken by the
-// blocks before u (every round after a block's first takes one).  The
+// blocks before u (every chunk after a block's first takes one).  The
 // per-row error bounds are cleared for the workgroups' atomic maxima.  One
 // workgroup of 1024 threads per head, CQ <= 2048.
 __global__ __launch_bounds__(1024) void k_pama_plan(const int* __restrict__ q_offsets, int N,
@@ -753,7 +754,7 @@ __global__ __launch_bounds__(1024) void k_pama_plan(const int* __restrict__ q_of
   __shared__ int ps[MAXC + 1];
   const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int* off = q_offsets + (size_t)h * (CQ + 1);
-  // two blocks per thread: rounds, then a workgroup scan
+  // two blocks per thread: chunks, then a workgroup scan
   int c[2];
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
@@ -761,11 +762,11 @@ __global__ __launch_bounds__(1024) void k_pama_plan(const int* __restrict__ q_of
     c[k] = 0;
     if (u < CQ) {
       const int a = min(max(off[u], 0), N), b = min(max(off[u + 1], a), N);
-      c[k] = (b - a + 63) >> 6;
+      c[k] = (b - a + 31) >> 5;
       delta[(size_t)h * CQ + u] = 0.0f;
     }
   }
-  // exclusive scans of the rounds (items) and of the rounds after the first
+  // exclusive scans of the chunks (items) and of the chunks after the first
   // (part rows), packed in one 64-bit word (32 bits each)
   const int e0 = c[0] > 1 ? c[0] - 1 : 0, e1 = c[1] > 1 ? c[1] - 1 : 0;
   const long long sum = (long long)(c[0] + c[1]) | ((long long)(e0 + e1) << 32);
@@ -857,24 +858,33 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
   __shared__ __attribute__((aligned(16))) float cbuf[4][64];  // c_q of each wavefront's chunk
   __shared__ float mx_s[2];
   // workgroups of a head on one XCD (its L2 holds the head's centroids)
-  const int G = (icap + 3) / 4, nwgs = G * H, per = (nwgs + 7) >> 3;
+  const int G = (icap + 7) / 8, nwgs = G * H, per = (nwgs + 7) >> 3;
   const int wgi = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
   if (wgi >= nwgs) return;
-  const int h = wgi / G, grp4 = wgi - h * G;
+  const int h = wgi / G, grp8 = wgi - h * G;
   const int T = min(nitem[h], icap);
-  if (4 * grp4 >= T) return;
+  if (8 * grp8 >= T) return;
   const int tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int k = 4 * grp4 + w;
-  const int4 itm = k < T ? items[(size_t)h * icap + k] : make_int4(-1, 0, -1, 0);
-  const int u = (unsigned)itm.x < (unsigned)CQ ? itm.x : -1;
-  const int rb = itm.y, pslot = itm.z;
   const int* off = q_offsets + (size_t)h * (CQ + 1);
-  const int q0 = u >= 0 ? min(max(off[u], 0), N) : 0;
-  const int q1 = u >= 0 ? min(max(off[u + 1], q0), N) : 0;
-  const int nu = q1 - q0;
-  const size_t wrow = ((size_t)h * CQ + (u >= 0 ? u : 0)) * CK;
-  float* prow = (pslot >= 0 && pslot < pcap) ? part + ((size_t)h * pcap + pslot) * CK : nullptr;
+  // this wavefront's two chunks (group g: queries q0[g] + 32 rc[g] + l % 32)
+  int ug[2], rc[2], q0[2], q1[2], nu[2];
+  float* orow[2];
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    const int k = 8 * grp8 + 2 * w + g;
+    const int4 itm = k < T ? items[(size_t)h * icap + k] : make_int4(-1, 0, -1, 0);
+    const int u = (unsigned)itm.x < (unsigned)CQ ? itm.x : -1;
+    ug[g] = u;
+    rc[g] = itm.y;
+    q0[g] = u >= 0 ? min(max(off[u], 0), N) : 0;
+    q1[g] = u >= 0 ? min(max(off[u + 1], q0[g]), N) : 0;
+    nu[g] = q1[g] - q0[g];
+    if (u >= 0 && 32 * rc[g] < nu[g] && rc[g] == 0) orow[g] = W32 + ((size_t)h * CQ + u) * CK;
+    else if (u >= 0 && 32 * rc[g] < nu[g] && itm.z >= 0 && itm.z < pcap)
+      orow[g] = part + ((size_t)h * pcap + itm.z) * CK;
+    else orow[g] = nullptr;
+  }
   if (tid < 64) {
     float a = 0.0f, c = 0.0f;
     for (int i = tid; i < nbm; i += 64) {
@@ -912,7 +922,7 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
   // the centroid fragment of this lane: row c32 of a tile, dims 16 s + 8 hf ..
   const int crow = c32 * D, cswz = pm_swz<D>(c32);
 
-  float dmax = 0.0f;  // this wavefront's relative error bound
+  float dmax[2] = {0.0f, 0.0f};  // relative error bound of each chunk
   const int total = 2 * nt;
 #pragma unroll
   for (int p = 0; p < NS - 1; ++p)
@@ -974,14 +984,15 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
   };
   bf16x8_t qf[2][KS];
   {
-    // this wavefront's round: queries q0 + 64 rb + 32 g + l%32
-    const int rr = rb;
-    const bool on = u >= 0 && 64 * rr < nu;
+    bool ong[2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) ong[g] = orow[g] != nullptr;
+    const bool on = ong[0] || ong[1];
     float m[2], z[2];
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
-      const int qa = q0 + 64 * rr + 32 * g + c32;
-      const bool qv = on && qa < q1;
+      const int qa = q0[g] + 32 * rc[g] + c32;
+      const bool qv = ong[g] && qa < q1[g];
       float qsq = 0.0f;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
@@ -1007,8 +1018,8 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
         const float dZ = DEL * (10.0f + 3.0f * log2f((float)CK + 1.0f) + 2.0f * nadd +
                                 3.0f * argmax) +
                          2.0f * U24 * (nadd + 24.0f);
-        dmax = fmaxf(dmax, 2.02f * ei + dZ +
-                               DEL * (3.0f + 2.5f * argmax + 2.0f * log2f((float)CK + 1.0f)));
+        dmax[g] = fmaxf(dmax[g], 2.02f * ei + dZ +
+                                     DEL * (3.0f + 2.5f * argmax + 2.0f * log2f((float)CK + 1.0f)));
       }
       m[g] = -INFINITY;
       z[g] = 0.0f;
@@ -1054,8 +1065,8 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
       float zz = 0.0f;
       if (M != -INFINITY)
         zz = z[g] * __builtin_amdgcn_exp2f(m[g] - M) + oz * __builtin_amdgcn_exp2f(om - M);
-      const int qa = q0 + 64 * rr + 32 * g + c32;
-      const float c = (on && qa < q1 && zz > 0.0f) ? M + __builtin_amdgcn_logf(zz) : INFINITY;
+      const int qa = q0[g] + 32 * rc[g] + c32;
+      const float c = (ong[g] && qa < q1[g] && zz > 0.0f) ? M + __builtin_amdgcn_logf(zz) : INFINITY;
       if (hf == 0) cbuf[w][32 * g + c32] = c;
     }
     // pass 2: lane holds centroid c0 + c32, queries 8b + 4hf + r of each group
@@ -1063,7 +1074,7 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
       const int slot = ring_step();
       if (!on) continue;
       const float lgj = Lt[slot][c32] * L2E;
-      float ws = 0.0f;
+      float ws[2];
       f32x16_t hi[2], rest[2];
       products(qf, &Ct[slot][0], true, hi, rest);
 #pragma unroll
@@ -1082,29 +1093,29 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
         for (int o = 8; o > 0; o >>= 1)
 #pragma unroll
           for (int q = 0; q < o; ++q) e[q] += e[q + o];
-        ws += e[0];
+        ws[g] = e[0] + __shfl_xor(e[0], 32, 64);
       }
-      ws += __shfl_xor(ws, 32, 64);
+      // lanes of half g write chunk g's sums
       const int v = tile * CT + c32;
-      if (hf == 0 && v < CK) {
-        const float add = ws / (float)nu;
-        if (rr == 0) W32[wrow + v] = add;
-        else if (prow) prow[v] = add;
-      }
+      float* dst = hf ? orow[1] : orow[0];
+      if (dst && v < CK) dst[v] = (hf ? ws[1] : ws[0]) / (float)(hf ? nu[1] : nu[0]);
     }
   }
-  if (u >= 0 && nu > 0) {
-    // the row's bound: the largest over its rounds (non-negative floats
-    // order as their bit patterns), finished by k_pama_combine
-    for (int o = 32; o > 0; o >>= 1) dmax = fmaxf(dmax, __shfl_xor(dmax, o, 64));
-    if (l == 0) atomicMax((int*)&delta[(size_t)h * CQ + u], __float_as_int(dmax));
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    if (orow[g]) {
+      // the row's bound: the largest over its chunks (non-negative floats
+      // order as their bit patterns), finished by k_pama_combine
+      float dm = dmax[g];
+      for (int o = 32; o > 0; o >>= 1) dm = fmaxf(dm, __shfl_xor(dm, o, 64));
+      if (l == 0) atomicMax((int*)&delta[(size_t)h * CQ + ug[g]], __float_as_int(dm));
+    }
   }
 }
 
-// Rows of the fast retrieval: W^ = round 0 + round 1 + ... in round order
-// (the additions a single pass over the rounds would make), empty blocks a
-// zero row; the bound becomes delta_u = (max over rounds + (17 + 2 rounds)
-// 2^-24) 1.01.  Grid-stride over the rows of all heads.
+// Rows of the fast retrieval: W^ = chunk 0 + chunk 1 + ... in chunk order,
+// empty blocks a zero row; the bound becomes delta_u = (max over chunks +
+// (17 + 2 chunks) 2^-24) 1.01.  Grid-stride over the rows of all heads.
 __global__ __launch_bounds__(256) void k_pama_combine(const int* __restrict__ q_offsets,
                                                       const int* __restrict__ pstart, int H,
                                                       int N, int CQ, int CK,
@@ -1116,7 +1127,7 @@ __global__ __launch_bounds__(256) void k_pama_combine(const int* __restrict__ q_
     const int h = row / CQ, u = row - h * CQ;
     const int* off = q_offsets + (size_t)h * (CQ + 1);
     const int a = min(max(off[u], 0), N), b = min(max(off[u + 1], a), N);
-    const int nch = (b - a + 63) >> 6;
+    const int nch = (b - a + 31) >> 5;
     float* wr = W32 + (size_t)row * CK;
     if (nch == 0) {
       for (int v = threadIdx.x; v < CK; v += 256) wr[v] = 0.0f;
@@ -1125,7 +1136,7 @@ __global__ __launch_bounds__(256) void k_pama_combine(const int* __restrict__ q_
     }
     if (threadIdx.x == 0) delta[row] = (delta[row] + (17.0f + 2.0f * nch) * U24) * 1.01f;
     if (nch == 1) continue;
-    const int s0 = pstart[(size_t)h * (CQ + 1) + u];  // part row of round 1
+    const int s0 = pstart[(size_t)h * (CQ + 1) + u];  // part row of chunk 1
     for (int v = threadIdx.x; v < CK; v += 256) {
       float acc = wr[v];
       for (int r = 1; r < nch; ++r) {
@@ -1550,9 +1561,9 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   const int nbm = (CK + 15) / 16;
   float* W32 = W_out ? W_out : rb.W32;
   const int CKpad = pama_ckpad(CK);
-  // rounds of 64 queries, four per workgroup (work list per head)
+  // chunks of 32 queries, eight per workgroup (work list per head)
   const int icap = pama_icap(N, CQ), pcap = pama_pcap(N);
-  const unsigned nwg = 8u * ((((unsigned)icap + 3u) / 4u * (unsigned)H + 7u) / 8u);
+  const unsigned nwg = 8u * ((((unsigned)icap + 7u) / 8u * (unsigned)H + 7u) / 8u);
   float* part = (float*)rb.W64;  // free until the float64 rows are computed
   PARK_LAUNCH("pama_plan", k_pama_plan, dim3(H), dim3(1024), 0, st, q_offsets, N, CQ, icap,
               rb.qitems, rb.nitem, rb.qstart, rb.delta);

@@ -101,7 +101,7 @@ struct RetrieveBufs {
   float* lg;      // [H][pama_ckpad(CK)] log n_v (-inf for empty and padding blocks)
   float* cn;      // [H][CK]     |c_v|
   float* bmax;    // [H][ceil(CK/16)][2] per-block max |c_v|, |log n_v|
-  int4* qitems;   // [H][pama_icap] fast-retrieval work list (rounds of 64 queries)
+  int4* qitems;   // [H][pama_icap] fast-retrieval work list (chunks of 32 queries)
   int* nitem;     // [H] items per head
   int* qstart;    // [H][CQ+1] first item of each query block
   double* part;   // [p64_cap][CK] raw column sums of the later items of split rows
@@ -117,8 +117,8 @@ struct RetrieveBufs {
 // fast retrieval: items (rounds of 64 queries) per head, and rows of round
 // partial sums per head (every round after a block's first), kept in the
 // float64 W^ buffer, which is free until the float64 rows are computed
-inline int pama_icap(int N, int CQ) { return (N + 63) / 64 + CQ + 4; }
-inline int pama_pcap(int N) { return (N + 63) / 64 + 1; }
+inline int pama_icap(int N, int CQ) { return (N + 31) / 32 + CQ + 8; }
+inline int pama_pcap(int N) { return (N + 31) / 32 + 1; }
 // partial-sum rows available to the float64 pass (a quarter of the rows)
 inline int p64_cap(int H, int CQ) { return (H * CQ + 3) / 4; }
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
