@@ -222,6 +222,18 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
       }
       const int slot = it % NS;
       const float* cs = &Ct[slot][0];
+      if (r0 + 16 * w >= q1) {
+        // no query of this wavefront is in the block (the last chunk of a
+        // block that is not a multiple of 64): its column sums are zero, as
+        // the exponentials of its rows would be, and its SIMD is left to the
+        // other workgroup
+        if (pass == 1 && g == 0) {
+#pragma unroll
+          for (int cb = 0; cb < CT / 16; ++cb) stg[it & 1][w][16 * cb + c16] = 0.0;
+        }
+        prev_t = pass == 1 ? tile : -1;
+        continue;
+      }
       constexpr int UNR = W2 ? 1 : CT / 16;
 #pragma unroll UNR
       for (int cb = 0; cb < CT / 16; ++cb) {
