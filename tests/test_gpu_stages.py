@@ -167,6 +167,54 @@ def test_retrieval_matches_oracle(case, mode):
             assert np.array_equal(kvi[h][u, :kvc[h][u]], kvi2[h][u, :kvc2[h][u]]), (h, u)
 
 
+@pytest.mark.parametrize("mode", ["topk", "topp"])
+def test_retrieval_small_query_blocks(mode):
+    # query blocks of 0-40 rows and a few of 100-300 (bf16): a wavefront's
+    # two 32-query chunks often belong to different blocks, blocks end on
+    # odd chunk counts, and empty blocks sit between them
+    rng = np.random.default_rng(21)
+    H, N, d, CQ, CK = 2, 3000, 128, 160, 96
+    param = 0.2 if mode == "topk" else 0.9
+    qps, qoffs, cens, ns, Ws = [], [], [], [], []
+    for h in range(H):
+        sizes = rng.choice([0, 1, 5, 17, 31, 33, 40, 150, 300], size=CQ,
+                           p=[0.1, 0.1, 0.15, 0.15, 0.1, 0.1, 0.1, 0.1, 0.1]).astype(np.int64)
+        while sizes.sum() > N:
+            i = int(np.argmax(sizes))
+            sizes[i] -= min(sizes[i], sizes.sum() - N)
+        sizes[-1] += N - sizes.sum()
+        off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+        Qp = synth.bf16_round(rng.standard_normal((N, d)).astype(np.float32) * 1.5)
+        kz = rng.integers(0, CK, N)
+        Kx = rng.standard_normal((N, d)).astype(np.float32)
+        pk, ok = O.stable_argsort(kz, CK)
+        c, n = O.block_centroids(Kx[pk], ok)
+        qps.append(Qp)
+        qoffs.append(off)
+        cens.append(c)
+        ns.append(n)
+        Ws.append(O.pama(Qp, off, c, n))
+    Qd = PT.to_dev(np.stack(qps), "bf16")
+    qoff = torch.from_numpy(np.stack(qoffs).astype(np.int32)).cuda()
+    cen = torch.from_numpy(np.stack(cens)).cuda()
+    ksz = torch.from_numpy(np.stack(ns).astype(np.int32)).cuda()
+    sel = P.PARK_SELECT_TOPK if mode == "topk" else P.PARK_SELECT_TOPP
+    kvc, kvi, W = P.park_retrieve_blocks(Qd, qoff, cen, ksz, CQ, CK, sel, param, want_W=True)
+    kvc2, kvi2, _ = P.park_retrieve_blocks(Qd, qoff, cen, ksz, CQ, CK, sel, param)
+    kvc, kvi, W = kvc.cpu().numpy(), kvi.cpu().numpy(), W.cpu().numpy()
+    kvc2, kvi2 = kvc2.cpu().numpy(), kvi2.cpu().numpy()
+    for h in range(H):
+        ok, werr = PT.w_error_ok("bf16", W[h], Ws[h])
+        print(f"[small query blocks {mode} h={h}] W max-abs err {werr:.3g}")
+        assert ok, werr
+        qs = np.diff(qoffs[h])
+        assert np.all(W[h][qs == 0] == 0.0)
+        for kc, ki in ((kvc[h], kvi[h]), (kvc2[h], kvi2[h])):
+            nd, nb = PT.compare_masks(Ws[h], ns[h], qs, mode, param, kc, ki)
+            print(f"[small query blocks {mode} h={h}] mask rows differing={nd} not-exempt={nb}")
+            assert nb == 0
+
+
 @pytest.mark.parametrize("out_dtype", [P.PARK_F32, P.PARK_BF16])
 def test_attention_matches_oracle(case, out_dtype):
     tag, cfg, q, k, v = case
