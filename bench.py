@@ -138,8 +138,9 @@ def kernel_work(name, cfg, st, C):
         return "hbm", (1.0 * N * d * eb + 12.0 * N + C * d * 8.0) * H, "byte", "hbm"
     if name == "kfilter_cand":  # mu . w_v for every centroid pair, three split products
         return "mfma", 3.0 * 2.0 * C * C * d * H, "flop", "mfma_bf16"
-    if name == "pama_fast":
+    if name in ("pama_fast", "pama_fullk"):
         # one q.c product per (query, key block); the centroid split issues it 3x on MFMA
+        # (the two-pass kernel twice, the single-sweep one once)
         return "mfma", 2.0 * N * C * d * H, "flop", "mfma_bf16"
     if name == "pama64":
         return "alu", 2.0 * N * C * d * H, "flop", "alu_f64"

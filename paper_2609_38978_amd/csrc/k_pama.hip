@@ -1125,6 +1125,256 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
   }
 }
 
+// centroid tiles of the single-sweep retrieval (its logits stay in registers)
+constexpr int FULLK_NT = 8;
+
+// Full-K retrieval (Alg. 1) for small key-block counts (CK <= 32 FK_NT): one
+// sweep over the centroids instead of two.  A wavefront takes one 32-query
+// chunk (items as in the fast retrieval, four per workgroup) and computes S^T
+// (lane: one query, 16 of each tile's 32 centroids) exactly as the fast
+// path's first pass, keeping every final logit of its query row in
+// registers; the online normaliser (m, z) is the fast path's, so the row
+// bound delta_u is the same.  The probabilities then come from the kept
+// logits, and each centroid's sum over the chunk's 32 queries is a fixed
+// five-level butterfly over the lanes (the fast path's pass 2 sums the same
+// values in a five-level tree), written to the chunk's row as before.
+template <int D, int FK_NT>
+__global__ __launch_bounds__(256, 2) void k_pama_fullk(const bf16_t* __restrict__ Qp,
+                                                       const int* __restrict__ q_offsets,
+                                                       const int4* __restrict__ items,
+                                                       const int* __restrict__ nitem, int icap,
+                                                       float* __restrict__ part, int pcap,
+                                                       const bf16_t* __restrict__ c3,
+                                                       size_t plane, const float* __restrict__ lg,
+                                                       int CKpad, const float* __restrict__ bmax,
+                                                       int nbm, int H, int N, int CQ, int CK,
+                                                       float* __restrict__ W32,
+                                                       float* __restrict__ delta) {
+  constexpr int CT = 32, KS = D / 16, CPR = D / 8, RPI = 64 / CPR;
+  constexpr int NI = 3 * CT / (4 * RPI);  // DMAs per wavefront and tile
+  static_assert(NI * 4 * RPI == 3 * CT && KS % 2 == 0, "tile shape");
+  constexpr int NS = 3;
+  constexpr float U24 = 5.9604645e-08f, DEL = 1.1920929e-07f, L2E = 1.4426950408889634f;
+  constexpr float ET = U24 * 1.01f + (32.0f * DEL + (KS / 2 - 1) * U24) * 1.01f +
+                       0.00390625f * 1.01f * (2 * D) * DEL + U24 * 1.01f;
+  __shared__ __attribute__((aligned(16))) bf16_t Ct[NS][3 * CT * D];  // [slot][part][row][D]
+  __shared__ __attribute__((aligned(16))) float Lt[NS][CT];
+  __shared__ float mx_s[2];
+  // workgroups of a head on one XCD (its L2 holds the head's centroids)
+  const int G = (icap + 3) / 4, nwgs = G * H, per = (nwgs + 7) >> 3;
+  const int wgi = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (wgi >= nwgs) return;
+  const int h = wgi / G, grp4 = wgi - h * G;
+  const int T = min(nitem[h], icap);
+  if (4 * grp4 >= T) return;
+  const int tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int* off = q_offsets + (size_t)h * (CQ + 1);
+  // this wavefront's chunk: queries q0 + 32 rc + l % 32
+  const int k = 4 * grp4 + w;
+  const int4 itm = k < T ? items[(size_t)h * icap + k] : make_int4(-1, 0, -1, 0);
+  const int u = (unsigned)itm.x < (unsigned)CQ ? itm.x : -1;
+  const int rc = itm.y;
+  const int q0 = u >= 0 ? min(max(off[u], 0), N) : 0;
+  const int q1 = u >= 0 ? min(max(off[u + 1], q0), N) : 0;
+  const int nu = q1 - q0;
+  float* orow = nullptr;
+  if (u >= 0 && 32 * rc < nu) {
+    if (rc == 0) orow = W32 + ((size_t)h * CQ + u) * CK;
+    else if (itm.z >= 0 && itm.z < pcap) orow = part + ((size_t)h * pcap + itm.z) * CK;
+  }
+  if (tid < 64) {
+    float a = 0.0f, c = 0.0f;
+    for (int i = tid; i < nbm; i += 64) {
+      a = fmaxf(a, bmax[((size_t)h * nbm + i) * 2]);
+      c = fmaxf(c, bmax[((size_t)h * nbm + i) * 2 + 1]);
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      a = fmaxf(a, __shfl_xor(a, o, 64));
+      c = fmaxf(c, __shfl_xor(c, o, 64));
+    }
+    if (tid == 0) {
+      mx_s[0] = a;
+      mx_s[1] = c;
+    }
+  }
+  __syncthreads();
+  const float cmax = mx_s[0], lgmax = mx_s[1];
+  const float isd = 1.0f / sqrtf((float)D), isdL = isd * L2E;
+  const bf16_t* P1 = c3 + (size_t)h * CK * D;
+  const float* lgh = lg + (size_t)h * CKpad;
+  const int pch = l % CPR;
+  const int nt = (CK + CT - 1) / CT;  // <= FK_NT (the launcher checks)
+  auto issue = [&](int tile, int slot) {
+    const int c0 = tile * CT;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int row = (w * NI + i) * RPI + l / CPR;
+      const int part = row / CT, r = row % CT;
+      const int v = min(c0 + r, CK - 1);
+      const bf16_t* src = P1 + part * plane + (size_t)v * D + 8 * (pch ^ pm_swz<D>(r));
+      pm_dma16(src, pm_lds_addr(&Ct[slot][0] + (w * NI + i) * 512));
+    }
+    if (w == 0 && l < CT / 4) pm_dma16(lgh + c0 + 4 * l, pm_lds_addr(&Lt[slot][0]));
+  };
+  const int crow = c32 * D, cswz = pm_swz<D>(c32);
+  const bool on = orow != nullptr;
+  // the query fragment and the row bound of this lane's query
+  const int qa = q0 + 32 * rc + c32;
+  const bool qv = on && qa < q1;
+  bf16x8_t qf[KS];
+  float dmax = 0.0f;
+  {
+    float qsq = 0.0f;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+      if (qv) raw = *(const uint4*)(Qp + ((size_t)h * N + qa) * D + 16 * s + 8 * hf);
+      qf[s] = __builtin_bit_cast(bf16x8_t, raw);
+      asm volatile("" ::"v"(qf[s]));  // loads complete here, not inside the ring waits
+      const uint32_t q[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(q[e] << 16), hi = __uint_as_float(q[e] & 0xffff0000u);
+        qsq = fmaf(lo, lo, fmaf(hi, hi, qsq));
+      }
+    }
+    qsq += __shfl_xor(qsq, 32, 64);
+    if (qv) {
+      // the row error bound of this query, as in the fast path
+      const float qn = sqrtf(qsq) * 1.0001f;
+      const float ei = isd * (ET + 1.01f * U24) * qn * cmax +
+                       1.01f * U24 * (3.0f * lgmax + 2.02f * isd * qn * cmax);
+      const float argmax = 2.0f * (isd * qn * cmax + lgmax) * L2E;
+      const float nadd = fmaxf((float)(CK / 16 + 1), (float)(CK / 32 + 5));
+      const float dZ = DEL * (10.0f + 3.0f * log2f((float)CK + 1.0f) + 2.0f * nadd +
+                              3.0f * argmax) +
+                       2.0f * U24 * (nadd + 24.0f);
+      dmax = 2.02f * ei + dZ + DEL * (3.0f + 2.5f * argmax + 2.0f * log2f((float)CK + 1.0f));
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < nt) issue(p, p);
+  // the sweep: S^T of each tile (lane: query c32, centroids 8b + 4hf + r),
+  // kept in registers, and the online normaliser
+  float L[FK_NT][16];
+  float m = -INFINITY, z = 0.0f;
+#pragma unroll
+  for (int tile = 0; tile < FK_NT; ++tile) {
+    if (tile < nt) {
+      if (tile + 1 < nt) {
+        if (w == 0) pm_wait_vmcnt<NI + 1>();
+        else pm_wait_vmcnt<NI>();
+      } else {
+        pm_wait_vmcnt<0>();
+      }
+      __syncthreads();  // tile landed everywhere; the tile before consumed (its slot is free)
+      if (tile + NS - 1 < nt) issue(tile + NS - 1, (tile + NS - 1) % NS);
+      const int slot = tile % NS;
+      if (!on) continue;  // no chunk: the ring steps only
+      const bf16_t* B1 = &Ct[slot][0];
+      const bf16_t* B2 = B1 + CT * D;
+      const bf16_t* B3 = B2 + CT * D;
+      f32x16_t hi, rest;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) rest[q] = 0.0f;
+#pragma unroll
+      for (int sp = 0; sp < KS / 2; ++sp) {
+        f32x16_t seg;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) seg[q] = 0.0f;
+#pragma unroll
+        for (int s = 2 * sp; s < 2 * sp + 2; ++s) {
+          const int co = crow + 8 * ((2 * s + hf) ^ cswz);
+          const bf16x8_t b1 = *(const bf16x8_t*)(B1 + co);
+          const bf16x8_t b2 = *(const bf16x8_t*)(B2 + co);
+          const bf16x8_t b3 = *(const bf16x8_t*)(B3 + co);
+          seg = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, qf[s], seg, 0, 0, 0);
+          rest = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b2, qf[s], rest, 0, 0, 0);
+          rest = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b3, qf[s], rest, 0, 0, 0);
+        }
+        hi = sp == 0 ? seg : hi + seg;
+      }
+#pragma unroll
+      for (int bq = 0; bq < 4; ++bq) {
+        const float4 l4 = *(const float4*)(&Lt[slot][8 * bq + 4 * hf]);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          L[tile][4 * bq + r] = fmaf(hi[4 * bq + r] + rest[4 * bq + r], isdL, lv[r] * L2E);
+      }
+      {
+        float tmax = fmaxf(L[tile][0], L[tile][1]);
+#pragma unroll
+        for (int q = 2; q < 16; ++q) tmax = fmaxf(tmax, L[tile][q]);
+        const float mn = fmaxf(m, tmax);
+        if (mn != -INFINITY) {
+          float sv[16];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) sv[q] = __builtin_amdgcn_exp2f(L[tile][q] - mn);
+#pragma unroll
+          for (int o = 8; o > 0; o >>= 1)
+#pragma unroll
+            for (int q = 0; q < o; ++q) sv[q] += sv[q + o];
+          z = (m == mn ? z : z * __builtin_amdgcn_exp2f(m - mn)) + sv[0];
+          m = mn;
+        }
+      }
+    }
+  }
+  // c_q = m + log2 z per query (the two halves of a query merged); invalid
+  // queries +inf, so their probabilities are zero
+  float cq;
+  {
+    const float om = __shfl_xor(m, 32, 64), oz = __shfl_xor(z, 32, 64);
+    const float M = fmaxf(m, om);
+    float zz = 0.0f;
+    if (M != -INFINITY) zz = z * __builtin_amdgcn_exp2f(m - M) + oz * __builtin_amdgcn_exp2f(om - M);
+    cq = (qv && zz > 0.0f) ? M + __builtin_amdgcn_logf(zz) : INFINITY;
+  }
+  // probabilities from the kept logits, summed over the chunk's 32 queries
+  // per centroid: each tile's 32 x 32 probabilities go through LDS (this
+  // wavefront's part of the ring, free after the sweep) from query lanes to
+  // centroid lanes; lane (c, half) sums queries 16 half .. 16 half + 15 of
+  // centroid c in a four-level tree and adds the other half's sum (the
+  // five-level depth of the fast path's in-chunk sums)
+  __syncthreads();  // every wavefront is done with the ring
+  if (on) {
+    constexpr int TS = 36;  // row stride (floats) of the transpose buffer
+    float* tb = (float*)&Ct[0][0] + w * (32 * TS);
+    const float fnu = (float)nu;
+#pragma unroll
+    for (int tile = 0; tile < FK_NT; ++tile) {
+      if (tile < nt) {
+        float e[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) e[q] = __builtin_amdgcn_exp2f(L[tile][q] - cq);
+        // lane (query c32, hf) holds centroids 8b + 4hf + r
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          *(float4*)&tb[c32 * TS + 8 * b + 4 * hf] =
+              make_float4(e[4 * b], e[4 * b + 1], e[4 * b + 2], e[4 * b + 3]);
+        float x[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) x[j] = tb[(16 * hf + j) * TS + c32];
+#pragma unroll
+        for (int o = 8; o > 0; o >>= 1)
+#pragma unroll
+          for (int j = 0; j < o; ++j) x[j] += x[j + o];
+        const float other = __shfl_xor(x[0], 32, 64);
+        const float sum = hf ? other + x[0] : x[0] + other;
+        const int v = tile * CT + c32;
+        if (hf == 0 && v < CK) orow[v] = sum / fnu;
+      }
+    }
+    // the row's bound: the largest over its chunks, finished by k_pama_combine
+    float dm = dmax;
+    for (int o = 32; o > 0; o >>= 1) dm = fmaxf(dm, __shfl_xor(dm, o, 64));
+    if (l == 0) atomicMax((int*)&delta[(size_t)h * CQ + u], __float_as_int(dm));
+  }
+}
+
 // Rows of the fast retrieval: W^ = chunk 0 + chunk 1 + ... in chunk order,
 // empty blocks a zero row; the bound becomes delta_u = (max over chunks +
 // (17 + 2 chunks) 2^-24) 1.01.  Grid-stride over the rows of all heads.
@@ -1579,7 +1829,27 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   float* part = (float*)rb.W64;  // free until the float64 rows are computed
   PARK_LAUNCH("pama_plan", k_pama_plan, dim3(H), dim3(1024), 0, st, q_offsets, N, CQ, icap,
               rb.qitems, rb.nitem, rb.qstart, rb.delta);
-  if (D == 128) {
+  // at most FULLK_NT centroid tiles: the single-sweep (Full-K) retrieval,
+  // one chunk per wavefront, four per workgroup
+  const bool fullk = CK <= 32 * FULLK_NT;
+  const unsigned nwg4 = 8u * ((((unsigned)icap + 3u) / 4u * (unsigned)H + 7u) / 8u);
+  if (fullk) {
+    if (D == 128) {
+      PARK_LAUNCH("pama_cen_prep", k_cen_prep<128>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes,
+                  CK, rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
+      PARK_LAUNCH("pama_fullk", (k_pama_fullk<128, FULLK_NT>), dim3(nwg4), dim3(256), 0, st,
+                  (const bf16_t*)Qp, q_offsets, (const int4*)rb.qitems, (const int*)rb.nitem,
+                  icap, part, pcap, (const bf16_t*)rb.c3, plane, (const float*)rb.lg, CKpad,
+                  (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
+    } else {
+      PARK_LAUNCH("pama_cen_prep", k_cen_prep<64>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes,
+                  CK, rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
+      PARK_LAUNCH("pama_fullk", (k_pama_fullk<64, FULLK_NT>), dim3(nwg4), dim3(256), 0, st,
+                  (const bf16_t*)Qp, q_offsets, (const int4*)rb.qitems, (const int*)rb.nitem,
+                  icap, part, pcap, (const bf16_t*)rb.c3, plane, (const float*)rb.lg, CKpad,
+                  (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
+    }
+  } else if (D == 128) {
     PARK_LAUNCH("pama_cen_prep", k_cen_prep<128>, dim3(nbm, H), dim3(256), 0, st, cen, k_sizes, CK,
                 rb.c3, plane, rb.lg, CKpad, rb.cn, rb.bmax);
     PARK_LAUNCH("pama_fast", k_pama_fast<128>, dim3(nwg), dim3(256), 0, st, (const bf16_t*)Qp,
