@@ -144,6 +144,8 @@ def kernel_work(name, cfg, st, C):
         return "mfma", 2.0 * N * C * d * H, "flop", "mfma_bf16"
     if name == "pama64":
         return "alu", 2.0 * N * C * d * H, "flop", "alu_f64"
+    if name == "qcen64":  # one qbar_u . c_v product per (query block, key block)
+        return "alu", 2.0 * C * C * d * H, "flop", "alu_f64"
     if name == "gram_partial":
         return "alu", 2.0 * N * d * d * H, "flop", "alu_f64"
     if name in ("attn_valu", "attn_mfma"):

@@ -61,9 +61,20 @@ __device__ int block_exclusive_scan_2048(int* a, int n, int* tmp) {
 // ring filled by LDS DMA (rows swizzled in 16-byte chunks so the B-operand
 // reads are free of bank conflicts).  Logits, exponentials and all sums in
 // float64; a tile's per-wavefront column sums go through LDS and are added to
-// the row's column sums in wavefront order, chunk after chunk (deterministic).  With a row list it recomputes only the listed query
-// blocks (the rows the fast path could not certify); the workgroups of a
-// head run on one XCD.
+// the row's column sums in wavefront order, chunk after chunk (deterministic).
+// With a row list it recomputes only the listed query blocks (the rows the
+// fast path could not certify); the workgroups of a head run on one XCD.
+//
+// Given the fast path's W^ and its certified relative error delta_u (plus
+// 4 2^-126 absolute near float's underflow), the normaliser pass leaves out
+// the blocks that cannot matter to it: every query i of block u has
+// P_iv <= n_u W_uv, so a block with n_u CK (W^_uv (1 + delta_u) + 4 2^-126)
+// below P64_DROP carries less than P64_DROP / CK of every Z_i, all such
+// blocks together less than P64_DROP.  Each Z_i then comes out between
+// (1 - P64_DROP) Z_i and Z_i, each W^ of the row between W^ and
+// W^ (1 + 2 P64_DROP): far inside float32's resolution, and far below the
+// near-tie gaps the float64 selection is meant to resolve.  On clustered
+// DiT activations only a few percent of the blocks of a row remain.
 __device__ __forceinline__ void p64_dma16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
                : "memory", "m0");
@@ -72,6 +83,31 @@ __device__ __forceinline__ uint32_t p64_lds_addr(const void* p) {
   return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
 }
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
+constexpr double P64_DROP = 0x1p-33;
+
+// exclusive scan of one int per thread over a 256-thread workgroup; `tmp`
+// needs 4 ints
+__device__ int wg256_exclusive(int x, int* tmp, int& total) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  int inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) tmp[wid] = inc;
+  __syncthreads();
+  int pre = 0;
+  total = 0;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int t = tmp[v];
+    if (v < wid) pre += t;
+    total += t;
+  }
+  __syncthreads();  // tmp is free for the next scan
+  return pre + inc - x;
+}
 
 // W2: two wavefronts per SIMD (centroid blocks of a tile one after the other,
 // registers within 256); otherwise one wavefront per SIMD with the two blocks
@@ -85,7 +121,10 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
                                                 int* __restrict__ cnt, double* __restrict__ part,
                                                 double* __restrict__ W64, float* __restrict__ W32,
                                                 const int* __restrict__ bandc,
-                                                const int* __restrict__ kv_index, int* status) {
+                                                const int* __restrict__ kv_index,
+                                                const float* __restrict__ wfast,
+                                                const float* __restrict__ dfast, int plist,
+                                                int* status) {
   constexpr int CT = 32, CPR = D / 4, RPI = 64 / CPR, NI = CT / (4 * RPI), KS = D / 4;
   static_assert(NI * 4 * RPI == CT, "tile shape");
   constexpr int NS = 3;  // centroid ring: one tile in flight while one is used
@@ -93,11 +132,12 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
   __shared__ double Lt[NS][CT];
   __shared__ double stg[2][4][CT];  // per-wavefront column sums of a tile (by step parity)
   extern __shared__ double wacc64[];  // [CK] column sums of the item, in chunk and wavefront order
-  __shared__ int item_s;
+  int* keep = (int*)(wacc64 + CK);    // [CK] blocks of the normaliser pass, ascending
+  __shared__ int item_s, ktmp[4];
   const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const double isd = 1.0 / sqrt((double)D);
-  const int nt = (CK + CT - 1) / CT;
+  const int ntf = (CK + CT - 1) / CT;
   const int pch = l % CPR;
   const int nall = H * CQ, per = (nall + 7) >> 3;
   for (int k = -1;;) {
@@ -128,17 +168,25 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
     const T* Qh = Qp + (size_t)h * N * D;
     // band rows: the probability pass covers only the listed (ambiguous)
     // blocks, which sit at the end of the row of kv_index; the normaliser
-    // pass always covers every block
+    // pass covers every block that can matter to it (n0 blocks: keep[], or
+    // all of them)
     const int nb = bandc ? min(bandc[rid], CK) : -1;
     const int* blist = nb >= 0 ? kv_index + (size_t)rid * CK + (CK - nb) : nullptr;
-    const int nt2 = nb >= 0 ? (nb + CT - 1) / CT : nt;
-    const int Lc = nt + nt2;  // steps per chunk of 64 queries
+    int nt2 = nb >= 0 ? (nb + CT - 1) / CT : ntf;
+    int n0 = CK, nt = ntf;
+    bool lst = false;
+    // with plist, whole rows (top-p) take the list in the probability pass
+    // too: the blocks left out weigh less than P64_DROP / n_u together, so a
+    // cut at p < 1 - P64_DROP lies among the listed ones; theirs stay 0
+    const bool pl = plist && nb < 0;
     // column of tile row r in a pass (-1: none)
     auto column = [&](int pass, int tile, int r) {
       const int ix = tile * CT + r;
       if (pass == 1 && nb >= 0) return ix < nb ? min(max(blist[ix], 0), CK - 1) : -1;
+      if (pass == 0 || pl) return ix < n0 ? (lst ? keep[ix] : ix) : -1;
       return ix < CK ? ix : -1;
     };
+    int Lc = nt + nt2;  // steps per chunk of 64 queries
     auto issue = [&](int step, int slot) {
       const int j = step % Lc, pass = j >= nt ? 1 : 0, tile = pass ? j - nt : j;
 #pragma unroll
@@ -165,8 +213,37 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
       }
       continue;
     }
-    __syncthreads();  // the previous item's column sums have been read
+    __syncthreads();  // the previous item's column sums and block list have been read
     for (int v = tid; v < CK; v += 256) wacc64[v] = 0.0;
+    if (wfast) {
+      // the normaliser's blocks: thread t tests blocks 8t .. 8t + 7
+      const float* wr = wfast + wrow;
+      const double dl = (double)dfast[rid];
+      const double thr = P64_DROP / ((double)nu * (double)CK);
+      int fl = 0, c = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int e = 8 * tid + k;
+        // NaN / infinite bounds keep the block
+        const bool kp = e < CK && nh[e] > 0 &&
+                        !((double)wr[e] * (1.0 + dl) + 4.0 * 1.1754943508222875e-38 < thr);
+        fl |= (int)kp << k;
+        c += kp;
+      }
+      int tot;
+      int pos = wg256_exclusive(c, ktmp, tot);
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if ((fl >> k) & 1) keep[pos++] = 8 * tid + k;
+      __syncthreads();
+      if (tot > 0) {  // a row always holds a block of weight >= 1 / CK
+        lst = true;
+        n0 = tot;
+        nt = (tot + CT - 1) / CT;
+        if (pl) nt2 = nt;
+        Lc = nt + nt2;
+      }
+    }
     const int nch = min(ce, (nu + 63) / 64) - cb;  // chunks of 64 queries from cb on
     const int total = nch * Lc;
     float qa[KS];  // float holds bf16 and float32 inputs exactly
@@ -296,6 +373,154 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
         if (!isfinite(wv)) raise_status(status, ST_NONFINITE);
         if (W64) W64[wrow + v] = wv;
         if (W32) W32[wrow + v] = (float)wv;
+      }
+    }
+  }
+}
+
+// Query-centroid estimate (Sec. 4.1; the "w/o PAMA" variant of Sec. 6):
+//   W^_uv = softmax_v (qbar_u . c_v / sqrt(d) + log n_v)
+// for the float mean qbar_u of each nonempty query block (an empty block's
+// row is 0), in float64.  The float64 MFMA tiles of k_pama64, but each of a
+// tile's 64 query rows is a block of its own: a wavefront holds 16 blocks,
+// the normaliser pass keeps an online (max, sum) per block, and the
+// probability pass writes every block's row directly (no column sums).
+// Workgroup = 64 consecutive blocks of one head, the workgroups of a head on
+// one XCD.
+template <int D>
+__global__ __launch_bounds__(256, 2) void k_qcen64(const float* __restrict__ qbar,
+                                                  const int* __restrict__ qsizes,
+                                                  const float* __restrict__ cen,
+                                                  const int* __restrict__ k_sizes, int H, int CQ,
+                                                  int CK, double* __restrict__ W64,
+                                                  float* __restrict__ W32,
+                                                  float* __restrict__ delta, int* status) {
+  constexpr int CT = 32, CPR = D / 4, RPI = 64 / CPR, NI = CT / (4 * RPI), KS = D / 4;
+  static_assert(NI * 4 * RPI == CT, "tile shape");
+  constexpr int NS = 3;  // centroid ring: one tile in flight while one is used
+  __shared__ __attribute__((aligned(16))) float Ct[NS][CT * D];
+  __shared__ double Lt[NS][CT];
+  const int tid = threadIdx.x, l = tid & 63, g = l >> 4, c16 = l & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const double isd = 1.0 / sqrt((double)D);
+  const int nt = (CK + CT - 1) / CT, total = 2 * nt;  // normaliser tiles, then probability tiles
+  const int pch = l % CPR;
+  const int nchunk = (CQ + 63) / 64, nall = H * nchunk, per = (nall + 7) >> 3;
+  const int k = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (k >= nall) return;
+  const int h = k / nchunk, u0 = 64 * (k - h * nchunk);
+  const float* ch = cen + (size_t)h * CK * D;
+  const int* nh = k_sizes + (size_t)h * CK;
+  const int* qs = qsizes + (size_t)h * CQ;
+  auto issue = [&](int step, int slot) {
+    const int tile = step % nt;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = (w * NI + i) * RPI + l / CPR;
+      const int v = min(tile * CT + r, CK - 1);
+      const float* src = ch + (size_t)v * D + 4 * (pch ^ (r & (CPR - 1)));
+      p64_dma16(src, p64_lds_addr(&Ct[slot][0] + (w * NI + i) * 256));
+    }
+    if (tid < CT) {
+      const int v = tile * CT + tid;
+      const int n = v < CK ? nh[v] : 0;
+      Lt[slot][tid] = n > 0 ? log((double)n) : -INFINITY;
+    }
+  };
+  // A operand: block u0 + 16w + c16, dimensions 4s + g
+  float qa[KS];
+  {
+    const int ua = u0 + 16 * w + c16;
+    const bool ok = ua < CQ && qs[min(ua, CQ - 1)] > 0;
+    const float* qr = qbar + ((size_t)h * CQ + min(ua, CQ - 1)) * D;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qa[s] = ok ? qr[4 * s + g] : 0.0f;
+  }
+  // this lane's output blocks g + 4r of the wavefront
+  double m[4], z[4], mf[4];
+  bool qv[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int uo = u0 + 16 * w + g + 4 * r;
+    qv[r] = uo < CQ && qs[min(uo, CQ - 1)] > 0;
+    m[r] = -INFINITY;
+    z[r] = 0.0;
+  }
+  issue(0, 0);
+  if (total > 1) issue(1, 1);
+  for (int it = 0; it < total; ++it) {
+    const int pass = it >= nt ? 1 : 0, tile = pass ? it - nt : it;
+    if (it == nt) {
+      // merge (max, sum) over the 16 lanes holding the same blocks
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        double mm = m[r], zz = z[r];
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          const double om = __shfl_xor(mm, o, 64), oz = __shfl_xor(zz, o, 64);
+          const double nm = fmax(mm, om);
+          zz = (nm == -INFINITY) ? 0.0 : zz * exp(mm - nm) + oz * exp(om - nm);
+          mm = nm;
+        }
+        // P = exp(S - (m + log z)); empty blocks get exp(-inf) = 0
+        mf[r] = qv[r] && zz > 0.0 ? mm + log(zz) : INFINITY;
+        // the float row is the float64 one rounded once (2^-24), the float64
+        // row within ~1e-13 of exact: 2^-23 bounds the float row's error
+        const int uo = u0 + 16 * w + g + 4 * r;
+        if (c16 == 0 && uo < CQ) delta[(size_t)h * CQ + uo] = 0x1p-23f;
+      }
+    }
+    // own DMAs of this tile done (the next one may stay in flight)
+    if (it + 1 < total) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // tile landed everywhere; tile it-1 consumed (its slot is free)
+    if (it + 2 < total) issue(it + 2, (it + 2) % NS);
+    if (u0 + 16 * w >= CQ) continue;  // no block of this wavefront (the head's last chunk)
+    const int slot = it % NS;
+    const float* cs = &Ct[slot][0];
+#pragma unroll 1
+    for (int cb = 0; cb < CT / 16; ++cb) {
+      const int row = 16 * cb + c16;  // B operand: centroid row, dimension 4s + g
+      const float* crow = cs + row * D + g;
+      const int sw = row & (CPR - 1);
+      float bf[KS];
+#pragma unroll
+      for (int s = 0; s < KS; ++s) bf[s] = crow[4 * (s ^ sw)];
+      f64x4_t acc = {0.0, 0.0, 0.0, 0.0}, acc1 = acc;
+#pragma unroll
+      for (int s = 0; s < KS; s += 2) {
+        float a0 = qa[s], a1 = qa[s + 1];
+        asm volatile("" : "+v"(a0), "+v"(a1));
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a0, (double)bf[s], acc, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a1, (double)bf[s + 1], acc1, 0, 0, 0);
+      }
+      acc += acc1;
+      const double lg = Lt[slot][row];
+      if (pass == 0) {
+        if (lg != -INFINITY) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const double sv = acc[r] * isd + lg;
+            const double d = sv - m[r];
+            const double e = exp(-fabs(d));
+            z[r] = d <= 0.0 ? z[r] + e : fma(z[r], e, 1.0);
+            m[r] = fmax(m[r], sv);
+          }
+        }
+      } else {
+        const int col = tile * CT + row;
+        if (col < CK) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int uo = u0 + 16 * w + g + 4 * r;
+            if (uo >= CQ) continue;
+            const double pv = lg != -INFINITY ? exp(fma(acc[r], isd, lg - mf[r])) : 0.0;
+            if (!isfinite(pv)) raise_status(status, ST_NONFINITE);
+            const size_t o = ((size_t)h * CQ + uo) * CK + col;
+            W64[o] = pv;
+            W32[o] = (float)pv;
+          }
+        }
       }
     }
   }
@@ -1813,7 +2038,8 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   const int kcount = mode == PARK_SELECT_TOPK ? topk_count(CK, param) : 0;
   if (dtype != PARK_BF16) {  // float32 queries: float64 PAMA and selection of every row
     PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, nullptr, nullptr,
-                           nullptr, rb.W64, W_out, nullptr, nullptr, status, st));
+                           nullptr, rb.W64, W_out, nullptr, nullptr, nullptr, nullptr, 0, status,
+                           st));
     PARK_LAUNCH("select", k_select64, dim3(CQ, H), dim3(256), 0, st, (const double*)rb.W64,
                 q_offsets, k_sizes, CQ, CK, P, mode, param, kcount, (const int*)nullptr,
                 (const int*)nullptr, kv_count, kv_index, (const int*)nullptr);
@@ -1882,8 +2108,13 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
   PARK_LAUNCH("pama_plan64", k_p64_plan, dim3(1), dim3(1024), 0, st, q_offsets,
               (const int*)rb.rows, (const int*)rb.nrows, H, N, CQ, p64_cap(H, CQ), rb.items,
               rb.srows, rb.pcnt);
+  // the fast W^ rows and their bounds prune the normaliser pass (a row's
+  // float32 W^ is written only at the end of its last item), and the
+  // probability pass of top-p rows when W^ is not asked for
+  const int plist = (mode == PARK_SELECT_TOPP && !W_out) ? 1 : 0;
   PARK_TRY(launch_pama64(Qp, q_offsets, cen, k_sizes, H, N, D, dtype, CQ, CK, rb.items, rb.pcnt,
-                         rb.part, rb.W64, W32r, bandc, kv_index, status, st));
+                         rb.part, rb.W64, W32r, bandc, kv_index, W32, rb.delta, plist, status,
+                         st));
   PARK_LAUNCH("pama_combine64", k_p64_combine, dim3(256), dim3(256), 0, st,
               (const int4*)rb.srows, (const int*)rb.pcnt, (const double*)rb.part, CK, rb.W64, W32r,
               status);
@@ -1902,10 +2133,11 @@ static park_status pama64_launch(const char* nm, unsigned nwg, size_t lds, const
                                  int dtype, const int* q_offsets, const float* cen,
                                  const int* k_sizes, int H, int N, int CQ, int CK,
                                  const int4* items, int* cnt, double* part, double* W64,
-                                 float* W32, const int* bandc, const int* kv_index, int* status,
-                                 hipStream_t st) {
+                                 float* W32, const int* bandc, const int* kv_index,
+                                 const float* wfast, const float* dfast, int plist,
+                                 int* status, hipStream_t st) {
   // reserved once for the largest CK (2048), outside any stream capture that may follow
-  static const int lds_max = (int)(MAXC * sizeof(double));
+  static const int lds_max = (int)(MAXC * (sizeof(double) + sizeof(int)));
   static const hipError_t a1 = hipFuncSetAttribute(
       (const void*)k_pama64<bf16_t, D, W2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
   static const hipError_t a2 = hipFuncSetAttribute(
@@ -1915,35 +2147,70 @@ static park_status pama64_launch(const char* nm, unsigned nwg, size_t lds, const
   if (dtype == PARK_BF16)
     PARK_LAUNCH(nm, (k_pama64<bf16_t, D, W2>), dim3(nwg), dim3(256), lds, st, (const bf16_t*)Qp,
                 q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, bandc, kv_index,
-                status);
+                wfast, dfast, plist, status);
   else
     PARK_LAUNCH(nm, (k_pama64<float, D, W2>), dim3(nwg), dim3(256), lds, st, (const float*)Qp,
                 q_offsets, cen, k_sizes, H, N, CQ, CK, items, cnt, part, W64, W32, bandc, kv_index,
-                status);
+                wfast, dfast, plist, status);
   return PARK_OK;
 }
 
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                           const int4* items, int* cnt, double* part, double* W64, float* W32,
-                          const int* bandc, const int* kv_index, int* status, hipStream_t st) {
+                          const int* bandc, const int* kv_index, const float* wfast,
+                          const float* dfast, int plist, int* status, hipStream_t st) {
   // with an item list: a queue drained by a fixed grid; without: one
   // workgroup per row, the rows of a head on one XCD
   const unsigned nwg = items ? 512u : 8u * (((unsigned)H * (unsigned)CQ + 7u) / 8u);
-  const size_t lds = (size_t)CK * sizeof(double);
+  const size_t lds = (size_t)CK * (sizeof(double) + sizeof(int));
   const char* nm = items ? "pama_refine64" : "pama64";
   // small layers have few items: the shorter steps of one wavefront per SIMD
   // win; large ones fill the chip, and two wavefronts per SIMD hide latency
   const bool w2 = (long)H * CQ >= 8192;
   if (D == 128)
     return w2 ? pama64_launch<128, true>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N,
-                                         CQ, CK, items, cnt, part, W64, W32, bandc, kv_index, status, st)
+                                         CQ, CK, items, cnt, part, W64, W32, bandc, kv_index,
+                                         wfast, dfast, plist, status, st)
               : pama64_launch<128, false>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N,
-                                          CQ, CK, items, cnt, part, W64, W32, bandc, kv_index, status, st);
+                                          CQ, CK, items, cnt, part, W64, W32, bandc, kv_index,
+                                          wfast, dfast, plist, status, st);
   return w2 ? pama64_launch<64, true>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N, CQ,
-                                      CK, items, cnt, part, W64, W32, bandc, kv_index, status, st)
+                                      CK, items, cnt, part, W64, W32, bandc, kv_index, wfast,
+                                      dfast, plist, status, st)
             : pama64_launch<64, false>(nm, nwg, lds, Qp, dtype, q_offsets, cen, k_sizes, H, N, CQ,
-                                       CK, items, cnt, part, W64, W32, bandc, kv_index, status, st);
+                                       CK, items, cnt, part, W64, W32, bandc, kv_index, wfast,
+                                       dfast, plist, status, st);
+}
+
+// Query-centroid estimate and its selection: the float rows through the
+// certified float selection, the rows it cannot settle by float64 weights.
+park_status launch_qcen_retrieve(const float* qbar, const int* qsizes, const int* uoff,
+                                 const float* cen, const int* k_sizes, int H, int D, int CQ,
+                                 int CK, int mode, double param, const RetrieveBufs& rb,
+                                 float* W_out, int* kv_count, int* kv_index, int* status,
+                                 hipStream_t st) {
+  const int nall = H * ((CQ + 63) / 64);
+  const unsigned nwg = 8u * (((unsigned)nall + 7u) / 8u);
+  float* W32 = W_out ? W_out : rb.W32;
+  if (D == 128)
+    PARK_LAUNCH("qcen64", k_qcen64<128>, dim3(nwg), dim3(256), 0, st, qbar, qsizes, cen, k_sizes,
+                H, CQ, CK, rb.W64, W32, rb.delta, status);
+  else
+    PARK_LAUNCH("qcen64", k_qcen64<64>, dim3(nwg), dim3(256), 0, st, qbar, qsizes, cen, k_sizes,
+                H, CQ, CK, rb.W64, W32, rb.delta, status);
+  const int P = pow2_at_least(CK);
+  const int kcount = mode == PARK_SELECT_TOPK ? topk_count(CK, param) : 0;
+  PARK_LAUNCH("pama_reset", k_zero_counts, dim3((H + 63) / 64), dim3(64), 0, st, rb.nrows, H);
+  PARK_LAUNCH("select_fast", k_select_fast, dim3(CQ, H), dim3(256), 0, st, (const float*)W32,
+              (const float*)rb.delta, uoff, k_sizes, CQ, CK, P, mode, param, kcount, kv_count,
+              kv_index, rb.rows, rb.nrows, (int*)nullptr);
+  int rg = (1024 + H - 1) / H;
+  rg = rg < 1 ? 1 : (rg > CQ ? CQ : rg);
+  PARK_LAUNCH("select_refine", k_select64, dim3(rg, H), dim3(256), 0, st, (const double*)rb.W64,
+              uoff, k_sizes, CQ, CK, P, mode, param, kcount, (const int*)rb.rows,
+              (const int*)rb.nrows, kv_count, kv_index, (const int*)nullptr);
+  return PARK_OK;
 }
 
 }  // namespace park

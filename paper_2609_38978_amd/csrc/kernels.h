@@ -124,7 +124,13 @@ inline int p64_cap(int H, int CQ) { return (H * CQ + 3) / 4; }
 park_status launch_pama64(const void* Qp, const int* q_offsets, const float* cen,
                           const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                           const int4* items, int* cnt, double* part, double* W64, float* W32,
-                          const int* bandc, const int* kv_index, int* status, hipStream_t st);
+                          const int* bandc, const int* kv_index, const float* wfast,
+                          const float* dfast, int plist, int* status, hipStream_t st);
+park_status launch_qcen_retrieve(const float* qbar, const int* qsizes, const int* uoff,
+                                 const float* cen, const int* k_sizes, int H, int D, int CQ,
+                                 int CK, int mode, double param, const RetrieveBufs& rb,
+                                 float* W_out, int* kv_count, int* kv_index, int* status,
+                                 hipStream_t st);
 park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* cen,
                             const int* k_sizes, int H, int N, int D, int dtype, int CQ, int CK,
                             int mode, double param, const RetrieveBufs& rb, float* W_out,

@@ -708,8 +708,9 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
       PARK_TRY(retrieve_body(s->Qp, s->q_offsets, s->k_centroids, s->k_sizes, *dims, p->CQ,
                              p->CK, p->select, param, s->W, s->kv_count, s->kv_index, ws, st));
     } else {
-      // query-centroid estimate: one float row (the block mean) per nonempty
-      // query block, scored and selected by the float64 retrieval path
+      // query-centroid estimate: one float row (the block mean) per query
+      // block, scored in float64 (empty blocks: a zero row) and selected by
+      // the float64 selection (uoff: one row per nonempty block)
       Carver qc(ws);
       int* status = qc.take<int>(64);
       const QcenBufs qb = carve_qcen(qc, H, D, p->CQ);
@@ -717,9 +718,9 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
       PARK_TRY(launch_segment_mean(s->Qp, nullptr, s->q_offsets, H, N, D, dims->dtype, p->CQ,
                                    nullptr, qb.qbar, qb.qsizes, st));
       PARK_TRY(launch_compact_rows(qb.qbar, qb.qsizes, H, p->CQ, D, qb.qrows, qb.uoff, st));
-      PARK_TRY(launch_retrieve(qb.qrows, qb.uoff, s->k_centroids, s->k_sizes, H, p->CQ, D,
-                               PARK_F32, p->CQ, p->CK, p->select, param, rb, s->W, s->kv_count,
-                               s->kv_index, status, st));
+      PARK_TRY(launch_qcen_retrieve(qb.qbar, qb.qsizes, qb.uoff, s->k_centroids, s->k_sizes, H,
+                                    D, p->CQ, p->CK, p->select, param, rb, s->W,
+                                    s->kv_count, s->kv_index, status, st));
     }
   }
   return launch_attention(s->Qp, s->Kp, s->Vp, s->q_offsets, s->k_offsets, s->kv_count,

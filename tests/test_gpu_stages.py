@@ -548,6 +548,50 @@ def test_retrieval_float64_work_items(sizes):
     assert nb == 0 and nd == 0
 
 
+@pytest.mark.parametrize("mode,param", [("topk", 21 / 64), ("topp", 0.9)])
+def test_retrieval_float64_normaliser_leaves_out_negligible_blocks(mode, param):
+    # tight query blocks and long centroids spread each block's logits over
+    # tens of nats, so most blocks of a row weigh far below 2^-33 / (n_u CK)
+    # and the float64 pass leaves them out of its normalisers; twin blocks
+    # send every row to that pass.  The left-out mass is below 2^-33 of each
+    # normaliser, so the float64 rows still round to within one float32 ulp
+    # of the oracle
+    rng = np.random.default_rng(5)
+    d, CK = 128, 64
+    sizes = [700, 60, 240, 1, 299, 600, 50, 50, 0, 130]
+    offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N, CQ = int(offs[-1]), len(sizes)
+    mu = rng.standard_normal((CQ, d))
+    q = mu[np.repeat(np.arange(CQ), sizes)] + 0.3 * rng.standard_normal((N, d))
+    Qp = torch.from_numpy(q.astype(np.float32)).bfloat16().float().numpy()
+    c = (30.0 * rng.standard_normal((CK, d))).astype(np.float32)
+    n = rng.integers(1, 100, CK)
+    n[7] = 0  # an empty block
+    c[1::2] = c[0::2]
+    n[1::2] = n[0::2]
+    Wo = O.pama(Qp, offs, c, n)
+    nu = np.diff(offs).astype(np.float64)
+    small = (Wo * nu[:, None] * CK < 2.0 ** -34) & (n[None, :] > 0)
+    live = nu > 0
+    print(f"[{mode}] blocks below the drop threshold: {small[live].mean():.2f} of each row",
+          flush=True)
+    assert small[live].mean() > 0.3
+    sel = P.PARK_SELECT_TOPK if mode == "topk" else P.PARK_SELECT_TOPP
+    args = (PT.to_dev(Qp[None], "bf16"), torch.from_numpy(offs[None].astype(np.int32)).cuda(),
+            torch.from_numpy(c[None]).cuda(), torch.from_numpy(n[None].astype(np.int32)).cuda(),
+            CQ, CK, sel, param)
+    for want_W in (True, False):
+        kvc, kvi, W = P.park_retrieve_blocks(*args, want_W=want_W)
+        if want_W:
+            W = W.cpu().numpy()[0]
+            ref = Wo.astype(np.float32)
+            err = np.abs(W - ref)
+            assert np.all(err <= np.spacing(np.abs(ref))), err.max()
+        nd, nb = PT.compare_masks(Wo, n, nu, mode, param, kvc.cpu().numpy()[0],
+                                  kvi.cpu().numpy()[0])
+        assert nb == 0 and nd == 0, want_W
+
+
 @pytest.mark.parametrize("dtype,N,d,C", [("fp32", 256, 64, 8), ("bf16", 2048, 128, 32)])
 def test_rank_deficient_metric_clusters_like_the_square_root(dtype, N, d, C):
     # App. D: the symmetric square root realises the metric when Gbar is
