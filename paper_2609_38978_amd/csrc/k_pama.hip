@@ -872,11 +872,16 @@ __global__ __launch_bounds__(256) void k_select_band(const double* __restrict__ 
 // Fast PAMA on bf16 MFMA (bf16 queries), with a per-row error bound.
 //
 // Centroids (float) are split into three bf16 parts, c = c1 + c2 + c3 + r with
-// |r| <= 2^-24 |c|.  t = q.c is accumulated as q.c1 (a fresh accumulator per
-// 32-wide k-step, partials added on the VALU) plus q.(c2 + c3) in one chain;
-// with 2^-23 per MFMA addition and 2^-24 per VALU rounding,
-//   |t^ - t| <= et |q| |c|,  et = 2^-24 1.01 + (32 2^-23 + (KS-1) 2^-24) 1.01
-//                                + 2^-8 1.01 (2D) 2^-23 + 2^-24 1.01.
+// |r| <= 2^-24 |c|.  t = q.c is accumulated as q.(c2 + c3) in one chain over
+// all dimensions plus q.c1 in 32-dimension segments, each a fresh
+// accumulator except the last, which starts from the finished c2 + c3 chain;
+// the D/32 segment results are added on the VALU.  With 2^-23 per MFMA
+// addition and 2^-24 per VALU rounding,
+//   |t^ - t| <= et |q| |c|,  et = 2^-24 1.01 + (32 2^-23 + (D/32-1) 2^-24) 1.01
+//                                + 2^-8 1.01 (2D) 2^-23 + 2^-24 1.01
+// (residual r; the c1 segments and their sum; the c2 + c3 chain; the last
+// segment's 32 additions onto the seed, 32 2^-23 |q.(c2 + c3)| < 2^-24 |q||c|).
+// The logit adds log2(e) log n_v, precomputed in float (k_cen_prep).
 // The logit S = t/sqrt(d) + log n is formed with one FMA; its error
 //   e_i = isd (et + 1.01 2^-24) |q_i| cmax + 1.01 2^-24 (2 lgmax + 1.01 isd |q_i| cmax)
 // bounds every centroid of query i (cmax = max |c_v|, lgmax = max log n_v).
@@ -895,8 +900,9 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-// Splits the centroids into three bf16 planes and records log n_v (-inf for
-// empty blocks), |c_v| rounded up, and per-block maxima of |c_v| and |log n_v|.
+// Splits the centroids into three bf16 planes and records log2(e) log n_v
+// (-inf for empty blocks; the logits are in base 2), |c_v| rounded up, and
+// per-block maxima of |c_v| and |log n_v|.
 template <int D>
 __global__ __launch_bounds__(256) void k_cen_prep(const float* __restrict__ cen,
                                                   const int* __restrict__ k_sizes, int CK,
@@ -936,7 +942,7 @@ __global__ __launch_bounds__(256) void k_cen_prep(const float* __restrict__ cen,
       const int n = k_sizes[(size_t)h * CK + vv];
       const float l = n > 0 ? (float)log((double)n) : -INFINITY;
       cn[(size_t)h * CK + vv] = fn;
-      lg[(size_t)h * CKpad + vv] = l;
+      lg[(size_t)h * CKpad + vv] = l * 1.4426950408889634f;  // log2(e) log n, one rounding
       fl = n > 0 ? fabsf(l) : 0.0f;
     }
   }
@@ -1178,17 +1184,23 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
     return it % NS;
   };
   // products of both query groups with one tile: S^T (pass 1: lane = query,
-  // 16 centroids) or S (pass 2: lane = centroid, 16 queries); c1 part in
-  // 32-dimension segments (two MFMAs from zero) added in float, c2 + c3 in
-  // one chain over all dimensions
-  auto products = [&](const bf16x8_t (*q2)[KS], const bf16_t* B1, bool qa_left, f32x16_t* hi,
-                      f32x16_t* rest) {
+  // 16 centroids) or S (pass 2: lane = centroid, 16 queries); c2 + c3 in one
+  // chain over all dimensions, c1 in 32-dimension segments (two MFMAs from
+  // zero, the last from the finished c2 + c3 chain) added in float
+  auto products = [&](const bf16x8_t (*q2)[KS], const bf16_t* B1, bool qa_left, f32x16_t* hi) {
     const bf16_t* B2 = B1 + CT * D;
     const bf16_t* B3 = B2 + CT * D;
+    constexpr int LS = KS / 2 - 1;  // the last segment
+    auto mm = [&](const bf16x8_t& b, const bf16x8_t& q, const f32x16_t& c) {
+      return qa_left ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(q, b, c, 0, 0, 0)
+                     : __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, q, c, 0, 0, 0);
+    };
+    f32x16_t rest[2];
 #pragma unroll
     for (int g = 0; g < 2; ++g)
 #pragma unroll
       for (int q = 0; q < 16; ++q) rest[g][q] = 0.0f;
+    bf16x8_t bl[2];  // c1 fragments of the last segment
 #pragma unroll
     for (int sp = 0; sp < KS / 2; ++sp) {
       f32x16_t seg[2];
@@ -1202,21 +1214,25 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
         const bf16x8_t b1 = *(const bf16x8_t*)(B1 + co);
         const bf16x8_t b2 = *(const bf16x8_t*)(B2 + co);
         const bf16x8_t b3 = *(const bf16x8_t*)(B3 + co);
+        if (sp == LS) bl[s - 2 * sp] = b1;
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
-          if (qa_left) {
-            seg[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q2[g][s], b1, seg[g], 0, 0, 0);
-            rest[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q2[g][s], b2, rest[g], 0, 0, 0);
-            rest[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q2[g][s], b3, rest[g], 0, 0, 0);
-          } else {
-            seg[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, q2[g][s], seg[g], 0, 0, 0);
-            rest[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b2, q2[g][s], rest[g], 0, 0, 0);
-            rest[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b3, q2[g][s], rest[g], 0, 0, 0);
-          }
+          if (sp < LS) seg[g] = mm(b1, q2[g][s], seg[g]);
+          rest[g] = mm(b2, q2[g][s], rest[g]);
+          rest[g] = mm(b3, q2[g][s], rest[g]);
         }
       }
+      if (sp < LS) {
 #pragma unroll
-      for (int g = 0; g < 2; ++g) hi[g] = sp == 0 ? seg[g] : hi[g] + seg[g];
+        for (int g = 0; g < 2; ++g) hi[g] = sp == 0 ? seg[g] : hi[g] + seg[g];
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      f32x16_t seg = rest[g];
+#pragma unroll
+      for (int s = 2 * LS; s < 2 * LS + 2; ++s) seg = mm(bl[s - 2 * LS], q2[g][s], seg);
+      hi[g] = LS == 0 ? seg : hi[g] + seg;
     }
   };
   bf16x8_t qf[2][KS];
@@ -1265,8 +1281,8 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
     for (int tile = 0; tile < nt; ++tile, ++it) {
       const int slot = ring_step();
       if (!on) continue;
-      f32x16_t hi[2], rest[2];
-      products(qf, &Ct[slot][0], false, hi, rest);
+      f32x16_t hi[2];
+      products(qf, &Ct[slot][0], false, hi);
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         float sv[16];
@@ -1276,7 +1292,7 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
           const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            sv[4 * bq + r] = fmaf(hi[g][4 * bq + r] + rest[g][4 * bq + r], isdL, lv[r] * L2E);
+            sv[4 * bq + r] = fmaf(hi[g][4 * bq + r], isdL, lv[r]);
         }
         float tmax = fmaxf(sv[0], sv[1]);
 #pragma unroll
@@ -1310,10 +1326,10 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
     for (int tile = 0; tile < nt; ++tile, ++it) {
       const int slot = ring_step();
       if (!on) continue;
-      const float lgj = Lt[slot][c32] * L2E;
+      const float lgj = Lt[slot][c32];
       float ws[2];
-      f32x16_t hi[2], rest[2];
-      products(qf, &Ct[slot][0], true, hi, rest);
+      f32x16_t hi[2];
+      products(qf, &Ct[slot][0], true, hi);
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         float e[16];
@@ -1324,7 +1340,7 @@ __global__ __launch_bounds__(256, 2) void k_pama_fast(const bf16_t* __restrict__
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             e[4 * bq + r] = __builtin_amdgcn_exp2f(
-                fmaf(hi[g][4 * bq + r] + rest[g][4 * bq + r], isdL, lgj) - cv[r]);
+                fmaf(hi[g][4 * bq + r], isdL, lgj) - cv[r]);
         }
 #pragma unroll
         for (int o = 8; o > 0; o >>= 1)
@@ -1501,9 +1517,13 @@ __global__ __launch_bounds__(256, 2) void k_pama_fullk(const bf16_t* __restrict_
       const bf16_t* B1 = &Ct[slot][0];
       const bf16_t* B2 = B1 + CT * D;
       const bf16_t* B3 = B2 + CT * D;
+      // c2 + c3 in one chain, c1 in 32-dimension segments (the last one
+      // from the finished c2 + c3 chain) added in float, as the fast path
+      constexpr int LS = KS / 2 - 1;
       f32x16_t hi, rest;
 #pragma unroll
       for (int q = 0; q < 16; ++q) rest[q] = 0.0f;
+      bf16x8_t bl[2];
 #pragma unroll
       for (int sp = 0; sp < KS / 2; ++sp) {
         f32x16_t seg;
@@ -1515,11 +1535,19 @@ __global__ __launch_bounds__(256, 2) void k_pama_fullk(const bf16_t* __restrict_
           const bf16x8_t b1 = *(const bf16x8_t*)(B1 + co);
           const bf16x8_t b2 = *(const bf16x8_t*)(B2 + co);
           const bf16x8_t b3 = *(const bf16x8_t*)(B3 + co);
-          seg = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, qf[s], seg, 0, 0, 0);
+          if (sp == LS) bl[s - 2 * sp] = b1;
+          else seg = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, qf[s], seg, 0, 0, 0);
           rest = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b2, qf[s], rest, 0, 0, 0);
           rest = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b3, qf[s], rest, 0, 0, 0);
         }
-        hi = sp == 0 ? seg : hi + seg;
+        if (sp < LS) hi = sp == 0 ? seg : hi + seg;
+      }
+      {
+        f32x16_t seg = rest;
+#pragma unroll
+        for (int s = 2 * LS; s < 2 * LS + 2; ++s)
+          seg = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bl[s - 2 * LS], qf[s], seg, 0, 0, 0);
+        hi = LS == 0 ? seg : hi + seg;
       }
 #pragma unroll
       for (int bq = 0; bq < 4; ++bq) {
@@ -1527,7 +1555,7 @@ __global__ __launch_bounds__(256, 2) void k_pama_fullk(const bf16_t* __restrict_
         const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          L[tile][4 * bq + r] = fmaf(hi[4 * bq + r] + rest[4 * bq + r], isdL, lv[r] * L2E);
+          L[tile][4 * bq + r] = fmaf(hi[4 * bq + r], isdL, lv[r]);
       }
       {
         float tmax = fmaxf(L[tile][0], L[tile][1]);

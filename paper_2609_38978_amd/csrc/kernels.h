@@ -98,7 +98,7 @@ struct RetrieveBufs {
   int* rows;      // [H][CQ]     rows left for the float64 path
   int* nrows;     // [H]
   bf16_t* c3;     // [3][H][CK][D] centroids as three bf16 parts
-  float* lg;      // [H][pama_ckpad(CK)] log n_v (-inf for empty and padding blocks)
+  float* lg;      // [H][pama_ckpad(CK)] log2(e) log n_v (-inf: empty and padding blocks)
   float* cn;      // [H][CK]     |c_v|
   float* bmax;    // [H][ceil(CK/16)][2] per-block max |c_v|, |log n_v|
   int4* qitems;   // [H][pama_icap] fast-retrieval work list (chunks of 32 queries)
