@@ -1630,7 +1630,7 @@ __global__ __launch_bounds__(256, 2) void k_pama_fullk(const bf16_t* __restrict_
 
 // Rows of the fast retrieval: W^ = chunk 0 + chunk 1 + ... in chunk order,
 // empty blocks a zero row; the bound becomes delta_u = (max over chunks +
-// (17 + 2 chunks) 2^-24) 1.01.  Grid-stride over the rows of all heads.
+// (17 + 2 chunks) 2^-24) 1.01.  One workgroup per (query block, head).
 __global__ __launch_bounds__(256) void k_pama_combine(const int* __restrict__ q_offsets,
                                                       const int* __restrict__ pstart, int H,
                                                       int N, int CQ, int CK,
@@ -1638,28 +1638,40 @@ __global__ __launch_bounds__(256) void k_pama_combine(const int* __restrict__ q_
                                                       float* __restrict__ W32,
                                                       float* __restrict__ delta) {
   constexpr float U24 = 5.9604645e-08f;
-  for (int row = blockIdx.x; row < H * CQ; row += gridDim.x) {
-    const int h = row / CQ, u = row - h * CQ;
-    const int* off = q_offsets + (size_t)h * (CQ + 1);
-    const int a = min(max(off[u], 0), N), b = min(max(off[u + 1], a), N);
-    const int nch = (b - a + 31) >> 5;
-    float* wr = W32 + (size_t)row * CK;
-    if (nch == 0) {
-      for (int v = threadIdx.x; v < CK; v += 256) wr[v] = 0.0f;
-      if (threadIdx.x == 0) delta[row] = 0.0f;
-      continue;
+  constexpr int E = MAXC / 256;  // columns per thread, loads issued together
+  const int h = blockIdx.y, u = blockIdx.x, row = h * CQ + u;
+  const int* off = q_offsets + (size_t)h * (CQ + 1);
+  const int a = min(max(off[u], 0), N), b = min(max(off[u + 1], a), N);
+  const int nch = (b - a + 31) >> 5;
+  float* wr = W32 + (size_t)row * CK;
+  if (nch == 0) {
+    for (int v = threadIdx.x; v < CK; v += 256) wr[v] = 0.0f;
+    if (threadIdx.x == 0) delta[row] = 0.0f;
+    return;
+  }
+  if (threadIdx.x == 0) delta[row] = (delta[row] + (17.0f + 2.0f * nch) * U24) * 1.01f;
+  if (nch == 1) return;
+  const int s0 = pstart[(size_t)h * (CQ + 1) + u];  // part row of chunk 1
+  float acc[E];
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int v = threadIdx.x + 256 * k;
+    acc[k] = v < CK ? wr[v] : 0.0f;
+  }
+  for (int r = 1; r < nch; ++r) {
+    const int sl = s0 + r - 1;
+    if (sl >= pcap) break;
+    const float* pr = part + ((size_t)h * pcap + sl) * CK;
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      const int v = threadIdx.x + 256 * k;
+      if (v < CK) acc[k] = acc[k] + pr[v];
     }
-    if (threadIdx.x == 0) delta[row] = (delta[row] + (17.0f + 2.0f * nch) * U24) * 1.01f;
-    if (nch == 1) continue;
-    const int s0 = pstart[(size_t)h * (CQ + 1) + u];  // part row of chunk 1
-    for (int v = threadIdx.x; v < CK; v += 256) {
-      float acc = wr[v];
-      for (int r = 1; r < nch; ++r) {
-        const int sl = s0 + r - 1;
-        if (sl < pcap) acc = acc + part[((size_t)h * pcap + sl) * CK + v];
-      }
-      wr[v] = acc;
-    }
+  }
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int v = threadIdx.x + 256 * k;
+    if (v < CK) wr[v] = acc[k];
   }
 }
 
@@ -2118,7 +2130,7 @@ park_status launch_retrieve(const void* Qp, const int* q_offsets, const float* c
                 (const bf16_t*)rb.c3, plane,
                 (const float*)rb.lg, CKpad, (const float*)rb.bmax, nbm, H, N, CQ, CK, W32, rb.delta);
   }
-  PARK_LAUNCH("pama_combine", k_pama_combine, dim3(1024), dim3(256), 0, st, q_offsets,
+  PARK_LAUNCH("pama_combine", k_pama_combine, dim3(CQ, H), dim3(256), 0, st, q_offsets,
               (const int*)rb.qstart, H, N, CQ, CK, (const float*)part, pcap, W32, rb.delta);
   PARK_LAUNCH("pama_reset", k_zero_counts, dim3((H + 63) / 64), dim3(64), 0, st, rb.nrows, H);
   // top-k rows the bound cannot settle are settled by their band of
