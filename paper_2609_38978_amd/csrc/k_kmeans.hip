@@ -383,7 +383,8 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
   constexpr float KXC = 1.1f * (2.0f * ET + 2.01f * U24) * 1.0001f;
   constexpr int NS = PARK_KM_NS;  // LDS ring slots: NS - 1 tiles in flight
   __shared__ __attribute__((aligned(16))) bf16_t Wt[NS][NP * CT * D];  // [slot][part][row][D]
-  __shared__ __attribute__((aligned(16))) float Bt[NS][CT];
+  // b values by tile (tile % (NS + 1)): a tile's stay until its deferred ranking
+  __shared__ __attribute__((aligned(16))) float Bt[NS + 1][CT];
   __shared__ float mx_s[2];
   __shared__ int wcnt[4];
   const int h = blockIdx.y, tid = threadIdx.x, l = tid & 63, hf = l >> 5, c32 = l & 31;
@@ -405,7 +406,7 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
       const bf16_t* src = P1 + part * plane + (size_t)v * D + 8 * (pch ^ km_swz<D>(r));
       km_dma16(src, km_lds_addr(&Wt[slot][0] + (w * NI + i) * 512));
     }
-    if (w == 0 && l < CT / 4) km_dma16(bh + c0 + 4 * l, km_lds_addr(&Bt[slot][0]));
+    if (w == 0 && l < CT / 4) km_dma16(bh + c0 + 4 * l, km_lds_addr(&Bt[tile % (NS + 1)][0]));
   };
   // the first tiles travel while the points are loaded
 #pragma unroll
@@ -470,7 +471,9 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
 
   const int swk = km_swz<D>(c32);
   const int rowo = c32 * D;
-  for (int t = 0; t < ntiles; ++t) {
+  // tile t: its DMAs done, barrier, the next tile's DMAs issued; its scores
+  // (-2 x.w without b) into a
+  auto scores = [&](int t, f32x16_t (&a)[TB]) {
     // own DMAs of tile t done (wavefront 0 also fetches the b tile)
     if (NS > 2 && t + 1 < ntiles) {
       if (w == 0) km_wait_vmcnt<NI + 1>();
@@ -486,11 +489,10 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
     const bf16_t* W3 = W2 + CT * D;  // third part (NP == 3)
     // the small parts first, then the leading part on top of them (one
     // accumulator, no separate addition of the two sums)
-    f32x16_t acc[TB];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) acc[tb][q] = 0.0f;
+      for (int q = 0; q < 16; ++q) a[tb][q] = 0.0f;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int co = rowo + 8 * ((2 * s + hf) ^ swk);
@@ -499,9 +501,9 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
       if constexpr (NP == 3) a3 = *(const bf16x8_t*)(W3 + co);
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
-        acc[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, xf[tb][s], acc[tb], 0, 0, 0);
+        a[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, xf[tb][s], a[tb], 0, 0, 0);
         if constexpr (NP == 3)
-          acc[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, xf[tb][s], acc[tb], 0, 0, 0);
+          a[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, xf[tb][s], a[tb], 0, 0, 0);
       }
     }
 #pragma unroll
@@ -510,28 +512,55 @@ __global__ __launch_bounds__(256, 2) void k_assign_fast(const bf16_t* __restrict
       const bf16x8_t a1 = *(const bf16x8_t*)(W1 + co);
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb)
-        acc[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xf[tb][s], acc[tb], 0, 0, 0);
+        a[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, xf[tb][s], a[tb], 0, 0, 0);
     }
-    float bv[16];
+  };
+  // ranking of tile t's scores, tiles in order
+  auto rank = [&](const f32x16_t (&a)[TB], int t) {
+    float bvt[16];
 #pragma unroll
     for (int bq = 0; bq < 4; ++bq) {
-      const float4 b4 = *(const float4*)(&Bt[slot][8 * bq + 4 * hf]);
-      bv[4 * bq] = b4.x;
-      bv[4 * bq + 1] = b4.y;
-      bv[4 * bq + 2] = b4.z;
-      bv[4 * bq + 3] = b4.w;
+      const float4 b4 = *(const float4*)(&Bt[t % (NS + 1)][8 * bq + 4 * hf]);
+      bvt[4 * bq] = b4.x;
+      bvt[4 * bq + 1] = b4.y;
+      bvt[4 * bq + 2] = b4.z;
+      bvt[4 * bq + 3] = b4.w;
     }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        const float sc = fmaf(-2.0f, acc[tb][q], bv[q]);
+        const float sc = fmaf(-2.0f, a[tb][q], bvt[q]);
         const bool nb = sc < best[tb];
         L[tb] = __builtin_amdgcn_fmed3f(best[tb], L[tb], sc);
         best[tb] = fminf(best[tb], sc);
         brel[tb] = nb ? 8 * (q >> 2) + (q & 3) : brel[tb];
       }
       brel[tb] -= CT;  // relative to the next tile
+      // done before the next step's wait (not sunk past it, where its
+      // scores would have to outlive the next tile's)
+      asm volatile("" ::"v"(best[tb]), "v"(L[tb]), "v"(brel[tb]));
+    }
+  };
+  // software pipeline: the MFMAs of tile t and the ranking of tile t-1 in
+  // the same step (two score sets, alternating), so that the VALU ranking
+  // runs while the matrix unit works
+  f32x16_t A0[TB], A1[TB];
+  if (ntiles > 0) {
+    scores(0, A0);
+    int t = 1;
+    for (; t + 1 < ntiles; t += 2) {
+      scores(t, A1);
+      rank(A0, t - 1);
+      scores(t + 1, A0);
+      rank(A1, t);
+    }
+    if (t < ntiles) {
+      scores(t, A1);
+      rank(A0, t - 1);
+      rank(A1, t);
+    } else {
+      rank(A0, t - 1);
     }
   }
 #pragma unroll
