@@ -21,6 +21,7 @@
 //   k_xnorm        x^T Gbar x per token, plus a bound of its error
 //   k_radius       R_a^2 per cluster (float64 from the bounds above)
 //   k_cand         the bit matrix of S_a on bf16 MFMA over split operands
+//   k_tile_union   per tile of sorted tokens, the union of its clusters' S_a
 //   k_assign_cand  the certified bf16-MFMA assignment of each tile of sorted
 //                  tokens against the union of its clusters' candidate sets
 //   k_refine_union float64 labels of the tokens it cannot certify, against
@@ -46,19 +47,6 @@ __device__ __forceinline__ int kf_swz(int r) { return D == 128 ? (r & 15) : ((r 
 template <int N>
 __device__ __forceinline__ void kf_wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// OR of the candidate rows of clusters alo..ahi into uw[64] (LDS, cleared
-// before): word-parallel, each of the 256 threads ORs one word of every
-// fourth row in registers (independent loads), then one LDS atomic.  Rows
-// of empty clusters are all zero.
-__device__ __forceinline__ void kf_union_rows(const uint32_t* __restrict__ ch, int alo, int ahi,
-                                              int nwd, uint32_t* uw, int tid) {
-  const int word = tid & 63, ph = tid >> 6;
-  uint32_t x = 0u;
-  if (word < nwd)
-    for (int a = alo + ph; a <= ahi; a += 4) x |= ch[(size_t)a * 64 + word];
-  if (x) atomicOr(&uw[word], x);
 }
 
 // ------------------------------------------------------------ Gbar split
@@ -429,6 +417,40 @@ __global__ __launch_bounds__(256, 2) void k_cand(const bf16_t* __restrict__ m2, 
   }
 }
 
+// ------------------------------------------------------------ tile unions
+// The union of the candidate sets of the clusters a tile of kmeans_tile
+// sorted positions spans (from the cluster of its first position to that of
+// its last, previous labels): 64 bit words and the first cluster per tile,
+// built once per round so that the assignment starts from one load.  One
+// wavefront per tile (lane = bit word).
+__global__ __launch_bounds__(256) void k_tile_union(const int* __restrict__ perm,
+                                                    const int* __restrict__ labels,
+                                                    const uint32_t* __restrict__ cand, int H,
+                                                    int N, int C, int NT,
+                                                    uint32_t* __restrict__ tun,
+                                                    int* __restrict__ talo) {
+  const int wv = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6), l = threadIdx.x & 63;
+  if (wv >= H * NT) return;
+  const int h = wv / NT, t = wv - h * NT;
+  const int p0 = t * kmeans_tile, pend = min(N, p0 + kmeans_tile);
+  const int* ph = perm + (size_t)h * N;
+  const int* zh = labels + (size_t)h * N;
+  int z = l == 0 ? 0 : C - 1;
+  if (l < 2) {
+    const int tk = ph[l == 0 ? p0 : pend - 1];
+    if ((unsigned)tk < (unsigned)N) z = zh[tk];
+  }
+  const int alo = min(max(__shfl(z, 0, 64), 0), C - 1);
+  const int ahi = min(max(__shfl(z, 1, 64), alo), C - 1);
+  uint32_t x = 0u;
+  if (l < (C + 31) / 32) {
+    const uint32_t* ch = cand + (size_t)h * C * 64 + l;
+    for (int a = alo; a <= ahi; ++a) x |= ch[(size_t)a * 64];
+  }
+  tun[(size_t)wv * 64 + l] = x;
+  if (l == 0) talo[wv] = alo;
+}
+
 // ------------------------------------------------------------ filtered assignment
 // As k_assign_fast (same split, scores, bookkeeping, certification and listing
 // of uncertified tokens), but the workgroup takes kmeans_tile consecutive
@@ -454,8 +476,8 @@ __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ w3, size_t plane,
     const float* __restrict__ b32, int Cpad, const float* __restrict__ wn,
     const float* __restrict__ eb, const float* __restrict__ bmax, int nbm, int N, int C,
-    const int* __restrict__ perm, const uint32_t* __restrict__ cand,
-    int* __restrict__ labels, int* __restrict__ flags,
+    const int* __restrict__ perm, const uint32_t* __restrict__ tun,
+    const int* __restrict__ talo, int* __restrict__ labels, int* __restrict__ flags,
     float* __restrict__ flagu, int* __restrict__ nflag, const double* __restrict__ xn,
     unsigned long long* __restrict__ dmax) {
   constexpr int TB = PARK_KM_TB, CT = 32, KS = D / 16, CPR = D / 8, RPI = 64 / CPR;
@@ -483,22 +505,16 @@ __global__ __launch_bounds__(256, NP == 2 ? PARK_KM_CAND_OCC : 2) void k_assign_
   const int pend = min(N, p0 + kmeans_tile);
   const int* ph = perm + (size_t)h * N;
   const int* zh = labels + (size_t)h * N;
-  // clusters of the first and last position (previous labels, read before
-  // this workgroup writes any label; other workgroups own other tokens)
-  if (tid == 0) {
-    const int ta = ph[p0], tb = ph[pend - 1];
-    seg[0] = (unsigned)ta < (unsigned)N ? zh[ta] : 0;
-    seg[1] = (unsigned)tb < (unsigned)N ? zh[tb] : C - 1;
-  }
+  // the union of the candidate sets of the clusters this tile spans, and its
+  // first cluster (k_tile_union, from the previous labels)
+  const size_t ti = (size_t)h * gridDim.x + blockIdx.x;
   if (tid < 64) {
-    uw[tid] = 0u;
+    uw[tid] = tun[ti * 64 + tid];
     dm_s[tid] = 0ull;
   }
+  if (tid == 0) seg[0] = talo[ti];
   __syncthreads();
-  const int alo = min(max(seg[0], 0), C - 1), ahi = min(max(seg[1], alo), C - 1);
-  const int nwd = (C + 31) / 32;
-  kf_union_rows(cand + (size_t)h * C * 64, alo, ahi, nwd, uw, tid);
-  __syncthreads();
+  const int alo = min(max(seg[0], 0), C - 1);
   if (tid < 64) {
     const uint32_t x = tid * 32 < C ? uw[tid] : 0u;
     int inc = __popc(x);
@@ -1118,17 +1134,20 @@ park_status launch_kfilter_round(const bf16_t* X, int H, int N, int D, int C,
     PARK_LAUNCH("kfilter_cand", k_cand<128>, gc, dim3(256), 0, st, (const bf16_t*)kf.m2, plane,
                 (const bf16_t*)kb.w3, plane, (const float*)kf.mn, (const float*)kb.wn, Cpad,
                 (const double*)kb.b, (const double*)kf.r2, C, kf.cand);
+    PARK_LAUNCH("kfilter_union", k_tile_union, dim3((H * NT + 3) / 4), dim3(256), 0, st,
+                (const int*)kb.perm, (const int*)kb.labels, (const uint32_t*)kf.cand, H, N, C, NT,
+                kf.tun, kf.talo);
     if (C >= 512 && PARK_KM_CAND_NP == 2)
       PARK_LAUNCH("kmeans_assign_cand", (k_assign_cand<128, 2>), ga, dim3(256), 0, st, X,
                   (const bf16_t*)kb.w3, plane, (const float*)kb.b32, Cpad, (const float*)kb.wn,
                   (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C, (const int*)kb.perm,
-                  (const uint32_t*)kf.cand, kb.labels, kb.flags, kb.flagu,
+                  (const uint32_t*)kf.tun, (const int*)kf.talo, kb.labels, kb.flags, kb.flagu,
                   kb.nflag, (const double*)kf.xn, kf.dmax);
     else
       PARK_LAUNCH("kmeans_assign_cand", (k_assign_cand<128, 3>), ga, dim3(256), 0, st, X,
                   (const bf16_t*)kb.w3, plane, (const float*)kb.b32, Cpad, (const float*)kb.wn,
                   (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C, (const int*)kb.perm,
-                  (const uint32_t*)kf.cand, kb.labels, kb.flags, kb.flagu,
+                  (const uint32_t*)kf.tun, (const int*)kf.talo, kb.labels, kb.flags, kb.flagu,
                   kb.nflag, (const double*)kf.xn, kf.dmax);
     PARK_LAUNCH("kmeans_refine_union", k_refine_union<128>, gu, dim3(64), 0, st, X,
                 (const bf16_t*)kb.w3, plane, (const float*)kb.b32, (const float*)kb.wn,
@@ -1144,17 +1163,20 @@ park_status launch_kfilter_round(const bf16_t* X, int H, int N, int D, int C,
     PARK_LAUNCH("kfilter_cand", k_cand<64>, gc, dim3(256), 0, st, (const bf16_t*)kf.m2, plane,
                 (const bf16_t*)kb.w3, plane, (const float*)kf.mn, (const float*)kb.wn, Cpad,
                 (const double*)kb.b, (const double*)kf.r2, C, kf.cand);
+    PARK_LAUNCH("kfilter_union", k_tile_union, dim3((H * NT + 3) / 4), dim3(256), 0, st,
+                (const int*)kb.perm, (const int*)kb.labels, (const uint32_t*)kf.cand, H, N, C, NT,
+                kf.tun, kf.talo);
     if (C >= 512 && PARK_KM_CAND_NP == 2)
       PARK_LAUNCH("kmeans_assign_cand", (k_assign_cand<64, 2>), ga, dim3(256), 0, st, X,
                   (const bf16_t*)kb.w3, plane, (const float*)kb.b32, Cpad, (const float*)kb.wn,
                   (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C, (const int*)kb.perm,
-                  (const uint32_t*)kf.cand, kb.labels, kb.flags, kb.flagu,
+                  (const uint32_t*)kf.tun, (const int*)kf.talo, kb.labels, kb.flags, kb.flagu,
                   kb.nflag, (const double*)kf.xn, kf.dmax);
     else
       PARK_LAUNCH("kmeans_assign_cand", (k_assign_cand<64, 3>), ga, dim3(256), 0, st, X,
                   (const bf16_t*)kb.w3, plane, (const float*)kb.b32, Cpad, (const float*)kb.wn,
                   (const float*)kb.eb, (const float*)kb.hmax, nbm, N, C, (const int*)kb.perm,
-                  (const uint32_t*)kf.cand, kb.labels, kb.flags, kb.flagu,
+                  (const uint32_t*)kf.tun, (const int*)kf.talo, kb.labels, kb.flags, kb.flagu,
                   kb.nflag, (const double*)kf.xn, kf.dmax);
     PARK_LAUNCH("kmeans_refine_union", k_refine_union<64>, gu, dim3(64), 0, st, X,
                 (const bf16_t*)kb.w3, plane, (const float*)kb.b32, (const float*)kb.wn,

@@ -58,6 +58,11 @@ struct KfilterBufs {
   // upper bound of D(x, mu_a)^2 over the tokens an assignment gave label a
   // (the radius of the next round, before the centroid's move)
   unsigned long long* dmax;
+  // per tile of kmeans_tile sorted positions: the union of the candidate
+  // sets of the clusters it spans ([H][tiles][64] bit words) and its first
+  // cluster ([H][tiles])
+  uint32_t* tun;
+  int* talo;
 };
 
 struct KmeansBufs {

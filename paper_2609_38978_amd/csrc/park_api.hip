@@ -165,6 +165,8 @@ static ClusterWs carve_cluster(Carver& cv, int H, int N, int D, int C) {
   c.kf.m2 = cv.take<bf16_t>((size_t)2 * H * C * D);
   c.kf.mn = cv.take<float>((size_t)H * C);
   c.kf.dmax = cv.take<unsigned long long>((size_t)H * C);
+  c.kf.tun = cv.take<uint32_t>((size_t)H * ((N + kmeans_tile - 1) / kmeans_tile) * 64);
+  c.kf.talo = cv.take<int>((size_t)H * ((N + kmeans_tile - 1) / kmeans_tile));
   return c;
 }
 

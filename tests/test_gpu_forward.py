@@ -109,6 +109,9 @@ VARIANTS = {
     "fixed_tiny": ("tiny", None, None, None, "pama", "fixed", "qrkc"),
     "fixed_ragged_topp": ("medium", (3, 11, 13), [0, 1], ("topp", 0.9), "pama", "fixed", "qrkc"),
     "fixed_qcentroid_hunyuan": ("hunyuan", (2, 9, 16), [0], None, "qcentroid", "fixed", "qrkc"),
+    # 150 query blocks: two full 64-block tiles of the query-centroid kernel and a ragged 22
+    "qcentroid_ragged_150": ("medium", (3, 20, 160), [3], ("topk", 0.2), "qcentroid", "cluster",
+                             "qrkc"),
     "euclid_keys_medium": ("medium", (2, 16, 32), [1, 2], None, "pama", "cluster", "euclid"),
 }
 
