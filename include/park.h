@@ -220,7 +220,10 @@ park_status park_block_centroids(const void* X, const int32_t* perm, const int32
  *   kv_count   [H][CQ] int32;  kv_index [H][CQ][CK] int32, the first
  *              kv_count entries of each row hold the selected ids ascending.
  * The mask equals the one obtained from float64 W^ (rows whose fast-path
- * margin is below its error bound are recomputed in float64). */
+ * margin is below its error bound are recomputed in float64; that pass
+ * leaves out of each query's normaliser the blocks whose certified bound
+ * keeps them below 2^-33 of it, so a recomputed W^ is within 2^-32 relative
+ * of its float64 value before the rounding to float). */
 park_status park_retrieve_blocks(const void* Qp, const int32_t* q_offsets, const float* centroids,
                                  const int32_t* k_sizes, const park_dims* dims, int32_t CQ,
                                  int32_t CK, int32_t select, double param, float* W_out,
