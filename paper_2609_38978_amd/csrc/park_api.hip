@@ -306,7 +306,8 @@ static park_status static_scratch(void** out) {
 
 // ------------------------------------------------------------ side stream
 // The query side's clustering runs on a second stream of the device, beside
-// the key side's metric Gbar and k-means on the caller's stream: the two
+// the key side's metric Gbar and k-means on the caller's stream, and later
+// the key and value gathers run there beside the retrieval: the two streams
 // share nothing but the status word, which kernels only OR into.  The stream
 // (default priority) and its fork/join events are created on the first call
 // that is not being captured; until then the sides run one after the other.
@@ -429,6 +430,32 @@ static park_status retrieve_body(const void* Qp, const int* q_offsets, const flo
 using namespace park;
 
 // ============================================================ C ABI
+// The retrieval of park_forward: key centroids (through the permutation),
+// then PAMA or the query-centroid estimate and the mask, on `st`.
+static park_status retrieve_stage(const void* K, const park_params* p, const park_state* s,
+                                  const park_dims* dims, double param, void* ws, hipStream_t st) {
+  const int H = dims->H, N = dims->N, D = dims->d;
+  PARK_TRY(launch_segment_mean(K, s->k_perm, s->k_offsets, H, N, D, dims->dtype, p->CK, nullptr,
+                               s->k_centroids, s->k_sizes, st));
+  if (p->estimator == PARK_EST_PAMA)
+    return retrieve_body(s->Qp, s->q_offsets, s->k_centroids, s->k_sizes, *dims, p->CQ, p->CK,
+                         p->select, param, s->W, s->kv_count, s->kv_index, ws, st);
+  // query-centroid estimate: one float row (the block mean) per query block,
+  // scored in float64 (empty blocks: a zero row) and selected by the
+  // certified float selection, the rows it cannot settle by the float64 one
+  // (uoff: one row per nonempty block)
+  Carver qc(ws);
+  int* status = qc.take<int>(64);
+  const QcenBufs qb = carve_qcen(qc, H, D, p->CQ);
+  const RetrieveBufs rb = carve_retrieve(qc, H, p->CQ, D, p->CQ, p->CK);
+  PARK_TRY(launch_segment_mean(s->Qp, nullptr, s->q_offsets, H, N, D, dims->dtype, p->CQ,
+                               nullptr, qb.qbar, qb.qsizes, st));
+  PARK_TRY(launch_compact_rows(qb.qbar, qb.qsizes, H, p->CQ, D, qb.qrows, qb.uoff, st));
+  return launch_qcen_retrieve(qb.qbar, qb.qsizes, qb.uoff, s->k_centroids, s->k_sizes, H, D,
+                              p->CQ, p->CK, p->select, param, rb, s->W, s->kv_count, s->kv_index,
+                              status, st);
+}
+
 extern "C" {
 
 const char* park_status_string(park_status s) {
@@ -701,34 +728,39 @@ park_status park_forward(const void* Q, const void* K, const void* V, const park
     }
   }
   PARK_TRY(launch_gather(Q, s->q_perm, H, N, D, dims->dtype, s->Qp, st));
-  PARK_TRY(launch_gather(K, s->k_perm, H, N, D, dims->dtype, s->Kp, st));
-  PARK_TRY(launch_gather(V, s->k_perm, H, N, D, dims->dtype, s->Vp, st));
-  if (reuse != PARK_REUSE_CLUSTERS_AND_MASK) {
-    PARK_TRY(launch_segment_mean(s->Kp, nullptr, s->k_offsets, H, N, D, dims->dtype, p->CK,
-                                 nullptr, s->k_centroids, s->k_sizes, st));
-    if (p->estimator == PARK_EST_PAMA) {
-      PARK_TRY(retrieve_body(s->Qp, s->q_offsets, s->k_centroids, s->k_sizes, *dims, p->CQ,
-                             p->CK, p->select, param, s->W, s->kv_count, s->kv_index, ws, st));
-    } else {
-      // query-centroid estimate: one float row (the block mean) per query
-      // block, scored in float64 (empty blocks: a zero row) and selected by
-      // the float64 selection (uoff: one row per nonempty block)
-      Carver qc(ws);
-      int* status = qc.take<int>(64);
-      const QcenBufs qb = carve_qcen(qc, H, D, p->CQ);
-      const RetrieveBufs rb = carve_retrieve(qc, H, p->CQ, D, p->CQ, p->CK);
-      PARK_TRY(launch_segment_mean(s->Qp, nullptr, s->q_offsets, H, N, D, dims->dtype, p->CQ,
-                                   nullptr, qb.qbar, qb.qsizes, st));
-      PARK_TRY(launch_compact_rows(qb.qbar, qb.qsizes, H, p->CQ, D, qb.qrows, qb.uoff, st));
-      PARK_TRY(launch_qcen_retrieve(qb.qbar, qb.qsizes, qb.uoff, s->k_centroids, s->k_sizes, H,
-                                    D, p->CQ, p->CK, p->select, param, rb, s->W,
-                                    s->kv_count, s->kv_index, status, st));
-    }
+  // with a retrieval to run, the keys and values are gathered on the side
+  // stream meanwhile (the retrieval reads the key centroids, which are taken
+  // through the permutation: the same rows in the same order), joined before
+  // the attention
+  const bool retrieve = reuse != PARK_REUSE_CLUSTERS_AND_MASK;
+  SideStream* kv_side = retrieve ? side_stream(st) : nullptr;
+  hipStream_t skv = kv_side ? kv_side->s : st;
+  std::unique_lock<std::mutex> kv_lk;
+  if (kv_side) {
+    kv_lk = std::unique_lock<std::mutex>(kv_side->mu);
+    PARK_TRY(ev_record(kv_side->fork, st));
+    PARK_TRY(ev_wait(skv, kv_side->fork));
   }
+  park_status rkv = launch_gather(K, s->k_perm, H, N, D, dims->dtype, s->Kp, skv);
+  if (rkv == PARK_OK) rkv = launch_gather(V, s->k_perm, H, N, D, dims->dtype, s->Vp, skv);
+  if (kv_side) {  // joined also after an error
+    const park_status rj = ev_record(kv_side->join, skv);
+    if (rkv == PARK_OK) rkv = rj;
+  }
+  park_status rr = rkv == PARK_OK && retrieve
+                       ? retrieve_stage(K, p, s, dims, param, ws, st)
+                       : PARK_OK;
+  if (kv_side) {
+    const park_status rw = ev_wait(st, kv_side->join);
+    if (rr == PARK_OK) rr = rw;
+  }
+  PARK_TRY(rkv);
+  PARK_TRY(rr);
   return launch_attention(s->Qp, s->Kp, s->Vp, s->q_offsets, s->k_offsets, s->kv_count,
                           s->kv_index, s->q_perm, H, N, D, dims->dtype, p->CQ, p->CK, O,
                           p->out_dtype, nullptr, carve_attn_plan(ws, H, N, p->CQ), st);
 }
+
 
 park_status park_schedule_step(int32_t step, const int32_t* steps, int32_t n_steps,
                                int32_t* reuse_out) {
