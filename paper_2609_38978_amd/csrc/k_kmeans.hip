@@ -166,10 +166,16 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
     const double* G = Gbar + (size_t)h * D * D;
 #pragma unroll
     for (int k = 0; k < PER; ++k) acc[k] = 0.0;
-    for (int c = 0; c < D; ++c) {
-      const double g = G[(size_t)c * D + a];
+    // sixteen metric rows' loads issued together, then their products (the
+    // same fma order over the columns)
+    for (int c0 = 0; c0 < D; c0 += 16) {
+      double g[16];
 #pragma unroll
-      for (int k = 0; k < PER; ++k) acc[k] = fma(g, ms[grp + NG * k][c], acc[k]);
+      for (int j = 0; j < 16; ++j) g[j] = G[(size_t)(c0 + j) * D + a];
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+#pragma unroll
+        for (int k = 0; k < PER; ++k) acc[k] = fma(g[j], ms[grp + NG * k][c0 + j], acc[k]);
     }
   } else {
 #pragma unroll
@@ -208,15 +214,18 @@ __global__ __launch_bounds__(NT) void k_prep(const double* __restrict__ mu,
     const int r = tid / LPC, sub = tid % LPC;
     double s = 0.0, n2 = 0.0, m2s = 0.0, dso = 0.0, dsa = 0.0;
     const double* wold = w + ((size_t)h * C + min(v0 + r, C - 1)) * D;
+    double wo[D / LPC];  // the old w of this lane's columns, loaded together
 #pragma unroll
-    for (int c = sub; c < D; c += LPC) {
+    for (int j = 0; j < D / LPC; ++j) wo[j] = rmode == 2 ? wold[sub + LPC * j] : 0.0;
+#pragma unroll
+    for (int j = 0; j < D / LPC; ++j) {
+      const int c = sub + LPC * j;
       s = fma(ms[r][c], ws[r][c], s);
       n2 = fma(ws[r][c], ws[r][c], n2);
       m2s = fma(ms[r][c], ms[r][c], m2s);
       if (rmode == 2) {
-        const double wo = wold[c];
-        dso = fma(ms[r][c], wo, dso);
-        dsa += fabs(ms[r][c] * wo);
+        dso = fma(ms[r][c], wo[j], dso);
+        dsa += fabs(ms[r][c] * wo[j]);
       }
     }
 #pragma unroll

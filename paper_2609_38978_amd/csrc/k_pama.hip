@@ -189,12 +189,17 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
     int Lc = nt + nt2;  // steps per chunk of 64 queries
     auto issue = [&](int step, int slot) {
       const int j = step % Lc, pass = j >= nt ? 1 : 0, tile = pass ? j - nt : j;
+      // the step's columns first (list reads go out together), then the DMAs
+      int vs[NI];
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int c = column(pass, tile, (w * NI + i) * RPI + l / CPR);
+        vs[i] = c >= 0 ? c : CK - 1;
+      }
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int r = (w * NI + i) * RPI + l / CPR;
-        const int c = column(pass, tile, r);
-        const int v = c >= 0 ? c : CK - 1;
-        const float* src = ch + (size_t)v * D + 4 * (pch ^ (r & (CPR - 1)));
+        const float* src = ch + (size_t)vs[i] * D + 4 * (pch ^ (r & (CPR - 1)));
         p64_dma16(src, p64_lds_addr(&Ct[slot][0] + (w * NI + i) * 256));
       }
       if (tid < CT) {
@@ -221,12 +226,20 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
       const double dl = (double)dfast[rid];
       const double thr = P64_DROP / ((double)nu * (double)CK);
       int fl = 0, c = 0;
+      int ns[8];
+      float ws8[8];  // loads first (clamped ids), so that they go out together
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int e = min(8 * tid + k, CK - 1);
+        ns[k] = nh[e];
+        ws8[k] = wr[e];
+      }
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int e = 8 * tid + k;
         // NaN / infinite bounds keep the block
-        const bool kp = e < CK && nh[e] > 0 &&
-                        !((double)wr[e] * (1.0 + dl) + 4.0 * 1.1754943508222875e-38 < thr);
+        const bool kp = e < CK && ns[k] > 0 &&
+                        !((double)ws8[k] * (1.0 + dl) + 4.0 * 1.1754943508222875e-38 < thr);
         fl |= (int)kp << k;
         c += kp;
       }
@@ -256,11 +269,14 @@ __global__ __launch_bounds__(256, W2 ? 2 : 1) void k_pama64(const T* __restrict_
       const int j = it % Lc, pass = j >= nt ? 1 : 0, tile = pass ? j - nt : j;
       const int r0 = q0 + 64 * (cb + it / Lc);
       if (tile == 0 && pass == 0) {
-        // A operand: query r0 + 16w + c16, dimensions 4s + g
+        // A operand: query r0 + 16w + c16, dimensions 4s + g (loads from a
+        // clamped row, so that they go out together; rows past the block 0)
         const int qi = r0 + 16 * w + c16;
+        const T* qrow = Qh + (size_t)min(qi, q1 - 1) * D + g;
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-          qa[s] = qi < q1 ? to_f(Qh[(size_t)qi * D + 4 * s + g]) : 0.0f;
+        for (int s = 0; s < KS; ++s) qa[s] = to_f(qrow[4 * s]);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) qa[s] = qi < q1 ? qa[s] : 0.0f;
 #pragma unroll
         for (int s = 0; s < KS; ++s) asm volatile("" ::"v"(qa[s]));
 #pragma unroll
@@ -434,7 +450,9 @@ __global__ __launch_bounds__(256, 2) void k_qcen64(const float* __restrict__ qba
     const bool ok = ua < CQ && qs[min(ua, CQ - 1)] > 0;
     const float* qr = qbar + ((size_t)h * CQ + min(ua, CQ - 1)) * D;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) qa[s] = ok ? qr[4 * s + g] : 0.0f;
+    for (int s = 0; s < KS; ++s) qa[s] = qr[4 * s + g];  // loads together, then masked
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qa[s] = ok ? qa[s] : 0.0f;
   }
   // this lane's output blocks g + 4r of the wavefront
   double m[4], z[4], mf[4];
@@ -1662,11 +1680,12 @@ __global__ __launch_bounds__(256) void k_pama_combine(const int* __restrict__ q_
     const int sl = s0 + r - 1;
     if (sl >= pcap) break;
     const float* pr = part + ((size_t)h * pcap + sl) * CK;
+    float x[E];  // loads first (clamped columns), so that they go out together
 #pragma unroll
-    for (int k = 0; k < E; ++k) {
-      const int v = threadIdx.x + 256 * k;
-      if (v < CK) acc[k] = acc[k] + pr[v];
-    }
+    for (int k = 0; k < E; ++k) x[k] = pr[min((int)threadIdx.x + 256 * k, CK - 1)];
+#pragma unroll
+    for (int k = 0; k < E; ++k)
+      if ((int)threadIdx.x + 256 * k < CK) acc[k] = acc[k] + x[k];
   }
 #pragma unroll
   for (int k = 0; k < E; ++k) {
@@ -1692,12 +1711,20 @@ __device__ void select_topk_radix(const float* __restrict__ w, const int* __rest
   constexpr int E = MAXC / 256;
   uint32_t kv[E];
   int nv = 0;
+  int ks[E];
+  float xs[E];  // loads first (clamped columns), so that they go out together
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int e = min(tid + 256 * k, CK - 1);
+    ks[k] = ksz[e];
+    xs[k] = w[e];
+  }
 #pragma unroll
   for (int k = 0; k < E; ++k) {
     const int e = tid + 256 * k;
-    const bool ok = e < CK && ksz[e] > 0;
+    const bool ok = e < CK && ks[k] > 0;
     // valid keys have bit 31 clear (W^ >= 0); invalid ones are all ones and never match
-    const float x = ok ? w[e] : 0.0f;
+    const float x = xs[k];
     kv[k] = ok ? (x > 0.0f ? __float_as_uint(x) : 0u) : 0xffffffffu;
     nv += ok;
   }
@@ -1856,11 +1883,19 @@ __device__ void select_topp_radix(const float* __restrict__ w, const int* __rest
   constexpr int E = MAXC / 256;
   uint32_t kv[E];
   int nv = 0;
+  int ks[E];
+  float xs[E];  // loads first (clamped columns), so that they go out together
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    const int e = min(tid + 256 * k, CK - 1);
+    ks[k] = ksz[e];
+    xs[k] = w[e];
+  }
 #pragma unroll
   for (int k = 0; k < E; ++k) {
     const int e = tid + 256 * k;
-    const bool ok = e < CK && ksz[e] > 0;
-    const float x = ok ? w[e] : 0.0f;
+    const bool ok = e < CK && ks[k] > 0;
+    const float x = xs[k];
     kv[k] = ok ? (x > 0.0f ? __float_as_uint(x) : 0u) : 0xffffffffu;
     nv += ok;
   }
