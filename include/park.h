@@ -259,7 +259,7 @@ park_status park_block_sparse_attn(const void* Qp, const void* Kp, const void* V
  * status word and the per-call work plan live in a static device array of the
  * library, 32 MiB per device (held until the process ends), so the call needs
  * no buffer beyond its inputs and outputs and allocates nothing.  The plan
- * takes about H (268 CQ + 16 (N/128 + (CQ + N/128)/16 + 2)) bytes;
+ * takes about H (284 CQ + 16 (N/128 + (CQ + N/128)/16 + 2)) bytes;
  * PARK_ERR_WORKSPACE (nothing enqueued) when it does not fit.  Every call on
  * one device uses that device's array, so calls that overlap on one device
  * (concurrent streams or host threads) race: order them on one stream. */

@@ -287,29 +287,57 @@ int attn_groups_per_head(int N, int CQ) {
 // the group plan.
 //
 // k_attn_selbits: the selection of every (head, query block) as a 64-word bit
-// row (CK <= 2048), one wavefront per row, and fam = u.
+// row (CK <= 2048), one wavefront per row, fam = u, and the parts of the
+// plan's sort key that come from the selection (MinHash values, key tiles).
 __global__ __launch_bounds__(256) void k_attn_selbits(const int* __restrict__ kv_count,
-                                                      const int* __restrict__ kv_index, int H,
-                                                      int CQ, int CK, uint32_t* __restrict__ bits,
-                                                      int* __restrict__ fam) {
+                                                      const int* __restrict__ kv_index,
+                                                      const int* __restrict__ q_offsets,
+                                                      const int* __restrict__ k_offsets, int H,
+                                                      int N, int CQ, int CK,
+                                                      uint32_t* __restrict__ bits,
+                                                      int* __restrict__ fam,
+                                                      uint4* __restrict__ rkey) {
   __shared__ uint32_t rowb[4][64];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const size_t row = (size_t)blockIdx.x * 4 + wid;
   const bool valid = row < (size_t)H * CQ;
   rowb[wid][lane] = 0u;
   __syncthreads();
+  uint32_t m1 = 0xffffffffu, m2 = 0xffffffffu;
+  int nkey = 0;
   if (valid) {
+    const int h = (int)(row / (size_t)CQ);
+    const int* koff = k_offsets + (size_t)h * (CK + 1);
     const int n = min(max(kv_count[row], 0), CK);
     const int* sel = kv_index + row * CK;
     for (int j = lane; j < n; j += 64) {
       const int v = sel[j];
-      if ((unsigned)v < (unsigned)CK) atomicOr(&rowb[wid][v >> 5], 1u << (v & 31));
+      m1 = min(m1, attn_hash((uint32_t)v));
+      m2 = min(m2, attn_hash((uint32_t)v + 7919u));
+      if ((unsigned)v < (unsigned)CK) {
+        atomicOr(&rowb[wid][v >> 5], 1u << (v & 31));
+        nkey += max(0, koff[v + 1] - koff[v]);
+      }
     }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    m1 = min(m1, (uint32_t)__shfl_xor((int)m1, o, 64));
+    m2 = min(m2, (uint32_t)__shfl_xor((int)m2, o, 64));
+    nkey += __shfl_xor(nkey, o, 64);
   }
   __syncthreads();
   if (valid) {
     bits[row * 64 + lane] = rowb[wid][lane];
-    if (lane == 0) fam[row] = (int)(row % (size_t)CQ);
+    if (lane == 0) {
+      const int h = (int)(row / (size_t)CQ), u = (int)(row % (size_t)CQ);
+      const int* qo = q_offsets + (size_t)h * (CQ + 1);
+      const int a = min(max(qo[u], 0), N), b = min(max(qo[u + 1], a), N);
+      fam[row] = u;
+      // the plan's sort-key parts: the two MinHash values, the key tiles of
+      // the block's own selection, whether the block has rows
+      rkey[row] = make_uint4(m1, m2, (uint32_t)((nkey + 31) >> 5), b > a ? 1u : 0u);
+    }
   }
 }
 
@@ -371,9 +399,7 @@ __global__ __launch_bounds__(256) void k_attn_family(const int* __restrict__ kv_
 //                the coordinates of the sorted concatenation; {0,0,0,0} when
 //                g is past the last group.
 __global__ __launch_bounds__(1024) void k_attn_gplan(const int* __restrict__ q_offsets,
-                                                     const int* __restrict__ kv_count,
-                                                     const int* __restrict__ kv_index,
-                                                     const int* __restrict__ k_offsets,
+                                                     const uint4* __restrict__ rkey,
                                                      const int* __restrict__ fam, int N,
                                                      int CQ, int CK, int GPH,
                                                      int* __restrict__ order,
@@ -386,45 +412,28 @@ __global__ __launch_bounds__(1024) void k_attn_gplan(const int* __restrict__ q_o
   __shared__ int wsum[16];
   const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int* qo = q_offsets + (size_t)h * (CQ + 1);
-  const int* koff = k_offsets + (size_t)h * (CK + 1);
   int SZ = 2;
   while (SZ < CQ) SZ <<= 1;
   // sort keys (selection family, top bits of the first MinHash, top bits of
   // the second, block id); blocks without rows sort last with the key ~0.
-  // One wavefront per block.
-  for (int u = wid; u < SZ; u += 16) {
+  // One thread per block.
+  for (int u = tid; u < SZ; u += 1024) {
     unsigned long long kk = ~0ull;
     if (u < CQ) {
-      const int a = min(max(qo[u], 0), N), b = min(max(qo[u + 1], a), N);
-      if (b > a) {
-        const size_t row = (size_t)h * CQ + u;
-        const int n = min(max(kv_count[row], 0), CK);
-        const int* sel = kv_index + row * CK;
-        uint32_t m1 = 0xffffffffu, m2 = 0xffffffffu;
-        int nkey = 0;
-        for (int j = lane; j < n; j += 64) {
-          const uint32_t v = (uint32_t)sel[j];
-          m1 = min(m1, attn_hash(v));
-          m2 = min(m2, attn_hash(v + 7919u));
-          if (v < (uint32_t)CK) nkey += max(0, koff[v + 1] - koff[v]);
-        }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          m1 = min(m1, (uint32_t)__shfl_xor((int)m1, o, 64));
-          m2 = min(m2, (uint32_t)__shfl_xor((int)m2, o, 64));
-          nkey += __shfl_xor(nkey, o, 64);
-        }
-        if (lane == 0) tiles[u] = (nkey + 31) >> 5;
+      // MinHash values and key tiles of the selection (k_attn_selbits)
+      const uint4 rk = rkey[(size_t)h * CQ + u];
+      tiles[u] = (int)rk.z;
+      if (rk.w) {
         // family label: the partner of u's smallest partner (one pointer jump)
         const int* fh = fam + (size_t)h * CQ;
         int f = fh[u];
         f = (unsigned)f < (unsigned)CQ ? fh[f] : u;
         f = (unsigned)f < (unsigned)CQ ? f : u;
-        kk = ((unsigned long long)f << 52) | ((unsigned long long)(m1 >> 12) << 32) |
-             (m2 & 0xfffff800u) | (uint32_t)u;
+        kk = ((unsigned long long)f << 52) | ((unsigned long long)(rk.x >> 12) << 32) |
+             (rk.y & 0xfffff800u) | (uint32_t)u;
       }
     }
-    if (lane == 0) key[u] = kk;
+    key[u] = kk;
   }
   __syncthreads();
   for (int len = 2; len <= SZ; len <<= 1)
@@ -1049,13 +1058,14 @@ static park_status attn_grp_launch(const void* Qp, const void* Kp, const void* V
   int4* grp = (int4*)((char*)plan + attn_grp_offset(H, CQ));
   int* fam = (int*)(grp + (size_t)H * GPH);
   uint32_t* bits = (uint32_t*)((char*)fam + attn_fam_bytes(H, CQ));
+  uint4* rkey = (uint4*)(bits + (size_t)H * CQ * 64);
   const unsigned nrow = (unsigned)H * (unsigned)CQ, ntile = (unsigned)(CQ + 63) / 64;
-  PARK_LAUNCH("attn_selbits", k_attn_selbits, dim3((nrow + 3) / 4), dim3(256), 0, st, kc, ki, H,
-              CQ, CK, bits, fam);
+  PARK_LAUNCH("attn_selbits", k_attn_selbits, dim3((nrow + 3) / 4), dim3(256), 0, st, kc, ki, qo,
+              ko, H, N, CQ, CK, bits, fam, rkey);
   PARK_LAUNCH("attn_family", k_attn_family, dim3(ntile * (ntile + 1) / 2, H), dim3(256), 0, st,
               kc, bits, CQ, CK, fam);
-  PARK_LAUNCH("attn_plan", k_attn_gplan, dim3(H), dim3(1024), 0, st, qo, kc, ki, ko, fam, N, CQ,
-              CK, GPH, order, spre, grp);
+  PARK_LAUNCH("attn_plan", k_attn_gplan, dim3(H), dim3(1024), 0, st, qo, (const uint4*)rkey,
+              (const int*)fam, N, CQ, CK, GPH, order, spre, grp);
   // K ring, V ring, score biases, key-block flags, stream table, selection words
   constexpr size_t lds = (size_t)(2 * ATTN_KSLOTS + 1) * 32 * D * sizeof(bf16_t) +
                          (size_t)ATTN_KSLOTS * ATTN_LB * 32 * 4 + (size_t)AT_MAXC / 2 * 4 +
@@ -1086,15 +1096,16 @@ static park_status attn_mfma_d(const void* Qp, const void* Kp, const void* Vp, c
 }
 
 // order [H][CQ], spre [H][CQ + 1], then the groups [H][GPH] at 16-byte
-// alignment, the selection families [H][CQ] (padded to 16 bytes) and the
-// selection bit rows [H][CQ][64]
+// alignment, the selection families [H][CQ] (padded to 16 bytes), the
+// selection bit rows [H][CQ][64] and the sort-key parts [H][CQ] (uint4)
 size_t attn_grp_offset(int H, int CQ) {
   return (((size_t)H * CQ + (size_t)H * (CQ + 1)) * sizeof(int) + 15) & ~(size_t)15;
 }
 
 size_t attn_plan_bytes(int H, int N, int CQ) {
   return attn_grp_offset(H, CQ) + (size_t)H * attn_groups_per_head(N, CQ) * sizeof(int4) +
-         attn_fam_bytes(H, CQ) + (size_t)H * CQ * 64 * sizeof(uint32_t);
+         attn_fam_bytes(H, CQ) + (size_t)H * CQ * 64 * sizeof(uint32_t) +
+         (size_t)H * CQ * sizeof(uint4);
 }
 
 park_status launch_attention(const void* Qp, const void* Kp, const void* Vp, const int* q_offsets,
