@@ -668,7 +668,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
   uint32_t* flg = (uint32_t*)(bias + NSK * ATTN_LB * KT);  // [AT_MAXC / 2]: 16 bits per key block
   int2* ut = (int2*)(flg + AT_MAXC / 2);            // [ATTN_UCAP + 1]
   uint16_t* selw = (uint16_t*)(ut + ATTN_UCAP + 1);  // [ATTN_UCAP]
-  __shared__ int sg_row[ATTN_LB], sg_lr[ATTN_LB + 1], sg_u[ATTN_LB];
+  __shared__ int sg_row[ATTN_LB], sg_lr[ATTN_LB + 1], sg_u[ATTN_LB], sg_n[ATTN_LB + 1];
   __shared__ int tmp[2][NW];
   static_assert(ATTN_LB <= 16, "selection words are 16 bits");
 
@@ -700,19 +700,29 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
     sg_u[tid] = u;
     sg_row[tid] = min(max(qo[u], 0), N) + (a - s0);
     sg_lr[tid] = a - gd.x;
+    sg_n[tid] = min(max(kv_count[(size_t)h * CQ + u], 0), CK);
   }
   if (tid == 0) sg_lr[nb] = gd.y - gd.x;
   for (int v = tid; v < AT_MAXC / 2; v += NT) flg[v] = 0u;
   __syncthreads();
-  // bit b of key block v's flag: query block b of the group selected v
-  for (int b = 0; b < nb; ++b) {
-    const size_t row = (size_t)h * CQ + sg_u[b];
-    const int n = min(max(kv_count[row], 0), CK);
-    const int* sel = kv_index + row * CK;
-    for (int j = tid; j < n; j += NT) {
-      const int v = sel[j];
-      if ((unsigned)v < (unsigned)CK) atomicOr(&flg[v >> 1], (1u << b) << (16 * (v & 1)));
+  // selection entries of the group's blocks, end-to-end (a prefix over the
+  // few blocks, then one parallel pass: the entries' loads go out together)
+  if (tid == 0) {
+    int c = 0;
+    for (int b = 0; b < nb; ++b) {
+      const int n = sg_n[b];
+      sg_n[b] = c;
+      c += n;
     }
+    sg_n[nb] = c;
+  }
+  __syncthreads();
+  // bit b of key block v's flag: query block b of the group selected v
+  for (int e = tid; e < sg_n[nb]; e += NT) {
+    int b = 0;
+    while (b + 1 < nb && sg_n[b + 1] <= e) ++b;
+    const int v = kv_index[((size_t)h * CQ + sg_u[b]) * CK + (e - sg_n[b])];
+    if ((unsigned)v < (unsigned)CK) atomicOr(&flg[v >> 1], (1u << b) << (16 * (v & 1)));
   }
   __syncthreads();
   const bf16_t* Qh = Qp + (size_t)h * N * D;
@@ -784,6 +794,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
     {
       uint32_t f[EPT];
       int x[EPT], kst[EPT], c = 0, s = 0;
+      int2 kb2[EPT];  // block boundaries, loaded together (clamped ids)
+#pragma unroll
+      for (int k = 0; k < EPT; ++k) kb2[k] = *(const int2*)(koff + min(tid * EPT + k, CK - 1));
 #pragma unroll
       for (int k = 0; k < EPT; ++k) {
         const int v = tid * EPT + k;
@@ -791,8 +804,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void k_attn_grp(
         x[k] = 0;
         kst[k] = -1;
         if (f[k]) {
-          kst[k] = koff[v];
-          x[k] = max(0, koff[v + 1] - kst[k]);
+          kst[k] = kb2[k].x;
+          x[k] = max(0, kb2[k].y - kst[k]);
           ++c;
         }
         s += x[k];
