@@ -459,7 +459,12 @@ static park_status retrieve_stage(const void* K, const park_params* p, const par
 extern "C" {
 
 const char* park_status_string(park_status s) {
-  switch (s) {
+  // a C caller may pass any int; outside the enumerators a C++ park_status
+  // value is undefined, so the argument's bits are read as an int
+  static_assert(sizeof(park_status) == sizeof(int), "park_status is an int in C");
+  int v;
+  memcpy(&v, &s, sizeof v);
+  switch (v) {
     case PARK_OK: return "ok";
     case PARK_ERR_INVALID_ARG: return "invalid argument";
     case PARK_ERR_UNSUPPORTED: return "unsupported configuration";
