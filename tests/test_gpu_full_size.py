@@ -7,6 +7,7 @@ Oracle clusterings are cached per (layer, block size, iterations, head): the
 selection sweep and the output dtypes reuse them.
 """
 import functools
+import os
 
 import numpy as np
 import pytest
@@ -136,6 +137,8 @@ def test_full_layer_sampled_heads(name, out_dtype):
     mode = base.select
     param = base.ratio if mode == "topk" else base.topp
     heads = ((0, 39) + wan_scale_extremes()) if name == "wan" else (0, 11, 23)
+    if os.environ.get("PARK_FULL_ALL_HEADS") == "1":
+        heads = tuple(range(base.H))  # every head (an extended run, ~10 min per layer)
     cfg, C, T, Og, st, _, _ = run_layer(name, mode, param, out_dtype=out_dtype)
     q, k, v = layer(name)
     for h in dict.fromkeys(heads):
