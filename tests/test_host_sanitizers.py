@@ -49,7 +49,7 @@ def test_host_code_clean_under_asan_ubsan(tmp_path):
     assert "__asan_report" in syms and "__ubsan_handle" in syms
     exe = str(tmp_path / "host_checks")
     _run([HIPCC, "--offload-arch=gfx950", *HOST_SAN, "-o", exe, *drv, *objs])
-    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=0",
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=0:verify_asan_link_order=0",
                UBSAN_OPTIONS="print_stacktrace=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
     assert r.returncode == 0, r.stdout + r.stderr
